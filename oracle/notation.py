@@ -1,0 +1,160 @@
+"""conv_einsum strings and size binding (test infrastructure; see package doc).
+
+Grammar, from Section 2.2 ('From einsum to conv_einsum') and the layer
+strings of Appendix A.3:
+
+    spec   := terms '->' term [ '|' convs ]
+    terms  := term ( ',' term )*
+    term   := label*
+    label  := a single letter  |  '(' name ')'        e.g. (s1), (r0)
+    convs  := label ( [','] label )*                  e.g. |hw  or  |h,w
+
+Blanks are ignored.  A label may occur at most once per operand and once in
+the output.  A label that is not convolved must have one size everywhere
+(Appendix A, contraction: the method fails when sizes of the same letter
+differ); a convolved label may carry a different size in each operand
+(Section 2.2: 'the same letter is used for different modes, even if their
+dimension sizes differ').
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+
+def _labels(term: str, where: str):
+    out, i = [], 0
+    while i < len(term):
+        c = term[i]
+        if c == "(":
+            j = term.find(")", i)
+            if j < 0:
+                raise ValueError(f"unclosed '(' in {where}")
+            name = term[i + 1:j]
+            if not name or not all(ch.isalnum() or ch == "_" for ch in name):
+                raise ValueError(f"bad label '({name})' in {where}")
+            out.append(name)
+            i = j + 1
+        elif c.isalpha():
+            out.append(c)
+            i += 1
+        else:
+            raise ValueError(f"unexpected character {c!r} in {where}")
+    return out
+
+
+@dataclass
+class Expr:
+    inputs: list            # list of label lists, one per operand
+    output: list            # output label list
+    conv: list              # convolved labels, in the order written after '|'
+    sizes: list = None      # per operand: {label: size}; set by bind()
+    feature: dict = None    # conv label -> operand index of its feature side
+    out_sizes: dict = None  # output label -> size
+
+    @property
+    def n(self):
+        return len(self.inputs)
+
+    def all_labels(self):
+        seen = []
+        for t in self.inputs:
+            for l in t:
+                if l not in seen:
+                    seen.append(l)
+        return seen
+
+    def holders(self, label):
+        return [i for i, t in enumerate(self.inputs) if label in t]
+
+
+def parse(spec: str) -> Expr:
+    s = "".join(spec.split())
+    if s.count("->") != 1:
+        raise ValueError("a conv_einsum string needs exactly one '->'")
+    lhs, rhs = s.split("->")
+    if "|" in rhs:
+        if rhs.count("|") != 1:
+            raise ValueError("at most one '|'")
+        out_s, conv_s = rhs.split("|")
+    else:
+        out_s, conv_s = rhs, ""
+    if "|" in lhs:
+        raise ValueError("'|' must follow the output term")
+    terms = lhs.split(",")
+    inputs = [_labels(t, f"operand {i}") for i, t in enumerate(terms)]
+    for i, t in enumerate(inputs):
+        if len(set(t)) != len(t):
+            raise ValueError(f"operand {i} repeats a label")
+    output = _labels(out_s, "output")
+    if len(set(output)) != len(output):
+        raise ValueError("output repeats a label")
+    conv = []
+    for piece in conv_s.split(","):
+        for l in _labels(piece, "convolution list"):
+            if l in conv:
+                raise ValueError(f"convolved label {l} listed twice")
+            conv.append(l)
+    present = {l for t in inputs for l in t}
+    for l in output:
+        if l not in present:
+            raise ValueError(f"output label {l} is in no operand")
+    for l in conv:
+        if l not in present:
+            raise ValueError(f"convolved label {l} is in no operand")
+        if l not in output:
+            raise ValueError(f"convolved label {l} must be kept in the output")
+    return Expr(inputs=inputs, output=output, conv=conv)
+
+
+def bind(expr: Expr, shapes, feature_operand: int = 0) -> Expr:
+    """Attach operand sizes and resolve the feature side of each convolved label.
+
+    Feature side (Appendix B, 'Convolution Varieties'): of the two operands
+    holding a convolved label, the one with the larger size holds features and
+    the other holds filters.  On equal sizes the designated feature operand
+    wins if it is one of the two, otherwise the operand with the lower index.
+    A convolved label held by more than two operands is multi-way; it is kept
+    (its cost is defined) but has no feature side.
+    """
+    if len(shapes) != expr.n:
+        raise ValueError("one shape per operand is required")
+    sizes = []
+    for i, (t, shp) in enumerate(zip(expr.inputs, shapes)):
+        shp = tuple(int(d) for d in shp)
+        if len(shp) != len(t):
+            raise ValueError(f"operand {i}: rank {len(shp)} != {len(t)} labels")
+        if any(d < 1 for d in shp):
+            raise ValueError(f"operand {i}: sizes must be >= 1")
+        sizes.append(dict(zip(t, shp)))
+    common = {}
+    for i, sz in enumerate(sizes):
+        for l, d in sz.items():
+            if l in expr.conv:
+                continue
+            if l in common and common[l] != d:
+                raise ValueError(f"label {l}: size {d} in operand {i} != {common[l]}")
+            common[l] = d
+    feature = {}
+    for l in expr.conv:
+        hold = expr.holders(l)
+        if len(hold) == 2:
+            a, b = hold
+            da, db = sizes[a][l], sizes[b][l]
+            if da != db:
+                feature[l] = a if da > db else b
+            elif feature_operand in (a, b):
+                feature[l] = feature_operand
+            else:
+                feature[l] = min(a, b)
+    out_sizes = {}
+    for l in expr.output:
+        if l in feature:            # same padding keeps the feature size
+            out_sizes[l] = sizes[feature[l]][l]
+        elif l in expr.conv:        # one holder, or multi-way: the largest size
+            out_sizes[l] = max(sizes[i][l] for i in expr.holders(l))
+        else:
+            out_sizes[l] = common[l]
+    expr.sizes = sizes
+    expr.feature = feature
+    expr.out_sizes = out_sizes
+    return expr

@@ -1,0 +1,146 @@
+"""Brute-force optimal sequencer (test infrastructure).
+
+Section 3.2 evaluates an N-operand conv_einsum as a sequence of pairwise
+steps and picks the sequence with the fewest multiplications under tnn-cost.
+The oracle enumerates every full binary tree over the operands (outer products
+included) and keeps the cheapest.
+
+Trees are nested pairs of operand indices; in each pair the first child is
+the one holding the lowest operand index.  When several trees share the
+minimum cost the paper does not say which one is returned; the reading used
+here is the lexicographically smallest key
+
+    key(leaf) = ()
+    key((L, R)) = (bitmask of L's operands, key(L), key(R))
+
+which a subset dynamic programme reproduces by always taking, among the
+cheapest splits of a set, the split whose first part has the smallest
+bitmask.  Steps execute in post order, first child first.
+"""
+from __future__ import annotations
+
+import itertools
+
+from .cost import step_cost
+
+
+def leaves(t):
+    return (t,) if isinstance(t, int) else leaves(t[0]) + leaves(t[1])
+
+
+def _mask(t):
+    m = 0
+    for i in leaves(t):
+        m |= 1 << i
+    return m
+
+
+def key(t):
+    if isinstance(t, int):
+        return ()
+    return (_mask(t[0]), key(t[0]), key(t[1]))
+
+
+def all_trees(ops):
+    """Every full binary tree over the operand indices in `ops`."""
+    ops = tuple(sorted(ops))
+    if len(ops) == 1:
+        yield ops[0]
+        return
+    first, rest = ops[0], ops[1:]
+    for r in range(len(rest)):
+        for comb in itertools.combinations(rest, r):
+            a = (first,) + comb
+            b = tuple(o for o in rest if o not in comb)
+            for ta in all_trees(a):
+                for tb in all_trees(b):
+                    yield (ta, tb)
+
+
+def count_trees(n):
+    """(2n-3)!! full binary trees over n labelled leaves."""
+    c = 1
+    for k in range(1, 2 * n - 2, 2):
+        c *= k
+    return c
+
+
+def optimal_tree(expr, mode: str = "fwd", return_all: bool = False):
+    """Cheapest tree by exhaustive search, ties broken by the smallest key."""
+    memo = {}
+
+    def sc(a, b):
+        k = (a, b)
+        if k not in memo:
+            memo[k] = step_cost(expr, leaves_of_mask(a), leaves_of_mask(b), mode)
+        return memo[k]
+
+    def cost(t):
+        if isinstance(t, int):
+            return 0
+        return cost(t[0]) + cost(t[1]) + sc(_mask(t[0]), _mask(t[1]))
+
+    best, best_cost, ties = None, None, []
+    for t in all_trees(range(expr.n)):
+        c = cost(t)
+        if best_cost is None or c < best_cost:
+            best, best_cost, ties = t, c, [t]
+        elif c == best_cost:
+            ties.append(t)
+            if key(t) < key(best):
+                best = t
+    if return_all:
+        return best, best_cost, ties
+    return best, best_cost
+
+
+def leaves_of_mask(m):
+    out, i = [], 0
+    while m:
+        if m & 1:
+            out.append(i)
+        m >>= 1
+        i += 1
+    return tuple(out)
+
+
+def left_to_right_tree(n):
+    """((((0,1),2),3),...): operands paired in string order (Section 3.2,
+    'Better than left-to-right evaluation'; the naive baseline of Section 5)."""
+    t = 0
+    for i in range(1, n):
+        t = (t, i)
+    return t
+
+
+def tree_from_pairs(n, pairs):
+    """Tree from a list of (i, j) positions in the current operand list; the
+    merged tensor is appended to the end of the list (opt_einsum's path
+    format)."""
+    cur = list(range(n))
+    for i, j in pairs:
+        if i == j or not (0 <= i < len(cur)) or not (0 <= j < len(cur)):
+            raise ValueError("bad pair")
+        a, b = cur[i], cur[j]
+        for k in sorted((i, j), reverse=True):
+            del cur[k]
+        node = (a, b) if min(leaves(a)) < min(leaves(b)) else (b, a)
+        cur.append(node)
+    if len(cur) != 1:
+        raise ValueError("pairs do not merge every operand")
+    return cur[0]
+
+
+def post_order_steps(t):
+    """[(left, right), ...] in execution order."""
+    out = []
+
+    def rec(x):
+        if isinstance(x, int):
+            return
+        rec(x[0])
+        rec(x[1])
+        out.append((x[0], x[1]))
+
+    rec(t)
+    return out

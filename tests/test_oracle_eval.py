@@ -1,0 +1,178 @@
+"""Pins for the oracle's evaluators (CPU): the plain definition, every
+pairwise tree, the dense reconstruction, closed forms and library routines
+(PyTorch CPU float64 convolutions, numpy.einsum)."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from conftest import load_layer_strings
+
+STRINGS = load_layer_strings()
+rng = np.random.default_rng(1234)
+
+
+def _e(spec, shapes, **kw):
+    return O.bind(O.parse(spec), shapes, **kw)
+
+
+def _rand(shapes, seed=0):
+    g = np.random.default_rng(seed)
+    return [g.standard_normal(s) for s in shapes]
+
+
+TINY = {
+    "cp_conv": [(2, 3, 5, 4), (2, 2), (2, 3), (2, 3), (2, 3)],
+    "tucker_conv": [(2, 3, 4, 5), (2, 2), (2, 3), (2, 2, 3, 2)],
+    "tt_conv": [(1, 3, 5, 4), (2, 2), (2, 2, 3), (2, 2, 2), (2, 3)],
+    "tr_conv": [(1, 2, 4, 4), (2, 2, 2), (2, 2, 3), (2, 2, 3), (2, 2, 2)],
+    "rcp_conv": [(1, 2, 1, 2, 4, 3), (2, 2, 2), (2, 1, 1), (2, 2, 2), (2, 3, 2)],
+    "rtt_conv": [(1, 2, 1, 2, 4, 3), (2, 2, 2), (2, 2, 1, 1), (2, 2, 2, 2), (2, 3, 2)],
+    "standard_conv": [(2, 3, 5, 4), (2, 3, 3, 2)],
+    "separable_depthwise": [(2, 3, 5, 4), (3, 3), (3, 2)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+def test_definition_equals_every_pairwise_tree(name):
+    spec = STRINGS[name][0]
+    shapes = TINY[name]
+    e = _e(spec, shapes)
+    arr = _rand(shapes, seed=len(name))
+    y = O.eval_definition(e, arr)
+    n_trees = 0
+    for t in O.all_trees(range(e.n)):
+        yp = O.eval_pairwise(e, arr, t)
+        np.testing.assert_allclose(yp, y, rtol=1e-12, atol=1e-12 * np.abs(y).max())
+        n_trees += 1
+    assert n_trees == O.count_trees(e.n)
+
+
+@pytest.mark.parametrize("name", ["cp_conv", "tucker_conv", "rcp_conv", "rtt_conv", "standard_conv"])
+def test_dense_equals_definition(name):
+    spec = STRINGS[name][0]
+    e = _e(spec, TINY[name])
+    arr = _rand(TINY[name], seed=7)
+    np.testing.assert_allclose(O.eval_dense(e, arr), O.eval_definition(e, arr), rtol=1e-12,
+                               atol=1e-12)
+
+
+@pytest.mark.parametrize("K,L", [(3, 3), (5, 3), (2, 4), (1, 3), (4, 1)])
+def test_standard_conv_matches_torch_conv2d(K, L):
+    """bshw,tshw->bthw|hw is the standard 2-D convolution layer (Section 2.3);
+    PyTorch's conv2d(padding='same') is cross-correlation with
+    floor((K-1)/2) zeros before."""
+    X = rng.standard_normal((2, 3, 9, 7))
+    W = rng.standard_normal((4, 3, K, L))
+    e = _e("bshw,tshw->bthw|hw", [X.shape, W.shape])
+    ref = torch.nn.functional.conv2d(torch.tensor(X), torch.tensor(W), padding="same").numpy()
+    np.testing.assert_allclose(O.eval_pairwise(e, [X, W], (0, 1)), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.eval_dense(e, [X, W]), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv1d_and_group_conv1d_match_torch():
+    X = rng.standard_normal((2, 3, 11))
+    W = rng.standard_normal((4, 3, 3))
+    e = _e("bsh,tsh->bth|h", [X.shape, W.shape])
+    ref = torch.nn.functional.conv1d(torch.tensor(X), torch.tensor(W), padding="same").numpy()
+    np.testing.assert_allclose(O.eval_pairwise(e, [X, W], (0, 1)), ref, rtol=1e-12, atol=1e-12)
+    # grouped: gtsh,bgsh->bgth|h (Section 3.1); the input is the larger-h operand
+    G, T, S = 2, 3, 2
+    Wg = rng.standard_normal((G, T, S, 3))
+    Xg = rng.standard_normal((2, G, S, 10))
+    e = _e("gtsh,bgsh->bgth|h", [Wg.shape, Xg.shape])
+    assert e.feature == {"h": 1}
+    ref = torch.nn.functional.conv1d(torch.tensor(Xg.reshape(2, G * S, 10)),
+                                     torch.tensor(Wg.reshape(G * T, S, 3)), padding="same",
+                                     groups=G).numpy().reshape(2, G, T, 10)
+    np.testing.assert_allclose(O.eval_pairwise(e, [Wg, Xg], (0, 1)), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_separable_depthwise_matches_torch_grouped_conv2d():
+    S = 4
+    X = rng.standard_normal((2, S, 8, 6))
+    kh = rng.standard_normal((S, 3))
+    kw = rng.standard_normal((S, 5))
+    e = _e("bshw,sh,sw->bshw|hw", [X.shape, kh.shape, kw.shape])
+    w = np.einsum("sh,sw->shw", kh, kw)[:, None]
+    ref = torch.nn.functional.conv2d(torch.tensor(X), torch.tensor(w), padding="same",
+                                     groups=S).numpy()
+    for t in O.all_trees(range(3)):
+        np.testing.assert_allclose(O.eval_pairwise(e, [X, kh, kw], t), ref, rtol=1e-12,
+                                   atol=1e-12)
+
+
+def test_tucker_with_identity_factors_is_standard_conv():
+    S, T = 3, 4
+    X = rng.standard_normal((2, S, 7, 6))
+    G = rng.standard_normal((S, T, 3, 3))
+    e = _e("bshw,sp,pqhw,qt->bthw|hw", [X.shape, (S, S), G.shape, (T, T)])
+    y = O.eval_pairwise(e, [X, np.eye(S), G, np.eye(T)], O.optimal_tree(e)[0])
+    ref = torch.nn.functional.conv2d(torch.tensor(X), torch.tensor(G.transpose(1, 0, 2, 3)),
+                                     padding="same").numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_unit_filters_reduce_to_plain_einsum():
+    shapes = [(2, 3, 5, 4), (2, 3), (2, 4), (2, 1), (2, 1)]
+    e = _e("bshw,rs,rt,rh,rw->bthw|hw", shapes)
+    X, Us, Ut, Kh, Kw = _rand(shapes, seed=3)
+    ref = np.einsum("bshw,rs,rt,r,r->bthw", X, Us, Ut, Kh[:, 0], Kw[:, 0], optimize=False)
+    for t in O.all_trees(range(5)):
+        np.testing.assert_allclose(O.eval_pairwise(e, [X, Us, Ut, Kh, Kw], t), ref, rtol=1e-12,
+                                   atol=1e-12)
+
+
+@pytest.mark.parametrize("K", [3, 5, 4])
+def test_rank1_impulse_closed_form(K):
+    """R = 1, X = e_{b0,s0,h0,w0}:
+    Y[b,t,h,w] = d(b,b0) U_t[0,t] U_s[0,s0] K_h[0,h0-h+c] K_w[0,w0-w+c]."""
+    B, S, T, H, W = 2, 3, 2, 7, 6
+    c = (K - 1) // 2
+    Us, Ut = rng.standard_normal((1, S)), rng.standard_normal((1, T))
+    Kh, Kw = rng.standard_normal((1, K)), rng.standard_normal((1, K))
+    e = _e("bshw,rs,rt,rh,rw->bthw|hw", [(B, S, H, W), Us.shape, Ut.shape, Kh.shape, Kw.shape])
+    for b0, s0, h0, w0 in [(1, 2, 3, 2), (0, 0, 0, 5), (1, 1, 6, 0)]:
+        X = np.zeros((B, S, H, W))
+        X[b0, s0, h0, w0] = 1.0
+        y = O.eval_pairwise(e, [X, Us, Ut, Kh, Kw], O.optimal_tree(e)[0])
+        ref = np.zeros_like(y)
+        for t, h, w in itertools.product(range(T), range(H), range(W)):
+            kh, kw = h0 - h + c, w0 - w + c
+            if 0 <= kh < K and 0 <= kw < K:
+                ref[b0, t, h, w] = Ut[0, t] * Us[0, s0] * Kh[0, kh] * Kw[0, kw]
+        np.testing.assert_allclose(y, ref, rtol=1e-13, atol=1e-15)
+
+
+def test_constant_input_border_closed_form():
+    """R = 1, X = 1: interior entries are U_t[0,t] sum(U_s) sum(K_h) sum(K_w);
+    border rows and columns drop the taps that fall outside."""
+    B, S, T, H, W, K = 1, 3, 2, 6, 5, 3
+    Us, Ut = rng.standard_normal((1, S)), rng.standard_normal((1, T))
+    Kh, Kw = rng.standard_normal((1, K)), rng.standard_normal((1, K))
+    e = _e("bshw,rs,rt,rh,rw->bthw|hw", [(B, S, H, W), Us.shape, Ut.shape, Kh.shape, Kw.shape])
+    y = O.eval_dense(e, [np.ones((B, S, H, W)), Us, Ut, Kh, Kw])
+    c = 1
+    for h, w in itertools.product(range(H), range(W)):
+        sh = sum(Kh[0, k] for k in range(K) if 0 <= h + k - c < H)
+        sw = sum(Kw[0, k] for k in range(K) if 0 <= w + k - c < W)
+        np.testing.assert_allclose(y[0, :, h, w], Ut[0] * Us.sum() * sh * sw, rtol=1e-13)
+
+
+def test_multiway_convolution_is_not_evaluated():
+    e = _e(STRINGS["interleaved_group"][0], [(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)])
+    with pytest.raises(NotImplementedError):
+        O.eval_definition(e, _rand([(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)]))
+    with pytest.raises(NotImplementedError):
+        O.eval_pairwise(e, _rand([(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)]), ((0, 1), 2))
+
+
+def test_self_contracted_label_is_presummed():
+    X = rng.standard_normal((2, 3, 4))
+    A = rng.standard_normal((4, 5))
+    e = _e("bsm,mt->bt", [X.shape, A.shape])   # s is self-contracted
+    ref = np.einsum("bsm,mt->bt", X, A)
+    np.testing.assert_allclose(O.eval_pairwise(e, [X, A], (0, 1)), ref, rtol=1e-12)
+    np.testing.assert_allclose(O.eval_definition(e, [X, A]), ref, rtol=1e-12)

@@ -1,0 +1,168 @@
+"""Seeded synthetic inputs for the tensorial-convolution layers.
+
+This module is shared by the oracle (CPU, float64) and by the HIP path.  It
+holds no arithmetic of the method itself: only layer strings, operand shapes,
+the random draws and the rounding of those draws to the storage type.
+
+Layer strings follow the conv_einsum notation of Section 2.2 and the layer
+catalogue of Appendix A.3 (CP, Tucker-2, reshaped TT, reshaped CP); the shapes
+are ResNet stage shapes standing in for the paper's ImageNet/CIFAR activations
+(Section 5), which are not available here.
+
+Recipe, per workload:
+  * numpy Generator(PCG64) streams from SeedSequence(seed).spawn(n_in + 1); the
+    last stream draws the output gradient dY;
+  * the feature operand (operand 0) is N(0, 1); factors are N(0, sigma^2);
+  * values are drawn in float64, rounded to float32, and for bf16 workloads
+    rounded again to bfloat16 (round-to-nearest-even on the float32 bit
+    pattern, from the format definition: 1 sign, 8 exponent, 7 mantissa bits).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = ["Workload", "WORKLOADS", "PARITY_WORKLOADS", "make_inputs",
+           "round_to_bf16", "bf16_bits", "f32_bits"]
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    spec: str
+    shapes: tuple            # one shape per input operand, label order of the string
+    dtype: str               # "f32" or "bf16": storage type of inputs
+    seed: int
+    sigmas: tuple            # std of each input operand
+    out_shape: tuple         # output shape, label order of the string
+    backward: bool = True
+    note: str = ""
+
+
+def _kaiming_sigma(fan_in: int, ranks: int, n_factors: int) -> float:
+    """Per-factor std so that the reconstructed dense kernel has variance
+    2/fan_in: each dense entry is a sum of `ranks` products of `n_factors`
+    independent factor entries."""
+    return (2.0 / (fan_in * ranks)) ** (1.0 / (2 * n_factors))
+
+
+def _cp(name, b, s, t, h, w, r, k, dtype, seed, backward=True, sig=None, note=""):
+    spec = "bshw,rs,rt,rh,rw->bthw|hw"
+    shapes = ((b, s, h, w), (r, s), (r, t), (r, k), (r, k))
+    if sig is None:
+        sg = _kaiming_sigma(s * k * k, r, 4)
+        sig = (1.0, sg, sg, sg, sg)
+    return Workload(name, spec, shapes, dtype, seed, tuple(sig), (b, t, h, w), backward, note)
+
+
+def _tucker2(name, b, s, t, h, w, p, q, k, dtype, seed, note=""):
+    spec = "bshw,sp,pqhw,qt->bthw|hw"
+    shapes = ((b, s, h, w), (s, p), (p, q, k, k), (q, t))
+    sg = _kaiming_sigma(s * k * k, p * q, 3)
+    return Workload(name, spec, shapes, dtype, seed, (1.0, sg, sg, sg), (b, t, h, w), True, note)
+
+
+def _rtt(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
+    spec = ("b(s1)(s2)(s3)hw,(r1)(t1)(s1),(r1)(r2)(t2)(s2),(r2)(r3)(t3)(s3),(r3)hw"
+            "->b(t1)(t2)(t3)hw|hw")
+    s1, s2, s3 = s3s
+    t1, t2, t3 = t3s
+    shapes = ((b, s1, s2, s3, h, w), (r, t1, s1), (r, r, t2, s2), (r, r, t3, s3), (r, k, k))
+    sg = _kaiming_sigma(s1 * s2 * s3 * k * k, r ** 3, 4)
+    return Workload(name, spec, shapes, dtype, seed, (1.0, sg, sg, sg, sg),
+                    (b, t1, t2, t3, h, w), True, note)
+
+
+def _rcp(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
+    spec = "b(s1)(s2)(s3)hw,r(t1)(s1),r(t2)(s2),r(t3)(s3),rhw->b(t1)(t2)(t3)hw|hw"
+    s1, s2, s3 = s3s
+    t1, t2, t3 = t3s
+    shapes = ((b, s1, s2, s3, h, w), (r, t1, s1), (r, t2, s2), (r, t3, s3), (r, k, k))
+    sg = _kaiming_sigma(s1 * s2 * s3 * k * k, r, 4)
+    return Workload(name, spec, shapes, dtype, seed, (1.0, sg, sg, sg, sg),
+                    (b, t1, t2, t3, h, w), True, note)
+
+
+# Full-size layers.  C1 uses std 1/sqrt(fan), fan = the size summed when the
+# factor is applied (U_s: s, U_t: r, K_h/K_w: taps).
+WORKLOADS = {
+    "C1": _cp("C1", 2, 16, 16, 8, 8, 8, 3, "f32", 1, backward=False,
+              sig=(1.0, 1 / math.sqrt(16), 1 / math.sqrt(8), 1 / math.sqrt(3), 1 / math.sqrt(3)),
+              note="CP 3x3, tiny, forward only"),
+    "C2": _cp("C2", 128, 64, 64, 56, 56, 32, 3, "f32", 2,
+              note="CP 3x3, ResNet stage-1 shape, rank 32"),
+    "C2_bf16": _cp("C2_bf16", 128, 64, 64, 56, 56, 32, 3, "bf16", 2,
+                   note="CP 3x3, ResNet stage-1 shape, rank 32, bf16 inputs"),
+    "C3": _tucker2("C3", 128, 256, 256, 14, 14, 64, 64, 3, "bf16", 3,
+                   note="Tucker-2 3x3, core 64x64"),
+    "C4": _rtt("C4", 64, (4, 8, 8), (4, 8, 8), 28, 28, 16, 3, "f32", 4,
+               note="reshaped tensor-train 3x3, channels 4x8x8, TT rank 16"),
+    "C5a": _rcp("C5a", 32, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 5,
+                note="reshaped CP 3x3, channels 8x8x8, rank 64, 7x7"),
+    "C5b": _rcp("C5b", 32, (4, 4, 8), (4, 4, 8), 28, 28, 64, 5, "bf16", 6,
+                note="reshaped CP 5x5, channels 4x4x8, rank 64, 28x28"),
+}
+
+# Reduced sizes (same strings, same ranks) that the float64 oracle finishes in
+# seconds while still spanning several kernel tiles and a ragged tail.
+PARITY_WORKLOADS = {
+    "C1": WORKLOADS["C1"],
+    "C2s": _cp("C2s", 2, 64, 64, 19, 19, 32, 3, "f32", 12),
+    "C2s_bf16": _cp("C2s_bf16", 2, 64, 64, 19, 19, 32, 3, "bf16", 12),
+    "C3s": _tucker2("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
+    "C3s_f32": _tucker2("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
+    "C4s": _rtt("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
+    "C5as": _rcp("C5as", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 15),
+    "C5as_f32": _rcp("C5as_f32", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "f32", 15),
+    "C5bs": _rcp("C5bs", 2, (4, 4, 8), (4, 4, 8), 11, 11, 64, 5, "bf16", 16),
+}
+
+
+def round_to_bf16(x) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); returns
+    float32 arrays holding exactly representable bfloat16 values."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    u = (u + 0x7FFF + lsb) & 0xFFFF0000
+    out = u.astype(np.uint32).view(np.float32)
+    nan = np.isnan(f)
+    if nan.any():
+        out = out.copy()
+        out[nan] = np.float32("nan")
+    return out
+
+
+def bf16_bits(x) -> np.ndarray:
+    """Raw bfloat16 bit patterns (uint16) of values already representable in
+    bfloat16 (as produced by round_to_bf16)."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    return (f.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def f32_bits(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+
+
+def make_inputs(w: Workload, with_dy: bool = True):
+    """Draw the operands (and dY) of workload `w`.
+
+    Returns (inputs, dy): a list of float64 arrays and one float64 array (or
+    None) whose values are exactly the stored values (float32, or bfloat16
+    for bf16 workloads).
+    """
+    n = len(w.shapes)
+    streams = np.random.SeedSequence(w.seed).spawn(n + 1)
+    rnd = round_to_bf16 if w.dtype == "bf16" else (lambda a: np.asarray(a, np.float32))
+    ins = []
+    for i, shp in enumerate(w.shapes):
+        g = np.random.Generator(np.random.PCG64(streams[i]))
+        a = g.standard_normal(size=shp) * w.sigmas[i]
+        ins.append(rnd(a.astype(np.float32)).astype(np.float64))
+    dy = None
+    if with_dy:
+        g = np.random.Generator(np.random.PCG64(streams[n]))
+        dy = rnd(g.standard_normal(size=tuple(w.out_shape)).astype(np.float32)).astype(np.float64)
+    return ins, dy
