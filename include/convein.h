@@ -1,0 +1,221 @@
+/*
+ * convein.h - C ABI of the conv_einsum engine for AMD Instinct MI355X (gfx950).
+ *
+ * The engine evaluates one tensorial convolution layer written as a
+ * conv_einsum string (arXiv 2401.03384, Section 2.2 'From einsum to
+ * conv_einsum'; layer strings of Section 2.3 and Appendix A.3), e.g.
+ *
+ *     "bshw,rs,rt,rh,rw->bthw|hw"          CP layer
+ *     "bshw,sp,pqhw,qt->bthw|hw"           Tucker-2 layer
+ *
+ * as a sequence of pairwise multilinear steps chosen to minimise the number
+ * of multiplications under the paper's tnn-cost model (Section 3.2 and
+ * Appendix B), and runs the forward pass and the backward pass (gradients of
+ * every operand) with HIP kernels.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Grammar: operands separated by ',', then '->', the output, and
+ *    optionally '|' followed by the convolved labels ("|hw" or "|h,w").  A
+ *    label is one letter or a parenthesised name such as "(s1)".  Blanks are
+ *    ignored.  A label occurs at most once per operand and once in the output;
+ *    every convolved label must be kept in the output.
+ *  - Sizes: a label that is not convolved has one size everywhere.  A
+ *    convolved label held by two operands may have two sizes: the larger is
+ *    the feature side, the smaller the filter side (Appendix B, 'Convolution
+ *    Varieties'); equal sizes go to the designated feature operand when it is
+ *    one of the two (operand 0 unless ce_expr_set_feature says otherwise),
+ *    else to the lower operand index.
+ *  - Convolution: cross-correlation, stride 1, zero 'same' padding:
+ *        out[p] = sum_k feat[p + k - floor((K-1)/2)] * filt[k],  p in [0, I)
+ *    with feat zero outside [0, I).  The output keeps the feature size I.
+ *  - A label held by one operand only and absent from the output is summed
+ *    away (Section 3.1, case (5)) before the pairwise steps.
+ *  - A convolved label held by more than two operands (multi-way) can be
+ *    parsed and planned (its cost uses the larger size) but not executed:
+ *    ce_forward / ce_backward return CE_ERR_UNSUPPORTED.
+ *  - Tensors are dense, row-major, in the label order written in the string
+ *    (operands) or after '->' (output).  Element type is the plan's dtype,
+ *    except gradients of operands other than the feature operand, which are
+ *    always float32.  bfloat16 is stored as its raw 16-bit pattern.
+ *  - Device memory (inputs, output, gradients, workspace) is owned by the
+ *    caller.  The library never allocates device memory: all scratch lives in
+ *    the caller's workspace, sized by ce_plan_workspace_size and aligned to
+ *    256 bytes.
+ *  - Host objects (ce_expr, ce_plan) are owned by the library, created by the
+ *    *_parse / *_create calls and released by the *_destroy calls.  After
+ *    creation they are immutable: one plan may be used from several threads
+ *    and streams at once provided each call gets its own workspace.
+ *  - Errors: every call returns a ce_status; on failure nothing has been
+ *    launched, outputs are untouched, out-parameters are left unset, and
+ *    ce_last_error() returns a message (thread-local, valid until the next
+ *    call on the same thread).  No C++ exception crosses this interface.
+ */
+#ifndef CONVEIN_H
+#define CONVEIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CE_OK = 0,
+    CE_ERR_PARSE = -1,        /* malformed string */
+    CE_ERR_SHAPE = -2,        /* ranks or sizes inconsistent with the string */
+    CE_ERR_UNSUPPORTED = -3,  /* valid but not executable (multi-way convolution, too many operands) */
+    CE_ERR_ARG = -4,          /* null or out-of-range argument */
+    CE_ERR_WORKSPACE = -5,    /* workspace too small or misaligned */
+    CE_ERR_OVERFLOW = -6,     /* a cost or a size exceeds 64 bits */
+    CE_ERR_HIP = -7           /* a HIP runtime call failed */
+} ce_status;
+
+typedef enum { CE_F32 = 0, CE_BF16 = 1 } ce_dtype;
+
+/* Cost model of the sequencer.
+ * CE_COST_FWD          multiplications of the forward pass (Appendix B cost
+ *                      equations: contraction, batch, outer product, convolution).
+ * CE_COST_TRAIN_PAPER  cost(f) + cost(g1) + cost(g2) per step (Appendix B,
+ *                      'Modification of the cost model for training'). */
+typedef enum { CE_COST_FWD = 0, CE_COST_TRAIN_PAPER = 1 } ce_cost_mode;
+
+typedef struct ce_expr ce_expr;
+typedef struct ce_plan ce_plan;
+
+/* Opaque HIP stream handle (hipStream_t); NULL is the default stream. */
+typedef void* ce_stream;
+
+/* Maximum number of operands and of distinct labels. */
+#define CE_MAX_OPERANDS 16
+#define CE_MAX_LABELS 64
+
+/* ---- expression ---------------------------------------------------------- */
+
+/* Parse `spec` and bind operand sizes (Section 2.2; Appendix A sizes rule).
+ *   n_in     number of operands; must equal the operands in `spec`
+ *   ranks    [n_in] rank of each operand (must equal its label count)
+ *   dims     [n_in] pointers to [ranks[i]] sizes, each >= 1
+ *   out      receives a new ce_expr (release with ce_expr_destroy)
+ * Errors: CE_ERR_PARSE, CE_ERR_SHAPE, CE_ERR_ARG, CE_ERR_UNSUPPORTED (more
+ * than CE_MAX_OPERANDS operands or CE_MAX_LABELS labels). */
+ce_status ce_expr_parse(const char* spec, int n_in, const int* ranks,
+                        const int64_t* const* dims, ce_expr** out);
+
+/* Designate the operand whose convolved labels are features when the two
+ * sizes are equal (default 0).  Must be called before ce_plan_create. */
+ce_status ce_expr_set_feature(ce_expr* e, int operand);
+
+/* Output rank and sizes (a convolved output label takes its feature size).
+ *   rank   receives the output rank
+ *   dims   if non-NULL, receives [rank] sizes */
+ce_status ce_expr_output_shape(const ce_expr* e, int* rank, int64_t* dims);
+
+void ce_expr_destroy(ce_expr* e);
+
+/* ---- plan ----------------------------------------------------------------- */
+
+/* Plan flags. */
+#define CE_FLAG_GENERIC_ONLY 0x1u  /* run every step on the generic strided kernel */
+
+/* Choose the pairwise evaluation order with the fewest multiplications under
+ * `mode` (Section 3.2, optimal sequencer; Appendix B tnn-cost), searching
+ * every binary tree including outer products.  Among trees of equal cost the
+ * one whose first split (the part holding the lowest operand index) has the
+ * smallest operand bitmask is taken, recursively.  Then lower each step to
+ * kernels and lay out the workspace.  `e` may be destroyed afterwards.
+ * Errors: CE_ERR_ARG, CE_ERR_OVERFLOW, CE_ERR_UNSUPPORTED. */
+ce_status ce_plan_create(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype,
+                         unsigned flags, ce_plan** out);
+
+/* Same, with a caller-given order (e.g. the left-to-right baseline of
+ * Section 5): `pairs` holds n_pairs = n_in - 1 pairs (i, j) of positions in
+ * the current operand list; the merged tensor is appended to the end of the
+ * list (opt_einsum's path format).  Left-to-right is (0,1) followed by
+ * (0, len-1) for the current list length len, e.g. (0,1),(0,3),(0,2),(0,1)
+ * for five operands.  Costs are reported in CE_COST_FWD. */
+ce_status ce_plan_create_with_path(const ce_expr* e, const int* pairs, int n_pairs,
+                                   ce_dtype dtype, unsigned flags, ce_plan** out);
+
+/* Number of pairwise steps (n_in - 1). */
+ce_status ce_plan_num_steps(const ce_plan* p, int* n);
+
+/* Step i in execution order (post order, first child first): operand bitmasks
+ * of its two inputs (lhs holds the lowest operand index of the step) and its
+ * multiplications under CE_COST_FWD.  Any out-pointer may be NULL. */
+ce_status ce_plan_step(const ce_plan* p, int i, uint64_t* lhs_mask, uint64_t* rhs_mask,
+                       uint64_t* macs);
+
+/* Total cost of the plan in the plan's cost mode, and its forward
+ * multiplications.  Either pointer may be NULL. */
+ce_status ce_plan_cost(const ce_plan* p, uint64_t* total_cost, uint64_t* fwd_macs);
+
+/* Multiplications of the left-to-right order under the plan's cost mode. */
+ce_status ce_plan_left_to_right_cost(const ce_plan* p, uint64_t* cost);
+
+/* Workspace bytes needed by ce_forward (for_backward = 0) or ce_backward
+ * (for_backward = 1). */
+ce_status ce_plan_workspace_size(const ce_plan* p, int for_backward, size_t* bytes);
+
+/* Human-readable description of the steps and kernels (valid while p lives). */
+const char* ce_plan_describe(const ce_plan* p);
+
+void ce_plan_destroy(ce_plan* p);
+
+/* ---- execution -------------------------------------------------------------- */
+
+/* Forward pass (Section 3.1 atomic steps in the planned order).
+ *   in        [n_in] device pointers to the operands
+ *   out       device pointer to the output
+ *   ws        device workspace of ws_bytes >= ce_plan_workspace_size(p, 0),
+ *             256-byte aligned (may be NULL when the size is 0)
+ *   stream    HIP stream; all work is enqueued asynchronously on it
+ * Errors: CE_ERR_ARG, CE_ERR_WORKSPACE, CE_ERR_UNSUPPORTED, CE_ERR_HIP. */
+ce_status ce_forward(const ce_plan* p, const void* const* in, void* out,
+                     void* ws, size_t ws_bytes, ce_stream stream);
+
+/* Backward pass: gradients of L = <Y, dout> with respect to the operands
+ * (Appendix B: g1 and g2 of every step, in reverse order).  Intermediates are
+ * recomputed from the inputs (gradient checkpointing, Section 3.3), so no
+ * forward call needs to precede it.
+ *   in        [n_in] device pointers to the operands
+ *   dout      device pointer to dL/dY (plan dtype, output layout)
+ *   din       [n_in] device pointers receiving dL/d operand_i in the operand's
+ *             layout (plan dtype for the feature operand, float32 for the
+ *             others); a NULL entry means that gradient is not wanted
+ *   ws        workspace of ws_bytes >= ce_plan_workspace_size(p, 1)
+ * Errors: as ce_forward. */
+ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
+                      void* const* din, void* ws, size_t ws_bytes, ce_stream stream);
+
+/* ---- launch timing (profiling harnesses) ---------------------------------- */
+
+/* Start recording on the calling thread: every kernel that ce_forward /
+ * ce_backward enqueue from now on is bracketed by two HIP events recorded on
+ * the same stream (events are created by the library and reused; no device
+ * memory is allocated).  Adds two event records per launch. */
+ce_status ce_timing_begin(void);
+
+/* Stop recording; waits for the recorded events and keeps the records until
+ * the next ce_timing_begin on this thread.  n_records receives their count. */
+ce_status ce_timing_end(int* n_records);
+
+/* Record i (enqueue order): kernel name, step description (valid until the
+ * next ce_timing_begin), elapsed milliseconds, and the launch's algorithmic
+ * bytes (each operand read once, the result written once) and flops
+ * (2 x multiplications of its pairwise step).  Any out-pointer may be NULL. */
+ce_status ce_timing_record(int i, const char** kernel, const char** step, float* ms,
+                           double* bytes, double* flops);
+
+/* Message for the last non-OK status returned on this thread. */
+const char* ce_last_error(void);
+
+/* Library version string. */
+const char* ce_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONVEIN_H */

@@ -1,0 +1,180 @@
+// Executor: validates the call, resolves symbolic buffers to device pointers
+// and enqueues the plan's launches on the caller's stream.  No host
+// synchronisation, no device allocation.
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "capi_internal.h"
+#include "kernels.h"
+#include "plan.h"
+
+namespace ce {
+namespace {
+
+struct Ptrs {
+    const void* const* in;
+    void* out;
+    const void* dout;
+    void* const* din;
+    void* ws;
+};
+
+void* resolve(const BufRef& b, const Ptrs& P) {
+    switch (b.kind) {
+        case BUF_IN: return const_cast<void*>(P.in[b.index]);
+        case BUF_OUT: return P.out;
+        case BUF_DOUT: return const_cast<void*>(P.dout);
+        case BUF_DIN: return P.din ? P.din[b.index] : nullptr;
+        case BUF_WS: return (char*)P.ws + b.offset;
+        default: return nullptr;
+    }
+}
+
+hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
+    const void* a = resolve(ln.a, P);
+    const void* b = resolve(ln.b, P);
+    void* c = resolve(ln.c, P);
+    void* d = resolve(ln.d, P);
+    int variant = ln.kind & 0xff;
+    switch (variant) {
+        case K_GENERIC_THREAD:
+        case K_GENERIC_WAVE:
+        case K_GENERIC_BLOCK: return launch_generic(ln, a, b, c, s);
+        default: return launch_fast(ln, a, b, c, d, s);
+    }
+}
+
+// ---- launch timing ---------------------------------------------------------
+struct TimingRec {
+    hipEvent_t a, b;
+    const Launch* ln;
+    std::string kname, what;
+    float ms = 0;
+    double bytes = 0, flops = 0;
+};
+thread_local bool g_timing = false;
+thread_local std::vector<TimingRec> g_recs;
+thread_local std::vector<hipEvent_t> g_pool;
+thread_local size_t g_pool_used = 0;
+
+hipEvent_t next_event() {
+    if (g_pool_used == g_pool.size()) {
+        hipEvent_t ev;
+        if (hipEventCreate(&ev) != hipSuccess) fail(CE_ERR_HIP, "hipEventCreate failed");
+        g_pool.push_back(ev);
+    }
+    return g_pool[g_pool_used++];
+}
+
+void check_ws(const ce_plan* p, size_t need, void* ws, size_t ws_bytes) {
+    if (ws_bytes < need)
+        fail(CE_ERR_WORKSPACE, "workspace of " + std::to_string(ws_bytes) + " B < required " +
+                                   std::to_string(need) + " B");
+    if (need && !ws) fail(CE_ERR_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)ws) & 255) fail(CE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    (void)p;
+}
+
+hipError_t run_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
+    if (!g_timing) return raw_launch(ln, P, s);
+    TimingRec r;
+    r.a = next_event();
+    r.b = next_event();
+    r.ln = &ln;
+    r.kname = ln.kname;
+    r.what = ln.what;
+    r.bytes = ln.alg_bytes;
+    r.flops = ln.alg_flops;
+    hipError_t e = hipEventRecord(r.a, s);
+    if (e != hipSuccess) return e;
+    e = raw_launch(ln, P, s);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(r.b, s);
+    if (e == hipSuccess) g_recs.push_back(r);
+    return e;
+}
+
+}  // namespace
+}  // namespace ce
+
+using namespace ce;
+
+extern "C" ce_status ce_timing_begin(void) {
+    return guard([&] {
+        g_recs.clear();
+        g_pool_used = 0;
+        g_timing = true;
+    });
+}
+
+extern "C" ce_status ce_timing_end(int* n_records) {
+    return guard([&] {
+        g_timing = false;
+        if (!g_recs.empty()) {
+            hipError_t e = hipEventSynchronize(g_recs.back().b);
+            if (e != hipSuccess) fail(CE_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
+            for (auto& r : g_recs) {
+                e = hipEventElapsedTime(&r.ms, r.a, r.b);
+                if (e != hipSuccess) fail(CE_ERR_HIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(e));
+            }
+        }
+        if (n_records) *n_records = (int)g_recs.size();
+    });
+}
+
+extern "C" ce_status ce_timing_record(int i, const char** kernel, const char** step, float* ms,
+                                      double* bytes, double* flops) {
+    return guard([&] {
+        if (i < 0 || i >= (int)g_recs.size()) fail(CE_ERR_ARG, "record index out of range");
+        const TimingRec& r = g_recs[i];
+        if (kernel) *kernel = r.kname.c_str();
+        if (step) *step = r.what.c_str();
+        if (ms) *ms = r.ms;
+        if (bytes) *bytes = r.bytes;
+        if (flops) *flops = r.flops;
+    });
+}
+
+extern "C" ce_status ce_forward(const ce_plan* p, const void* const* in, void* out, void* ws,
+                                size_t ws_bytes, ce_stream stream) {
+    return guard([&] {
+        if (!p || !in || !out) fail(CE_ERR_ARG, "NULL plan, inputs or output");
+        if (!p->executable) fail(CE_ERR_UNSUPPORTED, p->why_not);
+        for (int i = 0; i < p->e.n; i++)
+            if (!in[i]) fail(CE_ERR_ARG, "input " + std::to_string(i) + " is NULL");
+        check_ws(p, p->ws_fwd, ws, ws_bytes);
+        Ptrs P{in, out, nullptr, nullptr, ws};
+        hipStream_t s = (hipStream_t)stream;
+        for (const Launch& ln : p->fwd) {
+            hipError_t err = run_launch(ln, P, s);
+            if (err != hipSuccess)
+                fail(CE_ERR_HIP, std::string("kernel launch failed (") + ln.what + "): " +
+                                     hipGetErrorString(err));
+        }
+    });
+}
+
+extern "C" ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
+                                 void* const* din, void* ws, size_t ws_bytes, ce_stream stream) {
+    return guard([&] {
+        if (!p || !in || !dout || !din) fail(CE_ERR_ARG, "NULL plan, inputs, dout or din");
+        if (!p->executable) fail(CE_ERR_UNSUPPORTED, p->why_not);
+        uint32_t wanted = 0;
+        for (int i = 0; i < p->e.n; i++) {
+            if (!in[i]) fail(CE_ERR_ARG, "input " + std::to_string(i) + " is NULL");
+            if (din[i]) wanted |= 1u << i;
+        }
+        check_ws(p, p->ws_bwd, ws, ws_bytes);
+        if (!wanted) return;
+        Ptrs P{in, nullptr, dout, din, ws};
+        hipStream_t s = (hipStream_t)stream;
+        for (const Launch& ln : p->bwd) {
+            if (ln.need && !(ln.need & wanted)) continue;
+            hipError_t err = run_launch(ln, P, s);
+            if (err != hipSuccess)
+                fail(CE_ERR_HIP, std::string("kernel launch failed (") + ln.what + "): " +
+                                     hipGetErrorString(err));
+        }
+    });
+}

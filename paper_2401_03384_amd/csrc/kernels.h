@@ -1,0 +1,17 @@
+// Launchers of the HIP kernels, called by the executor.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "plan.h"
+
+namespace ce {
+
+// Generic strided pairwise step (any kind in K_GENERIC_*).
+hipError_t launch_generic(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s);
+
+// Specialised kernels (every other kind).
+hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, void* d,
+                       hipStream_t s);
+
+}  // namespace ce

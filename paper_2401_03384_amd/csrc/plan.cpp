@@ -1,0 +1,742 @@
+// Host planner.
+//
+// Cost model (Appendix B): a pairwise step costs the product, over the union
+// of the labels its two operands keep, of the label size; a label shared by
+// both operands counts once, except a convolved label held by both, which
+// counts (feature size) * (filter size).  Training mode adds the two gradient
+// steps (Appendix B, 'Modification of the cost model for training').
+//
+// Sequencer (Section 3.2): exhaustive dynamic programme over operand subsets,
+// every binary tree including outer products; ties go to the split whose part
+// holding the lowest operand index has the smallest bitmask.
+#include "plan.h"
+
+#include <algorithm>
+#include <cstring>
+#include <memory>
+#include <sstream>
+
+namespace ce {
+
+int64_t TensorRef::numel() const {
+    int64_t n = 1;
+    for (auto d : dims) n *= d;
+    return n;
+}
+
+int TensorRef::pos(int label) const {
+    for (size_t k = 0; k < labels.size(); k++)
+        if (labels[k] == label) return (int)k;
+    return -1;
+}
+
+namespace {
+
+constexpr uint64_t kSat = ~uint64_t(0);
+
+uint64_t mul_sat(uint64_t a, uint64_t b) {
+    unsigned __int128 r = (unsigned __int128)a * b;
+    return (r >> 64) ? kSat : (uint64_t)r;
+}
+uint64_t add_sat(uint64_t a, uint64_t b) {
+    uint64_t r = a + b;
+    return r < a ? kSat : r;
+}
+
+// Labels kept by the intermediate merging operand set S: held in S and either
+// in the output or still held outside S.
+uint64_t kept_mask(const ce_expr& e, uint32_t S) {
+    uint64_t m = 0;
+    for (int l = 0; l < e.num_labels(); l++) {
+        uint32_t h = e.holders[l];
+        if ((h & S) && (e.in_out(l) || (h & ~S))) m |= 1ull << l;
+    }
+    return m;
+}
+
+// Size of label l in the intermediate of S: the largest size among S's
+// operands holding it (for a convolved label, the feature size once both
+// sides are merged).
+int64_t size_in_set(const ce_expr& e, uint32_t S, int l) {
+    int64_t m = 0;
+    for (int i = 0; i < e.n; i++)
+        if (((S >> i) & 1) && ((e.holders[l] >> i) & 1)) m = std::max(m, e.size_in(i, l));
+    return m;
+}
+
+// Is side A the feature side of convolved label l in the step (A, B)?
+bool feature_on_a(const ce_expr& e, uint32_t A, uint32_t B, int l) {
+    int f = e.feature_of(l);
+    if (f >= 0) return (A >> f) & 1;
+    return size_in_set(e, A, l) >= size_in_set(e, B, l);   // multi-way label
+}
+
+uint64_t step_cost_sat(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) {
+    uint64_t ka = kept_mask(e, A), kb = kept_mask(e, B);
+    uint64_t plain = 1, conv_f = 1, conv_ga = 1, conv_gb = 1;
+    for (int l = 0; l < e.num_labels(); l++) {
+        bool ia = (ka >> l) & 1, ib = (kb >> l) & 1;
+        if (!ia && !ib) continue;
+        if (ia && ib && e.is_conv(l)) {
+            uint64_t sa = size_in_set(e, A, l), sb = size_in_set(e, B, l);
+            bool fa = feature_on_a(e, A, B, l);
+            uint64_t feat = fa ? sa : sb, filt = fa ? sb : sa, out = feat;
+            conv_f = mul_sat(conv_f, mul_sat(feat, filt));
+            // gradient of the feature side: output * filter; of the filter side: feature * output
+            conv_ga = mul_sat(conv_ga, fa ? mul_sat(out, filt) : mul_sat(feat, out));
+            conv_gb = mul_sat(conv_gb, fa ? mul_sat(feat, out) : mul_sat(out, filt));
+        } else {
+            plain = mul_sat(plain, (uint64_t)size_in_set(e, ia ? A : B, l));
+        }
+    }
+    uint64_t f = mul_sat(plain, conv_f);
+    if (mode == CE_COST_FWD) return f;
+    return add_sat(f, add_sat(mul_sat(plain, conv_ga), mul_sat(plain, conv_gb)));
+}
+
+std::string mask_str(uint32_t m) {
+    std::string s = "{";
+    bool first = true;
+    for (int i = 0; i < 32; i++)
+        if ((m >> i) & 1) {
+            if (!first) s += ",";
+            s += std::to_string(i);
+            first = false;
+        }
+    return s + "}";
+}
+
+// Layout of an intermediate: output labels that are not convolved (output
+// order), then labels still to be reduced (order of first appearance), then
+// convolved labels (output order), so spatial labels are innermost.
+std::vector<int> node_layout(const ce_expr& e, uint64_t kept, bool is_root) {
+    std::vector<int> r;
+    if (is_root) return e.out;
+    for (int l : e.out)
+        if (((kept >> l) & 1) && !e.is_conv(l)) r.push_back(l);
+    for (int l = 0; l < e.num_labels(); l++)
+        if (((kept >> l) & 1) && !e.in_out(l)) r.push_back(l);
+    for (int l : e.out)
+        if (((kept >> l) & 1) && e.is_conv(l)) r.push_back(l);
+    return r;
+}
+
+struct Builder {
+    const ce_expr& e;
+    ce_plan& p;
+    int n;
+    Builder(const ce_expr& e_, ce_plan& p_) : e(e_), p(p_), n(e_.n) {}
+
+    // ---- search ---------------------------------------------------------
+    std::vector<uint32_t> optimal_splits(uint64_t* best_cost) {
+        uint32_t full = (n >= 32) ? 0xffffffffu : ((1u << n) - 1);
+        std::vector<uint64_t> best(size_t(full) + 1, 0);
+        std::vector<uint32_t> split(size_t(full) + 1, 0);
+        for (uint32_t S = 1; S <= full; S++) {
+            if (popcount64(S) == 1) continue;
+            uint32_t low = S & (~S + 1), rest = S ^ low;
+            uint64_t bc = kSat;
+            uint32_t bA = 0;
+            bool found = false;
+            for (uint32_t sub = rest;; sub = (sub - 1) & rest) {
+                uint32_t A = sub | low, B = S ^ A;
+                if (B) {
+                    uint64_t c = add_sat(add_sat(best[A], best[B]), step_cost_sat(e, A, B, p.mode));
+                    if (!found || c < bc || (c == bc && A < bA)) {
+                        bc = c;
+                        bA = A;
+                        found = true;
+                    }
+                }
+                if (!sub) break;
+            }
+            best[S] = bc;
+            split[S] = bA;
+        }
+        *best_cost = best[full];
+        return split;
+    }
+
+    int build_tree(uint32_t S, const std::vector<uint32_t>& split) {
+        if (popcount64(S) == 1) return lowest_bit(S);
+        uint32_t A = split[S], B = S ^ A;
+        int a = build_tree(A, split);
+        int b = build_tree(B, split);
+        return add_node(a, b);
+    }
+
+    int add_node(int a, int b) {
+        Node nd;
+        nd.mask = p.nodes[a].mask | p.nodes[b].mask;
+        nd.left = a;
+        nd.right = b;
+        p.nodes.push_back(nd);
+        int c = (int)p.nodes.size() - 1;
+        Step st;
+        st.a = a;
+        st.b = b;
+        st.c = c;
+        st.macs = step_cost_sat(e, p.nodes[a].mask, p.nodes[b].mask, CE_COST_FWD);
+        st.cost = step_cost_sat(e, p.nodes[a].mask, p.nodes[b].mask, p.mode);
+        p.steps.push_back(st);
+        return c;
+    }
+
+    void make_leaves() {
+        for (int i = 0; i < n; i++) {
+            Node nd;
+            nd.mask = 1u << i;
+            nd.labels = e.ops[i];
+            nd.dims = e.dims[i];
+            p.nodes.push_back(nd);
+        }
+    }
+
+    void tree_from_pairs(const int* pairs, int n_pairs) {
+        if (n_pairs != n - 1) fail(CE_ERR_ARG, "a path needs n_in - 1 pairs");
+        std::vector<int> cur;
+        for (int i = 0; i < n; i++) cur.push_back(i);
+        for (int k = 0; k < n_pairs; k++) {
+            int i = pairs[2 * k], j = pairs[2 * k + 1];
+            if (i == j || i < 0 || j < 0 || i >= (int)cur.size() || j >= (int)cur.size())
+                fail(CE_ERR_ARG, "bad pair in path");
+            int a = cur[i], b = cur[j];
+            cur.erase(cur.begin() + std::max(i, j));
+            cur.erase(cur.begin() + std::min(i, j));
+            if (lowest_bit(p.nodes[b].mask) < lowest_bit(p.nodes[a].mask)) std::swap(a, b);
+            cur.push_back(add_node(a, b));
+        }
+    }
+
+    uint64_t left_to_right_cost() {
+        uint64_t c = 0;
+        uint32_t acc = 1;
+        for (int i = 1; i < n; i++) {
+            c = add_sat(c, step_cost_sat(e, acc, 1u << i, p.mode));
+            acc |= 1u << i;
+        }
+        return c;
+    }
+
+    // ---- layouts ------------------------------------------------------------
+    void assign_layouts() {
+        for (size_t s = 0; s < p.steps.size(); s++) {
+            Node& nd = p.nodes[p.steps[s].c];
+            bool root = (s + 1 == p.steps.size());
+            uint64_t kept = kept_mask(e, nd.mask);
+            nd.labels = node_layout(e, kept, root);
+            nd.dims.clear();
+            for (int l : nd.labels) {
+                int64_t d = root ? e.out_size(l) : size_in_set(e, nd.mask, l);
+                nd.dims.push_back(d);
+            }
+        }
+    }
+
+    TensorRef tensor_of(int node, DType dt, BufRef buf) const {
+        const Node& nd = p.nodes[node];
+        TensorRef t;
+        t.labels = nd.labels;
+        t.dims = nd.dims;
+        t.strides.assign(nd.dims.size(), 1);
+        for (int k = (int)nd.dims.size() - 2; k >= 0; k--) t.strides[k] = t.strides[k + 1] * nd.dims[k + 1];
+        t.dtype = dt;
+        t.buf = buf;
+        return t;
+    }
+
+    // Conv maps of a step.  mode 0: forward C = f(A, B); 1: dA = g(dC, B); 2: dB = g(A, dC).
+    std::vector<ConvMap> conv_maps(const Step& st, int which) const {
+        std::vector<ConvMap> v;
+        uint32_t A = p.nodes[st.a].mask, B = p.nodes[st.b].mask;
+        uint64_t ka = kept_mask(e, A), kb = kept_mask(e, B);
+        for (int l = 0; l < e.num_labels(); l++) {
+            if (!e.is_conv(l) || !((ka >> l) & 1) || !((kb >> l) & 1)) continue;
+            bool fa = feature_on_a(e, A, B, l);
+            int64_t I = size_in_set(e, fa ? A : B, l);
+            int64_t K = size_in_set(e, fa ? B : A, l);
+            int64_t c = (K - 1) / 2;
+            ConvMap m{};
+            m.label = l;
+            if (which == 0) {
+                // C[p] = sum_j feat[p + j - c] * filt[j]
+                m.O = I;
+                m.J = K;
+                if (fa) { m.aL = 1; m.bL = 1; m.gL = -c; m.limL = I; m.aR = 0; m.bR = 1; m.gR = 0; m.limR = K; }
+                else    { m.aL = 0; m.bL = 1; m.gL = 0; m.limL = K; m.aR = 1; m.bR = 1; m.gR = -c; m.limR = I; }
+            } else if (which == 1) {
+                // L = dC, R = B, output dA
+                if (fa) {  // dA[q] = sum_j dC[q - j + c] B[j]
+                    m.O = I; m.J = K;
+                    m.aL = 1; m.bL = -1; m.gL = c; m.limL = I;
+                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = K;
+                } else {   // dA[k] = sum_j dC[j] B[j + k - c]
+                    m.O = K; m.J = I;
+                    m.aL = 0; m.bL = 1; m.gL = 0; m.limL = I;
+                    m.aR = 1; m.bR = 1; m.gR = -c; m.limR = I;
+                }
+            } else {
+                // L = A, R = dC, output dB
+                if (fa) {  // dB[k] = sum_j A[j + k - c] dC[j]
+                    m.O = K; m.J = I;
+                    m.aL = 1; m.bL = 1; m.gL = -c; m.limL = I;
+                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = I;
+                } else {   // dB[q] = sum_j A[j] dC[q - j + c]
+                    m.O = I; m.J = K;
+                    m.aL = 0; m.bL = 1; m.gL = 0; m.limL = K;
+                    m.aR = 1; m.bR = -1; m.gR = c; m.limR = I;
+                }
+            }
+            v.push_back(m);
+        }
+        return v;
+    }
+
+    bool has_multiway() const {
+        for (int l = 0; l < e.num_labels(); l++)
+            if (e.is_conv(l) && popcount64(e.holders[l]) > 2) return true;
+        return false;
+    }
+};
+
+// ---- workspace layout: greedy interval packing ---------------------------
+struct WsItem {
+    size_t bytes;
+    int t0, t1;
+    size_t offset = 0;
+    int id;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t pack(std::vector<WsItem>& items) {
+    std::vector<int> order(items.size());
+    for (size_t i = 0; i < items.size(); i++) order[i] = (int)i;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+        if (items[a].bytes != items[b].bytes) return items[a].bytes > items[b].bytes;
+        return items[a].t0 < items[b].t0;
+    });
+    std::vector<int> placed;
+    size_t total = 0;
+    for (int id : order) {
+        WsItem& it = items[id];
+        std::vector<std::pair<size_t, size_t>> busy;
+        for (int q : placed) {
+            const WsItem& o = items[q];
+            if (o.t1 < it.t0 || it.t1 < o.t0) continue;
+            busy.push_back({o.offset, o.offset + align256(o.bytes)});
+        }
+        std::sort(busy.begin(), busy.end());
+        size_t off = 0;
+        for (auto& b : busy) {
+            if (off + align256(it.bytes) <= b.first) break;
+            off = std::max(off, b.second);
+        }
+        it.offset = off;
+        total = std::max(total, off + align256(it.bytes));
+        placed.push_back(id);
+    }
+    return total;
+}
+
+// ---- generic lowering ----------------------------------------------------
+Launch lower_generic(const PairOp& op) {
+    GenericDesc d;
+    std::memset(&d, 0, sizeof(d));
+    struct Dim { int64_t size, sL, sR, sC; bool conv; };
+    std::vector<Dim> od, rd;
+    auto conv_of = [&](int l) -> int {
+        for (size_t k = 0; k < op.convs.size(); k++)
+            if (op.convs[k].label == l) return (int)k;
+        return -1;
+    };
+    std::vector<int> cv_out(op.convs.size(), -1), cv_red(op.convs.size(), -1);
+    for (size_t k = 0; k < op.C.labels.size(); k++) {
+        int l = op.C.labels[k];
+        int ci = conv_of(l);
+        if (ci >= 0) {
+            cv_out[ci] = (int)od.size();
+            od.push_back({op.convs[ci].O, 0, 0, op.C.strides[k], true});
+        } else {
+            od.push_back({op.C.dims[k], op.L.stride_of(l), op.has_r ? op.R.stride_of(l) : 0,
+                          op.C.strides[k], false});
+        }
+    }
+    for (size_t k = 0; k < op.convs.size(); k++) {
+        cv_red[k] = (int)rd.size();
+        rd.push_back({op.convs[k].J, 0, 0, 0, true});
+    }
+    for (size_t k = 0; k < op.L.labels.size(); k++) {
+        int l = op.L.labels[k];
+        if (op.C.has(l) || conv_of(l) >= 0) continue;
+        rd.push_back({op.L.dims[k], op.L.strides[k], op.has_r ? op.R.stride_of(l) : 0, 0, false});
+    }
+    if (op.has_r)
+        for (size_t k = 0; k < op.R.labels.size(); k++) {
+            int l = op.R.labels[k];
+            if (op.C.has(l) || op.L.has(l) || conv_of(l) >= 0) continue;
+            rd.push_back({op.R.dims[k], 0, op.R.strides[k], 0, false});
+        }
+    // merge neighbouring plain dims whose strides chain in every operand
+    auto merge = [](std::vector<Dim>& v, std::vector<int>& idx_fix) {
+        for (size_t i = 0; i + 1 < v.size();) {
+            Dim& a = v[i];
+            Dim& b = v[i + 1];
+            bool ok = !a.conv && !b.conv && a.sL == b.sL * b.size && a.sR == b.sR * b.size &&
+                      a.sC == b.sC * b.size;
+            if (ok) {
+                a.size *= b.size;
+                a.sL = b.sL;
+                a.sR = b.sR;
+                a.sC = b.sC;
+                v.erase(v.begin() + i + 1);
+                for (auto& x : idx_fix)
+                    if (x > (int)i) x--;
+            } else {
+                i++;
+            }
+        }
+    };
+    merge(od, cv_out);
+    merge(rd, cv_red);
+    if ((int)od.size() > kMaxDims || (int)rd.size() > kMaxDims || (int)op.convs.size() > kMaxConv)
+        fail(CE_ERR_UNSUPPORTED, "step has too many loop dimensions for the generic kernel");
+    d.nout = (int)od.size();
+    d.nred = (int)rd.size();
+    d.nconv = (int)op.convs.size();
+    d.has_r = op.has_r ? 1 : 0;
+    d.total_out = 1;
+    d.total_red = 1;
+    for (int i = 0; i < d.nout; i++) {
+        d.out_size[i] = od[i].size;
+        d.out_sL[i] = od[i].sL;
+        d.out_sR[i] = od[i].sR;
+        d.out_sC[i] = od[i].sC;
+        d.total_out *= od[i].size;
+    }
+    for (int i = 0; i < d.nred; i++) {
+        d.red_size[i] = rd[i].size;
+        d.red_sL[i] = rd[i].sL;
+        d.red_sR[i] = rd[i].sR;
+        d.total_red *= rd[i].size;
+    }
+    for (int k = 0; k < d.nconv; k++) {
+        const ConvMap& m = op.convs[k];
+        d.cv_out[k] = cv_out[k];
+        d.cv_red[k] = cv_red[k];
+        d.cv_aL[k] = m.aL;
+        d.cv_bL[k] = m.bL;
+        d.cv_gL[k] = m.gL;
+        d.cv_limL[k] = m.limL;
+        d.cv_sL[k] = op.L.stride_of(m.label);
+        d.cv_aR[k] = m.aR;
+        d.cv_bR[k] = m.bR;
+        d.cv_gR[k] = m.gR;
+        d.cv_limR[k] = m.limR;
+        d.cv_sR[k] = op.has_r ? op.R.stride_of(m.label) : 0;
+    }
+    Launch ln;
+    ln.a = op.L.buf;
+    ln.b = op.R.buf;
+    ln.c = op.C.buf;
+    ln.need = op.need;
+    ln.what = op.what;
+    int32_t tL = op.L.dtype, tR = op.has_r ? op.R.dtype : DT_F32, tC = op.C.dtype;
+    // kind encodes the variant and the three element types
+    int variant;
+    if (d.total_red <= 256) {
+        variant = K_GENERIC_THREAD;
+        ln.block[0] = 256;
+        ln.grid[0] = (uint32_t)((d.total_out + 255) / 256);
+    } else if (d.total_red <= 65536) {
+        variant = K_GENERIC_WAVE;
+        ln.block[0] = 256;
+        ln.grid[0] = (uint32_t)((d.total_out + 3) / 4);
+    } else {
+        variant = K_GENERIC_BLOCK;
+        ln.block[0] = 256;
+        ln.grid[0] = (uint32_t)d.total_out;
+    }
+    if (d.total_out > (int64_t)0x7fffffff * 4) fail(CE_ERR_UNSUPPORTED, "step too large");
+    ln.kind = variant | (tL << 8) | (tR << 9) | (tC << 10);
+    ln.desc.resize(sizeof(d));
+    std::memcpy(ln.desc.data(), &d, sizeof(d));
+    return ln;
+}
+
+std::string tensor_str(const ce_expr& e, const TensorRef& t) {
+    std::string s;
+    for (size_t k = 0; k < t.labels.size(); k++) {
+        const std::string& nm = e.names[t.labels[k]];
+        s += nm.size() == 1 ? nm : "(" + nm + ")";
+    }
+    return s;
+}
+
+}  // namespace
+
+uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) {
+    uint64_t c = step_cost_sat(e, A, B, mode);
+    if (c == kSat) fail(CE_ERR_OVERFLOW, "step cost exceeds 64 bits");
+    return c;
+}
+
+// Lowering of one pairwise op to launches.  Fast kernels are tried first
+// unless the plan asks for the generic kernel only.
+std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags);
+
+ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
+                   bool use_path, const int* pairs, int n_pairs) {
+    if (!e.bound) fail(CE_ERR_ARG, "expression is not bound");
+    if (mode != CE_COST_FWD && mode != CE_COST_TRAIN_PAPER) fail(CE_ERR_ARG, "bad cost mode");
+    if (dtype != CE_F32 && dtype != CE_BF16) fail(CE_ERR_ARG, "bad dtype");
+    std::unique_ptr<ce_plan> p(new ce_plan());
+    p->e = e;
+    p->mode = mode;
+    p->dtype = dtype;
+    p->flags = flags;
+    Builder bld(p->e, *p);
+    const ce_expr& E = p->e;
+    int n = E.n;
+    bld.make_leaves();
+    if (use_path && n_pairs != n - 1) fail(CE_ERR_ARG, "a path needs n_in - 1 pairs");
+    if (n >= 2) {
+        if (use_path) {
+            bld.tree_from_pairs(pairs, n_pairs);
+        } else {
+            uint64_t best;
+            auto split = bld.optimal_splits(&best);
+            bld.build_tree((n >= 32) ? 0xffffffffu : ((1u << n) - 1), split);
+        }
+    }
+    p->total_cost = 0;
+    p->fwd_macs = 0;
+    for (auto& st : p->steps) {
+        if (st.macs == kSat || st.cost == kSat) fail(CE_ERR_OVERFLOW, "plan cost exceeds 64 bits");
+        p->total_cost = add_checked(p->total_cost, st.cost);
+        p->fwd_macs = add_checked(p->fwd_macs, st.macs);
+    }
+    p->ltr_cost = bld.left_to_right_cost();
+    bld.assign_layouts();
+
+    if (bld.has_multiway()) {
+        p->executable = false;
+        p->why_not = "a convolved label is held by more than two operands (multi-way)";
+    }
+    DType dt = dtype == CE_BF16 ? DT_BF16 : DT_F32;
+    int m = (int)p->steps.size();
+    std::ostringstream txt;
+    txt << "conv_einsum plan: " << n << " operands, " << m << " steps, "
+        << (mode == CE_COST_FWD ? "fwd" : "train_paper") << " cost " << p->total_cost
+        << ", forward MACs " << p->fwd_macs << ", left-to-right " << p->ltr_cost << "\n";
+
+    if (p->executable) {
+        auto node_buf_fwd = [&](int node) -> BufRef {
+            BufRef b;
+            if (node < n) { b.kind = BUF_IN; b.index = node; }
+            else if (node == (int)p->nodes.size() - 1) { b.kind = BUF_OUT; }
+            else { b.kind = BUF_WS; b.index = node; }
+            return b;
+        };
+        auto value_tensor = [&](int node) -> TensorRef {
+            TensorRef t = bld.tensor_of(node, dt, node_buf_fwd(node));
+            return t;
+        };
+        // ---------------- forward ----------------
+        std::vector<PairOp> fops;
+        if (m == 0) {
+            PairOp op;
+            op.L = value_tensor(0);
+            op.has_r = false;
+            TensorRef out;
+            out.labels = E.out;
+            out.dims = E.out_dims();
+            out.strides.assign(out.dims.size(), 1);
+            for (int k = (int)out.dims.size() - 2; k >= 0; k--) out.strides[k] = out.strides[k + 1] * out.dims[k + 1];
+            out.dtype = dt;
+            out.buf.kind = BUF_OUT;
+            op.C = out;
+            op.what = "unary";
+            fops.push_back(op);
+        }
+        for (int s = 0; s < m; s++) {
+            const Step& st = p->steps[s];
+            PairOp op;
+            op.L = value_tensor(st.a);
+            op.R = value_tensor(st.b);
+            op.C = value_tensor(st.c);
+            op.convs = bld.conv_maps(st, 0);
+            op.macs = st.macs;
+            op.what = "step " + std::to_string(s) + " fwd " + tensor_str(E, op.L) + "," +
+                      tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
+            fops.push_back(op);
+        }
+        // workspace: intermediates live from their step to their consumer's step
+        auto consumer_step = [&](int node) -> int {
+            for (int s = 0; s < m; s++)
+                if (p->steps[s].a == node || p->steps[s].b == node) return s;
+            return m;
+        };
+        std::vector<WsItem> items;
+        std::vector<int> ws_node;
+        for (int s = 0; s + 1 < m; s++) {
+            int c = p->steps[s].c;
+            WsItem it;
+            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * (dt == DT_BF16 ? 2 : 4);
+            it.t0 = s;
+            it.t1 = consumer_step(c);
+            it.id = c;
+            items.push_back(it);
+        }
+        p->ws_fwd = pack(items);
+        auto ws_off = [&](const std::vector<WsItem>& v, int id) -> size_t {
+            for (auto& it : v)
+                if (it.id == id) return it.offset;
+            fail(CE_ERR_ARG, "internal: workspace item missing");
+        };
+        for (auto& op : fops) {
+            for (TensorRef* t : {&op.L, &op.R, &op.C})
+                if (t->buf.kind == BUF_WS) t->buf.offset = ws_off(items, t->buf.index);
+        }
+            for (auto& op : fops) {
+            auto ls = lower_op(E, op, flags);
+            for (auto& l : ls) p->fwd.push_back(l);
+        }
+
+        // ---------------- backward ----------------
+        // timeline: recompute step t at time t (t < m-1); backward of step s at
+        // time (m-1) + (m-1-s).
+        std::vector<PairOp> bops;
+        std::vector<WsItem> bitems;
+        auto T = [&](int s) { return (m - 1) + (m - 1 - s); };
+        auto parent_step = [&](int node) { return consumer_step(node); };
+        const int GRAD_ID = 1 << 20;   // item ids for gradient buffers
+        for (int s = 0; s + 1 < m; s++) {
+            int c = p->steps[s].c;
+            WsItem it;
+            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * (dt == DT_BF16 ? 2 : 4);
+            it.t0 = s;
+            it.t1 = T(parent_step(c));
+            it.id = c;
+            bitems.push_back(it);
+            WsItem g = it;
+            g.t0 = T(parent_step(c));
+            g.t1 = T(s);
+            g.id = GRAD_ID + c;
+            bitems.push_back(g);
+        }
+        p->ws_bwd = pack(bitems);
+        auto bval = [&](int node) -> TensorRef {
+            BufRef b;
+            if (node < n) { b.kind = BUF_IN; b.index = node; }
+            else { b.kind = BUF_WS; b.index = node; b.offset = ws_off(bitems, node); }
+            return bld.tensor_of(node, dt, b);
+        };
+        auto bgrad = [&](int node) -> TensorRef {
+            BufRef b;
+            DType gdt = dt;
+            if (node < n) {
+                b.kind = BUF_DIN;
+                b.index = node;
+                gdt = (node == E.feature_operand) ? dt : DT_F32;
+            } else if (node == (int)p->nodes.size() - 1) {
+                b.kind = BUF_DOUT;
+            } else {
+                b.kind = BUF_WS;
+                b.index = node;
+                b.offset = ws_off(bitems, GRAD_ID + node);
+            }
+            return bld.tensor_of(node, gdt, b);
+        };
+        if (m == 0) {
+            // Y = unary(X): dX = broadcast of dY through the same label map
+            PairOp op;
+            op.L = bgrad(0);   // placeholder replaced below
+            TensorRef dy;
+            dy.labels = E.out;
+            dy.dims = E.out_dims();
+            dy.strides.assign(dy.dims.size(), 1);
+            for (int k = (int)dy.dims.size() - 2; k >= 0; k--) dy.strides[k] = dy.strides[k + 1] * dy.dims[k + 1];
+            dy.dtype = dt;
+            dy.buf.kind = BUF_DOUT;
+            op.L = dy;
+            op.has_r = false;
+            op.C = bgrad(0);
+            op.need = 1u;
+            op.what = "unary bwd";
+            bops.push_back(op);
+        }
+        for (int s = 0; s + 1 < m; s++) {
+            const Step& st = p->steps[s];
+            PairOp op;
+            op.L = bval(st.a);
+            op.R = bval(st.b);
+            op.C = bval(st.c);
+            op.convs = bld.conv_maps(st, 0);
+            op.macs = st.macs;
+            op.what = "step " + std::to_string(s) + " recompute";
+            bops.push_back(op);
+        }
+        for (int s = m - 1; s >= 0; s--) {
+            const Step& st = p->steps[s];
+            TensorRef dC = bgrad(st.c);
+            {
+                PairOp op;
+                op.L = dC;
+                op.R = bval(st.b);
+                op.C = bgrad(st.a);
+                op.convs = bld.conv_maps(st, 1);
+                op.macs = st.macs;
+                op.need = p->nodes[st.a].mask;
+                op.what = "step " + std::to_string(s) + " grad lhs " + tensor_str(E, op.L) + "," +
+                          tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
+                bops.push_back(op);
+            }
+            {
+                PairOp op;
+                op.L = bval(st.a);
+                op.R = dC;
+                op.C = bgrad(st.b);
+                op.convs = bld.conv_maps(st, 2);
+                op.macs = st.macs;
+                op.need = p->nodes[st.b].mask;
+                op.what = "step " + std::to_string(s) + " grad rhs " + tensor_str(E, op.L) + "," +
+                          tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
+                bops.push_back(op);
+            }
+        }
+        for (auto& op : bops) {
+            auto ls = lower_op(E, op, flags);
+            for (auto& l : ls) p->bwd.push_back(l);
+        }
+    }
+    for (int s = 0; s < m; s++) {
+        const Step& st = p->steps[s];
+        txt << "  step " << s << ": " << mask_str(p->nodes[st.a].mask) << " x "
+            << mask_str(p->nodes[st.b].mask) << "  macs " << st.macs << "\n";
+    }
+    txt << "  workspace fwd " << p->ws_fwd << " B, bwd " << p->ws_bwd << " B\n";
+    for (auto& l : p->fwd) txt << "  fwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
+    for (auto& l : p->bwd) txt << "  bwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
+    if (!p->executable) txt << "  not executable: " << p->why_not << "\n";
+    p->text = txt.str();
+    return p.release();
+}
+
+static double tensor_bytes(const TensorRef& t) {
+    return (double)t.numel() * (t.dtype == DT_BF16 ? 2 : 4);
+}
+
+std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags) {
+    (void)e;
+    (void)flags;
+    Launch ln = lower_generic(op);
+    int v = ln.kind & 0xff;
+    ln.kname = v == K_GENERIC_THREAD ? "generic_thread" : v == K_GENERIC_WAVE ? "generic_wave"
+                                                                                : "generic_block";
+    ln.alg_bytes = tensor_bytes(op.L) + (op.has_r ? tensor_bytes(op.R) : 0) + tensor_bytes(op.C);
+    ln.alg_flops = 2.0 * (double)op.macs;
+    return {ln};
+}
+
+}  // namespace ce

@@ -1,0 +1,108 @@
+// Host planner: tnn-cost, optimal sequencer, tensor layouts, pairwise step
+// lowering for the forward and backward passes, workspace layout.
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "desc.h"
+#include "expr.h"
+
+namespace ce {
+
+enum BufKind : int { BUF_NONE = 0, BUF_IN, BUF_OUT, BUF_DOUT, BUF_DIN, BUF_WS };
+
+struct BufRef {
+    BufKind kind = BUF_NONE;
+    int index = 0;        // operand index for BUF_IN / BUF_DIN
+    size_t offset = 0;    // byte offset for BUF_WS
+};
+
+struct TensorRef {
+    std::vector<int> labels;
+    std::vector<int64_t> dims;
+    std::vector<int64_t> strides;   // in elements
+    DType dtype = DT_F32;
+    BufRef buf;
+    int64_t numel() const;
+    int pos(int label) const;       // -1 if absent
+    int64_t stride_of(int label) const { int p = pos(label); return p < 0 ? 0 : strides[p]; }
+    int64_t dim_of(int label) const { int p = pos(label); return p < 0 ? 1 : dims[p]; }
+    bool has(int label) const { return pos(label) >= 0; }
+};
+
+// One convolved label of a pairwise step (see GenericDesc): output index p in
+// [0, O), reduction index j in [0, J), operand position a*p + b*j + g, valid
+// in [0, lim).
+struct ConvMap {
+    int label;
+    int64_t O, J;
+    int aL, bL;
+    int64_t gL, limL;
+    int aR, bR;
+    int64_t gR, limR;
+};
+
+// C = sum over the reduced labels (and taps) of L * R.
+struct PairOp {
+    TensorRef L, R, C;
+    bool has_r = true;
+    std::vector<ConvMap> convs;
+    uint32_t need = 0;     // backward: run only if a wanted gradient lies below
+    uint64_t macs = 0;     // multiplications of the pairwise step it belongs to
+    std::string what;
+};
+
+struct Launch {
+    int32_t kind = 0;
+    BufRef a, b, c, d;                // operands (meaning depends on kind)
+    uint32_t need = 0;
+    uint32_t grid[3] = {1, 1, 1}, block[3] = {1, 1, 1};
+    uint32_t lds = 0;
+    std::vector<unsigned char> desc;  // descriptor bytes passed to the kernel
+    std::string what;                 // step description
+    std::string kname;                // kernel name
+    double alg_bytes = 0, alg_flops = 0;
+};
+
+struct Node {
+    uint32_t mask = 0;                // operands merged in this node
+    int left = -1, right = -1;        // children (internal nodes)
+    std::vector<int> labels;          // layout, outermost first
+    std::vector<int64_t> dims;
+};
+
+struct Step {
+    int a, b, c;                      // node ids: inputs (a holds the lowest operand), result
+    uint64_t macs;                    // CE_COST_FWD multiplications
+    uint64_t cost;                    // in the plan's cost mode
+};
+
+}  // namespace ce
+
+struct ce_plan {
+    ce_expr e;
+    ce_cost_mode mode = CE_COST_FWD;
+    ce_dtype dtype = CE_F32;
+    unsigned flags = 0;
+    std::vector<ce::Node> nodes;      // 0..n-1 leaves, then one per step
+    std::vector<ce::Step> steps;      // execution order
+    uint64_t total_cost = 0, fwd_macs = 0, ltr_cost = 0;
+    std::vector<ce::Launch> fwd, bwd;
+    size_t ws_fwd = 0, ws_bwd = 0;
+    bool executable = true;
+    std::string why_not;
+    std::string text;
+};
+
+namespace ce {
+
+// Build a plan: the optimal order when use_path is false, else the order
+// given by `pairs` (opt_einsum path format, n_pairs = n_in - 1).
+ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
+                   bool use_path, const int* pairs, int n_pairs);
+
+// Exposed for tests of the search: cost of merging operand sets A and B.
+uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode);
+
+}  // namespace ce

@@ -1,0 +1,167 @@
+"""PyTorch-facing layer over the C ABI.
+
+PyTorch supplies device memory (tensors, the workspace) and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import threading
+
+import torch
+
+from . import binding as B
+
+_DT = {"f32": B.CE_F32, "bf16": B.CE_BF16}
+_TORCH_DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+_MODE = {"fwd": B.CE_COST_FWD, "train_paper": B.CE_COST_TRAIN_PAPER}
+
+
+class Plan:
+    """A planned conv_einsum layer: string, operand shapes, dtype.
+
+    `path` (optional) is an opt_einsum-style list of pairs replacing the
+    optimal order (e.g. the left-to-right baseline)."""
+
+    def __init__(self, spec: str, shapes, dtype: str = "f32", mode: str = "fwd", flags: int = 0,
+                 path=None, feature_operand: int = 0):
+        if dtype not in _DT:
+            raise ValueError(f"dtype must be one of {list(_DT)}")
+        self.spec = spec
+        self.shapes = [tuple(int(d) for d in s) for s in shapes]
+        self.dtype = dtype
+        self.torch_dtype = _TORCH_DT[dtype]
+        self.feature_operand = feature_operand
+        self._expr = B.ce_expr_parse(spec, self.shapes)
+        self._plan = None
+        try:
+            if feature_operand:
+                B.ce_expr_set_feature(self._expr, feature_operand)
+            self.out_shape = B.ce_expr_output_shape(self._expr)
+            if path is None:
+                self._plan = B.ce_plan_create(self._expr, _MODE[mode], _DT[dtype], flags)
+            else:
+                self._plan = B.ce_plan_create_with_path(self._expr, path, _DT[dtype], flags)
+        finally:
+            B.ce_expr_destroy(self._expr)
+            self._expr = None
+        self.num_steps = B.ce_plan_num_steps(self._plan)
+        self.steps = [B.ce_plan_step(self._plan, i) for i in range(self.num_steps)]
+        self.total_cost, self.fwd_macs = B.ce_plan_cost(self._plan)
+        self.ws_fwd = B.ce_plan_workspace_size(self._plan, 0)
+        self.ws_bwd = B.ce_plan_workspace_size(self._plan, 1)
+
+    def __del__(self):
+        if getattr(self, "_plan", None):
+            B.ce_plan_destroy(self._plan)
+            self._plan = None
+
+    @property
+    def handle(self):
+        return self._plan
+
+    def left_to_right_cost(self) -> int:
+        return B.ce_plan_left_to_right_cost(self._plan)
+
+    def describe(self) -> str:
+        return B.ce_plan_describe(self._plan)
+
+    def grad_dtype(self, i: int):
+        return self.torch_dtype if i == self.feature_operand else torch.float32
+
+    def _check_inputs(self, inputs):
+        if len(inputs) != len(self.shapes):
+            raise ValueError(f"expected {len(self.shapes)} operands")
+        dev = inputs[0].device
+        for i, (t, s) in enumerate(zip(inputs, self.shapes)):
+            if tuple(t.shape) != s:
+                raise ValueError(f"operand {i}: shape {tuple(t.shape)} != {s}")
+            if t.dtype != self.torch_dtype:
+                raise TypeError(f"operand {i}: dtype {t.dtype} != {self.torch_dtype}")
+            if not t.is_cuda or t.device != dev:
+                raise ValueError(f"operand {i} must be on {dev}")
+            if not t.is_contiguous():
+                raise ValueError(f"operand {i} must be contiguous")
+        return dev
+
+    @staticmethod
+    def _stream(dev):
+        return torch.cuda.current_stream(dev).cuda_stream
+
+    def workspace(self, backward: bool, device) -> torch.Tensor:
+        n = self.ws_bwd if backward else self.ws_fwd
+        return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+
+    def forward(self, inputs, out=None, workspace=None):
+        dev = self._check_inputs(inputs)
+        if out is None:
+            out = torch.empty(self.out_shape, dtype=self.torch_dtype, device=dev)
+        if workspace is None:
+            workspace = self.workspace(False, dev)
+        B.ce_forward(self._plan, [t.data_ptr() for t in inputs], out.data_ptr(),
+                     workspace.data_ptr(), workspace.numel(), self._stream(dev))
+        return out
+
+    def backward(self, inputs, dout, needs=None, grads=None, workspace=None):
+        dev = self._check_inputs(inputs)
+        if tuple(dout.shape) != tuple(self.out_shape) or dout.dtype != self.torch_dtype or \
+                not dout.is_contiguous():
+            raise ValueError("dout must be contiguous, of the output shape and plan dtype")
+        n = len(inputs)
+        needs = [True] * n if needs is None else list(needs)
+        if grads is None:
+            grads = [torch.empty(self.shapes[i], dtype=self.grad_dtype(i), device=dev)
+                     if needs[i] else None for i in range(n)]
+        if workspace is None:
+            workspace = self.workspace(True, dev)
+        B.ce_backward(self._plan, [t.data_ptr() for t in inputs], dout.data_ptr(),
+                      [g.data_ptr() if g is not None else 0 for g in grads],
+                      workspace.data_ptr(), workspace.numel(), self._stream(dev))
+        return grads
+
+
+_cache = {}
+_cache_lock = threading.Lock()
+
+
+def plan(spec: str, shapes, dtype: str = "f32", mode: str = "fwd", flags: int = 0) -> Plan:
+    """Cached Plan for (spec, shapes, dtype, mode, flags)."""
+    key = (spec, tuple(tuple(s) for s in shapes), dtype, mode, flags)
+    with _cache_lock:
+        p = _cache.get(key)
+        if p is None:
+            p = Plan(spec, shapes, dtype, mode, flags)
+            _cache[key] = p
+        return p
+
+
+class _ConvEinsumFn(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, spec, flags, *tensors):
+        dtype = "bf16" if tensors[0].dtype == torch.bfloat16 else "f32"
+        p = plan(spec, [t.shape for t in tensors], dtype, flags=flags)
+        ctx.plan = p
+        ctx.save_for_backward(*tensors)
+        return p.forward(list(tensors))
+
+    @staticmethod
+    def backward(ctx, dy):
+        tensors = ctx.saved_tensors
+        p = ctx.plan
+        needs = list(ctx.needs_input_grad[2:])
+        grads = p.backward(list(tensors), dy.contiguous().to(p.torch_dtype), needs=needs)
+        grads = [g.to(t.dtype) if g is not None else None for g, t in zip(grads, tensors)]
+        return (None, None, *grads)
+
+
+def conv_einsum(spec: str, *tensors, flags: int = 0):
+    """Evaluate a conv_einsum string on device tensors (differentiable)."""
+    tensors = [t.contiguous() for t in tensors]
+    return _ConvEinsumFn.apply(spec, flags, *tensors)
+
+
+def contract_path(spec: str, *shapes, mode: str = "fwd"):
+    """Planned order without executing: ([(lhs_mask, rhs_mask, macs)], info)."""
+    p = Plan(spec, shapes, "f32", mode)
+    info = {"total_cost": p.total_cost, "fwd_macs": p.fwd_macs,
+            "left_to_right_cost": p.left_to_right_cost(), "text": p.describe()}
+    return p.steps, info

@@ -1,0 +1,187 @@
+// CPU emulation of a plan's launch list (test infrastructure).
+//
+// Builds a plan with the library's own host planner (compiled in from the
+// package sources) restricted to the generic kernel, then executes every
+// launch on the CPU with the semantics of GenericDesc: the same loops the
+// generic HIP kernel runs, with every memory access checked against the size
+// of the buffer it falls in.  A test compares the results with the oracle, so
+// descriptor, layout and workspace bugs show up without a GPU, and an
+// out-of-bounds access is reported instead of faulting a device.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "expr.h"
+#include "plan.h"
+
+using namespace ce;
+
+namespace {
+
+struct Buf {
+    unsigned char* base = nullptr;
+    size_t bytes = 0;
+};
+
+struct Ctx {
+    std::vector<Buf> in, din;
+    Buf out, dout, ws;
+    std::string err;
+};
+
+Buf resolve(const BufRef& b, Ctx& c, int esize, bool& ok) {
+    ok = true;
+    switch (b.kind) {
+        case BUF_IN: return c.in[b.index];
+        case BUF_OUT: return c.out;
+        case BUF_DOUT: return c.dout;
+        case BUF_DIN: return c.din[b.index];
+        case BUF_WS: {
+            Buf r;
+            if (b.offset > c.ws.bytes) { ok = false; return r; }
+            r.base = c.ws.base + b.offset;
+            r.bytes = c.ws.bytes - b.offset;
+            return r;
+        }
+        default: ok = false; return Buf();
+    }
+    (void)esize;
+}
+
+float ld(const Buf& b, int dt, int64_t i, bool& ok) {
+    int es = dt ? 2 : 4;
+    if (i < 0 || (size_t)(i + 1) * es > b.bytes) { ok = false; return 0.f; }
+    if (dt) {
+        uint16_t v;
+        std::memcpy(&v, b.base + i * 2, 2);
+        uint32_t u = (uint32_t)v << 16;
+        float f;
+        std::memcpy(&f, &u, 4);
+        return f;
+    }
+    float f;
+    std::memcpy(&f, b.base + i * 4, 4);
+    return f;
+}
+
+void st(Buf& b, int dt, int64_t i, float v, bool& ok) {
+    int es = dt ? 2 : 4;
+    if (i < 0 || (size_t)(i + 1) * es > b.bytes) { ok = false; return; }
+    if (dt) {
+        uint32_t u;
+        std::memcpy(&u, &v, 4);
+        if ((u & 0x7fffffffu) > 0x7f800000u) u = (u >> 16 | 0x40) << 16;
+        else u += 0x7fffu + ((u >> 16) & 1u);
+        uint16_t h = (uint16_t)(u >> 16);
+        std::memcpy(b.base + i * 2, &h, 2);
+    } else {
+        std::memcpy(b.base + i * 4, &v, 4);
+    }
+}
+
+bool run_generic(const Launch& ln, Ctx& c) {
+    GenericDesc d;
+    std::memcpy(&d, ln.desc.data(), sizeof(d));
+    int tL = (ln.kind >> 8) & 1, tR = (ln.kind >> 9) & 1, tC = (ln.kind >> 10) & 1;
+    bool ok1, ok2, ok3;
+    Buf L = resolve(ln.a, c, 0, ok1), R = resolve(ln.b, c, 0, ok2), C = resolve(ln.c, c, 0, ok3);
+    if (!ok1 || !ok3 || (d.has_r && !ok2) || !C.base) { c.err = "unresolved buffer: " + ln.what; return false; }
+    // the launch grid must cover every output element exactly
+    int variant = ln.kind & 0xff;
+    uint64_t covered = variant == K_GENERIC_THREAD ? (uint64_t)ln.grid[0] * 256
+                     : variant == K_GENERIC_WAVE ? (uint64_t)ln.grid[0] * 4 : ln.grid[0];
+    if (covered < (uint64_t)d.total_out || ln.block[0] != 256) { c.err = "grid does not cover: " + ln.what; return false; }
+    for (int64_t o = 0; o < d.total_out; o++) {
+        int64_t rem = o, offL = 0, offR = 0, offC = 0, oidx[kMaxDims] = {0};
+        for (int i = d.nout - 1; i >= 0; --i) {
+            int64_t x = rem % d.out_size[i];
+            rem /= d.out_size[i];
+            oidx[i] = x;
+            offL += x * d.out_sL[i];
+            offR += x * d.out_sR[i];
+            offC += x * d.out_sC[i];
+        }
+        double acc = 0;   // order differs from the device; precision is not under test
+        for (int64_t r = 0; r < d.total_red; r++) {
+            int64_t rr = r, aL = offL, aR = offR, ridx[kMaxDims] = {0};
+            for (int i = d.nred - 1; i >= 0; --i) {
+                int64_t x = rr % d.red_size[i];
+                rr /= d.red_size[i];
+                ridx[i] = x;
+                aL += x * d.red_sL[i];
+                aR += x * d.red_sR[i];
+            }
+            bool skip = false;
+            for (int k = 0; k < d.nconv; k++) {
+                int64_t p = oidx[d.cv_out[k]], j = ridx[d.cv_red[k]];
+                int64_t pl = d.cv_aL[k] * p + d.cv_bL[k] * j + d.cv_gL[k];
+                int64_t pr = d.cv_aR[k] * p + d.cv_bR[k] * j + d.cv_gR[k];
+                if (pl < 0 || pl >= d.cv_limL[k] || pr < 0 || pr >= d.cv_limR[k]) { skip = true; break; }
+                aL += pl * d.cv_sL[k];
+                aR += pr * d.cv_sR[k];
+            }
+            if (skip) continue;
+            bool ok = true;
+            float a = ld(L, tL, aL, ok);
+            float b = d.has_r ? ld(R, tR, aR, ok) : 1.f;
+            if (!ok) { c.err = "out-of-bounds read: " + ln.what; return false; }
+            acc += (double)a * b;
+        }
+        bool ok = true;
+        st(C, tC, offC, (float)acc, ok);
+        if (!ok) { c.err = "out-of-bounds write: " + ln.what; return false; }
+    }
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Runs the forward (mode 0) or backward (mode 1) launch list of a
+// generic-only plan.  Buffers are host memory in the plan's storage types.
+// Returns 0 on success, else writes a message to err.
+int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* dims, int bf16,
+             int mode, void* const* ins, void* out, const void* dout, void* const* din,
+             char* err, int errlen) {
+    try {
+        std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
+        std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32,
+                                             CE_FLAG_GENERIC_ONLY, false, nullptr, 0));
+        if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
+        Ctx c;
+        int es = bf16 ? 2 : 4;
+        for (int i = 0; i < n; i++) {
+            int64_t numel = 1;
+            for (int k = 0; k < ranks[i]; k++) numel *= dims[i][k];
+            c.in.push_back({(unsigned char*)ins[i], (size_t)numel * es});
+            size_t ges = (i == e->feature_operand) ? es : 4;
+            c.din.push_back({din ? (unsigned char*)din[i] : nullptr, (size_t)numel * ges});
+        }
+        int64_t onum = 1;
+        for (auto d : e->out_dims()) onum *= d;
+        c.out = {(unsigned char*)out, (size_t)onum * es};
+        c.dout = {(unsigned char*)const_cast<void*>(dout), (size_t)onum * es};
+        size_t wsb = mode ? p->ws_bwd : p->ws_fwd;
+        std::vector<unsigned char> ws(wsb + 1, 0xCD);   // poisoned: unset reads show up
+        c.ws = {ws.data(), wsb};
+        const auto& list = mode ? p->bwd : p->fwd;
+        for (const Launch& ln : list) {
+            int v = ln.kind & 0xff;
+            if (v != K_GENERIC_THREAD && v != K_GENERIC_WAVE && v != K_GENERIC_BLOCK) {
+                std::snprintf(err, errlen, "non-generic launch in a generic-only plan");
+                return 3;
+            }
+            if (!run_generic(ln, c)) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
+        }
+        return 0;
+    } catch (const Error& ex) {
+        std::snprintf(err, errlen, "%s", ex.what());
+        return 1;
+    }
+}
+
+}

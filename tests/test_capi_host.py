@@ -1,0 +1,259 @@
+"""C-ABI host-side tests (no GPU): the library loads and exports every symbol
+include/convein.h declares; the C++ planner reproduces the oracle's brute-force
+plan (tree, per-step multiplications, totals, both cost modes) on every
+workload, every printed layer string and random expressions; error paths
+return their status codes before any device call."""
+import ctypes as C
+import os
+import random
+import re
+
+import pytest
+
+import oracle as O
+import workloads as W
+from conftest import ROOT, load_layer_strings
+
+B = pytest.importorskip("paper_2401_03384_amd.binding")
+
+STRINGS = load_layer_strings()
+
+
+def _mask(t):
+    return sum(1 << i for i in O.leaves(t))
+
+
+def _oracle_steps(e, tree, mode="fwd"):
+    steps = O.post_order_steps(tree)
+    costs = O.step_costs(e, tree, "fwd")
+    return [(_mask(a), _mask(b), c) for (a, b), c in zip(steps, costs)]
+
+
+def _plan(spec, shapes, mode=B.CE_COST_FWD, dtype=B.CE_F32, feature=0):
+    e = B.ce_expr_parse(spec, shapes)
+    try:
+        if feature:
+            B.ce_expr_set_feature(e, feature)
+        return B.ce_plan_create(e, mode, dtype, 0)
+    finally:
+        B.ce_expr_destroy(e)
+
+
+def _steps(p):
+    return [B.ce_plan_step(p, i) for i in range(B.ce_plan_num_steps(p))]
+
+
+def test_every_declared_symbol_is_exported():
+    header = open(os.path.join(ROOT, "include", "convein.h")).read()
+    declared = set(re.findall(r"^(?:ce_status|void|const char\*)\s+(ce_[a-z_]+)\s*\(", header,
+                              re.M))
+    L = B.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+        assert isinstance(getattr(L, name), C._CFuncPtr)
+    assert declared == set(B.EXPORTS)
+    assert "gfx950" in B.ce_version()
+
+
+def _compare(spec, shapes, feature=0):
+    e = O.bind(O.parse(spec), shapes, feature_operand=feature)
+    for mode, cmode in (("fwd", B.CE_COST_FWD), ("train_paper", B.CE_COST_TRAIN_PAPER)):
+        tree, cost = O.optimal_tree(e, mode)
+        p = _plan(spec, shapes, cmode, feature=feature)
+        try:
+            assert _steps(p) == _oracle_steps(e, tree), (spec, mode)
+            total, fwd = B.ce_plan_cost(p)
+            assert total == cost
+            assert fwd == O.tree_cost(e, tree, "fwd")
+            assert B.ce_plan_left_to_right_cost(p) == O.tree_cost(e, O.left_to_right_tree(e.n), mode)
+        finally:
+            B.ce_plan_destroy(p)
+
+
+@pytest.mark.parametrize("name", sorted(set(W.WORKLOADS) | set(W.PARITY_WORKLOADS)))
+def test_planner_matches_oracle_on_workloads(name):
+    w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS[name]
+    _compare(w.spec, w.shapes)
+
+
+PAPER_SHAPES = {
+    "standard_conv": [(2, 3, 9, 9), (4, 3, 3, 3)],
+    "cp_conv": [(2, 6, 9, 9), (3, 5), (3, 6), (3, 3), (3, 3)],
+    "rcp_conv": [(2, 2, 3, 2, 9, 9), (4, 2, 2), (4, 3, 3), (4, 2, 2), (4, 3, 3)],
+    "tucker_conv": [(2, 6, 9, 9), (3, 5), (2, 6), (3, 2, 3, 3)],
+    "rtk_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2), (3, 3, 3), (2, 2, 2), (2, 3, 3), (2, 2, 3, 2)],
+    "tt_conv": [(2, 6, 9, 9), (2, 5), (2, 3, 3), (3, 2, 3), (2, 6)],
+    "rtt_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2), (2, 3, 3, 3), (3, 2, 2, 2), (2, 3, 3)],
+    "tr_conv": [(2, 6, 9, 9), (2, 3, 5), (3, 2, 3), (2, 2, 3), (2, 2, 6)],
+    "rtr_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2, 2), (2, 3, 3, 3), (3, 2, 2, 2), (2, 2, 3, 3)],
+    "bt_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2, 2), (2, 2, 3, 3), (2, 2, 2, 2), (2, 2, 3, 3),
+                (2, 2, 2, 2, 2)],
+    "ht_conv": [(1, 2, 3, 2, 9, 9), (2, 2, 2), (2, 3, 3), (2, 2, 2), (2, 3, 3), (2, 2, 2),
+                (2, 2, 2), (2, 2)],
+    "separable_depthwise": [(2, 5, 9, 9), (5, 3), (5, 3)],
+    "interleaved_group": [(2, 2, 3, 9, 9), (4, 2, 3, 3), (5, 3, 3, 3)],
+    "sequencer_example": [(4, 7, 9), (10, 5), (5, 4, 2), (6, 8, 9, 2)],
+    "conv1d": [(2, 3, 11), (4, 3, 3)],
+    "group_conv1d": [(2, 3, 2, 3), (2, 2, 2, 10)],
+    "three_way_contraction": [(2, 3, 4), (3, 5, 3), (4, 4, 5)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(PAPER_SHAPES))
+def test_planner_matches_oracle_on_paper_strings(name):
+    _compare(STRINGS[name][0], PAPER_SHAPES[name])
+
+
+def _random_expr(rnd):
+    n = rnd.randint(2, 6)
+    pool = "abcdefghijk"
+    nl = rnd.randint(2, 8)
+    labels = list(pool[:nl])
+    size = {l: rnd.randint(1, 4) for l in labels}
+    ops = [[] for _ in range(n)]
+    for l in labels:
+        k = rnd.choice([1, 1, 2, 2, 2, 3])
+        for i in rnd.sample(range(n), min(k, n)):
+            ops[i].append(l)
+    for i in range(n):
+        if not ops[i]:
+            ops[i].append(rnd.choice(labels))
+        rnd.shuffle(ops[i])
+    present = sorted({l for t in ops for l in t})
+    holders = {l: [i for i in range(n) if l in ops[i]] for l in present}
+    conv = [l for l in present if len(holders[l]) >= 2 and rnd.random() < 0.3]
+    out = [l for l in present if l in conv or rnd.random() < 0.4]
+    rnd.shuffle(out)
+    shapes = []
+    for i in range(n):
+        shp = []
+        for l in ops[i]:
+            if l in conv:
+                shp.append(rnd.randint(1, 6))
+            else:
+                shp.append(size[l])
+        shapes.append(tuple(shp))
+    spec = ",".join("".join(t) for t in ops) + "->" + "".join(out)
+    if conv:
+        spec += "|" + "".join(conv)
+    return spec, shapes, rnd.randrange(n)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_planner_matches_oracle_on_random_expressions(seed):
+    rnd = random.Random(1000 + seed)
+    for _ in range(6):
+        spec, shapes, feat = _random_expr(rnd)
+        _compare(spec, shapes, feature=feat)
+
+
+def test_user_path_and_left_to_right():
+    w = W.WORKLOADS["C2"]
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    # merged tensors are appended: left-to-right pairs the last entry with position 0
+    p = B.ce_plan_create_with_path(e, [(0, 1), (0, 3), (0, 2), (0, 1)], B.CE_F32, 0)
+    B.ce_expr_destroy(e)
+    oe = O.bind(O.parse(w.spec), w.shapes)
+    ltr = O.left_to_right_tree(5)
+    assert _steps(p) == _oracle_steps(oe, ltr)
+    assert B.ce_plan_cost(p)[0] == O.tree_cost(oe, ltr) == 6576668672
+    # workspace of the left-to-right plan holds the 822M-element intermediate
+    assert B.ce_plan_workspace_size(p, 0) >= 128 * 32 * 64 * 56 * 56 * 4
+    B.ce_plan_destroy(p)
+
+
+def test_workspace_covers_live_intermediates():
+    w = W.WORKLOADS["C2"]
+    p = _plan(w.spec, w.shapes)
+    fwd, bwd = B.ce_plan_workspace_size(p, 0), B.ce_plan_workspace_size(p, 1)
+    inter = 128 * 32 * 56 * 56 * 4
+    assert fwd >= 2 * inter          # two intermediates are live at once
+    assert bwd >= 3 * inter          # three recomputed values, plus gradients
+    B.ce_plan_destroy(p)
+
+
+@pytest.mark.parametrize("spec,shapes,status", [
+    ("bshw,tshw", [(1, 2, 3, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
+    ("bssw,tshw->bthw|hw", [(1, 2, 2, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
+    ("bshw,tshw->bthwx", [(1, 2, 3, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
+    ("bshw,tshw->bt|hw", [(1, 2, 3, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
+    ("bs(h,tshw->bthw", [(1, 2, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
+    ("bshw,tshw->bthw|hw", [(1, 2, 3, 3), (1, 5, 3, 3)], B.CE_ERR_SHAPE),
+    ("bshw,tshw->bthw|hw", [(1, 2, 3), (1, 2, 3, 3)], B.CE_ERR_SHAPE),
+    ("bshw,tshw->bthw|hw", [(1, 2, 3, 3)], B.CE_ERR_SHAPE),
+    ("bshw,tshw->bthw|hw", [(1, 0, 3, 3), (1, 0, 3, 3)], B.CE_ERR_SHAPE),
+])
+def test_errors_are_reported(spec, shapes, status):
+    with pytest.raises(B.CeError) as ex:
+        B.ce_expr_parse(spec, shapes)
+    assert ex.value.status == status
+    assert B.ce_last_error()
+
+
+def test_cost_overflow_is_reported():
+    big = 1 << 30
+    e = B.ce_expr_parse("ab,bc,cd->ad", [(big, big), (big, big), (big, big)])
+    with pytest.raises(B.CeError) as ex:
+        B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, 0)
+    assert ex.value.status == B.CE_ERR_OVERFLOW
+    B.ce_expr_destroy(e)
+
+
+def test_execution_errors_before_any_device_call():
+    """Validation runs before any launch: these return without touching a GPU."""
+    L = B.lib()
+    fake = C.c_void_p(0x1000)
+    ins = (C.c_void_p * 2)(fake, fake)
+    # multi-way convolution: planned, not executable
+    p = _plan("bfhw,fghw,sghw->bshw|hw", [(1, 2, 5, 5), (2, 3, 3, 3), (4, 3, 3, 3)])
+    ins3 = (C.c_void_p * 3)(fake, fake, fake)
+    assert L.ce_forward(p, ins3, fake, fake, 1 << 20, None) == B.CE_ERR_UNSUPPORTED
+    assert "multi-way" in B.ce_last_error()
+    B.ce_plan_destroy(p)
+    p = _plan("bshw,tshw->bthw|hw", [(2, 3, 8, 8), (4, 3, 3, 3)])
+    assert L.ce_forward(p, ins, None, None, 0, None) == B.CE_ERR_ARG
+    assert L.ce_forward(None, ins, fake, None, 0, None) == B.CE_ERR_ARG
+    null_in = (C.c_void_p * 2)(fake, None)
+    assert L.ce_forward(p, null_in, fake, None, 0, None) == B.CE_ERR_ARG
+    din = (C.c_void_p * 2)(None, None)
+    assert L.ce_backward(p, ins, None, din, None, 0, None) == B.CE_ERR_ARG
+    B.ce_plan_destroy(p)
+    # a plan with intermediates: workspace too small / misaligned
+    w = W.PARITY_WORKLOADS["C2s"]
+    p = _plan(w.spec, w.shapes)
+    ins5 = (C.c_void_p * 5)(*([fake] * 5))
+    need = B.ce_plan_workspace_size(p, 0)
+    assert L.ce_forward(p, ins5, fake, fake, need - 1, None) == B.CE_ERR_WORKSPACE
+    assert L.ce_forward(p, ins5, fake, C.c_void_p(0x1008), need, None) == B.CE_ERR_WORKSPACE
+    assert L.ce_forward(p, ins5, fake, None, need, None) == B.CE_ERR_WORKSPACE
+    din5 = (C.c_void_p * 5)(*([fake] * 5))
+    needb = B.ce_plan_workspace_size(p, 1)
+    assert L.ce_backward(p, ins5, fake, din5, fake, needb - 1, None) == B.CE_ERR_WORKSPACE
+    # no gradient wanted: nothing to do, OK without launching
+    none5 = (C.c_void_p * 5)(*([None] * 5))
+    assert L.ce_backward(p, ins5, fake, none5, fake, needb, None) == B.CE_OK
+    B.ce_plan_destroy(p)
+
+
+def test_bad_path_rejected():
+    e = B.ce_expr_parse("ab,bc,cd->ad", [(2, 3), (3, 4), (4, 5)])
+    with pytest.raises(B.CeError) as ex:
+        B.ce_plan_create_with_path(e, [(0, 0), (0, 1)], B.CE_F32, 0)
+    assert ex.value.status == B.CE_ERR_ARG
+    with pytest.raises(B.CeError):
+        B.ce_plan_create_with_path(e, [(0, 1)], B.CE_F32, 0)
+    B.ce_expr_destroy(e)
+
+
+def test_feature_operand_designation():
+    # equal sizes: the designated operand is the feature side
+    spec, shapes = "bsh,tsh->bth|h", [(2, 3, 5), (4, 3, 5)]
+    for feat in (0, 1):
+        e = B.ce_expr_parse(spec, shapes)
+        B.ce_expr_set_feature(e, feat)
+        assert B.ce_expr_output_shape(e) == (2, 4, 5)
+        p = B.ce_plan_create(e, B.CE_COST_TRAIN_PAPER, B.CE_F32, 0)
+        oe = O.bind(O.parse(spec), shapes, feature_operand=feat)
+        assert B.ce_plan_cost(p)[0] == O.tree_cost(oe, (0, 1), "train_paper")
+        B.ce_plan_destroy(p)
+        B.ce_expr_destroy(e)

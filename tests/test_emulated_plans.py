@@ -1,0 +1,141 @@
+"""CPU emulation of generic-kernel plans against the oracle (no GPU).
+
+The host planner is compiled together with a CPU executor of the generic
+kernel's descriptor semantics (tests/cpu_emulator/emulate.cpp, with UBSan);
+every launch's reads and writes are bounds-checked.  Forward and backward of
+every workload at reduced size must match the float64 oracle."""
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from conftest import ROOT
+
+SRC = os.path.join(ROOT, "paper_2401_03384_amd", "csrc")
+
+
+@pytest.fixture(scope="module")
+def emul(tmp_path_factory):
+    out = str(tmp_path_factory.mktemp("emul") / "libce_emul.so")
+    cmd = ["g++", "-O1", "-g", "-shared", "-fPIC", "-std=c++17", "-fsanitize=undefined",
+           "-fno-sanitize-recover=undefined", "-I", os.path.join(ROOT, "include"), "-I", SRC,
+           os.path.join(ROOT, "tests", "cpu_emulator", "emulate.cpp"),
+           os.path.join(SRC, "expr.cpp"), os.path.join(SRC, "plan.cpp"),
+           os.path.join(SRC, "capi.cpp"), "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        pytest.fail(r.stderr)
+    L = C.CDLL(out)
+    L.emul_run.restype = C.c_int
+    return L
+
+
+def _to_storage(a, bf16):
+    a32 = np.ascontiguousarray(a, dtype=np.float32)
+    return W.bf16_bits(a32) if bf16 else a32
+
+
+def _from_storage(a, bf16):
+    if bf16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def _run(L, spec, shapes, bf16, mode, ins, dy=None, out_shape=None, feature=0):
+    n = len(shapes)
+    ranks = (C.c_int * n)(*[len(s) for s in shapes])
+    bufs = [(C.c_int64 * len(s))(*s) for s in shapes]
+    dims = (C.POINTER(C.c_int64) * n)(*[C.cast(b, C.POINTER(C.c_int64)) for b in bufs])
+    st = [_to_storage(a, bf16) for a in ins]
+    inp = (C.c_void_p * n)(*[a.ctypes.data for a in st])
+    err = C.create_string_buffer(512)
+    if mode == 0:
+        out = np.zeros(out_shape, dtype=np.uint16 if bf16 else np.float32)
+        rc = L.emul_run(spec.encode(), n, ranks, dims, int(bf16), 0, inp, out.ctypes.data_as(C.c_void_p),
+                        None, None, err, 512)
+        assert rc == 0, err.value.decode()
+        return _from_storage(out, bf16)
+    d = _to_storage(dy, bf16)
+    grads = [np.zeros(s, dtype=(np.uint16 if (bf16 and i == feature) else np.float32))
+             for i, s in enumerate(shapes)]
+    din = (C.c_void_p * n)(*[g.ctypes.data for g in grads])
+    rc = L.emul_run(spec.encode(), n, ranks, dims, int(bf16), 1, inp, None,
+                    d.ctypes.data_as(C.c_void_p), din, err, 512)
+    assert rc == 0, err.value.decode()
+    return [_from_storage(g, bf16 and i == feature) for i, g in enumerate(grads)]
+
+
+def _rel(a, b):
+    return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+
+
+# the parity strings at sizes a CPU emulation finishes quickly (ragged spatial sizes)
+CASES = {
+    "C1": W.PARITY_WORKLOADS["C1"],
+    "C2s": W.PARITY_WORKLOADS["C2s"],
+    "C2s_bf16": W.PARITY_WORKLOADS["C2s_bf16"],
+    "C3t": W.tucker2_layer("C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21),
+    "C3t_f32": W.tucker2_layer("C3t_f32", 2, 32, 24, 7, 9, 8, 16, 3, "f32", 21),
+    "C4t": W.rtt_layer("C4t", 1, (2, 4, 2), (2, 2, 4), 7, 6, 4, 3, "f32", 22),
+    "C5at": W.rcp_layer("C5at", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "bf16", 23),
+    "C5at_f32": W.rcp_layer("C5at_f32", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "f32", 23),
+    "C5bt": W.rcp_layer("C5bt", 1, (2, 2, 4), (2, 2, 4), 9, 8, 16, 5, "bf16", 24),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_emulated_generic_plan_matches_oracle(emul, name):
+    w = CASES[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    y_ref = O.eval_pairwise(e, ins, tree)
+    y = _run(emul, w.spec, w.shapes, bf16, 0, ins, out_shape=w.out_shape)
+    assert _rel(y, y_ref) <= tol
+    if not w.backward:
+        return
+    g_ref = O.grads_pairwise(e, ins, tree, dy)
+    g = _run(emul, w.spec, w.shapes, bf16, 1, ins, dy=dy)
+    for i, (a, b) in enumerate(zip(g, g_ref)):
+        assert _rel(a, b) <= tol, (name, i, _rel(a, b))
+
+
+@pytest.mark.parametrize("spec,shapes", [
+    ("bsh,tsh->bth|h", [(2, 3, 11), (4, 3, 4)]),                 # even filter
+    ("tsh,bsh->bth|h", [(4, 3, 3), (2, 3, 9)]),                  # feature second
+    ("bshw,sh,sw->bshw|hw", [(2, 3, 7, 6), (3, 3), (3, 5)]),     # depthwise
+    ("bsm,mt->bt", [(2, 3, 4), (4, 5)]),                          # self-contraction
+    ("ij->ji", [(3, 4)]),                                         # single operand
+    ("ijk->i", [(3, 4, 2)]),                                      # single operand, sums
+    ("bshw,(r1)t,(r1)(r2)h,(r2)(r3)w,(r3)s->bthw|hw",
+     [(2, 3, 6, 5), (2, 4), (2, 3, 3), (3, 2, 3), (2, 3)]),       # tensor-train
+    ("bshw,(r0)(r1)t,(r1)(r2)h,(r2)(r3)w,(r3)(r0)s->bthw|hw",
+     [(1, 3, 6, 5), (2, 2, 4), (2, 2, 3), (2, 2, 3), (2, 2, 3)]),  # tensor-ring
+])
+def test_emulated_generic_plan_edge_cases(emul, spec, shapes):
+    e = O.bind(O.parse(spec), shapes)
+    g0 = np.random.default_rng(3)
+    ins = [g0.standard_normal(s).astype(np.float32).astype(np.float64) for s in shapes]
+    out_shape = tuple(e.out_sizes[l] for l in e.output)
+    dy = g0.standard_normal(out_shape).astype(np.float32).astype(np.float64)
+    tree = O.optimal_tree(e)[0] if e.n > 1 else 0
+    y_ref = O.eval_pairwise(e, ins, tree)
+    y = _run(emul, spec, shapes, False, 0, ins, out_shape=out_shape)
+    assert _rel(y, y_ref) <= 1e-6
+    if e.n > 1:
+        g_ref = O.grads_pairwise(e, ins, tree, dy)
+    else:
+        g_ref = [np.broadcast_to(np.einsum(
+            "".join(chr(97 + k) for k in range(len(e.output))) + "->" +
+            "".join(chr(97 + e.output.index(l)) if l in e.output else "" for l in e.inputs[0]),
+            dy).reshape([s if l in e.output else 1 for l, s in zip(e.inputs[0], shapes[0])]),
+            shapes[0])]
+    g = _run(emul, spec, shapes, False, 1, ins, dy=dy)
+    for a, b in zip(g, g_ref):
+        assert _rel(a, b) <= 1e-6

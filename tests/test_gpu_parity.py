@@ -1,0 +1,144 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Reduced sizes compare every element of Y and of every gradient with the
+oracle's pairwise evaluation; full sizes compare with the oracle's dense
+evaluation.  Bar: rel-L2 <= 1e-5 for float32, <= 2e-2 for bfloat16 inputs.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def P():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a HIP device")
+    import paper_2401_03384_amd as P
+    P.lib()
+    return P
+
+
+def _dev(a, bf16):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return (t.to(torch.bfloat16) if bf16 else t).cuda()
+
+
+def _host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _rel(a, b):
+    return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+PARITY = sorted(W.PARITY_WORKLOADS)
+
+
+@pytest.mark.parametrize("generic", [False, True], ids=["default", "generic"])
+@pytest.mark.parametrize("name", PARITY)
+def test_parity_reduced(P, name, generic):
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} generic={generic} shapes={w.shapes}")
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    y_ref = O.eval_pairwise(e, ins, tree)
+    plan = P.Plan(w.spec, w.shapes, w.dtype, flags=P.CE_FLAG_GENERIC_ONLY if generic else 0)
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    torch.cuda.synchronize()
+    assert _rel(_host(y), y_ref) <= tol
+    if not w.backward:
+        return
+    g_ref = O.grads_pairwise(e, ins, tree, dy)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    for i, (g, r) in enumerate(zip(grads, g_ref)):
+        err = _rel(_host(g), r)
+        assert err <= tol, (name, i, err)
+
+
+@pytest.mark.parametrize("name", ["C2s", "C3s_f32", "C5bs"])
+def test_deterministic(P, name):
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    ins, dy = W.make_inputs(w)
+    plan = P.Plan(w.spec, w.shapes, w.dtype)
+    xs = [_dev(a, bf16) for a in ins]
+    d = _dev(dy, bf16)
+    y1, y2 = plan.forward(xs), plan.forward(xs)
+    g1, g2 = plan.backward(xs, d), plan.backward(xs, d)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
+
+
+def test_partial_gradients(P):
+    """NULL gradient entries are skipped; the others are unchanged."""
+    w = W.PARITY_WORKLOADS["C2s"]
+    ins, dy = W.make_inputs(w)
+    plan = P.Plan(w.spec, w.shapes, w.dtype)
+    xs = [_dev(a, False) for a in ins]
+    d = _dev(dy, False)
+    full = plan.backward(xs, d)
+    part = plan.backward(xs, d, needs=[False, True, False, False, True])
+    torch.cuda.synchronize()
+    assert part[0] is None and part[2] is None
+    assert torch.equal(part[1], full[1]) and torch.equal(part[4], full[4])
+
+
+def test_autograd_function(P):
+    w = W.PARITY_WORKLOADS["C2s"]
+    ins, dy = W.make_inputs(w)
+    xs = [_dev(a, False).requires_grad_(True) for a in ins]
+    y = P.conv_einsum(w.spec, *xs)
+    y.backward(_dev(dy, False))
+    e = O.bind(O.parse(w.spec), w.shapes)
+    g_ref = O.grads_dense(e, ins, dy)
+    for x, r in zip(xs, g_ref):
+        assert _rel(_host(x.grad), r) <= 1e-5
+
+
+FULL = ["C1", "C2", "C2_bf16", "C3", "C4", "C5a", "C5b"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_parity_full_size(P, name):
+    """Full-size layers against the oracle's dense evaluation (float64)."""
+    w = W.WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} full size shapes={w.shapes}")
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    plan = P.Plan(w.spec, w.shapes, w.dtype)
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    torch.cuda.synchronize()
+    assert _rel(_host(y), O.eval_dense(e, ins)) <= tol
+    del y
+    if not w.backward:
+        return
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    g_ref = O.grads_dense(e, ins, dy)
+    for i, (g, r) in enumerate(zip(grads, g_ref)):
+        err = _rel(_host(g), r)
+        _say(f"  grad {i} rel-L2 {err:.3e}")
+        assert err <= tol, (name, i, err)

@@ -24,8 +24,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "PARITY_WORKLOADS", "make_inputs",
-           "round_to_bf16", "bf16_bits", "f32_bits"]
+__all__ = ["Workload", "WORKLOADS", "PARITY_WORKLOADS", "make_inputs", "cp_layer",
+           "tucker2_layer", "rtt_layer", "rcp_layer", "round_to_bf16", "bf16_bits", "f32_bits"]
 
 
 @dataclass(frozen=True)
@@ -48,7 +48,7 @@ def _kaiming_sigma(fan_in: int, ranks: int, n_factors: int) -> float:
     return (2.0 / (fan_in * ranks)) ** (1.0 / (2 * n_factors))
 
 
-def _cp(name, b, s, t, h, w, r, k, dtype, seed, backward=True, sig=None, note=""):
+def cp_layer(name, b, s, t, h, w, r, k, dtype, seed, backward=True, sig=None, note=""):
     spec = "bshw,rs,rt,rh,rw->bthw|hw"
     shapes = ((b, s, h, w), (r, s), (r, t), (r, k), (r, k))
     if sig is None:
@@ -57,14 +57,14 @@ def _cp(name, b, s, t, h, w, r, k, dtype, seed, backward=True, sig=None, note=""
     return Workload(name, spec, shapes, dtype, seed, tuple(sig), (b, t, h, w), backward, note)
 
 
-def _tucker2(name, b, s, t, h, w, p, q, k, dtype, seed, note=""):
+def tucker2_layer(name, b, s, t, h, w, p, q, k, dtype, seed, note=""):
     spec = "bshw,sp,pqhw,qt->bthw|hw"
     shapes = ((b, s, h, w), (s, p), (p, q, k, k), (q, t))
     sg = _kaiming_sigma(s * k * k, p * q, 3)
     return Workload(name, spec, shapes, dtype, seed, (1.0, sg, sg, sg), (b, t, h, w), True, note)
 
 
-def _rtt(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
+def rtt_layer(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
     spec = ("b(s1)(s2)(s3)hw,(r1)(t1)(s1),(r1)(r2)(t2)(s2),(r2)(r3)(t3)(s3),(r3)hw"
             "->b(t1)(t2)(t3)hw|hw")
     s1, s2, s3 = s3s
@@ -75,7 +75,7 @@ def _rtt(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
                     (b, t1, t2, t3, h, w), True, note)
 
 
-def _rcp(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
+def rcp_layer(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
     spec = "b(s1)(s2)(s3)hw,r(t1)(s1),r(t2)(s2),r(t3)(s3),rhw->b(t1)(t2)(t3)hw|hw"
     s1, s2, s3 = s3s
     t1, t2, t3 = t3s
@@ -88,20 +88,20 @@ def _rcp(name, b, s3s, t3s, h, w, r, k, dtype, seed, note=""):
 # Full-size layers.  C1 uses std 1/sqrt(fan), fan = the size summed when the
 # factor is applied (U_s: s, U_t: r, K_h/K_w: taps).
 WORKLOADS = {
-    "C1": _cp("C1", 2, 16, 16, 8, 8, 8, 3, "f32", 1, backward=False,
+    "C1": cp_layer("C1", 2, 16, 16, 8, 8, 8, 3, "f32", 1, backward=False,
               sig=(1.0, 1 / math.sqrt(16), 1 / math.sqrt(8), 1 / math.sqrt(3), 1 / math.sqrt(3)),
               note="CP 3x3, tiny, forward only"),
-    "C2": _cp("C2", 128, 64, 64, 56, 56, 32, 3, "f32", 2,
+    "C2": cp_layer("C2", 128, 64, 64, 56, 56, 32, 3, "f32", 2,
               note="CP 3x3, ResNet stage-1 shape, rank 32"),
-    "C2_bf16": _cp("C2_bf16", 128, 64, 64, 56, 56, 32, 3, "bf16", 2,
+    "C2_bf16": cp_layer("C2_bf16", 128, 64, 64, 56, 56, 32, 3, "bf16", 2,
                    note="CP 3x3, ResNet stage-1 shape, rank 32, bf16 inputs"),
-    "C3": _tucker2("C3", 128, 256, 256, 14, 14, 64, 64, 3, "bf16", 3,
+    "C3": tucker2_layer("C3", 128, 256, 256, 14, 14, 64, 64, 3, "bf16", 3,
                    note="Tucker-2 3x3, core 64x64"),
-    "C4": _rtt("C4", 64, (4, 8, 8), (4, 8, 8), 28, 28, 16, 3, "f32", 4,
+    "C4": rtt_layer("C4", 64, (4, 8, 8), (4, 8, 8), 28, 28, 16, 3, "f32", 4,
                note="reshaped tensor-train 3x3, channels 4x8x8, TT rank 16"),
-    "C5a": _rcp("C5a", 32, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 5,
+    "C5a": rcp_layer("C5a", 32, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 5,
                 note="reshaped CP 3x3, channels 8x8x8, rank 64, 7x7"),
-    "C5b": _rcp("C5b", 32, (4, 4, 8), (4, 4, 8), 28, 28, 64, 5, "bf16", 6,
+    "C5b": rcp_layer("C5b", 32, (4, 4, 8), (4, 4, 8), 28, 28, 64, 5, "bf16", 6,
                 note="reshaped CP 5x5, channels 4x4x8, rank 64, 28x28"),
 }
 
@@ -109,14 +109,14 @@ WORKLOADS = {
 # seconds while still spanning several kernel tiles and a ragged tail.
 PARITY_WORKLOADS = {
     "C1": WORKLOADS["C1"],
-    "C2s": _cp("C2s", 2, 64, 64, 19, 19, 32, 3, "f32", 12),
-    "C2s_bf16": _cp("C2s_bf16", 2, 64, 64, 19, 19, 32, 3, "bf16", 12),
-    "C3s": _tucker2("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
-    "C3s_f32": _tucker2("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
-    "C4s": _rtt("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
-    "C5as": _rcp("C5as", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 15),
-    "C5as_f32": _rcp("C5as_f32", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "f32", 15),
-    "C5bs": _rcp("C5bs", 2, (4, 4, 8), (4, 4, 8), 11, 11, 64, 5, "bf16", 16),
+    "C2s": cp_layer("C2s", 2, 64, 64, 19, 19, 32, 3, "f32", 12),
+    "C2s_bf16": cp_layer("C2s_bf16", 2, 64, 64, 19, 19, 32, 3, "bf16", 12),
+    "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
+    "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
+    "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
+    "C5as": rcp_layer("C5as", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 15),
+    "C5as_f32": rcp_layer("C5as_f32", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "f32", 15),
+    "C5bs": rcp_layer("C5bs", 2, (4, 4, 8), (4, 4, 8), 11, 11, 64, 5, "bf16", 16),
 }
 
 
