@@ -40,6 +40,65 @@ enum KernelKind : int32_t {
     K_GENERIC_THREAD = 1,   // one thread per output element
     K_GENERIC_WAVE = 2,     // one 64-lane wavefront per output element
     K_GENERIC_BLOCK = 3,    // one 256-thread block per output element
+    K_GEMM = 16,            // channel-mixing GEMM (GemmDesc)
+    K_WGRAD = 17,           // split-reduction NT GEMM into partials (WgradDesc)
+    K_REDUCE = 18,          // ordered sum of partials (ReduceDesc)
+    K_DW = 19,              // depthwise convolution along one axis (DwDesc)
+    K_DW_TAPGRAD = 20,      // per-block partial filter-tap gradients (DwDesc)
+    K_DW_TAPREDUCE = 21,    // ordered sum of tap partials (DwDesc)
+};
+
+// Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
+constexpr int32_t kBitIn = 8;     // main inputs
+constexpr int32_t kBitAux = 9;    // second input (filter / factor) when it may differ
+constexpr int32_t kBitOut = 10;   // output
+constexpr int32_t kShiftOpt = 12; // kernel-specific option bits
+
+// C[g][m][n] = sum_k A[g][m][k] * B[g][k][n] with n unit-stride in B and C.
+// A is the small operand (a factor), B and C the large ones (activations).
+// Blocks: ntiles x mtiles x prod(g_size), flattened.
+struct GemmDesc {
+    int32_t M, N, K;
+    int32_t ng;
+    int64_t g_size[3], g_sA[3], g_sB[3], g_sC[3];
+    int64_t sAm, sAk, sBk, sCm;
+    int32_t mtiles, ntiles;
+    int64_t blocks;
+};
+
+// partial[s][m][n] = sum over reduction chunk s of A[kb][m][k] * B[kb][n][k]
+// with k unit-stride in A and B; s = (kb index) * ksplit + (k chunk).
+struct WgradDesc {
+    int32_t M, N;
+    int64_t K;                 // unit-stride reduction length
+    int32_t nkb;
+    int64_t kb_size[3], kb_sA[3], kb_sB[3];
+    int64_t sAm, sBn;
+    int32_t ksplit, kchunk;    // chunks of k per kb index and their length
+    int64_t nsplit;            // number of partials
+    int32_t mtiles, ntiles;
+    int64_t blocks;
+};
+
+// C[m * sCm + n * sCn] = sum_{s < nsplit} partial[s][m][n]
+struct ReduceDesc {
+    int32_t M, N;
+    int64_t nsplit;
+    int64_t sCm, sCn;
+};
+
+// Depthwise convolution along one axis of a dense tensor viewed as
+// [nslab][A][inner]: out[o][p][q] = sum_j in[o][p + sign*j + off][q] * f[frow(o) + j*f_sj]
+// with in zero outside [0, A) and frow(o) = ((o / r_div) % r_size) * r_stride.
+// A block covers spb consecutive slabs.  For the tap gradient the same view
+// gives part[block][j] = sum in[o][p + j + off][q] * g[o][p][q], reduced over the
+// blocks sharing a filter row into out[r * o_sr + j * o_sj].
+struct DwDesc {
+    int64_t nslab;
+    int32_t A, inner, K, sign, off, spb;
+    int64_t r_div, r_size, r_stride, f_sj;
+    int64_t nblocks;
+    int64_t o_sr, o_sj;        // tap reduce: output strides
 };
 
 }  // namespace ce

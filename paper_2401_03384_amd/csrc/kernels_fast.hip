@@ -1,14 +1,581 @@
-// Specialised kernels: dispatch by launch kind.
+// Specialised kernels for the pairwise steps of tensorial convolution layers
+// on gfx950 (wave64, MFMA, 160 KB LDS per CU).
+//
+//  gemm_f32 / gemm_bf16   channel mixing C[g][m][n] = sum_k A[m][k] B[g][k][n]:
+//                         the factor A is staged in LDS, the activation B
+//                         streams through LDS in coalesced 16-byte rows, the
+//                         product runs on 32x32 MFMA tiles (fp32: 32x32x2,
+//                         bf16: 32x32x16), results go straight from the
+//                         accumulators to HBM with unit-stride rows.
+//  wgrad                  factor gradients sum_{kb,k} A[kb][m][k] B[kb][n][k]:
+//                         each block reduces one chunk of the long unit-stride
+//                         reduction into a 64x64 partial tile.
+//  reduce_partials        ordered (deterministic) sum of the partial tiles.
+//  dw_conv                depthwise convolution along one axis (forward, or
+//                         transposed for the feature gradient): whole lines
+//                         of the axis are staged in LDS, taps in registers.
+//  dw_tapgrad / reduce    filter-tap gradients: per-block partial sums, then
+//                         an ordered reduction over the blocks of each row.
+#include <cstring>
+
 #include "desc.h"
 #include "hip_util.h"
 #include "kernels.h"
 
 namespace ce {
+namespace {
+
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+
+__device__ __forceinline__ bf16x8 lds_bf16x8(const bf16_t* p) {
+    bf16x8 v;
+    __builtin_memcpy(&v, p, 16);
+    return v;
+}
+
+// Row of the 32x32 MFMA result held by accumulator r of a lane.
+__device__ __forceinline__ int mfma32_row(int r, int lane) {
+    return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+// ---------------------------------------------------------------------------
+// channel-mixing GEMM
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void gemm_offsets(const GemmDesc& d, int64_t g, int64_t& oA,
+                                             int64_t& oB, int64_t& oC) {
+    oA = oB = oC = 0;
+    for (int i = d.ng - 1; i >= 0; --i) {
+        int64_t x = g % d.g_size[i];
+        g /= d.g_size[i];
+        oA += x * d.g_sA[i];
+        oB += x * d.g_sB[i];
+        oC += x * d.g_sC[i];
+    }
+}
+
+template <typename TC, int MT, bool VEC>
+__global__ void __launch_bounds__(256) gemm_f32(GemmDesc d, const float* __restrict__ A,
+                                                const float* __restrict__ B,
+                                                TC* __restrict__ C) {
+    constexpr int TM = 32 * MT, TN = 128, TK = 32;
+    __shared__ float As[TM][TK + 1];
+    __shared__ __attribute__((aligned(16))) float Bs[TK][TN + 4];
+    int64_t bid = blockIdx.x;
+    const int nt = (int)(bid % d.ntiles);
+    bid /= d.ntiles;
+    const int mt = (int)(bid % d.mtiles);
+    bid /= d.mtiles;
+    int64_t oA, oB, oC;
+    gemm_offsets(d, bid, oA, oB, oC);
+    const int m0 = mt * TM, n0 = nt * TN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    f32x16 acc[MT];
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
+
+    for (int k0 = 0; k0 < d.K; k0 += TK) {
+        for (int e = tid; e < TM * TK; e += 256) {
+            int mm = e / TK, kk = e % TK, m = m0 + mm, k = k0 + kk;
+            As[mm][kk] = (m < d.M && k < d.K) ? A[oA + (int64_t)m * d.sAm + (int64_t)k * d.sAk] : 0.f;
+        }
+#pragma unroll
+        for (int it = 0; it < TK * TN / 4 / 256; it++) {
+            int e = tid + it * 256;
+            int kk = e / (TN / 4), nn = (e % (TN / 4)) * 4, k = k0 + kk, n = n0 + nn;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (k < d.K) {
+                const float* p = B + oB + (int64_t)k * d.sBk + n;
+                if (VEC && n + 3 < d.N) {
+                    v = *(const f32x4*)p;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        if (n + j < d.N) v[j] = p[j];
+                }
+            }
+            *(f32x4*)&Bs[kk][nn] = v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < TK; kk += 2) {
+            float b = Bs[kk + (lane >> 5)][wave * 32 + (lane & 31)];
+#pragma unroll
+            for (int i = 0; i < MT; i++) {
+                float a = As[i * 32 + (lane & 31)][kk + (lane >> 5)];
+                acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[i], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    const int n = n0 + wave * 32 + (lane & 31);
+    if (n >= d.N) return;
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+            int m = m0 + i * 32 + mfma32_row(r, lane);
+            if (m < d.M) store(C, oC + (int64_t)m * d.sCm + n, acc[i][r]);
+        }
+}
+
+template <typename TC, int MT, bool VEC>
+__global__ void __launch_bounds__(256) gemm_bf16(GemmDesc d, const bf16_t* __restrict__ A,
+                                                 const bf16_t* __restrict__ B,
+                                                 TC* __restrict__ C) {
+    constexpr int TM = 32 * MT, TN = 128, TK = 32, LDK = TK + 8;
+    __shared__ __attribute__((aligned(16))) bf16_t As[TM][LDK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[TN][LDK];   // transposed: [n][k]
+    int64_t bid = blockIdx.x;
+    const int nt = (int)(bid % d.ntiles);
+    bid /= d.ntiles;
+    const int mt = (int)(bid % d.mtiles);
+    bid /= d.mtiles;
+    int64_t oA, oB, oC;
+    gemm_offsets(d, bid, oA, oB, oC);
+    const int m0 = mt * TM, n0 = nt * TN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    f32x16 acc[MT];
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
+
+    const int nn = (tid & 31) * 4, kq = (tid >> 5) * 4;
+    for (int k0 = 0; k0 < d.K; k0 += TK) {
+        for (int e = tid; e < TM * TK; e += 256) {
+            int mm = e / TK, kk = e % TK, m = m0 + mm, k = k0 + kk;
+            As[mm][kk] = (m < d.M && k < d.K) ? A[oA + (int64_t)m * d.sAm + (int64_t)k * d.sAk]
+                                              : (bf16_t)0;
+        }
+        // 4 k-rows x 4 n-columns per thread, written transposed as 4-element k-runs
+        bf16_t v[4][4];
+        const int n = n0 + nn;
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+            int k = k0 + kq + r;
+#pragma unroll
+            for (int j = 0; j < 4; j++) v[r][j] = 0;
+            if (k < d.K) {
+                const bf16_t* p = B + oB + (int64_t)k * d.sBk + n;
+                if (VEC && n + 3 < d.N) {
+                    uint2 raw = *(const uint2*)p;
+                    v[r][0] = (bf16_t)(raw.x & 0xffff);
+                    v[r][1] = (bf16_t)(raw.x >> 16);
+                    v[r][2] = (bf16_t)(raw.y & 0xffff);
+                    v[r][3] = (bf16_t)(raw.y >> 16);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        if (n + j < d.N) v[r][j] = p[j];
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            uint2 w;
+            w.x = (uint32_t)v[0][j] | ((uint32_t)v[1][j] << 16);
+            w.y = (uint32_t)v[2][j] | ((uint32_t)v[3][j] << 16);
+            *(uint2*)&Bs[nn + j][kq] = w;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < TK; kk += 16) {
+            bf16x8 b = lds_bf16x8(&Bs[wave * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+#pragma unroll
+            for (int i = 0; i < MT; i++) {
+                bf16x8 a = lds_bf16x8(&As[i * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+                acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    const int n = n0 + wave * 32 + (lane & 31);
+    if (n >= d.N) return;
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+            int m = m0 + i * 32 + mfma32_row(r, lane);
+            if (m < d.M) store(C, oC + (int64_t)m * d.sCm + n, acc[i][r]);
+        }
+}
+
+// ---------------------------------------------------------------------------
+// factor gradients: partial NT GEMM over a chunk of the reduction
+// ---------------------------------------------------------------------------
+template <typename T, bool VEC>
+__global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ A,
+                                             const T* __restrict__ B, float* __restrict__ part) {
+    constexpr int TM = 64, TN = 64, TK = 32;
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int LDK = BF ? TK + 8 : TK + 1;
+    __shared__ __attribute__((aligned(16))) T As[TM][LDK];
+    __shared__ __attribute__((aligned(16))) T Bs[TN][LDK];
+    int64_t bid = blockIdx.x;
+    const int nt = (int)(bid % d.ntiles);
+    bid /= d.ntiles;
+    const int mt = (int)(bid % d.mtiles);
+    bid /= d.mtiles;
+    const int64_t s = bid;                       // partial index
+    int64_t kbi = s / d.ksplit;
+    const int kc = (int)(s % d.ksplit);
+    int64_t oA = 0, oB = 0;
+    for (int i = d.nkb - 1; i >= 0; --i) {
+        int64_t x = kbi % d.kb_size[i];
+        kbi /= d.kb_size[i];
+        oA += x * d.kb_sA[i];
+        oB += x * d.kb_sB[i];
+    }
+    const int64_t kbeg = (int64_t)kc * d.kchunk;
+    const int64_t kend = min(d.K, kbeg + d.kchunk);
+    const int m0 = mt * TM, n0 = nt * TN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; r++) acc[r] = 0.f;
+
+    for (int64_t k0 = kbeg; k0 < kend; k0 += TK) {
+        // 64 rows x 32 k per operand: 4-element runs along k, 2 per thread per operand
+#pragma unroll
+        for (int it = 0; it < 2; it++) {
+            int e = tid + it * 256;
+            int row = e >> 3, kk = (e & 7) * 4;
+            int64_t k = k0 + kk;
+#pragma unroll
+            for (int op = 0; op < 2; op++) {
+                const T* src = op ? B : A;
+                int base_row = op ? n0 : m0;
+                int lim = op ? d.N : d.M;
+                int64_t o = op ? oB : oA;
+                int64_t sr = op ? d.sBn : d.sAm;
+                T (*dst)[LDK] = op ? Bs : As;
+                T v[4] = {0, 0, 0, 0};
+                int rr = base_row + row;
+                if (rr < lim) {
+                    const T* p = src + o + (int64_t)rr * sr + k;
+                    if (VEC && k + 3 < kend) {
+                        if constexpr (BF) {
+                            uint2 raw = *(const uint2*)p;
+                            v[0] = (T)(raw.x & 0xffff);
+                            v[1] = (T)(raw.x >> 16);
+                            v[2] = (T)(raw.y & 0xffff);
+                            v[3] = (T)(raw.y >> 16);
+                        } else {
+                            f32x4 raw = *(const f32x4*)p;
+                            __builtin_memcpy(v, &raw, 16);
+                        }
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; j++)
+                            if (k + j < kend) v[j] = p[j];
+                    }
+                }
+                if constexpr (BF) {
+                    uint2 w;
+                    w.x = (uint32_t)(uint16_t)v[0] | ((uint32_t)(uint16_t)v[1] << 16);
+                    w.y = (uint32_t)(uint16_t)v[2] | ((uint32_t)(uint16_t)v[3] << 16);
+                    *(uint2*)&dst[row][kk] = w;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; j++) dst[row][kk + j] = v[j];
+                }
+            }
+        }
+        __syncthreads();
+        if constexpr (BF) {
+#pragma unroll
+            for (int kk = 0; kk < TK; kk += 16) {
+                bf16x8 a = lds_bf16x8((const bf16_t*)&As[wm * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+                bf16x8 b = lds_bf16x8((const bf16_t*)&Bs[wn * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < TK; kk += 2) {
+                float a = (float)As[wm * 32 + (lane & 31)][kk + (lane >> 5)];
+                float b = (float)Bs[wn * 32 + (lane & 31)][kk + (lane >> 5)];
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    const int n = n0 + wn * 32 + (lane & 31);
+    if (n >= d.N) return;
+    float* out = part + s * (int64_t)d.M * d.N;
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+        int m = m0 + wm * 32 + mfma32_row(r, lane);
+        if (m < d.M) out[(int64_t)m * d.N + n] = acc[r];
+    }
+}
+
+template <typename TC>
+__global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float* __restrict__ part,
+                                                       TC* __restrict__ C) {
+    int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    int64_t mn = (int64_t)d.M * d.N;
+    if (e >= mn) return;
+    double acc = 0.0;
+    for (int64_t s = 0; s < d.nsplit; s++) acc += part[s * mn + e];
+    int64_t m = e / d.N, n = e - m * d.N;
+    store(C, m * d.sCm + n * d.sCn, (float)acc);
+}
+
+// ---------------------------------------------------------------------------
+// depthwise convolution along one axis
+// ---------------------------------------------------------------------------
+constexpr int kDwLds = 4096;   // elements of a block's region staged in LDS
+constexpr int kDwMaxSlabs = 256;
+
+template <typename T, typename TF, typename TC, int KT>
+__global__ void __launch_bounds__(256) dw_conv(DwDesc d, const T* __restrict__ in,
+                                               const TF* __restrict__ f, TC* __restrict__ out) {
+    __shared__ float buf[kDwLds];
+    __shared__ float taps[kDwMaxSlabs][KT];
+    const int64_t slab0 = (int64_t)blockIdx.x * d.spb;
+    const int nsl = (int)min((int64_t)d.spb, d.nslab - slab0);
+    const int slabsz = d.A * d.inner;
+    const int total = nsl * slabsz;
+    const int64_t base = slab0 * slabsz;
+    const int tid = threadIdx.x;
+    for (int e = tid; e < total; e += 256) buf[e] = load(in, base + e);
+    for (int e = tid; e < nsl * KT; e += 256) {
+        int sl = e / KT, j = e - sl * KT;
+        int64_t o = slab0 + sl;
+        int64_t frow = ((o / d.r_div) % d.r_size) * d.r_stride;
+        taps[sl][j] = load(f, frow + (int64_t)j * d.f_sj);
+    }
+    __syncthreads();
+    for (int e = tid; e < total; e += 256) {
+        int sl = e / slabsz, rem = e - sl * slabsz, p = rem / d.inner, q = rem - p * d.inner;
+        const float* row = buf + sl * slabsz + q;
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < KT; j++) {
+            int pp = p + d.sign * j + d.off;
+            if (pp >= 0 && pp < d.A) acc += row[pp * d.inner] * taps[sl][j];
+        }
+        store(out, base + e, acc);
+    }
+}
+
+// part[block][j] = sum over the block's region of in[p + j + off] * g[p]
+template <typename T, int KT>
+__global__ void __launch_bounds__(256) dw_tapgrad(DwDesc d, const T* __restrict__ in,
+                                                  const T* __restrict__ g, float* __restrict__ part) {
+    __shared__ float buf[kDwLds];
+    __shared__ float red[4][KT];
+    const int64_t slab0 = (int64_t)blockIdx.x * d.spb;
+    const int nsl = (int)min((int64_t)d.spb, d.nslab - slab0);
+    const int slabsz = d.A * d.inner;
+    const int total = nsl * slabsz;
+    const int64_t base = slab0 * slabsz;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int e = tid; e < total; e += 256) buf[e] = load(in, base + e);
+    __syncthreads();
+    float acc[KT];
+#pragma unroll
+    for (int j = 0; j < KT; j++) acc[j] = 0.f;
+    for (int e = tid; e < total; e += 256) {
+        int sl = e / slabsz, rem = e - sl * slabsz, p = rem / d.inner, q = rem - p * d.inner;
+        const float* row = buf + sl * slabsz + q;
+        float gv = load(g, base + e);
+#pragma unroll
+        for (int j = 0; j < KT; j++) {
+            int pp = p + j + d.off;
+            if (pp >= 0 && pp < d.A) acc[j] += row[pp * d.inner] * gv;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < KT; j++) {
+        float v = wave_sum(acc[j]);
+        if (lane == 0) red[wave][j] = v;
+    }
+    __syncthreads();
+    if (tid < KT) part[blockIdx.x * (int64_t)KT + tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+}
+
+// out[r][j] = sum over the blocks whose slabs use filter row r (block order)
+template <typename TC>
+__global__ void __launch_bounds__(256) dw_tapreduce(DwDesc d, const float* __restrict__ part,
+                                                    TC* __restrict__ out) {
+    int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= d.r_size * d.K) return;
+    int64_t r = t / d.K, j = t - r * d.K;
+    int64_t run = d.r_div / d.spb;              // consecutive blocks of one row
+    int64_t period = run * d.r_size;
+    int64_t reps = d.nblocks / period;
+    double acc = 0.0;
+    for (int64_t a = 0; a < reps; a++)
+        for (int64_t c = 0; c < run; c++) acc += part[(a * period + r * run + c) * d.K + j];
+    store(out, r * d.o_sr + j * d.o_sj, (float)acc);
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <typename D>
+D desc_of(const Launch& ln) {
+    D d;
+    std::memcpy(&d, ln.desc.data(), sizeof(D));
+    return d;
+}
+
+hipError_t launch_gemm(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s) {
+    GemmDesc d = desc_of<GemmDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    int opt = ln.kind >> kShiftOpt;
+    int MT = (opt & 1) ? 2 : 1;
+    // vector loads need 16 B (fp32) / 8 B (bf16) aligned rows of B
+    bool vec = (opt & 2) && ((uintptr_t)b % (tIn ? 8 : 16) == 0);
+    dim3 g(ln.grid[0]), bl(256);
+    if (tIn) {
+        const bf16_t* A = (const bf16_t*)a;
+        const bf16_t* B = (const bf16_t*)b;
+        if (tC) {
+            if (MT == 2) { if (vec) hipLaunchKernelGGL((gemm_bf16<bf16_t, 2, true>), g, bl, 0, s, d, A, B, (bf16_t*)c);
+                           else hipLaunchKernelGGL((gemm_bf16<bf16_t, 2, false>), g, bl, 0, s, d, A, B, (bf16_t*)c); }
+            else { if (vec) hipLaunchKernelGGL((gemm_bf16<bf16_t, 1, true>), g, bl, 0, s, d, A, B, (bf16_t*)c);
+                   else hipLaunchKernelGGL((gemm_bf16<bf16_t, 1, false>), g, bl, 0, s, d, A, B, (bf16_t*)c); }
+        } else {
+            if (MT == 2) { if (vec) hipLaunchKernelGGL((gemm_bf16<float, 2, true>), g, bl, 0, s, d, A, B, (float*)c);
+                           else hipLaunchKernelGGL((gemm_bf16<float, 2, false>), g, bl, 0, s, d, A, B, (float*)c); }
+            else { if (vec) hipLaunchKernelGGL((gemm_bf16<float, 1, true>), g, bl, 0, s, d, A, B, (float*)c);
+                   else hipLaunchKernelGGL((gemm_bf16<float, 1, false>), g, bl, 0, s, d, A, B, (float*)c); }
+        }
+    } else {
+        const float* A = (const float*)a;
+        const float* B = (const float*)b;
+        if (tC) {
+            if (MT == 2) { if (vec) hipLaunchKernelGGL((gemm_f32<bf16_t, 2, true>), g, bl, 0, s, d, A, B, (bf16_t*)c);
+                           else hipLaunchKernelGGL((gemm_f32<bf16_t, 2, false>), g, bl, 0, s, d, A, B, (bf16_t*)c); }
+            else { if (vec) hipLaunchKernelGGL((gemm_f32<bf16_t, 1, true>), g, bl, 0, s, d, A, B, (bf16_t*)c);
+                   else hipLaunchKernelGGL((gemm_f32<bf16_t, 1, false>), g, bl, 0, s, d, A, B, (bf16_t*)c); }
+        } else {
+            if (MT == 2) { if (vec) hipLaunchKernelGGL((gemm_f32<float, 2, true>), g, bl, 0, s, d, A, B, (float*)c);
+                           else hipLaunchKernelGGL((gemm_f32<float, 2, false>), g, bl, 0, s, d, A, B, (float*)c); }
+            else { if (vec) hipLaunchKernelGGL((gemm_f32<float, 1, true>), g, bl, 0, s, d, A, B, (float*)c);
+                   else hipLaunchKernelGGL((gemm_f32<float, 1, false>), g, bl, 0, s, d, A, B, (float*)c); }
+        }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad(const Launch& ln, const void* a, const void* b, void* part, hipStream_t s) {
+    WgradDesc d = desc_of<WgradDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1;
+    int opt = ln.kind >> kShiftOpt;
+    bool vec = (opt & 2) && ((uintptr_t)a % (tIn ? 8 : 16) == 0) && ((uintptr_t)b % (tIn ? 8 : 16) == 0);
+    dim3 g(ln.grid[0]), bl(256);
+    if (tIn) {
+        if (vec) hipLaunchKernelGGL((wgrad<bf16_t, true>), g, bl, 0, s, d, (const bf16_t*)a, (const bf16_t*)b, (float*)part);
+        else hipLaunchKernelGGL((wgrad<bf16_t, false>), g, bl, 0, s, d, (const bf16_t*)a, (const bf16_t*)b, (float*)part);
+    } else {
+        if (vec) hipLaunchKernelGGL((wgrad<float, true>), g, bl, 0, s, d, (const float*)a, (const float*)b, (float*)part);
+        else hipLaunchKernelGGL((wgrad<float, false>), g, bl, 0, s, d, (const float*)a, (const float*)b, (float*)part);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce(const Launch& ln, const void* part, void* c, hipStream_t s) {
+    ReduceDesc d = desc_of<ReduceDesc>(ln);
+    int tC = (ln.kind >> kBitOut) & 1;
+    dim3 g(ln.grid[0]), bl(256);
+    if (tC) hipLaunchKernelGGL((reduce_partials<bf16_t>), g, bl, 0, s, d, (const float*)part, (bf16_t*)c);
+    else hipLaunchKernelGGL((reduce_partials<float>), g, bl, 0, s, d, (const float*)part, (float*)c);
+    return hipGetLastError();
+}
+
+template <typename T, typename TF, typename TC>
+hipError_t dw_conv_k(int K, const DwDesc& d, dim3 g, const void* a, const void* b, void* c, hipStream_t s) {
+    const T* in = (const T*)a;
+    const TF* f = (const TF*)b;
+    TC* out = (TC*)c;
+    dim3 bl(256);
+    switch (K) {
+        case 1: hipLaunchKernelGGL((dw_conv<T, TF, TC, 1>), g, bl, 0, s, d, in, f, out); break;
+        case 2: hipLaunchKernelGGL((dw_conv<T, TF, TC, 2>), g, bl, 0, s, d, in, f, out); break;
+        case 3: hipLaunchKernelGGL((dw_conv<T, TF, TC, 3>), g, bl, 0, s, d, in, f, out); break;
+        case 4: hipLaunchKernelGGL((dw_conv<T, TF, TC, 4>), g, bl, 0, s, d, in, f, out); break;
+        case 5: hipLaunchKernelGGL((dw_conv<T, TF, TC, 5>), g, bl, 0, s, d, in, f, out); break;
+        case 6: hipLaunchKernelGGL((dw_conv<T, TF, TC, 6>), g, bl, 0, s, d, in, f, out); break;
+        case 7: hipLaunchKernelGGL((dw_conv<T, TF, TC, 7>), g, bl, 0, s, d, in, f, out); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_dw(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1, tF = (ln.kind >> kBitAux) & 1, tC = (ln.kind >> kBitOut) & 1;
+    dim3 g(ln.grid[0]);
+    if (tIn) {
+        if (tF) return tC ? dw_conv_k<bf16_t, bf16_t, bf16_t>(d.K, d, g, a, b, c, s)
+                          : dw_conv_k<bf16_t, bf16_t, float>(d.K, d, g, a, b, c, s);
+        return tC ? dw_conv_k<bf16_t, float, bf16_t>(d.K, d, g, a, b, c, s)
+                  : dw_conv_k<bf16_t, float, float>(d.K, d, g, a, b, c, s);
+    }
+    if (tF) return tC ? dw_conv_k<float, bf16_t, bf16_t>(d.K, d, g, a, b, c, s)
+                      : dw_conv_k<float, bf16_t, float>(d.K, d, g, a, b, c, s);
+    return tC ? dw_conv_k<float, float, bf16_t>(d.K, d, g, a, b, c, s)
+              : dw_conv_k<float, float, float>(d.K, d, g, a, b, c, s);
+}
+
+template <typename T>
+hipError_t dw_tapgrad_k(int K, const DwDesc& d, dim3 g, const void* a, const void* b, void* part,
+                        hipStream_t s) {
+    const T* in = (const T*)a;
+    const T* gr = (const T*)b;
+    float* p = (float*)part;
+    dim3 bl(256);
+    switch (K) {
+        case 1: hipLaunchKernelGGL((dw_tapgrad<T, 1>), g, bl, 0, s, d, in, gr, p); break;
+        case 2: hipLaunchKernelGGL((dw_tapgrad<T, 2>), g, bl, 0, s, d, in, gr, p); break;
+        case 3: hipLaunchKernelGGL((dw_tapgrad<T, 3>), g, bl, 0, s, d, in, gr, p); break;
+        case 4: hipLaunchKernelGGL((dw_tapgrad<T, 4>), g, bl, 0, s, d, in, gr, p); break;
+        case 5: hipLaunchKernelGGL((dw_tapgrad<T, 5>), g, bl, 0, s, d, in, gr, p); break;
+        case 6: hipLaunchKernelGGL((dw_tapgrad<T, 6>), g, bl, 0, s, d, in, gr, p); break;
+        case 7: hipLaunchKernelGGL((dw_tapgrad<T, 7>), g, bl, 0, s, d, in, gr, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_dw_tapgrad(const Launch& ln, const void* a, const void* b, void* part, hipStream_t s) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1;
+    dim3 g(ln.grid[0]);
+    return tIn ? dw_tapgrad_k<bf16_t>(d.K, d, g, a, b, part, s)
+               : dw_tapgrad_k<float>(d.K, d, g, a, b, part, s);
+}
+
+hipError_t launch_dw_tapreduce(const Launch& ln, const void* part, void* c, hipStream_t s) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tC = (ln.kind >> kBitOut) & 1;
+    dim3 g(ln.grid[0]), bl(256);
+    if (tC) hipLaunchKernelGGL((dw_tapreduce<bf16_t>), g, bl, 0, s, d, (const float*)part, (bf16_t*)c);
+    else hipLaunchKernelGGL((dw_tapreduce<float>), g, bl, 0, s, d, (const float*)part, (float*)c);
+    return hipGetLastError();
+}
+
+}  // namespace
 
 hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, void* d,
                        hipStream_t s) {
-    (void)ln; (void)a; (void)b; (void)c; (void)d; (void)s;
-    return hipErrorInvalidValue;
+    switch (ln.kind & 0xff) {
+        case K_GEMM: return launch_gemm(ln, a, b, c, s);
+        case K_WGRAD: return launch_wgrad(ln, a, b, d, s);
+        case K_REDUCE: return launch_reduce(ln, d, c, s);
+        case K_DW: return launch_dw(ln, a, b, c, s);
+        case K_DW_TAPGRAD: return launch_dw_tapgrad(ln, a, b, d, s);
+        case K_DW_TAPREDUCE: return launch_dw_tapreduce(ln, d, c, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace ce

@@ -1,0 +1,483 @@
+// Lowering of pairwise ops to specialised kernels.
+//
+// A pairwise op (Section 3.1: contraction, batch and outer-product labels,
+// plus convolved labels) is matched against the label structures the fast
+// kernels implement; anything else runs on the generic strided kernel.
+//
+//   channel-mixing GEMM   C[g][m][n] = sum_k F[g?][m][k] D[g][k][n], with the
+//                         output's innermost labels (n) unit-stride in the large
+//                         operand D and in C, absent from the small operand F
+//   factor gradient       C[m][n] = sum_{kb,k} L[kb][m][k] R[kb][n][k], with the
+//                         reduced labels k unit-stride in both operands
+//   depthwise conv        one convolved label, a large operand with the layout
+//                         of C, and a filter indexed by the conv label and by a
+//                         run of C's labels ahead of the convolved axis
+//   filter-tap gradient   the same structure with the filter as the result
+#include <algorithm>
+#include <cstring>
+
+#include "plan.h"
+
+namespace ce {
+namespace {
+
+double tensor_bytes(const TensorRef& t) {
+    return (double)t.numel() * (t.dtype == DT_BF16 ? 2 : 4);
+}
+
+bool has(const std::vector<int>& v, int l) { return std::find(v.begin(), v.end(), l) != v.end(); }
+
+// Labels `labs` (outer to inner) form one dimension of tensor t: strides chain.
+// Returns size and innermost stride (size 1, stride 0 for an empty group).
+bool merged(const TensorRef& t, const std::vector<int>& labs, int64_t& size, int64_t& stride) {
+    size = 1;
+    stride = 0;
+    if (labs.empty()) return true;
+    int64_t expect = -1;
+    for (int k = (int)labs.size() - 1; k >= 0; --k) {
+        int p = t.pos(labs[k]);
+        if (p < 0) return false;
+        if (k == (int)labs.size() - 1) {
+            stride = t.strides[p];
+            expect = stride * t.dims[p];
+        } else {
+            if (t.strides[p] != expect) return false;
+            expect *= t.dims[p];
+        }
+        size *= t.dims[p];
+    }
+    return true;
+}
+
+struct BDim {
+    int64_t size, s0, s1, s2;
+};
+
+// Merge neighbouring batch dims whose strides chain in all three tensors.
+std::vector<BDim> merge_dims(std::vector<BDim> v) {
+    for (size_t i = 0; i + 1 < v.size();) {
+        BDim& a = v[i];
+        BDim& b = v[i + 1];
+        if (a.s0 == b.s0 * b.size && a.s1 == b.s1 * b.size && a.s2 == b.s2 * b.size) {
+            a.size *= b.size;
+            a.s0 = b.s0;
+            a.s1 = b.s1;
+            a.s2 = b.s2;
+            v.erase(v.begin() + i + 1);
+        } else {
+            i++;
+        }
+    }
+    return v;
+}
+
+int32_t dt_bits(DType in, DType aux, DType out) {
+    return ((int32_t)in << kBitIn) | ((int32_t)aux << kBitAux) | ((int32_t)out << kBitOut);
+}
+
+template <typename D>
+void set_desc(Launch& ln, const D& d) {
+    ln.desc.resize(sizeof(D));
+    std::memcpy(ln.desc.data(), &d, sizeof(D));
+}
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---- channel-mixing GEMM -------------------------------------------------
+bool try_gemm(const PairOp& op, std::vector<Launch>& out) {
+    if (!op.convs.empty() || !op.has_r) return false;
+    const TensorRef& C = op.C;
+    for (int dside = 0; dside < 2; dside++) {
+        const TensorRef& D = dside == 0 ? op.L : op.R;
+        const TensorRef& F = dside == 0 ? op.R : op.L;
+        const BufRef& dbuf = dside == 0 ? op.L.buf : op.R.buf;
+        const BufRef& fbuf = dside == 0 ? op.R.buf : op.L.buf;
+        if (D.dtype != F.dtype) continue;
+        // n: innermost labels of C, unit-stride in C and D, not in F
+        std::vector<int> ng;
+        int64_t expect = 1;
+        for (int k = (int)C.labels.size() - 1; k >= 0; --k) {
+            int l = C.labels[k];
+            if (!D.has(l) || F.has(l)) break;
+            if (C.strides[k] != expect || D.stride_of(l) != expect) break;
+            ng.insert(ng.begin(), l);
+            expect *= C.dims[k];
+        }
+        if (ng.empty()) continue;
+        int64_t N = expect;
+        std::vector<int> mg, kg, gg;
+        for (int l : C.labels)
+            if (F.has(l) && !D.has(l)) mg.push_back(l);
+        for (int l : D.labels)
+            if (F.has(l) && !C.has(l)) kg.push_back(l);
+        bool ok = true;
+        for (int l : D.labels)
+            if (!C.has(l) && !F.has(l)) ok = false;     // self-contracted in D
+        for (int l : F.labels)
+            if (!C.has(l) && !D.has(l)) ok = false;     // self-contracted in F
+        std::vector<BDim> bd;
+        for (int l : C.labels) {
+            if (has(ng, l) || has(mg, l)) continue;
+            if (!D.has(l)) { ok = false; break; }
+            gg.push_back(l);
+            bd.push_back({C.dim_of(l), F.stride_of(l), D.stride_of(l), C.stride_of(l)});
+        }
+        if (!ok) continue;
+        int64_t M, sFm, sCm_unused, K, sFk, sDk, Mc;
+        if (!merged(F, mg, M, sFm) || !merged(C, mg, Mc, sCm_unused)) continue;
+        if (!merged(F, kg, K, sFk) || !merged(D, kg, K, sDk)) continue;
+        int64_t sCm = 0, tmp;
+        merged(C, mg, tmp, sCm);
+        bd = merge_dims(bd);
+        if (bd.size() > 3) continue;
+        if (M > (1 << 20) || N > (int64_t)1 << 31 || K > (1 << 20)) continue;
+        GemmDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.M = (int32_t)M;
+        d.N = (int32_t)N;
+        d.K = (int32_t)K;
+        d.ng = (int32_t)bd.size();
+        int64_t G = 1;
+        for (size_t i = 0; i < bd.size(); i++) {
+            d.g_size[i] = bd[i].size;
+            d.g_sA[i] = bd[i].s0;
+            d.g_sB[i] = bd[i].s1;
+            d.g_sC[i] = bd[i].s2;
+            G *= bd[i].size;
+        }
+        d.sAm = sFm;
+        d.sAk = sFk;
+        d.sBk = sDk;
+        d.sCm = sCm;
+        int MT = M > 32 ? 2 : 1;
+        d.mtiles = (int32_t)cdiv(M, 32 * MT);
+        d.ntiles = (int32_t)cdiv(N, 128);
+        d.blocks = (int64_t)d.mtiles * d.ntiles * G;
+        if (d.blocks > 0x7fffffff) continue;
+        bool vec = (d.sBk % 4 == 0);
+        for (int i = 0; i < d.ng; i++) vec = vec && (d.g_sB[i] % 4 == 0);
+        Launch ln;
+        ln.kind = K_GEMM | dt_bits(D.dtype, F.dtype, C.dtype) |
+                  (((MT == 2 ? 1 : 0) | (vec ? 2 : 0)) << kShiftOpt);
+        ln.a = fbuf;
+        ln.b = dbuf;
+        ln.c = C.buf;
+        ln.grid[0] = (uint32_t)d.blocks;
+        ln.block[0] = 256;
+        set_desc(ln, d);
+        ln.kname = std::string(D.dtype == DT_BF16 ? "gemm_bf16" : "gemm_f32") +
+                   (MT == 2 ? "_mt2" : "_mt1");
+        out.push_back(ln);
+        return true;
+    }
+    return false;
+}
+
+// ---- factor gradient: split NT GEMM + ordered reduction ---------------------
+bool try_wgrad(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if (!op.convs.empty() || !op.has_r) return false;
+    const TensorRef &L = op.L, &R = op.R, &C = op.C;
+    if (L.dtype != R.dtype) return false;
+    // k: innermost labels of L, unit-stride in L and R, reduced (not in C)
+    std::vector<int> kg;
+    int64_t expect = 1;
+    for (int k = (int)L.labels.size() - 1; k >= 0; --k) {
+        int l = L.labels[k];
+        if (!R.has(l) || C.has(l)) break;
+        if (L.strides[k] != expect || R.stride_of(l) != expect) break;
+        kg.insert(kg.begin(), l);
+        expect *= L.dims[k];
+    }
+    if (kg.empty()) return false;
+    int64_t K = expect;
+    std::vector<int> mg, ng;
+    std::vector<BDim> kb;
+    for (int l : C.labels) {
+        bool inL = L.has(l), inR = R.has(l);
+        if (inL && inR) return false;          // batch labels: not this kernel
+        if (inL) mg.push_back(l);
+        else if (inR) ng.push_back(l);
+        else return false;
+    }
+    for (int l : L.labels) {
+        if (C.has(l) || has(kg, l)) continue;
+        if (!R.has(l)) return false;           // self-contracted
+        kb.push_back({L.dim_of(l), L.stride_of(l), R.stride_of(l), 0});
+    }
+    for (int l : R.labels)
+        if (!C.has(l) && !L.has(l)) return false;
+    int64_t M, sAm, N, sBn, tmp, sCm, sCn;
+    if (!merged(L, mg, M, sAm) || !merged(C, mg, tmp, sCm)) return false;
+    if (!merged(R, ng, N, sBn) || !merged(C, ng, tmp, sCn)) return false;
+    kb = merge_dims(kb);
+    if (kb.size() > 3) return false;
+    if (K < 64 || M > 4096 || N > 4096) return false;
+    WgradDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.M = (int32_t)M;
+    d.N = (int32_t)N;
+    d.K = K;
+    d.nkb = (int32_t)kb.size();
+    int64_t KB = 1;
+    for (size_t i = 0; i < kb.size(); i++) {
+        d.kb_size[i] = kb[i].size;
+        d.kb_sA[i] = kb[i].s0;
+        d.kb_sB[i] = kb[i].s1;
+        KB *= kb[i].size;
+    }
+    d.sAm = sAm;
+    d.sBn = sBn;
+    d.mtiles = (int32_t)cdiv(M, 64);
+    d.ntiles = (int32_t)cdiv(N, 64);
+    int64_t tiles = (int64_t)d.mtiles * d.ntiles;
+    // aim at ~2048 blocks; chunks are multiples of the 32-element tile
+    int64_t want = std::max<int64_t>(1, cdiv(2048, KB * tiles));
+    int64_t kchunk = std::max<int64_t>(32, cdiv(cdiv(K, want), 32) * 32);
+    d.kchunk = (int32_t)std::min<int64_t>(kchunk, (int64_t)1 << 30);
+    d.ksplit = (int32_t)cdiv(K, d.kchunk);
+    d.nsplit = KB * d.ksplit;
+    d.blocks = d.nsplit * tiles;
+    if (d.blocks > 0x7fffffff || d.nsplit * M * N > ((int64_t)1 << 31)) return false;
+    bool vec = (d.sAm % 4 == 0) && (d.sBn % 4 == 0) && (d.kchunk % 4 == 0);
+    for (int i = 0; i < d.nkb; i++) vec = vec && (d.kb_sA[i] % 4 == 0) && (d.kb_sB[i] % 4 == 0);
+    BufRef part = scratch.alloc((size_t)(d.nsplit * M * N * 4));
+    Launch ln;
+    ln.kind = K_WGRAD | dt_bits(L.dtype, R.dtype, DT_F32) | ((vec ? 2 : 0) << kShiftOpt);
+    ln.a = L.buf;
+    ln.b = R.buf;
+    ln.d = part;
+    ln.grid[0] = (uint32_t)d.blocks;
+    ln.block[0] = 256;
+    set_desc(ln, d);
+    ln.kname = L.dtype == DT_BF16 ? "wgrad_bf16" : "wgrad_f32";
+    out.push_back(ln);
+    ReduceDesc rd;
+    std::memset(&rd, 0, sizeof(rd));
+    rd.M = (int32_t)M;
+    rd.N = (int32_t)N;
+    rd.nsplit = d.nsplit;
+    rd.sCm = sCm;
+    rd.sCn = sCn;
+    Launch lr;
+    lr.kind = K_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+    lr.d = part;
+    lr.c = C.buf;
+    lr.grid[0] = (uint32_t)cdiv(M * N, 256);
+    lr.block[0] = 256;
+    set_desc(lr, rd);
+    lr.kname = "reduce_partials";
+    out.push_back(lr);
+    return true;
+}
+
+// ---- depthwise convolution along one axis --------------------------------
+// View of a dense tensor t around its label `axis`: [slabs][A][inner].
+struct AxisView {
+    int pos;
+    int64_t nslab, A, inner;
+};
+
+bool axis_view(const TensorRef& t, int axis, AxisView& v) {
+    v.pos = t.pos(axis);
+    if (v.pos < 0) return false;
+    v.nslab = 1;
+    v.inner = 1;
+    for (int k = 0; k < v.pos; k++) v.nslab *= t.dims[k];
+    for (int k = v.pos + 1; k < (int)t.dims.size(); k++) v.inner *= t.dims[k];
+    v.A = t.dims[v.pos];
+    // dense row-major
+    int64_t s = 1;
+    for (int k = (int)t.dims.size() - 1; k >= 0; --k) {
+        if (t.strides[k] != s) return false;
+        s *= t.dims[k];
+    }
+    return true;
+}
+
+bool same_layout(const TensorRef& a, const TensorRef& b) {
+    return a.labels == b.labels && a.dims == b.dims && a.strides == b.strides;
+}
+
+// Filter-row labels: the labels of `filt` other than the axis must be a run of
+// `big`'s labels ahead of the axis, mergeable in `filt`.
+bool filter_rows(const TensorRef& big, const TensorRef& filt, int axis, const AxisView& v,
+                 int64_t& r_div, int64_t& r_size, int64_t& r_stride) {
+    std::vector<int> run;
+    for (int l : filt.labels)
+        if (l != axis) run.push_back(l);
+    r_size = 1;
+    r_div = 1;
+    r_stride = 0;
+    if (run.empty()) {
+        r_div = 1;
+        return true;
+    }
+    // order the run by its positions in `big` (must be consecutive, before the axis)
+    std::vector<int> pos;
+    for (int l : run) {
+        int p = big.pos(l);
+        if (p < 0 || p >= v.pos) return false;
+        pos.push_back(p);
+    }
+    std::sort(pos.begin(), pos.end());
+    for (size_t i = 1; i < pos.size(); i++)
+        if (pos[i] != pos[i - 1] + 1) return false;
+    std::vector<int> ordered;
+    for (int p : pos) ordered.push_back(big.labels[p]);
+    int64_t sz, st;
+    if (!merged(filt, ordered, sz, st)) return false;
+    r_size = sz;
+    r_stride = st;
+    r_div = 1;
+    for (int k = pos.back() + 1; k < v.pos; k++) r_div *= big.dims[k];
+    return true;
+}
+
+int64_t choose_spb(int64_t r_div, int64_t slabsz) {
+    int64_t best = 1;
+    for (int64_t d = 1; d <= std::min<int64_t>(r_div, 256); d++)
+        if (r_div % d == 0 && d * slabsz <= 4096) best = d;
+    return best;
+}
+
+bool try_dw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if (op.convs.size() != 1 || !op.has_r) return false;
+    const ConvMap& cm = op.convs[0];
+    const int axis = cm.label;
+    // (a) forward / transposed: the large operand has C's layout
+    for (int side = 0; side < 2; side++) {
+        const TensorRef& X = side == 0 ? op.L : op.R;
+        const TensorRef& Fl = side == 0 ? op.R : op.L;
+        int aX = side == 0 ? cm.aL : cm.aR, bX = side == 0 ? cm.bL : cm.bR;
+        int64_t gX = side == 0 ? cm.gL : cm.gR;
+        int aF = side == 0 ? cm.aR : cm.aL, bF = side == 0 ? cm.bR : cm.bL;
+        int64_t gF = side == 0 ? cm.gR : cm.gL;
+        if (!same_layout(X, op.C)) continue;
+        if (!(aX == 1 && (bX == 1 || bX == -1) && aF == 0 && bF == 1 && gF == 0)) continue;
+        AxisView v;
+        if (!axis_view(X, axis, v)) continue;
+        if (cm.O != v.A || cm.J > 7 || cm.J < 1) continue;
+        if (Fl.dim_of(axis) != cm.J) continue;
+        int64_t r_div, r_size, r_stride;
+        if (!filter_rows(X, Fl, axis, v, r_div, r_size, r_stride)) continue;
+        int64_t slabsz = v.A * v.inner;
+        if (slabsz > 4096) continue;
+        DwDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.nslab = v.nslab;
+        d.A = (int32_t)v.A;
+        d.inner = (int32_t)v.inner;
+        d.K = (int32_t)cm.J;
+        d.sign = bX;
+        d.off = (int32_t)gX;
+        d.spb = (int32_t)choose_spb(r_div, slabsz);
+        d.r_div = r_div;
+        d.r_size = r_size;
+        d.r_stride = r_stride;
+        d.f_sj = Fl.stride_of(axis);
+        d.nblocks = cdiv(d.nslab, d.spb);
+        if (d.nblocks > 0x7fffffff) continue;
+        Launch ln;
+        ln.kind = K_DW | dt_bits(X.dtype, Fl.dtype, op.C.dtype);
+        ln.a = X.buf;
+        ln.b = Fl.buf;
+        ln.c = op.C.buf;
+        ln.grid[0] = (uint32_t)d.nblocks;
+        ln.block[0] = 256;
+        set_desc(ln, d);
+        ln.kname = bX == 1 ? "dw_conv" : "dw_conv_transposed";
+        out.push_back(ln);
+        return true;
+    }
+    // (b) filter-tap gradient: C is the filter; feature and gradient share a layout
+    for (int side = 0; side < 2; side++) {
+        const TensorRef& Xf = side == 0 ? op.L : op.R;   // feature (read at p + j + off)
+        const TensorRef& Xg = side == 0 ? op.R : op.L;   // output gradient (read at p)
+        int aF = side == 0 ? cm.aL : cm.aR, bF = side == 0 ? cm.bL : cm.bR;
+        int64_t gF = side == 0 ? cm.gL : cm.gR;
+        int aG = side == 0 ? cm.aR : cm.aL, bG = side == 0 ? cm.bR : cm.bL;
+        int64_t gG = side == 0 ? cm.gR : cm.gL;
+        if (!same_layout(Xf, Xg) || Xf.dtype != Xg.dtype) continue;
+        if (!(aF == 1 && bF == 1 && aG == 0 && bG == 1 && gG == 0)) continue;
+        AxisView v;
+        if (!axis_view(Xf, axis, v)) continue;
+        if (cm.J != v.A || cm.O > 7 || cm.O < 1 || op.C.dim_of(axis) != cm.O) continue;
+        int64_t r_div, r_size, r_stride;
+        if (!filter_rows(Xf, op.C, axis, v, r_div, r_size, r_stride)) continue;
+        int64_t slabsz = v.A * v.inner;
+        if (slabsz > 4096) continue;
+        DwDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.nslab = v.nslab;
+        d.A = (int32_t)v.A;
+        d.inner = (int32_t)v.inner;
+        d.K = (int32_t)cm.O;
+        d.sign = 1;
+        d.off = (int32_t)gF;
+        d.spb = (int32_t)choose_spb(r_div, slabsz);
+        d.r_div = r_div;
+        d.r_size = r_size;
+        d.r_stride = r_stride;
+        d.nblocks = cdiv(d.nslab, d.spb);
+        d.o_sr = r_stride;
+        d.o_sj = op.C.stride_of(axis);
+        if (d.nblocks > 0x7fffffff || d.nslab % d.spb) continue;
+        BufRef part = scratch.alloc((size_t)(d.nblocks * d.K * 4));
+        Launch ln;
+        ln.kind = K_DW_TAPGRAD | dt_bits(Xf.dtype, Xg.dtype, DT_F32);
+        ln.a = Xf.buf;
+        ln.b = Xg.buf;
+        ln.d = part;
+        ln.grid[0] = (uint32_t)d.nblocks;
+        ln.block[0] = 256;
+        set_desc(ln, d);
+        ln.kname = "dw_tapgrad";
+        out.push_back(ln);
+        Launch lr;
+        lr.kind = K_DW_TAPREDUCE | dt_bits(DT_F32, DT_F32, op.C.dtype);
+        lr.d = part;
+        lr.c = op.C.buf;
+        lr.grid[0] = (uint32_t)cdiv(d.r_size * d.K, 256);
+        lr.block[0] = 256;
+        set_desc(lr, d);
+        lr.kname = "dw_tapreduce";
+        out.push_back(lr);
+        return true;
+    }
+    return false;
+}
+
+}  // namespace
+
+std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
+                             ScratchAlloc& scratch) {
+    (void)e;
+    std::vector<Launch> out;
+    bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
+                (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out));
+    if (!fast) {
+        out.clear();
+        Launch ln = lower_generic(op);
+        int v = ln.kind & 0xff;
+        ln.kname = v == K_GENERIC_THREAD ? "generic_thread" : v == K_GENERIC_WAVE ? "generic_wave"
+                                                                                    : "generic_block";
+        out.push_back(ln);
+    }
+    double bytes = tensor_bytes(op.L) + (op.has_r ? tensor_bytes(op.R) : 0) + tensor_bytes(op.C);
+    for (auto& ln : out) {
+        ln.need = op.need;
+        ln.what = op.what;
+        ln.alg_bytes = bytes / out.size();
+        ln.alg_flops = 2.0 * (double)op.macs / out.size();
+    }
+    // the main launch of a split op carries the op's bytes and flops
+    if (out.size() == 2) {
+        out[0].alg_bytes = bytes;
+        out[0].alg_flops = 2.0 * (double)op.macs;
+        out[1].alg_bytes = 0;
+        out[1].alg_flops = 0;
+    }
+    return out;
+}
+
+}  // namespace ce

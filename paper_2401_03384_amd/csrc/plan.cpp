@@ -339,6 +339,8 @@ size_t pack(std::vector<WsItem>& items) {
     return total;
 }
 
+}  // namespace
+
 // ---- generic lowering ----------------------------------------------------
 Launch lower_generic(const PairOp& op) {
     GenericDesc d;
@@ -464,6 +466,8 @@ Launch lower_generic(const PairOp& op) {
     return ln;
 }
 
+namespace {
+
 std::string tensor_str(const ce_expr& e, const TensorRef& t) {
     std::string s;
     for (size_t k = 0; k < t.labels.size(); k++) {
@@ -480,10 +484,6 @@ uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) 
     if (c == kSat) fail(CE_ERR_OVERFLOW, "step cost exceeds 64 bits");
     return c;
 }
-
-// Lowering of one pairwise op to launches.  Fast kernels are tried first
-// unless the plan asks for the generic kernel only.
-std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags);
 
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
                    bool use_path, const int* pairs, int n_pairs) {
@@ -531,105 +531,121 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
         << ", forward MACs " << p->fwd_macs << ", left-to-right " << p->ltr_cost << "\n";
 
     if (p->executable) {
-        auto node_buf_fwd = [&](int node) -> BufRef {
-            BufRef b;
-            if (node < n) { b.kind = BUF_IN; b.index = node; }
-            else if (node == (int)p->nodes.size() - 1) { b.kind = BUF_OUT; }
-            else { b.kind = BUF_WS; b.index = node; }
-            return b;
-        };
-        auto value_tensor = [&](int node) -> TensorRef {
-            TensorRef t = bld.tensor_of(node, dt, node_buf_fwd(node));
-            return t;
-        };
-        // ---------------- forward ----------------
-        std::vector<PairOp> fops;
-        if (m == 0) {
-            PairOp op;
-            op.L = value_tensor(0);
-            op.has_r = false;
-            TensorRef out;
-            out.labels = E.out;
-            out.dims = E.out_dims();
-            out.strides.assign(out.dims.size(), 1);
-            for (int k = (int)out.dims.size() - 2; k >= 0; k--) out.strides[k] = out.strides[k + 1] * out.dims[k + 1];
-            out.dtype = dt;
-            out.buf.kind = BUF_OUT;
-            op.C = out;
-            op.what = "unary";
-            fops.push_back(op);
-        }
-        for (int s = 0; s < m; s++) {
-            const Step& st = p->steps[s];
-            PairOp op;
-            op.L = value_tensor(st.a);
-            op.R = value_tensor(st.b);
-            op.C = value_tensor(st.c);
-            op.convs = bld.conv_maps(st, 0);
-            op.macs = st.macs;
-            op.what = "step " + std::to_string(s) + " fwd " + tensor_str(E, op.L) + "," +
-                      tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-            fops.push_back(op);
-        }
-        // workspace: intermediates live from their step to their consumer's step
+        // Workspace items: intermediates (id = node), their gradients
+        // (id = GRAD_ID + node) and per-launch scratch (ids from SCRATCH_ID).
+        // Launch buffers refer to items by id; offsets are patched after packing.
+        const int GRAD_ID = 1 << 20, SCRATCH_ID = 1 << 24;
+        auto elem = [&](DType t) { return t == DT_BF16 ? 2 : 4; };
         auto consumer_step = [&](int node) -> int {
             for (int s = 0; s < m; s++)
                 if (p->steps[s].a == node || p->steps[s].b == node) return s;
             return m;
         };
+        auto patch = [&](std::vector<Launch>& v, const std::vector<WsItem>& items) {
+            for (auto& ln : v)
+                for (BufRef* b : {&ln.a, &ln.b, &ln.c, &ln.d})
+                    if (b->kind == BUF_WS) {
+                        bool found = false;
+                        for (auto& it : items)
+                            if (it.id == b->index) { b->offset = it.offset; found = true; break; }
+                        if (!found) fail(CE_ERR_ARG, "internal: workspace item missing");
+                    }
+        };
+        struct ItemScratch : ScratchAlloc {
+            std::vector<WsItem>* items = nullptr;
+            int t = 0, next = 0;
+            BufRef alloc(size_t bytes) override {
+                WsItem it;
+                it.bytes = bytes;
+                it.t0 = it.t1 = t;
+                it.id = next++;
+                items->push_back(it);
+                BufRef b;
+                b.kind = BUF_WS;
+                b.index = it.id;
+                return b;
+            }
+        };
+        auto dense_out = [&](BufKind k) {
+            TensorRef out;
+            out.labels = E.out;
+            out.dims = E.out_dims();
+            out.strides.assign(out.dims.size(), 1);
+            for (int k2 = (int)out.dims.size() - 2; k2 >= 0; k2--)
+                out.strides[k2] = out.strides[k2 + 1] * out.dims[k2 + 1];
+            out.dtype = dt;
+            out.buf.kind = k;
+            return out;
+        };
+
+        // ---------------- forward ----------------
         std::vector<WsItem> items;
-        std::vector<int> ws_node;
         for (int s = 0; s + 1 < m; s++) {
             int c = p->steps[s].c;
             WsItem it;
-            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * (dt == DT_BF16 ? 2 : 4);
+            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * elem(dt);
             it.t0 = s;
             it.t1 = consumer_step(c);
             it.id = c;
             items.push_back(it);
         }
-        p->ws_fwd = pack(items);
-        auto ws_off = [&](const std::vector<WsItem>& v, int id) -> size_t {
-            for (auto& it : v)
-                if (it.id == id) return it.offset;
-            fail(CE_ERR_ARG, "internal: workspace item missing");
+        auto fval = [&](int node) -> TensorRef {
+            BufRef b;
+            if (node < n) { b.kind = BUF_IN; b.index = node; }
+            else if (node == (int)p->nodes.size() - 1) { b.kind = BUF_OUT; }
+            else { b.kind = BUF_WS; b.index = node; }
+            return bld.tensor_of(node, dt, b);
         };
-        for (auto& op : fops) {
-            for (TensorRef* t : {&op.L, &op.R, &op.C})
-                if (t->buf.kind == BUF_WS) t->buf.offset = ws_off(items, t->buf.index);
+        ItemScratch fs;
+        fs.items = &items;
+        fs.next = SCRATCH_ID;
+        if (m == 0) {
+            PairOp op;
+            op.L = fval(0);
+            op.has_r = false;
+            op.C = dense_out(BUF_OUT);
+            op.what = "unary";
+            for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
-            for (auto& op : fops) {
-            auto ls = lower_op(E, op, flags);
-            for (auto& l : ls) p->fwd.push_back(l);
+        for (int s = 0; s < m; s++) {
+            const Step& st = p->steps[s];
+            PairOp op;
+            op.L = fval(st.a);
+            op.R = fval(st.b);
+            op.C = fval(st.c);
+            op.convs = bld.conv_maps(st, 0);
+            op.macs = st.macs;
+            op.what = "step " + std::to_string(s) + " fwd " + tensor_str(E, op.L) + "," +
+                      tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
+            fs.t = s;
+            for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
+        p->ws_fwd = pack(items);
+        patch(p->fwd, items);
 
         // ---------------- backward ----------------
         // timeline: recompute step t at time t (t < m-1); backward of step s at
         // time (m-1) + (m-1-s).
-        std::vector<PairOp> bops;
         std::vector<WsItem> bitems;
         auto T = [&](int s) { return (m - 1) + (m - 1 - s); };
-        auto parent_step = [&](int node) { return consumer_step(node); };
-        const int GRAD_ID = 1 << 20;   // item ids for gradient buffers
         for (int s = 0; s + 1 < m; s++) {
             int c = p->steps[s].c;
             WsItem it;
-            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * (dt == DT_BF16 ? 2 : 4);
+            it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * elem(dt);
             it.t0 = s;
-            it.t1 = T(parent_step(c));
+            it.t1 = T(consumer_step(c));
             it.id = c;
             bitems.push_back(it);
             WsItem g = it;
-            g.t0 = T(parent_step(c));
+            g.t0 = T(consumer_step(c));
             g.t1 = T(s);
             g.id = GRAD_ID + c;
             bitems.push_back(g);
         }
-        p->ws_bwd = pack(bitems);
         auto bval = [&](int node) -> TensorRef {
             BufRef b;
             if (node < n) { b.kind = BUF_IN; b.index = node; }
-            else { b.kind = BUF_WS; b.index = node; b.offset = ws_off(bitems, node); }
+            else { b.kind = BUF_WS; b.index = node; }
             return bld.tensor_of(node, dt, b);
         };
         auto bgrad = [&](int node) -> TensorRef {
@@ -643,28 +659,22 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 b.kind = BUF_DOUT;
             } else {
                 b.kind = BUF_WS;
-                b.index = node;
-                b.offset = ws_off(bitems, GRAD_ID + node);
+                b.index = GRAD_ID + node;
             }
             return bld.tensor_of(node, gdt, b);
         };
+        ItemScratch bs;
+        bs.items = &bitems;
+        bs.next = SCRATCH_ID;
         if (m == 0) {
-            // Y = unary(X): dX = broadcast of dY through the same label map
+            // Y = unary(X): dX = dY broadcast back through the same label map
             PairOp op;
-            op.L = bgrad(0);   // placeholder replaced below
-            TensorRef dy;
-            dy.labels = E.out;
-            dy.dims = E.out_dims();
-            dy.strides.assign(dy.dims.size(), 1);
-            for (int k = (int)dy.dims.size() - 2; k >= 0; k--) dy.strides[k] = dy.strides[k + 1] * dy.dims[k + 1];
-            dy.dtype = dt;
-            dy.buf.kind = BUF_DOUT;
-            op.L = dy;
+            op.L = dense_out(BUF_DOUT);
             op.has_r = false;
             op.C = bgrad(0);
             op.need = 1u;
             op.what = "unary bwd";
-            bops.push_back(op);
+            for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
         for (int s = 0; s + 1 < m; s++) {
             const Step& st = p->steps[s];
@@ -675,11 +685,13 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.convs = bld.conv_maps(st, 0);
             op.macs = st.macs;
             op.what = "step " + std::to_string(s) + " recompute";
-            bops.push_back(op);
+            bs.t = s;
+            for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
         for (int s = m - 1; s >= 0; s--) {
             const Step& st = p->steps[s];
             TensorRef dC = bgrad(st.c);
+            bs.t = T(s);
             {
                 PairOp op;
                 op.L = dC;
@@ -690,7 +702,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 op.need = p->nodes[st.a].mask;
                 op.what = "step " + std::to_string(s) + " grad lhs " + tensor_str(E, op.L) + "," +
                           tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                bops.push_back(op);
+                for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
             }
             {
                 PairOp op;
@@ -702,13 +714,11 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 op.need = p->nodes[st.b].mask;
                 op.what = "step " + std::to_string(s) + " grad rhs " + tensor_str(E, op.L) + "," +
                           tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                bops.push_back(op);
+                for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
             }
         }
-        for (auto& op : bops) {
-            auto ls = lower_op(E, op, flags);
-            for (auto& l : ls) p->bwd.push_back(l);
-        }
+        p->ws_bwd = pack(bitems);
+        patch(p->bwd, bitems);
     }
     for (int s = 0; s < m; s++) {
         const Step& st = p->steps[s];
@@ -721,22 +731,6 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
     if (!p->executable) txt << "  not executable: " << p->why_not << "\n";
     p->text = txt.str();
     return p.release();
-}
-
-static double tensor_bytes(const TensorRef& t) {
-    return (double)t.numel() * (t.dtype == DT_BF16 ? 2 : 4);
-}
-
-std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags) {
-    (void)e;
-    (void)flags;
-    Launch ln = lower_generic(op);
-    int v = ln.kind & 0xff;
-    ln.kname = v == K_GENERIC_THREAD ? "generic_thread" : v == K_GENERIC_WAVE ? "generic_wave"
-                                                                                : "generic_block";
-    ln.alg_bytes = tensor_bytes(op.L) + (op.has_r ? tensor_bytes(op.R) : 0) + tensor_bytes(op.C);
-    ln.alg_flops = 2.0 * (double)op.macs;
-    return {ln};
 }
 
 }  // namespace ce

@@ -105,4 +105,19 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
 // Exposed for tests of the search: cost of merging operand sets A and B.
 uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode);
 
+// Workspace scratch requested by a lowering (e.g. split-reduction partials);
+// lives for the duration of the op's launches.
+struct ScratchAlloc {
+    virtual BufRef alloc(size_t bytes) = 0;
+    virtual ~ScratchAlloc() = default;
+};
+
+// The generic strided kernel for any pairwise op.
+Launch lower_generic(const PairOp& op);
+
+// Lowering of one pairwise op to launches: a specialised kernel when the
+// op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.
+std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
+                             ScratchAlloc& scratch);
+
 }  // namespace ce

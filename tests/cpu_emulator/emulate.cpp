@@ -1,10 +1,11 @@
 // CPU emulation of a plan's launch list (test infrastructure).
 //
 // Builds a plan with the library's own host planner (compiled in from the
-// package sources) restricted to the generic kernel, then executes every
-// launch on the CPU with the semantics of GenericDesc: the same loops the
-// generic HIP kernel runs, with every memory access checked against the size
-// of the buffer it falls in.  A test compares the results with the oracle, so
+// package sources), then executes every launch on the CPU with the semantics
+// of its descriptor (the index arithmetic each HIP kernel performs, element
+// by element), with every memory access checked against the size of the
+// buffer it falls in and every launch grid checked against what the kernel
+// assumes.  A test compares the results with the oracle, so
 // descriptor, layout and workspace bugs show up without a GPU, and an
 // out-of-bounds access is reported instead of faulting a device.
 #include <cmath>
@@ -137,6 +138,172 @@ bool run_generic(const Launch& ln, Ctx& c) {
     return true;
 }
 
+template <typename D>
+D desc_of(const Launch& ln) {
+    D d;
+    std::memcpy(&d, ln.desc.data(), sizeof(D));
+    return d;
+}
+
+#define REQ(cond, msg) do { if (!(cond)) { c.err = std::string(msg) + ": " + ln.what; return false; } } while (0)
+
+// C[g][m][n] = sum_k A[g][m][k] B[g][k][n]
+bool run_gemm(const Launch& ln, Ctx& c) {
+    GemmDesc d = desc_of<GemmDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    int MT = ((ln.kind >> kShiftOpt) & 1) ? 2 : 1;
+    bool o1, o2, o3;
+    Buf A = resolve(ln.a, c, 0, o1), B = resolve(ln.b, c, 0, o2), C = resolve(ln.c, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks == (int64_t)d.mtiles * d.ntiles *
+        [&] { int64_t g = 1; for (int i = 0; i < d.ng; i++) g *= d.g_size[i]; return g; }(), "grid");
+    REQ(d.mtiles * 32 * MT >= d.M && d.ntiles * 128 >= d.N, "tiles do not cover");
+    int64_t G = 1;
+    for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
+    for (int64_t g = 0; g < G; g++) {
+        int64_t gg = g, oA = 0, oB = 0, oC = 0;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            int64_t x = gg % d.g_size[i];
+            gg /= d.g_size[i];
+            oA += x * d.g_sA[i]; oB += x * d.g_sB[i]; oC += x * d.g_sC[i];
+        }
+        for (int m = 0; m < d.M; m++)
+            for (int n = 0; n < d.N; n++) {
+                double acc = 0;
+                bool ok = true;
+                for (int k = 0; k < d.K; k++)
+                    acc += (double)ld(A, tIn, oA + (int64_t)m * d.sAm + (int64_t)k * d.sAk, ok) *
+                           ld(B, tIn, oB + (int64_t)k * d.sBk + n, ok);
+                REQ(ok, "out-of-bounds read (gemm)");
+                st(C, tC, oC + (int64_t)m * d.sCm + n, (float)acc, ok);
+                REQ(ok, "out-of-bounds write (gemm)");
+            }
+    }
+    return true;
+}
+
+bool run_wgrad(const Launch& ln, Ctx& c) {
+    WgradDesc d = desc_of<WgradDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1;
+    bool o1, o2, o3;
+    Buf A = resolve(ln.a, c, 0, o1), B = resolve(ln.b, c, 0, o2), P = resolve(ln.d, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] == d.nsplit * d.mtiles * d.ntiles && d.blocks == (int64_t)ln.grid[0], "grid");
+    REQ((int64_t)d.ksplit * d.kchunk >= d.K && d.mtiles * 64 >= d.M && d.ntiles * 64 >= d.N, "cover");
+    for (int64_t s = 0; s < d.nsplit; s++) {
+        int64_t kbi = s / d.ksplit, kc = s % d.ksplit, oA = 0, oB = 0;
+        for (int i = d.nkb - 1; i >= 0; --i) {
+            int64_t x = kbi % d.kb_size[i];
+            kbi /= d.kb_size[i];
+            oA += x * d.kb_sA[i]; oB += x * d.kb_sB[i];
+        }
+        int64_t k0 = kc * d.kchunk, k1 = std::min(d.K, k0 + d.kchunk);
+        for (int m = 0; m < d.M; m++)
+            for (int n = 0; n < d.N; n++) {
+                double acc = 0;
+                bool ok = true;
+                for (int64_t k = k0; k < k1; k++)
+                    acc += (double)ld(A, tIn, oA + m * d.sAm + k, ok) * ld(B, tIn, oB + n * d.sBn + k, ok);
+                REQ(ok, "out-of-bounds read (wgrad)");
+                st(P, 0, s * d.M * d.N + (int64_t)m * d.N + n, (float)acc, ok);
+                REQ(ok, "out-of-bounds write (wgrad)");
+            }
+    }
+    return true;
+}
+
+bool run_reduce(const Launch& ln, Ctx& c) {
+    ReduceDesc d = desc_of<ReduceDesc>(ln);
+    int tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2;
+    Buf P = resolve(ln.d, c, 0, o1), C = resolve(ln.c, c, 0, o2);
+    REQ(o1 && o2, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] * 256 >= (int64_t)d.M * d.N, "grid");
+    for (int64_t e = 0; e < (int64_t)d.M * d.N; e++) {
+        double acc = 0;
+        bool ok = true;
+        for (int64_t s = 0; s < d.nsplit; s++) acc += ld(P, 0, s * d.M * d.N + e, ok);
+        int64_t m = e / d.N, n = e % d.N;
+        st(C, tC, m * d.sCm + n * d.sCn, (float)acc, ok);
+        REQ(ok, "out-of-bounds (reduce)");
+    }
+    return true;
+}
+
+bool run_dw(const Launch& ln, Ctx& c) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1, tF = (ln.kind >> kBitAux) & 1, tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2, o3;
+    Buf I = resolve(ln.a, c, 0, o1), F = resolve(ln.b, c, 0, o2), O = resolve(ln.c, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] * d.spb >= d.nslab && d.spb * d.A * d.inner <= 4096 && d.spb <= 256 &&
+        d.K >= 1 && d.K <= 7, "launch shape");
+    for (int64_t o = 0; o < d.nslab; o++) {
+        int64_t frow = ((o / d.r_div) % d.r_size) * d.r_stride;
+        for (int p = 0; p < d.A; p++)
+            for (int q = 0; q < d.inner; q++) {
+                double acc = 0;
+                bool ok = true;
+                for (int j = 0; j < d.K; j++) {
+                    int pp = p + d.sign * j + d.off;
+                    float fv = ld(F, tF, frow + (int64_t)j * d.f_sj, ok);
+                    if (pp >= 0 && pp < d.A) acc += (double)ld(I, tIn, (o * d.A + pp) * d.inner + q, ok) * fv;
+                }
+                REQ(ok, "out-of-bounds read (dw)");
+                st(O, tC, (o * d.A + p) * d.inner + q, (float)acc, ok);
+                REQ(ok, "out-of-bounds write (dw)");
+            }
+    }
+    return true;
+}
+
+bool run_tapgrad(const Launch& ln, Ctx& c) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1;
+    bool o1, o2, o3;
+    Buf I = resolve(ln.a, c, 0, o1), G = resolve(ln.b, c, 0, o2), P = resolve(ln.d, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] == d.nblocks && d.nblocks * d.spb == d.nslab && d.r_div % d.spb == 0 &&
+        d.spb * d.A * d.inner <= 4096 && d.K >= 1 && d.K <= 7, "launch shape");
+    for (int64_t b = 0; b < d.nblocks; b++)
+        for (int j = 0; j < d.K; j++) {
+            double acc = 0;
+            bool ok = true;
+            for (int64_t o = b * d.spb; o < (b + 1) * d.spb; o++)
+                for (int p = 0; p < d.A; p++)
+                    for (int q = 0; q < d.inner; q++) {
+                        int pp = p + j + d.off;
+                        if (pp >= 0 && pp < d.A)
+                            acc += (double)ld(I, tIn, (o * d.A + pp) * d.inner + q, ok) *
+                                   ld(G, tIn, (o * d.A + p) * d.inner + q, ok);
+                    }
+            REQ(ok, "out-of-bounds read (tapgrad)");
+            st(P, 0, b * d.K + j, (float)acc, ok);
+            REQ(ok, "out-of-bounds write (tapgrad)");
+        }
+    return true;
+}
+
+bool run_tapreduce(const Launch& ln, Ctx& c) {
+    DwDesc d = desc_of<DwDesc>(ln);
+    int tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2;
+    Buf P = resolve(ln.d, c, 0, o1), O = resolve(ln.c, c, 0, o2);
+    REQ(o1 && o2, "unresolved buffer");
+    int64_t run = d.r_div / d.spb, period = run * d.r_size;
+    REQ(d.nblocks % period == 0, "blocks do not tile the filter rows");
+    for (int64_t r = 0; r < d.r_size; r++)
+        for (int j = 0; j < d.K; j++) {
+            double acc = 0;
+            bool ok = true;
+            for (int64_t a = 0; a < d.nblocks / period; a++)
+                for (int64_t cc = 0; cc < run; cc++) acc += ld(P, 0, (a * period + r * run + cc) * d.K + j, ok);
+            st(O, tC, r * d.o_sr + j * d.o_sj, (float)acc, ok);
+            REQ(ok, "out-of-bounds (tapreduce)");
+        }
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -146,11 +313,12 @@ extern "C" {
 // Returns 0 on success, else writes a message to err.
 int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* dims, int bf16,
              int mode, void* const* ins, void* out, const void* dout, void* const* din,
-             char* err, int errlen) {
+             char* err, int errlen, int generic_only) {
     try {
         std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
         std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32,
-                                             CE_FLAG_GENERIC_ONLY, false, nullptr, 0));
+                                             generic_only ? CE_FLAG_GENERIC_ONLY : 0, false,
+                                             nullptr, 0));
         if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
         Ctx c;
         int es = bf16 ? 2 : 4;
@@ -171,11 +339,20 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
         const auto& list = mode ? p->bwd : p->fwd;
         for (const Launch& ln : list) {
             int v = ln.kind & 0xff;
-            if (v != K_GENERIC_THREAD && v != K_GENERIC_WAVE && v != K_GENERIC_BLOCK) {
+            bool generic = v == K_GENERIC_THREAD || v == K_GENERIC_WAVE || v == K_GENERIC_BLOCK;
+            if (generic_only && !generic) {
                 std::snprintf(err, errlen, "non-generic launch in a generic-only plan");
                 return 3;
             }
-            if (!run_generic(ln, c)) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
+            bool ok = generic ? run_generic(ln, c)
+                    : v == K_GEMM ? run_gemm(ln, c)
+                    : v == K_WGRAD ? run_wgrad(ln, c)
+                    : v == K_REDUCE ? run_reduce(ln, c)
+                    : v == K_DW ? run_dw(ln, c)
+                    : v == K_DW_TAPGRAD ? run_tapgrad(ln, c)
+                    : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
+                    : (c.err = "unknown launch kind", false);
+            if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
         }
         return 0;
     } catch (const Error& ex) {

@@ -25,7 +25,7 @@ def emul(tmp_path_factory):
            "-fno-sanitize-recover=undefined", "-I", os.path.join(ROOT, "include"), "-I", SRC,
            os.path.join(ROOT, "tests", "cpu_emulator", "emulate.cpp"),
            os.path.join(SRC, "expr.cpp"), os.path.join(SRC, "plan.cpp"),
-           os.path.join(SRC, "capi.cpp"), "-o", out]
+           os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "capi.cpp"), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         pytest.fail(r.stderr)
@@ -45,7 +45,7 @@ def _from_storage(a, bf16):
     return a.astype(np.float64)
 
 
-def _run(L, spec, shapes, bf16, mode, ins, dy=None, out_shape=None, feature=0):
+def _run(L, spec, shapes, bf16, mode, ins, dy=None, out_shape=None, feature=0, generic=1):
     n = len(shapes)
     ranks = (C.c_int * n)(*[len(s) for s in shapes])
     bufs = [(C.c_int64 * len(s))(*s) for s in shapes]
@@ -56,7 +56,7 @@ def _run(L, spec, shapes, bf16, mode, ins, dy=None, out_shape=None, feature=0):
     if mode == 0:
         out = np.zeros(out_shape, dtype=np.uint16 if bf16 else np.float32)
         rc = L.emul_run(spec.encode(), n, ranks, dims, int(bf16), 0, inp, out.ctypes.data_as(C.c_void_p),
-                        None, None, err, 512)
+                        None, None, err, 512, generic)
         assert rc == 0, err.value.decode()
         return _from_storage(out, bf16)
     d = _to_storage(dy, bf16)
@@ -64,7 +64,7 @@ def _run(L, spec, shapes, bf16, mode, ins, dy=None, out_shape=None, feature=0):
              for i, s in enumerate(shapes)]
     din = (C.c_void_p * n)(*[g.ctypes.data for g in grads])
     rc = L.emul_run(spec.encode(), n, ranks, dims, int(bf16), 1, inp, None,
-                    d.ctypes.data_as(C.c_void_p), din, err, 512)
+                    d.ctypes.data_as(C.c_void_p), din, err, 512, generic)
     assert rc == 0, err.value.decode()
     return [_from_storage(g, bf16 and i == feature) for i, g in enumerate(grads)]
 
@@ -87,8 +87,9 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("generic", [1, 0], ids=["generic", "fast"])
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_emulated_generic_plan_matches_oracle(emul, name):
+def test_emulated_plan_matches_oracle(emul, name, generic):
     w = CASES[name]
     bf16 = w.dtype == "bf16"
     tol = 2e-2 if bf16 else 1e-5
@@ -96,16 +97,17 @@ def test_emulated_generic_plan_matches_oracle(emul, name):
     e = O.bind(O.parse(w.spec), w.shapes)
     tree = O.optimal_tree(e)[0]
     y_ref = O.eval_pairwise(e, ins, tree)
-    y = _run(emul, w.spec, w.shapes, bf16, 0, ins, out_shape=w.out_shape)
+    y = _run(emul, w.spec, w.shapes, bf16, 0, ins, out_shape=w.out_shape, generic=generic)
     assert _rel(y, y_ref) <= tol
     if not w.backward:
         return
     g_ref = O.grads_pairwise(e, ins, tree, dy)
-    g = _run(emul, w.spec, w.shapes, bf16, 1, ins, dy=dy)
+    g = _run(emul, w.spec, w.shapes, bf16, 1, ins, dy=dy, generic=generic)
     for i, (a, b) in enumerate(zip(g, g_ref)):
         assert _rel(a, b) <= tol, (name, i, _rel(a, b))
 
 
+@pytest.mark.parametrize("generic", [1, 0], ids=["generic", "fast"])
 @pytest.mark.parametrize("spec,shapes", [
     ("bsh,tsh->bth|h", [(2, 3, 11), (4, 3, 4)]),                 # even filter
     ("tsh,bsh->bth|h", [(4, 3, 3), (2, 3, 9)]),                  # feature second
@@ -118,7 +120,7 @@ def test_emulated_generic_plan_matches_oracle(emul, name):
     ("bshw,(r0)(r1)t,(r1)(r2)h,(r2)(r3)w,(r3)(r0)s->bthw|hw",
      [(1, 3, 6, 5), (2, 2, 4), (2, 2, 3), (2, 2, 3), (2, 2, 3)]),  # tensor-ring
 ])
-def test_emulated_generic_plan_edge_cases(emul, spec, shapes):
+def test_emulated_plan_edge_cases(emul, spec, shapes, generic):
     e = O.bind(O.parse(spec), shapes)
     g0 = np.random.default_rng(3)
     ins = [g0.standard_normal(s).astype(np.float32).astype(np.float64) for s in shapes]
@@ -126,7 +128,7 @@ def test_emulated_generic_plan_edge_cases(emul, spec, shapes):
     dy = g0.standard_normal(out_shape).astype(np.float32).astype(np.float64)
     tree = O.optimal_tree(e)[0] if e.n > 1 else 0
     y_ref = O.eval_pairwise(e, ins, tree)
-    y = _run(emul, spec, shapes, False, 0, ins, out_shape=out_shape)
+    y = _run(emul, spec, shapes, False, 0, ins, out_shape=out_shape, generic=generic)
     assert _rel(y, y_ref) <= 1e-6
     if e.n > 1:
         g_ref = O.grads_pairwise(e, ins, tree, dy)
@@ -136,6 +138,6 @@ def test_emulated_generic_plan_edge_cases(emul, spec, shapes):
             "".join(chr(97 + e.output.index(l)) if l in e.output else "" for l in e.inputs[0]),
             dy).reshape([s if l in e.output else 1 for l, s in zip(e.inputs[0], shapes[0])]),
             shapes[0])]
-    g = _run(emul, spec, shapes, False, 1, ins, dy=dy)
+    g = _run(emul, spec, shapes, False, 1, ins, dy=dy, generic=generic)
     for a, b in zip(g, g_ref):
         assert _rel(a, b) <= 1e-6
