@@ -33,7 +33,23 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=128, help="batch of the oracle CPU sample")
     ap.add_argument("--generic", action="store_true", help="generic kernel only")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
+                    help="only run plain device copies of this size (counter calibration)")
     return ap.parse_args()
+
+
+def measured_traffic(kname, dtype):
+    """HBM bytes per dispatch of `kname` from the committed counter summary,
+    or None when there is none or the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_c2_{dtype}.json")
+    if not os.path.exists(path):
+        return None
+    info = json.load(open(path))
+    src = os.path.join(ROOT, info["source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != info["source_sha256"]:
+        return None
+    return info["bytes_per_dispatch"].get(kname)
 
 
 def roofline(records, dtype):
@@ -54,8 +70,11 @@ def roofline(records, dtype):
     else:
         achieved, peak, unit, bound = flops / n / avg_s / 1e12, PEAK_MFMA_TFLOPS[dtype], "TFLOP/s", "mfma"
     total = sum(v[0] for v in by.values())
+    traffic = measured_traffic(kname, dtype)
     return {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+            "unit": unit, "frac": round(achieved / peak, 4),
+            "traffic": None if traffic is None else round(traffic),
+            "alg_bytes_per_launch": round(nbytes / n),
             "launches": n, "avg_us": round(ms / n * 1e3, 2),
             "share_of_kernel_time": round(ms / total, 3)}
 
@@ -93,6 +112,17 @@ def main():
         sys.exit(2)
     import numpy as np
     import torch
+
+    if args.calibrate_copy:
+        # a plain copy kernel of known size: read n bytes, write n bytes
+        n = args.calibrate_copy << 20
+        a = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
+        return
 
     import paper_2401_03384_amd as P
     import workloads as W

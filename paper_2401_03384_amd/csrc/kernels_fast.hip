@@ -314,16 +314,37 @@ __global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ 
     }
 }
 
+// C[e] = sum_s part[s][e]: a block takes 64 consecutive outputs (one per
+// lane); its 4 wavefronts sum contiguous quarters of s with 8 loads in
+// flight, then the quarters are added in a fixed order.
 template <typename TC>
 __global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float* __restrict__ part,
                                                        TC* __restrict__ C) {
-    int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    int64_t mn = (int64_t)d.M * d.N;
-    if (e >= mn) return;
+    __shared__ double q[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t mn = (int64_t)d.M * d.N;
+    const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t per = (d.nsplit + 3) / 4;
+    const int64_t s0 = wave * per, s1 = min(d.nsplit, s0 + per);
     double acc = 0.0;
-    for (int64_t s = 0; s < d.nsplit; s++) acc += part[s * mn + e];
-    int64_t m = e / d.N, n = e - m * d.N;
-    store(C, m * d.sCm + n * d.sCn, (float)acc);
+    if (e < mn) {
+        int64_t s = s0;
+        for (; s + 8 <= s1; s += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) v[u] = part[(s + u) * mn + e];
+#pragma unroll
+            for (int u = 0; u < 8; u++) acc += v[u];
+        }
+        for (; s < s1; s++) acc += part[s * mn + e];
+    }
+    q[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && e < mn) {
+        double t = (q[0][lane] + q[1][lane]) + (q[2][lane] + q[3][lane]);
+        int64_t m = e / d.N, n = e - m * d.N;
+        store(C, m * d.sCm + n * d.sCn, (float)t);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -400,20 +421,36 @@ __global__ void __launch_bounds__(256) dw_tapgrad(DwDesc d, const T* __restrict_
     if (tid < KT) part[blockIdx.x * (int64_t)KT + tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
 }
 
-// out[r][j] = sum over the blocks whose slabs use filter row r (block order)
-template <typename TC>
+// out[r][j] = sum over the blocks whose slabs use filter row r: one block per
+// r, threads stride over that row's partials, then a fixed-order block sum.
+template <typename TC, int KT>
 __global__ void __launch_bounds__(256) dw_tapreduce(DwDesc d, const float* __restrict__ part,
                                                     TC* __restrict__ out) {
-    int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (t >= d.r_size * d.K) return;
-    int64_t r = t / d.K, j = t - r * d.K;
-    int64_t run = d.r_div / d.spb;              // consecutive blocks of one row
-    int64_t period = run * d.r_size;
-    int64_t reps = d.nblocks / period;
-    double acc = 0.0;
-    for (int64_t a = 0; a < reps; a++)
-        for (int64_t c = 0; c < run; c++) acc += part[(a * period + r * run + c) * d.K + j];
-    store(out, r * d.o_sr + j * d.o_sj, (float)acc);
+    __shared__ double red[4][KT];
+    const int64_t r = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t run = d.r_div / d.spb;              // consecutive blocks of one row
+    const int64_t period = run * d.r_size;
+    const int64_t cnt = (d.nblocks / period) * run;   // partials of row r
+    double acc[KT];
+#pragma unroll
+    for (int j = 0; j < KT; j++) acc[j] = 0.0;
+    for (int64_t i = tid; i < cnt; i += 256) {
+        int64_t a = i / run, c = i - a * run;
+        const float* p = part + (a * period + r * run + c) * KT;
+#pragma unroll
+        for (int j = 0; j < KT; j++) acc[j] += p[j];
+    }
+#pragma unroll
+    for (int j = 0; j < KT; j++) {
+        double v = acc[j];
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+        if (lane == 0) red[wave][j] = v;
+    }
+    __syncthreads();
+    if (tid < KT)
+        store(out, r * d.o_sr + tid * d.o_sj, (float)((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid])));
 }
 
 // ---------------------------------------------------------------------------
@@ -554,13 +591,30 @@ hipError_t launch_dw_tapgrad(const Launch& ln, const void* a, const void* b, voi
                : dw_tapgrad_k<float>(d.K, d, g, a, b, part, s);
 }
 
+template <typename TC>
+hipError_t dw_tapreduce_k(int K, const DwDesc& d, dim3 g, const void* part, void* c, hipStream_t s) {
+    const float* p = (const float*)part;
+    TC* out = (TC*)c;
+    dim3 bl(256);
+    switch (K) {
+        case 1: hipLaunchKernelGGL((dw_tapreduce<TC, 1>), g, bl, 0, s, d, p, out); break;
+        case 2: hipLaunchKernelGGL((dw_tapreduce<TC, 2>), g, bl, 0, s, d, p, out); break;
+        case 3: hipLaunchKernelGGL((dw_tapreduce<TC, 3>), g, bl, 0, s, d, p, out); break;
+        case 4: hipLaunchKernelGGL((dw_tapreduce<TC, 4>), g, bl, 0, s, d, p, out); break;
+        case 5: hipLaunchKernelGGL((dw_tapreduce<TC, 5>), g, bl, 0, s, d, p, out); break;
+        case 6: hipLaunchKernelGGL((dw_tapreduce<TC, 6>), g, bl, 0, s, d, p, out); break;
+        case 7: hipLaunchKernelGGL((dw_tapreduce<TC, 7>), g, bl, 0, s, d, p, out); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_dw_tapreduce(const Launch& ln, const void* part, void* c, hipStream_t s) {
     DwDesc d = desc_of<DwDesc>(ln);
     int tC = (ln.kind >> kBitOut) & 1;
-    dim3 g(ln.grid[0]), bl(256);
-    if (tC) hipLaunchKernelGGL((dw_tapreduce<bf16_t>), g, bl, 0, s, d, (const float*)part, (bf16_t*)c);
-    else hipLaunchKernelGGL((dw_tapreduce<float>), g, bl, 0, s, d, (const float*)part, (float*)c);
-    return hipGetLastError();
+    dim3 g(ln.grid[0]);
+    return tC ? dw_tapreduce_k<bf16_t>(d.K, d, g, part, c, s)
+              : dw_tapreduce_k<float>(d.K, d, g, part, c, s);
 }
 
 }  // namespace

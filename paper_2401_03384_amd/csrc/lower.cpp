@@ -83,6 +83,9 @@ void set_desc(Launch& ln, const D& d) {
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Element type as it appears in the kernel's template arguments.
+const char* tname(DType t) { return t == DT_BF16 ? "unsigned short" : "float"; }
+
 // ---- channel-mixing GEMM -------------------------------------------------
 bool try_gemm(const PairOp& op, std::vector<Launch>& out) {
     if (!op.convs.empty() || !op.has_r) return false;
@@ -165,8 +168,8 @@ bool try_gemm(const PairOp& op, std::vector<Launch>& out) {
         ln.grid[0] = (uint32_t)d.blocks;
         ln.block[0] = 256;
         set_desc(ln, d);
-        ln.kname = std::string(D.dtype == DT_BF16 ? "gemm_bf16" : "gemm_f32") +
-                   (MT == 2 ? "_mt2" : "_mt1");
+        ln.kname = std::string(D.dtype == DT_BF16 ? "gemm_bf16<" : "gemm_f32<") + tname(C.dtype) +
+                   (MT == 2 ? ", 2, " : ", 1, ") + (vec ? "true>" : "false>");
         out.push_back(ln);
         return true;
     }
@@ -230,8 +233,9 @@ bool try_wgrad(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out
     d.mtiles = (int32_t)cdiv(M, 64);
     d.ntiles = (int32_t)cdiv(N, 64);
     int64_t tiles = (int64_t)d.mtiles * d.ntiles;
-    // aim at ~2048 blocks; chunks are multiples of the 32-element tile
-    int64_t want = std::max<int64_t>(1, cdiv(2048, KB * tiles));
+    // aim at ~512 blocks (two per CU): few partials to reduce, long chunks;
+    // chunks are multiples of the 32-element tile
+    int64_t want = std::max<int64_t>(1, cdiv(512, KB * tiles));
     int64_t kchunk = std::max<int64_t>(32, cdiv(cdiv(K, want), 32) * 32);
     d.kchunk = (int32_t)std::min<int64_t>(kchunk, (int64_t)1 << 30);
     d.ksplit = (int32_t)cdiv(K, d.kchunk);
@@ -249,7 +253,7 @@ bool try_wgrad(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out
     ln.grid[0] = (uint32_t)d.blocks;
     ln.block[0] = 256;
     set_desc(ln, d);
-    ln.kname = L.dtype == DT_BF16 ? "wgrad_bf16" : "wgrad_f32";
+    ln.kname = std::string("wgrad<") + tname(L.dtype) + (vec ? ", true>" : ", false>");
     out.push_back(ln);
     ReduceDesc rd;
     std::memset(&rd, 0, sizeof(rd));
@@ -262,10 +266,10 @@ bool try_wgrad(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out
     lr.kind = K_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
     lr.d = part;
     lr.c = C.buf;
-    lr.grid[0] = (uint32_t)cdiv(M * N, 256);
+    lr.grid[0] = (uint32_t)cdiv(M * N, 64);
     lr.block[0] = 256;
     set_desc(lr, rd);
-    lr.kname = "reduce_partials";
+    lr.kname = std::string("reduce_partials<") + tname(C.dtype) + ">";
     out.push_back(lr);
     return true;
 }
@@ -385,7 +389,8 @@ bool try_dw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
         ln.grid[0] = (uint32_t)d.nblocks;
         ln.block[0] = 256;
         set_desc(ln, d);
-        ln.kname = bX == 1 ? "dw_conv" : "dw_conv_transposed";
+        ln.kname = std::string("dw_conv<") + tname(X.dtype) + ", " + tname(Fl.dtype) + ", " +
+                   tname(op.C.dtype) + ", " + std::to_string(d.K) + ">";
         out.push_back(ln);
         return true;
     }
@@ -431,16 +436,16 @@ bool try_dw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
         ln.grid[0] = (uint32_t)d.nblocks;
         ln.block[0] = 256;
         set_desc(ln, d);
-        ln.kname = "dw_tapgrad";
+        ln.kname = std::string("dw_tapgrad<") + tname(Xf.dtype) + ", " + std::to_string(d.K) + ">";
         out.push_back(ln);
         Launch lr;
         lr.kind = K_DW_TAPREDUCE | dt_bits(DT_F32, DT_F32, op.C.dtype);
         lr.d = part;
         lr.c = op.C.buf;
-        lr.grid[0] = (uint32_t)cdiv(d.r_size * d.K, 256);
+        lr.grid[0] = (uint32_t)d.r_size;
         lr.block[0] = 256;
         set_desc(lr, d);
-        lr.kname = "dw_tapreduce";
+        lr.kname = std::string("dw_tapreduce<") + tname(op.C.dtype) + ", " + std::to_string(d.K) + ">";
         out.push_back(lr);
         return true;
     }
@@ -459,8 +464,11 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
         out.clear();
         Launch ln = lower_generic(op);
         int v = ln.kind & 0xff;
-        ln.kname = v == K_GENERIC_THREAD ? "generic_thread" : v == K_GENERIC_WAVE ? "generic_wave"
-                                                                                    : "generic_block";
+        ln.kname = std::string(v == K_GENERIC_THREAD ? "generic_thread<" : v == K_GENERIC_WAVE
+                                                                              ? "generic_wave<"
+                                                                              : "generic_block<") +
+                   tname(op.L.dtype) + ", " + tname(op.has_r ? op.R.dtype : DT_F32) + ", " +
+                   tname(op.C.dtype) + ">";
         out.push_back(ln);
     }
     double bytes = tensor_bytes(op.L) + (op.has_r ? tensor_bytes(op.R) : 0) + tensor_bytes(op.C);

@@ -218,7 +218,7 @@ bool run_reduce(const Launch& ln, Ctx& c) {
     bool o1, o2;
     Buf P = resolve(ln.d, c, 0, o1), C = resolve(ln.c, c, 0, o2);
     REQ(o1 && o2, "unresolved buffer");
-    REQ((int64_t)ln.grid[0] * 256 >= (int64_t)d.M * d.N, "grid");
+    REQ((int64_t)ln.grid[0] * 64 >= (int64_t)d.M * d.N, "grid");
     for (int64_t e = 0; e < (int64_t)d.M * d.N; e++) {
         double acc = 0;
         bool ok = true;
@@ -292,6 +292,7 @@ bool run_tapreduce(const Launch& ln, Ctx& c) {
     REQ(o1 && o2, "unresolved buffer");
     int64_t run = d.r_div / d.spb, period = run * d.r_size;
     REQ(d.nblocks % period == 0, "blocks do not tile the filter rows");
+    REQ((int64_t)ln.grid[0] == d.r_size, "grid");
     for (int64_t r = 0; r < d.r_size; r++)
         for (int j = 0; j < d.K; j++) {
             double acc = 0;
