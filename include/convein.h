@@ -118,6 +118,7 @@ void ce_expr_destroy(ce_expr* e);
 
 /* Plan flags. */
 #define CE_FLAG_GENERIC_ONLY 0x1u  /* run every step on the generic strided kernel */
+#define CE_FLAG_NO_FUSION 0x2u     /* one launch per pairwise step (no fused chains) */
 
 /* Choose the pairwise evaluation order with the fewest multiplications under
  * `mode` (Section 3.2, optimal sequencer; Appendix B tnn-cost), searching

@@ -26,6 +26,7 @@ CE_BF16 = 1
 CE_COST_FWD = 0
 CE_COST_TRAIN_PAPER = 1
 CE_FLAG_GENERIC_ONLY = 0x1
+CE_FLAG_NO_FUSION = 0x2
 
 _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR_UNSUPPORTED",
                  -4: "CE_ERR_ARG", -5: "CE_ERR_WORKSPACE", -6: "CE_ERR_OVERFLOW", -7: "CE_ERR_HIP"}

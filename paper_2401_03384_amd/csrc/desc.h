@@ -46,6 +46,7 @@ enum KernelKind : int32_t {
     K_DW = 19,              // depthwise convolution along one axis (DwDesc)
     K_DW_TAPGRAD = 20,      // per-block partial filter-tap gradients (DwDesc)
     K_DW_TAPREDUCE = 21,    // ordered sum of tap partials (DwDesc)
+    K_CP_FWD = 22,          // fused CP chain forward (CpDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -99,6 +100,25 @@ struct DwDesc {
     int64_t r_div, r_size, r_stride, f_sj;
     int64_t nblocks;
     int64_t o_sr, o_sj;        // tap reduce: output strides
+};
+
+// Fused CP chain (the four forward steps of a CP-factorised 2-D conv layer):
+//   Z1[r][p] = sum_s Us[r][s] X[b][s][p]          (channel contraction)
+//   Z2 = Z1 (*)_h Kh[r],  Z3 = Z2 (*)_w Kw[r]     (depthwise, same padding)
+//   Y[b][t][p] = sum_r Ut[r][t] Z3[r][p]          (channel expansion)
+// p = h*W + w is unit-stride in X and Y.  A block owns the rows
+// [seg*seg_rows, ...) of one image and walks them in chunks of TH rows,
+// keeping the last KH-1 rows of Z1 in a ring.
+struct CpDesc {
+    int32_t B, S, R, T, H, W, KH, KW;
+    int32_t TH, segs, seg_rows, nthreads;
+    int64_t x_sb, x_ss, y_sb, y_st;
+    int64_t us_sr, us_ss, ut_sr, ut_st;
+    int64_t kh_sr, kh_sj, kw_sr, kw_sj;
+    int64_t blocks;
+    // LDS carve-up (byte offsets) and leading dimensions, set by the planner
+    uint32_t lds_bytes, o_us, o_ut, o_kh, o_kw, o_ring, o_z2, o_xz;
+    int32_t lda, ldu, pxp, nr;
 };
 
 }  // namespace ce

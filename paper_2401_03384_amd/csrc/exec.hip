@@ -41,6 +41,11 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
         case K_GENERIC_THREAD:
         case K_GENERIC_WAVE:
         case K_GENERIC_BLOCK: return launch_generic(ln, a, b, c, s);
+        case K_CP_FWD: {
+            const void* ops[5] = {a, b, resolve(ln.extra[0], P), resolve(ln.extra[1], P),
+                                  resolve(ln.extra[2], P)};
+            return launch_cp_fwd(ln, ops, c, s);
+        }
         default: return launch_fast(ln, a, b, c, d, s);
     }
 }

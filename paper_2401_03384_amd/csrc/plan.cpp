@@ -542,14 +542,17 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             return m;
         };
         auto patch = [&](std::vector<Launch>& v, const std::vector<WsItem>& items) {
-            for (auto& ln : v)
-                for (BufRef* b : {&ln.a, &ln.b, &ln.c, &ln.d})
+            for (auto& ln : v) {
+                std::vector<BufRef*> refs = {&ln.a, &ln.b, &ln.c, &ln.d};
+                for (auto& x : ln.extra) refs.push_back(&x);
+                for (BufRef* b : refs)
                     if (b->kind == BUF_WS) {
                         bool found = false;
                         for (auto& it : items)
                             if (it.id == b->index) { b->offset = it.offset; found = true; break; }
                         if (!found) fail(CE_ERR_ARG, "internal: workspace item missing");
                     }
+            }
         };
         struct ItemScratch : ScratchAlloc {
             std::vector<WsItem>* items = nullptr;
@@ -620,6 +623,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             fs.t = s;
             for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) fuse_launches(p->fwd, false);
         p->ws_fwd = pack(items);
         patch(p->fwd, items);
 

@@ -56,6 +56,7 @@ struct PairOp {
 struct Launch {
     int32_t kind = 0;
     BufRef a, b, c, d;                // operands (meaning depends on kind)
+    std::vector<BufRef> extra;        // further operands of fused kernels
     uint32_t need = 0;
     uint32_t grid[3] = {1, 1, 1}, block[3] = {1, 1, 1};
     uint32_t lds = 0;
@@ -114,6 +115,10 @@ struct ScratchAlloc {
 
 // The generic strided kernel for any pairwise op.
 Launch lower_generic(const PairOp& op);
+
+// Replace runs of launches that form a fused chain (e.g. the CP chain) by one
+// fused launch.  Returns the number of fusions done.
+int fuse_launches(std::vector<Launch>& v, bool backward);
 
 // Lowering of one pairwise op to launches: a specialised kernel when the
 // op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.

@@ -8,6 +8,7 @@
 // assumes.  A test compares the results with the oracle, so
 // descriptor, layout and workspace bugs show up without a GPU, and an
 // out-of-bounds access is reported instead of faulting a device.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -305,6 +306,86 @@ bool run_tapreduce(const Launch& ln, Ctx& c) {
     return true;
 }
 
+// Fused CP chain forward: the four steps with the descriptor's strides, plus
+// the launch-shape and LDS-layout invariants the kernel relies on.
+bool run_cp_fwd(const Launch& ln, Ctx& c) {
+    CpDesc d = desc_of<CpDesc>(ln);
+    int bf = (ln.kind >> kBitIn) & 1;
+    bool o1, o2, o3;
+    Buf X = resolve(ln.a, c, 0, o1), Us = resolve(ln.b, c, 0, o2), Y = resolve(ln.c, c, 0, o3);
+    REQ(o1 && o2 && o3 && ln.extra.size() == 3, "unresolved buffer");
+    bool o4, o5, o6;
+    Buf Kh = resolve(ln.extra[0], c, 0, o4), Kw = resolve(ln.extra[1], c, 0, o5),
+        Ut = resolve(ln.extra[2], c, 0, o6);
+    REQ(o4 && o5 && o6, "unresolved buffer");
+    REQ((d.R == 32 || d.R == 64) && d.T % 32 == 0 && d.T <= 64 && d.S % 32 == 0, "sizes");
+    REQ(d.TH >= 1 && d.TH * d.W <= 256 && d.KH >= 1 && d.KH <= 7 && d.KW >= 1 && d.KW <= 7, "tile");
+    REQ(d.nthreads == 256 && ln.block[0] == 256, "block");
+    REQ((int64_t)ln.grid[0] == d.blocks && d.blocks == (int64_t)d.B * d.segs &&
+        (int64_t)d.segs * d.seg_rows >= d.H, "grid");
+    int e = bf ? 2 : 4;
+    int nr = d.TH + d.KH - 1, pxp = (d.TH * d.W + 31) / 32 * 32;
+    REQ(d.nr == nr && d.pxp == pxp, "layout dims");
+    REQ(d.lda >= d.S + (bf ? 8 : 1) && d.ldu >= d.R + (bf ? 8 : 1), "leading dims");
+    REQ(d.o_ut >= d.o_us + (uint64_t)d.R * d.lda * e && d.o_kh >= d.o_ut + (uint64_t)d.T * d.ldu * e &&
+        d.o_kw >= d.o_kh + (uint64_t)d.R * d.KH * 4 && d.o_ring >= d.o_kw + (uint64_t)d.R * d.KW * 4 &&
+        d.o_z2 >= d.o_ring + (uint64_t)nr * d.R * d.W * 4 && d.o_xz >= d.o_z2 + (uint64_t)d.TH * d.R * d.W * 4,
+        "LDS regions overlap");
+    uint64_t xs = bf ? (uint64_t)pxp * 40 * 2 : (uint64_t)32 * pxp * 4;
+    uint64_t z3 = bf ? (uint64_t)pxp * d.ldu * 2 : (uint64_t)d.R * pxp * 4;
+    REQ(d.lds_bytes >= d.o_xz + std::max(xs, z3) && d.lds_bytes <= 160 * 1024, "LDS size");
+    REQ(ln.lds == d.lds_bytes, "launch LDS");
+    // bf16 operands are read as 16-byte k-runs
+    REQ((d.o_us | d.o_ut | d.o_xz) % 16 == 0 &&
+        (!bf || ((d.lda * e) % 16 == 0 && (d.ldu * e) % 16 == 0 && d.S % 8 == 0 && d.R % 8 == 0)),
+        "alignment");
+    const int H = d.H, W = d.W, R = d.R, ch = (d.KH - 1) / 2, cw = (d.KW - 1) / 2;
+    std::vector<double> z1((size_t)R * H * W), z2((size_t)R * H * W), z3v((size_t)R * H * W);
+    bool ok = true;
+    for (int b = 0; b < d.B; b++) {
+        for (int r = 0; r < R; r++)
+            for (int p = 0; p < H * W; p++) {
+                double a = 0;
+                for (int s2 = 0; s2 < d.S; s2++)
+                    a += (double)ld(Us, bf, (int64_t)r * d.us_sr + (int64_t)s2 * d.us_ss, ok) *
+                         ld(X, bf, (int64_t)b * d.x_sb + (int64_t)s2 * d.x_ss + p, ok);
+                z1[(size_t)r * H * W + p] = a;
+            }
+        for (int r = 0; r < R; r++)
+            for (int h = 0; h < H; h++)
+                for (int w = 0; w < W; w++) {
+                    double a = 0;
+                    for (int j = 0; j < d.KH; j++) {
+                        int hh = h + j - ch;
+                        if (hh >= 0 && hh < H)
+                            a += z1[((size_t)r * H + hh) * W + w] * ld(Kh, bf, (int64_t)r * d.kh_sr + (int64_t)j * d.kh_sj, ok);
+                    }
+                    z2[((size_t)r * H + h) * W + w] = a;
+                }
+        for (int r = 0; r < R; r++)
+            for (int h = 0; h < H; h++)
+                for (int w = 0; w < W; w++) {
+                    double a = 0;
+                    for (int j = 0; j < d.KW; j++) {
+                        int ww = w + j - cw;
+                        if (ww >= 0 && ww < W)
+                            a += z2[((size_t)r * H + h) * W + ww] * ld(Kw, bf, (int64_t)r * d.kw_sr + (int64_t)j * d.kw_sj, ok);
+                    }
+                    z3v[((size_t)r * H + h) * W + w] = a;
+                }
+        for (int t = 0; t < d.T; t++)
+            for (int p = 0; p < H * W; p++) {
+                double a = 0;
+                for (int r = 0; r < R; r++)
+                    a += (double)ld(Ut, bf, (int64_t)r * d.ut_sr + (int64_t)t * d.ut_st, ok) *
+                         z3v[(size_t)r * H * W + p];
+                st(Y, bf, (int64_t)b * d.y_sb + (int64_t)t * d.y_st + p, (float)a, ok);
+            }
+        REQ(ok, "out-of-bounds access (cp_fwd)");
+    }
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -352,6 +433,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_DW ? run_dw(ln, c)
                     : v == K_DW_TAPGRAD ? run_tapgrad(ln, c)
                     : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
+                    : v == K_CP_FWD ? run_cp_fwd(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
         }

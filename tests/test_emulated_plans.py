@@ -25,7 +25,8 @@ def emul(tmp_path_factory):
            "-fno-sanitize-recover=undefined", "-I", os.path.join(ROOT, "include"), "-I", SRC,
            os.path.join(ROOT, "tests", "cpu_emulator", "emulate.cpp"),
            os.path.join(SRC, "expr.cpp"), os.path.join(SRC, "plan.cpp"),
-           os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "capi.cpp"), "-o", out]
+           os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "fuse.cpp"),
+           os.path.join(SRC, "capi.cpp"), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         pytest.fail(r.stderr)
