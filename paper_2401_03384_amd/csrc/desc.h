@@ -106,19 +106,20 @@ struct DwDesc {
 //   Z1[r][p] = sum_s Us[r][s] X[b][s][p]          (channel contraction)
 //   Z2 = Z1 (*)_h Kh[r],  Z3 = Z2 (*)_w Kw[r]     (depthwise, same padding)
 //   Y[b][t][p] = sum_r Ut[r][t] Z3[r][p]          (channel expansion)
-// p = h*W + w is unit-stride in X and Y.  A block owns the rows
-// [seg*seg_rows, ...) of one image and walks them in chunks of TH rows,
-// keeping the last KH-1 rows of Z1 in a ring.
+// p = h*W + w is unit-stride in X and Y.  One wavefront owns a strip of 32
+// columns (overlapping its neighbours by the conv_w halo) over seg_rows rows
+// of one sample.
 struct CpDesc {
     int32_t B, S, R, T, H, W, KH, KW;
-    int32_t TH, segs, seg_rows, nthreads;
+    int32_t ncb, colstride, segs, seg_rows;
     int64_t x_sb, x_ss, y_sb, y_st;
     int64_t us_sr, us_ss, ut_sr, ut_st;
     int64_t kh_sr, kh_sj, kw_sr, kw_sj;
-    int64_t blocks;
-    // LDS carve-up (byte offsets) and leading dimensions, set by the planner
-    uint32_t lds_bytes, o_us, o_ut, o_kh, o_kw, o_ring, o_z2, o_xz;
-    int32_t lda, ldu, pxp, nr;
+    int64_t waves, blocks;
+    // LDS operand tables, laid out by the planner: UsL [32][lda] at 0, the
+    // permuted Ut operands at o_ut, the permuted taps at o_kh / o_kw
+    uint32_t lds_bytes, o_ut, o_kh, o_kw;
+    int32_t lda;
 };
 
 }  // namespace ce

@@ -18,31 +18,21 @@ namespace {
 
 size_t al16(size_t x) { return (x + 15) & ~size_t(15); }
 
-// LDS carve-up of the fused CP kernel: factors, taps, the Z1 ring of
-// TH+KH-1 rows, Z2 (TH rows) and a region shared by the X slice staging and Z3.
-// bf16 operands are stored k-contiguous with 8 elements of padding so every
-// 16-byte MFMA operand read is aligned.
-size_t cp_layout(CpDesc& d, bool bf) {
-    d.nr = d.TH + d.KH - 1;
-    d.pxp = (d.TH * d.W + 31) / 32 * 32;
+// LDS operand tables of the fused CP kernel: Us as [32][S+pad] (the GEMM1 A
+// operand rows; bf16 rows padded to keep 16-byte k-runs aligned), Ut permuted
+// to the accumulator-layout pairing of GEMM2 (fp32 [16][2][T], bf16
+// [2][2][T][8]) and the taps permuted the same way ([16][2][K]).
+void cp_tables(CpDesc& d, bool bf) {
     d.lda = bf ? d.S + 8 : d.S + 1;
-    d.ldu = bf ? d.R + 8 : d.R + 1;
-    size_t e = bf ? 2 : 4;
-    size_t o = 0;
-    d.o_us = (uint32_t)o; o = al16(o + (size_t)d.R * d.lda * e);
-    d.o_ut = (uint32_t)o; o = al16(o + (size_t)d.T * d.ldu * e);
-    d.o_kh = (uint32_t)o; o = al16(o + (size_t)d.R * d.KH * 4);
-    d.o_kw = (uint32_t)o; o = al16(o + (size_t)d.R * d.KW * 4);
-    d.o_ring = (uint32_t)o; o = al16(o + (size_t)d.nr * d.R * d.W * 4);
-    d.o_z2 = (uint32_t)o; o = al16(o + (size_t)d.TH * d.R * d.W * 4);
-    d.o_xz = (uint32_t)o;
-    size_t xs = bf ? (size_t)d.pxp * 40 * 2 : (size_t)32 * d.pxp * 4;
-    size_t z3 = bf ? (size_t)d.pxp * d.ldu * 2 : (size_t)d.R * d.pxp * 4;
-    o = al16(o + std::max(xs, z3));
-    d.lds_bytes = (uint32_t)o;
-    return o;
+    size_t o = al16((size_t)32 * d.lda * (bf ? 2 : 4));
+    d.o_ut = (uint32_t)o;
+    o = al16(o + (bf ? (size_t)2 * 2 * d.T * 8 * 2 : (size_t)16 * 2 * d.T * 4));
+    d.o_kh = (uint32_t)o;
+    o += (size_t)16 * 2 * d.KH * 4;
+    d.o_kw = (uint32_t)o;
+    o += (size_t)16 * 2 * d.KW * 4;
+    d.lds_bytes = (uint32_t)al16(o);
 }
-
 
 template <typename D>
 D desc(const Launch& ln) {
@@ -86,7 +76,9 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     if (w.nslab != B * R * H || w.A != W || w.inner != 1 || w.r_div != H || w.r_size != R ||
         w.sign != 1 || w.off != -((w.K - 1) / 2))
         return false;
-    if (!(R == 32 || R == 64) || T % 32 || T > 64 || S % 32 || W > 256) return false;
+    // register-resident strips: rank 32, T in {32, 64}, 3x3 or 5x5 filters
+    if (R != 32 || !(T == 32 || T == 64) || S % 32 || h.K != w.K || !(h.K == 3 || h.K == 5))
+        return false;
     CpDesc d;
     std::memset(&d, 0, sizeof(d));
     d.B = (int32_t)B;
@@ -109,21 +101,18 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     d.kh_sj = h.f_sj;
     d.kw_sr = w.r_stride;
     d.kw_sj = w.f_sj;
-    d.nthreads = 256;
-    // rows per chunk: at most 8 column blocks of 32 pixels, LDS within 150 KB
-    d.TH = 0;
-    for (int th = 4; th >= 1; th--) {
-        if (th * W > 256) continue;
-        d.TH = th;
-        if (cp_layout(d, dt == 1) <= 150 * 1024) break;
-        d.TH = 0;
-    }
-    if (d.TH == 0) return false;
-    cp_layout(d, dt == 1);
-    int64_t segs = std::max<int64_t>(1, (512 + B - 1) / B);
+    d.colstride = 32 - (w.K - 1);
+    d.ncb = (int32_t)((W + d.colstride - 1) / d.colstride);
+    // wavefronts: about two (fp32) or four (bf16) per SIMD of the 1024 SIMDs;
+    // each strip segment recomputes KH-1 rows of Z1
+    int64_t want = dt ? 4096 : 2048;
+    int64_t segs = std::max<int64_t>(1, std::min<int64_t>(H, want / std::max<int64_t>(1, B * d.ncb)));
     d.seg_rows = (int32_t)((H + segs - 1) / segs);
     d.segs = (int32_t)((H + d.seg_rows - 1) / d.seg_rows);
-    d.blocks = B * d.segs;
+    d.waves = B * d.ncb * d.segs;
+    d.blocks = (d.waves + 3) / 4;
+    if (d.blocks > 0x7fffffff) return false;
+    cp_tables(d, dt == 1);
     fused = Launch();
     fused.kind = K_CP_FWD | (dt << kBitIn) | (dt << kBitAux) | (dt << kBitOut);
     fused.a = g1.b;                       // X
@@ -137,7 +126,8 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     std::memcpy(fused.desc.data(), &d, sizeof(d));
     fused.need = g1.need | d1.need | d2.need | g2.need;
     fused.what = "fused CP chain: " + g1.what + " | " + d1.what + " | " + d2.what + " | " + g2.what;
-    fused.kname = std::string("cp_fwd<") + (dt ? "unsigned short" : "float") + ", 4, 2>";
+    fused.kname = std::string("cp_fwd<") + (dt ? "unsigned short" : "float") + ", " +
+                  std::to_string(h.K) + ", " + std::to_string(w.K) + ", " + std::to_string(T / 32) + ">";
     fused.alg_bytes = g1.alg_bytes + d1.alg_bytes + d2.alg_bytes + g2.alg_bytes;
     fused.alg_flops = g1.alg_flops + d1.alg_flops + d2.alg_flops + g2.alg_flops;
     // algorithmic bytes of the fused launch: X, factors and Y only

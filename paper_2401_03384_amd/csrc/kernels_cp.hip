@@ -1,17 +1,23 @@
 // Fused CP chain for gfx950: the four forward steps of a CP-factorised 2-D
 // convolution layer (Section 2.3, CP convolutional layer; the pairwise steps
 // the sequencer picks for it: contract s, convolve h, convolve w, contract r)
-// in one kernel, so the rank-R intermediates never leave the CU.
+// in one kernel, with the rank-32 intermediates held in registers.
 //
-// A block owns seg_rows image rows of one sample and walks them in chunks of
-// TH rows.  Per chunk:
-//   GEMM1  Z1 rows entering the ring:  Z1[r][p] = sum_s Us[r][s] X[s][p]
-//          (X staged through LDS in 32-channel slices; bf16 staged transposed
-//          so each lane reads one 16-byte k-run per MFMA)
-//   conv_h Z2[row][r][w] from the ring of KH-1 + TH rows of Z1
-//   conv_w Z3 (MFMA-ready layout, zero padding at the row ends)
-//   GEMM2  Y[t][p] = sum_r Ut[r][t] Z3[r][p], stored from the accumulators.
-// Rows outside the image are zero in the ring (same padding of conv_h).
+// One wavefront owns a strip of 32 image columns of one sample (strips
+// overlap by the conv_w halo) and walks seg_rows rows down it:
+//   GEMM1   Z1 for the row entering the ring (32x32 MFMA, X read straight from
+//           HBM in the B-operand layout: lanes 0-31 one channel row, 32-63 the
+//           next).  The accumulator layout holds Z1[r][col] with col = lane%32
+//           and r = 8*(i/4) + 4*(lane/32) + i%4 for accumulator i.
+//   conv_h  a ring of KH such accumulator sets: per-element FMAs.
+//   conv_w  neighbouring columns are neighbouring lanes of the same half:
+//           lane permutes; the strip's edge lanes are discarded.
+//   GEMM2   consumes Z3 straight from the accumulator layout: instruction i
+//           pairs k-slot 0 (lanes 0-31) with r = row(i, 0) and k-slot 1 (lanes
+//           32-63) with r = row(i, 32); the A operand (Ut) is permuted to the
+//           same pairing in LDS, so no data movement is needed.
+// Rows and columns outside the image read X as zero, which is the same
+// padding of both convolutions.
 #include <cstring>
 
 #include "desc.h"
@@ -30,234 +36,220 @@ __device__ __forceinline__ bf16x8 lds8(const bf16_t* p) {
     return v;
 }
 
-__device__ __forceinline__ int row32(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+__device__ __forceinline__ bf16x8 pack8(const bf16_t* v) {
+    bf16x8 r;
+    __builtin_memcpy(&r, v, 16);
+    return r;
+}
 
-// CBW column blocks of 32 pixels per wave at most; M blocks (R/32, T/32) at most 2.
-template <typename T, int NW, int CBW>
-__global__ void __launch_bounds__(NW * 64) cp_fwd(CpDesc d, const T* __restrict__ X,
-                                                  const T* __restrict__ Us, const T* __restrict__ Kh,
-                                                  const T* __restrict__ Kw, const T* __restrict__ Ut,
-                                                  T* __restrict__ Y) {
+// r held by accumulator i of a lane in a 32x32 MFMA result
+__device__ __forceinline__ int row32(int i, int lane) {
+    return 8 * (i >> 2) + 4 * ((lane >> 5) & 1) + (i & 3);
+}
+
+// Two blocks per CU (256 VGPRs a lane) except for the bf16 5x5 variant, whose
+// larger ring and bf16 operand packing do not fit that without spilling.
+template <typename T, int KH, int KW, int MB2>
+__global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_fwd(CpDesc d, const T* __restrict__ X,
+                                              const T* __restrict__ Us, const T* __restrict__ Kh,
+                                              const T* __restrict__ Kw, const T* __restrict__ Ut,
+                                              T* __restrict__ Y) {
     constexpr bool BF = sizeof(T) == 2;
+    constexpr int TT = 32 * MB2;
+    constexpr int CH = (KH - 1) / 2, HWW = (KW - 1) / 2;
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    T* UsL = (T*)(smem + d.o_us);
-    T* UtL = (T*)(smem + d.o_ut);
-    float* KhL = (float*)(smem + d.o_kh);
-    float* KwL = (float*)(smem + d.o_kw);
-    float* ring = (float*)(smem + d.o_ring);
-    float* Z2 = (float*)(smem + d.o_z2);
-    unsigned char* XZ = smem + d.o_xz;
-    const int R = d.R, S = d.S, TT = d.T, W = d.W, H = d.H, KH = d.KH, KW = d.KW, TH = d.TH;
-    const int NR = d.nr, PXP = d.pxp, LDA = d.lda, LDU = d.ldu;
-    const int ch = (KH - 1) / 2, cw = (KW - 1) / 2;
-    const int nmb = R / 32, nmb2 = TT / 32;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = (int)(blockIdx.x / d.segs), seg = (int)(blockIdx.x % d.segs);
-    const int h_begin = seg * d.seg_rows;
-    const int h_end = min(H, h_begin + d.seg_rows);
-    if (h_begin >= h_end) return;   // whole block
+    const int S = d.S, H = d.H, W = d.W;
+    const int LDA = d.lda;
+    T* UsL = (T*)smem;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
 
-    for (int e = tid; e < R * S; e += NW * 64) {
+    // ---- tables ----
+    {
+    T* UtP = (T*)(smem + d.o_ut);
+    float* KhP = (float*)(smem + d.o_kh);
+    float* KwP = (float*)(smem + d.o_kw);
+    for (int e = tid; e < 32 * S; e += 256) {
         int r = e / S, s = e - r * S;
         UsL[r * LDA + s] = Us[r * d.us_sr + s * d.us_ss];
     }
-    for (int e = tid; e < TT * R; e += NW * 64) {
-        int t = e / R, r = e - t * R;
-        UtL[t * LDU + r] = Ut[r * d.ut_sr + t * d.ut_st];
+    if constexpr (BF) {
+        // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t]
+        for (int e = tid; e < 2 * 2 * TT * 8; e += 256) {
+            int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
+            UtP[e] = Ut[row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st];
+        }
+    } else {
+        // UtP[i][hf][t] = Ut[row32(i, 32*hf)][t]
+        for (int e = tid; e < 16 * 2 * TT; e += 256) {
+            int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
+            UtP[e] = Ut[row32(i, 32 * hf) * d.ut_sr + t * d.ut_st];
+        }
     }
-    for (int e = tid; e < R * KH; e += NW * 64) {
-        int r = e / KH, j = e - r * KH;
-        KhL[e] = load(Kh, r * d.kh_sr + j * d.kh_sj);
+    for (int e = tid; e < 16 * 2 * KH; e += 256) {
+        int j = e % KH, hf = (e / KH) & 1, i = e / (2 * KH);
+        KhP[e] = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
     }
-    for (int e = tid; e < R * KW; e += NW * 64) {
-        int r = e / KW, j = e - r * KW;
-        KwL[e] = load(Kw, r * d.kw_sr + j * d.kw_sj);
+    for (int e = tid; e < 16 * 2 * KW; e += 256) {
+        int j = e % KW, hf = (e / KW) & 1, i = e / (2 * KW);
+        KwP[e] = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
+    }
     }
     __syncthreads();
 
-    const T* Xb = X + (int64_t)b * d.x_sb;
-    T* Yb = Y + (int64_t)b * d.y_sb;
-    const int base_row = h_begin - ch;
-    auto slot = [&](int hh) { return (hh - base_row) % NR; };
+    // ---- this wavefront's strip ----
+    const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
+    if (gw >= d.waves) return;
+    const int seg = (int)(gw % d.segs);
+    const int64_t rest = gw / d.segs;
+    const int cb = (int)(rest % d.ncb);
+    const int b = (int)(rest / d.ncb);
+    const int col = cb * d.colstride - HWW + (lane & 31);
+    const bool colok = col >= 0 && col < W;
+    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
+    const T* Xc = X + (int64_t)b * d.x_sb + (colok ? col : 0);
+    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
+    const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
 
-    // Z1 for image rows [r0, r0 + nr), nr <= TH, into the ring
-    auto gemm1 = [&](int r0, int nr) {
-        const int np = nr * W, ncb = (np + 31) / 32;
-        f32x16 acc[CBW][2];
+    auto gemm1 = [&](int row) {
+        f32x16 acc;
 #pragma unroll
-        for (int c = 0; c < CBW; c++)
+        for (int i = 0; i < 16; i++) acc[i] = 0.f;
+        if (row < 0 || row >= H) return acc;   // uniform over the wave
+        const T* xr = Xc + (int64_t)row * W;
+        if constexpr (BF) {
+            for (int k = 0; k < S; k += 16) {
+                bf16_t xv[8];
 #pragma unroll
-            for (int mb = 0; mb < 2; mb++)
-#pragma unroll
-                for (int i = 0; i < 16; i++) acc[c][mb][i] = 0.f;
-        for (int s0 = 0; s0 < S; s0 += 32) {
-            for (int e = tid; e < 32 * PXP; e += NW * 64) {
-                int ss = e / PXP, px = e - ss * PXP;
-                int row = r0 + px / W;
-                T v = (T)0;
-                if (px < np && row >= 0 && row < H)
-                    v = Xb[(int64_t)(s0 + ss) * d.x_ss + (int64_t)r0 * W + px];
-                if constexpr (BF)
-                    ((bf16_t*)XZ)[px * 40 + ss] = v;
-                else
-                    ((float*)XZ)[ss * PXP + px] = v;
+                for (int j = 0; j < 8; j++)
+                    xv[j] = colok ? xr[(int64_t)(k + 8 * half + j) * d.x_ss] : (bf16_t)0;
+                bf16x8 av = lds8(UsL + (lane & 31) * LDA + k + 8 * half);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(xv), acc, 0, 0, 0);
             }
-            __syncthreads();
+        } else {
+            for (int k = 0; k < S; k += 16) {
+                float xv[8];
 #pragma unroll
-            for (int c = 0; c < CBW; c++) {
-                int cb = wave + c * NW;
-                if (cb < ncb) {
-                    if constexpr (BF) {
+                for (int u = 0; u < 8; u++)
+                    xv[u] = colok ? xr[(int64_t)(k + 2 * u + half) * d.x_ss] : 0.f;
 #pragma unroll
-                        for (int kk = 0; kk < 32; kk += 16) {
-                            bf16x8 bv = lds8((const bf16_t*)XZ + (cb * 32 + (lane & 31)) * 40 + kk + 8 * (lane >> 5));
-#pragma unroll
-                            for (int mb = 0; mb < 2; mb++)
-                                if (mb < nmb) {
-                                    bf16x8 av = lds8((const bf16_t*)UsL + (mb * 32 + (lane & 31)) * LDA + s0 + kk + 8 * (lane >> 5));
-                                    acc[c][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc[c][mb], 0, 0, 0);
-                                }
-                        }
-                    } else {
-#pragma unroll 4
-                        for (int kk = 0; kk < 32; kk += 2) {
-                            float bv = ((const float*)XZ)[(kk + (lane >> 5)) * PXP + cb * 32 + (lane & 31)];
-#pragma unroll
-                            for (int mb = 0; mb < 2; mb++)
-                                if (mb < nmb) {
-                                    float av = ((const float*)UsL)[(mb * 32 + (lane & 31)) * LDA + s0 + kk + (lane >> 5)];
-                                    acc[c][mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[c][mb], 0, 0, 0);
-                                }
-                        }
-                    }
+                for (int u = 0; u < 8; u++) {
+                    float av = UsL[(lane & 31) * LDA + k + 2 * u + half];
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, xv[u], acc, 0, 0, 0);
                 }
             }
-            __syncthreads();
         }
-#pragma unroll
-        for (int c = 0; c < CBW; c++) {
-            int cb = wave + c * NW;
-            int px = cb * 32 + (lane & 31);
-            if (cb < ncb && px < np) {
-                int row = r0 + px / W, w = px - (px / W) * W;
-                float* dst = ring + (size_t)slot(row) * R * W + w;
-#pragma unroll
-                for (int mb = 0; mb < 2; mb++)
-                    if (mb < nmb)
-#pragma unroll
-                        for (int i = 0; i < 16; i++) dst[(mb * 32 + row32(i, lane)) * W] = acc[c][mb][i];
-            }
-        }
+        return acc;
     };
 
-    // fill the ring with the KH-1 rows above the first chunk's lookahead
-    {
-        int pre = KH - 1;
-        for (int r0 = base_row; r0 < base_row + pre; r0 += TH) gemm1(r0, min(TH, base_row + pre - r0));
-    }
-    for (int h = h_begin; h < h_end; h += TH) {
-        const int nr = min(TH, h_end - h);
-        // rows entering the ring: [h + KH-1-ch, h + nr + KH-1-ch)
-        gemm1(h + (KH - 1 - ch), nr);
-        __syncthreads();
+    f32x16 ring[KH];
+#pragma unroll
+    for (int j = 0; j < KH - 1; j++) ring[j] = gemm1(h0 - CH + j);
+    for (int h = h0; h < h1; h++) {
+        // The tap and Ut tables are re-read from LDS every row: the offsets
+        // pass through an empty asm so the loads are not hoisted out of the
+        // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
+        uint32_t o_ut = d.o_ut, o_kh = d.o_kh, o_kw = d.o_kw;
+        asm volatile("" : "+s"(o_ut), "+s"(o_kh), "+s"(o_kw));
+        const T* UtP = (const T*)(smem + o_ut);
+        const float* KhP = (const float*)(smem + o_kh);
+        const float* KwP = (const float*)(smem + o_kw);
+        ring[KH - 1] = gemm1(h + KH - 1 - CH);
         // conv along h
-        for (int e = tid; e < nr * R * W; e += NW * 64) {
-            int row = e / (R * W), rem = e - row * R * W, r = rem / W, w = rem - r * W;
+        f32x16 z2;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
             float a = 0.f;
-            for (int j = 0; j < KH; j++)
-                a += ring[((size_t)slot(h + row + j - ch) * R + r) * W + w] * KhL[r * KH + j];
-            Z2[e] = a;
+#pragma unroll
+            for (int j = 0; j < KH; j++) a += KhP[(i * 2 + half) * KH + j] * ring[j][i];
+            z2[i] = a;
         }
-        __syncthreads();
-        // conv along w into the MFMA layout of Z3
-        const int np = nr * W;
-        for (int e = tid; e < R * PXP; e += NW * 64) {
-            int r = e / PXP, px = e - r * PXP;
+#pragma unroll
+        for (int j = 0; j < KH - 1; j++) ring[j] = ring[j + 1];
+        // conv along w: neighbouring columns are neighbouring lanes of the half
+        f32x16 z3;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
             float a = 0.f;
-            if (px < np) {
-                int row = px / W, w = px - row * W;
-                const float* z = Z2 + ((size_t)row * R + r) * W;
-                for (int j = 0; j < KW; j++) {
-                    int ww = w + j - cw;
-                    if (ww >= 0 && ww < W) a += z[ww] * KwL[r * KW + j];
+#pragma unroll
+            for (int jw = 0; jw < KW; jw++) {
+                int dd = jw - HWW;
+                float v;
+                if (dd == 0) {
+                    v = z2[i];
+                } else {
+                    int src = (lane & 31) + dd;
+                    src = src < 0 ? 0 : (src > 31 ? 31 : src);
+                    v = __shfl(z2[i], (lane & 32) | src, 64);
                 }
+                a += KwP[(i * 2 + half) * KW + jw] * v;
             }
-            if constexpr (BF)
-                ((bf16_t*)XZ)[px * LDU + r] = f32_to_bf16(a);
-            else
-                ((float*)XZ)[r * PXP + px] = a;
+            z3[i] = a;
         }
-        __syncthreads();
-        // GEMM2 and store
-        const int ncb = (np + 31) / 32;
+        // GEMM2: Y[t][col] = sum_r Ut[r][t] Z3[r][col]
+        f32x16 acc2[MB2];
 #pragma unroll
-        for (int c = 0; c < CBW; c++) {
-            int cb = wave + c * NW;
-            if (cb >= ncb) continue;
-            f32x16 acc[2];
+        for (int mb = 0; mb < MB2; mb++)
 #pragma unroll
-            for (int mb = 0; mb < 2; mb++)
+            for (int i = 0; i < 16; i++) acc2[mb][i] = 0.f;
+        if constexpr (BF) {
 #pragma unroll
-                for (int i = 0; i < 16; i++) acc[mb][i] = 0.f;
-            if constexpr (BF) {
-                for (int kk = 0; kk < R; kk += 16) {
-                    bf16x8 bv = lds8((const bf16_t*)XZ + (cb * 32 + (lane & 31)) * LDU + kk + 8 * (lane >> 5));
+            for (int q = 0; q < 2; q++) {
+                bf16_t zb[8];
 #pragma unroll
-                    for (int mb = 0; mb < 2; mb++)
-                        if (mb < nmb2) {
-                            bf16x8 av = lds8((const bf16_t*)UtL + (mb * 32 + (lane & 31)) * LDU + kk + 8 * (lane >> 5));
-                            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc[mb], 0, 0, 0);
-                        }
-                }
-            } else {
-#pragma unroll 4
-                for (int kk = 0; kk < R; kk += 2) {
-                    float bv = ((const float*)XZ)[(kk + (lane >> 5)) * PXP + cb * 32 + (lane & 31)];
+                for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(z3[8 * q + j]);
+                bf16x8 bv = pack8(zb);
 #pragma unroll
-                    for (int mb = 0; mb < 2; mb++)
-                        if (mb < nmb2) {
-                            float av = ((const float*)UtL)[(mb * 32 + (lane & 31)) * LDU + kk + (lane >> 5)];
-                            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[mb], 0, 0, 0);
-                        }
+                for (int mb = 0; mb < MB2; mb++) {
+                    bf16x8 av = lds8(UtP + (((q * 2 + half) * TT) + mb * 32 + (lane & 31)) * 8);
+                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc2[mb], 0, 0, 0);
                 }
             }
-            int px = cb * 32 + (lane & 31);
-            if (px < np) {
-                T* dst = Yb + (int64_t)h * W + px;
+        } else {
 #pragma unroll
-                for (int mb = 0; mb < 2; mb++)
-                    if (mb < nmb2)
+            for (int i = 0; i < 16; i++) {
 #pragma unroll
-                        for (int i = 0; i < 16; i++) store(dst, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc[mb][i]);
+                for (int mb = 0; mb < MB2; mb++) {
+                    float av = UtP[(i * 2 + half) * TT + mb * 32 + (lane & 31)];
+                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, z3[i], acc2[mb], 0, 0, 0);
+                }
             }
         }
-        __syncthreads();
+        if (store_lane) {
+            T* yr = Yc + (int64_t)h * W;
+#pragma unroll
+            for (int mb = 0; mb < MB2; mb++)
+#pragma unroll
+                for (int i = 0; i < 16; i++)
+                    store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
+        }
     }
+}
+
+template <typename T, int K, int MB2>
+hipError_t launch_cp_t(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
+    auto k = cp_fwd<T, K, K, MB2>;
+    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)ops[0],
+                       (const T*)ops[1], (const T*)ops[2], (const T*)ops[3], (const T*)ops[4], (T*)y);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
+    if (d.KH == 3 && d.KW == 3)
+        return d.T == 32 ? launch_cp_t<T, 3, 1>(d, ops, y, s) : launch_cp_t<T, 3, 2>(d, ops, y, s);
+    if (d.KH == 5 && d.KW == 5)
+        return d.T == 32 ? launch_cp_t<T, 5, 1>(d, ops, y, s) : launch_cp_t<T, 5, 2>(d, ops, y, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-
-
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s) {
     CpDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
+    if (d.R != 32 || !(d.T == 32 || d.T == 64)) return hipErrorInvalidValue;
     int bf = (ln.kind >> kBitIn) & 1;
-    dim3 g((uint32_t)d.blocks), bl(d.nthreads);
-    size_t lds = d.lds_bytes;
-    if (d.nthreads != 256) return hipErrorInvalidValue;
-    if (bf) {
-        auto k = cp_fwd<bf16_t, 4, 2>;
-        hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k, g, bl, lds, s, d, (const bf16_t*)ops[0], (const bf16_t*)ops[1],
-                           (const bf16_t*)ops[2], (const bf16_t*)ops[3], (const bf16_t*)ops[4], (bf16_t*)y);
-    } else {
-        auto k = cp_fwd<float, 4, 2>;
-        hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k, g, bl, lds, s, d, (const float*)ops[0], (const float*)ops[1],
-                           (const float*)ops[2], (const float*)ops[3], (const float*)ops[4], (float*)y);
-    }
-    return hipGetLastError();
+    return bf ? launch_cp_ty<bf16_t>(d, ops, y, s) : launch_cp_ty<float>(d, ops, y, s);
 }
 
 }  // namespace ce

@@ -318,27 +318,20 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     Buf Kh = resolve(ln.extra[0], c, 0, o4), Kw = resolve(ln.extra[1], c, 0, o5),
         Ut = resolve(ln.extra[2], c, 0, o6);
     REQ(o4 && o5 && o6, "unresolved buffer");
-    REQ((d.R == 32 || d.R == 64) && d.T % 32 == 0 && d.T <= 64 && d.S % 32 == 0, "sizes");
-    REQ(d.TH >= 1 && d.TH * d.W <= 256 && d.KH >= 1 && d.KH <= 7 && d.KW >= 1 && d.KW <= 7, "tile");
-    REQ(d.nthreads == 256 && ln.block[0] == 256, "block");
-    REQ((int64_t)ln.grid[0] == d.blocks && d.blocks == (int64_t)d.B * d.segs &&
-        (int64_t)d.segs * d.seg_rows >= d.H, "grid");
-    int e = bf ? 2 : 4;
-    int nr = d.TH + d.KH - 1, pxp = (d.TH * d.W + 31) / 32 * 32;
-    REQ(d.nr == nr && d.pxp == pxp, "layout dims");
-    REQ(d.lda >= d.S + (bf ? 8 : 1) && d.ldu >= d.R + (bf ? 8 : 1), "leading dims");
-    REQ(d.o_ut >= d.o_us + (uint64_t)d.R * d.lda * e && d.o_kh >= d.o_ut + (uint64_t)d.T * d.ldu * e &&
-        d.o_kw >= d.o_kh + (uint64_t)d.R * d.KH * 4 && d.o_ring >= d.o_kw + (uint64_t)d.R * d.KW * 4 &&
-        d.o_z2 >= d.o_ring + (uint64_t)nr * d.R * d.W * 4 && d.o_xz >= d.o_z2 + (uint64_t)d.TH * d.R * d.W * 4,
-        "LDS regions overlap");
-    uint64_t xs = bf ? (uint64_t)pxp * 40 * 2 : (uint64_t)32 * pxp * 4;
-    uint64_t z3 = bf ? (uint64_t)pxp * d.ldu * 2 : (uint64_t)d.R * pxp * 4;
-    REQ(d.lds_bytes >= d.o_xz + std::max(xs, z3) && d.lds_bytes <= 160 * 1024, "LDS size");
-    REQ(ln.lds == d.lds_bytes, "launch LDS");
-    // bf16 operands are read as 16-byte k-runs
-    REQ((d.o_us | d.o_ut | d.o_xz) % 16 == 0 &&
-        (!bf || ((d.lda * e) % 16 == 0 && (d.ldu * e) % 16 == 0 && d.S % 8 == 0 && d.R % 8 == 0)),
-        "alignment");
+    REQ(d.R == 32 && (d.T == 32 || d.T == 64) && d.S % 32 == 0, "sizes");
+    REQ(d.KH == d.KW && (d.KH == 3 || d.KH == 5), "filter size");
+    REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
+        (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
+    REQ((int64_t)d.segs * d.seg_rows >= d.H && (int64_t)(d.segs - 1) * d.seg_rows < d.H, "segments");
+    REQ(d.waves == (int64_t)d.B * d.ncb * d.segs && d.blocks * 4 >= d.waves &&
+        (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
+    // operand tables: UsL 32 x lda at 0, UtP at o_ut, tap tables at o_kh / o_kw
+    REQ(d.lda >= d.S + (bf ? 8 : 1) && (!bf || (d.lda * 2) % 16 == 0), "UsL rows");
+    REQ(d.o_ut >= (uint64_t)32 * d.lda * (bf ? 2 : 4) && d.o_ut % 16 == 0, "UtP offset");
+    REQ(d.o_kh >= d.o_ut + (bf ? (uint64_t)2 * 2 * d.T * 8 * 2 : (uint64_t)16 * 2 * d.T * 4), "Kh offset");
+    REQ(d.o_kw >= d.o_kh + (uint64_t)16 * 2 * d.KH * 4, "Kw offset");
+    REQ(d.lds_bytes >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4 && d.lds_bytes <= 64 * 1024 &&
+        ln.lds == d.lds_bytes, "LDS size");
     const int H = d.H, W = d.W, R = d.R, ch = (d.KH - 1) / 2, cw = (d.KW - 1) / 2;
     std::vector<double> z1((size_t)R * H * W), z2((size_t)R * H * W), z3v((size_t)R * H * W);
     bool ok = true;
