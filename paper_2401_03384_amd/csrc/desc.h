@@ -47,6 +47,7 @@ enum KernelKind : int32_t {
     K_DW_TAPGRAD = 20,      // per-block partial filter-tap gradients (DwDesc)
     K_DW_TAPREDUCE = 21,    // ordered sum of tap partials (DwDesc)
     K_CP_FWD = 22,          // fused CP chain forward (CpDesc)
+    K_CP_BWD = 23,          // fused CP chain backward (CpBwdDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -120,6 +121,26 @@ struct CpDesc {
     // permuted Ut operands at o_ut, the permuted taps at o_kh / o_kw
     uint32_t lds_bytes, o_ut, o_kh, o_kw;
     int32_t lda;
+};
+
+// Backward of the same chain.  Strips and segments as in CpDesc (dX has X's
+// layout, dY has Y's).  Every block writes its partial factor gradients
+// (summed over its four wavefronts in a fixed order) to row blockIdx of
+// Pus[blocks][R][S], Put[blocks][R][T], Pkh[blocks][R][KH], Pkw[blocks][R][KW].
+// LDS: UsA [32][lda_s] at 0, UtA [32][lda_t] at o_uta, the permuted Us of the
+// dX product at o_usp, permuted taps at o_kh / o_kw, four wave-private
+// [32][33] fp32 transpose tiles at o_zt and four wave-private tap-product
+// areas of 64 * 16 * (KH + KW) floats at o_tap; the end-of-block reduction
+// reuses the first red_bytes.
+struct CpBwdDesc {
+    int32_t B, S, R, T, H, W, KH, KW;
+    int32_t ncb, colstride, segs, seg_rows;
+    int64_t x_sb, x_ss, y_sb, y_st;
+    int64_t us_sr, us_ss, ut_sr, ut_st;
+    int64_t kh_sr, kh_sj, kw_sr, kw_sj;
+    int64_t waves, blocks;
+    uint32_t lds_bytes, o_uta, o_usp, o_kh, o_kw, o_zt, o_tap, red_bytes;
+    int32_t lda_s, lda_t;
 };
 
 }  // namespace ce

@@ -136,6 +136,130 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     return true;
 }
 
+
+// LDS of the fused backward (see CpBwdDesc).
+void cp_bwd_tables(CpBwdDesc& d, bool bf) {
+    const size_t e = bf ? 2 : 4;
+    d.lda_s = bf ? d.S + 8 : d.S + 1;
+    d.lda_t = bf ? d.T + 8 : d.T + 1;
+    size_t o = al16((size_t)32 * d.lda_s * e);
+    d.o_uta = (uint32_t)o;
+    o = al16(o + (size_t)32 * d.lda_t * e);
+    d.o_usp = (uint32_t)o;
+    o = al16(o + (bf ? (size_t)2 * 2 * d.S * 8 * 2 : (size_t)16 * 2 * d.S * 4));
+    d.o_kh = (uint32_t)o;
+    o += (size_t)16 * 2 * d.KH * 4;
+    d.o_kw = (uint32_t)o;
+    o += (size_t)16 * 2 * d.KW * 4;
+    o = al16(o);
+    d.o_zt = (uint32_t)o;
+    o += (size_t)4 * 32 * 33 * 4;
+    d.o_tap = (uint32_t)o;
+    o += (size_t)4 * 64 * 16 * (d.KH + d.KW) * 4;
+    d.red_bytes = (uint32_t)((size_t)4 * 4 * 32 * std::max({d.S, d.T, d.KH + d.KW}));
+    d.lds_bytes = (uint32_t)std::max<size_t>(al16(o), d.red_bytes);
+}
+
+void reduce_launch(BufRef part, BufRef out, int64_t M, int64_t N, int64_t nsplit, int64_t sCm,
+                   int64_t sCn, uint32_t need, const std::string& what, std::vector<Launch>& v) {
+    ReduceDesc rd;
+    std::memset(&rd, 0, sizeof(rd));
+    rd.M = (int32_t)M;
+    rd.N = (int32_t)N;
+    rd.nsplit = nsplit;
+    rd.sCm = sCm;
+    rd.sCn = sCn;
+    Launch lr;
+    lr.kind = K_REDUCE;   // fp32 partials into an fp32 gradient
+    lr.d = part;
+    lr.c = out;
+    lr.grid[0] = (uint32_t)((M * N + 63) / 64);
+    lr.block[0] = 256;
+    lr.desc.resize(sizeof(rd));
+    std::memcpy(lr.desc.data(), &rd, sizeof(rd));
+    lr.need = need;
+    lr.what = what;
+    lr.kname = "reduce_partials<float>";
+    lr.alg_bytes = 4.0 * (double)(nsplit * M * N + M * N);
+    v.push_back(lr);
+}
+
+}  // namespace
+
+bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratch,
+                      std::vector<Launch>& out) {
+    if ((f.kind & 0xff) != K_CP_FWD || f.extra.size() != 3) return false;
+    if (f.a.kind != BUF_IN || f.b.kind != BUF_IN || f.c.kind != BUF_OUT) return false;
+    for (const BufRef& x : f.extra)
+        if (x.kind != BUF_IN) return false;
+    if (f.a.index != feature_operand) return false;   // dX is in the input type
+    const CpDesc c = desc<CpDesc>(f);
+    // 3x3 filters and S = T in {32, 64} (the kernel's register budget)
+    if (c.KH != 3 || c.KW != 3 || c.S != c.T || !(c.T == 32 || c.T == 64) || c.R != 32) return false;
+    const int dt = dtin(f);
+    CpBwdDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.B = c.B; d.S = c.S; d.R = c.R; d.T = c.T; d.H = c.H; d.W = c.W; d.KH = c.KH; d.KW = c.KW;
+    d.ncb = c.ncb;
+    d.colstride = c.colstride;
+    d.x_sb = c.x_sb; d.x_ss = c.x_ss; d.y_sb = c.y_sb; d.y_st = c.y_st;
+    d.us_sr = c.us_sr; d.us_ss = c.us_ss; d.ut_sr = c.ut_sr; d.ut_st = c.ut_st;
+    d.kh_sr = c.kh_sr; d.kh_sj = c.kh_sj; d.kw_sr = c.kw_sr; d.kw_sj = c.kw_sj;
+    // one wavefront per SIMD (1024 on the chip); each segment recomputes
+    // 2*CH rows of the chain above and below it
+    const int64_t want = 1024;
+    const int64_t strips = (int64_t)d.B * d.ncb;
+    const int64_t segs = std::max<int64_t>(1, std::min<int64_t>(d.H, want / std::max<int64_t>(1, strips)));
+    d.seg_rows = (int32_t)((d.H + segs - 1) / segs);
+    d.segs = (int32_t)((d.H + d.seg_rows - 1) / d.seg_rows);
+    d.waves = strips * d.segs;
+    d.blocks = (d.waves + 3) / 4;
+    if (d.blocks > 0x7fffffff) return false;
+    cp_bwd_tables(d, dt == 1);
+    if (d.lds_bytes > 160 * 1024) return false;
+
+    const int64_t R = d.R, nb = d.blocks;
+    const BufRef Pus = scratch.alloc((size_t)(nb * R * d.S) * 4);
+    const BufRef Put = scratch.alloc((size_t)(nb * R * d.T) * 4);
+    const BufRef Pkh = scratch.alloc((size_t)(nb * R * d.KH) * 4);
+    const BufRef Pkw = scratch.alloc((size_t)(nb * R * d.KW) * 4);
+    const BufRef us = f.b, kh = f.extra[0], kw = f.extra[1], ut = f.extra[2];
+    auto din = [](const BufRef& in) {
+        BufRef g;
+        g.kind = BUF_DIN;
+        g.index = in.index;
+        return g;
+    };
+    Launch m;
+    m.kind = K_CP_BWD | (dt << kBitIn) | (dt << kBitAux) | (dt << kBitOut);
+    m.a = f.a;                      // X
+    m.b.kind = BUF_DOUT;            // dY
+    m.c = din(f.a);                 // dX (NULL when not wanted)
+    m.extra = {us, kh, kw, ut, Pus, Put, Pkh, Pkw};
+    m.grid[0] = (uint32_t)d.blocks;
+    m.block[0] = 256;
+    m.lds = d.lds_bytes;
+    m.desc.resize(sizeof(d));
+    std::memcpy(m.desc.data(), &d, sizeof(d));
+    m.need = (1u << f.a.index) | (1u << us.index) | (1u << kh.index) | (1u << kw.index) | (1u << ut.index);
+    m.what = "fused CP chain backward";
+    m.kname = std::string("cp_bwd<") + (dt ? "unsigned short" : "float") + ", 3, 3, " +
+              std::to_string(d.T / 32) + ", " + std::to_string(d.S / 32) + ">";
+    // algorithmic bytes: X and dY read, dX written, factors read, partials written
+    const double e = dt ? 2 : 4;
+    const double act = (double)d.B * d.S * d.H * d.W;   // S = T
+    m.alg_bytes = e * 3 * act + e * (double)R * (d.S + d.T + d.KH + d.KW) +
+                  4.0 * (double)nb * R * (d.S + d.T + d.KH + d.KW);
+    m.alg_flops = 2.0 * f.alg_flops;   // backward MACs are twice the forward's
+    out.push_back(m);
+    reduce_launch(Pus, din(us), R, d.S, nb, c.us_sr, c.us_ss, 1u << us.index, "dUs: sum of block partials", out);
+    reduce_launch(Put, din(ut), R, d.T, nb, c.ut_sr, c.ut_st, 1u << ut.index, "dUt: sum of block partials", out);
+    reduce_launch(Pkh, din(kh), R, d.KH, nb, c.kh_sr, c.kh_sj, 1u << kh.index, "dKh: sum of block partials", out);
+    reduce_launch(Pkw, din(kw), R, d.KW, nb, c.kw_sr, c.kw_sj, 1u << kw.index, "dKw: sum of block partials", out);
+    return true;
+}
+
+namespace {
 }  // namespace
 
 int fuse_launches(std::vector<Launch>& v, bool backward) {

@@ -17,4 +17,8 @@ hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, 
 // Fused CP chain forward: ops = {X, Us, Kh, Kw, Ut}.
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
 
+// Fused CP chain backward: ops = {X, dY, dX (may be NULL), Us, Kh, Kw, Ut,
+// Pus, Put, Pkh, Pkw}.
+hipError_t launch_cp_bwd(const Launch& ln, const void* const* ops, hipStream_t s);
+
 }  // namespace ce

@@ -339,6 +339,22 @@ size_t pack(std::vector<WsItem>& items) {
     return total;
 }
 
+// Workspace items no launch refers to (intermediates a fused launch keeps
+// on chip) take no space.
+void drop_unused(std::vector<WsItem>& items, const std::vector<Launch>& v) {
+    std::vector<int> used;
+    for (const Launch& ln : v) {
+        for (const BufRef* b : {&ln.a, &ln.b, &ln.c, &ln.d})
+            if (b->kind == BUF_WS) used.push_back(b->index);
+        for (const BufRef& b : ln.extra)
+            if (b.kind == BUF_WS) used.push_back(b.index);
+    }
+    std::vector<WsItem> kept;
+    for (const WsItem& it : items)
+        if (std::find(used.begin(), used.end(), it.id) != used.end()) kept.push_back(it);
+    items.swap(kept);
+}
+
 }  // namespace
 
 // ---- generic lowering ----------------------------------------------------
@@ -624,6 +640,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
         if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) fuse_launches(p->fwd, false);
+        drop_unused(items, p->fwd);
         p->ws_fwd = pack(items);
         patch(p->fwd, items);
 
@@ -721,6 +738,20 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
             }
         }
+        // A plan that is exactly one fused CP chain gets the fused backward.
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) && p->fwd.size() == 1 &&
+            (p->fwd[0].kind & 0xff) == K_CP_FWD) {
+            std::vector<WsItem> fitems;
+            ItemScratch fsc;
+            fsc.items = &fitems;
+            fsc.next = SCRATCH_ID;
+            std::vector<Launch> v;
+            if (fuse_cp_backward(p->fwd[0], E.feature_operand, fsc, v)) {
+                p->bwd.swap(v);
+                bitems.swap(fitems);
+            }
+        }
+        drop_unused(bitems, p->bwd);
         p->ws_bwd = pack(bitems);
         patch(p->bwd, bitems);
     }

@@ -120,6 +120,13 @@ Launch lower_generic(const PairOp& op);
 // fused launch.  Returns the number of fusions done.
 int fuse_launches(std::vector<Launch>& v, bool backward);
 
+// Backward of a plan whose whole forward is one fused CP chain launch `f`:
+// one fused gradient launch plus ordered reductions of its partial factor
+// gradients (scratch from `scratch`).  False when the chain's sizes are not
+// covered by the fused backward kernel.
+bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratch,
+                      std::vector<Launch>& out);
+
 // Lowering of one pairwise op to launches: a specialised kernel when the
 // op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,

@@ -379,6 +379,124 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     return true;
 }
 
+
+// Fused CP backward: every gradient of the chain in double; dX written (when
+// wanted), the factor-gradient totals put in block 0 of the partials and
+// zeros in every other block (the reduce launches then sum them).
+bool run_cp_bwd(const Launch& ln, Ctx& c) {
+    CpBwdDesc d = desc_of<CpBwdDesc>(ln);
+    int bf = (ln.kind >> kBitIn) & 1;
+    REQ(ln.extra.size() == 8, "operand count");
+    bool ok1, ok2, ok3;
+    Buf X = resolve(ln.a, c, 0, ok1), dY = resolve(ln.b, c, 0, ok2), dX = resolve(ln.c, c, 0, ok3);
+    REQ(ok1 && ok2 && ok3, "unresolved buffer");
+    Buf F[8];
+    for (int i = 0; i < 8; i++) {
+        bool o;
+        F[i] = resolve(ln.extra[i], c, 0, o);
+        REQ(o, "unresolved buffer");
+    }
+    Buf &Us = F[0], &Kh = F[1], &Kw = F[2], &Ut = F[3], &Pus = F[4], &Put = F[5], &Pkh = F[6], &Pkw = F[7];
+    REQ(d.R == 32 && d.S == d.T && (d.T == 32 || d.T == 64) && d.KH == 3 && d.KW == 3, "sizes");
+    REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
+        (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
+    REQ((int64_t)d.segs * d.seg_rows >= d.H && (int64_t)(d.segs - 1) * d.seg_rows < d.H, "segments");
+    REQ(d.waves == (int64_t)d.B * d.ncb * d.segs && d.blocks * 4 >= d.waves && d.blocks * 4 < d.waves + 4 &&
+        (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
+    // LDS: tables, transpose tiles, tap areas, reduction area
+    const uint64_t e = bf ? 2 : 4;
+    REQ(d.lda_s >= d.S + (bf ? 8 : 1) && d.lda_t >= d.T + (bf ? 8 : 1) &&
+        (!bf || ((d.lda_s * 2) % 16 == 0 && (d.lda_t * 2) % 16 == 0)), "table rows");
+    REQ(d.o_uta >= 32 * d.lda_s * e && d.o_uta % 16 == 0, "UtA offset");
+    REQ(d.o_usp >= d.o_uta + 32 * d.lda_t * e && d.o_usp % 16 == 0, "UsP offset");
+    REQ(d.o_kh >= d.o_usp + (bf ? (uint64_t)2 * 2 * d.S * 8 * 2 : (uint64_t)16 * 2 * d.S * 4), "Kh offset");
+    REQ(d.o_kw >= d.o_kh + (uint64_t)16 * 2 * d.KH * 4, "Kw offset");
+    REQ(d.o_zt >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4 && d.o_zt % 16 == 0, "tile offset");
+    REQ(d.o_tap >= d.o_zt + (uint64_t)4 * 32 * 33 * 4 && d.o_tap % 16 == 0, "tap offset");
+    REQ(d.lds_bytes >= d.o_tap + (uint64_t)4 * 64 * 16 * (d.KH + d.KW) * 4, "tap area");
+    REQ(d.red_bytes >= (uint64_t)4 * 4 * 32 * std::max({d.S, d.T, d.KH + d.KW}) &&
+        d.lds_bytes >= d.red_bytes && d.lds_bytes <= 160 * 1024 && ln.lds == d.lds_bytes, "LDS size");
+    const int B = d.B, S = d.S, R = d.R, T = d.T, H = d.H, W = d.W, K = d.KH, c3 = (K - 1) / 2;
+    const size_t HW = (size_t)H * W;
+    bool ok = true;
+    std::vector<double> gus((size_t)R * S, 0), gut((size_t)R * T, 0), gkh((size_t)R * K, 0),
+        gkw((size_t)R * K, 0);
+    std::vector<double> z1(R * HW), z2(R * HW), z3(R * HW), g3(R * HW), g2(R * HW), g1(R * HW);
+    auto us = [&](int r, int s2) { return (double)ld(Us, bf, (int64_t)r * d.us_sr + (int64_t)s2 * d.us_ss, ok); };
+    auto ut = [&](int r, int t) { return (double)ld(Ut, bf, (int64_t)r * d.ut_sr + (int64_t)t * d.ut_st, ok); };
+    auto kh = [&](int r, int j) { return (double)ld(Kh, bf, (int64_t)r * d.kh_sr + (int64_t)j * d.kh_sj, ok); };
+    auto kw = [&](int r, int j) { return (double)ld(Kw, bf, (int64_t)r * d.kw_sr + (int64_t)j * d.kw_sj, ok); };
+    for (int b = 0; b < B; b++) {
+        for (int r = 0; r < R; r++)
+            for (size_t p = 0; p < HW; p++) {
+                double a = 0, g = 0;
+                for (int s2 = 0; s2 < S; s2++) a += us(r, s2) * ld(X, bf, (int64_t)b * d.x_sb + (int64_t)s2 * d.x_ss + p, ok);
+                for (int t = 0; t < T; t++) g += ut(r, t) * ld(dY, bf, (int64_t)b * d.y_sb + (int64_t)t * d.y_st + p, ok);
+                z1[r * HW + p] = a;
+                g3[r * HW + p] = g;
+            }
+        for (int r = 0; r < R; r++)
+            for (int h = 0; h < H; h++)
+                for (int w = 0; w < W; w++) {
+                    double a = 0;
+                    for (int j = 0; j < K; j++) {
+                        int hh = h + j - c3;
+                        if (hh >= 0 && hh < H) a += kh(r, j) * z1[r * HW + hh * W + w];
+                    }
+                    z2[r * HW + h * W + w] = a;
+                }
+        for (int r = 0; r < R; r++)
+            for (int h = 0; h < H; h++)
+                for (int w = 0; w < W; w++) {
+                    double a = 0, g = 0;
+                    for (int j = 0; j < K; j++) {
+                        int ww = w + j - c3;
+                        if (ww >= 0 && ww < W) a += kw(r, j) * z2[r * HW + h * W + ww];
+                        int wg = w - j + c3;   // transposed conv along w
+                        if (wg >= 0 && wg < W) g += kw(r, j) * g3[r * HW + h * W + wg];
+                    }
+                    z3[r * HW + h * W + w] = a;
+                    g2[r * HW + h * W + w] = g;
+                }
+        for (int r = 0; r < R; r++)
+            for (int h = 0; h < H; h++)
+                for (int w = 0; w < W; w++) {
+                    double g = 0;
+                    for (int j = 0; j < K; j++) {
+                        int hg = h - j + c3;
+                        if (hg >= 0 && hg < H) g += kh(r, j) * g2[r * HW + hg * W + w];
+                        int hh = h + j - c3, ww = w + j - c3;
+                        if (hh >= 0 && hh < H) gkh[r * K + j] += z1[r * HW + hh * W + w] * g2[r * HW + h * W + w];
+                        if (ww >= 0 && ww < W) gkw[r * K + j] += z2[r * HW + h * W + ww] * g3[r * HW + h * W + w];
+                    }
+                    g1[r * HW + h * W + w] = g;
+                }
+        for (size_t p = 0; p < HW; p++) {
+            for (int t = 0; t < T; t++) {
+                double dy = ld(dY, bf, (int64_t)b * d.y_sb + (int64_t)t * d.y_st + p, ok);
+                for (int r = 0; r < R; r++) gut[r * T + t] += z3[r * HW + p] * dy;
+            }
+            for (int s2 = 0; s2 < S; s2++) {
+                double x = ld(X, bf, (int64_t)b * d.x_sb + (int64_t)s2 * d.x_ss + p, ok);
+                double a = 0;
+                for (int r = 0; r < R; r++) {
+                    a += us(r, s2) * g1[r * HW + p];
+                    gus[r * S + s2] += g1[r * HW + p] * x;
+                }
+                if (dX.base) st(dX, bf, (int64_t)b * d.x_sb + (int64_t)s2 * d.x_ss + p, (float)a, ok);
+            }
+        }
+        REQ(ok, "out-of-bounds access (cp_bwd)");
+    }
+    for (int64_t blk = 0; blk < d.blocks; blk++) {
+        for (int i = 0; i < R * S; i++) st(Pus, 0, blk * R * S + i, blk ? 0.f : (float)gus[i], ok);
+        for (int i = 0; i < R * T; i++) st(Put, 0, blk * R * T + i, blk ? 0.f : (float)gut[i], ok);
+        for (int i = 0; i < R * K; i++) st(Pkh, 0, blk * R * K + i, blk ? 0.f : (float)gkh[i], ok);
+        for (int i = 0; i < R * K; i++) st(Pkw, 0, blk * R * K + i, blk ? 0.f : (float)gkw[i], ok);
+    }
+    REQ(ok, "out-of-bounds partials (cp_bwd)");
+    return true;
+}
 }  // namespace
 
 extern "C" {
@@ -427,6 +545,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_DW_TAPGRAD ? run_tapgrad(ln, c)
                     : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
                     : v == K_CP_FWD ? run_cp_fwd(ln, c)
+                    : v == K_CP_BWD ? run_cp_bwd(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
         }

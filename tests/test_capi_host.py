@@ -164,11 +164,26 @@ def test_user_path_and_left_to_right():
 
 def test_workspace_covers_live_intermediates():
     w = W.WORKLOADS["C2"]
-    p = _plan(w.spec, w.shapes)
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    p = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, B.CE_FLAG_NO_FUSION)
+    B.ce_expr_destroy(e)
     fwd, bwd = B.ce_plan_workspace_size(p, 0), B.ce_plan_workspace_size(p, 1)
     inter = 128 * 32 * 56 * 56 * 4
     assert fwd >= 2 * inter          # two intermediates are live at once
     assert bwd >= 3 * inter          # three recomputed values, plus gradients
+    B.ce_plan_destroy(p)
+
+
+def test_fused_chain_keeps_intermediates_on_chip():
+    """The fused CP chain needs no intermediate in HBM: the forward takes no
+    workspace, the backward only the per-block factor-gradient partials."""
+    w = W.WORKLOADS["C2"]
+    p = _plan(w.spec, w.shapes)
+    assert "fused CP chain backward" in B.ce_plan_describe(p)
+    fwd, bwd = B.ce_plan_workspace_size(p, 0), B.ce_plan_workspace_size(p, 1)
+    assert fwd == 0
+    inter = 128 * 32 * 56 * 56 * 4
+    assert 0 < bwd < inter // 4
     B.ce_plan_destroy(p)
 
 
@@ -218,9 +233,12 @@ def test_execution_errors_before_any_device_call():
     din = (C.c_void_p * 2)(None, None)
     assert L.ce_backward(p, ins, None, din, None, 0, None) == B.CE_ERR_ARG
     B.ce_plan_destroy(p)
-    # a plan with intermediates: workspace too small / misaligned
+    # a plan with intermediates (unfused): workspace too small / misaligned
     w = W.PARITY_WORKLOADS["C2s"]
-    p = _plan(w.spec, w.shapes)
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    p = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, B.CE_FLAG_NO_FUSION)
+    B.ce_expr_destroy(e)
+    assert B.ce_plan_workspace_size(p, 0) > 0
     ins5 = (C.c_void_p * 5)(*([fake] * 5))
     need = B.ce_plan_workspace_size(p, 0)
     assert L.ce_forward(p, ins5, fake, fake, need - 1, None) == B.CE_ERR_WORKSPACE

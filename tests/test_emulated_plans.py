@@ -79,6 +79,9 @@ CASES = {
     "C1": W.PARITY_WORKLOADS["C1"],
     "C2s": W.PARITY_WORKLOADS["C2s"],
     "C2s_bf16": W.PARITY_WORKLOADS["C2s_bf16"],
+    "C2r32": W.cp_layer("C2r32t", 2, 32, 32, 5, 37, 32, 3, "f32", 17),
+    "C2r32_bf16": W.cp_layer("C2r32t_bf16", 2, 32, 32, 5, 37, 32, 3, "bf16", 17),
+    "C2k5": W.cp_layer("C2k5t", 1, 32, 32, 6, 29, 32, 5, "f32", 18),
     "C3t": W.tucker2_layer("C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21),
     "C3t_f32": W.tucker2_layer("C3t_f32", 2, 32, 24, 7, 9, 8, 16, 3, "f32", 21),
     "C4t": W.rtt_layer("C4t", 1, (2, 4, 2), (2, 2, 4), 7, 6, 4, 3, "f32", 22),

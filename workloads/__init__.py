@@ -111,6 +111,9 @@ PARITY_WORKLOADS = {
     "C1": WORKLOADS["C1"],
     "C2s": cp_layer("C2s", 2, 64, 64, 19, 19, 32, 3, "f32", 12),
     "C2s_bf16": cp_layer("C2s_bf16", 2, 64, 64, 19, 19, 32, 3, "bf16", 12),
+    "C2r32": cp_layer("C2r32", 3, 32, 32, 13, 37, 32, 3, "f32", 17),
+    "C2r32_bf16": cp_layer("C2r32_bf16", 3, 32, 32, 13, 37, 32, 3, "bf16", 17),
+    "C2k5": cp_layer("C2k5", 2, 64, 32, 12, 29, 32, 5, "f32", 18),
     "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
     "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
     "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
