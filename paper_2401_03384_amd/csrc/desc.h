@@ -127,11 +127,10 @@ struct CpDesc {
 // layout, dY has Y's).  Every block writes its partial factor gradients
 // (summed over its four wavefronts in a fixed order) to row blockIdx of
 // Pus[blocks][R][S], Put[blocks][R][T], Pkh[blocks][R][KH], Pkw[blocks][R][KW].
-// LDS: UsA [32][lda_s] at 0, UtA [32][lda_t] at o_uta, the permuted Us of the
-// dX product at o_usp, permuted taps at o_kh / o_kw, four wave-private
-// [32][33] fp32 transpose tiles at o_zt and four wave-private tap-product
-// areas of 64 * 16 * (KH + KW) floats at o_tap; the end-of-block reduction
-// reuses the first red_bytes.
+// LDS: UsA [32][lda_s] at 0, UtA [32][lda_t] at o_uta, for bf16 UsT [S][ldu]
+// (Us transposed) at o_ust, four wave-private fp32 [32][33] tiles at o_tz and
+// four wave-private [T][ly] tiles of yt_bytes each at o_yt; the end-of-block
+// reduction reuses the first red_bytes.
 struct CpBwdDesc {
     int32_t B, S, R, T, H, W, KH, KW;
     int32_t ncb, colstride, segs, seg_rows;
@@ -139,8 +138,8 @@ struct CpBwdDesc {
     int64_t us_sr, us_ss, ut_sr, ut_st;
     int64_t kh_sr, kh_sj, kw_sr, kw_sj;
     int64_t waves, blocks;
-    uint32_t lds_bytes, o_uta, o_usp, o_kh, o_kw, o_zt, o_tap, red_bytes;
-    int32_t lda_s, lda_t;
+    uint32_t lds_bytes, o_uta, o_ust, o_tz, o_yt, yt_bytes, red_bytes;
+    int32_t lda_s, lda_t, ldu, ly;
 };
 
 }  // namespace ce

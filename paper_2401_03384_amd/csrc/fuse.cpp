@@ -142,21 +142,20 @@ void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     const size_t e = bf ? 2 : 4;
     d.lda_s = bf ? d.S + 8 : d.S + 1;
     d.lda_t = bf ? d.T + 8 : d.T + 1;
+    d.ldu = bf ? 32 + 8 : 0;
+    d.ly = bf ? 40 : 33;
     size_t o = al16((size_t)32 * d.lda_s * e);
     d.o_uta = (uint32_t)o;
     o = al16(o + (size_t)32 * d.lda_t * e);
-    d.o_usp = (uint32_t)o;
-    o = al16(o + (bf ? (size_t)2 * 2 * d.S * 8 * 2 : (size_t)16 * 2 * d.S * 4));
-    d.o_kh = (uint32_t)o;
-    o += (size_t)16 * 2 * d.KH * 4;
-    d.o_kw = (uint32_t)o;
-    o += (size_t)16 * 2 * d.KW * 4;
-    o = al16(o);
-    d.o_zt = (uint32_t)o;
+    d.o_ust = (uint32_t)o;
+    if (bf) o = al16(o + (size_t)d.S * d.ldu * 2);
+    d.o_tz = (uint32_t)o;
     o += (size_t)4 * 32 * 33 * 4;
-    d.o_tap = (uint32_t)o;
-    o += (size_t)4 * 64 * 16 * (d.KH + d.KW) * 4;
-    d.red_bytes = (uint32_t)((size_t)4 * 4 * 32 * std::max({d.S, d.T, d.KH + d.KW}));
+    d.o_yt = (uint32_t)o;
+    d.yt_bytes = (uint32_t)al16((size_t)d.T * d.ly * e);
+    o += (size_t)4 * d.yt_bytes;
+    d.red_bytes = (uint32_t)(4 * std::max<size_t>({(size_t)4 * 32 * d.S, (size_t)4 * 32 * d.T,
+                                                   (size_t)8 * 32 * (d.KH + d.KW)}));
     d.lds_bytes = (uint32_t)std::max<size_t>(al16(o), d.red_bytes);
 }
 
@@ -197,6 +196,11 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
     // 3x3 filters and S = T in {32, 64} (the kernel's register budget)
     if (c.KH != 3 || c.KW != 3 || c.S != c.T || !(c.T == 32 || c.T == 64) || c.R != 32) return false;
     const int dt = dtin(f);
+    // one sample of X, dY and dX is addressed with 31-bit byte offsets
+    const int64_t e_in = dt ? 2 : 4;
+    if ((int64_t)c.S * c.x_ss * e_in >= (1ll << 31) || (int64_t)c.T * c.y_st * e_in >= (1ll << 31) ||
+        c.x_ss != (int64_t)c.H * c.W || c.y_st != (int64_t)c.H * c.W)
+        return false;
     CpBwdDesc d;
     std::memset(&d, 0, sizeof(d));
     d.B = c.B; d.S = c.S; d.R = c.R; d.T = c.T; d.H = c.H; d.W = c.W; d.KH = c.KH; d.KW = c.KW;

@@ -43,6 +43,16 @@ __device__ __forceinline__ bf16x8 pack8(const bf16_t* v) {
     return r;
 }
 
+// Twenty wait states after an MFMA chain whose result VALU code reads next.
+// The compiler's hazard padding has been seen to miss the read of a 16-pass
+// MFMA result on a branch path that skips straight to it; this pads on every
+// path, before any branch (about 1% of a row's MFMA time).
+__device__ __forceinline__ void mfma_drain() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // r held by accumulator i of a lane in a 32x32 MFMA result
 __device__ __forceinline__ int row32(int i, int lane) {
     return 8 * (i >> 2) + 4 * ((lane >> 5) & 1) + (i & 3);
@@ -139,6 +149,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
                 }
             }
         }
+        mfma_drain();
         return acc;
     };
 
@@ -215,6 +226,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
                 }
             }
         }
+        mfma_drain();
         if (store_lane) {
             T* yr = Yc + (int64_t)h * W;
 #pragma unroll
@@ -247,53 +259,122 @@ hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStr
 // ---------------------------------------------------------------------------
 // Backward of the chain (Section 3.2: every pairwise step's two gradients, in
 // reverse order, with the intermediates recomputed), fused the same way.  One
-// wavefront walks its strip over rows h = h0-CH .. h1+CH-1 and at row h
+// wavefront walks its 32-column strip over rows h = h0-CH .. h1+CH-1 and at row h
 //   recomputes  Z1[h+CH] (ring of KH rows), Z2[h], Z3[h]
-//   dZ3[h] = Ut^T dY[h]                  row GEMM over t
-//   dUt   += Z3[h] dY[h]^T               MFMA over the strip's columns
+//   dZ3[h] = Ut^T dY[h]
+//   dUt   += Z3[h] dY[h]^T               (reduction over the strip's columns)
 //   dKw   += sum_w Z2[h][w+j-c] dZ3[h][w]
-//   dZ2[h] = transposed conv along w of dZ3[h] (lane permutes)
+//   dZ2[h] = transposed conv along w of dZ3[h]
 //   dKh   += sum_w Z1[h+j-c][w] dZ2[h][w]
 //   dZ1[h-CH] from the ring of the last KH dZ2 rows
-//   dX[h-CH] = Us^T dZ1[h-CH]            (accumulator-layout product)
-//   dUs   += dZ1[h-CH] X[h-CH]^T         MFMA over the strip's columns
-// Every weight-gradient term is counted once: rows in [h0, h1) and the
-// strip's own columns only.  The column reductions of dUt / dUs need the
-// columns on the MFMA k axis: Z3 / dZ1 go through a wave-private LDS tile
-// ([col][r]) and dY / X are read channel-major straight from memory.  The tap
-// products are summed over the 32 lanes of each half by recursive halving.
+//   dX[h-CH] = Us^T dZ1[h-CH]
+//   dUs   += dZ1[h-CH] X[h-CH]^T
+// Each weight-gradient term is counted once: rows in [h0, h1) and the strip's
+// own columns only.
+//
+// The rank intermediates are held transposed: the MFMA computes Z^T[col][r]
+// (A operand = the activation row, one column per lane; B operand = the factor
+// table in LDS), so a lane holds one rank r (lane % 32) and the 16 columns
+// tcol(i, half) of its accumulators.  Then
+//   * conv along h is per element, conv along w a shift of the register index
+//     (four cross-half exchanges per shift);
+//   * the column reductions of dUt / dUs take Z^T straight from the
+//     accumulators as the MFMA A operand (k slot = column);
+//   * the tap-gradient products reduce over columns inside the lane;
+//   * dX goes through one LDS transpose of dZ1 (and is stored coalesced).
+// dY reaches the dUt product through a wave-private LDS tile; the X row of the
+// dUs product is read channel-major from memory (it was read two rows earlier
+// by the same wavefront).  The operands of the next row are loaded while the
+// current row is computed.
 
-template <int K>
-__device__ __forceinline__ float swz_xor(float v) {
-    // ds_swizzle bit-mask mode: lane i of each 32-lane group reads lane i ^ K
-    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1f | (K << 10)));
-}
+// column held by accumulator i of a lane in half hf of a transposed tile
+__device__ __forceinline__ int tcol(int i, int hf) { return 8 * (i >> 2) + 4 * hf + (i & 3); }
 
-template <int K>
-__device__ __forceinline__ void halve(float (&v)[32], bool up) {
+// w[i] = v at column tcol(i, hf) + DD of the same rank (DD = +-1); values
+// that would come from outside the 32 columns are unspecified.
+template <int DD>
+__device__ __forceinline__ f32x16 tshift(const f32x16& v, int hf) {
+    float snd[4], rcv[4];
 #pragma unroll
-    for (int q = 0; q < K; q++) {
-        float send = up ? v[q] : v[q + K];
-        float keep = up ? v[q + K] : v[q];
-        v[q] = keep + swz_xor<K>(send);
+    for (int a = 0; a < 4; a++) {
+        if constexpr (DD == 1) snd[a] = hf ? v[4 * a] : v[a < 3 ? 4 * a + 4 : 0];
+        else snd[a] = hf ? v[a > 0 ? 4 * a - 1 : 0] : v[4 * a + 3];
     }
+#pragma unroll
+    for (int a = 0; a < 4; a++) rcv[a] = __shfl_xor(snd[a], 32, 64);
+    f32x16 w;
+#pragma unroll
+    for (int i = 0; i < 16; i++) {
+        const int b = i & 3;
+        if constexpr (DD == 1) w[i] = b < 3 ? v[i + 1] : rcv[i >> 2];
+        else w[i] = b > 0 ? v[i - 1] : rcv[i >> 2];
+    }
+    return w;
 }
 
-// Sum of v[0..31] over the 32 lanes of each half-wavefront; lane cl gets the
-// total of entry cl.  Each step keeps the half of the list picked by one bit
-// of the lane index and adds the partner's copy of that half.
-__device__ __forceinline__ float half_reduce32(float (&v)[32], int cl) {
-    halve<16>(v, cl & 16);
-    halve<8>(v, cl & 8);
-    halve<4>(v, cl & 4);
-    halve<2>(v, cl & 2);
-    halve<1>(v, cl & 1);
-    return v[0];
+// Channel of A-operand slot u of a lane in half hf (K channels per row GEMM):
+// fp32 32x32x2 steps take channels 2u + hf; bf16 32x32x16 steps take
+// 16*(u/8) + 8*hf + u%8.
+template <bool BF>
+__device__ __forceinline__ int achan(int u, int hf) {
+    return BF ? 16 * (u >> 3) + 8 * hf + (u & 7) : 2 * u + hf;
 }
 
-// One 256-thread block per CU (the whole register file for one wavefront per
-// SIMD): the strip state and the factor-gradient accumulators do not fit half
-// of it.
+// Z^T[col][r] = sum_k a[k][col] tab[r][k]: a = one activation row in A-operand
+// slots (K/2 values a lane), tab = [32][lda] factor table in LDS.
+template <typename T, int K>
+__device__ __forceinline__ f32x16 tgemm(const T (&a)[K / 2], const T* tab, int lda, int cl, int hf) {
+    f32x16 acc;
+#pragma unroll
+    for (int i = 0; i < 16; i++) acc[i] = 0.f;
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < K / 16; q++)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack8(a + 8 * q), lds8(tab + cl * lda + 16 * q + 8 * hf),
+                                                          acc, 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int u = 0; u < K / 2; u++)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], tab[cl * lda + 2 * u + hf], acc, 0, 0, 0);
+    }
+    mfma_drain();
+    return acc;
+}
+
+// Raw buffer access (gfx9 family): a wave-uniform resource (base, byte range)
+// and a per-lane byte offset.  The range check covers the per-lane offset:
+// loads past the range return 0 and stores past it are dropped.
+constexpr int kBufCfg = 0x00020000;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t brsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufCfg);
+}
+template <typename T>
+__device__ __forceinline__ T bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    if constexpr (sizeof(T) == 2) return (T)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, 0);
+    else return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+__device__ __forceinline__ void bstore(float v, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)voff, 0, 0);
+}
+__device__ __forceinline__ void bstore(float v, bf16_t*, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), r, (int)voff, 0, 0);
+}
+__device__ __forceinline__ void bstore(float v, float*, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
+    bstore(v, r, voff);
+}
+
+// One activation row in A-operand slots: a[u] = src[achan(u, hf)][row][col].
+// voff = byte offset of (channel hf, row, the lane's column), or an offset
+// past the range for lanes outside the image (which then read zeros); cs =
+// channel stride in bytes.  The channel step goes in the uniform offset.
+template <typename T, int K>
+__device__ __forceinline__ void arow(T (&a)[K / 2], __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t cs) {
+#pragma unroll
+    for (int u = 0; u < K / 2; u++)
+        a[u] = bload<T>(r, voff, (uint32_t)(sizeof(T) == 2 ? 16 * (u >> 3) + (u & 7) : 2 * u) * cs);
+}
+
 template <typename T, int KH, int KW, int MT, int MS>
 __global__ void __launch_bounds__(256, 1)
     cp_bwd(CpBwdDesc d, const T* __restrict__ X, const T* __restrict__ dY,
@@ -303,24 +384,17 @@ __global__ void __launch_bounds__(256, 1)
     constexpr bool BF = sizeof(T) == 2;
     constexpr int NT = 32 * MT, NS = 32 * MS;
     constexpr int CH = (KH - 1) / 2, CW = (KW - 1) / 2;
-    constexpr int NG = (KH + KW) / 2;   // groups of two taps (32 products)
-    constexpr int LZ = 33;              // transpose tile row pitch (floats)
+    constexpr int LZ = 33;   // dZ1 transpose tile pitch (floats)
+    static_assert(KW == 3, "column shifts of one");
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int H = d.H, W = d.W;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, cl = lane & 31;
-    float* Zt = (float*)(smem + d.o_zt) + wave * (32 * LZ);
-    // per-lane running sums of the tap-gradient products, wave-private:
-    // float4 slot q of lane l at Tap[(q * 64 + l) * 4], q < 4 * (KW + KH)
-    // (taps 0..KW-1 along w, then KH along h; 16 values per tap)
-    float* Tap = (float*)(smem + d.o_tap) + wave * (64 * 16 * (KH + KW));
+    const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, cl = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // ---- tables ----
+    // ---- tables: UsA [32][lda_s], UtA [32][lda_t] (and UsT [NS][ldu] for bf16) ----
     {
         T* usa = (T*)smem;
         T* uta = (T*)(smem + d.o_uta);
-        T* UsP = (T*)(smem + d.o_usp);
-        float* KhP = (float*)(smem + d.o_kh);
-        float* KwP = (float*)(smem + d.o_kw);
         for (int e = tid; e < 32 * NS; e += 256) {
             int r = e / NS, s = e - r * NS;
             usa[r * d.lda_s + s] = Us[r * d.us_sr + s * d.us_ss];
@@ -330,28 +404,16 @@ __global__ void __launch_bounds__(256, 1)
             uta[r * d.lda_t + t] = Ut[r * d.ut_sr + t * d.ut_st];
         }
         if constexpr (BF) {
-            // UsP[q][hf][s][j] = Us[row32(8q+j, 32*hf)][s]
-            for (int e = tid; e < 2 * 2 * NS * 8; e += 256) {
-                int j = e & 7, s = (e >> 3) % NS, h2 = (e / (8 * NS)) & 1, q = e / (16 * NS);
-                UsP[e] = Us[row32(8 * q + j, 32 * h2) * d.us_sr + s * d.us_ss];
+            T* ust = (T*)(smem + d.o_ust);
+            for (int e = tid; e < 32 * NS; e += 256) {
+                int s = e / 32, r = e - s * 32;
+                ust[s * d.ldu + r] = Us[r * d.us_sr + s * d.us_ss];
             }
-        } else {
-            // UsP[i][hf][s] = Us[row32(i, 32*hf)][s]
-            for (int e = tid; e < 16 * 2 * NS; e += 256) {
-                int s = e % NS, h2 = (e / NS) & 1, i = e / (2 * NS);
-                UsP[e] = Us[row32(i, 32 * h2) * d.us_sr + s * d.us_ss];
-            }
-        }
-        for (int e = tid; e < 16 * 2 * KH; e += 256) {
-            int j = e % KH, h2 = (e / KH) & 1, i = e / (2 * KH);
-            KhP[e] = load(Kh, row32(i, 32 * h2) * d.kh_sr + j * d.kh_sj);
-        }
-        for (int e = tid; e < 16 * 2 * KW; e += 256) {
-            int j = e % KW, h2 = (e / KW) & 1, i = e / (2 * KW);
-            KwP[e] = load(Kw, row32(i, 32 * h2) * d.kw_sr + j * d.kw_sj);
         }
     }
     __syncthreads();
+    float* Tz = (float*)(smem + d.o_tz) + wave * (32 * LZ);
+    T* Yt = (T*)(smem + d.o_yt + (size_t)wave * d.yt_bytes);
 
     // ---- this wavefront's strip (waves past the end run no rows) ----
     const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
@@ -365,92 +427,29 @@ __global__ void __launch_bounds__(256, 1)
     }
     const int h0 = seg * d.seg_rows, h1 = wok ? min(H, h0 + d.seg_rows) : h0;
     const int col0 = cb * d.colstride - CW;
-    const int col = col0 + cl;
+    const int col = col0 + cl;                       // the lane's column (A operands, dX)
     const bool colok = col >= 0 && col < W;
-    const bool own = colok && cl >= CW && cl < 32 - CW;
-    const T* Xb = X + (int64_t)b * d.x_sb;
-    const T* dYb = dY + (int64_t)b * d.y_sb;
-
-    // Row GEMM: acc[r][col] = sum_k tab[r][k] src[k][row][col] (src channel
-    // stride cs), the B operand read in its MFMA layout (coalesced columns).
-    auto rowgemm = [&](const T* src, int64_t cs, const T* tab, int lda, int K, int row) {
-        f32x16 acc;
+    const bool ownlane = colok && cl >= CW && cl < 32 - CW;
+    uint32_t own = 0;                                // own columns among tcol(i, hf)
 #pragma unroll
-        for (int i = 0; i < 16; i++) acc[i] = 0.f;
-        if (row < 0 || row >= H) return acc;   // uniform over the wave
-        const T* sr = src + (int64_t)row * W + (colok ? col : 0);
-        if constexpr (BF) {
-#pragma unroll 1
-            for (int k = 0; k < K; k += 16) {
-                bf16_t xv[8];
+    for (int i = 0; i < 16; i++) {
+        const int c = tcol(i, hf), g = col0 + c;
+        if (c >= CW && c < 32 - CW && g >= 0 && g < W) own |= 1u << i;
+    }
+    constexpr uint32_t E = sizeof(T);
+    // one sample of X / dY / dX (fits a 32-bit byte range; checked by the planner)
+    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(d.S * d.x_ss * E));
+    const __amdgpu_buffer_rsrc_t rY = brsrc(dY + (int64_t)b * d.y_sb, (uint32_t)(d.T * d.y_st * E));
+    const uint32_t xcs = (uint32_t)(d.x_ss * E), ycs = (uint32_t)(d.y_st * E);
+    const uint32_t kOut = 0x80000000u;   // past every range: reads 0
+    // A-operand lane offsets (channel hf, row 0, the lane's column)
+    const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * hf * xcs : kOut;
+    const uint32_t ya0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * hf * ycs : kOut;
+    float kh[KH], kw[KW];                            // this lane's rank: r = cl
 #pragma unroll
-                for (int j = 0; j < 8; j++)
-                    xv[j] = colok ? sr[(int64_t)(k + 8 * hf + j) * cs] : (bf16_t)0;
-                bf16x8 av = lds8(tab + cl * lda + k + 8 * hf);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(xv), acc, 0, 0, 0);
-            }
-        } else {
-#pragma unroll 1
-            for (int k = 0; k < K; k += 16) {
-                float xv[8];
+    for (int j = 0; j < KH; j++) kh[j] = load(Kh, cl * d.kh_sr + j * d.kh_sj);
 #pragma unroll
-                for (int u = 0; u < 8; u++) xv[u] = colok ? sr[(int64_t)(k + 2 * u + hf) * cs] : 0.f;
-#pragma unroll
-                for (int u = 0; u < 8; u++)
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(tab[cl * lda + k + 2 * u + hf], xv[u],
-                                                               acc, 0, 0, 0);
-            }
-        }
-        return acc;
-    };
-
-    // acc[n][r][ch] += sum over the strip's columns of Zt[col][r] * src[32n+ch][row][col]
-    // (Zt holds zeros outside the strip's own columns).
-    auto colgemm = [&](f32x16* acc, int NN, const T* src, int64_t cs, int row) {
-        const T* sr = src + (int64_t)row * W;
-        if constexpr (BF) {
-#pragma unroll 1
-            for (int q = 0; q < 2; q++) {
-                bf16_t za[8];
-#pragma unroll
-                for (int j = 0; j < 8; j++) za[j] = f32_to_bf16(Zt[(16 * q + 8 * hf + j) * LZ + cl]);
-                const bf16x8 av = pack8(za);
-                for (int n = 0; n < NN; n++) {
-                    const T* sc = sr + (int64_t)(32 * n + cl) * cs;
-                    bf16_t bv[8];
-#pragma unroll
-                    for (int j = 0; j < 8; j++) {
-                        const int c = col0 + 16 * q + 8 * hf + j;
-                        bv[j] = (c >= 0 && c < W) ? sc[c] : (bf16_t)0;
-                    }
-                    acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(bv), acc[n], 0, 0, 0);
-                }
-            }
-        } else {
-            for (int n = 0; n < NN; n++) {
-                const T* sc = sr + (int64_t)(32 * n + cl) * cs;
-#pragma unroll 1
-                for (int u0 = 0; u0 < 16; u0 += 8) {
-                    float bv[8];
-#pragma unroll
-                    for (int u = 0; u < 8; u++) {
-                        const int c = col0 + 2 * (u0 + u) + hf;
-                        bv[u] = (c >= 0 && c < W) ? sc[c] : 0.f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 8; u++)
-                        acc[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            Zt[(2 * (u0 + u) + hf) * LZ + cl], bv[u], acc[n], 0, 0, 0);
-                }
-            }
-        }
-    };
-
-    // accumulator layout -> transpose tile, own columns only
-    auto to_tile = [&](const f32x16& v) {
-#pragma unroll
-        for (int i = 0; i < 16; i++) Zt[cl * LZ + row32(i, lane)] = own ? v[i] : 0.f;
-    };
+    for (int j = 0; j < KW; j++) kw[j] = load(Kw, cl * d.kw_sr + j * d.kw_sj);
 
     f32x16 ring[KH], dr[KH], accUt[MT], accUs[MS];
 #pragma unroll
@@ -462,106 +461,137 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int n = 0; n < MS; n++) accUs[n][i] = 0.f;
     }
-    for (int q = 0; q < 4 * (KH + KW); q++)
-        *(float4*)(Tap + (q * 64 + lane) * 4) = make_float4(0.f, 0.f, 0.f, 0.f);
-    // Tap[jj][i] += p[i] for this lane (16 values, four float4 slots)
-    auto tap_add = [&](int jj, const float* p) {
+    float tk[KH], tw[KW];                            // tap-gradient sums of rank cl
 #pragma unroll
-        for (int c = 0; c < 4; c++) {
-            float4* q = (float4*)(Tap + ((jj * 4 + c) * 64 + lane) * 4);
-            float4 v = *q;
-            v.x += p[4 * c];
-            v.y += p[4 * c + 1];
-            v.z += p[4 * c + 2];
-            v.w += p[4 * c + 3];
-            *q = v;
-        }
-    };
+    for (int j = 0; j < KH; j++) tk[j] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KW; j++) tw[j] = 0.f;
 
+    const T* UsA = (const T*)smem;
+    const T* UtA = (const T*)(smem + d.o_uta);
     const int hs = h0 - CH, he = wok ? h1 + CH : hs;
+    T xa[NS / 2], ya[NT / 2];
     if (wok) {
 #pragma unroll
-        for (int j = 0; j < KH - 1; j++)
-            ring[j] = rowgemm(Xb, d.x_ss, (const T*)smem, d.lda_s, NS, hs - CH + j);
+        for (int j = 0; j < KH - 1; j++) {
+            const int row = hs - CH + j;
+            if (row >= 0 && row < H) {
+                arow<T, NS>(xa, rX, xa0 + (uint32_t)(row * W) * E, xcs);
+                ring[j] = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+            }
+        }
+        if (hs + CH >= 0 && hs + CH < H) arow<T, NS>(xa, rX, xa0 + (uint32_t)((hs + CH) * W) * E, xcs);
+        if (hs >= 0 && hs < H) arow<T, NT>(ya, rY, ya0 + (uint32_t)(hs * W) * E, ycs);
     }
     for (int h = hs; h < he; h++) {
-        // Tables re-read from LDS every row: the offsets pass through an empty
-        // asm so that the loop-invariant loads are not hoisted into registers.
-        uint32_t o_usa = 0, o_uta = d.o_uta, o_usp = d.o_usp, o_kh = d.o_kh, o_kw = d.o_kw;
-        asm volatile("" : "+s"(o_usa), "+s"(o_uta), "+s"(o_usp), "+s"(o_kh), "+s"(o_kw));
-        const T* UsA = (const T*)(smem + o_usa);
-        const T* UtA = (const T*)(smem + o_uta);
-        const T* UsP = (const T*)(smem + o_usp);
-        const float* KhP = (const float*)(smem + o_kh);
-        const float* KwP = (const float*)(smem + o_kw);
+        const int hx = h - CH;
+        const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
+        // X row hx, channel-major, for the dUs product (issued first, used last)
+        T gx[MS][16];
+        if (xin) {
+            // whole offset per lane (range-checked); columns outside the image
+            // read a neighbour or 0 and are masked by `own` in the product
+#pragma unroll
+            for (int n = 0; n < MS; n++) {
+                const uint32_t v0 = (uint32_t)(32 * n + cl) * xcs + (uint32_t)((hx * W + col0 + 4 * hf) * (int)E);
+#pragma unroll
+                for (int i = 0; i < 16; i++)
+                    gx[n][i] = bload<T>(rX, v0 + (uint32_t)((8 * (i >> 2) + (i & 3)) * E), 0);
+            }
+        }
+        // Z1[h+CH]; then the next row's X operand
+        f32x16 z1n;
+#pragma unroll
+        for (int i = 0; i < 16; i++) z1n[i] = 0.f;
+        if (h + CH >= 0 && h + CH < H) z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+        ring[KH - 1] = z1n;
+        if (h + 1 < he && h + 1 + CH >= 0 && h + 1 + CH < H)
+            arow<T, NS>(xa, rX, xa0 + (uint32_t)((h + 1 + CH) * W) * E, xcs);
+        // dZ3[h]; dY[h] into the LDS tile for dUt; then the next row's dY operand
+        f32x16 dz3;
+#pragma unroll
+        for (int i = 0; i < 16; i++) dz3[i] = 0.f;
+        if (h >= 0 && h < H) {
+            dz3 = tgemm<T, NT>(ya, UtA, d.lda_t, cl, hf);
+            if (rin) {
+#pragma unroll
+                for (int u = 0; u < NT / 2; u++) Yt[achan<BF>(u, hf) * d.ly + cl] = ya[u];
+            }
+        }
+        if (h + 1 < he && h + 1 >= 0 && h + 1 < H) arow<T, NT>(ya, rY, ya0 + (uint32_t)((h + 1) * W) * E, ycs);
 
-        ring[KH - 1] = rowgemm(Xb, d.x_ss, UsA, d.lda_s, NS, h + CH);
-        const bool rin = h >= h0 && h < h1;
-        const f32x16 dz3 = rowgemm(dYb, d.y_st, UtA, d.lda_t, NT, h);
+        // Z2[h] (conv along h)
         f32x16 z2;
 #pragma unroll
         for (int i = 0; i < 16; i++) {
             float a = 0.f;
 #pragma unroll
-            for (int j = 0; j < KH; j++) a += KhP[(i * 2 + hf) * KH + j] * ring[j][i];
+            for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
             z2[i] = a;
         }
-        // conv along w (Z3) and the dKw products
+        // Z3[h] (conv along w: tap j reads column + j - 1) and the dKw products
         f32x16 z3;
+        {
+            const f32x16 zm = tshift<-1>(z2, hf);
+            const f32x16 zp = tshift<1>(z2, hf);
 #pragma unroll
-        for (int i = 0; i < 16; i++) z3[i] = 0.f;
+            for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
+            if (rin) {
 #pragma unroll
-        for (int jw = 0; jw < KW; jw++) {
-            const int dd = jw - CW;
-            float pr[16];
-#pragma unroll
-            for (int i = 0; i < 16; i++) {
-                float v;
-                if (dd == 0) {
-                    v = z2[i];
-                } else {
-                    int src = cl + dd;
-                    src = src < 0 ? 0 : (src > 31 ? 31 : src);
-                    v = __shfl(z2[i], (lane & 32) | src, 64);
+                for (int i = 0; i < 16; i++) {
+                    const float g = (own >> i) & 1 ? dz3[i] : 0.f;
+                    tw[0] += zm[i] * g;
+                    tw[1] += z2[i] * g;
+                    tw[2] += zp[i] * g;
                 }
-                z3[i] += KwP[(i * 2 + hf) * KW + jw] * v;
-                pr[i] = v * dz3[i];
             }
-            if (rin && own) tap_add(jw, pr);
         }
+        // dUt += Z3[h] dY[h]^T
         if (rin) {
-            to_tile(z3);
-            colgemm(accUt, MT, dYb, d.y_st, h);
-        }
-        // dZ2: transposed conv along w
-        f32x16 dz2;
+            if constexpr (BF) {
 #pragma unroll
-        for (int i = 0; i < 16; i++) {
-            float a = 0.f;
+                for (int q = 0; q < 2; q++) {
+                    bf16_t za[8];
 #pragma unroll
-            for (int jw = 0; jw < KW; jw++) {
-                const int dd = jw - CW;
-                float v;
-                if (dd == 0) {
-                    v = dz3[i];
-                } else {
-                    int src = cl - dd;
-                    src = src < 0 ? 0 : (src > 31 ? 31 : src);
-                    v = __shfl(dz3[i], (lane & 32) | src, 64);
+                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f);
+                    const bf16x8 av = pack8(za);
+#pragma unroll
+                    for (int n = 0; n < MT; n++) {
+                        // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
+                        const bf16_t* yr = Yt + (32 * n + cl) * d.ly + 16 * q + 4 * hf;
+                        bf16_t bv[8];
+                        __builtin_memcpy(bv, yr, 8);
+                        __builtin_memcpy(bv + 4, yr + 8, 8);
+                        accUt[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(bv), accUt[n], 0, 0, 0);
+                    }
                 }
-                a += KwP[(i * 2 + hf) * KW + jw] * v;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 16; i++) {
+                    const float av = (own >> i) & 1 ? z3[i] : 0.f;
+#pragma unroll
+                    for (int n = 0; n < MT; n++)
+                        accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            av, Yt[(32 * n + cl) * d.ly + tcol(i, hf)], accUt[n], 0, 0, 0);
+                }
             }
-            dz2[i] = a;
+        }
+        // dZ2[h]: transposed conv along w (tap j reads column - j + 1)
+        f32x16 dz2;
+        {
+            const f32x16 gp = tshift<1>(dz3, hf);
+            const f32x16 gm = tshift<-1>(dz3, hf);
+#pragma unroll
+            for (int i = 0; i < 16; i++) dz2[i] = kw[0] * gp[i] + kw[1] * dz3[i] + kw[2] * gm[i];
         }
         dr[KH - 1] = dz2;
         // dKh products
-        if (rin && own) {
+        if (rin) {
 #pragma unroll
-            for (int j = 0; j < KH; j++) {
-                float pr[16];
+            for (int i = 0; i < 16; i++) {
+                const float g = (own >> i) & 1 ? dz2[i] : 0.f;
 #pragma unroll
-                for (int i = 0; i < 16; i++) pr[i] = ring[j][i] * dz2[i];
-                tap_add(KW + j, pr);
+                for (int j = 0; j < KH; j++) tk[j] += ring[j][i] * g;
             }
         }
         // dZ1 for row h - CH
@@ -570,7 +600,7 @@ __global__ void __launch_bounds__(256, 1)
         for (int i = 0; i < 16; i++) {
             float a = 0.f;
 #pragma unroll
-            for (int j = 0; j < KH; j++) a += KhP[(i * 2 + hf) * KH + j] * dr[KH - 1 - j][i];
+            for (int j = 0; j < KH; j++) a += kh[j] * dr[KH - 1 - j][i];
             dz1[i] = a;
         }
 #pragma unroll
@@ -578,67 +608,70 @@ __global__ void __launch_bounds__(256, 1)
             ring[j] = ring[j + 1];
             dr[j] = dr[j + 1];
         }
-        const int hx = h - CH;
-        if (hx >= h0 && hx < h1) {
+        if (xin) {
+            // dX[hx] = Us^T dZ1[hx]: dZ1 through the LDS tile Tz[col][r]
             if (dX) {
+#pragma unroll
+                for (int i = 0; i < 16; i++) Tz[tcol(i, hf) * LZ + cl] = dz1[i];
                 f32x16 accX[MS];
 #pragma unroll
                 for (int n = 0; n < MS; n++)
 #pragma unroll
                     for (int i = 0; i < 16; i++) accX[n][i] = 0.f;
                 if constexpr (BF) {
+                    const T* UsT = (const T*)(smem + d.o_ust);
 #pragma unroll
                     for (int q = 0; q < 2; q++) {
                         bf16_t zb[8];
 #pragma unroll
-                        for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(dz1[8 * q + j]);
+                        for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(Tz[cl * LZ + 16 * q + 8 * hf + j]);
                         const bf16x8 bv = pack8(zb);
 #pragma unroll
-                        for (int n = 0; n < MS; n++) {
-                            bf16x8 av = lds8(UsP + (((q * 2 + hf) * NS) + n * 32 + cl) * 8);
-                            accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, accX[n], 0, 0, 0);
-                        }
+                        for (int n = 0; n < MS; n++)
+                            accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf), bv, accX[n], 0, 0, 0);
                     }
                 } else {
 #pragma unroll
-                    for (int i = 0; i < 16; i++)
+                    for (int u = 0; u < 16; u++) {
+                        const float bv = Tz[cl * LZ + 2 * u + hf];
 #pragma unroll
                         for (int n = 0; n < MS; n++)
                             accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                UsP[(i * 2 + hf) * NS + n * 32 + cl], dz1[i], accX[n], 0, 0, 0);
+                                UsA[(2 * u + hf) * d.lda_s + 32 * n + cl], bv, accX[n], 0, 0, 0);
+                    }
                 }
-                if (own) {
-                    T* xr = dX + (int64_t)b * d.x_sb + (int64_t)hx * W + col;
+                mfma_drain();
+                const __amdgpu_buffer_rsrc_t rD = brsrc(dX + (int64_t)b * d.x_sb, (uint32_t)(d.S * d.x_ss * E));
+                const uint32_t v0 = ownlane ? (uint32_t)((hx * W + col) * (int)E) : kOut;   // dropped
+#pragma unroll
+                for (int n = 0; n < MS; n++)
+#pragma unroll
+                    for (int i = 0; i < 16; i++)
+                        bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
+            }
+            // dUs += dZ1[hx] X[hx]^T
+            if constexpr (BF) {
+#pragma unroll
+                for (int q = 0; q < 2; q++) {
+                    bf16_t za[8];
+#pragma unroll
+                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
+                    const bf16x8 av = pack8(za);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(&gx[n][8 * q]), accUs[n], 0, 0, 0);
+                }
+            } else {
 #pragma unroll
-                        for (int i = 0; i < 16; i++)
-                            store(xr, (int64_t)(n * 32 + row32(i, lane)) * d.x_ss, accX[n][i]);
+                for (int i = 0; i < 16; i++) {
+                    const float av = (own >> i) & 1 ? dz1[i] : 0.f;
+#pragma unroll
+                    for (int n = 0; n < MS; n++)
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, gx[n][i], accUs[n], 0, 0, 0);
                 }
             }
-            to_tile(dz1);
-            colgemm(accUs, MS, Xb, d.x_ss, hx);
         }
-    }
-
-    // ---- tap products summed over the lanes of each half (wave-private area,
-    // read before any block-wide reuse of LDS) ----
-    constexpr int NJ = KH + KW;
-    // products of tap jj = 0..KW-1 (w) then KW..NJ-1 (h), 16 per tap; groups of
-    // two taps; lane cl of a half ends with tap 2g + cl/16, accumulator cl%16
-    float tsum[NG];
-#pragma unroll
-    for (int g = 0; g < NG; g++) {
-        float v[32];
-#pragma unroll
-        for (int c = 0; c < 8; c++) {
-            const float4 t4 = *(const float4*)(Tap + ((8 * g + c) * 64 + lane) * 4);
-            v[4 * c] = t4.x;
-            v[4 * c + 1] = t4.y;
-            v[4 * c + 2] = t4.z;
-            v[4 * c + 3] = t4.w;
-        }
-        tsum[g] = half_reduce32(v, cl);
     }
 
     // ---- block sums of the wavefront partials, in a fixed order ----
@@ -661,15 +694,18 @@ __global__ void __launch_bounds__(256, 1)
     for (int e = tid; e < 32 * NS; e += 256)
         Pus[blk * 32 * NS + e] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
     __syncthreads();
+    // taps: red[wave][half][r][KH + KW], summed over waves and halves in order
+    constexpr int NJ = KH + KW;
 #pragma unroll
-    for (int g = 0; g < NG; g++) {
-        const int jj = 2 * g + (cl >> 4), i = cl & 15;
-        red[wave * 32 * NJ + row32(i, lane) * NJ + jj] = tsum[g];
-    }
+    for (int j = 0; j < KW; j++) red[((wave * 2 + hf) * 32 + cl) * NJ + j] = tw[j];
+#pragma unroll
+    for (int j = 0; j < KH; j++) red[((wave * 2 + hf) * 32 + cl) * NJ + KW + j] = tk[j];
     __syncthreads();
     for (int e = tid; e < 32 * NJ; e += 256) {
         const int r = e / NJ, jj = e - r * NJ;
-        const float v = ((red[e] + red[32 * NJ + e]) + red[64 * NJ + e]) + red[96 * NJ + e];
+        float v = 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; q++) v += red[q * 32 * NJ + e];
         if (jj < KW) Pkw[blk * 32 * KW + r * KW + jj] = v;
         else Pkh[blk * 32 * KH + r * KH + (jj - KW)] = v;
     }

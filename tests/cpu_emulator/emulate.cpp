@@ -403,18 +403,20 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
     REQ((int64_t)d.segs * d.seg_rows >= d.H && (int64_t)(d.segs - 1) * d.seg_rows < d.H, "segments");
     REQ(d.waves == (int64_t)d.B * d.ncb * d.segs && d.blocks * 4 >= d.waves && d.blocks * 4 < d.waves + 4 &&
         (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
-    // LDS: tables, transpose tiles, tap areas, reduction area
+    // LDS: tables, transpose tiles, dY tiles, reduction area
     const uint64_t e = bf ? 2 : 4;
     REQ(d.lda_s >= d.S + (bf ? 8 : 1) && d.lda_t >= d.T + (bf ? 8 : 1) &&
         (!bf || ((d.lda_s * 2) % 16 == 0 && (d.lda_t * 2) % 16 == 0)), "table rows");
     REQ(d.o_uta >= 32 * d.lda_s * e && d.o_uta % 16 == 0, "UtA offset");
-    REQ(d.o_usp >= d.o_uta + 32 * d.lda_t * e && d.o_usp % 16 == 0, "UsP offset");
-    REQ(d.o_kh >= d.o_usp + (bf ? (uint64_t)2 * 2 * d.S * 8 * 2 : (uint64_t)16 * 2 * d.S * 4), "Kh offset");
-    REQ(d.o_kw >= d.o_kh + (uint64_t)16 * 2 * d.KH * 4, "Kw offset");
-    REQ(d.o_zt >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4 && d.o_zt % 16 == 0, "tile offset");
-    REQ(d.o_tap >= d.o_zt + (uint64_t)4 * 32 * 33 * 4 && d.o_tap % 16 == 0, "tap offset");
-    REQ(d.lds_bytes >= d.o_tap + (uint64_t)4 * 64 * 16 * (d.KH + d.KW) * 4, "tap area");
-    REQ(d.red_bytes >= (uint64_t)4 * 4 * 32 * std::max({d.S, d.T, d.KH + d.KW}) &&
+    REQ(d.o_ust >= d.o_uta + 32 * d.lda_t * e && d.o_ust % 16 == 0, "UsT offset");
+    REQ(!bf || (d.ldu >= 32 + 8 && (d.ldu * 2) % 16 == 0), "UsT rows");
+    REQ(d.o_tz >= d.o_ust + (bf ? (uint64_t)d.S * d.ldu * 2 : 0) && d.o_tz % 16 == 0, "tile offset");
+    REQ(d.ly >= 32 + (bf ? 8 : 1) && (!bf || (d.ly * 2) % 8 == 0), "dY tile rows");
+    REQ(d.o_yt >= d.o_tz + (uint64_t)4 * 32 * 33 * 4 && d.o_yt % 16 == 0 &&
+        d.yt_bytes >= (uint64_t)d.T * d.ly * e && d.yt_bytes % 16 == 0, "dY tiles");
+    REQ(d.lds_bytes >= d.o_yt + 4 * (uint64_t)d.yt_bytes, "LDS tiles");
+    REQ(d.red_bytes >= (uint64_t)4 * std::max({(uint64_t)4 * 32 * d.S, (uint64_t)4 * 32 * d.T,
+                                               (uint64_t)8 * 32 * (d.KH + d.KW)}) &&
         d.lds_bytes >= d.red_bytes && d.lds_bytes <= 160 * 1024 && ln.lds == d.lds_bytes, "LDS size");
     const int B = d.B, S = d.S, R = d.R, T = d.T, H = d.H, W = d.W, K = d.KH, c3 = (K - 1) / 2;
     const size_t HW = (size_t)H * W;
