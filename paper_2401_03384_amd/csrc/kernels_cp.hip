@@ -312,6 +312,13 @@ __device__ __forceinline__ f32x16 tshift(const f32x16& v, int hf) {
     return w;
 }
 
+// A-operand slots are stored as 32-bit words: one fp32 value, or two bf16
+// values built as a 16-bit pair so that the loads fill the two halves of a
+// register directly (no packing step that would wait for them).
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+template <typename T> struct Slots { static constexpr int per_word = sizeof(T) == 2 ? 2 : 1; };
+
 // Channel of A-operand slot u of a lane in half hf (K channels per row GEMM):
 // fp32 32x32x2 steps take channels 2u + hf; bf16 32x32x16 steps take
 // 16*(u/8) + 8*hf + u%8.
@@ -323,19 +330,23 @@ __device__ __forceinline__ int achan(int u, int hf) {
 // Z^T[col][r] = sum_k a[k][col] tab[r][k]: a = one activation row in A-operand
 // slots (K/2 values a lane), tab = [32][lda] factor table in LDS.
 template <typename T, int K>
-__device__ __forceinline__ f32x16 tgemm(const T (&a)[K / 2], const T* tab, int lda, int cl, int hf) {
+__device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::per_word], const T* tab, int lda,
+                                        int cl, int hf) {
     f32x16 acc;
 #pragma unroll
     for (int i = 0; i < 16; i++) acc[i] = 0.f;
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int q = 0; q < K / 16; q++)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack8(a + 8 * q), lds8(tab + cl * lda + 16 * q + 8 * hf),
-                                                          acc, 0, 0, 0);
+        for (int q = 0; q < K / 16; q++) {
+            bf16x8 av;
+            __builtin_memcpy(&av, a + 4 * q, 16);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, lds8(tab + cl * lda + 16 * q + 8 * hf), acc, 0, 0, 0);
+        }
     } else {
 #pragma unroll
         for (int u = 0; u < K / 2; u++)
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], tab[cl * lda + 2 * u + hf], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[u]), tab[cl * lda + 2 * u + hf], acc, 0,
+                                                       0, 0);
     }
     mfma_drain();
     return acc;
@@ -369,10 +380,22 @@ __device__ __forceinline__ void bstore(float v, float*, __amdgpu_buffer_rsrc_t r
 // past the range for lanes outside the image (which then read zeros); cs =
 // channel stride in bytes.  The channel step goes in the uniform offset.
 template <typename T, int K>
-__device__ __forceinline__ void arow(T (&a)[K / 2], __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t cs) {
+__device__ __forceinline__ void arow(uint32_t (&a)[K / 2 / Slots<T>::per_word], __amdgpu_buffer_rsrc_t r,
+                                     uint32_t voff, uint32_t cs) {
+    if constexpr (sizeof(T) == 2) {
 #pragma unroll
-    for (int u = 0; u < K / 2; u++)
-        a[u] = bload<T>(r, voff, (uint32_t)(sizeof(T) == 2 ? 16 * (u >> 3) + (u & 7) : 2 * u) * cs);
+        for (int p = 0; p < K / 4; p++) {
+            const int u0 = 2 * p, u1 = 2 * p + 1;
+            u16x2 v;
+            v.x = __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u0 >> 3) + (u0 & 7)) * cs), 0);
+            v.y = __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u1 >> 3) + (u1 & 7)) * cs), 0);
+            a[p] = __builtin_bit_cast(uint32_t, v);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < K / 2; u++)
+            a[u] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)(2 * u * cs), 0);
+    }
 }
 
 template <typename T, int KH, int KW, int MT, int MS>
@@ -470,7 +493,8 @@ __global__ void __launch_bounds__(256, 1)
     const T* UsA = (const T*)smem;
     const T* UtA = (const T*)(smem + d.o_uta);
     const int hs = h0 - CH, he = wok ? h1 + CH : hs;
-    T xa[NS / 2], ya[NT / 2];
+    constexpr int PW = Slots<T>::per_word;
+    uint32_t xa[NS / 2 / PW], ya[NT / 2 / PW];
     if (wok) {
 #pragma unroll
         for (int j = 0; j < KH - 1; j++) {
@@ -487,7 +511,7 @@ __global__ void __launch_bounds__(256, 1)
         const int hx = h - CH;
         const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
         // X row hx, channel-major, for the dUs product (issued first, used last)
-        T gx[MS][16];
+        uint32_t gx[MS][16 / PW];
         if (xin) {
             // whole offset per lane (range-checked); columns outside the image
             // read a neighbour or 0 and are masked by `own` in the product
@@ -495,8 +519,20 @@ __global__ void __launch_bounds__(256, 1)
             for (int n = 0; n < MS; n++) {
                 const uint32_t v0 = (uint32_t)(32 * n + cl) * xcs + (uint32_t)((hx * W + col0 + 4 * hf) * (int)E);
 #pragma unroll
-                for (int i = 0; i < 16; i++)
-                    gx[n][i] = bload<T>(rX, v0 + (uint32_t)((8 * (i >> 2) + (i & 3)) * E), 0);
+                for (int p = 0; p < 16 / PW; p++) {
+                    if constexpr (BF) {
+                        const int i0 = 2 * p, i1 = 2 * p + 1;
+                        u16x2 v;
+                        v.x = __builtin_amdgcn_raw_buffer_load_b16(
+                            rX, (int)(v0 + (uint32_t)((8 * (i0 >> 2) + (i0 & 3)) * E)), 0, 0);
+                        v.y = __builtin_amdgcn_raw_buffer_load_b16(
+                            rX, (int)(v0 + (uint32_t)((8 * (i1 >> 2) + (i1 & 3)) * E)), 0, 0);
+                        gx[n][p] = __builtin_bit_cast(uint32_t, v);
+                    } else {
+                        gx[n][p] = __builtin_amdgcn_raw_buffer_load_b32(
+                            rX, (int)(v0 + (uint32_t)((8 * (p >> 2) + (p & 3)) * E)), 0, 0);
+                    }
+                }
             }
         }
         // Z1[h+CH]; then the next row's X operand
@@ -515,7 +551,12 @@ __global__ void __launch_bounds__(256, 1)
             dz3 = tgemm<T, NT>(ya, UtA, d.lda_t, cl, hf);
             if (rin) {
 #pragma unroll
-                for (int u = 0; u < NT / 2; u++) Yt[achan<BF>(u, hf) * d.ly + cl] = ya[u];
+                for (int u = 0; u < NT / 2; u++) {
+                    const uint32_t w = ya[u / PW];
+                    const uint32_t v = PW == 2 ? ((u & 1) ? w >> 16 : w & 0xffffu) : w;
+                    if constexpr (BF) Yt[achan<BF>(u, hf) * d.ly + cl] = (T)v;
+                    else Yt[achan<BF>(u, hf) * d.ly + cl] = __uint_as_float(v);
+                }
             }
         }
         if (h + 1 < he && h + 1 >= 0 && h + 1 < H) arow<T, NT>(ya, rY, ya0 + (uint32_t)((h + 1) * W) * E, ycs);
@@ -659,8 +700,11 @@ __global__ void __launch_bounds__(256, 1)
                     for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
                     const bf16x8 av = pack8(za);
 #pragma unroll
-                    for (int n = 0; n < MS; n++)
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(&gx[n][8 * q]), accUs[n], 0, 0, 0);
+                    for (int n = 0; n < MS; n++) {
+                        bf16x8 bv;
+                        __builtin_memcpy(&bv, &gx[n][4 * q], 16);
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, accUs[n], 0, 0, 0);
+                    }
                 }
             } else {
 #pragma unroll
@@ -668,7 +712,8 @@ __global__ void __launch_bounds__(256, 1)
                     const float av = (own >> i) & 1 ? dz1[i] : 0.f;
 #pragma unroll
                     for (int n = 0; n < MS; n++)
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, gx[n][i], accUs[n], 0, 0, 0);
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(gx[n][i]), accUs[n],
+                                                                        0, 0, 0);
                 }
             }
         }
