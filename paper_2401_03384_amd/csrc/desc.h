@@ -48,6 +48,8 @@ enum KernelKind : int32_t {
     K_DW_TAPREDUCE = 21,    // ordered sum of tap partials (DwDesc)
     K_CP_FWD = 22,          // fused CP chain forward (CpDesc)
     K_CP_BWD = 23,          // fused CP chain backward (CpBwdDesc)
+    K_TC = 24,              // tiled MFMA contraction with convolved labels (TcDesc)
+    K_TC_REDUCE = 25,       // ordered sum of its split-reduction partials (TcDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -121,6 +123,34 @@ struct CpDesc {
     // permuted Ut operands at o_ut, the permuted taps at o_kh / o_kw
     uint32_t lds_bytes, o_ut, o_kh, o_kw;
     int32_t lda;
+};
+
+// General contraction on MFMA tiles:
+//
+//   C[g][m][n] = sum_k A[g][m][k] * B[g][k][n]
+//
+// g, m, n and k are each a list of up to four dims (outermost first) with a
+// stride per operand (zero where the operand lacks the dim).  A convolved
+// label (up to two) contributes one n dim (its output index p, n_cv = label
+// slot) and one k dim (its reduction index j, k_cv = slot): B is read at
+// position cv_a*p + cv_b*j + cv_g with stride cv_s, zero outside [0, cv_lim);
+// A reads j as a plain k index.  This covers the forward convolution, the
+// gradient of its feature side (transposed convolution) and of its filter
+// side (p = filter tap, j = image position).  With ksplit > 1 the k range is
+// cut in chunks of kchunk; block (g, chunk) writes P[g][chunk][m][n] (fp32)
+// and the reduce launch sums the chunks in order into C.
+struct TcDesc {
+    int32_t ng, nm, nn, nk, ncv, ksplit;
+    int64_t M, N, K, G;
+    int64_t g_size[4], g_sA[4], g_sB[4], g_sC[4];
+    int64_t m_size[4], m_sA[4], m_sC[4];
+    int64_t n_size[4], n_sB[4], n_sC[4];
+    int64_t k_size[4], k_sA[4], k_sB[4];
+    int32_t n_cv[4], k_cv[4];
+    int32_t cv_a[2], cv_b[2];
+    int64_t cv_g[2], cv_lim[2], cv_s[2];
+    int32_t mtiles, ntiles;
+    int64_t kchunk, blocks;
 };
 
 // Backward of the same chain.  Strips and segments as in CpDesc (dX has X's

@@ -14,6 +14,10 @@ hipError_t launch_generic(const Launch& ln, const void* a, const void* b, void* 
 hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, void* d,
                        hipStream_t s);
 
+// General contraction (K_TC main launch: a = A, b = B, c = C, d = partials;
+// K_TC_REDUCE: d = partials, c = C).
+hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, void* d, hipStream_t s);
+
 // Fused CP chain forward: ops = {X, Us, Kh, Kw, Ut}.
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
 

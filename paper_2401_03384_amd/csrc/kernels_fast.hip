@@ -628,6 +628,8 @@ hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, 
         case K_DW: return launch_dw(ln, a, b, c, s);
         case K_DW_TAPGRAD: return launch_dw_tapgrad(ln, a, b, d, s);
         case K_DW_TAPREDUCE: return launch_dw_tapreduce(ln, d, c, s);
+        case K_TC:
+        case K_TC_REDUCE: return launch_tc(ln, a, b, c, d, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -13,6 +13,10 @@
 //                         of C, and a filter indexed by the conv label and by a
 //                         run of C's labels ahead of the convolved axis
 //   filter-tap gradient   the same structure with the filter as the result
+//   general contraction   everything else with two operands, no self-contracted
+//                         labels and at most two convolved labels: batch, row,
+//                         column and reduction dims of any layout, convolved
+//                         labels read with shifted, bounds-checked positions
 #include <algorithm>
 #include <cstring>
 
@@ -452,6 +456,188 @@ bool try_dw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     return false;
 }
 
+
+// ---- general contraction on MFMA tiles --------------------------------------
+bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if (!op.has_r || op.convs.size() > 2 || op.L.dtype != op.R.dtype) return false;
+    // B is the operand whose positions mix an output and a reduction index
+    int bside = -1;   // 0: L is B, 1: R is B
+    for (const ConvMap& cm : op.convs) {
+        const bool lmix = cm.aL != 0, rmix = cm.aR != 0;
+        const int sd = (lmix && !rmix) ? 0 : (!lmix && rmix) ? 1 : -2;
+        if (sd == -2) return false;
+        if (bside == -1) bside = sd;
+        else if (bside != sd) return false;
+    }
+    const TensorRef& C = op.C;
+    if (bside == -1) {
+        // plain contraction: B holds the output's innermost label (unit-stride columns)
+        const int last = C.labels.empty() ? -1 : C.labels.back();
+        const bool inL = last >= 0 && op.L.has(last), inR = last >= 0 && op.R.has(last);
+        if (inR && !inL) bside = 1;
+        else if (inL && !inR) bside = 0;
+        else bside = op.R.numel() >= op.L.numel() ? 1 : 0;
+    }
+    const TensorRef& Bt = bside == 0 ? op.L : op.R;
+    const TensorRef& At = bside == 0 ? op.R : op.L;
+    const BufRef& bbuf = Bt.buf;
+    const BufRef& abuf = At.buf;
+    auto conv_of = [&](int l) -> int {
+        for (size_t k = 0; k < op.convs.size(); k++)
+            if (op.convs[k].label == l) return (int)k;
+        return -1;
+    };
+    // the A side reads a convolved label as its plain reduction index
+    for (const ConvMap& cm : op.convs) {
+        const int a = bside == 0 ? cm.aR : cm.aL, b = bside == 0 ? cm.bR : cm.bL;
+        const int64_t g = bside == 0 ? cm.gR : cm.gL, lim = bside == 0 ? cm.limR : cm.limL;
+        if (a != 0 || b != 1 || g != 0 || lim < cm.J || !At.has(cm.label)) return false;
+    }
+    struct Dm {
+        int64_t size, sA, sB, sC;
+        int cv;
+    };
+    std::vector<Dm> G, M, N, K;
+    for (size_t k = 0; k < C.labels.size(); k++) {
+        const int l = C.labels[k];
+        const int ci = conv_of(l);
+        if (ci >= 0) {
+            N.push_back({op.convs[ci].O, 0, 0, C.strides[k], ci});
+            continue;
+        }
+        const bool inA = At.has(l), inB = Bt.has(l);
+        if (inA && inB) G.push_back({C.dims[k], At.stride_of(l), Bt.stride_of(l), C.strides[k], -1});
+        else if (inA) M.push_back({C.dims[k], At.stride_of(l), 0, C.strides[k], -1});
+        else if (inB) N.push_back({C.dims[k], 0, Bt.stride_of(l), C.strides[k], -1});
+        else return false;   // output label broadcast from neither operand
+    }
+    for (size_t k = 0; k < At.labels.size(); k++) {   // reduction dims in A's order
+        const int l = At.labels[k];
+        const int ci = conv_of(l);   // a convolved label: its reduction index, even though C has it
+        if (ci >= 0) {
+            K.push_back({op.convs[ci].J, At.strides[k], 0, 0, ci});
+            continue;
+        }
+        if (C.has(l)) continue;
+        if (!Bt.has(l)) return false;   // self-contracted in A
+        K.push_back({At.dims[k], At.strides[k], Bt.stride_of(l), 0, -1});
+    }
+    for (int l : Bt.labels)
+        if (!C.has(l) && !At.has(l) && conv_of(l) < 0) return false;   // self-contracted in B
+    auto merge = [](std::vector<Dm>& v) {
+        for (size_t i = 0; i + 1 < v.size();) {
+            Dm& a = v[i];
+            const Dm& b = v[i + 1];
+            if (a.cv < 0 && b.cv < 0 && a.sA == b.sA * b.size && a.sB == b.sB * b.size &&
+                a.sC == b.sC * b.size) {
+                a.size *= b.size;
+                a.sA = b.sA;
+                a.sB = b.sB;
+                a.sC = b.sC;
+                v.erase(v.begin() + i + 1);
+            } else {
+                i++;
+            }
+        }
+    };
+    merge(G);
+    merge(M);
+    merge(N);
+    merge(K);
+    if (G.size() > 4 || M.size() > 4 || N.size() > 4 || K.size() > 4) return false;
+    auto total = [](const std::vector<Dm>& v) {
+        int64_t t = 1;
+        for (const Dm& x : v) t *= x.size;
+        return t;
+    };
+    const int64_t Mt = total(M), Nt = total(N), Kt = total(K), Gt = total(G);
+    if (Mt >= (1ll << 31) || Nt >= (1ll << 31) || Kt >= (1ll << 31) || Mt * Nt == 0 || Kt == 0) return false;
+    TcDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.ng = (int32_t)G.size();
+    d.nm = (int32_t)M.size();
+    d.nn = (int32_t)N.size();
+    d.nk = (int32_t)K.size();
+    d.ncv = (int32_t)op.convs.size();
+    d.M = Mt;
+    d.N = Nt;
+    d.K = Kt;
+    d.G = Gt;
+    for (size_t i = 0; i < G.size(); i++) {
+        d.g_size[i] = G[i].size;
+        d.g_sA[i] = G[i].sA;
+        d.g_sB[i] = G[i].sB;
+        d.g_sC[i] = G[i].sC;
+    }
+    for (size_t i = 0; i < M.size(); i++) {
+        d.m_size[i] = M[i].size;
+        d.m_sA[i] = M[i].sA;
+        d.m_sC[i] = M[i].sC;
+    }
+    for (size_t i = 0; i < 4; i++) d.n_cv[i] = d.k_cv[i] = -1;
+    for (size_t i = 0; i < N.size(); i++) {
+        d.n_size[i] = N[i].size;
+        d.n_sB[i] = N[i].sB;
+        d.n_sC[i] = N[i].sC;
+        d.n_cv[i] = N[i].cv;
+    }
+    for (size_t i = 0; i < K.size(); i++) {
+        d.k_size[i] = K[i].size;
+        d.k_sA[i] = K[i].sA;
+        d.k_sB[i] = K[i].sB;
+        d.k_cv[i] = K[i].cv;
+    }
+    for (size_t c = 0; c < op.convs.size(); c++) {
+        const ConvMap& cm = op.convs[c];
+        d.cv_a[c] = bside == 0 ? cm.aL : cm.aR;
+        d.cv_b[c] = bside == 0 ? cm.bL : cm.bR;
+        d.cv_g[c] = bside == 0 ? cm.gL : cm.gR;
+        d.cv_lim[c] = bside == 0 ? cm.limL : cm.limR;
+        d.cv_s[c] = Bt.stride_of(cm.label);
+    }
+    const int MT = Mt > 32 ? 2 : 1;
+    d.mtiles = (int32_t)cdiv(Mt, 32 * MT);
+    d.ntiles = (int32_t)cdiv(Nt, 128);
+    const int64_t tiles = Gt * d.mtiles * d.ntiles;
+    // split the reduction when the output alone gives too few blocks
+    int64_t ksplit = 1;
+    if (tiles < 1024 && Kt > 512) ksplit = std::min<int64_t>(cdiv(2048, tiles), cdiv(Kt, 256));
+    while (ksplit > 1 && (double)Gt * ksplit * Mt * Nt * 4.0 > 512.0 * (1 << 20)) ksplit /= 2;
+    d.kchunk = cdiv(cdiv(Kt, ksplit), 32) * 32;
+    d.ksplit = (int32_t)cdiv(Kt, d.kchunk);
+    d.blocks = tiles * d.ksplit;
+    if (d.blocks > 0x7fffffff || Gt * Mt * Nt > ((int64_t)1 << 40)) return false;
+    const char* tin = tname(At.dtype);
+    Launch ln;
+    ln.kind = K_TC | dt_bits(At.dtype, At.dtype, C.dtype);
+    ln.a = abuf;
+    ln.b = bbuf;
+    ln.grid[0] = (uint32_t)d.blocks;
+    ln.block[0] = 256;
+    ln.kname = std::string("tc_gemm<") + tin + ", " + tname(d.ksplit > 1 ? C.dtype : C.dtype) + ", " +
+               (MT == 2 ? "2>" : "1>");
+    if (d.ksplit == 1) {
+        ln.c = C.buf;
+        set_desc(ln, d);
+        out.push_back(ln);
+        return true;
+    }
+    const BufRef part = scratch.alloc((size_t)(Gt * d.ksplit * Mt * Nt) * 4);
+    ln.d = part;
+    set_desc(ln, d);
+    out.push_back(ln);
+    Launch lr;
+    lr.kind = K_TC_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+    lr.d = part;
+    lr.c = C.buf;
+    lr.grid[0] = (uint32_t)cdiv(Gt * Mt * Nt, 256);
+    lr.block[0] = 256;
+    set_desc(lr, d);
+    lr.kname = std::string("tc_reduce<") + tname(C.dtype) + ">";
+    out.push_back(lr);
+    return true;
+}
+
 }  // namespace
 
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
@@ -459,7 +645,8 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
     (void)e;
     std::vector<Launch> out;
     bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
-                (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out));
+                (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
+                 try_tc(op, scratch, out));
     if (!fast) {
         out.clear();
         Launch ln = lower_generic(op);

@@ -499,6 +499,122 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
     REQ(ok, "out-of-bounds partials (cp_bwd)");
     return true;
 }
+
+// General contraction: C (or the chunk partials) from the descriptor's dim
+// lists, in double, every access bounds-checked.
+bool run_tc(const Launch& ln, Ctx& c) {
+    TcDesc d = desc_of<TcDesc>(ln);
+    int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2;
+    Buf A = resolve(ln.a, c, 0, o1), B = resolve(ln.b, c, 0, o2);
+    REQ(o1 && o2, "unresolved buffer");
+    REQ(d.ng <= 4 && d.nm <= 4 && d.nn <= 4 && d.nk <= 4 && d.ncv <= 2 && d.ksplit >= 1, "dims");
+    int64_t Mt = 1, Nt = 1, Kt = 1, Gt = 1;
+    for (int i = 0; i < d.nm; i++) Mt *= d.m_size[i];
+    for (int i = 0; i < d.nn; i++) Nt *= d.n_size[i];
+    for (int i = 0; i < d.nk; i++) Kt *= d.k_size[i];
+    for (int i = 0; i < d.ng; i++) Gt *= d.g_size[i];
+    REQ(Mt == d.M && Nt == d.N && Kt == d.K && Gt == d.G, "totals");
+    REQ(d.kchunk % 32 == 0 && d.kchunk * (d.ksplit - 1) < d.K && d.kchunk * d.ksplit >= d.K, "split");
+    const int MT = d.M > 32 ? 2 : 1;
+    REQ(d.mtiles == (d.M + 32 * MT - 1) / (32 * MT) && d.ntiles == (d.N + 127) / 128 &&
+        d.blocks == d.G * d.mtiles * d.ntiles * d.ksplit && (int64_t)ln.grid[0] == d.blocks &&
+        ln.block[0] == 256, "grid");
+    for (int i = 0; i < d.nn; i++) REQ(d.n_cv[i] < d.ncv && (d.n_cv[i] < 0 || d.n_sB[i] == 0), "conv n dims");
+    for (int i = 0; i < d.nk; i++) REQ(d.k_cv[i] < d.ncv && (d.k_cv[i] < 0 || d.k_sB[i] == 0), "conv k dims");
+    Buf Cb, Pb;
+    if (d.ksplit == 1) {
+        bool o3;
+        Cb = resolve(ln.c, c, 0, o3);
+        REQ(o3, "unresolved buffer");
+    } else {
+        bool o4;
+        Pb = resolve(ln.d, c, 0, o4);
+        REQ(o4, "unresolved buffer");
+    }
+    bool ok = true;
+    std::vector<int64_t> gi(4), mi(4), ni(4), ki(4);
+    auto split = [](int64_t x, int nd, const int64_t* size, std::vector<int64_t>& idx) {
+        for (int i = nd - 1; i >= 0; --i) {
+            idx[i] = x % size[i];
+            x /= size[i];
+        }
+    };
+    for (int64_t g = 0; g < d.G; g++) {
+        split(g, d.ng, d.g_size, gi);
+        int64_t gA = 0, gB = 0, gC = 0;
+        for (int i = 0; i < d.ng; i++) {
+            gA += gi[i] * d.g_sA[i];
+            gB += gi[i] * d.g_sB[i];
+            gC += gi[i] * d.g_sC[i];
+        }
+        for (int64_t m = 0; m < d.M; m++) {
+            split(m, d.nm, d.m_size, mi);
+            int64_t oA = gA, oC = gC;
+            for (int i = 0; i < d.nm; i++) {
+                oA += mi[i] * d.m_sA[i];
+                oC += mi[i] * d.m_sC[i];
+            }
+            for (int64_t n = 0; n < d.N; n++) {
+                split(n, d.nn, d.n_size, ni);
+                int64_t oB = gB, oCn = oC, p[2] = {0, 0};
+                for (int i = 0; i < d.nn; i++) {
+                    oB += ni[i] * d.n_sB[i];
+                    oCn += ni[i] * d.n_sC[i];
+                    if (d.n_cv[i] >= 0) p[d.n_cv[i]] = ni[i];
+                }
+                for (int ks = 0; ks < d.ksplit; ks++) {
+                    double acc = 0;
+                    for (int64_t k = ks * d.kchunk; k < std::min(d.K, (ks + 1) * d.kchunk); k++) {
+                        split(k, d.nk, d.k_size, ki);
+                        int64_t a = oA, b = oB, j[2] = {0, 0};
+                        for (int i = 0; i < d.nk; i++) {
+                            a += ki[i] * d.k_sA[i];
+                            b += ki[i] * d.k_sB[i];
+                            if (d.k_cv[i] >= 0) j[d.k_cv[i]] = ki[i];
+                        }
+                        bool in = true;
+                        for (int cv = 0; cv < d.ncv; cv++) {
+                            int64_t pos = d.cv_a[cv] * p[cv] + d.cv_b[cv] * j[cv] + d.cv_g[cv];
+                            if (pos < 0 || pos >= d.cv_lim[cv]) in = false;
+                            b += pos * d.cv_s[cv];
+                        }
+                        if (in) acc += (double)ld(A, tIn, a, ok) * ld(B, tIn, b, ok);
+                    }
+                    if (d.ksplit == 1) st(Cb, tC, oCn, (float)acc, ok);
+                    else st(Pb, 0, ((g * d.ksplit + ks) * d.M + m) * d.N + n, (float)acc, ok);
+                }
+            }
+        }
+        REQ(ok, "out-of-bounds access (tc)");
+    }
+    return true;
+}
+
+bool run_tc_reduce(const Launch& ln, Ctx& c) {
+    TcDesc d = desc_of<TcDesc>(ln);
+    int tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2;
+    Buf P = resolve(ln.d, c, 0, o1), C = resolve(ln.c, c, 0, o2);
+    REQ(o1 && o2, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] * 256 >= d.G * d.M * d.N, "grid");
+    bool ok = true;
+    for (int64_t g = 0; g < d.G; g++)
+        for (int64_t m = 0; m < d.M; m++)
+            for (int64_t n = 0; n < d.N; n++) {
+                int64_t off = 0, x = g;
+                for (int i = d.ng - 1; i >= 0; --i) { off += (x % d.g_size[i]) * d.g_sC[i]; x /= d.g_size[i]; }
+                x = m;
+                for (int i = d.nm - 1; i >= 0; --i) { off += (x % d.m_size[i]) * d.m_sC[i]; x /= d.m_size[i]; }
+                x = n;
+                for (int i = d.nn - 1; i >= 0; --i) { off += (x % d.n_size[i]) * d.n_sC[i]; x /= d.n_size[i]; }
+                double s = 0;
+                for (int ks = 0; ks < d.ksplit; ks++) s += ld(P, 0, ((g * d.ksplit + ks) * d.M + m) * d.N + n, ok);
+                st(C, tC, off, (float)s, ok);
+            }
+    REQ(ok, "out-of-bounds access (tc reduce)");
+    return true;
+}
 }  // namespace
 
 extern "C" {
@@ -548,6 +664,8 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
                     : v == K_CP_FWD ? run_cp_fwd(ln, c)
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
+                    : v == K_TC ? run_tc(ln, c)
+                    : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
         }
