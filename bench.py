@@ -31,6 +31,8 @@ def parse_args():
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--dtype", default=None, help="f32 or bf16 (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--launch-table", action="store_true",
+                    help="print per-launch averages of the timed steps to stderr")
     ap.add_argument("--cpu-batch", type=int, default=128, help="batch of the oracle CPU sample")
     ap.add_argument("--generic", action="store_true", help="generic kernel only")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
@@ -38,16 +40,26 @@ def parse_args():
     return ap.parse_args()
 
 
+def kernel_sources_sha256():
+    """Hash of every kernel source: counter results stay valid only while it matches."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2401_03384_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith(".hip"):
+            h.update(f.encode())
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(kname, dtype):
     """HBM bytes per dispatch of `kname` from the committed counter summary,
-    or None when there is none or the kernel source changed since."""
-    import hashlib
+    or None when there is none or any kernel source changed since."""
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_c2_{dtype}.json")
     if not os.path.exists(path):
         return None
     info = json.load(open(path))
-    src = os.path.join(ROOT, info["source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != info["source_sha256"]:
+    if info.get("kernel_sources_sha256") != kernel_sources_sha256():
         return None
     return info["bytes_per_dispatch"].get(kname)
 
@@ -77,6 +89,24 @@ def roofline(records, dtype):
             "alg_bytes_per_launch": round(nbytes / n),
             "launches": n, "avg_us": round(ms / n * 1e3, 2),
             "share_of_kernel_time": round(ms / total, 3)}
+
+
+def launch_table(records, steps):
+    """Per-launch averages over the timed steps (launch order of one step)."""
+    per = len(records) // max(steps, 1)
+    rows = []
+    for i in range(per):
+        rs = records[i::per]
+        ms = sum(r[2] for r in rs) / len(rs)
+        kname, step, _, nbytes, flops = rs[0]
+        rows.append((ms, kname, step, nbytes, flops))
+    tot = sum(r[0] for r in rows)
+    lines = [f"{'us':>9s} {'share':>6s} {'GB/s':>8s} {'TF/s':>7s}  kernel | step"]
+    for ms, kname, step, nbytes, flops in rows:
+        s = ms / 1e3
+        lines.append(f"{ms * 1e3:9.1f} {ms / tot:6.1%} {nbytes / s / 1e9 if s else 0:8.0f} "
+                     f"{flops / s / 1e12 if s else 0:7.2f}  {kname} | {step}")
+    return "\n".join(lines)
 
 
 def cpu_baseline(w, batch):
@@ -173,6 +203,8 @@ def main():
     t_step = timed(args.steps)
     n_rec = P.ce_timing_end()
     records = [P.ce_timing_record(i) for i in range(n_rec)]
+    if args.launch_table:
+        print(launch_table(records, args.steps), file=sys.stderr, flush=True)
     # forward-only and backward-only steps (reported beside the main figure)
     t_fwd = timed(max(5, args.steps // 2), bwd=False)
     t_bwd = timed(max(5, args.steps // 2), fwd=False)
