@@ -53,6 +53,15 @@ __device__ __forceinline__ void mfma_drain() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// Logical tile of a block: the dispatcher deals consecutive blocks round-robin
+// to the 8 XCDs (each with its own L2), so XCD x gets a contiguous range of
+// logical tiles; neighbouring strips and segments, which share halo rows and
+// cache lines, then meet in one L2.
+__device__ __forceinline__ int64_t xcd_tile(int64_t bid, int64_t nb) {
+    const int64_t q = nb / 8, r = nb % 8, x = bid % 8, i = bid / 8;
+    return x * q + (x < r ? x : r) + i;
+}
+
 // r held by accumulator i of a lane in a 32x32 MFMA result
 __device__ __forceinline__ int row32(int i, int lane) {
     return 8 * (i >> 2) + 4 * ((lane >> 5) & 1) + (i & 3);
@@ -72,7 +81,8 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const int S = d.S, H = d.H, W = d.W;
     const int LDA = d.lda;
     T* UsL = (T*)smem;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
     // ---- tables ----
     {
@@ -108,12 +118,13 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     __syncthreads();
 
     // ---- this wavefront's strip ----
-    const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
+    // strips fastest: the waves of a block share halo rows and cache lines
+    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
     if (gw >= d.waves) return;
-    const int seg = (int)(gw % d.segs);
-    const int64_t rest = gw / d.segs;
-    const int cb = (int)(rest % d.ncb);
-    const int b = (int)(rest / d.ncb);
+    const int cb = (int)(gw % d.ncb);
+    const int64_t rest = gw / d.ncb;
+    const int seg = (int)(rest % d.segs);
+    const int b = (int)(rest / d.segs);
     const int col = cb * d.colstride - HWW + (lane & 31);
     const bool colok = col >= 0 && col < W;
     const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
@@ -312,12 +323,26 @@ __device__ __forceinline__ f32x16 tshift(const f32x16& v, int hf) {
     return w;
 }
 
-// A-operand slots are stored as 32-bit words: one fp32 value, or two bf16
-// values built as a 16-bit pair so that the loads fill the two halves of a
-// register directly (no packing step that would wait for them).
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+// A-operand slots are stored one per 32-bit word (a bf16 value zero-extended).
+// bf16 pairs are packed only where the MFMA consumes them, behind an empty asm
+// that pins the loaded word: packing right after the load would make the wave
+// wait for it there and undo the prefetch.
+template <typename T> struct Slots { static constexpr int per_word = 1; };
 
-template <typename T> struct Slots { static constexpr int per_word = sizeof(T) == 2 ? 2 : 1; };
+// bf16x8 from eight zero-extended 16-bit words, packed at the point of use
+__device__ __forceinline__ bf16x8 pack_words(const uint32_t* w) {
+    uint32_t p[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        uint32_t lo = w[2 * i], hi = w[2 * i + 1];
+        asm volatile("" : "+v"(lo), "+v"(hi));
+        p[i] = (lo & 0xffffu) | (hi << 16);
+    }
+    bf16x8 v;
+    __builtin_memcpy(&v, p, 16);
+    return v;
+}
+
 
 // Channel of A-operand slot u of a lane in half hf (K channels per row GEMM):
 // fp32 32x32x2 steps take channels 2u + hf; bf16 32x32x16 steps take
@@ -337,11 +362,9 @@ __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::pe
     for (int i = 0; i < 16; i++) acc[i] = 0.f;
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int q = 0; q < K / 16; q++) {
-            bf16x8 av;
-            __builtin_memcpy(&av, a + 4 * q, 16);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, lds8(tab + cl * lda + 16 * q + 8 * hf), acc, 0, 0, 0);
-        }
+        for (int q = 0; q < K / 16; q++)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack_words(a + 8 * q), lds8(tab + cl * lda + 16 * q + 8 * hf),
+                                                          acc, 0, 0, 0);
     } else {
 #pragma unroll
         for (int u = 0; u < K / 2; u++)
@@ -380,20 +403,12 @@ __device__ __forceinline__ void bstore(float v, float*, __amdgpu_buffer_rsrc_t r
 // past the range for lanes outside the image (which then read zeros); cs =
 // channel stride in bytes.  The channel step goes in the uniform offset.
 template <typename T, int K>
-__device__ __forceinline__ void arow(uint32_t (&a)[K / 2 / Slots<T>::per_word], __amdgpu_buffer_rsrc_t r,
-                                     uint32_t voff, uint32_t cs) {
-    if constexpr (sizeof(T) == 2) {
+__device__ __forceinline__ void arow(uint32_t (&a)[K / 2], __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t cs) {
 #pragma unroll
-        for (int p = 0; p < K / 4; p++) {
-            const int u0 = 2 * p, u1 = 2 * p + 1;
-            u16x2 v;
-            v.x = __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u0 >> 3) + (u0 & 7)) * cs), 0);
-            v.y = __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u1 >> 3) + (u1 & 7)) * cs), 0);
-            a[p] = __builtin_bit_cast(uint32_t, v);
-        }
-    } else {
-#pragma unroll
-        for (int u = 0; u < K / 2; u++)
+    for (int u = 0; u < K / 2; u++) {
+        if constexpr (sizeof(T) == 2)
+            a[u] = __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u >> 3) + (u & 7)) * cs), 0);
+        else
             a[u] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)(2 * u * cs), 0);
     }
 }
@@ -439,14 +454,14 @@ __global__ void __launch_bounds__(256, 1)
     T* Yt = (T*)(smem + d.o_yt + (size_t)wave * d.yt_bytes);
 
     // ---- this wavefront's strip (waves past the end run no rows) ----
-    const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
+    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
     const bool wok = gw < d.waves;
     int seg = 0, cb = 0, b = 0;
-    if (wok) {
-        seg = (int)(gw % d.segs);
-        const int64_t rest = gw / d.segs;
-        cb = (int)(rest % d.ncb);
-        b = (int)(rest / d.ncb);
+    if (wok) {   // strips fastest (see the forward kernel)
+        cb = (int)(gw % d.ncb);
+        const int64_t rest = gw / d.ncb;
+        seg = (int)(rest % d.segs);
+        b = (int)(rest / d.segs);
     }
     const int h0 = seg * d.seg_rows, h1 = wok ? min(H, h0 + d.seg_rows) : h0;
     const int col0 = cb * d.colstride - CW;
@@ -511,7 +526,7 @@ __global__ void __launch_bounds__(256, 1)
         const int hx = h - CH;
         const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
         // X row hx, channel-major, for the dUs product (issued first, used last)
-        uint32_t gx[MS][16 / PW];
+        uint32_t gx[MS][16];
         if (xin) {
             // whole offset per lane (range-checked); columns outside the image
             // read a neighbour or 0 and are masked by `own` in the product
@@ -519,19 +534,10 @@ __global__ void __launch_bounds__(256, 1)
             for (int n = 0; n < MS; n++) {
                 const uint32_t v0 = (uint32_t)(32 * n + cl) * xcs + (uint32_t)((hx * W + col0 + 4 * hf) * (int)E);
 #pragma unroll
-                for (int p = 0; p < 16 / PW; p++) {
-                    if constexpr (BF) {
-                        const int i0 = 2 * p, i1 = 2 * p + 1;
-                        u16x2 v;
-                        v.x = __builtin_amdgcn_raw_buffer_load_b16(
-                            rX, (int)(v0 + (uint32_t)((8 * (i0 >> 2) + (i0 & 3)) * E)), 0, 0);
-                        v.y = __builtin_amdgcn_raw_buffer_load_b16(
-                            rX, (int)(v0 + (uint32_t)((8 * (i1 >> 2) + (i1 & 3)) * E)), 0, 0);
-                        gx[n][p] = __builtin_bit_cast(uint32_t, v);
-                    } else {
-                        gx[n][p] = __builtin_amdgcn_raw_buffer_load_b32(
-                            rX, (int)(v0 + (uint32_t)((8 * (p >> 2) + (p & 3)) * E)), 0, 0);
-                    }
+                for (int i = 0; i < 16; i++) {
+                    const int vi = (int)(v0 + (uint32_t)((8 * (i >> 2) + (i & 3)) * E));
+                    if constexpr (BF) gx[n][i] = __builtin_amdgcn_raw_buffer_load_b16(rX, vi, 0, 0);
+                    else gx[n][i] = __builtin_amdgcn_raw_buffer_load_b32(rX, vi, 0, 0);
                 }
             }
         }
@@ -700,11 +706,9 @@ __global__ void __launch_bounds__(256, 1)
                     for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
                     const bf16x8 av = pack8(za);
 #pragma unroll
-                    for (int n = 0; n < MS; n++) {
-                        bf16x8 bv;
-                        __builtin_memcpy(&bv, &gx[n][4 * q], 16);
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, accUs[n], 0, 0, 0);
-                    }
+                    for (int n = 0; n < MS; n++)
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack_words(&gx[n][8 * q]), accUs[n],
+                                                                           0, 0, 0);
                 }
             } else {
 #pragma unroll
