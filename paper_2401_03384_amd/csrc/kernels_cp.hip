@@ -354,7 +354,7 @@ __device__ __forceinline__ int achan(int u, int hf) {
 
 // Z^T[col][r] = sum_k a[k][col] tab[r][k]: a = one activation row in A-operand
 // slots (K/2 values a lane), tab = [32][lda] factor table in LDS.
-template <typename T, int K>
+template <typename T, int K, bool DRAIN = true>
 __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::per_word], const T* tab, int lda,
                                         int cl, int hf) {
     f32x16 acc;
@@ -371,7 +371,7 @@ __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::pe
             acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[u]), tab[cl * lda + 2 * u + hf], acc, 0,
                                                        0, 0);
     }
-    mfma_drain();
+    if constexpr (DRAIN) mfma_drain();
     return acc;
 }
 
@@ -507,27 +507,68 @@ __global__ void __launch_bounds__(256, 1)
 
     const T* UsA = (const T*)smem;
     const T* UtA = (const T*)(smem + d.o_uta);
+    const T* UsT = (const T*)(smem + d.o_ust);
     const int hs = h0 - CH, he = wok ? h1 + CH : hs;
+    // A-operand row offsets: rows outside the image (and lanes outside it) read zeros
+    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    auto yoff = [&](int row) { return (row >= 0 && row < H) ? ya0 + (uint32_t)(row * W) * E : kOut; };
+    // dX: a zero range drops every store when the gradient is not wanted
+    const __amdgpu_buffer_rsrc_t rD =
+        brsrc(dX ? (const T*)dX + (int64_t)b * d.x_sb : X, dX ? (uint32_t)(d.S * d.x_ss * E) : 0u);
+    const uint32_t dx0 = ownlane ? (uint32_t)(col * (int)E) : kOut;
     constexpr int PW = Slots<T>::per_word;
     uint32_t xa[NS / 2 / PW], ya[NT / 2 / PW];
     if (wok) {
 #pragma unroll
         for (int j = 0; j < KH - 1; j++) {
-            const int row = hs - CH + j;
-            if (row >= 0 && row < H) {
-                arow<T, NS>(xa, rX, xa0 + (uint32_t)(row * W) * E, xcs);
-                ring[j] = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
-            }
+            arow<T, NS>(xa, rX, xoff(hs - CH + j), xcs);
+            ring[j] = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
         }
-        if (hs + CH >= 0 && hs + CH < H) arow<T, NS>(xa, rX, xa0 + (uint32_t)((hs + CH) * W) * E, xcs);
-        if (hs >= 0 && hs < H) arow<T, NT>(ya, rY, ya0 + (uint32_t)(hs * W) * E, ycs);
+        arow<T, NS>(xa, rX, xoff(hs + CH), xcs);
+        arow<T, NT>(ya, rY, yoff(hs), ycs);
     }
-    for (int h = hs; h < he; h++) {
+
+    // One row of the walk, branch-free so that the compiler can overlap the
+    // convolution arithmetic with the MFMA chains.  Row h counts for dUt, dKw
+    // and dKh only inside the segment (rin), row h - CH for dX and dUs (xin);
+    // outside, the products run on zeroed operands and the dX stores go past
+    // the buffer's range (dropped).
+    auto row_step = [&](int h) {
         const int hx = h - CH;
         const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
-        // X row hx, channel-major, for the dUs product (issued first, used last)
+        const uint32_t ownr = rin ? own : 0u, ownx = xin ? own : 0u;
+        // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
+        const f32x16 z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+        arow<T, NS>(xa, rX, xoff(h + 1 + CH), xcs);
+        const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, d.lda_t, cl, hf);
+        ring[KH - 1] = z1n;
+        // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1):
+        // VALU work independent of the dZ3 chain above, free to overlap it
+        f32x16 z2, z3;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
+            z2[i] = a;
+        }
+        const f32x16 zm = tshift<-1>(z2, hf);
+        const f32x16 zp = tshift<1>(z2, hf);
+#pragma unroll
+        for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
+        __builtin_amdgcn_sched_barrier(0);   // the next row's dY loads stay behind the chain
+        {   // dY[h] into the LDS tile of the dUt product
+#pragma unroll
+            for (int u = 0; u < NT / 2; u++) {
+                if constexpr (BF) Yt[achan<BF>(u, hf) * d.ly + cl] = (T)ya[u];
+                else Yt[achan<BF>(u, hf) * d.ly + cl] = __uint_as_float(ya[u]);
+            }
+        }
+        arow<T, NT>(ya, rY, yoff(h + 1), ycs);
+        mfma_drain();   // dz3 is read below
+        // X row hx, channel-major, for the dUs product (issued here, used last)
         uint32_t gx[MS][16];
-        if (xin) {
+        {
             // whole offset per lane (range-checked); columns outside the image
             // read a neighbour or 0 and are masked by `own` in the product
 #pragma unroll
@@ -541,66 +582,22 @@ __global__ void __launch_bounds__(256, 1)
                 }
             }
         }
-        // Z1[h+CH]; then the next row's X operand
-        f32x16 z1n;
-#pragma unroll
-        for (int i = 0; i < 16; i++) z1n[i] = 0.f;
-        if (h + CH >= 0 && h + CH < H) z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
-        ring[KH - 1] = z1n;
-        if (h + 1 < he && h + 1 + CH >= 0 && h + 1 + CH < H)
-            arow<T, NS>(xa, rX, xa0 + (uint32_t)((h + 1 + CH) * W) * E, xcs);
-        // dZ3[h]; dY[h] into the LDS tile for dUt; then the next row's dY operand
-        f32x16 dz3;
-#pragma unroll
-        for (int i = 0; i < 16; i++) dz3[i] = 0.f;
-        if (h >= 0 && h < H) {
-            dz3 = tgemm<T, NT>(ya, UtA, d.lda_t, cl, hf);
-            if (rin) {
-#pragma unroll
-                for (int u = 0; u < NT / 2; u++) {
-                    const uint32_t w = ya[u / PW];
-                    const uint32_t v = PW == 2 ? ((u & 1) ? w >> 16 : w & 0xffffu) : w;
-                    if constexpr (BF) Yt[achan<BF>(u, hf) * d.ly + cl] = (T)v;
-                    else Yt[achan<BF>(u, hf) * d.ly + cl] = __uint_as_float(v);
-                }
-            }
-        }
-        if (h + 1 < he && h + 1 >= 0 && h + 1 < H) arow<T, NT>(ya, rY, ya0 + (uint32_t)((h + 1) * W) * E, ycs);
-
-        // Z2[h] (conv along h)
-        f32x16 z2;
-#pragma unroll
-        for (int i = 0; i < 16; i++) {
-            float a = 0.f;
-#pragma unroll
-            for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
-            z2[i] = a;
-        }
-        // Z3[h] (conv along w: tap j reads column + j - 1) and the dKw products
-        f32x16 z3;
         {
-            const f32x16 zm = tshift<-1>(z2, hf);
-            const f32x16 zp = tshift<1>(z2, hf);
+            // dKw products
 #pragma unroll
-            for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
-            if (rin) {
-#pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const float g = (own >> i) & 1 ? dz3[i] : 0.f;
-                    tw[0] += zm[i] * g;
-                    tw[1] += z2[i] * g;
-                    tw[2] += zp[i] * g;
-                }
+            for (int i = 0; i < 16; i++) {
+                const float g = (ownr >> i) & 1 ? dz3[i] : 0.f;
+                tw[0] += zm[i] * g;
+                tw[1] += z2[i] * g;
+                tw[2] += zp[i] * g;
             }
-        }
-        // dUt += Z3[h] dY[h]^T
-        if (rin) {
+            // dUt += Z3[h] dY[h]^T
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
                     bf16_t za[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f);
+                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((ownr >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f);
                     const bf16x8 av = pack8(za);
 #pragma unroll
                     for (int n = 0; n < MT; n++) {
@@ -615,7 +612,7 @@ __global__ void __launch_bounds__(256, 1)
             } else {
 #pragma unroll
                 for (int i = 0; i < 16; i++) {
-                    const float av = (own >> i) & 1 ? z3[i] : 0.f;
+                    const float av = (ownr >> i) & 1 ? z3[i] : 0.f;
 #pragma unroll
                     for (int n = 0; n < MT; n++)
                         accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
@@ -632,11 +629,10 @@ __global__ void __launch_bounds__(256, 1)
             for (int i = 0; i < 16; i++) dz2[i] = kw[0] * gp[i] + kw[1] * dz3[i] + kw[2] * gm[i];
         }
         dr[KH - 1] = dz2;
-        // dKh products
-        if (rin) {
+        {   // dKh products
 #pragma unroll
             for (int i = 0; i < 16; i++) {
-                const float g = (own >> i) & 1 ? dz2[i] : 0.f;
+                const float g = (ownr >> i) & 1 ? dz2[i] : 0.f;
 #pragma unroll
                 for (int j = 0; j < KH; j++) tk[j] += ring[j][i] * g;
             }
@@ -655,47 +651,36 @@ __global__ void __launch_bounds__(256, 1)
             ring[j] = ring[j + 1];
             dr[j] = dr[j + 1];
         }
-        if (xin) {
+        {
             // dX[hx] = Us^T dZ1[hx]: dZ1 through the LDS tile Tz[col][r]
-            if (dX) {
 #pragma unroll
-                for (int i = 0; i < 16; i++) Tz[tcol(i, hf) * LZ + cl] = dz1[i];
-                f32x16 accX[MS];
+            for (int i = 0; i < 16; i++) Tz[tcol(i, hf) * LZ + cl] = dz1[i];
+            f32x16 accX[MS];
 #pragma unroll
-                for (int n = 0; n < MS; n++)
+            for (int n = 0; n < MS; n++)
 #pragma unroll
-                    for (int i = 0; i < 16; i++) accX[n][i] = 0.f;
-                if constexpr (BF) {
-                    const T* UsT = (const T*)(smem + d.o_ust);
+                for (int i = 0; i < 16; i++) accX[n][i] = 0.f;
+            if constexpr (BF) {
 #pragma unroll
-                    for (int q = 0; q < 2; q++) {
-                        bf16_t zb[8];
+                for (int q = 0; q < 2; q++) {
+                    bf16_t zb[8];
 #pragma unroll
-                        for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(Tz[cl * LZ + 16 * q + 8 * hf + j]);
-                        const bf16x8 bv = pack8(zb);
+                    for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(Tz[cl * LZ + 16 * q + 8 * hf + j]);
+                    const bf16x8 bv = pack8(zb);
 #pragma unroll
-                        for (int n = 0; n < MS; n++)
-                            accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf), bv, accX[n], 0, 0, 0);
-                    }
-                } else {
-#pragma unroll
-                    for (int u = 0; u < 16; u++) {
-                        const float bv = Tz[cl * LZ + 2 * u + hf];
-#pragma unroll
-                        for (int n = 0; n < MS; n++)
-                            accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                UsA[(2 * u + hf) * d.lda_s + 32 * n + cl], bv, accX[n], 0, 0, 0);
-                    }
+                    for (int n = 0; n < MS; n++)
+                        accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf),
+                                                                          bv, accX[n], 0, 0, 0);
                 }
-                mfma_drain();
-                const __amdgpu_buffer_rsrc_t rD = brsrc(dX + (int64_t)b * d.x_sb, (uint32_t)(d.S * d.x_ss * E));
-                const uint32_t v0 = ownlane ? (uint32_t)((hx * W + col) * (int)E) : kOut;   // dropped
+            } else {
 #pragma unroll
-                for (int n = 0; n < MS; n++)
+                for (int u = 0; u < 16; u++) {
+                    const float bv = Tz[cl * LZ + 2 * u + hf];
 #pragma unroll
-                    for (int i = 0; i < 16; i++)
-                        bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
+                    for (int n = 0; n < MS; n++)
+                        accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(UsA[(2 * u + hf) * d.lda_s + 32 * n + cl], bv,
+                                                                       accX[n], 0, 0, 0);
+                }
             }
             // dUs += dZ1[hx] X[hx]^T
             if constexpr (BF) {
@@ -703,7 +688,7 @@ __global__ void __launch_bounds__(256, 1)
                 for (int q = 0; q < 2; q++) {
                     bf16_t za[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((own >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
+                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((ownx >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
                     const bf16x8 av = pack8(za);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
@@ -713,15 +698,23 @@ __global__ void __launch_bounds__(256, 1)
             } else {
 #pragma unroll
                 for (int i = 0; i < 16; i++) {
-                    const float av = (own >> i) & 1 ? dz1[i] : 0.f;
+                    const float av = (ownx >> i) & 1 ? dz1[i] : 0.f;
 #pragma unroll
                     for (int n = 0; n < MS; n++)
                         accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(gx[n][i]), accUs[n],
                                                                         0, 0, 0);
                 }
             }
+            mfma_drain();   // accX is read by the stores
+            const uint32_t v0 = xin ? dx0 + (uint32_t)(hx * W) * E : kOut;   // kOut: past the range
+#pragma unroll
+            for (int n = 0; n < MS; n++)
+#pragma unroll
+                for (int i = 0; i < 16; i++)
+                    bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
         }
-    }
+    };
+    for (int h = hs; h < he; h++) row_step(h);
 
     // ---- block sums of the wavefront partials, in a fixed order ----
     __syncthreads();
