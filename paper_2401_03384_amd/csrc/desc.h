@@ -50,6 +50,11 @@ enum KernelKind : int32_t {
     K_CP_BWD = 23,          // fused CP chain backward (CpBwdDesc)
     K_TC = 24,              // tiled MFMA contraction with convolved labels (TcDesc)
     K_TC_REDUCE = 25,       // ordered sum of its split-reduction partials (TcDesc)
+    K_THIN = 26,            // channel mix with few rows and few reduced channels (GemmDesc)
+    K_CRED = 27,            // 2-D convolution summed over channels into one plane (CredDesc)
+    K_CREDW = 28,           // filter-tap partials of the same convolution (CredDesc)
+    K_THINW = 29,           // small-output contraction over a long reduction (ThinwDesc)
+    K_THINW_REDUCE = 30,    // ordered sum of its partials (ThinwDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -151,6 +156,46 @@ struct TcDesc {
     int64_t cv_g[2], cv_lim[2], cv_s[2];
     int32_t mtiles, ntiles;
     int64_t kchunk, blocks;
+};
+
+// Convolution of a stack of planes contracted over one shared index:
+//   C[u][p] = sum_s sum_j Z[u][s][p + j - c] * O[s][j]
+// over 2-D positions p (output) and j (reduction), Z zero outside its plane.
+// Two instances, both with the plane held in LDS with its zero halo:
+//   K_CRED  (forward): p runs over an H x W output plane, j over KH x KW
+//           filter taps; u = batch (up to two dims), s = rank (one dim);
+//           O = the filter F[s][jh][jw].
+//   K_CREDW (filter gradient): p runs over KH x KW taps, j over the H x W
+//           plane; u = rank (one dim), s = batch (up to two dims); O = the
+//           output gradient; writes per-chunk partials P[chunk][u][tap].
+// Planes (Z, the output of K_CRED, O of K_CREDW) are dense: row stride W,
+// unit columns.  ch, cw: zero padding before the first row / column.
+struct CredDesc {
+    int32_t H, W, KH, KW, ch, cw;
+    int32_t PH, PWp, wchunks, items;   // LDS plane (rows, padded row pitch); 4-pixel items
+    int32_t ng, per;                   // batch dims; planes per block
+    int64_t R, G;                      // rank count; batch count
+    int64_t g_size[2], g_sZ[2], g_sY[2];
+    int64_t z_sr, f_sr, f_sh, f_sw;    // K_CRED: F strides; K_CREDW: f_sr = 0
+    int64_t gchunk, nrb;               // K_CREDW: batch indices per block, rank groups
+    int64_t blocks;
+    uint32_t lds_bytes, threads;
+};
+
+// Contraction with a small output per batch index and a long reduction:
+//   C[g][m][n] = sum_k P[g][m][k] * Q[g][n][k]
+// (factor gradients of reshaped-CP layers), M, N <= 16.  k runs over an
+// inner run of Kin elements contiguous in P and Q and up to three outer
+// dims; g over up to three dims (a zero stride where an operand lacks one).
+// A block takes one g and `orows` consecutive outer indices and writes one
+// partial per (g, chunk, m, n); K_THINW_REDUCE sums the chunks in order.
+struct ThinwDesc {
+    int32_t ng, no, M, N;
+    int64_t G, Kin, Kout;
+    int64_t g_size[3], g_sP[3], g_sQ[3], g_sC[3];
+    int64_t o_size[3], o_sP[3], o_sQ[3];
+    int64_t sPm, sQn, sCm, sCn;
+    int64_t orows, kchunks, blocks;
 };
 
 // Backward of the same chain.  Strips and segments as in CpDesc (dX has X's

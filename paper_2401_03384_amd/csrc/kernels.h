@@ -14,6 +14,18 @@ hipError_t launch_generic(const Launch& ln, const void* a, const void* b, void* 
 hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, void* d,
                        hipStream_t s);
 
+// Small-output contraction over a long reduction (K_THINW / K_THINW_REDUCE,
+// ThinwDesc): p, q = the operands, part = fp32 partials, c = the output.
+hipError_t launch_thinw(const Launch& ln, const void* p, const void* q, void* part, void* c, hipStream_t s);
+
+// Plane convolution contracted over one index (K_CRED / K_CREDW, CredDesc):
+// z = the stacked planes, o = the filter (K_CRED) or the output gradient
+// (K_CREDW), y = the output plane (K_CRED) or the fp32 partials (K_CREDW).
+hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, hipStream_t s);
+
+// Thin channel mixing (K_THIN, GemmDesc): a = factor, b = activations, c = out.
+hipError_t launch_thin(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s);
+
 // General contraction (K_TC main launch: a = A, b = B, c = C, d = partials;
 // K_TC_REDUCE: d = partials, c = C).
 hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, void* d, hipStream_t s);

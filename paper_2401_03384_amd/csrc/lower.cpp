@@ -156,6 +156,24 @@ bool try_gemm(const PairOp& op, std::vector<Launch>& out) {
         d.sAk = sFk;
         d.sBk = sDk;
         d.sCm = sCm;
+        // few rows and few reduced channels: a column-streaming kernel, no tiles
+        const int thinM = M <= 4 ? 4 : M <= 8 ? 8 : 16, thinK = K <= 4 ? 4 : K <= 8 ? 8 : 16;
+        if (M <= 16 && K <= 16 && thinM * thinK <= 64 && N >= 16 && G * N < ((int64_t)1 << 31)) {
+            d.mtiles = d.ntiles = 1;
+            d.blocks = cdiv(G * N, 256);   // one column per thread
+            Launch ln;
+            ln.kind = K_THIN | dt_bits(D.dtype, F.dtype, C.dtype);
+            ln.a = fbuf;
+            ln.b = dbuf;
+            ln.c = C.buf;
+            ln.grid[0] = (uint32_t)d.blocks;
+            ln.block[0] = 256;
+            set_desc(ln, d);
+            ln.kname = std::string("thin_gemm<") + tname(D.dtype) + ", " + tname(C.dtype) + ", " +
+                       std::to_string(thinM) + ", " + std::to_string(thinK) + ">";
+            out.push_back(ln);
+            return true;
+        }
         int MT = M > 32 ? 2 : 1;
         d.mtiles = (int32_t)cdiv(M, 32 * MT);
         d.ntiles = (int32_t)cdiv(N, 128);
@@ -457,6 +475,317 @@ bool try_dw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
 }
 
 
+// ---- small output per batch index, long reduction ---------------------------
+//   C[g][m][n] = sum_k P[g][m][k] Q[g][n][k], M, N <= 16, k with an inner run
+// contiguous in both operands: a streaming kernel plus an ordered chunk sum.
+bool try_thinw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if (!op.has_r || !op.convs.empty() || op.L.dtype != op.R.dtype) return false;
+    const TensorRef &P = op.L, &Q = op.R, &C = op.C;
+    struct Dm {
+        int64_t size, sP, sQ, sC;
+    };
+    std::vector<Dm> G, Ko;
+    std::vector<int> ponly, qonly;   // C's labels held by one operand, in C's order
+    for (size_t k = 0; k < C.labels.size(); k++) {
+        const int l = C.labels[k];
+        const bool inP = P.has(l), inQ = Q.has(l);
+        if (inP && inQ) G.push_back({C.dims[k], P.stride_of(l), Q.stride_of(l), C.strides[k]});
+        else if (inP) ponly.push_back(l);
+        else if (inQ) qonly.push_back(l);
+        else return false;
+    }
+    // the innermost one-sided label of at most 16 becomes m (n); the rest are batch dims
+    auto pick = [&](std::vector<int>& only, const TensorRef& T, bool isP, int64_t& size, int64_t& sT,
+                    int64_t& sC) {
+        size = 1;
+        sT = sC = 0;
+        int sel = -1;
+        for (int i = (int)only.size() - 1; i >= 0; --i)
+            if (T.dim_of(only[i]) <= 16) {
+                sel = i;
+                break;
+            }
+        if (!only.empty() && sel < 0) return false;
+        for (int i = 0; i < (int)only.size(); i++) {
+            const int l = only[i];
+            if (i == sel) {
+                size = T.dim_of(l);
+                sT = T.stride_of(l);
+                sC = C.stride_of(l);
+            } else {
+                G.push_back({T.dim_of(l), isP ? T.stride_of(l) : 0, isP ? 0 : T.stride_of(l), C.stride_of(l)});
+            }
+        }
+        return true;
+    };
+    int64_t M, N, sPm, sQn, sCm, sCn;
+    if (!pick(ponly, P, true, M, sPm, sCm) || !pick(qonly, Q, false, N, sQn, sCn)) return false;
+    const int MM = M <= 4 ? 4 : M <= 8 ? 8 : 16, NN = N <= 4 ? 4 : N <= 8 ? 8 : 16;
+    if (MM * NN > 64) return false;
+    for (size_t k = 0; k < P.labels.size(); k++) {   // reduced labels in P's order
+        const int l = P.labels[k];
+        if (C.has(l)) continue;
+        if (!Q.has(l)) return false;
+        Ko.push_back({P.dims[k], P.strides[k], Q.stride_of(l), 0});
+    }
+    for (int l : Q.labels)
+        if (!C.has(l) && !P.has(l)) return false;
+    auto merge = [](std::vector<Dm>& v) {
+        for (size_t i = 0; i + 1 < v.size();) {
+            Dm& a = v[i];
+            const Dm& b = v[i + 1];
+            if (a.sP == b.sP * b.size && a.sQ == b.sQ * b.size && a.sC == b.sC * b.size) {
+                a.size *= b.size;
+                a.sP = b.sP;
+                a.sQ = b.sQ;
+                a.sC = b.sC;
+                v.erase(v.begin() + i + 1);
+            } else {
+                i++;
+            }
+        }
+    };
+    merge(G);
+    merge(Ko);
+    if (Ko.empty() || Ko.back().sP != 1 || Ko.back().sQ != 1) return false;
+    const int64_t Kin = Ko.back().size;
+    Ko.pop_back();
+    if (Kin < 16 || G.size() > 3 || Ko.size() > 3) return false;
+    ThinwDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.ng = (int32_t)G.size();
+    d.no = (int32_t)Ko.size();
+    d.M = (int32_t)M;
+    d.N = (int32_t)N;
+    d.G = 1;
+    for (size_t i = 0; i < G.size(); i++) {
+        d.g_size[i] = G[i].size;
+        d.g_sP[i] = G[i].sP;
+        d.g_sQ[i] = G[i].sQ;
+        d.g_sC[i] = G[i].sC;
+        d.G *= G[i].size;
+    }
+    d.Kout = 1;
+    for (size_t i = 0; i < Ko.size(); i++) {
+        d.o_size[i] = Ko[i].size;
+        d.o_sP[i] = Ko[i].sP;
+        d.o_sQ[i] = Ko[i].sQ;
+        d.Kout *= Ko[i].size;
+    }
+    d.Kin = Kin;
+    d.sPm = sPm;
+    d.sQn = sQn;
+    d.sCm = sCm;
+    d.sCn = sCn;
+    // enough reduction per g to be worth a stream, at least 32 elements per thread
+    if (d.Kout * Kin < 16384) return false;
+    const int64_t maxrows = std::min<int64_t>(512, ((int64_t)1 << 30) / Kin);
+    int64_t chunks = std::max<int64_t>(1, cdiv(2048, d.G));
+    chunks = std::min(chunks, std::max<int64_t>(1, d.Kout * Kin / (256 * 32)));
+    d.orows = std::min(cdiv(d.Kout, chunks), maxrows);
+    if (d.orows < 1) return false;
+    d.kchunks = cdiv(d.Kout, d.orows);
+    d.blocks = d.G * d.kchunks;
+    if (d.blocks > 0x7fffffff) return false;
+    const std::string shape = std::to_string(MM) + ", " + std::to_string(NN) + ">";
+    const BufRef part = scratch.alloc((size_t)(d.blocks * MM * NN * 4));
+    Launch ln;
+    ln.kind = K_THINW | dt_bits(P.dtype, P.dtype, DT_F32);
+    ln.a = P.buf;
+    ln.b = Q.buf;
+    ln.d = part;
+    ln.grid[0] = (uint32_t)d.blocks;
+    ln.block[0] = 256;
+    set_desc(ln, d);
+    ln.kname = std::string("thinw<") + tname(P.dtype) + ", " + shape;
+    out.push_back(ln);
+    Launch lr;
+    lr.kind = K_THINW_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+    lr.d = part;
+    lr.c = C.buf;
+    lr.grid[0] = (uint32_t)cdiv(d.G * M * N, 256);
+    lr.block[0] = 256;
+    set_desc(lr, d);
+    lr.kname = std::string("thinw_reduce<") + tname(C.dtype) + ", " + shape;
+    out.push_back(lr);
+    return true;
+}
+
+// ---- plane convolution contracted over one index ---------------------------
+//   C[u][p] = sum_s sum_j Z[u][s][p + j - c] * O[s][j]
+// Forward (p = output pixels, j = taps) runs as K_CRED; the filter gradient
+// (p = taps, j = pixels) as K_CREDW plus an ordered partial sum.
+bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if (!op.has_r || op.convs.size() != 2 || op.L.dtype != op.R.dtype) return false;
+    const int zside = op.convs[0].aL != 0 ? 0 : 1;
+    const TensorRef& Z = zside == 0 ? op.L : op.R;
+    const TensorRef& O = zside == 0 ? op.R : op.L;
+    const TensorRef& C = op.C;
+    struct Cv {
+        int label;
+        int64_t O, J, g, limZ, limO;
+    } cv[2];
+    for (int k = 0; k < 2; k++) {
+        const ConvMap& cm = op.convs[k];
+        const int aZ = zside == 0 ? cm.aL : cm.aR, bZ = zside == 0 ? cm.bL : cm.bR;
+        const int aO = zside == 0 ? cm.aR : cm.aL, bO = zside == 0 ? cm.bR : cm.bL;
+        const int64_t gO = zside == 0 ? cm.gR : cm.gL;
+        if (aZ != 1 || bZ != 1 || aO != 0 || bO != 1 || gO != 0) return false;
+        cv[k] = {cm.label, cm.O, cm.J, zside == 0 ? cm.gL : cm.gR, zside == 0 ? cm.limL : cm.limR,
+                 zside == 0 ? cm.limR : cm.limL};
+        if (cv[k].limO < cm.J || !Z.has(cm.label) || !O.has(cm.label) || !C.has(cm.label)) return false;
+    }
+    // w: the convolved label with unit stride in Z
+    if (Z.stride_of(cv[0].label) == 1) std::swap(cv[0], cv[1]);
+    const Cv& ch = cv[0];
+    const Cv& cw = cv[1];
+    if (Z.stride_of(cw.label) != 1 || Z.stride_of(ch.label) != cw.limZ) return false;
+    const bool wgrad = ch.O < ch.J;   // p over taps, j over the plane
+    const int64_t H = ch.limZ, W = cw.limZ;
+    const int64_t KH = wgrad ? ch.O : ch.J, KW = wgrad ? cw.O : cw.J;
+    if ((wgrad ? ch.J : ch.O) != H || (wgrad ? cw.J : cw.O) != W) return false;
+    const int64_t pch = -ch.g, pcw = -cw.g;
+    if (pch < 0 || pch >= KH || pcw < 0 || pcw >= KW) return false;
+    const bool kok = (KH == KW && (KH == 3 || KH == 5 || KH == 7)) || (KH == 1 && KW == 3) ||
+                     (KH == 3 && KW == 1);
+    if (!kok || (wgrad && KH * KW > 25)) return false;   // gradient taps live in registers
+    // the plane of the output (forward) or of O (gradient) is dense as well
+    const TensorRef& P = wgrad ? O : C;
+    if (P.stride_of(cw.label) != 1 || P.stride_of(ch.label) != W) return false;
+    if (wgrad && (ch.limO != H || cw.limO != W)) return false;
+    auto is_conv = [&](int l) { return l == ch.label || l == cw.label; };
+    struct Dm {
+        int64_t size, s1, s2;
+    };
+    auto merge = [](std::vector<Dm>& v) {
+        for (size_t i = 0; i + 1 < v.size();) {
+            if (v[i].s1 == v[i + 1].s1 * v[i + 1].size && v[i].s2 == v[i + 1].s2 * v[i + 1].size) {
+                v[i].size *= v[i + 1].size;
+                v[i].s1 = v[i + 1].s1;
+                v[i].s2 = v[i + 1].s2;
+                v.erase(v.begin() + i + 1);
+            } else {
+                i++;
+            }
+        }
+    };
+    // u: C's non-convolved labels (in Z only); s: the reduced ones (in Z and O)
+    std::vector<Dm> U, S;
+    for (size_t k = 0; k < C.labels.size(); k++) {
+        const int l = C.labels[k];
+        if (is_conv(l)) continue;
+        if (!Z.has(l) || O.has(l)) return false;
+        U.push_back({C.dims[k], Z.stride_of(l), C.strides[k]});
+    }
+    for (size_t k = 0; k < Z.labels.size(); k++) {
+        const int l = Z.labels[k];
+        if (is_conv(l) || C.has(l)) continue;
+        if (!O.has(l)) return false;
+        S.push_back({Z.dims[k], Z.strides[k], O.stride_of(l)});
+    }
+    for (int l : O.labels)
+        if (!is_conv(l) && !C.has(l) && !Z.has(l)) return false;
+    merge(U);
+    merge(S);
+    // the batch dims (forward: u, gradient: s) and the single rank dim
+    std::vector<Dm>& Bd = wgrad ? S : U;
+    std::vector<Dm>& Rd = wgrad ? U : S;
+    if (Bd.size() > 2 || Rd.size() > 1) return false;
+    CredDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.H = (int32_t)H;
+    d.W = (int32_t)W;
+    d.KH = (int32_t)KH;
+    d.KW = (int32_t)KW;
+    d.ch = (int32_t)pch;
+    d.cw = (int32_t)pcw;
+    d.wchunks = (int32_t)cdiv(W, 4);
+    d.items = (int32_t)(H * d.wchunks);
+    if (d.items > 1024) return false;
+    const int n4 = (int)cdiv(4 + KW - 1, 4);
+    d.PH = (int32_t)(H + KH - 1);
+    d.PWp = (int32_t)(cdiv(std::max<int64_t>(W + KW - 1, 4 * (d.wchunks - 1) + 4 * n4), 4) * 4);
+    d.ng = (int32_t)Bd.size();
+    d.G = 1;
+    for (size_t i = 0; i < Bd.size(); i++) {
+        d.g_size[i] = Bd[i].size;
+        d.g_sZ[i] = Bd[i].s1;
+        d.g_sY[i] = Bd[i].s2;
+        d.G *= Bd[i].size;
+    }
+    d.R = Rd.empty() ? 1 : Rd[0].size;
+    d.z_sr = Rd.empty() ? 0 : Rd[0].s1;
+    const int64_t plane = (int64_t)d.PH * d.PWp;
+    const int maxper = 1024 / d.items;
+    if (!wgrad) {
+        d.f_sr = Rd.empty() ? 0 : Rd[0].s2;
+        d.f_sh = O.stride_of(ch.label);
+        d.f_sw = O.stride_of(cw.label);
+        // batch indices per block: enough blocks to fill the chip first
+        d.per = (int32_t)std::max<int64_t>(1, std::min<int64_t>(maxper, d.G / 1024));
+        while (d.per > 1 && 2 * d.per * plane * 4 > 64 * 1024) d.per--;
+        d.blocks = cdiv(d.G, d.per);
+    } else {
+        if (C.stride_of(ch.label) != KW * C.stride_of(cw.label)) return false;
+        // ranks per block: the largest divisor of R that fits 1024 threads
+        int64_t per = std::min<int64_t>(maxper, d.R);
+        while (per > 1 && d.R % per) per--;
+        while (per > 1 && 2 * per * plane * 4 > 96 * 1024) per--;
+        d.per = (int32_t)per;
+        d.nrb = cdiv(d.R, per);
+        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(2048, d.nrb)));
+        d.gchunk = cdiv(d.G, chunks);
+        d.blocks = d.nrb * cdiv(d.G, d.gchunk);
+    }
+    if (d.blocks > 0x7fffffff) return false;
+    d.threads = (uint32_t)(cdiv((int64_t)d.per * d.items, 64) * 64);
+    int64_t lds = 2 * (int64_t)d.per * plane * 4;
+    if (wgrad) lds = std::max<int64_t>(lds, (int64_t)d.threads * KH * KW * 4);
+    if (lds > 160 * 1024) return false;
+    d.lds_bytes = (uint32_t)lds;
+    const std::string shape = std::to_string(KH) + ", " + std::to_string(KW);
+    Launch ln;
+    ln.grid[0] = (uint32_t)d.blocks;
+    ln.block[0] = d.threads;
+    ln.lds = d.lds_bytes;
+    if (!wgrad) {
+        ln.kind = K_CRED | dt_bits(Z.dtype, Z.dtype, C.dtype);
+        ln.a = O.buf;
+        ln.b = Z.buf;
+        ln.c = C.buf;
+        set_desc(ln, d);
+        ln.kname = std::string("cred<") + tname(Z.dtype) + ", " + tname(C.dtype) + ", " + shape + ">";
+        out.push_back(ln);
+        return true;
+    }
+    const int64_t nsplit = cdiv(d.G, d.gchunk);
+    const BufRef part = scratch.alloc((size_t)(nsplit * d.R * KH * KW * 4));
+    ln.kind = K_CREDW | dt_bits(Z.dtype, Z.dtype, DT_F32);
+    ln.a = Z.buf;
+    ln.b = O.buf;
+    ln.d = part;
+    set_desc(ln, d);
+    ln.kname = std::string("credw<") + tname(Z.dtype) + ", " + shape + ">";
+    out.push_back(ln);
+    ReduceDesc rd;
+    std::memset(&rd, 0, sizeof(rd));
+    rd.M = (int32_t)d.R;
+    rd.N = (int32_t)(KH * KW);
+    rd.nsplit = nsplit;
+    rd.sCm = Rd.empty() ? 0 : Rd[0].s2;
+    rd.sCn = C.stride_of(cw.label);
+    Launch lr;
+    lr.kind = K_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+    lr.d = part;
+    lr.c = C.buf;
+    lr.grid[0] = (uint32_t)cdiv(d.R * KH * KW, 64);
+    lr.block[0] = 256;
+    set_desc(lr, rd);
+    lr.kname = std::string("reduce_partials<") + tname(C.dtype) + ">";
+    out.push_back(lr);
+    return true;
+}
+
 // ---- general contraction on MFMA tiles --------------------------------------
 bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     if (!op.has_r || op.convs.size() > 2 || op.L.dtype != op.R.dtype) return false;
@@ -646,7 +975,7 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
     std::vector<Launch> out;
     bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
                 (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
-                 try_tc(op, scratch, out));
+                 try_cred(op, scratch, out) || try_thinw(op, scratch, out) || try_tc(op, scratch, out));
     if (!fast) {
         out.clear();
         Launch ln = lower_generic(op);

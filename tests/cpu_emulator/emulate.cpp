@@ -156,9 +156,20 @@ bool run_gemm(const Launch& ln, Ctx& c) {
     bool o1, o2, o3;
     Buf A = resolve(ln.a, c, 0, o1), B = resolve(ln.b, c, 0, o2), C = resolve(ln.c, c, 0, o3);
     REQ(o1 && o2 && o3, "unresolved buffer");
-    REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks == (int64_t)d.mtiles * d.ntiles *
-        [&] { int64_t g = 1; for (int i = 0; i < d.ng; i++) g *= d.g_size[i]; return g; }(), "grid");
-    REQ(d.mtiles * 32 * MT >= d.M && d.ntiles * 128 >= d.N, "tiles do not cover");
+    const int64_t Gall = [&] { int64_t g = 1; for (int i = 0; i < d.ng; i++) g *= d.g_size[i]; return g; }();
+    if ((ln.kind & 0xff) == K_THIN) {
+        // one column per thread; M, K within the kernel's 16 x 16 (64 products) bounds; a
+        // block spans at most 256 / 16 + 2 batch indices (its LDS slices), flat index in 31 bits
+        const int mm = d.M <= 4 ? 4 : d.M <= 8 ? 8 : 16, kk = d.K <= 4 ? 4 : d.K <= 8 ? 8 : 16;
+        REQ(d.M <= 16 && d.K <= 16 && mm * kk <= 64 && d.N >= 16 && Gall * d.N < ((int64_t)1 << 31),
+            "thin bounds");
+        const int64_t runs = Gall * d.N;
+        REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks * 256 >= runs && (d.blocks - 1) * 256 < runs &&
+            ln.block[0] == 256, "grid");
+    } else {
+        REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks == (int64_t)d.mtiles * d.ntiles * Gall, "grid");
+        REQ(d.mtiles * 32 * MT >= d.M && d.ntiles * 128 >= d.N, "tiles do not cover");
+    }
     int64_t G = 1;
     for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
     for (int64_t g = 0; g < G; g++) {
@@ -615,6 +626,159 @@ bool run_tc_reduce(const Launch& ln, Ctx& c) {
     REQ(ok, "out-of-bounds access (tc reduce)");
     return true;
 }
+// Plane convolution contracted over one index (K_CRED forward, K_CREDW
+// partials): the kernels' thread mapping, with their LDS plane indices
+// checked against the block's allocation, in double.
+bool run_cred(const Launch& ln, Ctx& c) {
+    CredDesc d = desc_of<CredDesc>(ln);
+    const bool wgrad = (ln.kind & 0xff) == K_CREDW;
+    int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    bool o1, o2, o3;
+    Buf Z = resolve(wgrad ? ln.a : ln.b, c, 0, o1), O = resolve(wgrad ? ln.b : ln.a, c, 0, o2);
+    Buf Y = resolve(wgrad ? ln.d : ln.c, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    const int n4 = (4 + d.KW - 1 + 3) / 4, KK = d.KH * d.KW;
+    REQ(d.wchunks == (d.W + 3) / 4 && d.items == d.H * d.wchunks && d.PH == d.H + d.KH - 1 &&
+        d.PWp % 4 == 0 && d.PWp >= d.W + d.KW - 1 && d.PWp >= 4 * (d.wchunks - 1) + 4 * n4, "plane");
+    REQ(d.ch >= 0 && d.ch < d.KH && d.cw >= 0 && d.cw < d.KW && d.ng <= 2 && d.per >= 1, "pads");
+    const int64_t plane = (int64_t)d.PH * d.PWp;
+    REQ((int64_t)d.threads % 64 == 0 && d.threads <= 1024 && (int64_t)d.threads >= (int64_t)d.per * d.items &&
+        ln.block[0] == d.threads && (int64_t)ln.grid[0] == d.blocks, "grid");
+    REQ((int64_t)d.lds_bytes >= 2 * d.per * plane * 4 && d.lds_bytes <= 160 * 1024 &&
+        (!wgrad || (int64_t)d.lds_bytes >= (int64_t)d.threads * KK * 4), "lds");
+    // the last LDS word any thread writes or reads
+    const int64_t wr_max = (int64_t)(d.per - 1) * plane + (d.H - 1 + d.ch) * d.PWp + 4 * (d.wchunks - 1) + d.cw + 3;
+    const int64_t rd_max = (int64_t)(d.per - 1) * plane + (d.H - 1 + d.KH - 1) * d.PWp + 4 * (d.wchunks - 1) + 4 * n4 - 1;
+    REQ(d.per * plane + std::max(wr_max, rd_max) < 2 * d.per * plane, "lds range");
+    if (!wgrad) REQ(d.blocks * d.per >= d.G && (d.blocks - 1) * d.per < d.G, "grid (batch)");
+    else REQ(d.nrb * d.per >= d.R && (d.nrb - 1) * d.per < d.R && d.gchunk >= 1 &&
+             d.blocks == d.nrb * ((d.G + d.gchunk - 1) / d.gchunk), "grid (ranks)");
+    bool ok = true;
+    auto offs = [&](int64_t g, int64_t& oz, int64_t& oy) {
+        oz = oy = 0;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            const int64_t x = g % d.g_size[i];
+            g /= d.g_size[i];
+            oz += x * d.g_sZ[i];
+            oy += x * d.g_sY[i];
+        }
+    };
+    // Z at in-plane position (h, w) of batch offset oz and rank r, zero outside
+    auto zat = [&](int64_t oz, int64_t r, int64_t h, int64_t w) -> double {
+        if (h < 0 || h >= d.H || w < 0 || w >= d.W) return 0.0;
+        return ld(Z, tIn, oz + r * d.z_sr + h * d.W + w, ok);
+    };
+    if (!wgrad) {
+        for (int64_t b = 0; b < d.blocks; b++)
+            for (int64_t gl = 0; gl < d.per; gl++) {
+                const int64_t g = b * d.per + gl;
+                if (g >= d.G) continue;
+                int64_t oz, oy;
+                offs(g, oz, oy);
+                for (int64_t oh = 0; oh < d.H; oh++)
+                    for (int64_t ow = 0; ow < d.W; ow++) {
+                        double acc = 0;
+                        for (int64_t r = 0; r < d.R; r++)
+                            for (int jh = 0; jh < d.KH; jh++)
+                                for (int jw = 0; jw < d.KW; jw++)
+                                    acc += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) *
+                                           ld(O, tIn, r * d.f_sr + jh * d.f_sh + jw * d.f_sw, ok);
+                        st(Y, tC, oy + oh * d.W + ow, (float)acc, ok);
+                    }
+            }
+        REQ(ok, "out-of-bounds access (cred)");
+        return true;
+    }
+    for (int64_t b = 0; b < d.blocks; b++) {
+        const int64_t rgi = b % d.nrb, gci = b / d.nrb;
+        const int64_t g0 = gci * d.gchunk, g1 = std::min(d.G, g0 + d.gchunk);
+        for (int64_t rl = 0; rl < d.per; rl++) {
+            const int64_t r = rgi * d.per + rl;
+            if (r >= d.R) continue;
+            std::vector<double> acc(KK, 0.0);
+            for (int64_t g = g0; g < g1; g++) {
+                int64_t oz, oy;
+                offs(g, oz, oy);
+                for (int64_t oh = 0; oh < d.H; oh++)
+                    for (int64_t ow = 0; ow < d.W; ow++) {
+                        const double dy = ld(O, tIn, oy + oh * d.W + ow, ok);
+                        for (int jh = 0; jh < d.KH; jh++)
+                            for (int jw = 0; jw < d.KW; jw++)
+                                acc[jh * d.KW + jw] += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) * dy;
+                    }
+            }
+            for (int k = 0; k < KK; k++) st(Y, 0, (gci * d.R + r) * KK + k, (float)acc[k], ok);
+        }
+    }
+    REQ(ok, "out-of-bounds access (credw)");
+    return true;
+}
+// Small-output contraction over a long reduction: per-block partials over
+// the block's outer rows (K_THINW), then the ordered chunk sum (K_THINW_REDUCE).
+bool run_thinw(const Launch& ln, Ctx& c) {
+    ThinwDesc d = desc_of<ThinwDesc>(ln);
+    const bool red = (ln.kind & 0xff) == K_THINW_REDUCE;
+    int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    const int MM = d.M <= 4 ? 4 : d.M <= 8 ? 8 : 16, NN = d.N <= 4 ? 4 : d.N <= 8 ? 8 : 16;
+    REQ(d.M >= 1 && d.N >= 1 && d.M <= 16 && d.N <= 16 && MM * NN <= 64 && d.ng <= 3 && d.no <= 3, "thinw dims");
+    int64_t G = 1, Ko = 1;
+    for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
+    for (int i = 0; i < d.no; i++) Ko *= d.o_size[i];
+    REQ(G == d.G && Ko == d.Kout && d.Kin >= 1 && d.orows >= 1 && d.orows <= 512 &&
+        d.orows * d.Kin < ((int64_t)1 << 31) && d.kchunks == (d.Kout + d.orows - 1) / d.orows &&
+        d.blocks == d.G * d.kchunks, "thinw split");
+    bool ok = true, o1, o2;
+    Buf Pt = resolve(ln.d, c, 0, o1);
+    REQ(o1, "unresolved buffer");
+    if (red) {
+        Buf Cb = resolve(ln.c, c, 0, o2);
+        REQ(o2, "unresolved buffer");
+        REQ((int64_t)ln.grid[0] * 256 >= d.G * d.M * d.N && ln.block[0] == 256, "grid");
+        for (int64_t g = 0; g < d.G; g++)
+            for (int m = 0; m < d.M; m++)
+                for (int n = 0; n < d.N; n++) {
+                    double acc = 0;
+                    for (int64_t kc = 0; kc < d.kchunks; kc++)
+                        acc += ld(Pt, 0, (g * d.kchunks + kc) * (MM * NN) + m * NN + n, ok);
+                    int64_t off = m * d.sCm + n * d.sCn, x = g;
+                    for (int i = d.ng - 1; i >= 0; --i) { off += (x % d.g_size[i]) * d.g_sC[i]; x /= d.g_size[i]; }
+                    st(Cb, tC, off, (float)acc, ok);
+                }
+        REQ(ok, "out-of-bounds access (thinw reduce)");
+        return true;
+    }
+    Buf P = resolve(ln.a, c, 0, o1), Q = resolve(ln.b, c, 0, o2);
+    REQ(o1 && o2, "unresolved buffer");
+    REQ((int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
+    for (int64_t b = 0; b < d.blocks; b++) {
+        const int64_t g = b / d.kchunks, kc = b % d.kchunks;
+        int64_t gP = 0, gQ = 0, x = g;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            const int64_t y = x % d.g_size[i];
+            x /= d.g_size[i];
+            gP += y * d.g_sP[i];
+            gQ += y * d.g_sQ[i];
+        }
+        std::vector<double> acc(MM * NN, 0.0);
+        for (int64_t o = kc * d.orows; o < std::min(d.Kout, (kc + 1) * d.orows); o++) {
+            int64_t sp = 0, sq = 0, y = o;
+            for (int i = d.no - 1; i >= 0; --i) {
+                const int64_t z = y % d.o_size[i];
+                y /= d.o_size[i];
+                sp += z * d.o_sP[i];
+                sq += z * d.o_sQ[i];
+            }
+            for (int64_t i = 0; i < d.Kin; i++)
+                for (int m = 0; m < d.M; m++) {
+                    const double a = ld(P, tIn, gP + sp + i + m * d.sPm, ok);
+                    for (int n = 0; n < d.N; n++) acc[m * NN + n] += a * ld(Q, tIn, gQ + sq + i + n * d.sQn, ok);
+                }
+        }
+        for (int q = 0; q < MM * NN; q++) st(Pt, 0, b * MM * NN + q, (float)acc[q], ok);
+        REQ(ok, "out-of-bounds access (thinw)");
+    }
+    return true;
+}
 }  // namespace
 
 extern "C" {
@@ -656,7 +820,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                 return 3;
             }
             bool ok = generic ? run_generic(ln, c)
-                    : v == K_GEMM ? run_gemm(ln, c)
+                    : (v == K_GEMM || v == K_THIN) ? run_gemm(ln, c)
                     : v == K_WGRAD ? run_wgrad(ln, c)
                     : v == K_REDUCE ? run_reduce(ln, c)
                     : v == K_DW ? run_dw(ln, c)
@@ -666,6 +830,8 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
+                    : (v == K_CRED || v == K_CREDW) ? run_cred(ln, c)
+                    : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }
         }

@@ -120,6 +120,10 @@ PARITY_WORKLOADS = {
     "C5as": rcp_layer("C5as", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 15),
     "C5as_f32": rcp_layer("C5as_f32", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "f32", 15),
     "C5bs": rcp_layer("C5bs", 2, (4, 4, 8), (4, 4, 8), 11, 11, 64, 5, "bf16", 16),
+    # enough reduction per rank for the streaming factor-gradient kernel
+    # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
+    "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
+    "C5cs_f32": rcp_layer("C5cs_f32", 16, (2, 2, 4), (2, 2, 4), 16, 16, 8, 5, "f32", 20),
 }
 
 
