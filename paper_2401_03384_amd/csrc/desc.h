@@ -55,6 +55,7 @@ enum KernelKind : int32_t {
     K_CREDW = 28,           // filter-tap partials of the same convolution (CredDesc)
     K_THINW = 29,           // small-output contraction over a long reduction (ThinwDesc)
     K_THINW_REDUCE = 30,    // ordered sum of its partials (ThinwDesc)
+    K_CREDW_REDUCE = 31,    // ordered sum of the K_CREDW partials (CredDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -159,25 +160,29 @@ struct TcDesc {
 };
 
 // Convolution of a stack of planes contracted over one shared index:
-//   C[u][p] = sum_s sum_j Z[u][s][p + j - c] * O[s][j]
-// over 2-D positions p (output) and j (reduction), Z zero outside its plane.
-// Two instances, both with the plane held in LDS with its zero halo:
+//   C[u][m][p] = sum_s sum_j Z[u][s][p + j - c] * O[m][s][j]
+// over 2-D positions p (output) and j (reduction), Z zero outside its plane,
+// m < M <= 16 a channel of O only.  Two instances, both with the plane held
+// in LDS with its zero halo:
 //   K_CRED  (forward): p runs over an H x W output plane, j over KH x KW
 //           filter taps; u = batch (up to two dims), s = rank (one dim);
-//           O = the filter F[s][jh][jw].
+//           O = the filter F[m][s][jh][jw].
 //   K_CREDW (filter gradient): p runs over KH x KW taps, j over the H x W
 //           plane; u = rank (one dim), s = batch (up to two dims); O = the
-//           output gradient; writes per-chunk partials P[chunk][u][tap].
+//           output gradient; writes partials P[chunk][u][m][tap], summed in
+//           chunk order by K_CREDW_REDUCE.
 // Planes (Z, the output of K_CRED, O of K_CREDW) are dense: row stride W,
 // unit columns.  ch, cw: zero padding before the first row / column.
 struct CredDesc {
     int32_t H, W, KH, KW, ch, cw;
     int32_t PH, PWp, wchunks, items;   // LDS plane (rows, padded row pitch); 4-pixel items
-    int32_t ng, per;                   // batch dims; planes per block
+    int32_t ng, per, M, pad_;          // batch dims; planes per block; channels m
     int64_t R, G;                      // rank count; batch count
     int64_t g_size[2], g_sZ[2], g_sY[2];
-    int64_t z_sr, f_sr, f_sh, f_sw;    // K_CRED: F strides; K_CREDW: f_sr = 0
-    int64_t gchunk, nrb;               // K_CREDW: batch indices per block, rank groups
+    int64_t z_sr, f_sr, f_sh, f_sw;    // K_CRED: F strides
+    int64_t o_sm, y_sm;                // m strides: of O; of the output (K_CRED)
+    int64_t c_sm, c_sr, c_sh, c_sw;    // K_CREDW_REDUCE: output strides
+    int64_t gchunk, nrb, nchunks;      // K_CREDW: batch indices per block, rank groups, chunks
     int64_t blocks;
     uint32_t lds_bytes, threads;
 };

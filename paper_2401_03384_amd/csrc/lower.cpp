@@ -612,9 +612,9 @@ bool try_thinw(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out
 }
 
 // ---- plane convolution contracted over one index ---------------------------
-//   C[u][p] = sum_s sum_j Z[u][s][p + j - c] * O[s][j]
+//   C[u][m][p] = sum_s sum_j Z[u][s][p + j - c] * O[m][s][j],  M <= 16
 // Forward (p = output pixels, j = taps) runs as K_CRED; the filter gradient
-// (p = taps, j = pixels) as K_CREDW plus an ordered partial sum.
+// (p = taps, j = pixels) as K_CREDW plus an ordered chunk sum.
 bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     if (!op.has_r || op.convs.size() != 2 || op.L.dtype != op.R.dtype) return false;
     const int zside = op.convs[0].aL != 0 ? 0 : 1;
@@ -669,13 +669,16 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
             }
         }
     };
-    // u: C's non-convolved labels (in Z only); s: the reduced ones (in Z and O)
-    std::vector<Dm> U, S;
+    // u: C's labels in Z only; m: C's labels in O only (strides in O, C);
+    // s: the reduced ones (in Z and O)
+    std::vector<Dm> U, S, Mv;
     for (size_t k = 0; k < C.labels.size(); k++) {
         const int l = C.labels[k];
         if (is_conv(l)) continue;
-        if (!Z.has(l) || O.has(l)) return false;
-        U.push_back({C.dims[k], Z.stride_of(l), C.strides[k]});
+        const bool inZ = Z.has(l), inO = O.has(l);
+        if (inZ && !inO) U.push_back({C.dims[k], Z.stride_of(l), C.strides[k]});
+        else if (inO && !inZ) Mv.push_back({C.dims[k], O.stride_of(l), C.strides[k]});
+        else return false;
     }
     for (size_t k = 0; k < Z.labels.size(); k++) {
         const int l = Z.labels[k];
@@ -687,10 +690,14 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
         if (!is_conv(l) && !C.has(l) && !Z.has(l)) return false;
     merge(U);
     merge(S);
+    merge(Mv);
     // the batch dims (forward: u, gradient: s) and the single rank dim
     std::vector<Dm>& Bd = wgrad ? S : U;
     std::vector<Dm>& Rd = wgrad ? U : S;
-    if (Bd.size() > 2 || Rd.size() > 1) return false;
+    if (Bd.size() > 2 || Rd.size() > 1 || Mv.size() > 1) return false;
+    const int64_t M = Mv.empty() ? 1 : Mv[0].size;
+    const int MO = M == 1 ? 1 : M <= 4 ? 4 : M <= 8 ? 8 : 16;
+    if (M > 16 || (wgrad && (MO > 8 || MO * KH * KW > 72))) return false;
     CredDesc d;
     std::memset(&d, 0, sizeof(d));
     d.H = (int32_t)H;
@@ -699,9 +706,12 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     d.KW = (int32_t)KW;
     d.ch = (int32_t)pch;
     d.cw = (int32_t)pcw;
+    d.M = (int32_t)M;
+    d.o_sm = Mv.empty() ? 0 : Mv[0].s1;
     d.wchunks = (int32_t)cdiv(W, 4);
     d.items = (int32_t)(H * d.wchunks);
-    if (d.items > 1024) return false;
+    const int maxthreads = wgrad && MO >= 4 ? 512 : 1024;
+    if (d.items > maxthreads) return false;
     const int n4 = (int)cdiv(4 + KW - 1, 4);
     d.PH = (int32_t)(H + KH - 1);
     d.PWp = (int32_t)(cdiv(std::max<int64_t>(W + KW - 1, 4 * (d.wchunks - 1) + 4 * n4), 4) * 4);
@@ -716,26 +726,32 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     d.R = Rd.empty() ? 1 : Rd[0].size;
     d.z_sr = Rd.empty() ? 0 : Rd[0].s1;
     const int64_t plane = (int64_t)d.PH * d.PWp;
-    const int maxper = 1024 / d.items;
+    const int maxper = maxthreads / d.items;
     if (!wgrad) {
+        if (C.dtype != Z.dtype) return false;
         d.f_sr = Rd.empty() ? 0 : Rd[0].s2;
         d.f_sh = O.stride_of(ch.label);
         d.f_sw = O.stride_of(cw.label);
+        d.y_sm = Mv.empty() ? 0 : Mv[0].s2;
         // batch indices per block: enough blocks to fill the chip first
         d.per = (int32_t)std::max<int64_t>(1, std::min<int64_t>(maxper, d.G / 1024));
         while (d.per > 1 && 2 * d.per * plane * 4 > 64 * 1024) d.per--;
         d.blocks = cdiv(d.G, d.per);
     } else {
-        if (C.stride_of(ch.label) != KW * C.stride_of(cw.label)) return false;
-        // ranks per block: the largest divisor of R that fits 1024 threads
+        d.c_sm = Mv.empty() ? 0 : Mv[0].s2;
+        d.c_sr = Rd.empty() ? 0 : Rd[0].s2;
+        d.c_sh = C.stride_of(ch.label);
+        d.c_sw = C.stride_of(cw.label);
+        // ranks per block: the largest divisor of R that fits the block
         int64_t per = std::min<int64_t>(maxper, d.R);
         while (per > 1 && d.R % per) per--;
         while (per > 1 && 2 * per * plane * 4 > 96 * 1024) per--;
         d.per = (int32_t)per;
         d.nrb = cdiv(d.R, per);
-        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(2048, d.nrb)));
+        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(1024, d.nrb)));
         d.gchunk = cdiv(d.G, chunks);
-        d.blocks = d.nrb * cdiv(d.G, d.gchunk);
+        d.nchunks = cdiv(d.G, d.gchunk);
+        d.blocks = d.nrb * d.nchunks;
     }
     if (d.blocks > 0x7fffffff) return false;
     d.threads = (uint32_t)(cdiv((int64_t)d.per * d.items, 64) * 64);
@@ -743,7 +759,7 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     if (wgrad) lds = std::max<int64_t>(lds, (int64_t)d.threads * KH * KW * 4);
     if (lds > 160 * 1024) return false;
     d.lds_bytes = (uint32_t)lds;
-    const std::string shape = std::to_string(KH) + ", " + std::to_string(KW);
+    const std::string shape = std::to_string(KH) + ", " + std::to_string(KW) + ", " + std::to_string(MO) + ">";
     Launch ln;
     ln.grid[0] = (uint32_t)d.blocks;
     ln.block[0] = d.threads;
@@ -754,34 +770,26 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
         ln.b = Z.buf;
         ln.c = C.buf;
         set_desc(ln, d);
-        ln.kname = std::string("cred<") + tname(Z.dtype) + ", " + tname(C.dtype) + ", " + shape + ">";
+        ln.kname = std::string("cred<") + tname(Z.dtype) + ", " + shape;
         out.push_back(ln);
         return true;
     }
-    const int64_t nsplit = cdiv(d.G, d.gchunk);
-    const BufRef part = scratch.alloc((size_t)(nsplit * d.R * KH * KW * 4));
+    const BufRef part = scratch.alloc((size_t)(d.nchunks * d.R * M * KH * KW * 4));
     ln.kind = K_CREDW | dt_bits(Z.dtype, Z.dtype, DT_F32);
     ln.a = Z.buf;
     ln.b = O.buf;
     ln.d = part;
     set_desc(ln, d);
-    ln.kname = std::string("credw<") + tname(Z.dtype) + ", " + shape + ">";
+    ln.kname = std::string("credw<") + tname(Z.dtype) + ", " + shape;
     out.push_back(ln);
-    ReduceDesc rd;
-    std::memset(&rd, 0, sizeof(rd));
-    rd.M = (int32_t)d.R;
-    rd.N = (int32_t)(KH * KW);
-    rd.nsplit = nsplit;
-    rd.sCm = Rd.empty() ? 0 : Rd[0].s2;
-    rd.sCn = C.stride_of(cw.label);
     Launch lr;
-    lr.kind = K_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+    lr.kind = K_CREDW_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
     lr.d = part;
     lr.c = C.buf;
-    lr.grid[0] = (uint32_t)cdiv(d.R * KH * KW, 64);
+    lr.grid[0] = (uint32_t)cdiv(d.R * M * KH * KW, 64);   // 64 outputs per block
     lr.block[0] = 256;
-    set_desc(lr, rd);
-    lr.kname = std::string("reduce_partials<") + tname(C.dtype) + ">";
+    set_desc(lr, d);
+    lr.kname = std::string("credw_reduce<") + tname(C.dtype) + ">";
     out.push_back(lr);
     return true;
 }

@@ -627,22 +627,44 @@ bool run_tc_reduce(const Launch& ln, Ctx& c) {
     return true;
 }
 // Plane convolution contracted over one index (K_CRED forward, K_CREDW
-// partials): the kernels' thread mapping, with their LDS plane indices
-// checked against the block's allocation, in double.
+// partials, K_CREDW_REDUCE chunk sum): the kernels' thread mapping, with
+// their LDS plane indices checked against the block's allocation, in double.
 bool run_cred(const Launch& ln, Ctx& c) {
     CredDesc d = desc_of<CredDesc>(ln);
-    const bool wgrad = (ln.kind & 0xff) == K_CREDW;
+    const int kind = ln.kind & 0xff;
+    const bool wgrad = kind == K_CREDW;
     int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
-    bool o1, o2, o3;
+    const int KK = d.KH * d.KW, MO = d.M == 1 ? 1 : d.M <= 4 ? 4 : d.M <= 8 ? 8 : 16;
+    REQ(d.M >= 1 && d.M <= 16, "channels");
+    bool ok = true, o1, o2, o3;
+    if (kind == K_CREDW_REDUCE) {
+        Buf Pb = resolve(ln.d, c, 0, o1), Cb = resolve(ln.c, c, 0, o2);
+        REQ(o1 && o2, "unresolved buffer");
+        const int64_t per_chunk = d.R * d.M * KK;
+        REQ((int64_t)ln.grid[0] * 64 >= per_chunk && ln.block[0] == 256, "grid");   // 64 outputs per block
+        for (int64_t r = 0; r < d.R; r++)
+            for (int m = 0; m < d.M; m++)
+                for (int k = 0; k < KK; k++) {
+                    double sum = 0;
+                    for (int64_t ck = 0; ck < d.nchunks; ck++)
+                        sum += ld(Pb, 0, ck * per_chunk + (r * d.M + m) * KK + k, ok);
+                    st(Cb, tC, m * d.c_sm + r * d.c_sr + (k / d.KW) * d.c_sh + (k % d.KW) * d.c_sw, (float)sum, ok);
+                }
+        REQ(ok, "out-of-bounds access (credw reduce)");
+        return true;
+    }
     Buf Z = resolve(wgrad ? ln.a : ln.b, c, 0, o1), O = resolve(wgrad ? ln.b : ln.a, c, 0, o2);
     Buf Y = resolve(wgrad ? ln.d : ln.c, c, 0, o3);
     REQ(o1 && o2 && o3, "unresolved buffer");
-    const int n4 = (4 + d.KW - 1 + 3) / 4, KK = d.KH * d.KW;
+    REQ(wgrad || tIn == tC, "forward output type");
+    REQ(!wgrad || (KK <= 25 && MO <= 8 && MO * KK <= 72), "gradient registers");
+    const int n4 = (4 + d.KW - 1 + 3) / 4;
     REQ(d.wchunks == (d.W + 3) / 4 && d.items == d.H * d.wchunks && d.PH == d.H + d.KH - 1 &&
         d.PWp % 4 == 0 && d.PWp >= d.W + d.KW - 1 && d.PWp >= 4 * (d.wchunks - 1) + 4 * n4, "plane");
     REQ(d.ch >= 0 && d.ch < d.KH && d.cw >= 0 && d.cw < d.KW && d.ng <= 2 && d.per >= 1, "pads");
     const int64_t plane = (int64_t)d.PH * d.PWp;
-    REQ((int64_t)d.threads % 64 == 0 && d.threads <= 1024 && (int64_t)d.threads >= (int64_t)d.per * d.items &&
+    const uint32_t maxthreads = wgrad && MO >= 4 ? 512 : 1024;   // the kernels' launch bounds
+    REQ((int64_t)d.threads % 64 == 0 && d.threads <= maxthreads && (int64_t)d.threads >= (int64_t)d.per * d.items &&
         ln.block[0] == d.threads && (int64_t)ln.grid[0] == d.blocks, "grid");
     REQ((int64_t)d.lds_bytes >= 2 * d.per * plane * 4 && d.lds_bytes <= 160 * 1024 &&
         (!wgrad || (int64_t)d.lds_bytes >= (int64_t)d.threads * KK * 4), "lds");
@@ -652,8 +674,7 @@ bool run_cred(const Launch& ln, Ctx& c) {
     REQ(d.per * plane + std::max(wr_max, rd_max) < 2 * d.per * plane, "lds range");
     if (!wgrad) REQ(d.blocks * d.per >= d.G && (d.blocks - 1) * d.per < d.G, "grid (batch)");
     else REQ(d.nrb * d.per >= d.R && (d.nrb - 1) * d.per < d.R && d.gchunk >= 1 &&
-             d.blocks == d.nrb * ((d.G + d.gchunk - 1) / d.gchunk), "grid (ranks)");
-    bool ok = true;
+             d.nchunks == (d.G + d.gchunk - 1) / d.gchunk && d.blocks == d.nrb * d.nchunks, "grid (ranks)");
     auto offs = [&](int64_t g, int64_t& oz, int64_t& oy) {
         oz = oy = 0;
         for (int i = d.ng - 1; i >= 0; --i) {
@@ -675,16 +696,17 @@ bool run_cred(const Launch& ln, Ctx& c) {
                 if (g >= d.G) continue;
                 int64_t oz, oy;
                 offs(g, oz, oy);
-                for (int64_t oh = 0; oh < d.H; oh++)
-                    for (int64_t ow = 0; ow < d.W; ow++) {
-                        double acc = 0;
-                        for (int64_t r = 0; r < d.R; r++)
-                            for (int jh = 0; jh < d.KH; jh++)
-                                for (int jw = 0; jw < d.KW; jw++)
-                                    acc += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) *
-                                           ld(O, tIn, r * d.f_sr + jh * d.f_sh + jw * d.f_sw, ok);
-                        st(Y, tC, oy + oh * d.W + ow, (float)acc, ok);
-                    }
+                for (int m = 0; m < d.M; m++)
+                    for (int64_t oh = 0; oh < d.H; oh++)
+                        for (int64_t ow = 0; ow < d.W; ow++) {
+                            double acc = 0;
+                            for (int64_t r = 0; r < d.R; r++)
+                                for (int jh = 0; jh < d.KH; jh++)
+                                    for (int jw = 0; jw < d.KW; jw++)
+                                        acc += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) *
+                                               ld(O, tIn, m * d.o_sm + r * d.f_sr + jh * d.f_sh + jw * d.f_sw, ok);
+                            st(Y, tC, oy + m * d.y_sm + oh * d.W + ow, (float)acc, ok);
+                        }
             }
         REQ(ok, "out-of-bounds access (cred)");
         return true;
@@ -695,24 +717,26 @@ bool run_cred(const Launch& ln, Ctx& c) {
         for (int64_t rl = 0; rl < d.per; rl++) {
             const int64_t r = rgi * d.per + rl;
             if (r >= d.R) continue;
-            std::vector<double> acc(KK, 0.0);
+            std::vector<double> acc((size_t)d.M * KK, 0.0);
             for (int64_t g = g0; g < g1; g++) {
                 int64_t oz, oy;
                 offs(g, oz, oy);
-                for (int64_t oh = 0; oh < d.H; oh++)
-                    for (int64_t ow = 0; ow < d.W; ow++) {
-                        const double dy = ld(O, tIn, oy + oh * d.W + ow, ok);
-                        for (int jh = 0; jh < d.KH; jh++)
-                            for (int jw = 0; jw < d.KW; jw++)
-                                acc[jh * d.KW + jw] += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) * dy;
-                    }
+                for (int m = 0; m < d.M; m++)
+                    for (int64_t oh = 0; oh < d.H; oh++)
+                        for (int64_t ow = 0; ow < d.W; ow++) {
+                            const double dy = ld(O, tIn, oy + m * d.o_sm + oh * d.W + ow, ok);
+                            for (int jh = 0; jh < d.KH; jh++)
+                                for (int jw = 0; jw < d.KW; jw++)
+                                    acc[m * KK + jh * d.KW + jw] += zat(oz, r, oh + jh - d.ch, ow + jw - d.cw) * dy;
+                        }
             }
-            for (int k = 0; k < KK; k++) st(Y, 0, (gci * d.R + r) * KK + k, (float)acc[k], ok);
+            for (int q = 0; q < d.M * KK; q++) st(Y, 0, (gci * d.R + r) * d.M * KK + q, (float)acc[q], ok);
         }
     }
     REQ(ok, "out-of-bounds access (credw)");
     return true;
 }
+
 // Small-output contraction over a long reduction: per-block partials over
 // the block's outer rows (K_THINW), then the ordered chunk sum (K_THINW_REDUCE).
 bool run_thinw(const Launch& ln, Ctx& c) {
@@ -830,7 +854,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
-                    : (v == K_CRED || v == K_CREDW) ? run_cred(ln, c)
+                    : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
                     : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }

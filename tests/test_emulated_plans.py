@@ -88,6 +88,7 @@ CASES = {
     "C5at": W.rcp_layer("C5at", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "bf16", 23),
     "C5at_f32": W.rcp_layer("C5at_f32", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "f32", 23),
     "C5bt": W.rcp_layer("C5bt", 1, (2, 2, 4), (2, 2, 4), 9, 8, 16, 5, "bf16", 24),
+    "C4m": W.rtt_layer("C4m", 1, (4, 4, 8), (4, 4, 8), 5, 7, 16, 3, "f32", 26),
     "C5cs": W.PARITY_WORKLOADS["C5cs"],
     "C5cs_f32": W.PARITY_WORKLOADS["C5cs_f32"],
 }
