@@ -12,12 +12,24 @@ typedef uint16_t bf16_t;   // raw bfloat16 bit pattern
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
 
-// float32 -> bfloat16, round to nearest even (quiet NaN kept a NaN).
+// float32 -> bfloat16, round to nearest even (a NaN stays a NaN): gfx950's
+// hardware conversion.
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
+    const __bf16 h = (__bf16)f;
+    bf16_t u;
+    __builtin_memcpy(&u, &h, 2);
+    return u;
+}
+
+// two float32 -> one word of two bfloat16 (lo in the low half), one
+// conversion instruction
+__device__ __forceinline__ uint32_t pk_bf16(float lo, float hi) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    const b2 r = __builtin_convertvector((f2){lo, hi}, b2);
+    uint32_t u;
+    __builtin_memcpy(&u, &r, 4);
+    return u;
 }
 
 __device__ __forceinline__ void store(float* p, int64_t i, float v) { p[i] = v; }

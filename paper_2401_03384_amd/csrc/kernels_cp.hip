@@ -43,6 +43,16 @@ __device__ __forceinline__ bf16x8 pack8(const bf16_t* v) {
     return r;
 }
 
+// eight float32 -> bf16x8 by four paired conversions
+__device__ __forceinline__ bf16x8 cvt8(const float* v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) w[i] = pk_bf16(v[2 * i], v[2 * i + 1]);
+    bf16x8 r;
+    __builtin_memcpy(&r, w, 16);
+    return r;
+}
+
 // Twenty wait states after an MFMA chain whose result VALU code reads next.
 // The compiler's hazard padding has been seen to miss the read of a 16-pass
 // MFMA result on a branch path that skips straight to it; this pads on every
@@ -217,10 +227,10 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         if constexpr (BF) {
 #pragma unroll
             for (int q = 0; q < 2; q++) {
-                bf16_t zb[8];
+                float zf[8];
 #pragma unroll
-                for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(z3[8 * q + j]);
-                bf16x8 bv = pack8(zb);
+                for (int j = 0; j < 8; j++) zf[j] = z3[8 * q + j];
+                bf16x8 bv = cvt8(zf);
 #pragma unroll
                 for (int mb = 0; mb < MB2; mb++) {
                     bf16x8 av = lds8(UtP + (((q * 2 + half) * TT) + mb * 32 + (lane & 31)) * 8);
@@ -301,15 +311,29 @@ hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStr
 // column held by accumulator i of a lane in half hf of a transposed tile
 __device__ __forceinline__ int tcol(int i, int hf) { return 8 * (i >> 2) + 4 * hf + (i & 3); }
 
+// a where the mask m is all ones, b where it is zero (one v_bfi_b32).  m is
+// opaque to the compiler, which would otherwise turn a lane-dependent choice
+// between two fixed elements of a register array into a dynamic index (a
+// fifteen-step compare/select chain per use).
+__device__ __forceinline__ float blend(uint32_t m, float a, float b) {
+    return __uint_as_float((__float_as_uint(a) & m) | (__float_as_uint(b) & ~m));
+}
+__device__ __forceinline__ uint32_t half_mask(int hf) {
+    uint32_t m = hf ? 0xffffffffu : 0u;
+    asm volatile("" : "+v"(m));
+    return m;
+}
+
 // w[i] = v at column tcol(i, hf) + DD of the same rank (DD = +-1); values
-// that would come from outside the 32 columns are unspecified.
+// that would come from outside the 32 columns are unspecified.  hm =
+// half_mask(hf).
 template <int DD>
-__device__ __forceinline__ f32x16 tshift(const f32x16& v, int hf) {
+__device__ __forceinline__ f32x16 tshift(const f32x16& v, uint32_t hm) {
     float snd[4], rcv[4];
 #pragma unroll
     for (int a = 0; a < 4; a++) {
-        if constexpr (DD == 1) snd[a] = hf ? v[4 * a] : v[a < 3 ? 4 * a + 4 : 0];
-        else snd[a] = hf ? v[a > 0 ? 4 * a - 1 : 0] : v[4 * a + 3];
+        if constexpr (DD == 1) snd[a] = blend(hm, v[4 * a], v[a < 3 ? 4 * a + 4 : 0]);
+        else snd[a] = blend(hm, v[a > 0 ? 4 * a - 1 : 0], v[4 * a + 3]);
     }
 #pragma unroll
     for (int a = 0; a < 4; a++) rcv[a] = __shfl_xor(snd[a], 32, 64);
@@ -336,7 +360,7 @@ __device__ __forceinline__ bf16x8 pack_words(const uint32_t* w) {
     for (int i = 0; i < 4; i++) {
         uint32_t lo = w[2 * i], hi = w[2 * i + 1];
         asm volatile("" : "+v"(lo), "+v"(hi));
-        p[i] = (lo & 0xffffu) | (hi << 16);
+        p[i] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);   // low halves of lo, hi
     }
     bf16x8 v;
     __builtin_memcpy(&v, p, 16);
@@ -468,6 +492,7 @@ __global__ void __launch_bounds__(256, 1)
     const int col = col0 + cl;                       // the lane's column (A operands, dX)
     const bool colok = col >= 0 && col < W;
     const bool ownlane = colok && cl >= CW && cl < 32 - CW;
+    const uint32_t hm = half_mask(hf);
     uint32_t own = 0;                                // own columns among tcol(i, hf)
 #pragma unroll
     for (int i = 0; i < 16; i++) {
@@ -552,8 +577,8 @@ __global__ void __launch_bounds__(256, 1)
             for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
             z2[i] = a;
         }
-        const f32x16 zm = tshift<-1>(z2, hf);
-        const f32x16 zp = tshift<1>(z2, hf);
+        const f32x16 zm = tshift<-1>(z2, hm);
+        const f32x16 zp = tshift<1>(z2, hm);
 #pragma unroll
         for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
         __builtin_amdgcn_sched_barrier(0);   // the next row's dY loads stay behind the chain
@@ -595,10 +620,10 @@ __global__ void __launch_bounds__(256, 1)
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
-                    bf16_t za[8];
+                    float zf[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((ownr >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f);
-                    const bf16x8 av = pack8(za);
+                    for (int j = 0; j < 8; j++) zf[j] = (ownr >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f;
+                    const bf16x8 av = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MT; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
@@ -623,8 +648,8 @@ __global__ void __launch_bounds__(256, 1)
         // dZ2[h]: transposed conv along w (tap j reads column - j + 1)
         f32x16 dz2;
         {
-            const f32x16 gp = tshift<1>(dz3, hf);
-            const f32x16 gm = tshift<-1>(dz3, hf);
+            const f32x16 gp = tshift<1>(dz3, hm);
+            const f32x16 gm = tshift<-1>(dz3, hm);
 #pragma unroll
             for (int i = 0; i < 16; i++) dz2[i] = kw[0] * gp[i] + kw[1] * dz3[i] + kw[2] * gm[i];
         }
@@ -663,10 +688,10 @@ __global__ void __launch_bounds__(256, 1)
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
-                    bf16_t zb[8];
+                    float zf[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) zb[j] = f32_to_bf16(Tz[cl * LZ + 16 * q + 8 * hf + j]);
-                    const bf16x8 bv = pack8(zb);
+                    for (int j = 0; j < 8; j++) zf[j] = Tz[cl * LZ + 16 * q + 8 * hf + j];
+                    const bf16x8 bv = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
                         accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf),
@@ -686,10 +711,10 @@ __global__ void __launch_bounds__(256, 1)
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
-                    bf16_t za[8];
+                    float zf[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) za[j] = f32_to_bf16((ownx >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f);
-                    const bf16x8 av = pack8(za);
+                    for (int j = 0; j < 8; j++) zf[j] = (ownx >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f;
+                    const bf16x8 av = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
                         accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack_words(&gx[n][8 * q]), accUs[n],
