@@ -76,9 +76,11 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     if (w.nslab != B * R * H || w.A != W || w.inner != 1 || w.r_div != H || w.r_size != R ||
         w.sign != 1 || w.off != -((w.K - 1) / 2))
         return false;
-    // register-resident strips: rank 32, T in {32, 64}, 3x3 or 5x5 filters
-    if (R != 32 || !(T == 32 || T == 64) || S % 32 || h.K != w.K || !(h.K == 3 || h.K == 5))
+    // register-resident strips: rank 32, S and T in {32, 64}, 3x3 or 5x5 filters
+    if (R != 32 || !(T == 32 || T == 64) || !(S == 32 || S == 64) || h.K != w.K || !(h.K == 3 || h.K == 5))
         return false;
+    // one sample of X within a 32-bit byte range (raw buffer loads)
+    if (S * a.sBk * (dt ? 2 : 4) >= (1ll << 31) || a.sBk != H * W) return false;
     CpDesc d;
     std::memset(&d, 0, sizeof(d));
     d.B = (int32_t)B;

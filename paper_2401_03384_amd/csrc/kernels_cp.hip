@@ -72,279 +72,18 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t bid, int64_t nb) {
     return x * q + (x < r ? x : r) + i;
 }
 
+// the value of lane l - 1 (lane_prev) or l + 1 (lane_next) of the wavefront;
+// zero past its ends (DPP whole-wave shifts)
+__device__ __forceinline__ float lane_prev(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x138, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float lane_next(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x130, 0xf, 0xf, true));
+}
+
 // r held by accumulator i of a lane in a 32x32 MFMA result
 __device__ __forceinline__ int row32(int i, int lane) {
     return 8 * (i >> 2) + 4 * ((lane >> 5) & 1) + (i & 3);
-}
-
-// Two blocks per CU (256 VGPRs a lane) except for the bf16 5x5 variant, whose
-// larger ring and bf16 operand packing do not fit that without spilling.
-template <typename T, int KH, int KW, int MB2>
-__global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_fwd(CpDesc d, const T* __restrict__ X,
-                                              const T* __restrict__ Us, const T* __restrict__ Kh,
-                                              const T* __restrict__ Kw, const T* __restrict__ Ut,
-                                              T* __restrict__ Y) {
-    constexpr bool BF = sizeof(T) == 2;
-    constexpr int TT = 32 * MB2;
-    constexpr int CH = (KH - 1) / 2, HWW = (KW - 1) / 2;
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    const int S = d.S, H = d.H, W = d.W;
-    const int LDA = d.lda;
-    T* UsL = (T*)smem;
-    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-
-    // ---- tables ----
-    {
-    T* UtP = (T*)(smem + d.o_ut);
-    float* KhP = (float*)(smem + d.o_kh);
-    float* KwP = (float*)(smem + d.o_kw);
-    for (int e = tid; e < 32 * S; e += 256) {
-        int r = e / S, s = e - r * S;
-        UsL[r * LDA + s] = Us[r * d.us_sr + s * d.us_ss];
-    }
-    if constexpr (BF) {
-        // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t]
-        for (int e = tid; e < 2 * 2 * TT * 8; e += 256) {
-            int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
-            UtP[e] = Ut[row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st];
-        }
-    } else {
-        // UtP[i][hf][t] = Ut[row32(i, 32*hf)][t]
-        for (int e = tid; e < 16 * 2 * TT; e += 256) {
-            int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
-            UtP[e] = Ut[row32(i, 32 * hf) * d.ut_sr + t * d.ut_st];
-        }
-    }
-    for (int e = tid; e < 16 * 2 * KH; e += 256) {
-        int j = e % KH, hf = (e / KH) & 1, i = e / (2 * KH);
-        KhP[e] = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
-    }
-    for (int e = tid; e < 16 * 2 * KW; e += 256) {
-        int j = e % KW, hf = (e / KW) & 1, i = e / (2 * KW);
-        KwP[e] = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
-    }
-    }
-    __syncthreads();
-
-    // ---- this wavefront's strip ----
-    // strips fastest: the waves of a block share halo rows and cache lines
-    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
-    if (gw >= d.waves) return;
-    const int cb = (int)(gw % d.ncb);
-    const int64_t rest = gw / d.ncb;
-    const int seg = (int)(rest % d.segs);
-    const int b = (int)(rest / d.segs);
-    const int col = cb * d.colstride - HWW + (lane & 31);
-    const bool colok = col >= 0 && col < W;
-    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
-    const T* Xc = X + (int64_t)b * d.x_sb + (colok ? col : 0);
-    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
-    const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
-
-    auto gemm1 = [&](int row) {
-        f32x16 acc;
-#pragma unroll
-        for (int i = 0; i < 16; i++) acc[i] = 0.f;
-        if (row < 0 || row >= H) return acc;   // uniform over the wave
-        const T* xr = Xc + (int64_t)row * W;
-        if constexpr (BF) {
-            for (int k = 0; k < S; k += 16) {
-                bf16_t xv[8];
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    xv[j] = colok ? xr[(int64_t)(k + 8 * half + j) * d.x_ss] : (bf16_t)0;
-                bf16x8 av = lds8(UsL + (lane & 31) * LDA + k + 8 * half);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(xv), acc, 0, 0, 0);
-            }
-        } else {
-            for (int k = 0; k < S; k += 16) {
-                float xv[8];
-#pragma unroll
-                for (int u = 0; u < 8; u++)
-                    xv[u] = colok ? xr[(int64_t)(k + 2 * u + half) * d.x_ss] : 0.f;
-#pragma unroll
-                for (int u = 0; u < 8; u++) {
-                    float av = UsL[(lane & 31) * LDA + k + 2 * u + half];
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, xv[u], acc, 0, 0, 0);
-                }
-            }
-        }
-        mfma_drain();
-        return acc;
-    };
-
-    f32x16 ring[KH];
-#pragma unroll
-    for (int j = 0; j < KH - 1; j++) ring[j] = gemm1(h0 - CH + j);
-    for (int h = h0; h < h1; h++) {
-        // The tap and Ut tables are re-read from LDS every row: the offsets
-        // pass through an empty asm so the loads are not hoisted out of the
-        // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
-        uint32_t o_ut = d.o_ut, o_kh = d.o_kh, o_kw = d.o_kw;
-        asm volatile("" : "+s"(o_ut), "+s"(o_kh), "+s"(o_kw));
-        const T* UtP = (const T*)(smem + o_ut);
-        const float* KhP = (const float*)(smem + o_kh);
-        const float* KwP = (const float*)(smem + o_kw);
-        ring[KH - 1] = gemm1(h + KH - 1 - CH);
-        // conv along h
-        f32x16 z2;
-#pragma unroll
-        for (int i = 0; i < 16; i++) {
-            float a = 0.f;
-#pragma unroll
-            for (int j = 0; j < KH; j++) a += KhP[(i * 2 + half) * KH + j] * ring[j][i];
-            z2[i] = a;
-        }
-#pragma unroll
-        for (int j = 0; j < KH - 1; j++) ring[j] = ring[j + 1];
-        // conv along w: neighbouring columns are neighbouring lanes of the half
-        f32x16 z3;
-#pragma unroll
-        for (int i = 0; i < 16; i++) {
-            float a = 0.f;
-#pragma unroll
-            for (int jw = 0; jw < KW; jw++) {
-                int dd = jw - HWW;
-                float v;
-                if (dd == 0) {
-                    v = z2[i];
-                } else {
-                    int src = (lane & 31) + dd;
-                    src = src < 0 ? 0 : (src > 31 ? 31 : src);
-                    v = __shfl(z2[i], (lane & 32) | src, 64);
-                }
-                a += KwP[(i * 2 + half) * KW + jw] * v;
-            }
-            z3[i] = a;
-        }
-        // GEMM2: Y[t][col] = sum_r Ut[r][t] Z3[r][col]
-        f32x16 acc2[MB2];
-#pragma unroll
-        for (int mb = 0; mb < MB2; mb++)
-#pragma unroll
-            for (int i = 0; i < 16; i++) acc2[mb][i] = 0.f;
-        if constexpr (BF) {
-#pragma unroll
-            for (int q = 0; q < 2; q++) {
-                float zf[8];
-#pragma unroll
-                for (int j = 0; j < 8; j++) zf[j] = z3[8 * q + j];
-                bf16x8 bv = cvt8(zf);
-#pragma unroll
-                for (int mb = 0; mb < MB2; mb++) {
-                    bf16x8 av = lds8(UtP + (((q * 2 + half) * TT) + mb * 32 + (lane & 31)) * 8);
-                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc2[mb], 0, 0, 0);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < 16; i++) {
-#pragma unroll
-                for (int mb = 0; mb < MB2; mb++) {
-                    float av = UtP[(i * 2 + half) * TT + mb * 32 + (lane & 31)];
-                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, z3[i], acc2[mb], 0, 0, 0);
-                }
-            }
-        }
-        mfma_drain();
-        if (store_lane) {
-            T* yr = Yc + (int64_t)h * W;
-#pragma unroll
-            for (int mb = 0; mb < MB2; mb++)
-#pragma unroll
-                for (int i = 0; i < 16; i++)
-                    store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
-        }
-    }
-}
-
-template <typename T, int K, int MB2>
-hipError_t launch_cp_t(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
-    auto k = cp_fwd<T, K, K, MB2>;
-    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)ops[0],
-                       (const T*)ops[1], (const T*)ops[2], (const T*)ops[3], (const T*)ops[4], (T*)y);
-    return hipGetLastError();
-}
-
-template <typename T>
-hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
-    if (d.KH == 3 && d.KW == 3)
-        return d.T == 32 ? launch_cp_t<T, 3, 1>(d, ops, y, s) : launch_cp_t<T, 3, 2>(d, ops, y, s);
-    if (d.KH == 5 && d.KW == 5)
-        return d.T == 32 ? launch_cp_t<T, 5, 1>(d, ops, y, s) : launch_cp_t<T, 5, 2>(d, ops, y, s);
-    return hipErrorInvalidValue;
-}
-
-
-// ---------------------------------------------------------------------------
-// Backward of the chain (Section 3.2: every pairwise step's two gradients, in
-// reverse order, with the intermediates recomputed), fused the same way.  One
-// wavefront walks its 32-column strip over rows h = h0-CH .. h1+CH-1 and at row h
-//   recomputes  Z1[h+CH] (ring of KH rows), Z2[h], Z3[h]
-//   dZ3[h] = Ut^T dY[h]
-//   dUt   += Z3[h] dY[h]^T               (reduction over the strip's columns)
-//   dKw   += sum_w Z2[h][w+j-c] dZ3[h][w]
-//   dZ2[h] = transposed conv along w of dZ3[h]
-//   dKh   += sum_w Z1[h+j-c][w] dZ2[h][w]
-//   dZ1[h-CH] from the ring of the last KH dZ2 rows
-//   dX[h-CH] = Us^T dZ1[h-CH]
-//   dUs   += dZ1[h-CH] X[h-CH]^T
-// Each weight-gradient term is counted once: rows in [h0, h1) and the strip's
-// own columns only.
-//
-// The rank intermediates are held transposed: the MFMA computes Z^T[col][r]
-// (A operand = the activation row, one column per lane; B operand = the factor
-// table in LDS), so a lane holds one rank r (lane % 32) and the 16 columns
-// tcol(i, half) of its accumulators.  Then
-//   * conv along h is per element, conv along w a shift of the register index
-//     (four cross-half exchanges per shift);
-//   * the column reductions of dUt / dUs take Z^T straight from the
-//     accumulators as the MFMA A operand (k slot = column);
-//   * the tap-gradient products reduce over columns inside the lane;
-//   * dX goes through one LDS transpose of dZ1 (and is stored coalesced).
-// dY reaches the dUt product through a wave-private LDS tile; the X row of the
-// dUs product is read channel-major from memory (it was read two rows earlier
-// by the same wavefront).  The operands of the next row are loaded while the
-// current row is computed.
-
-// column held by accumulator i of a lane in half hf of a transposed tile
-__device__ __forceinline__ int tcol(int i, int hf) { return 8 * (i >> 2) + 4 * hf + (i & 3); }
-
-// a where the mask m is all ones, b where it is zero (one v_bfi_b32).  m is
-// opaque to the compiler, which would otherwise turn a lane-dependent choice
-// between two fixed elements of a register array into a dynamic index (a
-// fifteen-step compare/select chain per use).
-__device__ __forceinline__ float blend(uint32_t m, float a, float b) {
-    return __uint_as_float((__float_as_uint(a) & m) | (__float_as_uint(b) & ~m));
-}
-__device__ __forceinline__ uint32_t half_mask(int hf) {
-    uint32_t m = hf ? 0xffffffffu : 0u;
-    asm volatile("" : "+v"(m));
-    return m;
-}
-
-// w[i] = v at column tcol(i, hf) + DD of the same rank (DD = +-1); values
-// that would come from outside the 32 columns are unspecified.  hm =
-// half_mask(hf).
-template <int DD>
-__device__ __forceinline__ f32x16 tshift(const f32x16& v, uint32_t hm) {
-    float snd[4], rcv[4];
-#pragma unroll
-    for (int a = 0; a < 4; a++) {
-        if constexpr (DD == 1) snd[a] = blend(hm, v[4 * a], v[a < 3 ? 4 * a + 4 : 0]);
-        else snd[a] = blend(hm, v[a > 0 ? 4 * a - 1 : 0], v[4 * a + 3]);
-    }
-#pragma unroll
-    for (int a = 0; a < 4; a++) rcv[a] = __shfl_xor(snd[a], 32, 64);
-    f32x16 w;
-#pragma unroll
-    for (int i = 0; i < 16; i++) {
-        const int b = i & 3;
-        if constexpr (DD == 1) w[i] = b < 3 ? v[i + 1] : rcv[i >> 2];
-        else w[i] = b > 0 ? v[i - 1] : rcv[i >> 2];
-    }
-    return w;
 }
 
 // A-operand slots are stored one per 32-bit word (a bf16 value zero-extended).
@@ -435,6 +174,277 @@ __device__ __forceinline__ void arow(uint32_t (&a)[K / 2], __amdgpu_buffer_rsrc_
         else
             a[u] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)(2 * u * cs), 0);
     }
+}
+
+// Two blocks per CU (256 VGPRs a lane) except for the bf16 5x5 variant, whose
+// larger ring and bf16 operand packing do not fit that without spilling.
+template <typename T, int KH, int KW, int MB2, int MS>
+__global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_fwd(CpDesc d, const T* __restrict__ X,
+                                              const T* __restrict__ Us, const T* __restrict__ Kh,
+                                              const T* __restrict__ Kw, const T* __restrict__ Ut,
+                                              T* __restrict__ Y) {
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int TT = 32 * MB2, NS = 32 * MS;
+    constexpr int CH = (KH - 1) / 2, HWW = (KW - 1) / 2;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int S = d.S, H = d.H, W = d.W;
+    const int LDA = d.lda;
+    T* UsL = (T*)smem;
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // ---- tables ----
+    {
+    T* UtP = (T*)(smem + d.o_ut);
+    float* KhP = (float*)(smem + d.o_kh);
+    float* KwP = (float*)(smem + d.o_kw);
+    for (int e = tid; e < 32 * S; e += 256) {
+        int r = e / S, s = e - r * S;
+        UsL[r * LDA + s] = Us[r * d.us_sr + s * d.us_ss];
+    }
+    if constexpr (BF) {
+        // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t]
+        for (int e = tid; e < 2 * 2 * TT * 8; e += 256) {
+            int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
+            UtP[e] = Ut[row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st];
+        }
+    } else {
+        // UtP[i][hf][t] = Ut[row32(i, 32*hf)][t]
+        for (int e = tid; e < 16 * 2 * TT; e += 256) {
+            int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
+            UtP[e] = Ut[row32(i, 32 * hf) * d.ut_sr + t * d.ut_st];
+        }
+    }
+    for (int e = tid; e < 16 * 2 * KH; e += 256) {
+        int j = e % KH, hf = (e / KH) & 1, i = e / (2 * KH);
+        KhP[e] = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
+    }
+    for (int e = tid; e < 16 * 2 * KW; e += 256) {
+        int j = e % KW, hf = (e / KW) & 1, i = e / (2 * KW);
+        KwP[e] = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
+    }
+    }
+    __syncthreads();
+
+    // ---- this wavefront's strip ----
+    // strips fastest: the waves of a block share halo rows and cache lines
+    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
+    if (gw >= d.waves) return;
+    const int cb = (int)(gw % d.ncb);
+    const int64_t rest = gw / d.ncb;
+    const int seg = (int)(rest % d.segs);
+    const int b = (int)(rest / d.segs);
+    const int col = cb * d.colstride - HWW + (lane & 31);
+    const bool colok = col >= 0 && col < W;
+    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
+    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
+    const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
+    const int cl = lane & 31;
+
+    // X rows as B-operand slots (the same slot layout as arow), loaded one row
+    // ahead through a raw buffer: rows and lanes outside the image read zeros
+    constexpr uint32_t E = sizeof(T);
+    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(NS * d.x_ss * E));
+    const uint32_t xcs = (uint32_t)(d.x_ss * E);
+    const uint32_t kOut = 0x80000000u;   // past the range: reads 0
+    const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
+    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    uint32_t xa[NS / 2];
+    // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in xa
+    auto gemm1 = [&]() {
+        f32x16 acc;
+#pragma unroll
+        for (int i = 0; i < 16; i++) acc[i] = 0.f;
+        if constexpr (BF) {
+#pragma unroll
+            for (int q = 0; q < NS / 16; q++)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsL + cl * LDA + 16 * q + 8 * half),
+                                                              pack_words(xa + 8 * q), acc, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < NS / 2; u++)
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(UsL[cl * LDA + 2 * u + half], __uint_as_float(xa[u]),
+                                                           acc, 0, 0, 0);
+        }
+        mfma_drain();
+        return acc;
+    };
+
+    f32x16 ring[KH];
+#pragma unroll
+    for (int j = 0; j < KH - 1; j++) {
+        arow<T, NS>(xa, rX, xoff(h0 - CH + j), xcs);
+        ring[j] = gemm1();
+    }
+    arow<T, NS>(xa, rX, xoff(h0 + KH - 1 - CH), xcs);
+    for (int h = h0; h < h1; h++) {
+        // The tap and Ut tables are re-read from LDS every row: the offsets
+        // pass through an empty asm so the loads are not hoisted out of the
+        // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
+        uint32_t o_ut = d.o_ut, o_kh = d.o_kh, o_kw = d.o_kw;
+        asm volatile("" : "+s"(o_ut), "+s"(o_kh), "+s"(o_kw));
+        const T* UtP = (const T*)(smem + o_ut);
+        const float* KhP = (const float*)(smem + o_kh);
+        const float* KwP = (const float*)(smem + o_kw);
+        ring[KH - 1] = gemm1();
+        arow<T, NS>(xa, rX, xoff(h + KH - CH), xcs);   // the next row's, used one row later
+        // conv along h
+        f32x16 z2;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < KH; j++) a += KhP[(i * 2 + half) * KH + j] * ring[j][i];
+            z2[i] = a;
+        }
+#pragma unroll
+        for (int j = 0; j < KH - 1; j++) ring[j] = ring[j + 1];
+        // conv along w: neighbouring columns are neighbouring lanes of the half;
+        // whole-wave lane shifts (DPP) bring lane l - 1 and l + 1; what crosses
+        // the half boundary lands in a halo column, which is never stored
+        f32x16 z3;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            float sh[KW];
+            sh[HWW] = z2[i];
+#pragma unroll
+            for (int k = 1; k <= HWW; k++) {
+                sh[HWW - k] = lane_prev(sh[HWW - k + 1]);
+                sh[HWW + k] = lane_next(sh[HWW + k - 1]);
+            }
+            float a = 0.f;
+#pragma unroll
+            for (int jw = 0; jw < KW; jw++) a += KwP[(i * 2 + half) * KW + jw] * sh[jw];
+            z3[i] = a;
+        }
+        // GEMM2: Y[t][col] = sum_r Ut[r][t] Z3[r][col]
+        f32x16 acc2[MB2];
+#pragma unroll
+        for (int mb = 0; mb < MB2; mb++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) acc2[mb][i] = 0.f;
+        if constexpr (BF) {
+#pragma unroll
+            for (int q = 0; q < 2; q++) {
+                float zf[8];
+#pragma unroll
+                for (int j = 0; j < 8; j++) zf[j] = z3[8 * q + j];
+                bf16x8 bv = cvt8(zf);
+#pragma unroll
+                for (int mb = 0; mb < MB2; mb++) {
+                    bf16x8 av = lds8(UtP + (((q * 2 + half) * TT) + mb * 32 + (lane & 31)) * 8);
+                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc2[mb], 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 16; i++) {
+#pragma unroll
+                for (int mb = 0; mb < MB2; mb++) {
+                    float av = UtP[(i * 2 + half) * TT + mb * 32 + (lane & 31)];
+                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, z3[i], acc2[mb], 0, 0, 0);
+                }
+            }
+        }
+        mfma_drain();
+        if (store_lane) {
+            T* yr = Yc + (int64_t)h * W;
+#pragma unroll
+            for (int mb = 0; mb < MB2; mb++)
+#pragma unroll
+                for (int i = 0; i < 16; i++)
+                    store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
+        }
+    }
+}
+
+template <typename T, int K, int MB2>
+hipError_t launch_cp_t(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
+    if (d.S != 32 && d.S != 64) return hipErrorInvalidValue;
+    auto k = d.S == 32 ? cp_fwd<T, K, K, MB2, 1> : cp_fwd<T, K, K, MB2, 2>;
+    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)ops[0],
+                       (const T*)ops[1], (const T*)ops[2], (const T*)ops[3], (const T*)ops[4], (T*)y);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
+    if (d.KH == 3 && d.KW == 3)
+        return d.T == 32 ? launch_cp_t<T, 3, 1>(d, ops, y, s) : launch_cp_t<T, 3, 2>(d, ops, y, s);
+    if (d.KH == 5 && d.KW == 5)
+        return d.T == 32 ? launch_cp_t<T, 5, 1>(d, ops, y, s) : launch_cp_t<T, 5, 2>(d, ops, y, s);
+    return hipErrorInvalidValue;
+}
+
+
+// ---------------------------------------------------------------------------
+// Backward of the chain (Section 3.2: every pairwise step's two gradients, in
+// reverse order, with the intermediates recomputed), fused the same way.  One
+// wavefront walks its 32-column strip over rows h = h0-CH .. h1+CH-1 and at row h
+//   recomputes  Z1[h+CH] (ring of KH rows), Z2[h], Z3[h]
+//   dZ3[h] = Ut^T dY[h]
+//   dUt   += Z3[h] dY[h]^T               (reduction over the strip's columns)
+//   dKw   += sum_w Z2[h][w+j-c] dZ3[h][w]
+//   dZ2[h] = transposed conv along w of dZ3[h]
+//   dKh   += sum_w Z1[h+j-c][w] dZ2[h][w]
+//   dZ1[h-CH] from the ring of the last KH dZ2 rows
+//   dX[h-CH] = Us^T dZ1[h-CH]
+//   dUs   += dZ1[h-CH] X[h-CH]^T
+// Each weight-gradient term is counted once: rows in [h0, h1) and the strip's
+// own columns only.
+//
+// The rank intermediates are held transposed: the MFMA computes Z^T[col][r]
+// (A operand = the activation row, one column per lane; B operand = the factor
+// table in LDS), so a lane holds one rank r (lane % 32) and the 16 columns
+// tcol(i, half) of its accumulators.  Then
+//   * conv along h is per element, conv along w a shift of the register index
+//     (four cross-half exchanges per shift);
+//   * the column reductions of dUt / dUs take Z^T straight from the
+//     accumulators as the MFMA A operand (k slot = column);
+//   * the tap-gradient products reduce over columns inside the lane;
+//   * dX goes through one LDS transpose of dZ1 (and is stored coalesced).
+// dY reaches the dUt product through a wave-private LDS tile; the X row of the
+// dUs product is read channel-major from memory (it was read two rows earlier
+// by the same wavefront).  The operands of the next row are loaded while the
+// current row is computed.
+
+// column held by accumulator i of a lane in half hf of a transposed tile
+__device__ __forceinline__ int tcol(int i, int hf) { return 8 * (i >> 2) + 4 * hf + (i & 3); }
+
+// a where the mask m is all ones, b where it is zero (one v_bfi_b32).  m is
+// opaque to the compiler, which would otherwise turn a lane-dependent choice
+// between two fixed elements of a register array into a dynamic index (a
+// fifteen-step compare/select chain per use).
+__device__ __forceinline__ float blend(uint32_t m, float a, float b) {
+    return __uint_as_float((__float_as_uint(a) & m) | (__float_as_uint(b) & ~m));
+}
+__device__ __forceinline__ uint32_t half_mask(int hf) {
+    uint32_t m = hf ? 0xffffffffu : 0u;
+    asm volatile("" : "+v"(m));
+    return m;
+}
+
+// w[i] = v at column tcol(i, hf) + DD of the same rank (DD = +-1); values
+// that would come from outside the 32 columns are unspecified.  hm =
+// half_mask(hf).
+template <int DD>
+__device__ __forceinline__ f32x16 tshift(const f32x16& v, uint32_t hm) {
+    float snd[4], rcv[4];
+#pragma unroll
+    for (int a = 0; a < 4; a++) {
+        if constexpr (DD == 1) snd[a] = blend(hm, v[4 * a], v[a < 3 ? 4 * a + 4 : 0]);
+        else snd[a] = blend(hm, v[a > 0 ? 4 * a - 1 : 0], v[4 * a + 3]);
+    }
+#pragma unroll
+    for (int a = 0; a < 4; a++) rcv[a] = __shfl_xor(snd[a], 32, 64);
+    f32x16 w;
+#pragma unroll
+    for (int i = 0; i < 16; i++) {
+        const int b = i & 3;
+        if constexpr (DD == 1) w[i] = b < 3 ? v[i + 1] : rcv[i >> 2];
+        else w[i] = b > 0 ? v[i - 1] : rcv[i >> 2];
+    }
+    return w;
 }
 
 template <typename T, int KH, int KW, int MT, int MS>
