@@ -220,6 +220,11 @@ struct CpBwdDesc {
     int64_t waves, blocks;
     uint32_t lds_bytes, o_uta, o_ust, o_tz, o_yt, yt_bytes, red_bytes;
     int32_t lda_s, lda_t, ldu, ly;
+    // per-wave ring of the last three X rows (channel-major, row pitch lx);
+    // the dZ1 transpose tile of a wave sits at o_tz + wave * tz_stride (it may
+    // share the wave's dY tile: o_tz == o_yt, tz_stride == yt_bytes)
+    uint32_t o_xl, xl_bytes, tz_stride;
+    int32_t lx;
 };
 
 }  // namespace ce

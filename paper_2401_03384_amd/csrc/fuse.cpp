@@ -146,16 +146,26 @@ void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     d.lda_t = bf ? d.T + 8 : d.T + 1;
     d.ldu = bf ? 32 + 8 : 0;
     d.ly = bf ? 40 : 33;
+    d.lx = bf ? 40 : 36;   // 8-byte (bf16) / 16-byte (fp32) column runs stay aligned
     size_t o = al16((size_t)32 * d.lda_s * e);
     d.o_uta = (uint32_t)o;
     o = al16(o + (size_t)32 * d.lda_t * e);
     d.o_ust = (uint32_t)o;
     if (bf) o = al16(o + (size_t)d.S * d.ldu * 2);
+    const size_t tz = (size_t)32 * 33 * 4, yt = al16((size_t)d.T * d.ly * e);
+    const size_t xl = al16((size_t)3 * d.S * d.lx * e);
+    // the dZ1 transpose tile gets its own space when everything fits, else it
+    // shares the wave's dY tile (used earlier in each row)
+    const bool share = o + 4 * (tz + yt + xl) > (size_t)160 * 1024;
     d.o_tz = (uint32_t)o;
-    o += (size_t)4 * 32 * 33 * 4;
+    d.tz_stride = (uint32_t)(share ? std::max(tz, yt) : tz);
+    if (!share) o += 4 * tz;
     d.o_yt = (uint32_t)o;
-    d.yt_bytes = (uint32_t)al16((size_t)d.T * d.ly * e);
+    d.yt_bytes = (uint32_t)(share ? d.tz_stride : yt);
     o += (size_t)4 * d.yt_bytes;
+    d.o_xl = (uint32_t)o;
+    d.xl_bytes = (uint32_t)xl;
+    o += 4 * xl;
     d.red_bytes = (uint32_t)(4 * std::max<size_t>({(size_t)4 * 32 * d.S, (size_t)4 * 32 * d.T,
                                                    (size_t)8 * 32 * (d.KH + d.KW)}));
     d.lds_bytes = (uint32_t)std::max<size_t>(al16(o), d.red_bytes);

@@ -484,8 +484,9 @@ __global__ void __launch_bounds__(256, 1)
         }
     }
     __syncthreads();
-    float* Tz = (float*)(smem + d.o_tz) + wave * (32 * LZ);
+    float* Tz = (float*)(smem + d.o_tz + (size_t)wave * d.tz_stride);
     T* Yt = (T*)(smem + d.o_yt + (size_t)wave * d.yt_bytes);
+    T* Xl = (T*)(smem + d.o_xl + (size_t)wave * d.xl_bytes);   // ring of 3 X rows [slot][s][col]
 
     // ---- this wavefront's strip (waves past the end run no rows) ----
     const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
@@ -553,11 +554,23 @@ __global__ void __launch_bounds__(256, 1)
     const uint32_t dx0 = ownlane ? (uint32_t)(col * (int)E) : kOut;
     constexpr int PW = Slots<T>::per_word;
     uint32_t xa[NS / 2 / PW], ya[NT / 2 / PW];
+    // the X row held in xa into ring slot `slot` (channel-major), for the dUs
+    // product CH rows later; X row r sits in slot (r - (hs - CH)) % 3
+    const int lx = d.lx;
+    auto xl_put = [&](int slot) {
+        T* dst = Xl + slot * NS * lx + cl;
+#pragma unroll
+        for (int u = 0; u < NS / 2; u++) {
+            if constexpr (BF) dst[achan<BF>(u, hf) * lx] = (T)xa[u];
+            else dst[achan<BF>(u, hf) * lx] = __uint_as_float(xa[u]);
+        }
+    };
     if (wok) {
 #pragma unroll
         for (int j = 0; j < KH - 1; j++) {
             arow<T, NS>(xa, rX, xoff(hs - CH + j), xcs);
             ring[j] = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+            xl_put(j);
         }
         arow<T, NS>(xa, rX, xoff(hs + CH), xcs);
         arow<T, NT>(ya, rY, yoff(hs), ycs);
@@ -572,8 +585,10 @@ __global__ void __launch_bounds__(256, 1)
         const int hx = h - CH;
         const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
         const uint32_t ownr = rin ? own : 0u, ownx = xin ? own : 0u;
+        const int k = h - hs;   // ring slots: X row h + CH goes to (k + 2) % 3, row hx is read from k % 3
         // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
         const f32x16 z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+        xl_put((k + 2) % 3);
         arow<T, NS>(xa, rX, xoff(h + 1 + CH), xcs);
         const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, d.lda_t, cl, hf);
         ring[KH - 1] = z1n;
@@ -601,22 +616,6 @@ __global__ void __launch_bounds__(256, 1)
         }
         arow<T, NT>(ya, rY, yoff(h + 1), ycs);
         mfma_drain();   // dz3 is read below
-        // X row hx, channel-major, for the dUs product (issued here, used last)
-        uint32_t gx[MS][16];
-        {
-            // whole offset per lane (range-checked); columns outside the image
-            // read a neighbour or 0 and are masked by `own` in the product
-#pragma unroll
-            for (int n = 0; n < MS; n++) {
-                const uint32_t v0 = (uint32_t)(32 * n + cl) * xcs + (uint32_t)((hx * W + col0 + 4 * hf) * (int)E);
-#pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const int vi = (int)(v0 + (uint32_t)((8 * (i >> 2) + (i & 3)) * E));
-                    if constexpr (BF) gx[n][i] = __builtin_amdgcn_raw_buffer_load_b16(rX, vi, 0, 0);
-                    else gx[n][i] = __builtin_amdgcn_raw_buffer_load_b32(rX, vi, 0, 0);
-                }
-            }
-        }
         {
             // dKw products
 #pragma unroll
@@ -687,7 +686,9 @@ __global__ void __launch_bounds__(256, 1)
             dr[j] = dr[j + 1];
         }
         {
-            // dX[hx] = Us^T dZ1[hx]: dZ1 through the LDS tile Tz[col][r]
+            // dX[hx] = Us^T dZ1[hx]: dZ1 through the LDS tile Tz[col][r], which
+            // may share the dY tile: every read of that precedes these writes
+            asm volatile("" ::: "memory");
 #pragma unroll
             for (int i = 0; i < 16; i++) Tz[tcol(i, hf) * LZ + cl] = dz1[i];
             f32x16 accX[MS];
@@ -717,7 +718,8 @@ __global__ void __launch_bounds__(256, 1)
                                                                        accX[n], 0, 0, 0);
                 }
             }
-            // dUs += dZ1[hx] X[hx]^T
+            // dUs += dZ1[hx] X[hx]^T, X row hx from its ring slot (channel 32n + cl)
+            const T* xrow = Xl + (k % 3) * NS * lx + cl * lx;
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
@@ -726,18 +728,34 @@ __global__ void __launch_bounds__(256, 1)
                     for (int j = 0; j < 8; j++) zf[j] = (ownx >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f;
                     const bf16x8 av = cvt8(zf);
 #pragma unroll
-                    for (int n = 0; n < MS; n++)
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack_words(&gx[n][8 * q]), accUs[n],
-                                                                           0, 0, 0);
+                    for (int n = 0; n < MS; n++) {
+                        // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
+                        const bf16_t* xr = xrow + (32 * n) * lx + 16 * q + 4 * hf;
+                        bf16_t bv[8];
+                        __builtin_memcpy(bv, xr, 8);
+                        __builtin_memcpy(bv + 4, xr + 8, 8);
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(bv), accUs[n], 0, 0, 0);
+                    }
                 }
             } else {
+                // columns tcol(i, hf) = 8(i/4) + 4hf + i%4: four aligned runs of four
+                float xv[MS][16];
+#pragma unroll
+                for (int n = 0; n < MS; n++)
+#pragma unroll
+                    for (int a = 0; a < 4; a++) {
+                        const float4 t = *reinterpret_cast<const float4*>(xrow + (32 * n) * lx + 8 * a + 4 * hf);
+                        xv[n][4 * a] = t.x;
+                        xv[n][4 * a + 1] = t.y;
+                        xv[n][4 * a + 2] = t.z;
+                        xv[n][4 * a + 3] = t.w;
+                    }
 #pragma unroll
                 for (int i = 0; i < 16; i++) {
                     const float av = (ownx >> i) & 1 ? dz1[i] : 0.f;
 #pragma unroll
                     for (int n = 0; n < MS; n++)
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(gx[n][i]), accUs[n],
-                                                                        0, 0, 0);
+                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, xv[n][i], accUs[n], 0, 0, 0);
                 }
             }
             mfma_drain();   // accX is read by the stores

@@ -423,9 +423,17 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
     REQ(!bf || (d.ldu >= 32 + 8 && (d.ldu * 2) % 16 == 0), "UsT rows");
     REQ(d.o_tz >= d.o_ust + (bf ? (uint64_t)d.S * d.ldu * 2 : 0) && d.o_tz % 16 == 0, "tile offset");
     REQ(d.ly >= 32 + (bf ? 8 : 1) && (!bf || (d.ly * 2) % 8 == 0), "dY tile rows");
-    REQ(d.o_yt >= d.o_tz + (uint64_t)4 * 32 * 33 * 4 && d.o_yt % 16 == 0 &&
-        d.yt_bytes >= (uint64_t)d.T * d.ly * e && d.yt_bytes % 16 == 0, "dY tiles");
-    REQ(d.lds_bytes >= d.o_yt + 4 * (uint64_t)d.yt_bytes, "LDS tiles");
+    REQ(d.yt_bytes >= (uint64_t)d.T * d.ly * e && d.yt_bytes % 16 == 0 && d.o_yt % 16 == 0, "dY tiles");
+    REQ(d.tz_stride >= 32 * 33 * 4 && d.tz_stride % 16 == 0, "transpose tiles");
+    if (d.o_tz == d.o_yt)   // the transpose tile shares the wave's dY tile
+        REQ(d.tz_stride == d.yt_bytes, "shared tiles");
+    else
+        REQ(d.o_yt >= d.o_tz + 4 * (uint64_t)d.tz_stride, "tile regions");
+    // X-row rings: three rows of S channels, aligned column runs
+    REQ(d.lx >= 32 + (bf ? 8 : 4) && (d.lx * e) % (bf ? 8 : 16) == 0 && d.o_xl % 16 == 0 &&
+        d.xl_bytes >= 3 * (uint64_t)d.S * d.lx * e && d.xl_bytes % 16 == 0, "X rings");
+    REQ(d.o_xl >= d.o_yt + 4 * (uint64_t)d.yt_bytes && d.lds_bytes >= d.o_xl + 4 * (uint64_t)d.xl_bytes,
+        "LDS tiles");
     REQ(d.red_bytes >= (uint64_t)4 * std::max({(uint64_t)4 * 32 * d.S, (uint64_t)4 * 32 * d.T,
                                                (uint64_t)8 * 32 * (d.KH + d.KW)}) &&
         d.lds_bytes >= d.red_bytes && d.lds_bytes <= 160 * 1024 && ln.lds == d.lds_bytes, "LDS size");
