@@ -56,6 +56,7 @@ enum KernelKind : int32_t {
     K_THINW = 29,           // small-output contraction over a long reduction (ThinwDesc)
     K_THINW_REDUCE = 30,    // ordered sum of its partials (ThinwDesc)
     K_CREDW_REDUCE = 31,    // ordered sum of the K_CREDW partials (CredDesc)
+    K_REDUCE_MULTI = 32,    // up to four ordered partial sums in one launch (MultiReduceDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -95,6 +96,15 @@ struct ReduceDesc {
     int32_t M, N;
     int64_t nsplit;
     int64_t sCm, sCn;
+};
+
+// Up to four independent ordered sums (ReduceDesc each, fp32 outputs) in one
+// launch: part j owns blocks [block0[j], block0[j+1]); a part whose output
+// pointer is null (gradient not requested) is skipped.
+struct MultiReduceDesc {
+    int32_t n, pad_;
+    ReduceDesc part[4];
+    int64_t block0[5];
 };
 
 // Depthwise convolution along one axis of a dense tensor viewed as

@@ -51,6 +51,15 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
             for (int i = 0; i < 8; i++) ops[3 + i] = resolve(ln.extra[i], P);
             return launch_cp_bwd(ln, ops, s);
         }
+        case K_REDUCE_MULTI: {
+            const void* parts[4] = {};
+            void* outs[4] = {};
+            for (size_t j = 0; j < 4 && 2 * j + 1 < ln.extra.size(); j++) {
+                parts[j] = resolve(ln.extra[2 * j], P);
+                outs[j] = resolve(ln.extra[2 * j + 1], P);
+            }
+            return launch_reduce_multi(ln, parts, outs, s);
+        }
         default: return launch_fast(ln, a, b, c, d, s);
     }
 }

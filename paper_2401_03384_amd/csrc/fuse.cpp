@@ -171,29 +171,6 @@ void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     d.lds_bytes = (uint32_t)std::max<size_t>(al16(o), d.red_bytes);
 }
 
-void reduce_launch(BufRef part, BufRef out, int64_t M, int64_t N, int64_t nsplit, int64_t sCm,
-                   int64_t sCn, uint32_t need, const std::string& what, std::vector<Launch>& v) {
-    ReduceDesc rd;
-    std::memset(&rd, 0, sizeof(rd));
-    rd.M = (int32_t)M;
-    rd.N = (int32_t)N;
-    rd.nsplit = nsplit;
-    rd.sCm = sCm;
-    rd.sCn = sCn;
-    Launch lr;
-    lr.kind = K_REDUCE;   // fp32 partials into an fp32 gradient
-    lr.d = part;
-    lr.c = out;
-    lr.grid[0] = (uint32_t)((M * N + 63) / 64);
-    lr.block[0] = 256;
-    lr.desc.resize(sizeof(rd));
-    std::memcpy(lr.desc.data(), &rd, sizeof(rd));
-    lr.need = need;
-    lr.what = what;
-    lr.kname = "reduce_partials<float>";
-    lr.alg_bytes = 4.0 * (double)(nsplit * M * N + M * N);
-    v.push_back(lr);
-}
 
 }  // namespace
 
@@ -268,10 +245,33 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
                   4.0 * (double)nb * R * (d.S + d.T + d.KH + d.KW);
     m.alg_flops = 2.0 * f.alg_flops;   // backward MACs are twice the forward's
     out.push_back(m);
-    reduce_launch(Pus, din(us), R, d.S, nb, c.us_sr, c.us_ss, 1u << us.index, "dUs: sum of block partials", out);
-    reduce_launch(Put, din(ut), R, d.T, nb, c.ut_sr, c.ut_st, 1u << ut.index, "dUt: sum of block partials", out);
-    reduce_launch(Pkh, din(kh), R, d.KH, nb, c.kh_sr, c.kh_sj, 1u << kh.index, "dKh: sum of block partials", out);
-    reduce_launch(Pkw, din(kw), R, d.KW, nb, c.kw_sr, c.kw_sj, 1u << kw.index, "dKw: sum of block partials", out);
+    // the four factor gradients: ordered sums of the block partials, one launch
+    MultiReduceDesc md;
+    std::memset(&md, 0, sizeof(md));
+    md.n = 4;
+    const int64_t dims[4][4] = {{d.S, c.us_sr, c.us_ss, 0}, {d.T, c.ut_sr, c.ut_st, 0},
+                                {d.KH, c.kh_sr, c.kh_sj, 0}, {d.KW, c.kw_sr, c.kw_sj, 0}};
+    for (int j = 0; j < 4; j++) {
+        ReduceDesc& rd = md.part[j];
+        rd.M = (int32_t)R;
+        rd.N = (int32_t)dims[j][0];
+        rd.nsplit = nb;
+        rd.sCm = dims[j][1];
+        rd.sCn = dims[j][2];
+        md.block0[j + 1] = md.block0[j] + (R * dims[j][0] + 63) / 64;
+    }
+    Launch lr;
+    lr.kind = K_REDUCE_MULTI;
+    lr.extra = {Pus, din(us), Put, din(ut), Pkh, din(kh), Pkw, din(kw)};
+    lr.grid[0] = (uint32_t)md.block0[4];
+    lr.block[0] = 256;
+    lr.desc.resize(sizeof(md));
+    std::memcpy(lr.desc.data(), &md, sizeof(md));
+    lr.need = (1u << us.index) | (1u << ut.index) | (1u << kh.index) | (1u << kw.index);
+    lr.what = "dUs, dUt, dKh, dKw: sums of block partials";
+    lr.kname = "reduce_multi";
+    lr.alg_bytes = 4.0 * (double)nb * R * (d.S + d.T + d.KH + d.KW) + 4.0 * R * (d.S + d.T + d.KH + d.KW);
+    out.push_back(lr);
     return true;
 }
 

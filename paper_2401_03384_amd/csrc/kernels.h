@@ -14,6 +14,10 @@ hipError_t launch_generic(const Launch& ln, const void* a, const void* b, void* 
 hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, void* d,
                        hipStream_t s);
 
+// Up to four ordered partial sums (K_REDUCE_MULTI, MultiReduceDesc): parts[j]
+// the fp32 partials, outs[j] the fp32 output (null: skipped).
+hipError_t launch_reduce_multi(const Launch& ln, const void* const* parts, void* const* outs, hipStream_t s);
+
 // Small-output contraction over a long reduction (K_THINW / K_THINW_REDUCE,
 // ThinwDesc): p, q = the operands, part = fp32 partials, c = the output.
 hipError_t launch_thinw(const Launch& ln, const void* p, const void* q, void* part, void* c, hipStream_t s);

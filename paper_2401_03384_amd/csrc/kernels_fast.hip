@@ -318,12 +318,11 @@ __global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ 
 // lane); its 4 wavefronts sum contiguous quarters of s with 8 loads in
 // flight, then the quarters are added in a fixed order.
 template <typename TC>
-__global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float* __restrict__ part,
-                                                       TC* __restrict__ C) {
-    __shared__ double q[4][64];
+__device__ __forceinline__ void reduce_block(const ReduceDesc& d, const float* __restrict__ part,
+                                             TC* __restrict__ C, int64_t blk, double (*q)[64]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t mn = (int64_t)d.M * d.N;
-    const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t e = blk * 64 + lane;
     const int64_t per = (d.nsplit + 3) / 4;
     const int64_t s0 = wave * per, s1 = min(d.nsplit, s0 + per);
     double acc = 0.0;
@@ -345,6 +344,26 @@ __global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float
         int64_t m = e / d.N, n = e - m * d.N;
         store(C, m * d.sCm + n * d.sCn, (float)t);
     }
+}
+
+template <typename TC>
+__global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float* __restrict__ part,
+                                                       TC* __restrict__ C) {
+    __shared__ double q[4][64];
+    reduce_block(d, part, C, blockIdx.x, q);
+}
+
+struct MultiPtrs {
+    const float* part[4];
+    float* out[4];
+};
+
+__global__ void __launch_bounds__(256) reduce_multi(MultiReduceDesc d, MultiPtrs p) {
+    __shared__ double q[4][64];
+    int j = 0;
+    while (j + 1 < d.n && blockIdx.x >= d.block0[j + 1]) j++;
+    if (!p.out[j]) return;   // uniform over the block
+    reduce_block(d.part[j], p.part[j], p.out[j], blockIdx.x - d.block0[j], q);
 }
 
 // ---------------------------------------------------------------------------
@@ -518,6 +537,22 @@ hipError_t launch_wgrad(const Launch& ln, const void* a, const void* b, void* pa
     }
     return hipGetLastError();
 }
+
+}  // namespace
+
+hipError_t launch_reduce_multi(const Launch& ln, const void* const* parts, void* const* outs, hipStream_t s) {
+    MultiReduceDesc d = desc_of<MultiReduceDesc>(ln);
+    if (d.n < 1 || d.n > 4 || (int64_t)ln.grid[0] != d.block0[d.n]) return hipErrorInvalidValue;
+    MultiPtrs p;
+    for (int j = 0; j < 4; j++) {
+        p.part[j] = j < d.n ? (const float*)parts[j] : nullptr;
+        p.out[j] = j < d.n ? (float*)outs[j] : nullptr;
+    }
+    hipLaunchKernelGGL(reduce_multi, dim3(ln.grid[0]), dim3(256), 0, s, d, p);
+    return hipGetLastError();
+}
+
+namespace {
 
 hipError_t launch_reduce(const Launch& ln, const void* part, void* c, hipStream_t s) {
     ReduceDesc d = desc_of<ReduceDesc>(ln);

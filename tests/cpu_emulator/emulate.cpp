@@ -242,6 +242,29 @@ bool run_reduce(const Launch& ln, Ctx& c) {
     return true;
 }
 
+// Up to four ordered sums in one launch (K_REDUCE_MULTI): part j owns blocks
+// [block0[j], block0[j+1]), 64 outputs a block.
+bool run_reduce_multi(const Launch& ln, Ctx& c) {
+    MultiReduceDesc d = desc_of<MultiReduceDesc>(ln);
+    REQ(d.n >= 1 && d.n <= 4 && ln.extra.size() == (size_t)(2 * d.n) && d.block0[0] == 0 &&
+        (int64_t)ln.grid[0] == d.block0[d.n] && ln.block[0] == 256, "multi-reduce shape");
+    for (int j = 0; j < d.n; j++) {
+        const ReduceDesc& r = d.part[j];
+        REQ((d.block0[j + 1] - d.block0[j]) * 64 >= (int64_t)r.M * r.N &&
+            (d.block0[j + 1] - d.block0[j] - 1) * 64 < (int64_t)r.M * r.N, "multi-reduce blocks");
+        bool o1, o2, ok = true;
+        Buf P = resolve(ln.extra[2 * j], c, 0, o1), C = resolve(ln.extra[2 * j + 1], c, 0, o2);
+        REQ(o1 && o2, "unresolved buffer");
+        for (int64_t e = 0; e < (int64_t)r.M * r.N; e++) {
+            double acc = 0;
+            for (int64_t s2 = 0; s2 < r.nsplit; s2++) acc += ld(P, 0, s2 * r.M * r.N + e, ok);
+            st(C, 0, (e / r.N) * r.sCm + (e % r.N) * r.sCn, (float)acc, ok);
+        }
+        REQ(ok, "out-of-bounds (multi-reduce)");
+    }
+    return true;
+}
+
 bool run_dw(const Launch& ln, Ctx& c) {
     DwDesc d = desc_of<DwDesc>(ln);
     int tIn = (ln.kind >> kBitIn) & 1, tF = (ln.kind >> kBitAux) & 1, tC = (ln.kind >> kBitOut) & 1;
@@ -855,6 +878,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : (v == K_GEMM || v == K_THIN) ? run_gemm(ln, c)
                     : v == K_WGRAD ? run_wgrad(ln, c)
                     : v == K_REDUCE ? run_reduce(ln, c)
+                    : v == K_REDUCE_MULTI ? run_reduce_multi(ln, c)
                     : v == K_DW ? run_dw(ln, c)
                     : v == K_DW_TAPGRAD ? run_tapgrad(ln, c)
                     : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
