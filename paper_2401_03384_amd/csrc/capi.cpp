@@ -110,7 +110,11 @@ ce_status ce_plan_workspace_size(const ce_plan* p, int for_backward, size_t* byt
     });
 }
 
-const char* ce_plan_describe(const ce_plan* p) { return p ? p->text.c_str() : ""; }
+const char* ce_plan_describe(const ce_plan* p) {
+    if (!p) return "";
+    std::call_once(p->text_once, [p] { p->text = ce::describe_plan(*p); });
+    return p->text.c_str();
+}
 
 void ce_plan_destroy(ce_plan* p) { delete p; }
 

@@ -541,10 +541,6 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
     }
     DType dt = dtype == CE_BF16 ? DT_BF16 : DT_F32;
     int m = (int)p->steps.size();
-    std::ostringstream txt;
-    txt << "conv_einsum plan: " << n << " operands, " << m << " steps, "
-        << (mode == CE_COST_FWD ? "fwd" : "train_paper") << " cost " << p->total_cost
-        << ", forward MACs " << p->fwd_macs << ", left-to-right " << p->ltr_cost << "\n";
 
     if (p->executable) {
         // Workspace items: intermediates (id = node), their gradients
@@ -684,6 +680,22 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             }
             return bld.tensor_of(node, gdt, b);
         };
+        // A plan that is exactly one fused CP chain gets the fused backward
+        // (and the unfused backward is not lowered at all).
+        bool fused_bwd = false;
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) && p->fwd.size() == 1 &&
+            (p->fwd[0].kind & 0xff) == K_CP_FWD) {
+            std::vector<WsItem> fitems;
+            ItemScratch fsc;
+            fsc.items = &fitems;
+            fsc.next = SCRATCH_ID;
+            std::vector<Launch> v;
+            if (fuse_cp_backward(p->fwd[0], E.feature_operand, fsc, v)) {
+                p->bwd.swap(v);
+                bitems.swap(fitems);
+                fused_bwd = true;
+            }
+        }
         ItemScratch bs;
         bs.items = &bitems;
         bs.next = SCRATCH_ID;
@@ -697,7 +709,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.what = "unary bwd";
             for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
-        for (int s = 0; s + 1 < m; s++) {
+        for (int s = 0; !fused_bwd && s + 1 < m; s++) {
             const Step& st = p->steps[s];
             PairOp op;
             op.L = bval(st.a);
@@ -709,7 +721,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             bs.t = s;
             for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
-        for (int s = m - 1; s >= 0; s--) {
+        for (int s = m - 1; !fused_bwd && s >= 0; s--) {
             const Step& st = p->steps[s];
             TensorRef dC = bgrad(st.c);
             bs.t = T(s);
@@ -738,34 +750,30 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
             }
         }
-        // A plan that is exactly one fused CP chain gets the fused backward.
-        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) && p->fwd.size() == 1 &&
-            (p->fwd[0].kind & 0xff) == K_CP_FWD) {
-            std::vector<WsItem> fitems;
-            ItemScratch fsc;
-            fsc.items = &fitems;
-            fsc.next = SCRATCH_ID;
-            std::vector<Launch> v;
-            if (fuse_cp_backward(p->fwd[0], E.feature_operand, fsc, v)) {
-                p->bwd.swap(v);
-                bitems.swap(fitems);
-            }
-        }
         drop_unused(bitems, p->bwd);
         p->ws_bwd = pack(bitems);
         patch(p->bwd, bitems);
     }
-    for (int s = 0; s < m; s++) {
-        const Step& st = p->steps[s];
-        txt << "  step " << s << ": " << mask_str(p->nodes[st.a].mask) << " x "
-            << mask_str(p->nodes[st.b].mask) << "  macs " << st.macs << "\n";
-    }
-    txt << "  workspace fwd " << p->ws_fwd << " B, bwd " << p->ws_bwd << " B\n";
-    for (auto& l : p->fwd) txt << "  fwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
-    for (auto& l : p->bwd) txt << "  bwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
-    if (!p->executable) txt << "  not executable: " << p->why_not << "\n";
-    p->text = txt.str();
     return p.release();
+}
+
+// The plan's description (built on first request, not on every plan).
+std::string describe_plan(const ce_plan& p) {
+    const int m = (int)p.steps.size();
+    std::ostringstream txt;
+    txt << "conv_einsum plan: " << p.e.n << " operands, " << m << " steps, "
+        << (p.mode == CE_COST_FWD ? "fwd" : "train_paper") << " cost " << p.total_cost
+        << ", forward MACs " << p.fwd_macs << ", left-to-right " << p.ltr_cost << "\n";
+    for (int s = 0; s < m; s++) {
+        const Step& st = p.steps[s];
+        txt << "  step " << s << ": " << mask_str(p.nodes[st.a].mask) << " x "
+            << mask_str(p.nodes[st.b].mask) << "  macs " << st.macs << "\n";
+    }
+    txt << "  workspace fwd " << p.ws_fwd << " B, bwd " << p.ws_bwd << " B\n";
+    for (auto& l : p.fwd) txt << "  fwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
+    for (auto& l : p.bwd) txt << "  bwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
+    if (!p.executable) txt << "  not executable: " << p.why_not << "\n";
+    return txt.str();
 }
 
 }  // namespace ce

@@ -2,6 +2,7 @@
 // lowering for the forward and backward passes, workspace layout.
 #pragma once
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -93,7 +94,9 @@ struct ce_plan {
     size_t ws_fwd = 0, ws_bwd = 0;
     bool executable = true;
     std::string why_not;
-    std::string text;
+    // description, built once on first request (plans are shared across threads)
+    mutable std::once_flag text_once;
+    mutable std::string text;
 };
 
 namespace ce {
@@ -102,6 +105,9 @@ namespace ce {
 // given by `pairs` (opt_einsum path format, n_pairs = n_in - 1).
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
                    bool use_path, const int* pairs, int n_pairs);
+
+// Text description of a plan (steps, costs, workspace, launches).
+std::string describe_plan(const ce_plan& p);
 
 // Exposed for tests of the search: cost of merging operand sets A and B.
 uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode);
