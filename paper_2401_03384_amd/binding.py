@@ -7,6 +7,7 @@ of any kind.
 from __future__ import annotations
 
 import ctypes as C
+import functools
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -109,12 +110,24 @@ def ce_version() -> str:
     return lib().ce_version().decode()
 
 
-def ce_expr_parse(spec: str, shapes) -> int:
-    shapes = [tuple(int(d) for d in s) for s in shapes]
+@functools.lru_cache(maxsize=256)
+def _shape_args(shapes: tuple):
+    """ctypes arrays for a tuple of shapes (kept alive by the cache)."""
     n = len(shapes)
     ranks = (C.c_int * n)(*[len(s) for s in shapes])
     bufs = [(C.c_int64 * max(1, len(s)))(*s) for s in shapes]
     dims = (C.POINTER(C.c_int64) * n)(*[C.cast(b, C.POINTER(C.c_int64)) for b in bufs])
+    return n, ranks, bufs, dims
+
+
+@functools.lru_cache(maxsize=256)
+def _ptr_array(ptrs: tuple):
+    """A void* array of the given addresses (None for a null pointer)."""
+    return (C.c_void_p * len(ptrs))(*ptrs)
+
+
+def ce_expr_parse(spec: str, shapes) -> int:
+    n, ranks, _, dims = _shape_args(tuple(tuple(int(d) for d in s) for s in shapes))
     out = C.c_void_p()
     _check(lib().ce_expr_parse(spec.encode(), n, ranks, dims, C.byref(out)))
     return out.value
@@ -189,16 +202,14 @@ def ce_plan_destroy(p: int) -> None:
 
 
 def ce_forward(p: int, in_ptrs, out_ptr: int, ws_ptr: int, ws_bytes: int, stream: int) -> None:
-    n = len(in_ptrs)
-    arr = (C.c_void_p * n)(*in_ptrs)
+    arr = _ptr_array(tuple(in_ptrs))
     _check(lib().ce_forward(p, arr, out_ptr, ws_ptr or None, ws_bytes, stream or None))
 
 
 def ce_backward(p: int, in_ptrs, dout_ptr: int, din_ptrs, ws_ptr: int, ws_bytes: int,
                 stream: int) -> None:
-    n = len(in_ptrs)
-    arr = (C.c_void_p * n)(*in_ptrs)
-    darr = (C.c_void_p * n)(*[d or None for d in din_ptrs])
+    arr = _ptr_array(tuple(in_ptrs))
+    darr = _ptr_array(tuple(d or None for d in din_ptrs))
     _check(lib().ce_backward(p, arr, dout_ptr, darr, ws_ptr or None, ws_bytes, stream or None))
 
 
