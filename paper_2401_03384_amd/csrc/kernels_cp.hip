@@ -43,6 +43,16 @@ __device__ __forceinline__ bf16x8 pack8(const bf16_t* v) {
     return r;
 }
 
+// v where m is all ones, zero where it is zero
+__device__ __forceinline__ bf16x8 mask8(bf16x8 v, uint32_t m) {
+    uint32_t w[4];
+    __builtin_memcpy(w, &v, 16);
+#pragma unroll
+    for (int i = 0; i < 4; i++) w[i] &= m;
+    __builtin_memcpy(&v, w, 16);
+    return v;
+}
+
 // eight float32 -> bf16x8 by four paired conversions
 __device__ __forceinline__ bf16x8 cvt8(const float* v) {
     uint32_t w[4];
@@ -504,12 +514,15 @@ __global__ void __launch_bounds__(256, 1)
     const bool colok = col >= 0 && col < W;
     const bool ownlane = colok && cl >= CW && cl < 32 - CW;
     const uint32_t hm = half_mask(hf);
-    uint32_t own = 0;                                // own columns among tcol(i, hf)
-#pragma unroll
-    for (int i = 0; i < 16; i++) {
-        const int c = tcol(i, hf), g = col0 + c;
-        if (c >= CW && c < 32 - CW && g >= 0 && g < W) own |= 1u << i;
-    }
+    // v with the strip-overlap columns zeroed: column 0 is accumulator 0 of the
+    // lower lane half, column 31 accumulator 15 of the upper (one column of
+    // overlap on each side: KW == 3)
+    auto own_cols = [hm](const f32x16& v) {
+        f32x16 w = v;
+        w[0] = blend(hm, v[0], 0.f);
+        w[15] = blend(~hm, v[15], 0.f);
+        return w;
+    };
     constexpr uint32_t E = sizeof(T);
     // one sample of X / dY / dX (fits a 32-bit byte range; checked by the planner)
     const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(d.S * d.x_ss * E));
@@ -577,14 +590,19 @@ __global__ void __launch_bounds__(256, 1)
     }
 
     // One row of the walk, branch-free so that the compiler can overlap the
-    // convolution arithmetic with the MFMA chains.  Row h counts for dUt, dKw
-    // and dKh only inside the segment (rin), row h - CH for dX and dUs (xin);
-    // outside, the products run on zeroed operands and the dX stores go past
-    // the buffer's range (dropped).
+    // convolution arithmetic with the MFMA chains.  Ownership of the weight-
+    // gradient terms: loads outside the image read zeros, so every product
+    // there vanishes by itself (dY = 0 makes dZ3 = 0, X = 0 makes Z1 = 0);
+    // what remains is the strip overlap (columns 0 and 31, zeroed by own_cols)
+    // and the segment halo rows: row h counts for dUt, dKw and dKh only inside
+    // the segment (rin), row h - CH for dX and dUs (xin).  The row flags
+    // scale the tap sums and mask the packed MFMA operands; the dX stores of
+    // a halo row go past the buffer's range (dropped).
     auto row_step = [&](int h) {
         const int hx = h - CH;
         const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
-        const uint32_t ownr = rin ? own : 0u, ownx = xin ? own : 0u;
+        const float rf = rin ? 1.f : 0.f;
+        const uint32_t rmask = rin ? 0xffffffffu : 0u, xmask = xin ? 0xffffffffu : 0u;
         const int k = h - hs;   // ring slots: X row h + CH goes to (k + 2) % 3, row hx is read from k % 3
         // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
         const f32x16 z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
@@ -618,21 +636,26 @@ __global__ void __launch_bounds__(256, 1)
         mfma_drain();   // dz3 is read below
         {
             // dKw products
+            const f32x16 g = own_cols(dz3);
+            float t0 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
             for (int i = 0; i < 16; i++) {
-                const float g = (ownr >> i) & 1 ? dz3[i] : 0.f;
-                tw[0] += zm[i] * g;
-                tw[1] += z2[i] * g;
-                tw[2] += zp[i] * g;
+                t0 += zm[i] * g[i];
+                t1 += z2[i] * g[i];
+                t2 += zp[i] * g[i];
             }
+            tw[0] += rf * t0;
+            tw[1] += rf * t1;
+            tw[2] += rf * t2;
+            const f32x16 z3o = own_cols(z3);
             // dUt += Z3[h] dY[h]^T
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
                     float zf[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) zf[j] = (ownr >> (8 * q + j)) & 1 ? z3[8 * q + j] : 0.f;
-                    const bf16x8 av = cvt8(zf);
+                    for (int j = 0; j < 8; j++) zf[j] = z3o[8 * q + j];
+                    const bf16x8 av = mask8(cvt8(zf), rmask);
 #pragma unroll
                     for (int n = 0; n < MT; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
@@ -646,7 +669,7 @@ __global__ void __launch_bounds__(256, 1)
             } else {
 #pragma unroll
                 for (int i = 0; i < 16; i++) {
-                    const float av = (ownr >> i) & 1 ? z3[i] : 0.f;
+                    const float av = z3o[i] * rf;
 #pragma unroll
                     for (int n = 0; n < MT; n++)
                         accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
@@ -664,12 +687,16 @@ __global__ void __launch_bounds__(256, 1)
         }
         dr[KH - 1] = dz2;
         {   // dKh products
+            const f32x16 g = own_cols(dz2);
+            float t[KH];
 #pragma unroll
-            for (int i = 0; i < 16; i++) {
-                const float g = (ownr >> i) & 1 ? dz2[i] : 0.f;
+            for (int j = 0; j < KH; j++) t[j] = 0.f;
 #pragma unroll
-                for (int j = 0; j < KH; j++) tk[j] += ring[j][i] * g;
-            }
+            for (int i = 0; i < 16; i++)
+#pragma unroll
+                for (int j = 0; j < KH; j++) t[j] += ring[j][i] * g[i];
+#pragma unroll
+            for (int j = 0; j < KH; j++) tk[j] += rf * t[j];
         }
         // dZ1 for row h - CH
         f32x16 dz1;
@@ -719,14 +746,15 @@ __global__ void __launch_bounds__(256, 1)
                 }
             }
             // dUs += dZ1[hx] X[hx]^T, X row hx from its ring slot (channel 32n + cl)
+            const f32x16 dz1o = own_cols(dz1);
             const T* xrow = Xl + (k % 3) * NS * lx + cl * lx;
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
                     float zf[8];
 #pragma unroll
-                    for (int j = 0; j < 8; j++) zf[j] = (ownx >> (8 * q + j)) & 1 ? dz1[8 * q + j] : 0.f;
-                    const bf16x8 av = cvt8(zf);
+                    for (int j = 0; j < 8; j++) zf[j] = dz1o[8 * q + j];
+                    const bf16x8 av = mask8(cvt8(zf), xmask);
 #pragma unroll
                     for (int n = 0; n < MS; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
@@ -752,7 +780,7 @@ __global__ void __launch_bounds__(256, 1)
                     }
 #pragma unroll
                 for (int i = 0; i < 16; i++) {
-                    const float av = (ownx >> i) & 1 ? dz1[i] : 0.f;
+                    const float av = __uint_as_float(__float_as_uint(dz1o[i]) & xmask);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
                         accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, xv[n][i], accUs[n], 0, 0, 0);
