@@ -287,7 +287,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         ring[j] = gemm1();
     }
     arow<T, NS>(xa, rX, xoff(h0 + KH - 1 - CH), xcs);
-    for (int h = h0; h < h1; h++) {
+    auto fwd_row = [&](int h) {
         // The tap and Ut tables are re-read from LDS every row: the offsets
         // pass through an empty asm so the loads are not hoisted out of the
         // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
@@ -365,7 +365,14 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
                 for (int i = 0; i < 16; i++)
                     store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
         }
-    }
+    };
+    // The first row runs outside the loop: the loop is then entered, like its
+    // back edge, right after a row's stores, so the wait counts the compiler
+    // derives for the prefetched X row at the loop head are those of the
+    // steady state (entered from the prologue, every row would wait for all
+    // outstanding memory operations, the previous row's stores included).
+    if (h0 < h1) fwd_row(h0);
+    for (int h = h0 + 1; h < h1; h++) fwd_row(h);
 }
 
 template <typename T, int K, int MB2>
@@ -795,7 +802,13 @@ __global__ void __launch_bounds__(256, 1)
                     bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
         }
     };
-    for (int h = hs; h < he; h++) row_step(h);
+    // The first row runs outside the loop: the loop is then entered, like its
+    // back edge, right after a row's stores, so the wait counts the compiler
+    // derives for the prefetched operands at the loop head are those of the
+    // steady state (entered from the prologue, they force every row to wait
+    // for almost all outstanding memory operations).
+    if (hs < he) row_step(hs);
+    for (int h = hs + 1; h < he; h++) row_step(h);
 
     // ---- block sums of the wavefront partials, in a fixed order ----
     __syncthreads();
