@@ -167,6 +167,11 @@ struct TcDesc {
     int64_t cv_g[2], cv_lim[2], cv_s[2];
     int32_t mtiles, ntiles;
     int64_t kchunk, blocks;
+    // off32: every offset of A, B and C fits 31 bits and A, B fit 2 GiB
+    // (extA / extB bytes): 32-bit index arithmetic and range-checked buffer
+    // loads; else 64-bit offsets and predicated loads
+    int32_t off32, pad_;
+    int64_t extA, extB;
 };
 
 // Convolution of a stack of planes contracted over one shared index:

@@ -4,12 +4,17 @@
 // filter-side gradients, and channel products whose labels interleave in
 // memory.
 //
-// A block computes a 32*MT x 128 tile of C for one batch index g.  The index
-// maps of the tile's rows (m), columns (n) and of each 32-wide slice of the
-// reduction (k) are decoded once into LDS offset tables; the A and B slices
-// are then gathered through those tables (coalesced along n when n is
-// unit-stride in B) and multiplied on 32x32 MFMA tiles (fp32: 32x32x2, bf16:
-// 32x32x16).  Positions of convolved labels outside [0, lim) read zero.
+// A block computes a 32*MT x 128 tile of C for one batch index g, walking
+// the reduction in slices of 32 (fp32) or 64 (bf16).  Each thread owns one
+// row of the A tile and one column of the B tile for the whole block (their
+// offsets and convolution bases stay in registers); the k offsets of a slice
+// come from a small LDS table built one slice ahead.  Slices are double
+// buffered: the next slice's elements are loaded into registers (coalesced
+// along n when n is unit-stride in B) while the MFMAs run on the current one
+// (fp32: 32x32x2, bf16: 32x32x16), then written to the other LDS buffer, one
+// barrier a slice.  Positions of convolved labels outside [0, lim) read zero;
+// with 31-bit offsets the loads are range-checked buffer loads (an
+// out-of-range offset reads zero), else predicated 64-bit loads.
 #include <cstring>
 
 #include "desc.h"
@@ -30,18 +35,43 @@ __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
     return v;
 }
 
-template <typename T, typename TC, int MT>
+constexpr uint32_t kOff = 0x80000000u;   // a byte offset past every buffer range: reads 0
+
+// One element of an operand: a range-checked buffer load (off32) or a
+// predicated load.
+template <typename T, typename IT>
+__device__ __forceinline__ T gload(const T* base, __amdgpu_buffer_rsrc_t r, IT off, bool ok) {
+    if constexpr (sizeof(IT) == 4) {
+        const uint32_t b = ok ? (uint32_t)off * (uint32_t)sizeof(T) : kOff;
+        if constexpr (sizeof(T) == 2) return (T)__builtin_amdgcn_raw_buffer_load_b16(r, (int)b, 0, 0);
+        else return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)b, 0, 0));
+    } else {
+        return ok ? base[off] : (T)0;
+    }
+}
+
+template <typename T, typename TC, int MT, typename IT, int TK, int NB>
 __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A, const T* __restrict__ B,
                                                TC* __restrict__ C, float* __restrict__ P) {
     constexpr bool BF = sizeof(T) == 2;
-    constexpr int TM = 32 * MT, TN = 128, TK = 32;
-    constexpr int LA = BF ? TK + 8 : TK + 1;      // A tile row pitch
-    constexpr int LB = BF ? TK + 8 : TN + 4;      // B tile pitch ([n][k] for bf16, [k][n] for fp32)
-    __shared__ __attribute__((aligned(16))) T As[TM * LA];
-    __shared__ __attribute__((aligned(16))) T Bs[BF ? TN * LB : TK * LB];
-    __shared__ int64_t mA[TM], mC[TM], nB[TN], nC[TN], kA[TK], kB[TK];
-    __shared__ int32_t np[2][TN], kj[2][TK];
-    __shared__ unsigned char mok[TM], nok[TN], kok[TK];
+    constexpr int TM = 32 * MT, TN = 128;
+    static_assert(TK == 32 || (BF && TK == 64), "reduction slice");
+    constexpr int LA = BF ? TK + 8 : TK + 1;       // A tile: [m][k]
+    constexpr int LB = BF ? TK + 8 : TN + 4;       // B tile: [n][k] (bf16), [k][n] (fp32)
+    constexpr int ASZ = TM * LA, BSZ = BF ? TN * LB : TK * LB;
+    constexpr int EA = TM * TK / 256, EB = TN * TK / 256;   // tile elements a thread loads
+    constexpr int LC = TN + 4;                               // output tile pitch (fp32)
+    // NB = 1: every block's reduction is one slice (no second buffer)
+    constexpr int TILES = NB * (ASZ + BSZ) * (int)sizeof(T), CT = 32 * LC * 4;
+    // the operand slices, and after the reduction the output tile, in one area
+    __shared__ __attribute__((aligned(16))) unsigned char sm[TILES > CT ? TILES : CT];
+    T (*As)[ASZ] = reinterpret_cast<T (*)[ASZ]>(sm);
+    T (*Bs)[BSZ] = reinterpret_cast<T (*)[BSZ]>(sm + NB * ASZ * sizeof(T));
+    __shared__ IT kA[2][TK], kB[2][TK];
+    __shared__ int32_t kj[2][2][TK];
+    __shared__ unsigned char kok[2][TK];
+    __shared__ IT mC[TM], nC[TN];
+    __shared__ unsigned char mok[TM], nok[TN];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, cl = lane & 31, hf = lane >> 5;
     int64_t bid = blockIdx.x;
@@ -53,45 +83,136 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     const int64_t g = bid / d.ksplit;
     const int64_t m0 = (int64_t)mt * TM, n0 = (int64_t)nt * TN;
 
-    int64_t gA = 0, gB = 0, gC = 0;
+    IT gA = 0, gB = 0, gC = 0;
     {
         int64_t x = g;
         for (int i = d.ng - 1; i >= 0; --i) {
             const int64_t c = x % d.g_size[i];
             x /= d.g_size[i];
-            gA += c * d.g_sA[i];
-            gB += c * d.g_sB[i];
-            gC += c * d.g_sC[i];
+            gA += (IT)(c * d.g_sA[i]);
+            gB += (IT)(c * d.g_sB[i]);
+            gC += (IT)(c * d.g_sC[i]);
         }
     }
-    if (tid < TM) {
-        const int64_t m = m0 + tid;
-        int64_t x = m, oa = 0, oc = 0;
+    const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(A), (short)0,
+                                                                         (int)(sizeof(IT) == 4 ? d.extA : 0), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(B), (short)0,
+                                                                         (int)(sizeof(IT) == 4 ? d.extB : 0), 0x00020000);
+
+    // this thread's A row (fixed for the block) and its k positions in a slice
+    const int am = tid % TM;
+    IT aoff;
+    bool aok;
+    {
+        const int64_t m = m0 + am;
+        int64_t x = m;
+        IT oa = 0, oc = 0;
         for (int i = d.nm - 1; i >= 0; --i) {
             const int64_t c = x % d.m_size[i];
             x /= d.m_size[i];
-            oa += c * d.m_sA[i];
-            oc += c * d.m_sC[i];
+            oa += (IT)(c * d.m_sA[i]);
+            oc += (IT)(c * d.m_sC[i]);
         }
-        mA[tid] = oa;
-        mC[tid] = oc;
-        mok[tid] = m < d.M;
-    } else if (tid >= 128 && tid < 128 + TN) {
-        const int t = tid - 128;
-        const int64_t n = n0 + t;
-        int64_t x = n, ob = 0, oc = 0;
-        np[0][t] = np[1][t] = 0;
+        aoff = gA + oa;
+        aok = m < d.M;
+        if (tid < TM) {
+            mC[tid] = oc;
+            mok[tid] = aok;
+        }
+    }
+    auto akk = [&](int j) { return BF ? (tid / TM) * EA + j : tid / TM + (256 / TM) * j; };
+    // this thread's B column (fixed) and its k positions
+    const int bn = tid % TN, bkr = tid / TN;
+    IT boff, bpa[2] = {0, 0};
+    bool bok;
+    {
+        const int64_t n = n0 + bn;
+        int64_t x = n;
+        IT ob = 0, oc = 0;
+        int32_t np[2] = {0, 0};
         for (int i = d.nn - 1; i >= 0; --i) {
             const int64_t c = x % d.n_size[i];
             x /= d.n_size[i];
-            ob += c * d.n_sB[i];
-            oc += c * d.n_sC[i];
-            if (d.n_cv[i] >= 0) np[d.n_cv[i]][t] = (int32_t)c;
+            ob += (IT)(c * d.n_sB[i]);
+            oc += (IT)(c * d.n_sC[i]);
+            if (d.n_cv[i] >= 0) np[d.n_cv[i]] = (int32_t)c;
         }
-        nB[t] = ob;
-        nC[t] = oc;
-        nok[t] = n < d.N;
+        boff = gB + ob;
+        bok = n < d.N;
+        for (int c = 0; c < d.ncv; c++) bpa[c] = (IT)((int64_t)d.cv_a[c] * np[c] + d.cv_g[c]);
+        if (tid < TN) {
+            nC[tid] = oc;
+            nok[tid] = bok;
+        }
     }
+    auto bkk = [&](int j) { return BF ? bkr * EB + j : bkr + 2 * j; };
+
+    const int64_t kb = (int64_t)ks * d.kchunk;
+    const int64_t ke = min(d.K, kb + d.kchunk);
+    const int ns = (int)((ke - kb + TK - 1) / TK);
+
+    // k table of the slice at k0 into buffer t
+    auto ktab = [&](int t, int64_t k0) {
+        if (tid < TK) {
+            const int64_t k = k0 + tid;
+            int64_t x = k;
+            IT oa = 0, ob = 0;
+            kj[t][0][tid] = kj[t][1][tid] = 0;
+            for (int i = d.nk - 1; i >= 0; --i) {
+                const int64_t c = x % d.k_size[i];
+                x /= d.k_size[i];
+                oa += (IT)(c * d.k_sA[i]);
+                ob += (IT)(c * d.k_sB[i]);
+                if (d.k_cv[i] >= 0) kj[t][d.k_cv[i]][tid] = (int32_t)c;
+            }
+            kA[t][tid] = oa;
+            kB[t][tid] = ob;
+            kok[t][tid] = k < ke;
+        }
+    };
+    T ra[EA], rb[EB];
+    // loads of slice k0 (table t); k positions past the chunk end are skipped
+    // (a branch uniform over the wavefront where the thread's k positions are)
+    auto load = [&](int t, int64_t k0) {
+        const int kv = (int)min((int64_t)TK, ke - k0);   // valid k positions of the slice
+#pragma unroll
+        for (int j = 0; j < EA; j++) {
+            const int kk = akk(j);
+            ra[j] = (T)0;
+            if (TM == 64 && kk >= kv) continue;   // tid / 64: uniform
+            ra[j] = gload<T, IT>(A, rA, aoff + kA[t][kk], aok && kk < kv);
+        }
+#pragma unroll
+        for (int j = 0; j < EB; j++) {
+            const int kk = bkk(j);   // tid / 128: uniform
+            rb[j] = (T)0;
+            if (kk >= kv) continue;
+            bool ok = bok;
+            IT off = boff + kB[t][kk];
+            for (int c = 0; c < d.ncv; c++) {
+                const IT pos = bpa[c] + (IT)d.cv_b[c] * (IT)kj[t][c][kk];
+                ok = ok && pos >= 0 && pos < (IT)d.cv_lim[c];
+                off += pos * (IT)d.cv_s[c];
+            }
+            rb[j] = gload<T, IT>(B, rB, off, ok);
+        }
+    };
+    auto put = [&](int t) {
+        if constexpr (BF) {
+            // contiguous k runs: 16-byte LDS stores
+            T* pa = &As[t][am * LA + (tid / TM) * EA];
+#pragma unroll
+            for (int j = 0; j < EA; j += 8) __builtin_memcpy(pa + j, ra + j, 16);
+            T* pb = &Bs[t][bn * LB + bkr * EB];
+#pragma unroll
+            for (int j = 0; j < EB; j += 8) __builtin_memcpy(pb + j, rb + j, 16);
+        } else {
+#pragma unroll
+            for (int j = 0; j < EA; j++) As[t][am * LA + akk(j)] = ra[j];
+#pragma unroll
+            for (int j = 0; j < EB; j++) Bs[t][bkk(j) * LB + bn] = rb[j];
+        }
+    };
 
     f32x16 acc[MT];
 #pragma unroll
@@ -99,81 +220,93 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
 #pragma unroll
         for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
 
-    const int64_t kb = (int64_t)ks * d.kchunk;
-    const int64_t ke = min(d.K, kb + d.kchunk);
-    for (int64_t k0 = kb; k0 < ke; k0 += TK) {
-        __syncthreads();   // previous slice consumed; m / n tables written
-        if (tid < TK) {
-            const int64_t k = k0 + tid;
-            int64_t x = k, oa = 0, ob = 0;
-            kj[0][tid] = kj[1][tid] = 0;
-            for (int i = d.nk - 1; i >= 0; --i) {
-                const int64_t c = x % d.k_size[i];
-                x /= d.k_size[i];
-                oa += c * d.k_sA[i];
-                ob += c * d.k_sB[i];
-                if (d.k_cv[i] >= 0) kj[d.k_cv[i]][tid] = (int32_t)c;
-            }
-            kA[tid] = oa;
-            kB[tid] = ob;
-            kok[tid] = k < ke;
-        }
-        __syncthreads();
-        for (int e = tid; e < TM * TK; e += 256) {
-            const int mm = e / TK, kk = e - mm * TK;
-            As[mm * LA + kk] = (mok[mm] && kok[kk]) ? A[gA + mA[mm] + kA[kk]] : (T)0;
-        }
-#pragma unroll 4
-        for (int e = tid; e < TK * TN; e += 256) {
-            const int kk = e / TN, nn = e - kk * TN;
-            bool ok = kok[kk] && nok[nn];
-            int64_t off = gB + kB[kk] + nB[nn];
-            for (int c = 0; c < d.ncv; c++) {
-                const int64_t pos = (int64_t)d.cv_a[c] * np[c][nn] + (int64_t)d.cv_b[c] * kj[c][kk] + d.cv_g[c];
-                ok = ok && pos >= 0 && pos < d.cv_lim[c];
-                off += pos * d.cv_s[c];
-            }
-            const T v = ok ? B[off] : (T)0;
-            if constexpr (BF) Bs[nn * LB + kk] = v;
-            else Bs[kk * LB + nn] = v;
-        }
-        __syncthreads();
+    ktab(0, kb);
+    __syncthreads();
+    load(0, kb);
+    put(0);
+    if (NB == 2 && ns > 1) ktab(1, kb + TK);
+    __syncthreads();
+    for (int s = 0; s < (NB == 2 ? ns : 1); s++) {
+        const int cur = NB == 2 ? s & 1 : 0;
+        if (NB == 2 && s + 1 < ns) load(cur ^ 1, kb + (int64_t)(s + 1) * TK);   // next slice in flight during this one's MFMAs
+        const T* as = As[cur];
+        const T* bs = Bs[cur];
         if constexpr (BF) {
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 16) {
-                const bf16x8 b = ld8(&Bs[(wave * 32 + cl) * LB + kk + 8 * hf]);
+                const bf16x8 b = ld8(&bs[(wave * 32 + cl) * LB + kk + 8 * hf]);
 #pragma unroll
                 for (int i = 0; i < MT; i++)
-                    acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8(&As[(i * 32 + cl) * LA + kk + 8 * hf]), b,
+                    acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8(&as[(i * 32 + cl) * LA + kk + 8 * hf]), b,
                                                                      acc[i], 0, 0, 0);
             }
         } else {
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 2) {
-                const float b = Bs[(kk + hf) * LB + wave * 32 + cl];
+                const float b = bs[(kk + hf) * LB + wave * 32 + cl];
 #pragma unroll
                 for (int i = 0; i < MT; i++)
-                    acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(As[(i * 32 + cl) * LA + kk + hf], b, acc[i], 0, 0, 0);
+                    acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(as[(i * 32 + cl) * LA + kk + hf], b, acc[i], 0, 0, 0);
             }
         }
+        if (NB == 2 && s + 1 < ns) put(cur ^ 1);
+        if (NB == 2 && s + 2 < ns) ktab(cur, kb + (int64_t)(s + 2) * TK);
+        __syncthreads();
     }
-    // results (the MFMA results are read after the loop's barrier-free tail;
-    // pad so every path has the wait states before the first read)
+    // results (pad so every path has the wait states before the first read),
+    // through the output tile in LDS (the loop's last barrier freed it): each
+    // thread then writes runs of 8 consecutive n, 16 bytes at a time where C
+    // (or the partial) is contiguous there and the address 16-byte aligned
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    const int tn = wave * 32 + cl;
-    if (!nok[tn]) return;
-    const int64_t n = n0 + tn;
+    float* Ct = reinterpret_cast<float*>(sm);
 #pragma unroll
-    for (int i = 0; i < MT; i++)
+    for (int i = 0; i < MT; i++) {   // 32 rows of the tile a pass
+        if (i > 0) __syncthreads();   // the previous pass's rows are written out
 #pragma unroll
-        for (int r = 0; r < 16; r++) {
-            const int mm = i * 32 + row32(r, lane);
-            if (!mok[mm]) continue;
-            if (d.ksplit == 1) store(C, gC + mC[mm] + nC[tn], acc[i][r]);
-            else P[((g * d.ksplit + ks) * d.M + (m0 + mm)) * d.N + n] = acc[i][r];
+        for (int r = 0; r < 16; r++) Ct[row32(r, lane) * LC + wave * 32 + cl] = acc[i][r];
+        __syncthreads();
+        for (int q = tid; q < 32 * (TN / 8); q += 256) {
+            const int mr = q / (TN / 8), nn = (q - mr * (TN / 8)) * 8, mm = i * 32 + mr;
+            if (!mok[mm] || !nok[nn]) continue;
+            float v[8];
+            const float4 v0 = *reinterpret_cast<const float4*>(&Ct[mr * LC + nn]);
+            const float4 v1 = *reinterpret_cast<const float4*>(&Ct[mr * LC + nn + 4]);
+            v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w;
+            v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
+            if (d.ksplit > 1) {
+                const int64_t base = ((g * d.ksplit + ks) * d.M + (m0 + mm)) * d.N + n0 + nn;
+                if (nok[nn + 7] && ((uintptr_t)(P + base) & 15) == 0) {
+                    *reinterpret_cast<float4*>(P + base) = v0;
+                    *reinterpret_cast<float4*>(P + base + 4) = v1;
+                } else {
+                    for (int e = 0; e < 8; e++)
+                        if (nok[nn + e]) P[base + e] = v[e];
+                }
+                continue;
+            }
+            const IT base = gC + mC[mm] + nC[nn];
+            const bool run = nok[nn + 7] && nC[nn + 7] == nC[nn] + 7;
+            if constexpr (sizeof(TC) == 2) {
+                if (run && ((uintptr_t)(C + base) & 15) == 0) {
+                    uint32_t w[4];
+#pragma unroll
+                    for (int e = 0; e < 4; e++) w[e] = pk_bf16(v[2 * e], v[2 * e + 1]);
+                    *reinterpret_cast<uint4*>(C + base) = make_uint4(w[0], w[1], w[2], w[3]);
+                    continue;
+                }
+            } else {
+                if (run && ((uintptr_t)(C + base) & 15) == 0) {
+                    *reinterpret_cast<float4*>(C + base) = v0;
+                    *reinterpret_cast<float4*>(C + base + 4) = v1;
+                    continue;
+                }
+            }
+            for (int e = 0; e < 8; e++)
+                if (nok[nn + e]) store(C, (int64_t)(gC + mC[mm] + nC[nn + e]), v[e]);
         }
+    }
 }
 
 // C[g][m][n] = sum over chunks (in order) of P[g][chunk][m][n], in double.
@@ -209,10 +342,28 @@ hipError_t tc_launch_t(const TcDesc& d, const Launch& ln, const void* a, const v
                        hipStream_t s) {
     const int MT = d.M > 32 ? 2 : 1;
     dim3 g(ln.grid[0]), bl(256);
-    if (MT == 2)
-        hipLaunchKernelGGL((tc_gemm<T, TC, 2>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p);
-    else
-        hipLaunchKernelGGL((tc_gemm<T, TC, 1>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p);
+    if (d.off32 && (d.extA >= ((int64_t)1 << 31) || d.extB >= ((int64_t)1 << 31))) return hipErrorInvalidValue;
+    // bf16 reductions of 64 and more take slices of 64
+    constexpr int TKW = sizeof(T) == 2 ? 64 : 32;
+    const bool wide = sizeof(T) == 2 && d.K >= 64;
+    // one slice a block (every chunk within one slice): single-buffered
+    const bool one = d.kchunk <= (wide ? TKW : 32);
+#define TC_LAUNCH(mt, IT, tk, nb) \
+    hipLaunchKernelGGL((tc_gemm<T, TC, mt, IT, tk, nb>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p)
+#define TC_TK(mt, IT) \
+    do { \
+        if (wide) { if (one) TC_LAUNCH(mt, IT, TKW, 1); else TC_LAUNCH(mt, IT, TKW, 2); } \
+        else { if (one) TC_LAUNCH(mt, IT, 32, 1); else TC_LAUNCH(mt, IT, 32, 2); } \
+    } while (0)
+    if (d.off32) {
+        if (MT == 2) TC_TK(2, int32_t);
+        else TC_TK(1, int32_t);
+    } else {
+        if (MT == 2) TC_TK(2, int64_t);
+        else TC_TK(1, int64_t);
+    }
+#undef TC_TK
+#undef TC_LAUNCH
     return hipGetLastError();
 }
 

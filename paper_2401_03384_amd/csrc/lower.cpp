@@ -940,10 +940,23 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     int64_t ksplit = 1;
     if (tiles < 1024 && Kt > 512) ksplit = std::min<int64_t>(cdiv(2048, tiles), cdiv(Kt, 256));
     while (ksplit > 1 && (double)Gt * ksplit * Mt * Nt * 4.0 > 512.0 * (1 << 20)) ksplit /= 2;
-    d.kchunk = cdiv(cdiv(Kt, ksplit), 32) * 32;
+    const int64_t kq = At.dtype == DT_BF16 && Kt >= 64 ? 64 : 32;   // the kernel's reduction slice
+    d.kchunk = cdiv(cdiv(Kt, ksplit), kq) * kq;
     d.ksplit = (int32_t)cdiv(Kt, d.kchunk);
     d.blocks = tiles * d.ksplit;
     if (d.blocks > 0x7fffffff || Gt * Mt * Nt > ((int64_t)1 << 40)) return false;
+    // 31-bit offsets when every element offset of A, B and C (and the byte
+    // extents of A and B) fit
+    auto extent = [](const TensorRef& t) {
+        int64_t e = 1;
+        for (size_t i = 0; i < t.dims.size(); i++) e += (t.dims[i] - 1) * t.strides[i];
+        return e;
+    };
+    const int64_t esz = At.dtype == DT_BF16 ? 2 : 4, lim31 = (int64_t)1 << 31;
+    const int64_t eA = extent(At), eB = extent(Bt), eC = extent(C);
+    d.off32 = eA * esz < lim31 && eB * esz < lim31 && eC < lim31 ? 1 : 0;
+    d.extA = eA * esz;
+    d.extB = eB * esz;
     const char* tin = tname(At.dtype);
     Launch ln;
     ln.kind = K_TC | dt_bits(At.dtype, At.dtype, C.dtype);

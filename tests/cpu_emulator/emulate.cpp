@@ -562,6 +562,10 @@ bool run_tc(const Launch& ln, Ctx& c) {
     REQ(d.mtiles == (d.M + 32 * MT - 1) / (32 * MT) && d.ntiles == (d.N + 127) / 128 &&
         d.blocks == d.G * d.mtiles * d.ntiles * d.ksplit && (int64_t)ln.grid[0] == d.blocks &&
         ln.block[0] == 256, "grid");
+    // 31-bit offsets: the buffer ranges lie inside the operands' buffers
+    const int esz = tIn ? 2 : 4;
+    REQ(!d.off32 || (d.extA < ((int64_t)1 << 31) && d.extB < ((int64_t)1 << 31) && (size_t)d.extA <= A.bytes &&
+                     (size_t)d.extB <= B.bytes && d.extA % esz == 0 && d.extB % esz == 0), "31-bit ranges");
     for (int i = 0; i < d.nn; i++) REQ(d.n_cv[i] < d.ncv && (d.n_cv[i] < 0 || d.n_sB[i] == 0), "conv n dims");
     for (int i = 0; i < d.nk; i++) REQ(d.k_cv[i] < d.ncv && (d.k_cv[i] < 0 || d.k_sB[i] == 0), "conv k dims");
     Buf Cb, Pb;
@@ -621,8 +625,10 @@ bool run_tc(const Launch& ln, Ctx& c) {
                             if (pos < 0 || pos >= d.cv_lim[cv]) in = false;
                             b += pos * d.cv_s[cv];
                         }
+                        if (in && d.off32 && (a * esz >= d.extA || b * esz >= d.extB)) ok = false;
                         if (in) acc += (double)ld(A, tIn, a, ok) * ld(B, tIn, b, ok);
                     }
+                    if (d.off32 && oCn >= ((int64_t)1 << 31)) ok = false;
                     if (d.ksplit == 1) st(Cb, tC, oCn, (float)acc, ok);
                     else st(Pb, 0, ((g * d.ksplit + ks) * d.M + m) * d.N + n, (float)acc, ok);
                 }
