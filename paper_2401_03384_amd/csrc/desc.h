@@ -172,6 +172,10 @@ struct TcDesc {
     // loads; else 64-bit offsets and predicated loads
     int32_t off32, pad_;
     int64_t extA, extB;
+    // tapmask: the convolved reduction indices take at most 32 combinations
+    // (tap = j0 * tapJ1 + j1): a thread's valid taps form a bitmask, and the
+    // taps' offsets go into the k table
+    int32_t tapmask, tapJ1;
 };
 
 // Convolution of a stack of planes contracted over one shared index:

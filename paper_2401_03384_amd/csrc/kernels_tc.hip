@@ -125,6 +125,7 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     const int bn = tid % TN, bkr = tid / TN;
     IT boff, bpa[2] = {0, 0};
     bool bok;
+    uint32_t tmask = 0;
     {
         const int64_t n = n0 + bn;
         int64_t x = n;
@@ -140,6 +141,27 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
         boff = gB + ob;
         bok = n < d.N;
         for (int c = 0; c < d.ncv; c++) bpa[c] = (IT)((int64_t)d.cv_a[c] * np[c] + d.cv_g[c]);
+        if (d.tapmask) {
+            // valid taps of this output position; their offsets come from the k table
+            for (int c = 0; c < d.ncv; c++) boff += bpa[c] * (IT)d.cv_s[c];
+            const int J1 = d.tapJ1;
+            int Jc[2] = {1, 1};
+            for (int i = 0; i < d.nk; i++)
+                if (d.k_cv[i] >= 0) Jc[d.k_cv[i]] = (int)d.k_size[i];
+            uint32_t mask = 0;
+            for (int j0 = 0; j0 < Jc[0]; j0++) {
+                const IT p0 = bpa[0] + (IT)d.cv_b[0] * j0;
+                if (p0 < 0 || p0 >= (IT)d.cv_lim[0]) continue;
+                for (int j1 = 0; j1 < J1; j1++) {
+                    if (d.ncv > 1) {
+                        const IT p1 = bpa[1] + (IT)d.cv_b[1] * j1;
+                        if (p1 < 0 || p1 >= (IT)d.cv_lim[1]) continue;
+                    }
+                    mask |= 1u << (j0 * J1 + j1);
+                }
+            }
+            tmask = mask;
+        }
         if (tid < TN) {
             nC[tid] = oc;
             nok[tid] = bok;
@@ -165,6 +187,11 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
                 ob += (IT)(c * d.k_sB[i]);
                 if (d.k_cv[i] >= 0) kj[t][d.k_cv[i]][tid] = (int32_t)c;
             }
+            if (d.tapmask) {
+                // the taps' offsets, and the tap index in kj[t][0]
+                for (int c = 0; c < d.ncv; c++) ob += (IT)d.cv_b[c] * (IT)kj[t][c][tid] * (IT)d.cv_s[c];
+                kj[t][0][tid] = kj[t][0][tid] * d.tapJ1 + (d.ncv > 1 ? kj[t][1][tid] : 0);
+            }
             kA[t][tid] = oa;
             kB[t][tid] = ob;
             kok[t][tid] = k < ke;
@@ -182,19 +209,30 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
             if (TM == 64 && kk >= kv) continue;   // tid / 64: uniform
             ra[j] = gload<T, IT>(A, rA, aoff + kA[t][kk], aok && kk < kv);
         }
+        if (d.tapmask) {
 #pragma unroll
-        for (int j = 0; j < EB; j++) {
-            const int kk = bkk(j);   // tid / 128: uniform
-            rb[j] = (T)0;
-            if (kk >= kv) continue;
-            bool ok = bok;
-            IT off = boff + kB[t][kk];
-            for (int c = 0; c < d.ncv; c++) {
-                const IT pos = bpa[c] + (IT)d.cv_b[c] * (IT)kj[t][c][kk];
-                ok = ok && pos >= 0 && pos < (IT)d.cv_lim[c];
-                off += pos * (IT)d.cv_s[c];
+            for (int j = 0; j < EB; j++) {
+                const int kk = bkk(j);   // tid / 128: uniform
+                rb[j] = (T)0;
+                if (kk >= kv) continue;
+                const bool ok = bok && ((tmask >> kj[t][0][kk]) & 1u);
+                rb[j] = gload<T, IT>(B, rB, boff + kB[t][kk], ok);
             }
-            rb[j] = gload<T, IT>(B, rB, off, ok);
+        } else {
+#pragma unroll
+            for (int j = 0; j < EB; j++) {
+                const int kk = bkk(j);
+                rb[j] = (T)0;
+                if (kk >= kv) continue;
+                bool ok = bok;
+                IT off = boff + kB[t][kk];
+                for (int c = 0; c < d.ncv; c++) {
+                    const IT pos = bpa[c] + (IT)d.cv_b[c] * (IT)kj[t][c][kk];
+                    ok = ok && pos >= 0 && pos < (IT)d.cv_lim[c];
+                    off += pos * (IT)d.cv_s[c];
+                }
+                rb[j] = gload<T, IT>(B, rB, off, ok);
+            }
         }
     };
     auto put = [&](int t) {

@@ -957,6 +957,14 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     d.off32 = eA * esz < lim31 && eB * esz < lim31 && eC < lim31 ? 1 : 0;
     d.extA = eA * esz;
     d.extB = eB * esz;
+    // at most 32 combinations of the convolved reduction indices: tap bitmasks
+    if (!op.convs.empty()) {
+        const int64_t J0 = op.convs[0].J, J1 = op.convs.size() > 1 ? op.convs[1].J : 1;
+        if (J0 * J1 <= 32) {
+            d.tapmask = 1;
+            d.tapJ1 = (int32_t)J1;
+        }
+    }
     const char* tin = tname(At.dtype);
     Launch ln;
     ln.kind = K_TC | dt_bits(At.dtype, At.dtype, C.dtype);

@@ -562,6 +562,14 @@ bool run_tc(const Launch& ln, Ctx& c) {
     REQ(d.mtiles == (d.M + 32 * MT - 1) / (32 * MT) && d.ntiles == (d.N + 127) / 128 &&
         d.blocks == d.G * d.mtiles * d.ntiles * d.ksplit && (int64_t)ln.grid[0] == d.blocks &&
         ln.block[0] == 256, "grid");
+    // tap bitmasks: at most 32 combinations of the convolved reduction indices,
+    // which are the k dims marked as convolved
+    if (d.tapmask) {
+        int64_t Jc[2] = {1, 1};
+        for (int i = 0; i < d.nk; i++)
+            if (d.k_cv[i] >= 0) Jc[d.k_cv[i]] = d.k_size[i];
+        REQ(d.ncv >= 1 && d.tapJ1 == (d.ncv > 1 ? Jc[1] : 1) && Jc[0] * Jc[1] <= 32, "tap masks");
+    }
     // 31-bit offsets: the buffer ranges lie inside the operands' buffers
     const int esz = tIn ? 2 : 4;
     REQ(!d.off32 || (d.extA < ((int64_t)1 << 31) && d.extB < ((int64_t)1 << 31) && (size_t)d.extA <= A.bytes &&
