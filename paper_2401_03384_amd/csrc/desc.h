@@ -176,6 +176,9 @@ struct TcDesc {
     // (tap = j0 * tapJ1 + j1): a thread's valid taps form a bitmask, and the
     // taps' offsets go into the k table
     int32_t tapmask, tapJ1;
+    // kmajor: k (not n) is unit-stride in B and in A: lanes walk k when
+    // loading the tiles, the rows' / columns' offsets come from LDS tables
+    int32_t kmajor, pad2_;
 };
 
 // Convolution of a stack of planes contracted over one shared index:

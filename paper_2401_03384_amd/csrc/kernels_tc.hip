@@ -50,14 +50,14 @@ __device__ __forceinline__ T gload(const T* base, __amdgpu_buffer_rsrc_t r, IT o
     }
 }
 
-template <typename T, typename TC, int MT, typename IT, int TK, int NB>
+template <typename T, typename TC, int MT, typename IT, int TK, int NB, bool KM>
 __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A, const T* __restrict__ B,
                                                TC* __restrict__ C, float* __restrict__ P) {
     constexpr bool BF = sizeof(T) == 2;
     constexpr int TM = 32 * MT, TN = 128;
     static_assert(TK == 32 || (BF && TK == 64), "reduction slice");
     constexpr int LA = BF ? TK + 8 : TK + 1;       // A tile: [m][k]
-    constexpr int LB = BF ? TK + 8 : TN + 4;       // B tile: [n][k] (bf16), [k][n] (fp32)
+    constexpr int LB = BF ? TK + 8 : (KM ? TN + 1 : TN + 4);   // B tile: [n][k] (bf16), [k][n] (fp32)
     constexpr int ASZ = TM * LA, BSZ = BF ? TN * LB : TK * LB;
     constexpr int EA = TM * TK / 256, EB = TN * TK / 256;   // tile elements a thread loads
     constexpr int LC = TN + 4;                               // output tile pitch (fp32)
@@ -72,6 +72,9 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     __shared__ unsigned char kok[2][TK];
     __shared__ IT mC[TM], nC[TN];
     __shared__ unsigned char mok[TM], nok[TN];
+    // k-major loads: the rows' / columns' offsets (and convolution bases) by table
+    __shared__ IT mAt[KM ? TM : 1], nBt[KM ? TN : 1];
+    __shared__ IT npa[KM ? 2 : 1][KM ? TN : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, cl = lane & 31, hf = lane >> 5;
     int64_t bid = blockIdx.x;
@@ -118,6 +121,7 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
         if (tid < TM) {
             mC[tid] = oc;
             mok[tid] = aok;
+            if constexpr (KM) mAt[tid] = aoff;
         }
     }
     auto akk = [&](int j) { return BF ? (tid / TM) * EA + j : tid / TM + (256 / TM) * j; };
@@ -165,6 +169,11 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
         if (tid < TN) {
             nC[tid] = oc;
             nok[tid] = bok;
+            if constexpr (KM) {
+                nBt[tid] = boff;
+                npa[0][tid] = bpa[0];
+                if (d.ncv > 1) npa[1][tid] = bpa[1];
+            }
         }
     }
     auto bkk = [&](int j) { return BF ? bkr * EB + j : bkr + 2 * j; };
@@ -202,6 +211,31 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     // (a branch uniform over the wavefront where the thread's k positions are)
     auto load = [&](int t, int64_t k0) {
         const int kv = (int)min((int64_t)TK, ke - k0);   // valid k positions of the slice
+        if constexpr (KM) {
+            // lanes walk k (unit-stride in A and B): this thread's k position
+            const int kk = tid % TK;
+            const bool kin = kk < kv;
+            const IT ka = kA[t][kk], kbo = kB[t][kk];
+            int32_t kjv[2] = {kj[t][0][kk], kj[t][1][kk]};
+#pragma unroll
+            for (int j = 0; j < EA; j++) {
+                const int mm = tid / TK + (256 / TK) * j;
+                ra[j] = gload<T, IT>(A, rA, mAt[mm] + ka, kin && mok[mm]);
+            }
+#pragma unroll
+            for (int j = 0; j < EB; j++) {
+                const int nn = tid / TK + (256 / TK) * j;
+                bool ok = kin && nok[nn];
+                IT off = nBt[nn] + kbo;
+                for (int c = 0; c < d.ncv; c++) {
+                    const IT pos = npa[c][nn] + (IT)d.cv_b[c] * (IT)kjv[c];
+                    ok = ok && pos >= 0 && pos < (IT)d.cv_lim[c];
+                    off += pos * (IT)d.cv_s[c];
+                }
+                rb[j] = gload<T, IT>(B, rB, off, ok);
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < EA; j++) {
             const int kk = akk(j);
@@ -236,6 +270,18 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
         }
     };
     auto put = [&](int t) {
+        if constexpr (KM) {
+            const int kk = tid % TK;
+#pragma unroll
+            for (int j = 0; j < EA; j++) As[t][(tid / TK + (256 / TK) * j) * LA + kk] = ra[j];
+#pragma unroll
+            for (int j = 0; j < EB; j++) {
+                const int nn = tid / TK + (256 / TK) * j;
+                if constexpr (BF) Bs[t][nn * LB + kk] = rb[j];
+                else Bs[t][kk * LB + nn] = rb[j];
+            }
+            return;
+        }
         if constexpr (BF) {
             // contiguous k runs: 16-byte LDS stores
             T* pa = &As[t][am * LA + (tid / TM) * EA];
@@ -347,13 +393,36 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     }
 }
 
-// C[g][m][n] = sum over chunks (in order) of P[g][chunk][m][n], in double.
+// C[g][m][n] = sum over chunks (in order) of P[g][chunk][m][n], in double: a
+// block takes 64 consecutive outputs (one per lane) of one g; its four
+// wavefronts sum contiguous quarters of the chunks with eight loads in flight,
+// then the quarters are added in a fixed order.
 template <typename TC>
 __global__ void __launch_bounds__(256) tc_reduce(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t MN = d.M * d.N;
-    if (e >= d.G * MN) return;
-    const int64_t g = e / MN, mn = e - g * MN, m = mn / d.N, n = mn - m * d.N;
+    __shared__ double q4[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t MN = d.M * d.N, per_g = (MN + 63) / 64;
+    const int64_t g = blockIdx.x / per_g, mn = (blockIdx.x - g * per_g) * 64 + lane;
+    const int64_t quarter = (d.ksplit + 3) / 4;
+    const int64_t c0 = wave * quarter, c1 = min((int64_t)d.ksplit, c0 + quarter);
+    double acc = 0.0;
+    if (g < d.G && mn < MN) {
+        const float* p = P + g * d.ksplit * MN + mn;
+        int64_t c = c0;
+        for (; c + 8 <= c1; c += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) v[u] = p[(c + u) * MN];
+#pragma unroll
+            for (int u = 0; u < 8; u++) acc += v[u];
+        }
+        for (; c < c1; c++) acc += p[c * MN];
+    }
+    q4[wave][lane] = acc;
+    __syncthreads();
+    if (wave != 0 || g >= d.G || mn >= MN) return;
+    const double sum = (q4[0][lane] + q4[1][lane]) + (q4[2][lane] + q4[3][lane]);
+    const int64_t m = mn / d.N, n = mn - m * d.N;
     int64_t off = 0, x = g;
     for (int i = d.ng - 1; i >= 0; --i) {
         off += (x % d.g_size[i]) * d.g_sC[i];
@@ -369,10 +438,7 @@ __global__ void __launch_bounds__(256) tc_reduce(TcDesc d, const float* __restri
         off += (x % d.n_size[i]) * d.n_sC[i];
         x /= d.n_size[i];
     }
-    double s = 0.0;
-    const float* p = P + g * d.ksplit * MN + mn;
-    for (int c = 0; c < d.ksplit; c++) s += (double)p[c * MN];
-    store(C, off, (float)s);
+    store(C, off, (float)sum);
 }
 
 template <typename T, typename TC>
@@ -387,7 +453,10 @@ hipError_t tc_launch_t(const TcDesc& d, const Launch& ln, const void* a, const v
     // one slice a block (every chunk within one slice): single-buffered
     const bool one = d.kchunk <= (wide ? TKW : 32);
 #define TC_LAUNCH(mt, IT, tk, nb) \
-    hipLaunchKernelGGL((tc_gemm<T, TC, mt, IT, tk, nb>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p)
+    do { \
+        if (d.kmajor) hipLaunchKernelGGL((tc_gemm<T, TC, mt, IT, tk, nb, true>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p); \
+        else hipLaunchKernelGGL((tc_gemm<T, TC, mt, IT, tk, nb, false>), g, bl, 0, s, d, (const T*)a, (const T*)b, (TC*)c, (float*)p); \
+    } while (0)
 #define TC_TK(mt, IT) \
     do { \
         if (wide) { if (one) TC_LAUNCH(mt, IT, TKW, 1); else TC_LAUNCH(mt, IT, TKW, 2); } \

@@ -957,8 +957,13 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     d.off32 = eA * esz < lim31 && eB * esz < lim31 && eC < lim31 ? 1 : 0;
     d.extA = eA * esz;
     d.extB = eB * esz;
+    // k-major tile loads: the innermost reduction dim is unit-stride in A and
+    // B while the innermost column dim is not unit-stride in B
+    if (!K.empty() && K.back().cv < 0 && K.back().sA == 1 && K.back().sB == 1 &&
+        (N.empty() || N.back().cv >= 0 || N.back().sB != 1))
+        d.kmajor = 1;
     // at most 32 combinations of the convolved reduction indices: tap bitmasks
-    if (!op.convs.empty()) {
+    if (!d.kmajor && !op.convs.empty()) {
         const int64_t J0 = op.convs[0].J, J1 = op.convs.size() > 1 ? op.convs[1].J : 1;
         if (J0 * J1 <= 32) {
             d.tapmask = 1;
@@ -988,7 +993,7 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     lr.kind = K_TC_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
     lr.d = part;
     lr.c = C.buf;
-    lr.grid[0] = (uint32_t)cdiv(Gt * Mt * Nt, 256);
+    lr.grid[0] = (uint32_t)(Gt * cdiv(Mt * Nt, 64));   // 64 outputs of one g a block
     lr.block[0] = 256;
     set_desc(lr, d);
     lr.kname = std::string("tc_reduce<") + tname(C.dtype) + ">";
