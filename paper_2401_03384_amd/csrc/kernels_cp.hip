@@ -20,6 +20,7 @@
 // padding of both convolutions.
 #include <atomic>
 #include <cstring>
+#include <type_traits>
 
 #include "desc.h"
 #include "hip_util.h"
@@ -117,6 +118,27 @@ __device__ __forceinline__ bf16x8 pack_words(const uint32_t* w) {
 }
 
 
+// Operands of one chunk of an MFMA chain, read from LDS ahead of use.
+template <int N> struct Opnd { float v[N]; };
+
+// Runs the MFMA chunks mm(c, buf[c]) for c = 0..NC-1 with the LDS operands of
+// chunk c + D requested (ld) before chunk c's MFMAs issue; the scheduling
+// fences keep that order, so each chunk's LDS latency hides behind D chunks of
+// MFMA work instead of stalling the chain at every step.
+template <int NC, int D, int N, typename Ld, typename Mm>
+__device__ __forceinline__ void piped(Ld ld, Mm mm) {
+    Opnd<N> buf[NC];
+#pragma unroll
+    for (int c = 0; c < (D < NC ? D : NC); c++) buf[c] = ld(c);
+#pragma unroll
+    for (int c = 0; c < NC; c++) {
+        if (c + D < NC) buf[c + D] = ld(c + D);
+        __builtin_amdgcn_sched_barrier(0);
+        mm(c, buf[c]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Channel of A-operand slot u of a lane in half hf (K channels per row GEMM):
 // fp32 32x32x2 steps take channels 2u + hf; bf16 32x32x16 steps take
 // 16*(u/8) + 8*hf + u%8.
@@ -139,10 +161,19 @@ __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::pe
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack_words(a + 8 * q), lds8(tab + cl * lda + 16 * q + 8 * hf),
                                                           acc, 0, 0, 0);
     } else {
-#pragma unroll
-        for (int u = 0; u < K / 2; u++)
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[u]), tab[cl * lda + 2 * u + hf], acc, 0,
-                                                       0, 0);
+        // MFMA u takes k = 2u + hf; chunks of two MFMAs, operands four chunks ahead
+        const float* tb = tab + cl * lda + hf;
+        piped<K / 4, 4, 2>(
+            [&](int c) {
+                Opnd<2> o;
+                o.v[0] = tb[4 * c];
+                o.v[1] = tb[4 * c + 2];
+                return o;
+            },
+            [&](int c, const Opnd<2>& o) {
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[2 * c]), o.v[0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[2 * c + 1]), o.v[1], acc, 0, 0, 0);
+            });
     }
     if constexpr (DRAIN) mfma_drain();
     return acc;
@@ -203,6 +234,64 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
+    // ---- this wavefront's strip ----
+    // strips fastest: the waves of a block share halo rows and cache lines
+    // (set up before the tables, so that its first X rows are in flight
+    // while they load; waves past the end load nothing and leave after the
+    // barrier)
+    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
+    const bool wok = gw < d.waves;
+    int cb = 0, seg = 0, b = 0;
+    if (wok) {
+        cb = (int)(gw % d.ncb);
+        const int64_t rest = gw / d.ncb;
+        seg = (int)(rest % d.segs);
+        b = (int)(rest / d.segs);
+    }
+    const int col = cb * d.colstride - HWW + (lane & 31);
+    const bool colok = col >= 0 && col < W;
+    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
+    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
+    const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
+    const int cl = lane & 31;
+
+    // X rows as B-operand slots (the same slot layout as arow), loaded one row
+    // ahead through a raw buffer: rows and lanes outside the image read zeros
+    constexpr uint32_t E = sizeof(T);
+    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(NS * d.x_ss * E));
+    const uint32_t xcs = (uint32_t)(d.x_ss * E);
+    const uint32_t kOut = 0x80000000u;   // past the range: reads 0
+    const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
+    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    uint32_t xa[NS / 2];
+    // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in a
+    auto gemm1 = [&](const uint32_t (&a)[NS / 2]) {
+        f32x16 acc;
+#pragma unroll
+        for (int i = 0; i < 16; i++) acc[i] = 0.f;
+        if constexpr (BF) {
+#pragma unroll
+            for (int q = 0; q < NS / 16; q++)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsL + cl * LDA + 16 * q + 8 * half),
+                                                              pack_words(a + 8 * q), acc, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < NS / 2; u++)
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(UsL[cl * LDA + 2 * u + half], __uint_as_float(a[u]),
+                                                           acc, 0, 0, 0);
+        }
+        mfma_drain();
+        return acc;
+    };
+
+    // the first NP rows of the walk are requested before the tables load;
+    // later rows of the ring fill follow as buffers free up
+    constexpr int NP = KH < 3 ? KH : 3;
+    uint32_t xp[NP][NS / 2];
+    if (wok) {
+#pragma unroll
+        for (int p = 0; p < NP; p++) arow<T, NS>(xp[p], rX, xoff(h0 - CH + p), xcs);
+    }
     // ---- tables ----
     {
     T* UtP = (T*)(smem + d.o_ut);
@@ -235,58 +324,16 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     }
     }
     __syncthreads();
-
-    // ---- this wavefront's strip ----
-    // strips fastest: the waves of a block share halo rows and cache lines
-    const int64_t gw = xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
-    if (gw >= d.waves) return;
-    const int cb = (int)(gw % d.ncb);
-    const int64_t rest = gw / d.ncb;
-    const int seg = (int)(rest % d.segs);
-    const int b = (int)(rest / d.segs);
-    const int col = cb * d.colstride - HWW + (lane & 31);
-    const bool colok = col >= 0 && col < W;
-    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
-    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
-    const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
-    const int cl = lane & 31;
-
-    // X rows as B-operand slots (the same slot layout as arow), loaded one row
-    // ahead through a raw buffer: rows and lanes outside the image read zeros
-    constexpr uint32_t E = sizeof(T);
-    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(NS * d.x_ss * E));
-    const uint32_t xcs = (uint32_t)(d.x_ss * E);
-    const uint32_t kOut = 0x80000000u;   // past the range: reads 0
-    const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
-    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
-    uint32_t xa[NS / 2];
-    // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in xa
-    auto gemm1 = [&]() {
-        f32x16 acc;
-#pragma unroll
-        for (int i = 0; i < 16; i++) acc[i] = 0.f;
-        if constexpr (BF) {
-#pragma unroll
-            for (int q = 0; q < NS / 16; q++)
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsL + cl * LDA + 16 * q + 8 * half),
-                                                              pack_words(xa + 8 * q), acc, 0, 0, 0);
-        } else {
-#pragma unroll
-            for (int u = 0; u < NS / 2; u++)
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(UsL[cl * LDA + 2 * u + half], __uint_as_float(xa[u]),
-                                                           acc, 0, 0, 0);
-        }
-        mfma_drain();
-        return acc;
-    };
+    if (!wok) return;
 
     f32x16 ring[KH];
 #pragma unroll
     for (int j = 0; j < KH - 1; j++) {
-        arow<T, NS>(xa, rX, xoff(h0 - CH + j), xcs);
-        ring[j] = gemm1();
+        ring[j] = gemm1(xp[j % NP]);
+        if (j + NP < KH) arow<T, NS>(xp[j % NP], rX, xoff(h0 - CH + j + NP), xcs);
     }
-    arow<T, NS>(xa, rX, xoff(h0 + KH - 1 - CH), xcs);
+#pragma unroll
+    for (int u = 0; u < NS / 2; u++) xa[u] = xp[(KH - 1) % NP][u];
     auto fwd_row = [&](int h) {
         // The tap and Ut tables are re-read from LDS every row: the offsets
         // pass through an empty asm so the loads are not hoisted out of the
@@ -296,7 +343,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         const T* UtP = (const T*)(smem + o_ut);
         const float* KhP = (const float*)(smem + o_kh);
         const float* KwP = (const float*)(smem + o_kw);
-        ring[KH - 1] = gemm1();
+        ring[KH - 1] = gemm1(xa);
         arow<T, NS>(xa, rX, xoff(h + KH - CH), xcs);   // the next row's, used one row later
         // conv along h
         f32x16 z2;
@@ -443,17 +490,27 @@ __device__ __forceinline__ uint32_t half_mask(int hf) {
 
 // w[i] = v at column tcol(i, hf) + DD of the same rank (DD = +-1); values
 // that would come from outside the 32 columns are unspecified.  hm =
-// half_mask(hf).
+// half_mask(hf).  Columns that cross between the lane halves come from lane
+// l ^ 32: one v_permlane32_swap exchanges a pair of registers between the
+// halves (p's upper half with q's lower half), then each half keeps its part.
 template <int DD>
 __device__ __forceinline__ f32x16 tshift(const f32x16& v, uint32_t hm) {
-    float snd[4], rcv[4];
+    float rcv[4];
 #pragma unroll
     for (int a = 0; a < 4; a++) {
-        if constexpr (DD == 1) snd[a] = blend(hm, v[4 * a], v[a < 3 ? 4 * a + 4 : 0]);
-        else snd[a] = blend(hm, v[a > 0 ? 4 * a - 1 : 0], v[4 * a + 3]);
+        // p: wanted by the lower half from the upper; q: by the upper from the lower
+        float p, q;
+        if constexpr (DD == 1) {
+            p = v[4 * a];
+            q = v[a < 3 ? 4 * a + 4 : 0];
+        } else {
+            p = v[a > 0 ? 4 * a - 1 : 0];
+            q = v[4 * a + 3];
+        }
+        // r[0] = (p lanes 0-31, q lanes 0-31), r[1] = (p lanes 32-63, q lanes 32-63)
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(p), __float_as_uint(q), false, false);
+        rcv[a] = blend(hm, __uint_as_float(r[0]), __uint_as_float(r[1]));
     }
-#pragma unroll
-    for (int a = 0; a < 4; a++) rcv[a] = __shfl_xor(snd[a], 32, 64);
     f32x16 w;
 #pragma unroll
     for (int i = 0; i < 16; i++) {
@@ -480,27 +537,6 @@ __global__ void __launch_bounds__(256, 1)
     const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, cl = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // ---- tables: UsA [32][lda_s], UtA [32][lda_t] (and UsT [NS][ldu] for bf16) ----
-    {
-        T* usa = (T*)smem;
-        T* uta = (T*)(smem + d.o_uta);
-        for (int e = tid; e < 32 * NS; e += 256) {
-            int r = e / NS, s = e - r * NS;
-            usa[r * d.lda_s + s] = Us[r * d.us_sr + s * d.us_ss];
-        }
-        for (int e = tid; e < 32 * NT; e += 256) {
-            int r = e / NT, t = e - r * NT;
-            uta[r * d.lda_t + t] = Ut[r * d.ut_sr + t * d.ut_st];
-        }
-        if constexpr (BF) {
-            T* ust = (T*)(smem + d.o_ust);
-            for (int e = tid; e < 32 * NS; e += 256) {
-                int s = e / 32, r = e - s * 32;
-                ust[s * d.ldu + r] = Us[r * d.us_sr + s * d.us_ss];
-            }
-        }
-    }
-    __syncthreads();
     float* Tz = (float*)(smem + d.o_tz + (size_t)wave * d.tz_stride);
     T* Yt = (T*)(smem + d.o_yt + (size_t)wave * d.yt_bytes);
     T* Xl = (T*)(smem + d.o_xl + (size_t)wave * d.xl_bytes);   // ring of 3 X rows [slot][s][col]
@@ -564,7 +600,7 @@ __global__ void __launch_bounds__(256, 1)
     const T* UsA = (const T*)smem;
     const T* UtA = (const T*)(smem + d.o_uta);
     const T* UsT = (const T*)(smem + d.o_ust);
-    const int hs = h0 - CH, he = wok ? h1 + CH : hs;
+    const int hs = h0 - CH;
     // A-operand row offsets: rows outside the image (and lanes outside it) read zeros
     auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
     auto yoff = [&](int row) { return (row >= 0 && row < H) ? ya0 + (uint32_t)(row * W) * E : kOut; };
@@ -577,62 +613,93 @@ __global__ void __launch_bounds__(256, 1)
     // the X row held in xa into ring slot `slot` (channel-major), for the dUs
     // product CH rows later; X row r sits in slot (r - (hs - CH)) % 3
     const int lx = d.lx;
-    auto xl_put = [&](int slot) {
+    auto xl_put = [&](int slot, const uint32_t (&src)[NS / 2 / PW]) {
         T* dst = Xl + slot * NS * lx + cl;
 #pragma unroll
         for (int u = 0; u < NS / 2; u++) {
-            if constexpr (BF) dst[achan<BF>(u, hf) * lx] = (T)xa[u];
-            else dst[achan<BF>(u, hf) * lx] = __uint_as_float(xa[u]);
+            if constexpr (BF) dst[achan<BF>(u, hf) * lx] = (T)src[u];
+            else dst[achan<BF>(u, hf) * lx] = __uint_as_float(src[u]);
         }
     };
+    // Every operand of the ring fill and the first row is requested before
+    // the factor tables load, so that their memory latencies overlap.
+    uint32_t xp[KH - 1][NS / 2 / PW];
     if (wok) {
 #pragma unroll
-        for (int j = 0; j < KH - 1; j++) {
-            arow<T, NS>(xa, rX, xoff(hs - CH + j), xcs);
-            ring[j] = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
-            xl_put(j);
-        }
+        for (int j = 0; j < KH - 1; j++) arow<T, NS>(xp[j], rX, xoff(hs - CH + j), xcs);
         arow<T, NS>(xa, rX, xoff(hs + CH), xcs);
         arow<T, NT>(ya, rY, yoff(hs), ycs);
     }
+    // ---- tables: UsA [32][lda_s], UtA [32][lda_t] (and UsT [NS][ldu] for bf16) ----
+    {
+        T* usa = (T*)smem;
+        T* uta = (T*)(smem + d.o_uta);
+        for (int e = tid; e < 32 * NS; e += 256) {
+            int r = e / NS, s = e - r * NS;
+            usa[r * d.lda_s + s] = Us[r * d.us_sr + s * d.us_ss];
+        }
+        for (int e = tid; e < 32 * NT; e += 256) {
+            int r = e / NT, t = e - r * NT;
+            uta[r * d.lda_t + t] = Ut[r * d.ut_sr + t * d.ut_st];
+        }
+        if constexpr (BF) {
+            T* ust = (T*)(smem + d.o_ust);
+            for (int e = tid; e < 32 * NS; e += 256) {
+                int s = e / 32, r = e - s * 32;
+                ust[s * d.ldu + r] = Us[r * d.us_sr + s * d.us_ss];
+            }
+        }
+    }
+    __syncthreads();
+    if (wok) {
+#pragma unroll
+        for (int j = 0; j < KH - 1; j++) {
+            ring[j] = tgemm<T, NS>(xp[j], UsA, d.lda_s, cl, hf);
+            xl_put(j, xp[j]);
+        }
+    }
 
-    // One row of the walk, branch-free so that the compiler can overlap the
-    // convolution arithmetic with the MFMA chains.  Ownership of the weight-
-    // gradient terms: loads outside the image read zeros, so every product
-    // there vanishes by itself (dY = 0 makes dZ3 = 0, X = 0 makes Z1 = 0);
-    // what remains is the strip overlap (columns 0 and 31, zeroed by own_cols)
-    // and the segment halo rows: row h counts for dUt, dKw and dKh only inside
-    // the segment (rin), row h - CH for dX and dUs (xin).  The row flags
-    // scale the tap sums and mask the packed MFMA operands; the dX stores of
-    // a halo row go past the buffer's range (dropped).
-    auto row_step = [&](int h) {
+    // One row of the walk.  Ownership of the weight-gradient terms: loads
+    // outside the image read zeros, so every product there vanishes by
+    // itself (dY = 0 makes dZ3 = 0, X = 0 makes Z1 = 0); what remains is the
+    // strip overlap (columns 0 and 31, zeroed by own_cols) and the segment
+    // halo rows: row h counts for dUt, dKw and dKh only inside the segment
+    // (rin), row h - CH for dX and dUs (xin).  The halo rows run as separate
+    // instances of the row code (compile-time flags) without those products,
+    // and the last row also without Z1[h + CH], which only they would read;
+    // the loop body itself stays free of branches.
+    auto row_step = [&](int h, auto RIN, auto XIN, auto Z1N) {
+        constexpr bool rin = decltype(RIN)::value, xin = decltype(XIN)::value;
         const int hx = h - CH;
-        const bool rin = h >= h0 && h < h1, xin = hx >= h0 && hx < h1;
-        const float rf = rin ? 1.f : 0.f;
-        const uint32_t rmask = rin ? 0xffffffffu : 0u, xmask = xin ? 0xffffffffu : 0u;
         const int k = h - hs;   // ring slots: X row h + CH goes to (k + 2) % 3, row hx is read from k % 3
         // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
-        const f32x16 z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
-        xl_put((k + 2) % 3);
+        f32x16 z1n;
+        if constexpr (decltype(Z1N)::value) {
+            z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 16; i++) z1n[i] = 0.f;
+        }
+        xl_put((k + 2) % 3, xa);
         arow<T, NS>(xa, rX, xoff(h + 1 + CH), xcs);
         const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, d.lda_t, cl, hf);
         ring[KH - 1] = z1n;
-        // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1):
-        // VALU work independent of the dZ3 chain above, free to overlap it
-        f32x16 z2, z3;
+        // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1)
+        f32x16 z2, z3, zm, zp;
+        if constexpr (rin) {
 #pragma unroll
-        for (int i = 0; i < 16; i++) {
-            float a = 0.f;
+            for (int i = 0; i < 16; i++) {
+                float a = 0.f;
 #pragma unroll
-            for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
-            z2[i] = a;
-        }
-        const f32x16 zm = tshift<-1>(z2, hm);
-        const f32x16 zp = tshift<1>(z2, hm);
+                for (int j = 0; j < KH; j++) a += kh[j] * ring[j][i];
+                z2[i] = a;
+            }
+            zm = tshift<-1>(z2, hm);
+            zp = tshift<1>(z2, hm);
 #pragma unroll
-        for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
-        __builtin_amdgcn_sched_barrier(0);   // the next row's dY loads stay behind the chain
-        {   // dY[h] into the LDS tile of the dUt product
+            for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
+            __builtin_amdgcn_sched_barrier(0);   // the next row's dY loads stay behind the chain
+            // dY[h] into the LDS tile of the dUt product
 #pragma unroll
             for (int u = 0; u < NT / 2; u++) {
                 if constexpr (BF) Yt[achan<BF>(u, hf) * d.ly + cl] = (T)ya[u];
@@ -641,7 +708,7 @@ __global__ void __launch_bounds__(256, 1)
         }
         arow<T, NT>(ya, rY, yoff(h + 1), ycs);
         mfma_drain();   // dz3 is read below
-        {
+        if constexpr (rin) {
             // dKw products
             const f32x16 g = own_cols(dz3);
             float t0 = 0.f, t1 = 0.f, t2 = 0.f;
@@ -651,9 +718,9 @@ __global__ void __launch_bounds__(256, 1)
                 t1 += z2[i] * g[i];
                 t2 += zp[i] * g[i];
             }
-            tw[0] += rf * t0;
-            tw[1] += rf * t1;
-            tw[2] += rf * t2;
+            tw[0] += t0;
+            tw[1] += t1;
+            tw[2] += t2;
             const f32x16 z3o = own_cols(z3);
             // dUt += Z3[h] dY[h]^T
             if constexpr (BF) {
@@ -662,7 +729,7 @@ __global__ void __launch_bounds__(256, 1)
                     float zf[8];
 #pragma unroll
                     for (int j = 0; j < 8; j++) zf[j] = z3o[8 * q + j];
-                    const bf16x8 av = mask8(cvt8(zf), rmask);
+                    const bf16x8 av = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MT; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
@@ -674,14 +741,29 @@ __global__ void __launch_bounds__(256, 1)
                     }
                 }
             } else {
+                // chunk c: columns tcol(2c, hf) and tcol(2c + 1, hf) (adjacent) of each
+                // channel block, three chunks ahead
+                const float* yb = Yt + cl * d.ly + 4 * hf;
+                piped<8, 3, 2 * MT>(
+                    [&](int c) {
+                        Opnd<2 * MT> o;
+                        const int cc = 8 * (c >> 1) + 2 * (c & 1);   // tcol(2c, hf) - 4hf
 #pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const float av = z3o[i] * rf;
+                        for (int n = 0; n < MT; n++) {
+                            o.v[2 * n] = yb[32 * n * d.ly + cc];
+                            o.v[2 * n + 1] = yb[32 * n * d.ly + cc + 1];
+                        }
+                        return o;
+                    },
+                    [&](int c, const Opnd<2 * MT>& o) {
 #pragma unroll
-                    for (int n = 0; n < MT; n++)
-                        accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            av, Yt[(32 * n + cl) * d.ly + tcol(i, hf)], accUt[n], 0, 0, 0);
-                }
+                        for (int j = 0; j < 2; j++) {
+                            const float av = z3o[2 * c + j];
+#pragma unroll
+                            for (int n = 0; n < MT; n++)
+                                accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, o.v[2 * n + j], accUt[n], 0, 0, 0);
+                        }
+                    });
             }
         }
         // dZ2[h]: transposed conv along w (tap j reads column - j + 1)
@@ -693,7 +775,7 @@ __global__ void __launch_bounds__(256, 1)
             for (int i = 0; i < 16; i++) dz2[i] = kw[0] * gp[i] + kw[1] * dz3[i] + kw[2] * gm[i];
         }
         dr[KH - 1] = dz2;
-        {   // dKh products
+        if constexpr (rin) {   // dKh products
             const f32x16 g = own_cols(dz2);
             float t[KH];
 #pragma unroll
@@ -703,7 +785,7 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
                 for (int j = 0; j < KH; j++) t[j] += ring[j][i] * g[i];
 #pragma unroll
-            for (int j = 0; j < KH; j++) tk[j] += rf * t[j];
+            for (int j = 0; j < KH; j++) tk[j] += t[j];
         }
         // dZ1 for row h - CH
         f32x16 dz1;
@@ -719,7 +801,7 @@ __global__ void __launch_bounds__(256, 1)
             ring[j] = ring[j + 1];
             dr[j] = dr[j + 1];
         }
-        {
+        if constexpr (xin) {
             // dX[hx] = Us^T dZ1[hx]: dZ1 through the LDS tile Tz[col][r], which
             // may share the dY tile: every read of that precedes these writes
             asm volatile("" ::: "memory");
@@ -730,6 +812,9 @@ __global__ void __launch_bounds__(256, 1)
             for (int n = 0; n < MS; n++)
 #pragma unroll
                 for (int i = 0; i < 16; i++) accX[n][i] = 0.f;
+            // dUs += dZ1[hx] X[hx]^T, X row hx from its ring slot (channel 32n + cl)
+            const f32x16 dz1o = own_cols(dz1);
+            const T* xrow = Xl + (k % 3) * NS * lx + cl * lx;
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
@@ -742,26 +827,12 @@ __global__ void __launch_bounds__(256, 1)
                         accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf),
                                                                           bv, accX[n], 0, 0, 0);
                 }
-            } else {
-#pragma unroll
-                for (int u = 0; u < 16; u++) {
-                    const float bv = Tz[cl * LZ + 2 * u + hf];
-#pragma unroll
-                    for (int n = 0; n < MS; n++)
-                        accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(UsA[(2 * u + hf) * d.lda_s + 32 * n + cl], bv,
-                                                                       accX[n], 0, 0, 0);
-                }
-            }
-            // dUs += dZ1[hx] X[hx]^T, X row hx from its ring slot (channel 32n + cl)
-            const f32x16 dz1o = own_cols(dz1);
-            const T* xrow = Xl + (k % 3) * NS * lx + cl * lx;
-            if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
                     float zf[8];
 #pragma unroll
                     for (int j = 0; j < 8; j++) zf[j] = dz1o[8 * q + j];
-                    const bf16x8 av = mask8(cvt8(zf), xmask);
+                    const bf16x8 av = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MS; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
@@ -773,28 +844,57 @@ __global__ void __launch_bounds__(256, 1)
                     }
                 }
             } else {
-                // columns tcol(i, hf) = 8(i/4) + 4hf + i%4: four aligned runs of four
-                float xv[MS][16];
+                // One pipeline: chunks 0-3 the dUs product (columns tcol(i, hf) =
+                // 8(i/4) + 4hf + i%4: one aligned run of four a chunk and channel
+                // block), chunks 4-11 the dX product (ranks 2u + hf, two u a chunk),
+                // whose reads of the dZ1 tile are in flight while dUs runs.
+                constexpr int NO = 4 * MS > 2 * MS + 2 ? 4 * MS : 2 * MS + 2;
+                const float* tzr = Tz + cl * LZ + hf;
+                const float* usr = UsA + hf * d.lda_s + cl;
+                piped<12, 3, NO>(
+                    [&](int c) {
+                        Opnd<NO> o;
+                        if (c < 4) {
 #pragma unroll
-                for (int n = 0; n < MS; n++)
+                            for (int n = 0; n < MS; n++) {
+                                const float4 t = *reinterpret_cast<const float4*>(xrow + (32 * n) * lx + 8 * c + 4 * hf);
+                                o.v[4 * n] = t.x;
+                                o.v[4 * n + 1] = t.y;
+                                o.v[4 * n + 2] = t.z;
+                                o.v[4 * n + 3] = t.w;
+                            }
+                        } else {
+                            const int u = 2 * (c - 4);
 #pragma unroll
-                    for (int a = 0; a < 4; a++) {
-                        const float4 t = *reinterpret_cast<const float4*>(xrow + (32 * n) * lx + 8 * a + 4 * hf);
-                        xv[n][4 * a] = t.x;
-                        xv[n][4 * a + 1] = t.y;
-                        xv[n][4 * a + 2] = t.z;
-                        xv[n][4 * a + 3] = t.w;
-                    }
+                            for (int j = 0; j < 2; j++) {
 #pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const float av = __uint_as_float(__float_as_uint(dz1o[i]) & xmask);
+                                for (int n = 0; n < MS; n++) o.v[j * MS + n] = usr[2 * (u + j) * d.lda_s + 32 * n];
+                                o.v[2 * MS + j] = tzr[2 * (u + j)];
+                            }
+                        }
+                        return o;
+                    },
+                    [&](int c, const Opnd<NO>& o) {
+                        if (c < 4) {
 #pragma unroll
-                    for (int n = 0; n < MS; n++)
-                        accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, xv[n][i], accUs[n], 0, 0, 0);
-                }
+                            for (int j = 0; j < 4; j++) {
+                                const float av = dz1o[4 * c + j];
+#pragma unroll
+                                for (int n = 0; n < MS; n++)
+                                    accUs[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, o.v[4 * n + j], accUs[n], 0, 0, 0);
+                            }
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < 2; j++)
+#pragma unroll
+                                for (int n = 0; n < MS; n++)
+                                    accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(o.v[j * MS + n], o.v[2 * MS + j],
+                                                                                   accX[n], 0, 0, 0);
+                        }
+                    });
             }
             mfma_drain();   // accX is read by the stores
-            const uint32_t v0 = xin ? dx0 + (uint32_t)(hx * W) * E : kOut;   // kOut: past the range
+            const uint32_t v0 = dx0 + (uint32_t)(hx * W) * E;
 #pragma unroll
             for (int n = 0; n < MS; n++)
 #pragma unroll
@@ -802,13 +902,24 @@ __global__ void __launch_bounds__(256, 1)
                     bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
         }
     };
-    // The first row runs outside the loop: the loop is then entered, like its
-    // back edge, right after a row's stores, so the wait counts the compiler
-    // derives for the prefetched operands at the loop head are those of the
-    // steady state (entered from the prologue, they force every row to wait
-    // for almost all outstanding memory operations).
-    if (hs < he) row_step(hs);
-    for (int h = hs + 1; h < he; h++) row_step(h);
+    // Rows hs = h0 - 1 (halo), h0 (no dX row yet), h0 + 1 .. h1 - 1 and h1
+    // (halo).  The first full row runs outside the loop: the loop is then
+    // entered, like its back edge, right after a row's stores, so the wait
+    // counts the compiler derives for the prefetched operands at the loop
+    // head are those of the steady state (entered otherwise, they force every
+    // row to wait for almost all outstanding memory operations).
+    static_assert(CH == 1, "one halo row on each side");
+    const std::true_type yes;
+    const std::false_type no;
+    if (wok) {
+        row_step(hs, no, no, yes);
+        row_step(h0, yes, no, yes);
+        if (h0 + 1 < h1) {
+            row_step(h0 + 1, yes, yes, yes);
+            for (int h = h0 + 2; h < h1; h++) row_step(h, yes, yes, yes);
+        }
+        row_step(h1, no, yes, no);
+    }
 
     // ---- block sums of the wavefront partials, in a fixed order ----
     __syncthreads();

@@ -114,6 +114,10 @@ PARITY_WORKLOADS = {
     "C2r32": cp_layer("C2r32", 3, 32, 32, 13, 37, 32, 3, "f32", 17),
     "C2r32_bf16": cp_layer("C2r32_bf16", 3, 32, 32, 13, 37, 32, 3, "bf16", 17),
     "C2k5": cp_layer("C2k5", 2, 64, 32, 12, 29, 32, 5, "f32", 18),
+    # enough strips that the fused backward walks segments of several rows,
+    # with a one-row segment at the bottom (4-row and 2-row segments)
+    "C2seg": cp_layer("C2seg", 128, 32, 32, 29, 16, 32, 3, "f32", 21),
+    "C2seg_bf16": cp_layer("C2seg_bf16", 64, 64, 64, 23, 20, 32, 3, "bf16", 22),
     "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
     "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
     "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
