@@ -201,6 +201,13 @@ __device__ __forceinline__ void bstore(float v, bf16_t*, __amdgpu_buffer_rsrc_t 
 __device__ __forceinline__ void bstore(float v, float*, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
     bstore(v, r, voff);
 }
+// the same with a wave-uniform offset soff added (scalar register operand)
+__device__ __forceinline__ void bstore(float v, bf16_t*, __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), r, (int)voff, (int)soff, 0);
+}
+__device__ __forceinline__ void bstore(float v, float*, __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)voff, (int)soff, 0);
+}
 
 // One activation row in A-operand slots: a[u] = src[achan(u, hf)][row][col].
 // voff = byte offset of (channel hf, row, the lane's column), or an offset
@@ -293,35 +300,51 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         for (int p = 0; p < NP; p++) arow<T, NS>(xp[p], rX, xoff(h0 - CH + p), xcs);
     }
     // ---- tables ----
+    // Each thread issues all of its table loads before any LDS store, so that
+    // their memory latencies overlap.
     {
     T* UtP = (T*)(smem + d.o_ut);
     float* KhP = (float*)(smem + d.o_kh);
     float* KwP = (float*)(smem + d.o_kw);
-    for (int e = tid; e < 32 * S; e += 256) {
-        int r = e / S, s = e - r * S;
-        UsL[r * LDA + s] = Us[r * d.us_sr + s * d.us_ss];
-    }
-    if constexpr (BF) {
-        // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t]
-        for (int e = tid; e < 2 * 2 * TT * 8; e += 256) {
-            int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
-            UtP[e] = Ut[row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st];
+    constexpr int QS = NS / 8, QT = TT / 8;     // elements a thread (256 threads)
+    constexpr int NKH = 32 * KH, NKW = 32 * KW;  // tap tables, at most one element a thread
+    static_assert(NKH <= 256 && NKW <= 256, "tap tables fit one pass");
+    T vs[QS], vt[QT];
+    float vkh = 0.f, vkw = 0.f;
+    // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t] (bf16), UtP[i][hf][t] = Ut[row32(i, 32*hf)][t] (fp32)
+    auto ut_src = [&](int e) {
+        if constexpr (BF) {
+            const int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
+            return row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st;
+        } else {
+            const int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
+            return row32(i, 32 * hf) * d.ut_sr + t * d.ut_st;
         }
-    } else {
-        // UtP[i][hf][t] = Ut[row32(i, 32*hf)][t]
-        for (int e = tid; e < 16 * 2 * TT; e += 256) {
-            int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
-            UtP[e] = Ut[row32(i, 32 * hf) * d.ut_sr + t * d.ut_st];
-        }
+    };
+#pragma unroll
+    for (int q = 0; q < QS; q++) {
+        const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
+        vs[q] = Us[r * d.us_sr + s * d.us_ss];
     }
-    for (int e = tid; e < 16 * 2 * KH; e += 256) {
-        int j = e % KH, hf = (e / KH) & 1, i = e / (2 * KH);
-        KhP[e] = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
+#pragma unroll
+    for (int q = 0; q < QT; q++) vt[q] = Ut[ut_src(tid + 256 * q)];
+    if (tid < NKH) {
+        const int j = tid % KH, hf = (tid / KH) & 1, i = tid / (2 * KH);
+        vkh = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
     }
-    for (int e = tid; e < 16 * 2 * KW; e += 256) {
-        int j = e % KW, hf = (e / KW) & 1, i = e / (2 * KW);
-        KwP[e] = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
+    if (tid < NKW) {
+        const int j = tid % KW, hf = (tid / KW) & 1, i = tid / (2 * KW);
+        vkw = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
     }
+#pragma unroll
+    for (int q = 0; q < QS; q++) {
+        const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
+        UsL[r * LDA + s] = vs[q];
+    }
+#pragma unroll
+    for (int q = 0; q < QT; q++) UtP[tid + 256 * q] = vt[q];
+    if (tid < NKH) KhP[tid] = vkh;
+    if (tid < NKW) KwP[tid] = vkw;
     }
     __syncthreads();
     if (!wok) return;
@@ -521,6 +544,14 @@ __device__ __forceinline__ f32x16 tshift(const f32x16& v, uint32_t hm) {
     return w;
 }
 
+// LDS pitches (elements) of the backward kernel's tiles, fixed per type:
+// factor tables [32][C + pad], bf16 transposed Us [C][40], dY tile [C][LY],
+// X ring [3][C][LX] (8-byte bf16 / 16-byte fp32 column runs stay aligned).
+template <typename T, int C> constexpr int cp_bwd_pitch_s() { return sizeof(T) == 2 ? C + 8 : C + 1; }
+template <typename T> constexpr int cp_bwd_pitch_u() { return 40; }
+template <typename T> constexpr int cp_bwd_pitch_y() { return sizeof(T) == 2 ? 40 : 33; }
+template <typename T> constexpr int cp_bwd_pitch_x() { return sizeof(T) == 2 ? 40 : 36; }
+
 template <typename T, int KH, int KW, int MT, int MS>
 __global__ void __launch_bounds__(256, 1)
     cp_bwd(CpBwdDesc d, const T* __restrict__ X, const T* __restrict__ dY,
@@ -531,6 +562,10 @@ __global__ void __launch_bounds__(256, 1)
     constexpr int NT = 32 * MT, NS = 32 * MS;
     constexpr int CH = (KH - 1) / 2, CW = (KW - 1) / 2;
     constexpr int LZ = 33;   // dZ1 transpose tile pitch (floats)
+    // LDS pitches (elements) of the factor tables, the dY tile and the X ring;
+    // the launcher checks that the descriptor's layout uses the same
+    constexpr int LDA_S = cp_bwd_pitch_s<T, NS>(), LDA_T = cp_bwd_pitch_s<T, NT>();
+    constexpr int LDU = cp_bwd_pitch_u<T>(), LY = cp_bwd_pitch_y<T>(), LX = cp_bwd_pitch_x<T>();
     static_assert(KW == 3, "column shifts of one");
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int H = d.H, W = d.W;
@@ -607,18 +642,17 @@ __global__ void __launch_bounds__(256, 1)
     // dX: a zero range drops every store when the gradient is not wanted
     const __amdgpu_buffer_rsrc_t rD =
         brsrc(dX ? (const T*)dX + (int64_t)b * d.x_sb : X, dX ? (uint32_t)(d.S * d.x_ss * E) : 0u);
-    const uint32_t dx0 = ownlane ? (uint32_t)(col * (int)E) : kOut;
+    const uint32_t dx0 = ownlane ? (uint32_t)(col * (int)E) + 4u * hf * xcs : kOut;
     constexpr int PW = Slots<T>::per_word;
     uint32_t xa[NS / 2 / PW], ya[NT / 2 / PW];
     // the X row held in xa into ring slot `slot` (channel-major), for the dUs
     // product CH rows later; X row r sits in slot (r - (hs - CH)) % 3
-    const int lx = d.lx;
     auto xl_put = [&](int slot, const uint32_t (&src)[NS / 2 / PW]) {
-        T* dst = Xl + slot * NS * lx + cl;
+        T* dst = Xl + slot * NS * LX + cl;
 #pragma unroll
         for (int u = 0; u < NS / 2; u++) {
-            if constexpr (BF) dst[achan<BF>(u, hf) * lx] = (T)src[u];
-            else dst[achan<BF>(u, hf) * lx] = __uint_as_float(src[u]);
+            if constexpr (BF) dst[achan<BF>(u, hf) * LX] = (T)src[u];
+            else dst[achan<BF>(u, hf) * LX] = __uint_as_float(src[u]);
         }
     };
     // Every operand of the ring fill and the first row is requested before
@@ -631,30 +665,47 @@ __global__ void __launch_bounds__(256, 1)
         arow<T, NT>(ya, rY, yoff(hs), ycs);
     }
     // ---- tables: UsA [32][lda_s], UtA [32][lda_t] (and UsT [NS][ldu] for bf16) ----
+    // Each thread issues all of its table loads before any LDS store, so that
+    // their memory latencies overlap.
     {
+        constexpr int QS = NS / 8, QT = NT / 8;   // elements a thread (256 threads)
+        T vs[QS], vt[QT], vu[QS];
+#pragma unroll
+        for (int q = 0; q < QS; q++) {
+            const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
+            vs[q] = Us[r * d.us_sr + s * d.us_ss];
+            if constexpr (BF) {
+                const int s2 = e / 32, r2 = e - s2 * 32;
+                vu[q] = Us[r2 * d.us_sr + s2 * d.us_ss];
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < QT; q++) {
+            const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
+            vt[q] = Ut[r * d.ut_sr + t * d.ut_st];
+        }
         T* usa = (T*)smem;
         T* uta = (T*)(smem + d.o_uta);
-        for (int e = tid; e < 32 * NS; e += 256) {
-            int r = e / NS, s = e - r * NS;
-            usa[r * d.lda_s + s] = Us[r * d.us_sr + s * d.us_ss];
-        }
-        for (int e = tid; e < 32 * NT; e += 256) {
-            int r = e / NT, t = e - r * NT;
-            uta[r * d.lda_t + t] = Ut[r * d.ut_sr + t * d.ut_st];
-        }
-        if constexpr (BF) {
-            T* ust = (T*)(smem + d.o_ust);
-            for (int e = tid; e < 32 * NS; e += 256) {
-                int s = e / 32, r = e - s * 32;
-                ust[s * d.ldu + r] = Us[r * d.us_sr + s * d.us_ss];
+#pragma unroll
+        for (int q = 0; q < QS; q++) {
+            const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
+            usa[r * LDA_S + s] = vs[q];
+            if constexpr (BF) {
+                const int s2 = e / 32, r2 = e - s2 * 32;
+                ((T*)(smem + d.o_ust))[s2 * LDU + r2] = vu[q];
             }
+        }
+#pragma unroll
+        for (int q = 0; q < QT; q++) {
+            const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
+            uta[r * LDA_T + t] = vt[q];
         }
     }
     __syncthreads();
     if (wok) {
 #pragma unroll
         for (int j = 0; j < KH - 1; j++) {
-            ring[j] = tgemm<T, NS>(xp[j], UsA, d.lda_s, cl, hf);
+            ring[j] = tgemm<T, NS>(xp[j], UsA, LDA_S, cl, hf);
             xl_put(j, xp[j]);
         }
     }
@@ -675,14 +726,14 @@ __global__ void __launch_bounds__(256, 1)
         // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
         f32x16 z1n;
         if constexpr (decltype(Z1N)::value) {
-            z1n = tgemm<T, NS>(xa, UsA, d.lda_s, cl, hf);
+            z1n = tgemm<T, NS>(xa, UsA, LDA_S, cl, hf);
         } else {
 #pragma unroll
             for (int i = 0; i < 16; i++) z1n[i] = 0.f;
         }
         xl_put((k + 2) % 3, xa);
         arow<T, NS>(xa, rX, xoff(h + 1 + CH), xcs);
-        const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, d.lda_t, cl, hf);
+        const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, LDA_T, cl, hf);
         ring[KH - 1] = z1n;
         // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1)
         f32x16 z2, z3, zm, zp;
@@ -702,8 +753,8 @@ __global__ void __launch_bounds__(256, 1)
             // dY[h] into the LDS tile of the dUt product
 #pragma unroll
             for (int u = 0; u < NT / 2; u++) {
-                if constexpr (BF) Yt[achan<BF>(u, hf) * d.ly + cl] = (T)ya[u];
-                else Yt[achan<BF>(u, hf) * d.ly + cl] = __uint_as_float(ya[u]);
+                if constexpr (BF) Yt[achan<BF>(u, hf) * LY + cl] = (T)ya[u];
+                else Yt[achan<BF>(u, hf) * LY + cl] = __uint_as_float(ya[u]);
             }
         }
         arow<T, NT>(ya, rY, yoff(h + 1), ycs);
@@ -733,7 +784,7 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
                     for (int n = 0; n < MT; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
-                        const bf16_t* yr = Yt + (32 * n + cl) * d.ly + 16 * q + 4 * hf;
+                        const bf16_t* yr = Yt + (32 * n + cl) * LY + 16 * q + 4 * hf;
                         bf16_t bv[8];
                         __builtin_memcpy(bv, yr, 8);
                         __builtin_memcpy(bv + 4, yr + 8, 8);
@@ -743,15 +794,15 @@ __global__ void __launch_bounds__(256, 1)
             } else {
                 // chunk c: columns tcol(2c, hf) and tcol(2c + 1, hf) (adjacent) of each
                 // channel block, three chunks ahead
-                const float* yb = Yt + cl * d.ly + 4 * hf;
+                const float* yb = Yt + cl * LY + 4 * hf;
                 piped<8, 3, 2 * MT>(
                     [&](int c) {
                         Opnd<2 * MT> o;
                         const int cc = 8 * (c >> 1) + 2 * (c & 1);   // tcol(2c, hf) - 4hf
 #pragma unroll
                         for (int n = 0; n < MT; n++) {
-                            o.v[2 * n] = yb[32 * n * d.ly + cc];
-                            o.v[2 * n + 1] = yb[32 * n * d.ly + cc + 1];
+                            o.v[2 * n] = yb[32 * n * LY + cc];
+                            o.v[2 * n + 1] = yb[32 * n * LY + cc + 1];
                         }
                         return o;
                     },
@@ -814,7 +865,7 @@ __global__ void __launch_bounds__(256, 1)
                 for (int i = 0; i < 16; i++) accX[n][i] = 0.f;
             // dUs += dZ1[hx] X[hx]^T, X row hx from its ring slot (channel 32n + cl)
             const f32x16 dz1o = own_cols(dz1);
-            const T* xrow = Xl + (k % 3) * NS * lx + cl * lx;
+            const T* xrow = Xl + (k % 3) * NS * LX + cl * LX;
             if constexpr (BF) {
 #pragma unroll
                 for (int q = 0; q < 2; q++) {
@@ -824,7 +875,7 @@ __global__ void __launch_bounds__(256, 1)
                     const bf16x8 bv = cvt8(zf);
 #pragma unroll
                     for (int n = 0; n < MS; n++)
-                        accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsT + (32 * n + cl) * d.ldu + 16 * q + 8 * hf),
+                        accX[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsT + (32 * n + cl) * LDU + 16 * q + 8 * hf),
                                                                           bv, accX[n], 0, 0, 0);
                 }
 #pragma unroll
@@ -836,7 +887,7 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
                     for (int n = 0; n < MS; n++) {
                         // columns tcol(8q + j, hf): 16q + 4hf + {0..3} and 16q + 8 + 4hf + {0..3}
-                        const bf16_t* xr = xrow + (32 * n) * lx + 16 * q + 4 * hf;
+                        const bf16_t* xr = xrow + (32 * n) * LX + 16 * q + 4 * hf;
                         bf16_t bv[8];
                         __builtin_memcpy(bv, xr, 8);
                         __builtin_memcpy(bv + 4, xr + 8, 8);
@@ -850,14 +901,14 @@ __global__ void __launch_bounds__(256, 1)
                 // whose reads of the dZ1 tile are in flight while dUs runs.
                 constexpr int NO = 4 * MS > 2 * MS + 2 ? 4 * MS : 2 * MS + 2;
                 const float* tzr = Tz + cl * LZ + hf;
-                const float* usr = UsA + hf * d.lda_s + cl;
+                const float* usr = UsA + hf * LDA_S + cl;
                 piped<12, 3, NO>(
                     [&](int c) {
                         Opnd<NO> o;
                         if (c < 4) {
 #pragma unroll
                             for (int n = 0; n < MS; n++) {
-                                const float4 t = *reinterpret_cast<const float4*>(xrow + (32 * n) * lx + 8 * c + 4 * hf);
+                                const float4 t = *reinterpret_cast<const float4*>(xrow + (32 * n) * LX + 8 * c + 4 * hf);
                                 o.v[4 * n] = t.x;
                                 o.v[4 * n + 1] = t.y;
                                 o.v[4 * n + 2] = t.z;
@@ -868,7 +919,7 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
                             for (int j = 0; j < 2; j++) {
 #pragma unroll
-                                for (int n = 0; n < MS; n++) o.v[j * MS + n] = usr[2 * (u + j) * d.lda_s + 32 * n];
+                                for (int n = 0; n < MS; n++) o.v[j * MS + n] = usr[2 * (u + j) * LDA_S + 32 * n];
                                 o.v[2 * MS + j] = tzr[2 * (u + j)];
                             }
                         }
@@ -894,12 +945,16 @@ __global__ void __launch_bounds__(256, 1)
                     });
             }
             mfma_drain();   // accX is read by the stores
-            const uint32_t v0 = dx0 + (uint32_t)(hx * W) * E;
+            // lane offset of row hx (channel 4hf, or 4hf + 1); the even part of
+            // the channel goes in the uniform offset, the same as the loads'
+            const uint32_t v0 = dx0 + (uint32_t)(hx * W) * E, v1 = v0 + xcs;
 #pragma unroll
             for (int n = 0; n < MS; n++)
 #pragma unroll
-                for (int i = 0; i < 16; i++)
-                    bstore(accX[n][i], (T*)nullptr, rD, v0 + (uint32_t)(n * 32 + row32(i, lane)) * xcs);
+                for (int i = 0; i < 16; i++) {
+                    const int c = 32 * n + row32(i, 0);   // + 4hf, in dx0
+                    bstore(accX[n][i], (T*)nullptr, rD, (c & 1) ? v1 : v0, (uint32_t)(2 * (c >> 1)) * xcs);
+                }
         }
     };
     // Rows hs = h0 - 1 (halo), h0 (no dX row yet), h0 + 1 .. h1 - 1 and h1
@@ -963,6 +1018,10 @@ constexpr uint32_t kMaxLds = 160 * 1024;   // LDS of one gfx950 CU
 template <typename T, int K, int M>
 hipError_t launch_cpb_t(const CpBwdDesc& d, const void* const* o, hipStream_t s) {
     auto k = cp_bwd<T, K, K, M, M>;
+    // the kernel's compile-time LDS pitches must be the descriptor's
+    if (d.lda_s != cp_bwd_pitch_s<T, 32 * M>() || d.lda_t != cp_bwd_pitch_s<T, 32 * M>() || d.ly != cp_bwd_pitch_y<T>() ||
+        d.lx != cp_bwd_pitch_x<T>() || (sizeof(T) == 2 && d.ldu != cp_bwd_pitch_u<T>()))
+        return hipErrorInvalidValue;
     // dynamic LDS above 64 KB has to be allowed per kernel, once per device
     static std::atomic<uint64_t> allowed{0};
     int dev = 0;
