@@ -121,12 +121,20 @@ __device__ __forceinline__ bf16x8 pack_words(const uint32_t* w) {
 // Operands of one chunk of an MFMA chain, read from LDS ahead of use.
 template <int N> struct Opnd { float v[N]; };
 
+// No side work (see piped).
+struct NoSide {
+    __device__ void operator()(int) const {}
+};
+
 // Runs the MFMA chunks mm(c, buf[c]) for c = 0..NC-1 with the LDS operands of
 // chunk c + D requested (ld) before chunk c's MFMAs issue; the scheduling
 // fences keep that order, so each chunk's LDS latency hides behind D chunks of
-// MFMA work instead of stalling the chain at every step.
-template <int NC, int D, int N, typename Ld, typename Mm>
-__device__ __forceinline__ void piped(Ld ld, Mm mm) {
+// MFMA work instead of stalling the chain at every step.  side(c) is further
+// memory work (LDS writes, global loads and stores) issued with chunk c: such
+// instructions issue while a 32x32x2 fp32 MFMA executes (VALU instructions do
+// not), so spread over the chain they cost no time of their own.
+template <int NC, int D, int N, typename Ld, typename Mm, typename Sd = NoSide>
+__device__ __forceinline__ void piped(Ld ld, Mm mm, Sd side = {}) {
     Opnd<N> buf[NC];
 #pragma unroll
     for (int c = 0; c < (D < NC ? D : NC); c++) buf[c] = ld(c);
@@ -135,6 +143,7 @@ __device__ __forceinline__ void piped(Ld ld, Mm mm) {
         if (c + D < NC) buf[c + D] = ld(c + D);
         __builtin_amdgcn_sched_barrier(0);
         mm(c, buf[c]);
+        side(c);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -148,18 +157,22 @@ __device__ __forceinline__ int achan(int u, int hf) {
 }
 
 // Z^T[col][r] = sum_k a[k][col] tab[r][k]: a = one activation row in A-operand
-// slots (K/2 values a lane), tab = [32][lda] factor table in LDS.
-template <typename T, int K, bool DRAIN = true>
+// slots (K/2 values a lane), tab = [32][lda] factor table in LDS.  side(c),
+// c = 0..K/4-1, is memory work issued along the chain (see piped).
+template <typename T, int K, bool DRAIN = true, typename Sd = NoSide>
 __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::per_word], const T* tab, int lda,
-                                        int cl, int hf) {
+                                        int cl, int hf, Sd side = {}) {
     f32x16 acc;
 #pragma unroll
     for (int i = 0; i < 16; i++) acc[i] = 0.f;
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int q = 0; q < K / 16; q++)
+        for (int q = 0; q < K / 16; q++) {
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack_words(a + 8 * q), lds8(tab + cl * lda + 16 * q + 8 * hf),
                                                           acc, 0, 0, 0);
+#pragma unroll
+            for (int c = 4 * q; c < 4 * q + 4; c++) side(c);
+        }
     } else {
         // MFMA u takes k = 2u + hf; chunks of two MFMAs, operands four chunks ahead
         const float* tb = tab + cl * lda + hf;
@@ -173,7 +186,8 @@ __device__ __forceinline__ f32x16 tgemm(const uint32_t (&a)[K / 2 / Slots<T>::pe
             [&](int c, const Opnd<2>& o) {
                 acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[2 * c]), o.v[0], acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[2 * c + 1]), o.v[1], acc, 0, 0, 0);
-            });
+            },
+            side);
     }
     if constexpr (DRAIN) mfma_drain();
     return acc;
@@ -222,6 +236,15 @@ __device__ __forceinline__ void arow(uint32_t (&a)[K / 2], __amdgpu_buffer_rsrc_
         else
             a[u] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)(2 * u * cs), 0);
     }
+}
+
+// A-operand slot u of an activation row (one element of arow).
+template <typename T>
+__device__ __forceinline__ uint32_t aslot(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t cs, int u) {
+    if constexpr (sizeof(T) == 2)
+        return __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)((16 * (u >> 3) + (u & 7)) * cs), 0);
+    else
+        return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)(2 * u * cs), 0);
 }
 
 // Two blocks per CU (256 VGPRs a lane) except for the bf16 5x5 variant, whose
@@ -655,6 +678,16 @@ __global__ void __launch_bounds__(256, 1)
             else dst[achan<BF>(u, hf) * LX] = __uint_as_float(src[u]);
         }
     };
+    auto xl_one = [&](int slot, int u, uint32_t v) {
+        T* dst = Xl + slot * NS * LX + achan<BF>(u, hf) * LX + cl;
+        if constexpr (BF) *dst = (T)v;
+        else *dst = __uint_as_float(v);
+    };
+    f32x16 accXp[MS];   // the dX row of the previous row, stored along the next row's first chain
+#pragma unroll
+    for (int n = 0; n < MS; n++)
+#pragma unroll
+        for (int i = 0; i < 16; i++) accXp[n][i] = 0.f;
     // Every operand of the ring fill and the first row is requested before
     // the factor tables load, so that their memory latencies overlap.
     uint32_t xp[KH - 1][NS / 2 / PW];
@@ -719,20 +752,43 @@ __global__ void __launch_bounds__(256, 1)
     // instances of the row code (compile-time flags) without those products,
     // and the last row also without Z1[h + CH], which only they would read;
     // the loop body itself stays free of branches.
-    auto row_step = [&](int h, auto RIN, auto XIN, auto Z1N) {
+    auto row_step = [&](int h, auto RIN, auto XIN, auto Z1N, auto PST) {
         constexpr bool rin = decltype(RIN)::value, xin = decltype(XIN)::value;
+        constexpr bool z1 = decltype(Z1N)::value, pst = decltype(PST)::value;
         const int hx = h - CH;
         const int k = h - hs;   // ring slots: X row h + CH goes to (k + 2) % 3, row hx is read from k % 3
-        // Z1[h+CH] and dZ3[h]; the next row's operands are loaded right behind
+        // Memory work rides on the MFMA chains (see piped):
+        //   along Z1[h+CH]: dY[h] into the LDS tile of the dUt product, and the
+        //                   stores of the dX row of the previous row (pst)
+        //   along dUt:      X row h + CH into its ring slot and the loads of X
+        //                   row h + 1 + CH (rows followed by another: z1)
+        //   along dUs, dX:  the loads of dY[h + 1] (z1)
+        // Rows without one of those products issue its share on their own.
+        const uint32_t pv0 = dx0 + (uint32_t)((hx - 1) * W) * E, pv1 = pv0 + xcs;
+        const uint32_t xo = xoff(h + 1 + CH), yo = yoff(h + 1);   // the next rows' operands
+        auto side_a = [&](int c) {
+#pragma unroll
+            for (int j = 0; j < 2; j++) {
+                const int u = 2 * c + j;   // 0 .. NS/2 - 1 (= NT/2 - 1)
+                if constexpr (rin) {
+                    if constexpr (BF) Yt[achan<BF>(u, hf) * LY + cl] = (T)ya[u];
+                    else Yt[achan<BF>(u, hf) * LY + cl] = __uint_as_float(ya[u]);
+                }
+                if constexpr (pst) {
+                    const int n = u >> 4, i = u & 15, ch = 32 * n + row32(i, 0);   // + 4hf, in dx0
+                    bstore(accXp[n][i], (T*)nullptr, rD, (ch & 1) ? pv1 : pv0, (uint32_t)(2 * (ch >> 1)) * xcs);
+                }
+            }
+        };
         f32x16 z1n;
-        if constexpr (decltype(Z1N)::value) {
-            z1n = tgemm<T, NS>(xa, UsA, LDA_S, cl, hf);
+        if constexpr (z1) {
+            z1n = tgemm<T, NS>(xa, UsA, LDA_S, cl, hf, side_a);
         } else {
 #pragma unroll
             for (int i = 0; i < 16; i++) z1n[i] = 0.f;
+#pragma unroll
+            for (int c = 0; c < NS / 4; c++) side_a(c);
         }
-        xl_put((k + 2) % 3, xa);
-        arow<T, NS>(xa, rX, xoff(h + 1 + CH), xcs);
         const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, LDA_T, cl, hf);
         ring[KH - 1] = z1n;
         // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1)
@@ -749,15 +805,28 @@ __global__ void __launch_bounds__(256, 1)
             zp = tshift<1>(z2, hm);
 #pragma unroll
             for (int i = 0; i < 16; i++) z3[i] = kw[0] * zm[i] + kw[1] * z2[i] + kw[2] * zp[i];
-            __builtin_amdgcn_sched_barrier(0);   // the next row's dY loads stay behind the chain
-            // dY[h] into the LDS tile of the dUt product
-#pragma unroll
-            for (int u = 0; u < NT / 2; u++) {
-                if constexpr (BF) Yt[achan<BF>(u, hf) * LY + cl] = (T)ya[u];
-                else Yt[achan<BF>(u, hf) * LY + cl] = __uint_as_float(ya[u]);
-            }
         }
-        arow<T, NT>(ya, rY, yoff(h + 1), ycs);
+        auto side_c = [&](int c) {   // c = 0..7
+            if constexpr (z1) {
+                constexpr int PX = NS / 16;
+#pragma unroll
+                for (int j = 0; j < PX; j++) {
+                    const int u = c * PX + j;
+                    xl_one((k + 2) % 3, u, xa[u]);
+                    xa[u] = aslot<T>(rX, xo, xcs, u);
+                }
+            }
+        };
+        auto side_d = [&](int c) {   // c = 0..11
+            if constexpr (z1) {
+                constexpr int PY = (NT / 2 + 11) / 12;
+#pragma unroll
+                for (int j = 0; j < PY; j++) {
+                    const int u = c * PY + j;
+                    if (u < NT / 2) ya[u] = aslot<T>(rY, yo, ycs, u);
+                }
+            }
+        };
         mfma_drain();   // dz3 is read below
         if constexpr (rin) {
             // dKw products
@@ -790,6 +859,8 @@ __global__ void __launch_bounds__(256, 1)
                         __builtin_memcpy(bv + 4, yr + 8, 8);
                         accUt[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pack8(bv), accUt[n], 0, 0, 0);
                     }
+#pragma unroll
+                    for (int c = 4 * q; c < 4 * q + 4; c++) side_c(c);
                 }
             } else {
                 // chunk c: columns tcol(2c, hf) and tcol(2c + 1, hf) (adjacent) of each
@@ -814,8 +885,12 @@ __global__ void __launch_bounds__(256, 1)
                             for (int n = 0; n < MT; n++)
                                 accUt[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, o.v[2 * n + j], accUt[n], 0, 0, 0);
                         }
-                    });
+                    },
+                    side_c);
             }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 8; c++) side_c(c);
         }
         // dZ2[h]: transposed conv along w (tap j reads column - j + 1)
         f32x16 dz2;
@@ -858,7 +933,7 @@ __global__ void __launch_bounds__(256, 1)
             asm volatile("" ::: "memory");
 #pragma unroll
             for (int i = 0; i < 16; i++) Tz[tcol(i, hf) * LZ + cl] = dz1[i];
-            f32x16 accX[MS];
+            f32x16 (&accX)[MS] = accXp;   // stored along the next row's first chain
 #pragma unroll
             for (int n = 0; n < MS; n++)
 #pragma unroll
@@ -942,38 +1017,46 @@ __global__ void __launch_bounds__(256, 1)
                                     accX[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(o.v[j * MS + n], o.v[2 * MS + j],
                                                                                    accX[n], 0, 0, 0);
                         }
-                    });
+                    },
+                    side_d);
+            }
+            if constexpr (BF) {
+#pragma unroll
+                for (int c = 0; c < 12; c++) side_d(c);
             }
             mfma_drain();   // accX is read by the stores
-            // lane offset of row hx (channel 4hf, or 4hf + 1); the even part of
-            // the channel goes in the uniform offset, the same as the loads'
-            const uint32_t v0 = dx0 + (uint32_t)(hx * W) * E, v1 = v0 + xcs;
+        } else {
 #pragma unroll
-            for (int n = 0; n < MS; n++)
-#pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const int c = 32 * n + row32(i, 0);   // + 4hf, in dx0
-                    bstore(accX[n][i], (T*)nullptr, rD, (c & 1) ? v1 : v0, (uint32_t)(2 * (c >> 1)) * xcs);
-                }
+            for (int c = 0; c < 12; c++) side_d(c);
         }
     };
     // Rows hs = h0 - 1 (halo), h0 (no dX row yet), h0 + 1 .. h1 - 1 and h1
     // (halo).  The first full row runs outside the loop: the loop is then
-    // entered, like its back edge, right after a row's stores, so the wait
-    // counts the compiler derives for the prefetched operands at the loop
-    // head are those of the steady state (entered otherwise, they force every
-    // row to wait for almost all outstanding memory operations).
+    // entered, like its back edge, with a dX row pending and the same memory
+    // operations outstanding, so the wait counts the compiler derives for the
+    // prefetched operands at the loop head are those of the steady state.
     static_assert(CH == 1, "one halo row on each side");
     const std::true_type yes;
     const std::false_type no;
     if (wok) {
-        row_step(hs, no, no, yes);
-        row_step(h0, yes, no, yes);
+        row_step(hs, no, no, yes, no);
+        row_step(h0, yes, no, yes, no);
         if (h0 + 1 < h1) {
-            row_step(h0 + 1, yes, yes, yes);
-            for (int h = h0 + 2; h < h1; h++) row_step(h, yes, yes, yes);
+            row_step(h0 + 1, yes, yes, yes, no);
+            for (int h = h0 + 2; h < h1; h++) row_step(h, yes, yes, yes, yes);
+            row_step(h1, no, yes, no, yes);
+        } else {
+            row_step(h1, no, yes, no, no);
         }
-        row_step(h1, no, yes, no);
+        // the dX row of the last row
+        const uint32_t v0 = dx0 + (uint32_t)((h1 - CH) * W) * E, v1 = v0 + xcs;
+#pragma unroll
+        for (int n = 0; n < MS; n++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) {
+                const int ch = 32 * n + row32(i, 0);
+                bstore(accXp[n][i], (T*)nullptr, rD, (ch & 1) ? v1 : v0, (uint32_t)(2 * (ch >> 1)) * xcs);
+            }
     }
 
     // ---- block sums of the wavefront partials, in a fixed order ----
