@@ -79,8 +79,10 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     // register-resident strips: rank 32, S and T in {32, 64}, 3x3 or 5x5 filters
     if (R != 32 || !(T == 32 || T == 64) || !(S == 32 || S == 64) || h.K != w.K || !(h.K == 3 || h.K == 5))
         return false;
-    // one sample of X within a 32-bit byte range (raw buffer loads)
+    // one sample of X and of Y within a 32-bit byte range (raw buffer loads and
+    // stores), both with channel stride H*W
     if (S * a.sBk * (dt ? 2 : 4) >= (1ll << 31) || a.sBk != H * W) return false;
+    if (T * c.sCm * (dt ? 2 : 4) >= (1ll << 31) || c.sCm != H * W) return false;
     CpDesc d;
     std::memset(&d, 0, sizeof(d));
     d.B = (int32_t)B;

@@ -281,8 +281,8 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const int col = cb * d.colstride - HWW + (lane & 31);
     const bool colok = col >= 0 && col < W;
     const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
-    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
     const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
+    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
     const int cl = lane & 31;
 
     // X rows as B-operand slots (the same slot layout as arow), loaded one row
@@ -294,21 +294,35 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
     auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
     uint32_t xa[NS / 2];
-    // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in a
-    auto gemm1 = [&](const uint32_t (&a)[NS / 2]) {
+    // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in a; side(c),
+    // c = 0..NS/4-1, is memory work issued along the chain (see piped)
+    auto gemm1 = [&](const uint32_t (&a)[NS / 2], auto side) {
         f32x16 acc;
 #pragma unroll
         for (int i = 0; i < 16; i++) acc[i] = 0.f;
         if constexpr (BF) {
 #pragma unroll
-            for (int q = 0; q < NS / 16; q++)
+            for (int q = 0; q < NS / 16; q++) {
                 acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(UsL + cl * LDA + 16 * q + 8 * half),
                                                               pack_words(a + 8 * q), acc, 0, 0, 0);
-        } else {
 #pragma unroll
-            for (int u = 0; u < NS / 2; u++)
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(UsL[cl * LDA + 2 * u + half], __uint_as_float(a[u]),
-                                                           acc, 0, 0, 0);
+                for (int c = 4 * q; c < 4 * q + 4; c++) side(c);
+            }
+        } else {
+            // MFMA u takes channel 2u + half; chunks of two MFMAs, operands four chunks ahead
+            const T* ub = UsL + cl * LDA + half;
+            piped<NS / 4, 4, 2>(
+                [&](int c) {
+                    Opnd<2> o;
+                    o.v[0] = ub[4 * c];
+                    o.v[1] = ub[4 * c + 2];
+                    return o;
+                },
+                [&](int c, const Opnd<2>& o) {
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(o.v[0], __uint_as_float(a[2 * c]), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(o.v[1], __uint_as_float(a[2 * c + 1]), acc, 0, 0, 0);
+                },
+                side);
         }
         mfma_drain();
         return acc;
@@ -375,12 +389,27 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     f32x16 ring[KH];
 #pragma unroll
     for (int j = 0; j < KH - 1; j++) {
-        ring[j] = gemm1(xp[j % NP]);
+        ring[j] = gemm1(xp[j % NP], NoSide{});
         if (j + NP < KH) arow<T, NS>(xp[j % NP], rX, xoff(h0 - CH + j + NP), xcs);
     }
 #pragma unroll
     for (int u = 0; u < NS / 2; u++) xa[u] = xp[(KH - 1) % NP][u];
-    auto fwd_row = [&](int h) {
+    // Y rows through a raw buffer (one sample; stores past the range are
+    // dropped): the lane's column and channel 4*half in the lane offset, the
+    // rest of the channel in the uniform offset (Y's channel stride is X's)
+    const __amdgpu_buffer_rsrc_t rYo = brsrc(Y + (int64_t)b * d.y_sb, (uint32_t)(TT * d.x_ss * E));
+    const uint32_t yv0 = store_lane ? (uint32_t)(col * E) + 4u * half * xcs : kOut;
+    // Y row h - 1, stored along the next row's first chain
+    f32x16 accYp[MB2];
+#pragma unroll
+    for (int mb = 0; mb < MB2; mb++)
+#pragma unroll
+        for (int i = 0; i < 16; i++) accYp[mb][i] = 0.f;
+    auto store_y = [&](int item, uint32_t v0) {   // item = 16 mb + i
+        const int mb = item >> 4, i = item & 15, ch = 32 * mb + row32(i, 0);   // + 4 half, in yv0
+        bstore(accYp[mb][i], (T*)nullptr, rYo, (ch & 1) ? v0 + xcs : v0, (uint32_t)(2 * (ch >> 1)) * xcs);
+    };
+    auto fwd_row = [&](int h, auto PST) {
         // The tap and Ut tables are re-read from LDS every row: the offsets
         // pass through an empty asm so the loads are not hoisted out of the
         // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
@@ -389,8 +418,29 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         const T* UtP = (const T*)(smem + o_ut);
         const float* KhP = (const float*)(smem + o_kh);
         const float* KwP = (const float*)(smem + o_kw);
-        ring[KH - 1] = gemm1(xa);
-        arow<T, NS>(xa, rX, xoff(h + KH - CH), xcs);   // the next row's, used one row later
+        // fp32: memory work along the chains (their MFMAs leave the issue free
+        // for it): the stores of Y row h - 1 along Z1 (pst), the loads of the
+        // next X row along GEMM2.  bf16 (short chains): the loads right after
+        // Z1, the stores at the end of the row.
+        const uint32_t pv0 = yv0 + (uint32_t)((h - 1) * W) * E;
+        auto side_a = [&](int c) {   // c = 0..NS/4-1
+            if constexpr (!BF && decltype(PST)::value) {
+                constexpr int NC = NS / 4, PS = (16 * MB2 + NC - 1) / NC;
+#pragma unroll
+                for (int j = 0; j < PS; j++)
+                    if (c * PS + j < 16 * MB2) store_y(c * PS + j, pv0);
+            }
+        };
+        ring[KH - 1] = gemm1(xa, side_a);
+        const uint32_t xo = xoff(h + KH - CH);   // the next row's, used one row later
+        if constexpr (BF) arow<T, NS>(xa, rX, xo, xcs);
+        auto side_b = [&](int c) {   // c = 0..15
+            if constexpr (BF) return;
+            constexpr int PX = (NS / 2 + 15) / 16;
+#pragma unroll
+            for (int j = 0; j < PX; j++)
+                if (c * PX + j < NS / 2) xa[c * PX + j] = aslot<T>(rX, xo, xcs, c * PX + j);
+        };
         // conv along h
         f32x16 z2;
 #pragma unroll
@@ -420,8 +470,9 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
             for (int jw = 0; jw < KW; jw++) a += KwP[(i * 2 + half) * KW + jw] * sh[jw];
             z3[i] = a;
         }
-        // GEMM2: Y[t][col] = sum_r Ut[r][t] Z3[r][col]
-        f32x16 acc2[MB2];
+        // GEMM2: Y[t][col] = sum_r Ut[r][t] Z3[r][col] (fp32: into accYp, stored
+        // along the next row's first chain)
+        auto gemm2 = [&](f32x16 (&acc2)[MB2]) {
 #pragma unroll
         for (int mb = 0; mb < MB2; mb++)
 #pragma unroll
@@ -440,32 +491,52 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
                 }
             }
         } else {
+            // chunk i: rank row32(i, half) of each channel block, three chunks ahead
+            const T* ut = UtP + half * TT + (lane & 31);
+            piped<16, 3, MB2>(
+                [&](int i) {
+                    Opnd<MB2> o;
 #pragma unroll
-            for (int i = 0; i < 16; i++) {
+                    for (int mb = 0; mb < MB2; mb++) o.v[mb] = ut[2 * i * TT + mb * 32];
+                    return o;
+                },
+                [&](int i, const Opnd<MB2>& o) {
 #pragma unroll
-                for (int mb = 0; mb < MB2; mb++) {
-                    float av = UtP[(i * 2 + half) * TT + mb * 32 + (lane & 31)];
-                    acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, z3[i], acc2[mb], 0, 0, 0);
-                }
-            }
+                    for (int mb = 0; mb < MB2; mb++)
+                        acc2[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(o.v[mb], z3[i], acc2[mb], 0, 0, 0);
+                },
+                side_b);
         }
-        mfma_drain();
-        if (store_lane) {
-            T* yr = Yc + (int64_t)h * W;
+        mfma_drain();   // acc2 is read by the stores
+        };
+        if constexpr (BF) {
+            f32x16 acc2[MB2];
+            gemm2(acc2);
+            if (store_lane) {
+                T* yr = Yc + (int64_t)h * W;
 #pragma unroll
-            for (int mb = 0; mb < MB2; mb++)
+                for (int mb = 0; mb < MB2; mb++)
 #pragma unroll
-                for (int i = 0; i < 16; i++)
-                    store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
+                    for (int i = 0; i < 16; i++)
+                        store(yr, (int64_t)(mb * 32 + row32(i, lane)) * d.y_st, acc2[mb][i]);
+            }
+        } else {
+            gemm2(accYp);
         }
     };
     // The first row runs outside the loop: the loop is then entered, like its
-    // back edge, right after a row's stores, so the wait counts the compiler
-    // derives for the prefetched X row at the loop head are those of the
-    // steady state (entered from the prologue, every row would wait for all
-    // outstanding memory operations, the previous row's stores included).
-    if (h0 < h1) fwd_row(h0);
-    for (int h = h0 + 1; h < h1; h++) fwd_row(h);
+    // back edge, with a Y row pending and the same memory operations
+    // outstanding, so the wait counts the compiler derives for the prefetched
+    // X row at the loop head are those of the steady state.
+    const std::true_type yes;
+    const std::false_type no;
+    fwd_row(h0, no);
+    for (int h = h0 + 1; h < h1; h++) fwd_row(h, yes);
+    if constexpr (!BF) {
+        const uint32_t lv0 = yv0 + (uint32_t)((h1 - 1) * W) * E;
+#pragma unroll
+        for (int item = 0; item < 16 * MB2; item++) store_y(item, lv0);
+    }
 }
 
 template <typename T, int K, int MB2>
