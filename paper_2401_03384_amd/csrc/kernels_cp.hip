@@ -829,22 +829,19 @@ __global__ void __launch_bounds__(256, 1)
         const int hx = h - CH;
         const int k = h - hs;   // ring slots: X row h + CH goes to (k + 2) % 3, row hx is read from k % 3
         // Memory work rides on the MFMA chains (see piped):
-        //   along Z1[h+CH]: dY[h] into the LDS tile of the dUt product, and the
-        //                   stores of the dX row of the previous row (pst)
+        //   along Z1[h+CH]: the stores of the dX row of the previous row (pst)
         //   along dUt:      X row h + CH into its ring slot and the loads of X
         //                   row h + 1 + CH (rows followed by another: z1)
-        //   along dUs, dX:  the loads of dY[h + 1] (z1)
+        //   along dUs:      the loads of dY[h + 1] (z1)
         // Rows without one of those products issue its share on their own.
+        // Loaded rows are first used about half a row later or more: under
+        // the full load of the chip a load takes several microseconds.
         const uint32_t pv0 = dx0 + (uint32_t)((hx - 1) * W) * E, pv1 = pv0 + xcs;
         const uint32_t xo = xoff(h + 1 + CH), yo = yoff(h + 1);   // the next rows' operands
         auto side_a = [&](int c) {
 #pragma unroll
             for (int j = 0; j < 2; j++) {
                 const int u = 2 * c + j;   // 0 .. NS/2 - 1 (= NT/2 - 1)
-                if constexpr (rin) {
-                    if constexpr (BF) Yt[achan<BF>(u, hf) * LY + cl] = (T)ya[u];
-                    else Yt[achan<BF>(u, hf) * LY + cl] = __uint_as_float(ya[u]);
-                }
                 if constexpr (pst) {
                     const int n = u >> 4, i = u & 15, ch = 32 * n + row32(i, 0);   // + 4hf, in dx0
                     bstore(accXp[n][i], (T*)nullptr, rD, (ch & 1) ? pv1 : pv0, (uint32_t)(2 * (ch >> 1)) * xcs);
@@ -861,6 +858,13 @@ __global__ void __launch_bounds__(256, 1)
             for (int c = 0; c < NS / 4; c++) side_a(c);
         }
         const f32x16 dz3 = tgemm<T, NT, false>(ya, UtA, LDA_T, cl, hf);
+        if constexpr (rin) {   // dY[h] into the LDS tile of the dUt product
+#pragma unroll
+            for (int u = 0; u < NT / 2; u++) {
+                if constexpr (BF) Yt[achan<BF>(u, hf) * LY + cl] = (T)ya[u];
+                else Yt[achan<BF>(u, hf) * LY + cl] = __uint_as_float(ya[u]);
+            }
+        }
         ring[KH - 1] = z1n;
         // Z2[h] (conv along h), Z3[h] (conv along w: tap j reads column + j - 1)
         f32x16 z2, z3, zm, zp;
@@ -890,11 +894,11 @@ __global__ void __launch_bounds__(256, 1)
         };
         auto side_d = [&](int c) {   // c = 0..11
             if constexpr (z1) {
-                constexpr int PY = (NT / 2 + 11) / 12;
+                constexpr int PY = NT / 8;
 #pragma unroll
                 for (int j = 0; j < PY; j++) {
                     const int u = c * PY + j;
-                    if (u < NT / 2) ya[u] = aslot<T>(rY, yo, ycs, u);
+                    if (c < 4) ya[u] = aslot<T>(rY, yo, ycs, u);
                 }
             }
         };
