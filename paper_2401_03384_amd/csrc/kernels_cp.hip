@@ -328,13 +328,15 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         return acc;
     };
 
-    // the first NP rows of the walk are requested before the tables load;
-    // later rows of the ring fill follow as buffers free up
+    // The first row of the walk is requested before the tables load, each
+    // further row of the ring fill just before the row ahead of it is
+    // computed (NP row buffers): at the start every wavefront asks at once,
+    // and its first row then waits behind fewer requests.
     constexpr int NP = KH < 3 ? KH : 3;
     uint32_t xp[NP][NS / 2];
     if (wok) {
 #pragma unroll
-        for (int p = 0; p < NP; p++) arow<T, NS>(xp[p], rX, xoff(h0 - CH + p), xcs);
+        for (int p = 0; p < 1; p++) arow<T, NS>(xp[p], rX, xoff(h0 - CH + p), xcs);
     }
     // ---- tables ----
     // Each thread issues all of its table loads before any LDS store, so that
@@ -389,6 +391,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     f32x16 ring[KH];
 #pragma unroll
     for (int j = 0; j < KH - 1; j++) {
+        if (j + 1 < NP) arow<T, NS>(xp[j + 1], rX, xoff(h0 - CH + j + 1), xcs);
         ring[j] = gemm1(xp[j % NP], NoSide{});
         if (j + NP < KH) arow<T, NS>(xp[j % NP], rX, xoff(h0 - CH + j + NP), xcs);
     }
@@ -759,14 +762,13 @@ __global__ void __launch_bounds__(256, 1)
     for (int n = 0; n < MS; n++)
 #pragma unroll
         for (int i = 0; i < 16; i++) accXp[n][i] = 0.f;
-    // Every operand of the ring fill and the first row is requested before
-    // the factor tables load, so that their memory latencies overlap.
+    // The first ring row is requested before the factor tables load, each
+    // further operand row just before the ring row ahead of it is computed
+    // (at the start every wavefront asks at once; its first row then waits
+    // behind fewer requests).
     uint32_t xp[KH - 1][NS / 2 / PW];
     if (wok) {
-#pragma unroll
-        for (int j = 0; j < KH - 1; j++) arow<T, NS>(xp[j], rX, xoff(hs - CH + j), xcs);
-        arow<T, NS>(xa, rX, xoff(hs + CH), xcs);
-        arow<T, NT>(ya, rY, yoff(hs), ycs);
+        arow<T, NS>(xp[0], rX, xoff(hs - CH), xcs);
     }
     // ---- tables: UsA [32][lda_s], UtA [32][lda_t] (and UsT [NS][ldu] for bf16) ----
     // Each thread issues all of its table loads before any LDS store, so that
@@ -809,6 +811,11 @@ __global__ void __launch_bounds__(256, 1)
     if (wok) {
 #pragma unroll
         for (int j = 0; j < KH - 1; j++) {
+            if (j + 1 < KH - 1) arow<T, NS>(xp[j + 1], rX, xoff(hs - CH + j + 1), xcs);
+            if (j + 1 == KH - 1) {
+                arow<T, NS>(xa, rX, xoff(hs + CH), xcs);
+                arow<T, NT>(ya, rY, yoff(hs), ycs);
+            }
             ring[j] = tgemm<T, NS>(xp[j], UsA, LDA_S, cl, hf);
             xl_put(j, xp[j]);
         }
