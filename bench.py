@@ -35,37 +35,42 @@ def parse_args():
                     help="print per-launch averages of the timed steps to stderr")
     ap.add_argument("--cpu-batch", type=int, default=128, help="batch of the oracle CPU sample")
     ap.add_argument("--generic", action="store_true", help="generic kernel only")
+    ap.add_argument("--path", choices=["optimal", "ltr"], default="optimal",
+                    help="pairwise order: the planner's optimum or the left-to-right baseline")
+    ap.add_argument("--compare-ltr", action="store_true",
+                    help="also time the left-to-right order on the same kernels")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run plain device copies of this size (counter calibration)")
     return ap.parse_args()
 
 
-def kernel_sources_sha256():
-    """Hash of every kernel source: counter results stay valid only while it matches."""
+# device code of each kernel: its source file and the headers it includes
+KERNEL_SOURCES = {
+    "cp_": ("kernels_cp.hip", "desc.h", "hip_util.h"),
+    "reduce_multi": ("kernels_fast.hip", "desc.h", "hip_util.h"),
+}
+
+
+def source_hashes(files):
     import hashlib
     csrc = os.path.join(ROOT, "paper_2401_03384_amd", "csrc")
-    h = hashlib.sha256()
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith(".hip"):
-            h.update(f.encode())
-            h.update(open(os.path.join(csrc, f), "rb").read())
-    return h.hexdigest()
+    return {f: hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest() for f in files}
 
 
 def measured_traffic(kname, dtype):
     """HBM bytes per dispatch of `kname` from the committed counter summary,
-    or None when there is none or any kernel source changed since."""
+    or None when there is none or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_c2_{dtype}.json")
     if not os.path.exists(path):
         return None
     info = json.load(open(path))
-    if info.get("kernel_sources_sha256") != kernel_sources_sha256():
+    entry = info.get("kernels", {}).get(kname)
+    if entry is None or entry["sources"] != source_hashes(sorted(entry["sources"])):
         return None
-    return info["bytes_per_dispatch"].get(kname)
+    return entry["bytes_per_dispatch"]
 
 
-def roofline(records, dtype):
-    """Dominant kernel (largest total time) from the live launch records."""
+def kernel_totals(records):
     by = {}
     for kname, step, ms, nbytes, flops in records:
         d = by.setdefault(kname, [0.0, 0, 0.0, 0.0])
@@ -73,7 +78,15 @@ def roofline(records, dtype):
         d[1] += 1
         d[2] += nbytes
         d[3] += flops
-    kname, (ms, n, nbytes, flops) = max(by.items(), key=lambda kv: kv[1][0])
+    return by
+
+
+def roofline(records, dtype, share):
+    """Roofline of the dominant kernel from its live launch records (every
+    record is a launch of that kernel); `share` is its share of kernel time."""
+    by = kernel_totals(records)
+    assert len(by) == 1, by.keys()
+    kname, (ms, n, nbytes, flops) = next(iter(by.items()))
     ai = flops / max(nbytes, 1.0)
     ridge = PEAK_MFMA_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
     avg_s = ms / n / 1e3
@@ -81,14 +94,13 @@ def roofline(records, dtype):
         achieved, peak, unit, bound = nbytes / n / avg_s / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
     else:
         achieved, peak, unit, bound = flops / n / avg_s / 1e12, PEAK_MFMA_TFLOPS[dtype], "TFLOP/s", "mfma"
-    total = sum(v[0] for v in by.values())
     traffic = measured_traffic(kname, dtype)
     return {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": None if traffic is None else round(traffic),
             "alg_bytes_per_launch": round(nbytes / n),
             "launches": n, "avg_us": round(ms / n * 1e3, 2),
-            "share_of_kernel_time": round(ms / total, 3)}
+            "share_of_kernel_time": round(share, 3)}
 
 
 def launch_table(records, steps):
@@ -140,6 +152,38 @@ def cpu_baseline(w, batch):
                       f"{passes} passes"}
 
 
+def compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args):
+    """The paper's baseline order on the same kernels: forward + backward time,
+    forward multiplications and workspace of the left-to-right plan."""
+    import torch
+    import paper_2401_03384_amd as P
+
+    dev = xs[0].device
+    pl = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=ltr)
+    ws = torch.empty(max(pl.ws_fwd, pl.ws_bwd, 1), dtype=torch.uint8, device=dev)
+    out = torch.empty(pl.out_shape, dtype=xs[0].dtype, device=dev)
+    grads = [torch.empty(s, dtype=pl.grad_dtype(i), device=dev) for i, s in enumerate(w.shapes)]
+    in_ptrs = [x.data_ptr() for x in xs]
+    g_ptrs = [g.data_ptr() for g in grads]
+
+    def run():
+        P.ce_forward(pl.handle, in_ptrs, out.data_ptr(), ws.data_ptr(), ws.numel(), stream)
+        P.ce_backward(pl.handle, in_ptrs, d.data_ptr(), g_ptrs, ws.data_ptr(), ws.numel(), stream)
+
+    for _ in range(2):
+        run()
+    torch.cuda.synchronize()
+    n = max(3, args.steps // 5)
+    t0 = time.perf_counter()
+    for _ in range(n):
+        run()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / n
+    return {"ms_per_step": round(t * 1e3, 4), "fwd_macs": pl.fwd_macs,
+            "workspace_bytes": {"fwd": pl.ws_fwd, "bwd": pl.ws_bwd},
+            "steps": n}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -173,7 +217,11 @@ def main():
     xs = [torch.from_numpy(a.astype(np.float32)).to(tdt).to(dev) for a in ins]
     d = torch.from_numpy(dy.astype(np.float32)).to(tdt).to(dev)
     flags = P.CE_FLAG_GENERIC_ONLY if args.generic else 0
-    ref = P.Plan(w.spec, w.shapes, dtype, flags=flags)
+    n_in = len(w.shapes)
+    # left-to-right in the list format of ce_plan_create_with_path
+    ltr = [(0, 1)] + [(0, n_in - 1 - k) for k in range(1, n_in - 1)]
+    path = ltr if args.path == "ltr" else None
+    ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path)
     ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
     out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
     grads = [torch.empty(s, dtype=ref.grad_dtype(i), device=dev) for i, s in enumerate(w.shapes)]
@@ -185,7 +233,10 @@ def main():
 
     def step(fwd=True, bwd=True):
         e = P.ce_expr_parse(w.spec, shapes)
-        p = P.ce_plan_create(e, P.CE_COST_FWD, cdt, flags)
+        if path is None:
+            p = P.ce_plan_create(e, P.CE_COST_FWD, cdt, flags)
+        else:
+            p = P.ce_plan_create_with_path(e, path, cdt, flags)
         P.ce_expr_destroy(e)
         if fwd:
             P.ce_forward(p, in_ptrs, out.data_ptr(), ws.data_ptr(), ws.numel(), stream)
@@ -204,13 +255,24 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # timed region: whole steps, with per-launch HIP events recorded live
+    # one probe step with every launch timed names the dominant kernel (largest time)
     P.ce_timing_begin()
+    step()
+    probe = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
+    by = kernel_totals(probe)
+    dominant = max(by, key=lambda k: by[k][0])
+    share = by[dominant][0] / sum(v[0] for v in by.values())
+    # timed region: whole steps; the dominant kernel's launches are bracketed
+    # by HIP events on their stream (the other launches run without events)
+    P.ce_timing_begin_kernel(dominant)
     t_step = timed(args.steps)
     n_rec = P.ce_timing_end()
     records = [P.ce_timing_record(i) for i in range(n_rec)]
     if args.launch_table:
-        print(launch_table(records, args.steps), file=sys.stderr, flush=True)
+        P.ce_timing_begin()
+        timed(args.steps)
+        table = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
+        print(launch_table(table, args.steps), file=sys.stderr, flush=True)
     # forward-only and backward-only steps (reported beside the main figure)
     t_fwd = timed(max(5, args.steps // 2), bwd=False)
     t_bwd = timed(max(5, args.steps // 2), fwd=False)
@@ -239,12 +301,19 @@ def main():
         "data": "synthetic (seeded N(0,1) input, Kaiming-scaled factors)",
         "config": {"workload": f"{w.name}: {w.spec} X{list(w.shapes[0])} rank {w.shapes[1][0]}",
                    "global_batch": w.shapes[0][0], "fwd_macs": macs,
-                   "flops_per_step": 6 * macs, "path": "generic" if args.generic else "default"},
+                   "flops_per_step": 6 * macs,
+                   "path": ("left-to-right" if path else "optimal")
+                   + (", generic kernel" if args.generic else "")},
+        "workspace_bytes": {"fwd": ref.ws_fwd, "bwd": ref.ws_bwd},
         "fwd_ms": round(t_fwd * 1e3, 4),
         "bwd_ms": round(t_bwd * 1e3, 4),
         "plan_ms": round(t_plan * 1e3, 4),
-        "roofline": roofline(records, dtype),
+        "roofline": roofline(records, dtype, share),
     }
+    if args.compare_ltr and path is None:
+        lt = compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args)
+        lt["time_ratio_vs_optimal"] = round(lt["ms_per_step"] / (t_step * 1e3), 3)
+        line["left_to_right"] = lt
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_batch)
     print(json.dumps(line), flush=True)

@@ -198,6 +198,12 @@ ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
  * memory is allocated).  Adds two event records per launch. */
 ce_status ce_timing_begin(void);
 
+/* As ce_timing_begin, but only launches of the kernel labelled `kernel` (the
+ * label ce_timing_record reports, e.g. "cp_bwd<float, 3, 3, 2, 2>") are
+ * bracketed, so the other launches run without event records in between.
+ * NULL or "" records every launch.  The label is copied. */
+ce_status ce_timing_begin_kernel(const char* kernel);
+
 /* Stop recording; waits for the recorded events and keeps the records until
  * the next ce_timing_begin on this thread.  n_records receives their count. */
 ce_status ce_timing_end(int* n_records);

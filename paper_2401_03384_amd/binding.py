@@ -37,8 +37,8 @@ EXPORTS = [
     "ce_expr_parse", "ce_expr_set_feature", "ce_expr_output_shape", "ce_expr_destroy",
     "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps", "ce_plan_step",
     "ce_plan_cost", "ce_plan_left_to_right_cost", "ce_plan_workspace_size", "ce_plan_describe",
-    "ce_plan_destroy", "ce_forward", "ce_backward", "ce_timing_begin", "ce_timing_end",
-    "ce_timing_record", "ce_last_error", "ce_version",
+    "ce_plan_destroy", "ce_forward", "ce_backward", "ce_timing_begin", "ce_timing_begin_kernel",
+    "ce_timing_end", "ce_timing_record", "ce_last_error", "ce_version",
 ]
 
 
@@ -81,6 +81,7 @@ def lib():
         L.ce_forward.argtypes = [vp, C.POINTER(vp), vp, vp, C.c_size_t, vp]
         L.ce_backward.argtypes = [vp, C.POINTER(vp), vp, C.POINTER(vp), vp, C.c_size_t, vp]
         L.ce_timing_begin.argtypes = []
+        L.ce_timing_begin_kernel.argtypes = [C.c_char_p]
         L.ce_timing_end.argtypes = [C.POINTER(C.c_int)]
         L.ce_timing_record.argtypes = [C.c_int, C.POINTER(C.c_char_p), C.POINTER(C.c_char_p),
                                        C.POINTER(C.c_float), C.POINTER(C.c_double),
@@ -91,7 +92,7 @@ def lib():
                      "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps",
                      "ce_plan_step", "ce_plan_cost", "ce_plan_left_to_right_cost",
                      "ce_plan_workspace_size", "ce_forward", "ce_backward", "ce_timing_begin",
-                     "ce_timing_end", "ce_timing_record"):
+                     "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -215,6 +216,10 @@ def ce_backward(p: int, in_ptrs, dout_ptr: int, din_ptrs, ws_ptr: int, ws_bytes:
 
 def ce_timing_begin() -> None:
     _check(lib().ce_timing_begin())
+
+
+def ce_timing_begin_kernel(kernel) -> None:
+    _check(lib().ce_timing_begin_kernel(kernel.encode() if kernel else None))
 
 
 def ce_timing_end() -> int:

@@ -73,6 +73,7 @@ struct TimingRec {
     double bytes = 0, flops = 0;
 };
 thread_local bool g_timing = false;
+thread_local std::string g_only;   // record only this kernel label (empty: all)
 thread_local std::vector<TimingRec> g_recs;
 thread_local std::vector<hipEvent_t> g_pool;
 thread_local size_t g_pool_used = 0;
@@ -96,7 +97,7 @@ void check_ws(const ce_plan* p, size_t need, void* ws, size_t ws_bytes) {
 }
 
 hipError_t run_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
-    if (!g_timing) return raw_launch(ln, P, s);
+    if (!g_timing || (!g_only.empty() && ln.kname != g_only)) return raw_launch(ln, P, s);
     TimingRec r;
     r.a = next_event();
     r.b = next_event();
@@ -119,10 +120,13 @@ hipError_t run_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
 
 using namespace ce;
 
-extern "C" ce_status ce_timing_begin(void) {
+extern "C" ce_status ce_timing_begin(void) { return ce_timing_begin_kernel(nullptr); }
+
+extern "C" ce_status ce_timing_begin_kernel(const char* kernel) {
     return guard([&] {
         g_recs.clear();
         g_pool_used = 0;
+        g_only = kernel ? kernel : "";
         g_timing = true;
     });
 }
