@@ -57,6 +57,7 @@ enum KernelKind : int32_t {
     K_THINW_REDUCE = 30,    // ordered sum of its partials (ThinwDesc)
     K_CREDW_REDUCE = 31,    // ordered sum of the K_CREDW partials (CredDesc)
     K_REDUCE_MULTI = 32,    // up to four ordered partial sums in one launch (MultiReduceDesc)
+    K_RCP_FWD = 33,         // fused reshaped-CP chain forward (RcpDesc, desc_rcp.h)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).

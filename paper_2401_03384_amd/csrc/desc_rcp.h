@@ -1,0 +1,49 @@
+// Descriptor of the fused reshaped-CP chain (host planner and HIP kernel).
+//
+// Reshaped CP layer (Section 2.3, reshaped tensor decompositions; the RCP
+// string of Appendix A.3 with three modes):
+//   Y[b][t1][t2][t3][h][w] = sum_r sum_{s1 s2 s3} W1[r][t1][s1] W2[r][t2][s2] W3[r][t3][s3]
+//                            sum_{i j} W0[r][i][j] X[b][s1][s2][s3][h+i-c][w+j-c]
+// planned as the chain  Z1 = X x1 W1 (contract s1), Z2 = Z1 x2 W2 (contract s2),
+// Z3 = Z2 x3 W3 (contract s3), Y = sum_r Z3 (*) W0[r] (2-D convolution, same
+// zero padding), all tensors dense in their string's label order.
+#pragma once
+
+#include <cstdint>
+
+namespace ce {
+
+// One workgroup owns sample b, output mode index t1, a chunk of T2C values of
+// t2 and a tile of TH output rows; it computes Z2 and Z3 on the tile's rows
+// plus (K-1)/2 halo rows on each side (clipped to the image) and loops over
+// the rank in pairs.  LDS (32-bit words): two Zb buffers [T2C][S3/2][pixels]
+// of bf16 pairs along s3 (the Z2 values of one rank), then the Zc planes
+// [T2C*T3][HP][WP] holding Z3 of a rank pair as bf16 pairs (even rank in the
+// low half) with zero rows and columns outside the image.
+struct RcpDesc {
+    int32_t S1, S2, S3, T2, T3, K, T2C, NT;   // the instantiation's compile-time sizes
+    int32_t B, T1, R, H, W;
+    int32_t nc;                // t2 chunks = T2 / T2C
+    int32_t TH, ntiles;        // output rows per tile, tiles per image
+    int32_t QW, WP, HP;        // output column quads per row; Zc plane pitch and rows
+    int32_t zb_dw;             // one Zb buffer, 32-bit words (multiple of 4)
+    int32_t plane_dw;          // one Zc plane = HP * WP words (multiple of 4)
+    int32_t zc_dw;             // all Zc planes
+    uint32_t lds_bytes;
+    int64_t blocks;
+};
+
+// The compiled instantiations: mode sizes S1, S2, S3, T2, T3 (T1 is free),
+// filter size K, t2 chunk T2C, threads NT and the per-thread unit bounds of
+// phases A, B, C (the planner picks the first that fits; the kernel file
+// instantiates each).
+struct RcpCfgInfo {
+    int S1, S2, S3, T2, T3, K, T2C, NT, UA, UB, UC;
+};
+constexpr RcpCfgInfo kRcpCfgs[] = {
+    {8, 8, 8, 8, 8, 3, 8, 256, 1, 2, 4},    // 8x8x8 modes, 3x3 (tiles up to 9 x 7 with halo)
+    {4, 4, 8, 4, 8, 5, 2, 448, 4, 2, 4},    // 4x4x8 modes, 5x5 (tiles up to 16 x 28 with halo)
+};
+constexpr int kNumRcpCfgs = 2;
+
+}  // namespace ce

@@ -46,6 +46,11 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
                                   resolve(ln.extra[2], P)};
             return launch_cp_fwd(ln, ops, c, s);
         }
+        case K_RCP_FWD: {
+            const void* ops[5] = {a, b, resolve(ln.extra[0], P), resolve(ln.extra[1], P),
+                                  resolve(ln.extra[2], P)};
+            return launch_rcp_fwd(ln, ops, c, s);
+        }
         case K_CP_BWD: {
             const void* ops[11] = {a, b, c};
             for (int i = 0; i < 8; i++) ops[3 + i] = resolve(ln.extra[i], P);

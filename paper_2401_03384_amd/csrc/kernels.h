@@ -37,6 +37,9 @@ hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, vo
 // Fused CP chain forward: ops = {X, Us, Kh, Kw, Ut}.
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
 
+// Fused reshaped-CP chain forward: ops = {X, W1, W2, W3, W0}, y = Y.
+hipError_t launch_rcp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
+
 // Fused CP chain backward: ops = {X, dY, dX (may be NULL), Us, Kh, Kw, Ut,
 // Pus, Put, Pkh, Pkw}.
 hipError_t launch_cp_bwd(const Launch& ln, const void* const* ops, hipStream_t s);

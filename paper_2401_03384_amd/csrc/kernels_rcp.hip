@@ -1,0 +1,147 @@
+// Fused reshaped-CP chain forward for gfx950 (RcpDesc; the phases are in
+// rcp_body.h).
+//
+// The three mode products and the rank-summed 2-D convolution of a reshaped
+// CP layer (Section 2.3; Appendix A.3 RCP string) run in one launch: each
+// workgroup keeps its sample's X values in registers, builds Z2 and Z3 of one
+// rank at a time in LDS and accumulates Y over the ranks in registers, so none
+// of the three rank-expanded intermediates (64x the input at rank 64) touches
+// HBM.  bf16 pairs feed v_dot2_f32_bf16 throughout: pairs along s1, s2 and s3
+// for the mode products, pairs of ranks for the convolution.  The work is
+// plain vector ALU (the contractions have 4 or 8 terms), so the roofline is
+// the fp32 vector rate (two bf16 products per dot2 lane-op).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstring>
+
+#include "desc_rcp.h"
+#include "hip_util.h"
+#include "kernels.h"
+
+#define RCP_FN __device__ __forceinline__
+#define RCP_HD __host__ __device__ inline
+#include "rcp_body.h"
+
+namespace ce {
+namespace {
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+struct DevMem {
+    uint32_t* lds;
+    __device__ __forceinline__ uint16_t ld16(const uint16_t* p, int64_t i) const { return p[i]; }
+    __device__ __forceinline__ uint32_t ldw(const uint16_t* p, int64_t i) const {
+        return *reinterpret_cast<const uint32_t*>(p + i);
+    }
+    __device__ __forceinline__ void st16(uint16_t* p, int64_t i, uint16_t v) const { p[i] = v; }
+    __device__ __forceinline__ uint32_t lr(int i) const { return lds[i]; }
+    __device__ __forceinline__ void lr4(int i, uint32_t* o) const {
+        const uint4 v = *reinterpret_cast<const uint4*>(lds + i);
+        o[0] = v.x;
+        o[1] = v.y;
+        o[2] = v.z;
+        o[3] = v.w;
+    }
+    __device__ __forceinline__ void lw(int i, uint32_t v) const { lds[i] = v; }
+    __device__ __forceinline__ void lw16(int i, int half, uint16_t v) const {
+        reinterpret_cast<uint16_t*>(lds)[2 * i + half] = v;
+    }
+    __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) const {
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                              __builtin_bit_cast(bf16x2_t, b), c, false);
+    }
+    __device__ __forceinline__ uint32_t pk(float lo, float hi) const { return pk_bf16(lo, hi); }
+    __device__ __forceinline__ uint16_t bf(float f) const { return f32_to_bf16(f); }
+};
+
+template <class C>
+__global__ void __launch_bounds__(C::NT) rcp_fwd(RcpDesc d, const uint16_t* __restrict__ X,
+                                                const uint16_t* __restrict__ W1,
+                                                const uint16_t* __restrict__ W2,
+                                                const uint16_t* __restrict__ W3,
+                                                const uint16_t* __restrict__ W0,
+                                                uint16_t* __restrict__ Y) {
+    extern __shared__ uint32_t lds_words[];
+    DevMem m{lds_words};
+    const int tid = threadIdx.x;
+    int b, t1, tile, chunk;
+    rcp::block_coords(d, blockIdx.x, b, t1, tile, chunk);
+    const rcp::Tile t = rcp::tile_rows(d, tile);
+    rcp::State<C> st;
+    rcp::init<C>(m, d, tid, b, t, X, st);
+    rcp::phase_a<C>(m, d, t, 0, t1, chunk, 0, W1, W2, st);
+    __syncthreads();
+    const int np = d.R / 2;
+    for (int rp = 0; rp < np; rp++) {
+        const int r0 = 2 * rp;
+        rcp::phase_b<C>(m, d, t, r0, 0, W3, st);
+        rcp::phase_a<C>(m, d, t, r0 + 1, t1, chunk, 1, W1, W2, st);
+        __syncthreads();
+        rcp::phase_b<C>(m, d, t, r0 + 1, 1, W3, st);
+        __syncthreads();
+        rcp::phase_c<C>(m, d, r0, W0, st);
+        if (rp + 1 < np) rcp::phase_a<C>(m, d, t, r0 + 2, t1, chunk, 0, W1, W2, st);
+        __syncthreads();
+    }
+    rcp::store<C>(m, d, tid, b, t1, t, chunk, Y, st);
+}
+
+template <int I>
+using CfgOf = rcp::Cfg<kRcpCfgs[I].S1, kRcpCfgs[I].S2, kRcpCfgs[I].S3, kRcpCfgs[I].T2, kRcpCfgs[I].T3,
+                       kRcpCfgs[I].K, kRcpCfgs[I].T2C, kRcpCfgs[I].NT, kRcpCfgs[I].UA, kRcpCfgs[I].UB,
+                       kRcpCfgs[I].UC>;
+static_assert(kNumRcpCfgs == 2, "one launch branch per instantiation");
+
+// The descriptor matches instantiation C and every tile's units fit its
+// per-thread bounds.
+template <class C>
+bool fits(const RcpDesc& d) {
+    if (!rcp::layout_ok(d) || d.S1 != C::S1 || d.S2 != C::S2 || d.S3 != C::S3 || d.T2 != C::T2 ||
+        d.T3 != C::T3 || d.K != C::K || d.T2C != C::T2C || d.NT != C::NT)
+        return false;
+    for (int i = 0; i < d.ntiles; i++) {
+        const rcp::Tile t = rcp::tile_rows(d, i);
+        if (rcp::units_a(d, t) > C::UA * C::NT || rcp::units_b(d, t) > C::UB * C::NT ||
+            rcp::units_c(d, t) > C::UC * C::NT)
+            return false;
+    }
+    return true;
+}
+
+template <class C>
+hipError_t launch_rcp_c(const RcpDesc& d, const void* const* o, void* y, hipStream_t s) {
+    auto k = rcp_fwd<C>;
+    static std::atomic<uint64_t> allowed{0};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64 || d.lds_bytes > 160 * 1024) return hipErrorInvalidValue;
+    if (d.lds_bytes > 64 * 1024 && !(allowed.load() & (1ull << dev))) {
+        e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        allowed.fetch_or(1ull << dev);
+    }
+    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(C::NT), d.lds_bytes, s, d,
+                       (const uint16_t*)o[0], (const uint16_t*)o[1], (const uint16_t*)o[2],
+                       (const uint16_t*)o[3], (const uint16_t*)o[4], (uint16_t*)y);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// ops = {X, W1, W2, W3, W0}; y = Y.  The mode factors are read as 32-bit
+// words (bf16 pairs), so their base addresses must be 4-byte aligned.
+hipError_t launch_rcp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s) {
+    RcpDesc d;
+    std::memcpy(&d, ln.desc.data(), sizeof(d));
+    for (int i = 1; i <= 3; i++)
+        if (((uintptr_t)ops[i]) & 3) return hipErrorInvalidValue;
+    const int64_t want = (int64_t)d.B * d.T1 * d.ntiles * d.nc;
+    if (d.blocks != want || d.R % 2 || d.R < 2 || ln.lds != d.lds_bytes) return hipErrorInvalidValue;
+    if (fits<CfgOf<0>>(d)) return launch_rcp_c<CfgOf<0>>(d, ops, y, s);
+    if (fits<CfgOf<1>>(d)) return launch_rcp_c<CfgOf<1>>(d, ops, y, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace ce

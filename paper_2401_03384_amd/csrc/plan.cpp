@@ -635,7 +635,11 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             fs.t = s;
             for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
-        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) fuse_launches(p->fwd, false);
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) {
+            fuse_launches(p->fwd, false);
+            Launch rf;
+            if (fuse_rcp_forward(*p, rf)) p->fwd.assign(1, rf);
+        }
         drop_unused(items, p->fwd);
         p->ws_fwd = pack(items);
         patch(p->fwd, items);

@@ -133,6 +133,11 @@ int fuse_launches(std::vector<Launch>& v, bool backward);
 bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratch,
                       std::vector<Launch>& out);
 
+// The whole forward of a reshaped-CP plan (three mode factors and a spatial
+// factor applied one at a time) as one fused launch, when the layout and
+// sizes match a compiled instantiation.
+bool fuse_rcp_forward(const ce_plan& p, Launch& out);
+
 // Lowering of one pairwise op to launches: a specialised kernel when the
 // op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,

@@ -19,6 +19,10 @@
 #include "expr.h"
 #include "plan.h"
 
+#define RCP_FN inline
+#define RCP_HD inline
+#include "rcp_body.h"
+
 using namespace ce;
 
 namespace {
@@ -410,6 +414,210 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
             }
         REQ(ok, "out-of-bounds access (cp_fwd)");
     }
+    return true;
+}
+
+// Fused reshaped-CP forward: the kernel's own phases (rcp_body.h) run on the
+// CPU thread by thread between the kernel's barriers, with every global and
+// LDS access bounds-checked, LDS words poisoned until written, and a race
+// check: within one barrier interval no LDS word may be written by one
+// thread and read or written by another.  Every Y element must be written
+// exactly once.
+struct RcpHost {
+    std::vector<uint32_t> lds;
+    std::vector<int> w_seg, w_tid, r_seg, r_tid;
+    std::vector<char> r_multi;
+    const Buf* g[6] = {};
+    std::vector<int> ywrites;
+    int seg = 0, tid = 0;
+    bool ok = true;
+    std::string err;
+    void fail(const std::string& m) {
+        if (ok) err = m;
+        ok = false;
+    }
+    const Buf* buf_of(const void* p) {
+        for (const Buf* b : g)
+            if (b && (const void*)b->base == p) return b;
+        return nullptr;
+    }
+    void chk(const void* p, int64_t i, int bytes) {
+        const Buf* b = buf_of(p);
+        if (!b || i < 0 || (size_t)(i + bytes) > b->bytes) fail("global access out of bounds");
+    }
+    uint16_t ld16(const uint16_t* p, int64_t i) {
+        chk(p, 2 * i, 2);
+        return ok ? p[i] : 0;
+    }
+    uint32_t ldw(const uint16_t* p, int64_t i) {
+        chk(p, 2 * i, 4);
+        if (i & 1) fail("misaligned word load");
+        return ok ? (uint32_t)p[i] | ((uint32_t)p[i + 1] << 16) : 0;
+    }
+    void st16(uint16_t* p, int64_t i, uint16_t v) {
+        chk(p, 2 * i, 2);
+        if (!ok) return;
+        p[i] = v;
+        if (p == (uint16_t*)g[5]->base) ywrites[i]++;
+    }
+    void lds_chk(int i) {
+        if (i < 0 || i >= (int)lds.size()) fail("LDS access out of bounds");
+    }
+    void on_read(int i) {
+        if (w_seg[i] == seg && w_tid[i] != tid) fail("LDS race: read of a word another thread wrote");
+        if (w_seg[i] < 0) fail("LDS read of a word never written");
+        if (r_seg[i] == seg && r_tid[i] != tid) r_multi[i] = 1;
+        if (r_seg[i] != seg) r_multi[i] = 0;
+        r_seg[i] = seg;
+        r_tid[i] = tid;
+    }
+    void on_write(int i) {
+        if (w_seg[i] == seg && w_tid[i] != tid) fail("LDS race: two threads write one word");
+        if (r_seg[i] == seg && (r_multi[i] || r_tid[i] != tid)) fail("LDS race: write of a word another thread read");
+        w_seg[i] = seg;
+        w_tid[i] = tid;
+    }
+    uint32_t lr(int i) {
+        lds_chk(i);
+        if (!ok) return 0;
+        on_read(i);
+        return lds[i];
+    }
+    void lr4(int i, uint32_t* o) {
+        if (i % 4) fail("misaligned 16-byte LDS read");
+        for (int k = 0; k < 4; k++) o[k] = lr(i + k);
+    }
+    void lw(int i, uint32_t v) {
+        lds_chk(i);
+        if (!ok) return;
+        on_write(i);
+        lds[i] = v;
+    }
+    void lw16(int i, int half, uint16_t v) {
+        lds_chk(i);
+        if (!ok) return;
+        on_write(i);
+        lds[i] = half ? (lds[i] & 0xffffu) | ((uint32_t)v << 16) : (lds[i] & 0xffff0000u) | v;
+    }
+    static float f(uint32_t h) {
+        uint32_t u = h << 16;
+        float x;
+        std::memcpy(&x, &u, 4);
+        return x;
+    }
+    static uint16_t rne(float v) {
+        uint32_t u;
+        std::memcpy(&u, &v, 4);
+        if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+        u += 0x7fffu + ((u >> 16) & 1u);
+        return (uint16_t)(u >> 16);
+    }
+    float dot2(uint32_t a, uint32_t b, float c) {
+        return c + (f(a & 0xffff) * f(b & 0xffff) + f(a >> 16) * f(b >> 16));
+    }
+    uint32_t pk(float lo, float hi) { return (uint32_t)rne(lo) | ((uint32_t)rne(hi) << 16); }
+    uint16_t bf(float v) { return rne(v); }
+};
+
+template <class C>
+bool rcp_blocks(const RcpDesc& d, RcpHost& m, const uint16_t* X, const uint16_t* W1, const uint16_t* W2,
+                const uint16_t* W3, const uint16_t* W0, uint16_t* Y) {
+    for (int i = 0; i < d.ntiles; i++) {
+        const rcp::Tile t = rcp::tile_rows(d, i);
+        if (rcp::units_a(d, t) > C::UA * C::NT || rcp::units_b(d, t) > C::UB * C::NT ||
+            rcp::units_c(d, t) > C::UC * C::NT) {
+            m.fail("tile units exceed the instantiation");
+            return false;
+        }
+    }
+    std::vector<rcp::State<C>> st(C::NT);
+    for (int64_t blk = 0; blk < d.blocks && m.ok; blk++) {
+        int b, t1, tile, chunk;
+        rcp::block_coords(d, blk, b, t1, tile, chunk);
+        if (b < 0 || b >= d.B || t1 < 0 || t1 >= d.T1 || tile < 0 || tile >= d.ntiles || chunk < 0 || chunk >= d.nc) {
+            m.fail("block coordinates out of range");
+            return false;
+        }
+        const rcp::Tile t = rcp::tile_rows(d, tile);
+        std::fill(m.lds.begin(), m.lds.end(), 0xCDCDCDCDu);
+        std::fill(m.w_seg.begin(), m.w_seg.end(), -1);
+        std::fill(m.r_seg.begin(), m.r_seg.end(), -1);
+        m.seg = 0;
+        auto each = [&](auto&& fn) {
+            for (int tid = 0; tid < C::NT; tid++) {
+                m.tid = tid;
+                fn(tid);
+            }
+            m.seg++;   // barrier
+        };
+        each([&](int tid) {
+            rcp::init<C>(m, d, tid, b, t, X, st[tid]);
+            rcp::phase_a<C>(m, d, t, 0, t1, chunk, 0, W1, W2, st[tid]);
+        });
+        const int np = d.R / 2;
+        for (int rp = 0; rp < np; rp++) {
+            const int r0 = 2 * rp;
+            each([&](int tid) {
+                rcp::phase_b<C>(m, d, t, r0, 0, W3, st[tid]);
+                rcp::phase_a<C>(m, d, t, r0 + 1, t1, chunk, 1, W1, W2, st[tid]);
+            });
+            each([&](int tid) { rcp::phase_b<C>(m, d, t, r0 + 1, 1, W3, st[tid]); });
+            each([&](int tid) {
+                rcp::phase_c<C>(m, d, r0, W0, st[tid]);
+                if (rp + 1 < np) rcp::phase_a<C>(m, d, t, r0 + 2, t1, chunk, 0, W1, W2, st[tid]);
+            });
+        }
+        each([&](int tid) { rcp::store<C>(m, d, tid, b, t1, t, chunk, Y, st[tid]); });
+    }
+    return m.ok;
+}
+
+template <int I>
+using RcpCfgOf = rcp::Cfg<kRcpCfgs[I].S1, kRcpCfgs[I].S2, kRcpCfgs[I].S3, kRcpCfgs[I].T2, kRcpCfgs[I].T3,
+                          kRcpCfgs[I].K, kRcpCfgs[I].T2C, kRcpCfgs[I].NT, kRcpCfgs[I].UA, kRcpCfgs[I].UB,
+                          kRcpCfgs[I].UC>;
+
+template <class C>
+bool rcp_is(const RcpDesc& d) {
+    return d.S1 == C::S1 && d.S2 == C::S2 && d.S3 == C::S3 && d.T2 == C::T2 && d.T3 == C::T3 &&
+           d.K == C::K && d.T2C == C::T2C && d.NT == C::NT;
+}
+
+bool run_rcp_fwd(const Launch& ln, Ctx& c) {
+    RcpDesc d = desc_of<RcpDesc>(ln);
+    REQ(((ln.kind >> kBitIn) & 1) == 1 && ln.extra.size() == 3, "bf16 only, five operands");
+    bool o[6];
+    Buf X = resolve(ln.a, c, 0, o[0]), W1 = resolve(ln.b, c, 0, o[1]), W2 = resolve(ln.extra[0], c, 0, o[2]),
+        W3 = resolve(ln.extra[1], c, 0, o[3]), W0 = resolve(ln.extra[2], c, 0, o[4]), Y = resolve(ln.c, c, 0, o[5]);
+    REQ(o[0] && o[1] && o[2] && o[3] && o[4] && o[5], "unresolved buffer");
+    REQ(rcp::layout_ok(d), "LDS layout");
+    REQ(d.blocks == (int64_t)d.B * d.T1 * d.ntiles * d.nc && (int64_t)ln.grid[0] == d.blocks &&
+        (int)ln.block[0] == d.NT && ln.lds == d.lds_bytes && d.lds_bytes <= 160 * 1024, "grid / LDS");
+    // operand sizes implied by the descriptor
+    const int64_t HW = (int64_t)d.H * d.W;
+    REQ(X.bytes >= (size_t)(2 * (int64_t)d.B * d.S1 * d.S2 * d.S3 * HW) &&
+        Y.bytes >= (size_t)(2 * (int64_t)d.B * d.T1 * d.T2 * d.T3 * HW), "operand sizes");
+    RcpHost m;
+    const size_t nw = d.lds_bytes / 4;
+    m.lds.assign(nw, 0);
+    m.w_seg.assign(nw, -1);
+    m.w_tid.assign(nw, -1);
+    m.r_seg.assign(nw, -1);
+    m.r_tid.assign(nw, -1);
+    m.r_multi.assign(nw, 0);
+    const Buf* gb[6] = {&X, &W1, &W2, &W3, &W0, &Y};
+    for (int i = 0; i < 6; i++) m.g[i] = gb[i];
+    m.ywrites.assign(Y.bytes / 2, 0);
+    const uint16_t *px = (const uint16_t*)X.base, *p1 = (const uint16_t*)W1.base, *p2 = (const uint16_t*)W2.base,
+                   *p3 = (const uint16_t*)W3.base, *p0 = (const uint16_t*)W0.base;
+    uint16_t* py = (uint16_t*)Y.base;
+    bool ran = false;
+    if (rcp_is<RcpCfgOf<0>>(d)) ran = rcp_blocks<RcpCfgOf<0>>(d, m, px, p1, p2, p3, p0, py), ran = true;
+    else if (rcp_is<RcpCfgOf<1>>(d)) ran = rcp_blocks<RcpCfgOf<1>>(d, m, px, p1, p2, p3, p0, py), ran = true;
+    REQ(ran, "no instantiation matches");
+    REQ(m.ok, "rcp_fwd: " + m.err);
+    const int64_t ny = (int64_t)d.B * d.T1 * d.T2 * d.T3 * HW;
+    for (int64_t i = 0; i < ny; i++) REQ(m.ywrites[i] == 1, "a Y element is not written exactly once");
     return true;
 }
 
@@ -898,6 +1106,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_DW_TAPREDUCE ? run_tapreduce(ln, c)
                     : v == K_CP_FWD ? run_cp_fwd(ln, c)
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
+                    : v == K_RCP_FWD ? run_rcp_fwd(ln, c)
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)

@@ -187,6 +187,24 @@ def test_fused_chain_keeps_intermediates_on_chip():
     B.ce_plan_destroy(p)
 
 
+@pytest.mark.parametrize("name,fused", [("C5a", True), ("C5b", True), ("C5as", True), ("C5bs", True),
+                                        ("C5bt2", True), ("C5bt3", True), ("C5as_f32", False),
+                                        ("C5cs", False)])
+def test_fused_rcp_forward(name, fused):
+    """Reshaped-CP layers of a compiled instantiation run their whole forward
+    as one launch with no workspace; other shapes and float32 stay unfused."""
+    w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS[name]
+    p = _plan(w.spec, w.shapes, dtype=B.CE_BF16 if w.dtype == "bf16" else B.CE_F32)
+    text = B.ce_plan_describe(p)
+    fwd = [l for l in text.splitlines() if "fwd kernel" in l]
+    if fused:
+        assert len(fwd) == 1 and "fused RCP chain" in fwd[0]
+        assert B.ce_plan_workspace_size(p, 0) == 0
+    else:
+        assert not any("fused RCP" in l for l in fwd)
+    B.ce_plan_destroy(p)
+
+
 @pytest.mark.parametrize("spec,shapes,status", [
     ("bshw,tshw", [(1, 2, 3, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),
     ("bssw,tshw->bthw|hw", [(1, 2, 2, 3), (1, 2, 3, 3)], B.CE_ERR_PARSE),

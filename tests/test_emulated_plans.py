@@ -25,7 +25,7 @@ def emul(tmp_path_factory):
            "-fno-sanitize-recover=undefined", "-I", os.path.join(ROOT, "include"), "-I", SRC,
            os.path.join(ROOT, "tests", "cpu_emulator", "emulate.cpp"),
            os.path.join(SRC, "expr.cpp"), os.path.join(SRC, "plan.cpp"),
-           os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "fuse.cpp"),
+           os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "fuse.cpp"), os.path.join(SRC, "fuse_rcp.cpp"),
            os.path.join(SRC, "capi.cpp"), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -90,6 +90,11 @@ CASES = {
     "C5bt": W.rcp_layer("C5bt", 1, (2, 2, 4), (2, 2, 4), 9, 8, 16, 5, "bf16", 24),
     "C4m": W.rtt_layer("C4m", 1, (4, 4, 8), (4, 4, 8), 5, 7, 16, 3, "f32", 26),
     "C5cs": W.PARITY_WORKLOADS["C5cs"],
+    # fused reshaped-CP forward: both instantiations, one and several row tiles
+    "C5as": W.PARITY_WORKLOADS["C5as"],
+    "C5bs": W.PARITY_WORKLOADS["C5bs"],
+    "C5bt2": W.PARITY_WORKLOADS["C5bt2"],
+    "C5bt3": W.PARITY_WORKLOADS["C5bt3"],
     "C5cs_f32": W.PARITY_WORKLOADS["C5cs_f32"],
 }
 

@@ -124,6 +124,10 @@ PARITY_WORKLOADS = {
     "C5as": rcp_layer("C5as", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "bf16", 15),
     "C5as_f32": rcp_layer("C5as_f32", 3, (8, 8, 8), (8, 8, 8), 7, 7, 64, 3, "f32", 15),
     "C5bs": rcp_layer("C5bs", 2, (4, 4, 8), (4, 4, 8), 11, 11, 64, 5, "bf16", 16),
+    # fused reshaped-CP forward on row tiles: two tiles (23 x 26) and three
+    # (50 x 20, a middle tile with halo rows on both sides)
+    "C5bt2": rcp_layer("C5bt2", 1, (4, 4, 8), (2, 4, 8), 23, 26, 4, 5, "bf16", 27),
+    "C5bt3": rcp_layer("C5bt3", 1, (4, 4, 8), (3, 4, 8), 50, 20, 2, 5, "bf16", 28),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
