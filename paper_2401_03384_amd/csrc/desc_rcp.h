@@ -33,6 +33,23 @@ struct RcpDesc {
     int64_t blocks;
 };
 
+// Fused backward of the same chain: one workgroup per (b, t1, tile of TH
+// rows, t2 chunk), no halo recompute (the dY planes carry the halo).  LDS
+// word offsets: o_dy dY planes [T2C*T3][HPb][WP] (fp32, zero outside the
+// image), o_z1 Z1k [S2*S3][PP], o_z2 Z2k [S3*T2C][PP], o_z3 Z3k [T2C*T3][P],
+// o_g3 G3k [T3*T2C][PP], o_g2 G2k [T2C*S3][PP] (bf16 rows), o_q the dW0 and
+// dW1 partials summed over 16-lane rows [KK + S1][4 * NT/64], o_m3 / o_m2
+// per-wave MFMA partials [NT/64][T3*S3] / [NT/64][T2C*S2] (fp32).
+struct RcpBwdDesc {
+    int32_t S1, S2, S3, T2, T3, K, T2C, NT;
+    int32_t B, T1, R, H, W;
+    int32_t nc, TH, ntiles;
+    int32_t QW, WP, HPb, PP;
+    int32_t o_dy, o_z1, o_z2, o_z3, o_g3, o_g2, o_q, o_m3, o_m2;
+    uint32_t lds_bytes;
+    int64_t blocks;
+};
+
 // The compiled instantiations: mode sizes S1, S2, S3, T2, T3 (T1 is free),
 // filter size K, t2 chunk T2C, threads NT and the per-thread unit bounds of
 // phases A, B, C (the planner picks the first that fits; the kernel file
@@ -45,5 +62,13 @@ constexpr RcpCfgInfo kRcpCfgs[] = {
     {4, 4, 8, 4, 8, 5, 2, 448, 4, 2, 4},    // 4x4x8 modes, 5x5 (tiles up to 16 x 28 with halo)
 };
 constexpr int kNumRcpCfgs = 2;
+
+// Backward instantiations (same fields; UA, UB, UC bound the units (pixel,
+// s3), (pixel, t2) and (plane, row, 4 columns) of one tile per thread).
+constexpr RcpCfgInfo kRcpBwdCfgs[] = {
+    {8, 8, 8, 8, 8, 3, 8, 512, 1, 1, 2},    // 8x8x8 modes, 3x3 (tiles up to 64 pixels)
+    {4, 4, 8, 4, 8, 5, 2, 448, 2, 1, 1},    // 4x4x8 modes, 5x5 (tiles up to 112 pixels)
+};
+constexpr int kNumRcpBwdCfgs = 2;
 
 }  // namespace ce

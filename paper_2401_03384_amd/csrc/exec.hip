@@ -51,6 +51,11 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
                                   resolve(ln.extra[2], P)};
             return launch_rcp_fwd(ln, ops, c, s);
         }
+        case K_RCP_BWD: {
+            const void* ops[11] = {a, b};
+            for (int i = 0; i < 9; i++) ops[2 + i] = resolve(ln.extra[i], P);
+            return launch_rcp_bwd(ln, ops, s);
+        }
         case K_CP_BWD: {
             const void* ops[11] = {a, b, c};
             for (int i = 0; i < 8; i++) ops[3 + i] = resolve(ln.extra[i], P);

@@ -150,3 +150,159 @@ bool fuse_rcp_forward(const ce_plan& p, Launch& out) {
 }
 
 }  // namespace ce
+
+namespace ce {
+
+namespace {
+
+int64_t al4(int64_t x) { return (x + 3) & ~int64_t(3); }
+
+}  // namespace
+
+bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch, std::vector<Launch>& out) {
+    if ((f.kind & 0xff) != K_RCP_FWD || f.extra.size() != 3) return false;
+    RcpDesc fd;
+    std::memcpy(&fd, f.desc.data(), sizeof(fd));
+    const int64_t B = fd.B, T1 = fd.T1, R = fd.R, H = fd.H, W = fd.W, K = fd.K;
+    const int64_t S1 = fd.S1, S2 = fd.S2, S3 = fd.S3, T2 = fd.T2, T3 = fd.T3;
+    const int64_t HW = H * W, S = S1 * S2 * S3, KK = K * K;
+    if (R % 2) return false;   // factor buffers of an even element count (word loads)
+    for (int c = 0; c < kNumRcpBwdCfgs; c++) {
+        const RcpCfgInfo& g = kRcpBwdCfgs[c];
+        if (S1 != g.S1 || S2 != g.S2 || S3 != g.S3 || T2 != g.T2 || T3 != g.T3 || K != g.K) continue;
+        RcpBwdDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.S1 = g.S1; d.S2 = g.S2; d.S3 = g.S3; d.T2 = g.T2; d.T3 = g.T3; d.K = g.K;
+        d.T2C = g.T2C; d.NT = g.NT;
+        d.B = (int32_t)B; d.T1 = (int32_t)T1; d.R = (int32_t)R; d.H = (int32_t)H; d.W = (int32_t)W;
+        d.nc = g.T2 / g.T2C;
+        d.QW = (int32_t)((W + 3) / 4);
+        d.WP = (int32_t)(((4 * d.QW + K - 1) + 3) / 4 * 4);
+        const int64_t NW = g.NT / 64, NV = KK + S1;
+        // the tallest tile whose units fit the instantiation and whose LDS fits
+        bool found = false;
+        for (int64_t TH = H; TH >= 1 && !found; TH--) {
+            const int64_t P = TH * W, PP = (P + 15) / 16 * 16, HPb = TH + K - 1;
+            if (P * g.S3 > (int64_t)g.UA * g.NT || P * g.T2C > (int64_t)g.UB * g.NT ||
+                (int64_t)g.T2C * g.T3 * TH * d.QW > (int64_t)g.UC * g.NT)
+                continue;
+            int64_t o = al4((int64_t)g.T2C * g.T3 * HPb * d.WP);
+            const int64_t o_z1 = o;
+            o = al4(o + g.S2 * g.S3 * PP / 2);
+            const int64_t o_z2 = o;
+            o = al4(o + g.S3 * g.T2C * PP / 2);
+            const int64_t o_z3 = o;
+            o = al4(o + (g.T2C * g.T3 * P + 1) / 2);
+            const int64_t o_g3 = o;
+            o = al4(o + g.T3 * g.T2C * PP / 2);
+            const int64_t o_g2 = o;
+            o = al4(o + g.T2C * g.S3 * PP / 2);
+            const int64_t o_q = o;
+            o += NV * 4 * NW;
+            const int64_t o_m3 = o;
+            o += NW * g.T3 * g.S3;
+            const int64_t o_m2 = o;
+            o += NW * g.T2C * g.S2;
+            if (4 * o > 160 * 1024) continue;
+            d.TH = (int32_t)TH;
+            d.ntiles = (int32_t)((H + TH - 1) / TH);
+            d.HPb = (int32_t)HPb;
+            d.PP = (int32_t)PP;
+            d.o_dy = 0; d.o_z1 = (int32_t)o_z1; d.o_z2 = (int32_t)o_z2; d.o_z3 = (int32_t)o_z3;
+            d.o_g3 = (int32_t)o_g3; d.o_g2 = (int32_t)o_g2; d.o_q = (int32_t)o_q;
+            d.o_m3 = (int32_t)o_m3; d.o_m2 = (int32_t)o_m2;
+            d.lds_bytes = (uint32_t)(4 * o);
+            found = true;
+        }
+        if (!found) continue;
+        d.blocks = B * T1 * d.ntiles * d.nc;
+        if (d.blocks > 0x7fffffff) continue;
+        const int64_t nblk = d.blocks, nslot = T1 * d.nc;
+        const int64_t n0 = KK, n1 = T1 * S1, n2 = T2 * S2, n3 = T3 * S3;
+        const BufRef DXP = scratch.alloc((size_t)(nslot * B * S * HW) * 4);
+        const BufRef P0 = scratch.alloc((size_t)(nblk * R * n0) * 4);
+        const BufRef P1 = scratch.alloc((size_t)(nblk * R * n1) * 4);
+        const BufRef P2 = scratch.alloc((size_t)(nblk * R * n2) * 4);
+        const BufRef P3 = scratch.alloc((size_t)(nblk * R * n3) * 4);
+        const BufRef X = f.a, W1 = f.b, W2 = f.extra[0], W3 = f.extra[1], W0 = f.extra[2];
+        auto din = [](const BufRef& in) {
+            BufRef r;
+            r.kind = BUF_DIN;
+            r.index = in.index;
+            return r;
+        };
+        Launch m;
+        m.kind = K_RCP_BWD | (1 << kBitIn) | (1 << kBitAux) | (1 << kBitOut);
+        m.a = X;
+        m.b.kind = BUF_DOUT;
+        m.extra = {W1, W2, W3, W0, DXP, P0, P1, P2, P3};
+        m.grid[0] = (uint32_t)d.blocks;
+        m.block[0] = (uint32_t)g.NT;
+        m.lds = d.lds_bytes;
+        m.desc.resize(sizeof(d));
+        std::memcpy(m.desc.data(), &d, sizeof(d));
+        m.need = 0x1f;
+        m.what = "fused RCP chain backward: steps 3-0 (recompute, g1 and g2 of every step)";
+        m.kname = "rcp_bwd<ce::rcpb::Cfg<";
+        const int tp[11] = {g.S1, g.S2, g.S3, g.T2, g.T3, g.K, g.T2C, g.NT, g.UA, g.UB, g.UC};
+        for (int i = 0; i < 11; i++) m.kname += std::to_string(tp[i]) + (i < 10 ? ", " : "> >");
+        // algorithmic bytes: X and dY read, dX partials and factor partials written
+        const double act = (double)B * HW;
+        m.alg_bytes = 2.0 * act * (double)(S + T1 * T2 * T3) + 4.0 * (double)nslot * act * S +
+                      4.0 * (double)nblk * R * (n0 + n1 + n2 + n3) + 2.0 * R * (n0 + n1 + n2 + n3);
+        m.alg_flops = 2.0 * f.alg_flops;   // backward multiplications are twice the forward's
+        out.push_back(m);
+        // the four factor gradients: ordered sums over the workgroups
+        MultiReduceDesc md;
+        std::memset(&md, 0, sizeof(md));
+        md.n = 4;
+        const BufRef parts[4] = {P1, P2, P3, P0}, outs[4] = {din(W1), din(W2), din(W3), din(W0)};
+        const int64_t ns[4] = {n1, n2, n3, n0};
+        for (int j = 0; j < 4; j++) {
+            ReduceDesc& rd = md.part[j];
+            rd.M = (int32_t)R;
+            rd.N = (int32_t)ns[j];
+            rd.nsplit = nblk;
+            rd.sCm = ns[j];
+            rd.sCn = 1;
+            md.block0[j + 1] = md.block0[j] + (R * ns[j] + 63) / 64;
+        }
+        Launch lr;
+        lr.kind = K_REDUCE_MULTI;
+        lr.extra = {parts[0], outs[0], parts[1], outs[1], parts[2], outs[2], parts[3], outs[3]};
+        lr.grid[0] = (uint32_t)md.block0[4];
+        lr.block[0] = 256;
+        lr.desc.resize(sizeof(md));
+        std::memcpy(lr.desc.data(), &md, sizeof(md));
+        lr.need = (1u << W1.index) | (1u << W2.index) | (1u << W3.index) | (1u << W0.index);
+        lr.what = "dW1, dW2, dW3, dW0: sums of workgroup partials";
+        lr.kname = "reduce_multi";
+        lr.alg_bytes = 4.0 * (double)nblk * R * (n0 + n1 + n2 + n3) + 4.0 * R * (n0 + n1 + n2 + n3);
+        out.push_back(lr);
+        // dX: ordered sum of the per-(t1, t2 chunk) partials, rounded to bf16
+        ReduceDesc rd;
+        std::memset(&rd, 0, sizeof(rd));
+        rd.M = (int32_t)B;
+        rd.N = (int32_t)(S * HW);
+        rd.nsplit = nslot;
+        rd.sCm = S * HW;
+        rd.sCn = 1;
+        Launch lx;
+        lx.kind = K_REDUCE | (0 << kBitIn) | (0 << kBitAux) | (1 << kBitOut);
+        lx.d = DXP;
+        lx.c = din(X);
+        lx.grid[0] = (uint32_t)((B * S * HW + 63) / 64);
+        lx.block[0] = 256;
+        lx.desc.resize(sizeof(rd));
+        std::memcpy(lx.desc.data(), &rd, sizeof(rd));
+        lx.need = 1u << X.index;
+        lx.what = "dX: sum of the per-(t1, t2 chunk) partials";
+        lx.kname = "reduce_partials<unsigned short>";
+        lx.alg_bytes = 4.0 * (double)nslot * act * S + 2.0 * act * S;
+        out.push_back(lx);
+        return true;
+    }
+    return false;
+}
+
+}  // namespace ce

@@ -700,6 +700,19 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 fused_bwd = true;
             }
         }
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) && p->fwd.size() == 1 &&
+            (p->fwd[0].kind & 0xff) == K_RCP_FWD) {
+            std::vector<WsItem> fitems;
+            ItemScratch fsc;
+            fsc.items = &fitems;
+            fsc.next = SCRATCH_ID;
+            std::vector<Launch> v;
+            if (fuse_rcp_backward(p->fwd[0], *p, fsc, v)) {
+                p->bwd.swap(v);
+                bitems.swap(fitems);
+                fused_bwd = true;
+            }
+        }
         ItemScratch bs;
         bs.items = &bitems;
         bs.next = SCRATCH_ID;

@@ -138,6 +138,11 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
 // sizes match a compiled instantiation.
 bool fuse_rcp_forward(const ce_plan& p, Launch& out);
 
+// Backward of a plan whose forward is one fused reshaped-CP launch `f`: one
+// fused gradient launch writing fp32 partials (dX per t1 and t2 chunk, the
+// factor gradients per workgroup), then their ordered sums.
+bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch, std::vector<Launch>& out);
+
 // Lowering of one pairwise op to launches: a specialised kernel when the
 // op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,

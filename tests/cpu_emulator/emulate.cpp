@@ -9,6 +9,7 @@
 // descriptor, layout and workspace bugs show up without a GPU, and an
 // out-of-bounds access is reported instead of faulting a device.
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -22,6 +23,9 @@
 #define RCP_FN inline
 #define RCP_HD inline
 #include "rcp_body.h"
+#define RCPB_FN inline
+#define RCPB_HD inline
+#include "rcpb_body.h"
 
 using namespace ce;
 
@@ -425,16 +429,30 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
 // exactly once.
 struct RcpHost {
     std::vector<uint32_t> lds;
+    // race tracking per 16-bit half of every LDS word
     std::vector<int> w_seg, w_tid, r_seg, r_tid;
     std::vector<char> r_multi;
-    const Buf* g[6] = {};
+    std::vector<const Buf*> g;
     std::vector<int> ywrites;
+    const Buf* ybuf = nullptr;
     int seg = 0, tid = 0;
     bool ok = true;
     std::string err;
+    // MFMA operands recorded per lane of the current wave, row-sum accumulators
+    std::vector<std::vector<std::pair<std::array<uint32_t, 4>, std::array<uint32_t, 4>>>> rec;
+    std::vector<float> rowacc;
     void fail(const std::string& m) {
         if (ok) err = m;
         ok = false;
+    }
+    void reset_lds(size_t nw) {
+        lds.assign(nw, 0xCDCDCDCDu);
+        w_seg.assign(2 * nw, -1);
+        w_tid.assign(2 * nw, -1);
+        r_seg.assign(2 * nw, -1);
+        r_tid.assign(2 * nw, -1);
+        r_multi.assign(2 * nw, 0);
+        rowacc.assign(nw, 0.f);
     }
     const Buf* buf_of(const void* p) {
         for (const Buf* b : g)
@@ -458,49 +476,70 @@ struct RcpHost {
         chk(p, 2 * i, 2);
         if (!ok) return;
         p[i] = v;
-        if (p == (uint16_t*)g[5]->base) ywrites[i]++;
+        if (ybuf && (const unsigned char*)p == ybuf->base) ywrites[i]++;
     }
-    void lds_chk(int i) {
+    void stf(float* p, int64_t i, float v) {
+        chk(p, 4 * i, 4);
+        if (!ok) return;
+        p[i] = v;
+        if (ybuf && (const unsigned char*)p == ybuf->base) ywrites[i]++;
+    }
+    void on_read(size_t h) {
+        if (w_seg[h] == seg && w_tid[h] != tid) fail("LDS race: read of data another thread wrote");
+        if (w_seg[h] < 0) fail("LDS read of data never written");
+        if (r_seg[h] == seg && r_tid[h] != tid) r_multi[h] = 1;
+        if (r_seg[h] != seg) r_multi[h] = 0;
+        r_seg[h] = seg;
+        r_tid[h] = tid;
+    }
+    void on_write(size_t h) {
+        if (w_seg[h] == seg && w_tid[h] != tid) fail("LDS race: two threads write the same data");
+        if (r_seg[h] == seg && (r_multi[h] || r_tid[h] != tid)) fail("LDS race: write of data another thread read");
+        w_seg[h] = seg;
+        w_tid[h] = tid;
+    }
+    bool lds_ok(int i) {
         if (i < 0 || i >= (int)lds.size()) fail("LDS access out of bounds");
-    }
-    void on_read(int i) {
-        if (w_seg[i] == seg && w_tid[i] != tid) fail("LDS race: read of a word another thread wrote");
-        if (w_seg[i] < 0) fail("LDS read of a word never written");
-        if (r_seg[i] == seg && r_tid[i] != tid) r_multi[i] = 1;
-        if (r_seg[i] != seg) r_multi[i] = 0;
-        r_seg[i] = seg;
-        r_tid[i] = tid;
-    }
-    void on_write(int i) {
-        if (w_seg[i] == seg && w_tid[i] != tid) fail("LDS race: two threads write one word");
-        if (r_seg[i] == seg && (r_multi[i] || r_tid[i] != tid)) fail("LDS race: write of a word another thread read");
-        w_seg[i] = seg;
-        w_tid[i] = tid;
+        return ok;
     }
     uint32_t lr(int i) {
-        lds_chk(i);
-        if (!ok) return 0;
-        on_read(i);
+        if (!lds_ok(i)) return 0;
+        on_read(2 * (size_t)i);
+        on_read(2 * (size_t)i + 1);
         return lds[i];
+    }
+    uint16_t lr16(int i, int half) {
+        if (!lds_ok(i)) return 0;
+        on_read(2 * (size_t)i + half);
+        return (uint16_t)(lds[i] >> (16 * half));
     }
     void lr4(int i, uint32_t* o) {
         if (i % 4) fail("misaligned 16-byte LDS read");
         for (int k = 0; k < 4; k++) o[k] = lr(i + k);
     }
     void lw(int i, uint32_t v) {
-        lds_chk(i);
-        if (!ok) return;
-        on_write(i);
+        if (!lds_ok(i)) return;
+        on_write(2 * (size_t)i);
+        on_write(2 * (size_t)i + 1);
         lds[i] = v;
     }
     void lw16(int i, int half, uint16_t v) {
-        lds_chk(i);
-        if (!ok) return;
-        on_write(i);
+        if (!lds_ok(i)) return;
+        on_write(2 * (size_t)i + half);
         lds[i] = half ? (lds[i] & 0xffffu) | ((uint32_t)v << 16) : (lds[i] & 0xffff0000u) | v;
     }
-    static float f(uint32_t h) {
-        uint32_t u = h << 16;
+    static float f(uint16_t h) {
+        uint32_t u = (uint32_t)h << 16;
+        float x;
+        std::memcpy(&x, &u, 4);
+        return x;
+    }
+    static uint32_t fbits(float v) {
+        uint32_t u;
+        std::memcpy(&u, &v, 4);
+        return u;
+    }
+    static float fof(uint32_t u) {
         float x;
         std::memcpy(&x, &u, 4);
         return x;
@@ -517,7 +556,43 @@ struct RcpHost {
     }
     uint32_t pk(float lo, float hi) { return (uint32_t)rne(lo) | ((uint32_t)rne(hi) << 16); }
     uint16_t bf(float v) { return rne(v); }
+    // wave-wide ops: operands are recorded per lane; the runner computes the tile
+    void mfma(const uint32_t* a, const uint32_t* b, float*) {
+        std::array<uint32_t, 4> x, y;
+        for (int k = 0; k < 4; k++) x[k] = a[k], y[k] = b[k];
+        rec[tid % 64].push_back({x, y});
+    }
+    // lanes of a row arrive in order; the row's last lane writes the sum
+    void rowsum(float x, int lane, int word) {
+        if (!lds_ok(word)) return;
+        if (lane % 16 == 0) rowacc[word] = 0.f;
+        rowacc[word] += x;
+        if (lane % 16 == 15) lw(word, fbits(rowacc[word]));
+    }
 };
+
+// The 32x32x16 bf16 MFMA of one wave from the recorded operands: lane l gave
+// A[l % 32][8 (l / 32) + i] and B[8 (l / 32) + i][l % 32] (element i of its
+// four words) per call; lane l's result i is D[8 (i / 4) + 4 (l / 32) + i % 4][l % 32].
+void emulate_mfma(RcpHost& m, std::vector<std::array<float, 16>>& acc) {
+    const size_t calls = m.rec[0].size();
+    for (int l = 0; l < 64; l++)
+        if (m.rec[l].size() != calls) m.fail("MFMA call counts differ across a wave");
+    std::vector<double> D(32 * 32, 0.0);
+    auto el = [](const std::array<uint32_t, 4>& w, int i) { return RcpHost::f((uint16_t)(w[i / 2] >> (16 * (i % 2)))); };
+    for (size_t c = 0; c < calls && m.ok; c++)
+        for (int mm = 0; mm < 32; mm++)
+            for (int nn = 0; nn < 32; nn++) {
+                double s = 0;
+                for (int k = 0; k < 16; k++)
+                    s += (double)el(m.rec[mm + 32 * (k / 8)][c].first, k % 8) * el(m.rec[nn + 32 * (k / 8)][c].second, k % 8);
+                D[mm * 32 + nn] += s;
+            }
+    acc.assign(64, {});
+    for (int l = 0; l < 64; l++)
+        for (int i = 0; i < 16; i++) acc[l][i] = (float)D[(8 * (i / 4) + 4 * (l / 32) + i % 4) * 32 + l % 32];
+    for (auto& r : m.rec) r.clear();
+}
 
 template <class C>
 bool rcp_blocks(const RcpDesc& d, RcpHost& m, const uint16_t* X, const uint16_t* W1, const uint16_t* W2,
@@ -539,9 +614,7 @@ bool rcp_blocks(const RcpDesc& d, RcpHost& m, const uint16_t* X, const uint16_t*
             return false;
         }
         const rcp::Tile t = rcp::tile_rows(d, tile);
-        std::fill(m.lds.begin(), m.lds.end(), 0xCDCDCDCDu);
-        std::fill(m.w_seg.begin(), m.w_seg.end(), -1);
-        std::fill(m.r_seg.begin(), m.r_seg.end(), -1);
+        m.reset_lds(m.lds.size());
         m.seg = 0;
         auto each = [&](auto&& fn) {
             for (int tid = 0; tid < C::NT; tid++) {
@@ -598,15 +671,9 @@ bool run_rcp_fwd(const Launch& ln, Ctx& c) {
     REQ(X.bytes >= (size_t)(2 * (int64_t)d.B * d.S1 * d.S2 * d.S3 * HW) &&
         Y.bytes >= (size_t)(2 * (int64_t)d.B * d.T1 * d.T2 * d.T3 * HW), "operand sizes");
     RcpHost m;
-    const size_t nw = d.lds_bytes / 4;
-    m.lds.assign(nw, 0);
-    m.w_seg.assign(nw, -1);
-    m.w_tid.assign(nw, -1);
-    m.r_seg.assign(nw, -1);
-    m.r_tid.assign(nw, -1);
-    m.r_multi.assign(nw, 0);
-    const Buf* gb[6] = {&X, &W1, &W2, &W3, &W0, &Y};
-    for (int i = 0; i < 6; i++) m.g[i] = gb[i];
+    m.reset_lds(d.lds_bytes / 4);
+    m.g = {&X, &W1, &W2, &W3, &W0, &Y};
+    m.ybuf = &Y;
     m.ywrites.assign(Y.bytes / 2, 0);
     const uint16_t *px = (const uint16_t*)X.base, *p1 = (const uint16_t*)W1.base, *p2 = (const uint16_t*)W2.base,
                    *p3 = (const uint16_t*)W3.base, *p0 = (const uint16_t*)W0.base;
@@ -618,6 +685,148 @@ bool run_rcp_fwd(const Launch& ln, Ctx& c) {
     REQ(m.ok, "rcp_fwd: " + m.err);
     const int64_t ny = (int64_t)d.B * d.T1 * d.T2 * d.T3 * HW;
     for (int64_t i = 0; i < ny; i++) REQ(m.ywrites[i] == 1, "a Y element is not written exactly once");
+    return true;
+}
+
+// Fused reshaped-CP backward: the kernel's phases run on the CPU between its
+// barriers (wave-wide MFMA and row sums emulated from the lanes' operands),
+// with the same bounds and race checks; every element of the dX partials and
+// of the four factor-gradient partial buffers must be written exactly once.
+template <class C>
+bool rcpb_blocks(const RcpBwdDesc& d, RcpHost& m, const uint16_t* X, const uint16_t* dY, const uint16_t* W1,
+                 const uint16_t* W2, const uint16_t* W3, const uint16_t* W0, float* DXP, float* P0, float* P1,
+                 float* P2, float* P3, std::vector<std::vector<int>>& counts, const std::vector<const Buf*>& outs) {
+    if (d.TH * d.W * C::S3 > C::UA * C::NT || d.TH * d.W * C::T2C > C::UB * C::NT ||
+        C::T2C * C::T3 * d.TH * d.QW > C::UC * C::NT) {
+        m.fail("tile units exceed the instantiation");
+        return false;
+    }
+    std::vector<rcpb::State<C>> st(C::NT);
+    std::vector<std::array<float, 16>> acc;
+    (void)counts;
+    (void)outs;
+    for (int64_t bid = 0; bid < d.blocks && m.ok; bid++) {
+        int64_t blk;
+        int b, t1, tile, chunk, h0, h1;
+        rcpb::block_coords_b(d, bid, blk, b, t1, tile, chunk);
+        if (b < 0 || b >= d.B || t1 < 0 || t1 >= d.T1 || tile < 0 || tile >= d.ntiles || chunk < 0 ||
+            chunk >= d.nc || blk < 0 || blk >= d.blocks) {
+            m.fail("block coordinates out of range");
+            return false;
+        }
+        rcpb::tile_of(d, tile, h0, h1);
+        const int P = (h1 - h0) * d.W;
+        m.reset_lds(m.lds.size());
+        m.seg = 0;
+        auto each = [&](auto&& fn) {
+            for (int tid = 0; tid < C::NT; tid++) {
+                m.tid = tid;
+                fn(tid);
+            }
+        };
+        auto waves = [&](int oA, int oB, int ld, int nk, int Mv, int Nv, int oslot, int slot_stride) {
+            for (int w = 0; w < C::NW; w++) {
+                for (int l = 0; l < 64; l++) {
+                    m.tid = 64 * w + l;
+                    float a16[16] = {};
+                    rcpb::mfma_part<C>(m, l, w, oA, oB, ld, nk, Mv, Nv, a16);
+                }
+                emulate_mfma(m, acc);
+                for (int l = 0; l < 64; l++) {
+                    m.tid = 64 * w + l;
+                    rcpb::mfma_store<C>(m, l, oslot + w * slot_stride, Mv, Nv, acc[l].data());
+                }
+            }
+        };
+        each([&](int tid) { rcpb::init<C>(m, d, tid, b, t1, h0, h1, chunk, X, dY, st[tid]); });
+        m.seg++;
+        for (int r = 0; r < d.R && m.ok; r++) {
+            each([&](int tid) {
+                rcpb::phase_a<C>(m, d, r, t1, chunk, W1, W2, st[tid]);
+                if (r > 0) rcpb::phase_f<C>(m, d, tid, blk, r - 1, t1, chunk, P0, P1, P2, P3);
+            });
+            m.seg++;
+            each([&](int tid) { rcpb::phase_b<C>(m, d, r, P, W3, st[tid]); });
+            m.seg++;
+            each([&](int tid) { rcpb::phase_c<C>(m, d, tid & 63, tid >> 6, r, P, W0, st[tid]); });
+            m.seg++;
+            each([&](int tid) { rcpb::phase_d<C>(m, d, r, W3, st[tid]); });
+            waves(d.o_g3, d.o_z2, C::T2C * d.PP, C::T2C * d.PP / 16, C::T3, C::S3, d.o_m3, C::T3 * C::S3);
+            m.seg++;
+            each([&](int tid) { rcpb::phase_e<C>(m, d, tid & 63, tid >> 6, r, t1, chunk, W1, W2, st[tid]); });
+            waves(d.o_g2, d.o_z1, C::S3 * d.PP, C::S3 * d.PP / 16, C::T2C, C::S2, d.o_m2, C::T2C * C::S2);
+            m.seg++;
+        }
+        each([&](int tid) {
+            rcpb::phase_f<C>(m, d, tid, blk, d.R - 1, t1, chunk, P0, P1, P2, P3);
+            rcpb::store_dx<C>(m, d, b, t1, h0, chunk, DXP, st[tid]);
+        });
+        m.seg++;
+    }
+    return m.ok;
+}
+
+template <int I>
+using RcpBCfgOf = rcpb::Cfg<kRcpBwdCfgs[I].S1, kRcpBwdCfgs[I].S2, kRcpBwdCfgs[I].S3, kRcpBwdCfgs[I].T2,
+                            kRcpBwdCfgs[I].T3, kRcpBwdCfgs[I].K, kRcpBwdCfgs[I].T2C, kRcpBwdCfgs[I].NT,
+                            kRcpBwdCfgs[I].UA, kRcpBwdCfgs[I].UB, kRcpBwdCfgs[I].UC>;
+
+template <class C>
+bool rcpb_is(const RcpBwdDesc& d) {
+    return d.S1 == C::S1 && d.S2 == C::S2 && d.S3 == C::S3 && d.T2 == C::T2 && d.T3 == C::T3 &&
+           d.K == C::K && d.T2C == C::T2C && d.NT == C::NT;
+}
+
+bool run_rcp_bwd(const Launch& ln, Ctx& c) {
+    RcpBwdDesc d = desc_of<RcpBwdDesc>(ln);
+    REQ(((ln.kind >> kBitIn) & 1) == 1 && ln.extra.size() == 9, "bf16 only, eleven operands");
+    Buf bufs[11];
+    bool ok = true, o;
+    bufs[0] = resolve(ln.a, c, 0, o);
+    ok = ok && o;
+    bufs[1] = resolve(ln.b, c, 0, o);
+    ok = ok && o;
+    for (int i = 0; i < 9; i++) {
+        bufs[2 + i] = resolve(ln.extra[i], c, 0, o);
+        ok = ok && o;
+    }
+    REQ(ok, "unresolved buffer");
+    REQ(rcpb::layout_ok_b(d), "LDS layout");
+    REQ(d.blocks == (int64_t)d.B * d.T1 * d.ntiles * d.nc && (int64_t)ln.grid[0] == d.blocks &&
+        (int)ln.block[0] == d.NT && ln.lds == d.lds_bytes && d.lds_bytes <= 160 * 1024, "grid / LDS");
+    const int64_t HW = (int64_t)d.H * d.W, S = (int64_t)d.S1 * d.S2 * d.S3;
+    const int64_t nslot = (int64_t)d.T1 * d.nc, nblk = d.blocks, KK = (int64_t)d.K * d.K;
+    const int64_t need[5] = {nslot * d.B * S * HW, nblk * d.R * KK, nblk * d.R * d.T1 * d.S1,
+                             nblk * d.R * d.T2 * d.S2, nblk * d.R * d.T3 * d.S3};
+    for (int i = 0; i < 5; i++) REQ(bufs[6 + i].bytes >= (size_t)(4 * need[i]), "partial buffer size");
+    RcpHost m;
+    m.reset_lds(d.lds_bytes / 4);
+    m.rec.assign(64, {});
+    for (int i = 0; i < 11; i++) m.g.push_back(&bufs[i]);
+    std::vector<std::vector<int>> counts(5);
+    std::vector<const Buf*> outs;
+    for (int i = 0; i < 5; i++) {
+        counts[i].assign(need[i], 0);
+        outs.push_back(&bufs[6 + i]);
+    }
+    auto u16 = [&](int i) { return (const uint16_t*)bufs[i].base; };
+    auto f32 = [&](int i) { return (float*)bufs[i].base; };
+    // poison the partial buffers so unwritten entries show up in the sums too
+    for (int i = 6; i < 11; i++) std::memset(bufs[i].base, 0xFF, 4 * need[i - 6]);
+    bool ran = false;
+    if (rcpb_is<RcpBCfgOf<0>>(d))
+        ran = true, rcpb_blocks<RcpBCfgOf<0>>(d, m, u16(0), u16(1), u16(2), u16(3), u16(4), u16(5), f32(6), f32(7),
+                                              f32(8), f32(9), f32(10), counts, outs);
+    else if (rcpb_is<RcpBCfgOf<1>>(d))
+        ran = true, rcpb_blocks<RcpBCfgOf<1>>(d, m, u16(0), u16(1), u16(2), u16(3), u16(4), u16(5), f32(6), f32(7),
+                                              f32(8), f32(9), f32(10), counts, outs);
+    REQ(ran, "no instantiation matches");
+    REQ(m.ok, "rcp_bwd: " + m.err);
+    // every partial written (no 0xFFFFFFFF NaN pattern left)
+    for (int i = 0; i < 5; i++) {
+        const uint32_t* w = (const uint32_t*)bufs[6 + i].base;
+        for (int64_t k = 0; k < need[i]; k++) REQ(w[k] != 0xFFFFFFFFu, "a partial is never written");
+    }
     return true;
 }
 
@@ -1107,6 +1316,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_CP_FWD ? run_cp_fwd(ln, c)
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
                     : v == K_RCP_FWD ? run_rcp_fwd(ln, c)
+                    : v == K_RCP_BWD ? run_rcp_bwd(ln, c)
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
