@@ -59,6 +59,7 @@ enum KernelKind : int32_t {
     K_REDUCE_MULTI = 32,    // up to four ordered partial sums in one launch (MultiReduceDesc)
     K_RCP_FWD = 33,         // fused reshaped-CP chain forward (RcpDesc, desc_rcp.h)
     K_RCP_BWD = 34,         // fused reshaped-CP chain backward (RcpBwdDesc, desc_rcp.h)
+    K_RCP_PREP = 35,        // its prepared factor table (RcpBwdDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).

@@ -44,8 +44,9 @@ struct RcpBwdDesc {
     int32_t S1, S2, S3, T2, T3, K, T2C, NT;
     int32_t B, T1, R, H, W;
     int32_t nc, TH, ntiles;
-    int32_t QW, WP, HPb, PP;
+    int32_t QW, WP, HPb, PP, L13, L2;   // bf16 row pitches: L13 = S3*PP + 8, L2 = T2C*PP + 8
     int32_t o_dy, o_z1, o_z2, o_z3, o_g3, o_g2, o_q, o_m3, o_m2;
+    int32_t tbs;                        // words per rank of the prepared factor table
     uint32_t lds_bytes;
     int64_t blocks;
 };

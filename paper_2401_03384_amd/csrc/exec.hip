@@ -52,9 +52,14 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
             return launch_rcp_fwd(ln, ops, c, s);
         }
         case K_RCP_BWD: {
-            const void* ops[11] = {a, b};
-            for (int i = 0; i < 9; i++) ops[2 + i] = resolve(ln.extra[i], P);
+            const void* ops[12] = {a, b};
+            for (int i = 0; i < 10; i++) ops[2 + i] = resolve(ln.extra[i], P);
             return launch_rcp_bwd(ln, ops, s);
+        }
+        case K_RCP_PREP: {
+            const void* ops[5];
+            for (int i = 0; i < 5; i++) ops[i] = resolve(ln.extra[i], P);
+            return launch_rcp_prep(ln, ops, s);
         }
         case K_CP_BWD: {
             const void* ops[11] = {a, b, c};

@@ -183,20 +183,21 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         bool found = false;
         for (int64_t TH = H; TH >= 1 && !found; TH--) {
             const int64_t P = TH * W, PP = (P + 15) / 16 * 16, HPb = TH + K - 1;
+            const int64_t L13 = g.S3 * PP + 8, L2 = g.T2C * PP + 8;
             if (P * g.S3 > (int64_t)g.UA * g.NT || P * g.T2C > (int64_t)g.UB * g.NT ||
                 (int64_t)g.T2C * g.T3 * TH * d.QW > (int64_t)g.UC * g.NT)
                 continue;
             int64_t o = al4((int64_t)g.T2C * g.T3 * HPb * d.WP);
             const int64_t o_z1 = o;
-            o = al4(o + g.S2 * g.S3 * PP / 2);
+            o = al4(o + g.S2 * L13 / 2);
             const int64_t o_z2 = o;
-            o = al4(o + g.S3 * g.T2C * PP / 2);
+            o = al4(o + g.S3 * L2 / 2);
             const int64_t o_z3 = o;
             o = al4(o + (g.T2C * g.T3 * P + 1) / 2);
             const int64_t o_g3 = o;
-            o = al4(o + g.T3 * g.T2C * PP / 2);
+            o = al4(o + g.T3 * L2 / 2);
             const int64_t o_g2 = o;
-            o = al4(o + g.T2C * g.S3 * PP / 2);
+            o = al4(o + g.T2C * L13 / 2);
             const int64_t o_q = o;
             o += NV * 4 * NW;
             const int64_t o_m3 = o;
@@ -208,6 +209,8 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
             d.ntiles = (int32_t)((H + TH - 1) / TH);
             d.HPb = (int32_t)HPb;
             d.PP = (int32_t)PP;
+            d.L13 = (int32_t)L13;
+            d.L2 = (int32_t)L2;
             d.o_dy = 0; d.o_z1 = (int32_t)o_z1; d.o_z2 = (int32_t)o_z2; d.o_z3 = (int32_t)o_z3;
             d.o_g3 = (int32_t)o_g3; d.o_g2 = (int32_t)o_g2; d.o_q = (int32_t)o_q;
             d.o_m3 = (int32_t)o_m3; d.o_m2 = (int32_t)o_m2;
@@ -217,6 +220,7 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         if (!found) continue;
         d.blocks = B * T1 * d.ntiles * d.nc;
         if (d.blocks > 0x7fffffff) continue;
+        d.tbs = (int32_t)(KK + S3 * (T3 / 2) + T1 * S1 + S2 * (T2 / 2));
         const int64_t nblk = d.blocks, nslot = T1 * d.nc;
         const int64_t n0 = KK, n1 = T1 * S1, n2 = T2 * S2, n3 = T3 * S3;
         const BufRef DXP = scratch.alloc((size_t)(nslot * B * S * HW) * 4);
@@ -224,7 +228,21 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         const BufRef P1 = scratch.alloc((size_t)(nblk * R * n1) * 4);
         const BufRef P2 = scratch.alloc((size_t)(nblk * R * n2) * 4);
         const BufRef P3 = scratch.alloc((size_t)(nblk * R * n3) * 4);
+        const BufRef TB = scratch.alloc((size_t)(R * d.tbs) * 4);
         const BufRef X = f.a, W1 = f.b, W2 = f.extra[0], W3 = f.extra[1], W0 = f.extra[2];
+        // the factor table: fp32 taps and rows, pairs along the contracted mode
+        Launch lp;
+        lp.kind = K_RCP_PREP;
+        lp.extra = {W1, W2, W3, W0, TB};
+        lp.grid[0] = (uint32_t)((R * d.tbs + 255) / 256);
+        lp.block[0] = 256;
+        lp.desc.resize(sizeof(d));
+        std::memcpy(lp.desc.data(), &d, sizeof(d));
+        lp.need = 0x1f;
+        lp.what = "factor table of the fused RCP backward";
+        lp.kname = "rcp_prep";
+        lp.alg_bytes = 2.0 * R * (KK + T1 * S1 + T2 * S2 + T3 * S3) + 4.0 * R * d.tbs;
+        out.push_back(lp);
         auto din = [](const BufRef& in) {
             BufRef r;
             r.kind = BUF_DIN;
@@ -235,7 +253,7 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         m.kind = K_RCP_BWD | (1 << kBitIn) | (1 << kBitAux) | (1 << kBitOut);
         m.a = X;
         m.b.kind = BUF_DOUT;
-        m.extra = {W1, W2, W3, W0, DXP, P0, P1, P2, P3};
+        m.extra = {W1, W2, W3, W0, DXP, P0, P1, P2, P3, TB};
         m.grid[0] = (uint32_t)d.blocks;
         m.block[0] = (uint32_t)g.NT;
         m.lds = d.lds_bytes;

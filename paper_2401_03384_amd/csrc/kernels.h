@@ -40,8 +40,10 @@ hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipS
 // Fused reshaped-CP chain forward: ops = {X, W1, W2, W3, W0}, y = Y.
 hipError_t launch_rcp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
 
-// Fused reshaped-CP chain backward: ops = {X, dY, W1, W2, W3, W0, DXP, P0, P1, P2, P3}.
+// Fused reshaped-CP chain backward: ops = {X, dY, W1, W2, W3, W0, DXP, P0, P1, P2, P3, TB},
+// and its factor table: ops = {W1, W2, W3, W0, TB}.
 hipError_t launch_rcp_bwd(const Launch& ln, const void* const* ops, hipStream_t s);
+hipError_t launch_rcp_prep(const Launch& ln, const void* const* ops, hipStream_t s);
 
 // Fused CP chain backward: ops = {X, dY, dX (may be NULL), Us, Kh, Kw, Ut,
 // Pus, Put, Pkh, Pkw}.

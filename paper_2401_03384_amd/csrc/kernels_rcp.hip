@@ -65,6 +65,7 @@ struct DevMem {
     __device__ __forceinline__ uint32_t fbits(float v) const { return __float_as_uint(v); }
     __device__ __forceinline__ float fof(uint32_t u) const { return __uint_as_float(u); }
     __device__ __forceinline__ void stf(float* p, int64_t i, float v) const { p[i] = v; }
+    __device__ __forceinline__ uint32_t ldt(const uint32_t* p, int64_t i) const { return p[i]; }
     // sum of x over the 16 lanes of this lane's row (DPP row shifts); the
     // row's last lane writes it to LDS word `word`
     __device__ __forceinline__ void rowsum(float x, int lane, int word) const {
@@ -168,7 +169,8 @@ __global__ void __launch_bounds__(C::NT) rcp_bwd(RcpBwdDesc d, const uint16_t* _
                                                 const uint16_t* __restrict__ W3,
                                                 const uint16_t* __restrict__ W0, float* __restrict__ DXP,
                                                 float* __restrict__ P0, float* __restrict__ P1,
-                                                float* __restrict__ P2, float* __restrict__ P3) {
+                                                float* __restrict__ P2, float* __restrict__ P3,
+                                                const uint32_t* __restrict__ TB) {
     extern __shared__ uint32_t lds_words[];
     DevMem m{lds_words};
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -186,25 +188,36 @@ __global__ void __launch_bounds__(C::NT) rcp_bwd(RcpBwdDesc d, const uint16_t* _
         __syncthreads();
         rcpb::phase_b<C>(m, d, r, P, W3, st);
         __syncthreads();
-        rcpb::phase_c<C>(m, d, lane, wave, r, P, W0, st);
+        rcpb::phase_c<C>(m, d, lane, wave, r, P, TB, st);
         __syncthreads();
-        rcpb::phase_d<C>(m, d, r, W3, st);
+        rcpb::phase_d<C>(m, d, r, TB, st);
         {
             float acc[16] = {};
-            rcpb::mfma_part<C>(m, lane, wave, d.o_g3, d.o_z2, C::T2C * d.PP, C::T2C * d.PP / 16, C::T3, C::S3, acc);
+            rcpb::mfma_part<C>(m, lane, wave, d.o_g3, d.o_z2, d.L2, C::T2C * d.PP / 16, C::T3, C::S3, acc);
             rcpb::mfma_store<C>(m, lane, d.o_m3 + wave * C::T3 * C::S3, C::T3, C::S3, acc);
         }
         __syncthreads();
-        rcpb::phase_e<C>(m, d, lane, wave, r, t1, chunk, W1, W2, st);
+        rcpb::phase_e<C>(m, d, lane, wave, r, t1, chunk, TB, st);
         {
             float acc[16] = {};
-            rcpb::mfma_part<C>(m, lane, wave, d.o_g2, d.o_z1, C::S3 * d.PP, C::S3 * d.PP / 16, C::T2C, C::S2, acc);
+            rcpb::mfma_part<C>(m, lane, wave, d.o_g2, d.o_z1, d.L13, C::S3 * d.PP / 16, C::T2C, C::S2, acc);
             rcpb::mfma_store<C>(m, lane, d.o_m2 + wave * C::T2C * C::S2, C::T2C, C::S2, acc);
         }
         __syncthreads();
     }
     rcpb::phase_f<C>(m, d, tid, blk, d.R - 1, t1, chunk, P0, P1, P2, P3);
     rcpb::store_dx<C>(m, d, b, t1, h0, chunk, DXP, st);
+}
+
+// The prepared factor table of the backward (rcpb::table_word), one word a thread.
+__global__ void __launch_bounds__(256) rcp_prep(RcpBwdDesc d, const uint16_t* __restrict__ W1,
+                                                const uint16_t* __restrict__ W2,
+                                                const uint16_t* __restrict__ W3,
+                                                const uint16_t* __restrict__ W0, uint32_t* __restrict__ TB) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)d.R * d.tbs) return;
+    DevMem m{nullptr};
+    TB[i] = rcpb::table_word(m, d, i, W1, W2, W3, W0);
 }
 
 template <int I>
@@ -239,7 +252,7 @@ hipError_t launch_rcpb_c(const RcpBwdDesc& d, const void* const* o, hipStream_t 
     hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(C::NT), d.lds_bytes, s, d, (const uint16_t*)o[0],
                        (const uint16_t*)o[1], (const uint16_t*)o[2], (const uint16_t*)o[3],
                        (const uint16_t*)o[4], (const uint16_t*)o[5], (float*)o[6], (float*)o[7],
-                       (float*)o[8], (float*)o[9], (float*)o[10]);
+                       (float*)o[8], (float*)o[9], (float*)o[10], (const uint32_t*)o[11]);
     return hipGetLastError();
 }
 
@@ -259,20 +272,31 @@ hipError_t launch_rcp_fwd(const Launch& ln, const void* const* ops, void* y, hip
     return hipErrorInvalidValue;
 }
 
-// ops = {X, dY, W1, W2, W3, W0, DXP, P0, P1, P2, P3}; the mode factors are read
-// as 32-bit words (4-byte aligned base addresses).
+// ops = {X, dY, W1, W2, W3, W0, DXP, P0, P1, P2, P3, TB}; the mode factors are
+// read as 32-bit words (4-byte aligned base addresses).
 hipError_t launch_rcp_bwd(const Launch& ln, const void* const* ops, hipStream_t s) {
     RcpBwdDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
     for (int i = 2; i <= 4; i++)
         if (((uintptr_t)ops[i]) & 3) return hipErrorInvalidValue;
-    for (int i = 0; i < 11; i++)
+    for (int i = 0; i < 12; i++)
         if (!ops[i]) return hipErrorInvalidValue;
     const int64_t want = (int64_t)d.B * d.T1 * d.ntiles * d.nc;
     if (d.blocks != want || ln.lds != d.lds_bytes) return hipErrorInvalidValue;
     if (fits_b<BCfgOf<0>>(d)) return launch_rcpb_c<BCfgOf<0>>(d, ops, s);
     if (fits_b<BCfgOf<1>>(d)) return launch_rcpb_c<BCfgOf<1>>(d, ops, s);
     return hipErrorInvalidValue;
+}
+
+// ops = {W1, W2, W3, W0, TB}.
+hipError_t launch_rcp_prep(const Launch& ln, const void* const* ops, hipStream_t s) {
+    RcpBwdDesc d;
+    std::memcpy(&d, ln.desc.data(), sizeof(d));
+    const int64_t n = (int64_t)d.R * d.tbs;
+    if (n <= 0 || (int64_t)ln.grid[0] * 256 < n || !ops[4]) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(rcp_prep, dim3(ln.grid[0]), dim3(256), 0, s, d, (const uint16_t*)ops[0],
+                       (const uint16_t*)ops[1], (const uint16_t*)ops[2], (const uint16_t*)ops[3], (uint32_t*)ops[4]);
+    return hipGetLastError();
 }
 
 }  // namespace ce

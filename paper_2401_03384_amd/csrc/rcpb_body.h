@@ -64,13 +64,15 @@ RCPB_HD void tile_of(const RcpBwdDesc& d, int i, int& h0, int& h1) {
 // The LDS layout invariants every access relies on.
 RCPB_HD bool layout_ok_b(const RcpBwdDesc& d) {
     const int P = d.TH * d.W, S3 = d.S3, T3 = d.T3, T2C = d.T2C;
-    const int64_t e_z1 = (int64_t)d.S2 * S3 * d.PP, e_z2 = (int64_t)S3 * T2C * d.PP,
-                  e_z3 = (int64_t)T2C * T3 * P, e_g3 = (int64_t)T3 * T2C * d.PP, e_g2 = (int64_t)T2C * S3 * d.PP;
+    const int64_t e_z1 = (int64_t)d.S2 * d.L13, e_z2 = (int64_t)S3 * d.L2, e_z3 = (int64_t)T2C * T3 * P,
+                  e_g3 = (int64_t)T3 * d.L2, e_g2 = (int64_t)T2C * d.L13;
     const int64_t w_dy = (int64_t)T2C * T3 * d.HPb * d.WP;
     const int nv = d.K * d.K + d.S1, nw = d.NT / 64;
     return d.H > 0 && d.W > 0 && d.K % 2 == 1 && d.TH > 0 && d.ntiles == (d.H + d.TH - 1) / d.TH &&
            d.QW == (d.W + 3) / 4 && d.WP % 4 == 0 && d.WP >= 4 * d.QW + 4 && d.HPb == d.TH + d.K - 1 &&
            d.PP % 16 == 0 && d.PP >= P && d.T2 == d.nc * T2C && d.R >= 1 && d.NT % 64 == 0 &&
+           d.L13 == S3 * d.PP + 8 && d.L2 == T2C * d.PP + 8 &&
+           d.tbs == d.K * d.K + S3 * (T3 / 2) + d.T1 * d.S1 + d.S2 * (d.T2 / 2) &&
            d.o_dy == 0 && d.o_z1 >= d.o_dy + w_dy && d.o_z1 % 4 == 0 && d.o_z2 >= d.o_z1 + e_z1 / 2 &&
            d.o_z2 % 4 == 0 && d.o_z3 >= d.o_z2 + e_z2 / 2 && d.o_z3 % 4 == 0 &&
            d.o_g3 >= d.o_z3 + (e_z3 + 1) / 2 && d.o_g3 % 4 == 0 && d.o_g2 >= d.o_g3 + e_g3 / 2 && d.o_g2 % 4 == 0 &&
@@ -100,13 +102,6 @@ struct State {
     int c_pl[C::UC], c_hl[C::UC], c_q[C::UC];   // unit (plane, row, quad); c_pl = -1: none
 };
 
-// bf16 element e of a weight buffer (an even number of elements) through the
-// aligned 32-bit word that holds it.
-template <class M>
-RCPB_FN uint32_t welem(M& m, const uint16_t* p, int64_t e) {
-    return (m.ldw(p, e & ~(int64_t)1) >> (16 * (int)(e & 1))) & 0xffffu;
-}
-
 // bf16 element e of an LDS region that starts at word o.
 template <class M>
 RCPB_FN uint16_t lds_e(M& m, int o, int e) {
@@ -116,6 +111,15 @@ template <class M>
 RCPB_FN void lds_se(M& m, int o, int e, uint16_t v) {
     m.lw16(o + (e >> 1), e & 1, v);
 }
+
+// Element index of the k-contiguous rows: Z1k row s2 and G2k row t2l hold
+// k = s3 * PP + n (pitch L13), Z2k row s3 and G3k row t3 hold k = t2l * PP + n
+// (pitch L2); each pitch is 8 elements past the row so that consecutive
+// rows start 16 bytes apart in the LDS banks.
+RCPB_FN int iz1(const RcpBwdDesc& d, int s2, int s3, int n) { return s2 * d.L13 + s3 * d.PP + n; }
+RCPB_FN int ig2(const RcpBwdDesc& d, int t2l, int s3, int n) { return t2l * d.L13 + s3 * d.PP + n; }
+RCPB_FN int iz2(const RcpBwdDesc& d, int s3, int t2l, int n) { return s3 * d.L2 + t2l * d.PP + n; }
+RCPB_FN int ig3(const RcpBwdDesc& d, int t3, int t2l, int n) { return t3 * d.L2 + t2l * d.PP + n; }
 
 // Unit coordinates, X, zero dX, the dY planes (zero outside the image) and
 // zero padding columns of the k-contiguous rows.
@@ -184,17 +188,24 @@ RCPB_FN void init(M& m, const RcpBwdDesc& d, int tid, int b, int t1, int h0, int
     }
     // zero padding of the k-contiguous rows (pixels P .. PP-1), never written later
     const int pad = d.PP - P;
-    const int rows1 = C::S2 * C::S3, rows2 = C::S3 * C::T2C, rows3 = C::T3 * C::T2C, rows4 = C::T2C * C::S3;
-    for (int i = tid; i < (rows1 + rows2 + rows3 + rows4) * pad; i += C::NT) {
-        const int row = i / pad, e = P + i % pad;
-        if (row < rows1) lds_se(m, d.o_z1, row * d.PP + e, 0);
-        else if (row < rows1 + rows2) lds_se(m, d.o_z2, (row - rows1) * d.PP + e, 0);
-        else if (row < rows1 + rows2 + rows3) lds_se(m, d.o_g3, (row - rows1 - rows2) * d.PP + e, 0);
-        else lds_se(m, d.o_g2, (row - rows1 - rows2 - rows3) * d.PP + e, 0);
+    const int g1 = C::S2 * C::S3, g2 = C::S3 * C::T2C, g3 = C::T3 * C::T2C, g4 = C::T2C * C::S3;
+    for (int i = tid; i < (g1 + g2 + g3 + g4) * pad; i += C::NT) {
+        int row = i / pad;
+        const int e = P + i % pad;
+        if (row < g1) {
+            lds_se(m, d.o_z1, iz1(d, row / C::S3, row % C::S3, e), 0);
+        } else if ((row -= g1) < g2) {
+            lds_se(m, d.o_z2, iz2(d, row / C::T2C, row % C::T2C, e), 0);
+        } else if ((row -= g2) < g3) {
+            lds_se(m, d.o_g3, ig3(d, row / C::T2C, row % C::T2C, e), 0);
+        } else {
+            row -= g3;
+            lds_se(m, d.o_g2, ig2(d, row / C::S3, row % C::S3, e), 0);
+        }
     }
 }
 
-// A: Z1[s2] at (n, s3) for t1 -> Z1k[(s2 S3 + s3) PP + n]; Z2[t2l] -> Z2k[(s3 T2C + t2l) PP + n].
+// A: Z1[s2] at (n, s3) for t1 -> Z1k; Z2[t2l] -> Z2k.
 template <class C, class M>
 RCPB_FN void phase_a(M& m, const RcpBwdDesc& d, int r, int t1, int chunk, const uint16_t* W1,
                      const uint16_t* W2, const State<C>& st) {
@@ -221,15 +232,15 @@ RCPB_FN void phase_a(M& m, const RcpBwdDesc& d, int r, int t1, int chunk, const 
                 a1 = m.dot2(w1[j], st.xp[k][j][2 * i + 1], a1);
             }
             z1p[i] = m.pk(a0, a1);
-            lds_se(m, d.o_z1, ((2 * i) * C::S3 + s3) * d.PP + n, (uint16_t)(z1p[i] & 0xffff));
-            lds_se(m, d.o_z1, ((2 * i + 1) * C::S3 + s3) * d.PP + n, (uint16_t)(z1p[i] >> 16));
+            lds_se(m, d.o_z1, iz1(d, 2 * i, s3, n), (uint16_t)(z1p[i] & 0xffff));
+            lds_se(m, d.o_z1, iz1(d, 2 * i + 1, s3, n), (uint16_t)(z1p[i] >> 16));
         }
 #pragma unroll
         for (int t = 0; t < C::T2C; t++) {
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < C::S2P; i++) a = m.dot2(w2[t][i], z1p[i], a);
-            lds_se(m, d.o_z2, (s3 * C::T2C + t) * d.PP + n, m.bf(a));
+            lds_se(m, d.o_z2, iz2(d, s3, t, n), m.bf(a));
         }
     }
 }
@@ -249,8 +260,8 @@ RCPB_FN void phase_b(M& m, const RcpBwdDesc& d, int r, int P, const uint16_t* W3
         uint32_t z[C::S3P];
 #pragma unroll
         for (int i = 0; i < C::S3P; i++)
-            z[i] = (uint32_t)lds_e(m, d.o_z2, ((2 * i) * C::T2C + t2l) * d.PP + n) |
-                   ((uint32_t)lds_e(m, d.o_z2, ((2 * i + 1) * C::T2C + t2l) * d.PP + n) << 16);
+            z[i] = (uint32_t)lds_e(m, d.o_z2, iz2(d, 2 * i, t2l, n)) |
+                   ((uint32_t)lds_e(m, d.o_z2, iz2(d, 2 * i + 1, t2l, n)) << 16);
 #pragma unroll
         for (int t = 0; t < C::T3; t++) {
             float a = 0.f;
@@ -266,12 +277,12 @@ RCPB_FN void phase_b(M& m, const RcpBwdDesc& d, int r, int P, const uint16_t* W3
 // unit's dW0 terms; the thread's dW0 partials are summed over each 16-lane
 // row of the wave into Q.
 template <class C, class M>
-RCPB_FN void phase_c(M& m, const RcpBwdDesc& d, int lane, int wave, int r, int P, const uint16_t* W0,
+RCPB_FN void phase_c(M& m, const RcpBwdDesc& d, int lane, int wave, int r, int P, const uint32_t* TB,
                      const State<C>& st) {
     float w0[C::KK], dw[C::KK];
 #pragma unroll
     for (int t = 0; t < C::KK; t++) {
-        w0[t] = m.f((uint16_t)welem(m, W0, (int64_t)r * C::KK + t));
+        w0[t] = m.fof(m.ldt(TB, (int64_t)r * d.tbs + t));
         dw[t] = 0.f;
     }
 #pragma unroll
@@ -304,23 +315,21 @@ RCPB_FN void phase_c(M& m, const RcpBwdDesc& d, int lane, int wave, int r, int P
         }
 #pragma unroll
         for (int o = 0; o < 4; o++)
-            if (4 * q + o < d.W) lds_se(m, d.o_g3, (t3 * C::T2C + t2l) * d.PP + hl * d.W + 4 * q + o, m.bf(g[o]));
+            if (4 * q + o < d.W) lds_se(m, d.o_g3, ig3(d, t3, t2l, hl * d.W + 4 * q + o), m.bf(g[o]));
     }
     // sums over each 16-lane row of the wave: Q[tap][4 wave + row]
 #pragma unroll
     for (int t = 0; t < C::KK; t++) m.rowsum(dw[t], lane, d.o_q + t * 4 * C::NW + 4 * wave + (lane >> 4));
 }
 
-// D: G2[s3] at (n, t2l) -> G2k[(t2l S3 + s3) PP + n].
+// D: G2[s3] at (n, t2l) -> G2k.
 template <class C, class M>
-RCPB_FN void phase_d(M& m, const RcpBwdDesc& d, int r, const uint16_t* W3, const State<C>& st) {
+RCPB_FN void phase_d(M& m, const RcpBwdDesc& d, int r, const uint32_t* TB, const State<C>& st) {
     uint32_t w3t[C::S3][C::T3P];   // (W3[2i][s3], W3[2i+1][s3])
 #pragma unroll
     for (int s = 0; s < C::S3; s++)
 #pragma unroll
-        for (int i = 0; i < C::T3P; i++)
-            w3t[s][i] = welem(m, W3, ((int64_t)r * C::T3 + 2 * i) * C::S3 + s) |
-                        (welem(m, W3, ((int64_t)r * C::T3 + 2 * i + 1) * C::S3 + s) << 16);
+        for (int i = 0; i < C::T3P; i++) w3t[s][i] = m.ldt(TB, (int64_t)r * d.tbs + C::KK + s * C::T3P + i);
 #pragma unroll
     for (int k = 0; k < C::UB; k++) {
         if (st.b_n[k] < 0) continue;
@@ -328,14 +337,14 @@ RCPB_FN void phase_d(M& m, const RcpBwdDesc& d, int r, const uint16_t* W3, const
         uint32_t g[C::T3P];
 #pragma unroll
         for (int i = 0; i < C::T3P; i++)
-            g[i] = (uint32_t)lds_e(m, d.o_g3, ((2 * i) * C::T2C + t2l) * d.PP + n) |
-                   ((uint32_t)lds_e(m, d.o_g3, ((2 * i + 1) * C::T2C + t2l) * d.PP + n) << 16);
+            g[i] = (uint32_t)lds_e(m, d.o_g3, ig3(d, 2 * i, t2l, n)) |
+                   ((uint32_t)lds_e(m, d.o_g3, ig3(d, 2 * i + 1, t2l, n)) << 16);
 #pragma unroll
         for (int s = 0; s < C::S3; s++) {
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < C::T3P; i++) a = m.dot2(w3t[s][i], g[i], a);
-            lds_se(m, d.o_g2, (t2l * C::S3 + s) * d.PP + n, m.bf(a));
+            lds_se(m, d.o_g2, ig2(d, t2l, s, n), m.bf(a));
         }
     }
 }
@@ -374,22 +383,21 @@ RCPB_FN void mfma_store(M& m, int lane, int o, int Mv, int Nv, const float* acc)
 // dW1[s1] partial += G1[s2] X[s1][s2]; row sums of the dW1 partials -> Q.
 template <class C, class M>
 RCPB_FN void phase_e(M& m, const RcpBwdDesc& d, int lane, int wave, int r, int t1, int chunk,
-                     const uint16_t* W1, const uint16_t* W2, State<C>& st) {
+                     const uint32_t* TB, State<C>& st) {
     static_assert(C::T2C % 2 == 0, "t2 chunks come in pairs");
     constexpr int T2P = C::T2C / 2;
     float w1[C::S1], dw1[C::S1];
     uint32_t w2p[C::S2][T2P];   // (W2[2i][s2], W2[2i+1][s2]) of the chunk
+    const int64_t o1 = (int64_t)r * d.tbs + C::KK + C::S3 * C::T3P, o2 = o1 + (int64_t)d.T1 * C::S1;
 #pragma unroll
     for (int s = 0; s < C::S1; s++) {
-        w1[s] = m.f((uint16_t)welem(m, W1, ((int64_t)r * d.T1 + t1) * C::S1 + s));
+        w1[s] = m.fof(m.ldt(TB, o1 + t1 * C::S1 + s));
         dw1[s] = 0.f;
     }
 #pragma unroll
     for (int s = 0; s < C::S2; s++)
 #pragma unroll
-        for (int i = 0; i < T2P; i++)
-            w2p[s][i] = welem(m, W2, ((int64_t)r * C::T2 + chunk * C::T2C + 2 * i) * C::S2 + s) |
-                        (welem(m, W2, ((int64_t)r * C::T2 + chunk * C::T2C + 2 * i + 1) * C::S2 + s) << 16);
+        for (int i = 0; i < T2P; i++) w2p[s][i] = m.ldt(TB, o2 + s * (C::T2 / 2) + chunk * T2P + i);
 #pragma unroll
     for (int k = 0; k < C::UA; k++) {
         if (st.a_n[k] < 0) continue;
@@ -397,8 +405,8 @@ RCPB_FN void phase_e(M& m, const RcpBwdDesc& d, int lane, int wave, int r, int t
         uint32_t g2[T2P];
 #pragma unroll
         for (int i = 0; i < T2P; i++)
-            g2[i] = (uint32_t)lds_e(m, d.o_g2, ((2 * i) * C::S3 + s3) * d.PP + n) |
-                    ((uint32_t)lds_e(m, d.o_g2, ((2 * i + 1) * C::S3 + s3) * d.PP + n) << 16);
+            g2[i] = (uint32_t)lds_e(m, d.o_g2, ig2(d, 2 * i, s3, n)) |
+                    ((uint32_t)lds_e(m, d.o_g2, ig2(d, 2 * i + 1, s3, n)) << 16);
 #pragma unroll
         for (int s2 = 0; s2 < C::S2; s2++) {
             float g1 = 0.f;
@@ -453,6 +461,32 @@ RCPB_FN void phase_f(M& m, const RcpBwdDesc& d, int tid, int64_t blk, int r, int
             m.stf(P3, (blk * d.R + r) * n3 + e, s);
         }
     }
+}
+
+// Word i of the prepared factor table (row r = i / tbs):
+//   [0, KK)                W0[r][tap] as fp32
+//   [KK, + S3*T3/2)        (W3[r][2j][s3], W3[r][2j+1][s3]) at s3 * T3/2 + j
+//   [.., + T1*S1)          W1[r][t1][s1] as fp32 at t1 * S1 + s1
+//   [.., + S2*T2/2)        (W2[r][2j][s2], W2[r][2j+1][s2]) at s2 * T2/2 + j
+template <class M>
+RCPB_FN uint32_t table_word(M& m, const RcpBwdDesc& d, int64_t i, const uint16_t* W1, const uint16_t* W2,
+                            const uint16_t* W3, const uint16_t* W0) {
+    const int64_t r = i / d.tbs;
+    int64_t e = i % d.tbs;
+    const int KK = d.K * d.K, T3P = d.T3 / 2, T2P = d.T2 / 2;
+    if (e < KK) return m.fbits(m.f(m.ld16(W0, r * KK + e)));
+    e -= KK;
+    if (e < (int64_t)d.S3 * T3P) {
+        const int s3 = (int)(e / T3P), j = (int)(e % T3P);
+        return (uint32_t)m.ld16(W3, (r * d.T3 + 2 * j) * d.S3 + s3) |
+               ((uint32_t)m.ld16(W3, (r * d.T3 + 2 * j + 1) * d.S3 + s3) << 16);
+    }
+    e -= (int64_t)d.S3 * T3P;
+    if (e < (int64_t)d.T1 * d.S1) return m.fbits(m.f(m.ld16(W1, r * d.T1 * d.S1 + e)));
+    e -= (int64_t)d.T1 * d.S1;
+    const int s2 = (int)(e / T2P), j = (int)(e % T2P);
+    return (uint32_t)m.ld16(W2, (r * d.T2 + 2 * j) * d.S2 + s2) |
+           ((uint32_t)m.ld16(W2, (r * d.T2 + 2 * j + 1) * d.S2 + s2) << 16);
 }
 
 // dX partial of the workgroup: DXP[t1 * nc + chunk][b][s1][s2][s3][h0 W + n].

@@ -478,6 +478,14 @@ struct RcpHost {
         p[i] = v;
         if (ybuf && (const unsigned char*)p == ybuf->base) ywrites[i]++;
     }
+    uint32_t ldt(const uint32_t* p, int64_t i) {
+        chk(p, 4 * i, 4);
+        return ok ? p[i] : 0;
+    }
+    void stt(uint32_t* p, int64_t i, uint32_t v) {
+        chk(p, 4 * i, 4);
+        if (ok) p[i] = v;
+    }
     void stf(float* p, int64_t i, float v) {
         chk(p, 4 * i, 4);
         if (!ok) return;
@@ -695,7 +703,8 @@ bool run_rcp_fwd(const Launch& ln, Ctx& c) {
 template <class C>
 bool rcpb_blocks(const RcpBwdDesc& d, RcpHost& m, const uint16_t* X, const uint16_t* dY, const uint16_t* W1,
                  const uint16_t* W2, const uint16_t* W3, const uint16_t* W0, float* DXP, float* P0, float* P1,
-                 float* P2, float* P3, std::vector<std::vector<int>>& counts, const std::vector<const Buf*>& outs) {
+                 float* P2, float* P3, const uint32_t* TB, std::vector<std::vector<int>>& counts,
+                 const std::vector<const Buf*>& outs) {
     if (d.TH * d.W * C::S3 > C::UA * C::NT || d.TH * d.W * C::T2C > C::UB * C::NT ||
         C::T2C * C::T3 * d.TH * d.QW > C::UC * C::NT) {
         m.fail("tile units exceed the instantiation");
@@ -748,13 +757,13 @@ bool rcpb_blocks(const RcpBwdDesc& d, RcpHost& m, const uint16_t* X, const uint1
             m.seg++;
             each([&](int tid) { rcpb::phase_b<C>(m, d, r, P, W3, st[tid]); });
             m.seg++;
-            each([&](int tid) { rcpb::phase_c<C>(m, d, tid & 63, tid >> 6, r, P, W0, st[tid]); });
+            each([&](int tid) { rcpb::phase_c<C>(m, d, tid & 63, tid >> 6, r, P, TB, st[tid]); });
             m.seg++;
-            each([&](int tid) { rcpb::phase_d<C>(m, d, r, W3, st[tid]); });
-            waves(d.o_g3, d.o_z2, C::T2C * d.PP, C::T2C * d.PP / 16, C::T3, C::S3, d.o_m3, C::T3 * C::S3);
+            each([&](int tid) { rcpb::phase_d<C>(m, d, r, TB, st[tid]); });
+            waves(d.o_g3, d.o_z2, d.L2, C::T2C * d.PP / 16, C::T3, C::S3, d.o_m3, C::T3 * C::S3);
             m.seg++;
-            each([&](int tid) { rcpb::phase_e<C>(m, d, tid & 63, tid >> 6, r, t1, chunk, W1, W2, st[tid]); });
-            waves(d.o_g2, d.o_z1, C::S3 * d.PP, C::S3 * d.PP / 16, C::T2C, C::S2, d.o_m2, C::T2C * C::S2);
+            each([&](int tid) { rcpb::phase_e<C>(m, d, tid & 63, tid >> 6, r, t1, chunk, TB, st[tid]); });
+            waves(d.o_g2, d.o_z1, d.L13, C::S3 * d.PP / 16, C::T2C, C::S2, d.o_m2, C::T2C * C::S2);
             m.seg++;
         }
         each([&](int tid) {
@@ -777,16 +786,39 @@ bool rcpb_is(const RcpBwdDesc& d) {
            d.K == C::K && d.T2C == C::T2C && d.NT == C::NT;
 }
 
+// The factor table of the fused backward: every word from rcpb::table_word.
+bool run_rcp_prep(const Launch& ln, Ctx& c) {
+    RcpBwdDesc d = desc_of<RcpBwdDesc>(ln);
+    REQ(ln.extra.size() == 5, "five operands");
+    Buf b[5];
+    bool ok = true, o;
+    for (int i = 0; i < 5; i++) {
+        b[i] = resolve(ln.extra[i], c, 0, o);
+        ok = ok && o;
+    }
+    REQ(ok, "unresolved buffer");
+    const int64_t n = (int64_t)d.R * d.tbs;
+    REQ(n > 0 && (int64_t)ln.grid[0] * 256 >= n && ln.block[0] == 256, "grid");
+    RcpHost m;
+    for (int i = 0; i < 5; i++) m.g.push_back(&b[i]);
+    for (int64_t i = 0; i < n && m.ok; i++)
+        m.stt((uint32_t*)b[4].base, i,
+              rcpb::table_word(m, d, i, (const uint16_t*)b[0].base, (const uint16_t*)b[1].base,
+                               (const uint16_t*)b[2].base, (const uint16_t*)b[3].base));
+    REQ(m.ok, "rcp_prep: " + m.err);
+    return true;
+}
+
 bool run_rcp_bwd(const Launch& ln, Ctx& c) {
     RcpBwdDesc d = desc_of<RcpBwdDesc>(ln);
-    REQ(((ln.kind >> kBitIn) & 1) == 1 && ln.extra.size() == 9, "bf16 only, eleven operands");
-    Buf bufs[11];
+    REQ(((ln.kind >> kBitIn) & 1) == 1 && ln.extra.size() == 10, "bf16 only, twelve operands");
+    Buf bufs[12];
     bool ok = true, o;
     bufs[0] = resolve(ln.a, c, 0, o);
     ok = ok && o;
     bufs[1] = resolve(ln.b, c, 0, o);
     ok = ok && o;
-    for (int i = 0; i < 9; i++) {
+    for (int i = 0; i < 10; i++) {
         bufs[2 + i] = resolve(ln.extra[i], c, 0, o);
         ok = ok && o;
     }
@@ -799,10 +831,11 @@ bool run_rcp_bwd(const Launch& ln, Ctx& c) {
     const int64_t need[5] = {nslot * d.B * S * HW, nblk * d.R * KK, nblk * d.R * d.T1 * d.S1,
                              nblk * d.R * d.T2 * d.S2, nblk * d.R * d.T3 * d.S3};
     for (int i = 0; i < 5; i++) REQ(bufs[6 + i].bytes >= (size_t)(4 * need[i]), "partial buffer size");
+    REQ(bufs[11].bytes >= (size_t)(4 * (int64_t)d.R * d.tbs), "factor table size");
     RcpHost m;
     m.reset_lds(d.lds_bytes / 4);
     m.rec.assign(64, {});
-    for (int i = 0; i < 11; i++) m.g.push_back(&bufs[i]);
+    for (int i = 0; i < 12; i++) m.g.push_back(&bufs[i]);
     std::vector<std::vector<int>> counts(5);
     std::vector<const Buf*> outs;
     for (int i = 0; i < 5; i++) {
@@ -816,10 +849,10 @@ bool run_rcp_bwd(const Launch& ln, Ctx& c) {
     bool ran = false;
     if (rcpb_is<RcpBCfgOf<0>>(d))
         ran = true, rcpb_blocks<RcpBCfgOf<0>>(d, m, u16(0), u16(1), u16(2), u16(3), u16(4), u16(5), f32(6), f32(7),
-                                              f32(8), f32(9), f32(10), counts, outs);
+                                              f32(8), f32(9), f32(10), (const uint32_t*)bufs[11].base, counts, outs);
     else if (rcpb_is<RcpBCfgOf<1>>(d))
         ran = true, rcpb_blocks<RcpBCfgOf<1>>(d, m, u16(0), u16(1), u16(2), u16(3), u16(4), u16(5), f32(6), f32(7),
-                                              f32(8), f32(9), f32(10), counts, outs);
+                                              f32(8), f32(9), f32(10), (const uint32_t*)bufs[11].base, counts, outs);
     REQ(ran, "no instantiation matches");
     REQ(m.ok, "rcp_bwd: " + m.err);
     // every partial written (no 0xFFFFFFFF NaN pattern left)
@@ -1317,6 +1350,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_CP_BWD ? run_cp_bwd(ln, c)
                     : v == K_RCP_FWD ? run_rcp_fwd(ln, c)
                     : v == K_RCP_BWD ? run_rcp_bwd(ln, c)
+                    : v == K_RCP_PREP ? run_rcp_prep(ln, c)
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
