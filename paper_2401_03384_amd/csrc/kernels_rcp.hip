@@ -162,7 +162,7 @@ hipError_t launch_rcp_c(const RcpDesc& d, const void* const* o, void* y, hipStre
 }
 
 template <class C>
-__global__ void __launch_bounds__(C::NT) rcp_bwd(RcpBwdDesc d, const uint16_t* __restrict__ X,
+__global__ void __launch_bounds__(C::NT, C::MW) rcp_bwd(RcpBwdDesc d, const uint16_t* __restrict__ X,
                                                 const uint16_t* __restrict__ dY,
                                                 const uint16_t* __restrict__ W1,
                                                 const uint16_t* __restrict__ W2,
@@ -223,7 +223,7 @@ __global__ void __launch_bounds__(256) rcp_prep(RcpBwdDesc d, const uint16_t* __
 template <int I>
 using BCfgOf = rcpb::Cfg<kRcpBwdCfgs[I].S1, kRcpBwdCfgs[I].S2, kRcpBwdCfgs[I].S3, kRcpBwdCfgs[I].T2,
                          kRcpBwdCfgs[I].T3, kRcpBwdCfgs[I].K, kRcpBwdCfgs[I].T2C, kRcpBwdCfgs[I].NT,
-                         kRcpBwdCfgs[I].UA, kRcpBwdCfgs[I].UB, kRcpBwdCfgs[I].UC>;
+                         kRcpBwdCfgs[I].UA, kRcpBwdCfgs[I].UB, kRcpBwdCfgs[I].UC, kRcpBwdCfgs[I].MW>;
 static_assert(kNumRcpBwdCfgs == 2, "one launch branch per instantiation");
 
 template <class C>

@@ -41,8 +41,9 @@
 namespace ce {
 namespace rcpb {
 
-template <int S1_, int S2_, int S3_, int T2_, int T3_, int K_, int T2C_, int NT_, int UA_, int UB_, int UC_>
+template <int S1_, int S2_, int S3_, int T2_, int T3_, int K_, int T2C_, int NT_, int UA_, int UB_, int UC_, int MW_>
 struct Cfg {
+    static constexpr int MW = MW_;   // waves per SIMD of the launch bound
     static constexpr int S1 = S1_, S2 = S2_, S3 = S3_, T2 = T2_, T3 = T3_, K = K_, T2C = T2C_;
     static constexpr int NT = NT_, NW = NT_ / 64;
     static constexpr int UA = UA_;   // units (n, s3) per thread: phases A, E

@@ -778,7 +778,7 @@ bool rcpb_blocks(const RcpBwdDesc& d, RcpHost& m, const uint16_t* X, const uint1
 template <int I>
 using RcpBCfgOf = rcpb::Cfg<kRcpBwdCfgs[I].S1, kRcpBwdCfgs[I].S2, kRcpBwdCfgs[I].S3, kRcpBwdCfgs[I].T2,
                             kRcpBwdCfgs[I].T3, kRcpBwdCfgs[I].K, kRcpBwdCfgs[I].T2C, kRcpBwdCfgs[I].NT,
-                            kRcpBwdCfgs[I].UA, kRcpBwdCfgs[I].UB, kRcpBwdCfgs[I].UC>;
+                            kRcpBwdCfgs[I].UA, kRcpBwdCfgs[I].UB, kRcpBwdCfgs[I].UC, kRcpBwdCfgs[I].MW>;
 
 template <class C>
 bool rcpb_is(const RcpBwdDesc& d) {
