@@ -21,6 +21,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+# kernels whose arithmetic runs on the vector ALU (no MFMA tile fits their
+# contractions): peak = 256 CUs x 64 lanes x 2.4 GHz x flops per lane-op,
+# 4 for v_dot2_f32_bf16 (two products) and 2 for an fp32 FMA
+ALU_BOUND = {"rcp_fwd": 157.3, "rcp_bwd": 157.3, "cred": 78.6, "credw": 78.6}
 
 
 def parse_args():
@@ -90,7 +94,10 @@ def roofline(records, dtype, share):
     ai = flops / max(nbytes, 1.0)
     ridge = PEAK_MFMA_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
     avg_s = ms / n / 1e3
-    if ai < ridge:
+    alu = [v for k, v in ALU_BOUND.items() if kname.startswith(k)]
+    if alu:
+        achieved, peak, unit, bound = flops / n / avg_s / 1e12, alu[0], "TFLOP/s", "alu"
+    elif ai < ridge:
         achieved, peak, unit, bound = nbytes / n / avg_s / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
     else:
         achieved, peak, unit, bound = flops / n / avg_s / 1e12, PEAK_MFMA_TFLOPS[dtype], "TFLOP/s", "mfma"

@@ -262,8 +262,8 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         m.need = 0x1f;
         m.what = "fused RCP chain backward: steps 3-0 (recompute, g1 and g2 of every step)";
         m.kname = "rcp_bwd<ce::rcpb::Cfg<";
-        const int tp[11] = {g.S1, g.S2, g.S3, g.T2, g.T3, g.K, g.T2C, g.NT, g.UA, g.UB, g.UC};
-        for (int i = 0; i < 11; i++) m.kname += std::to_string(tp[i]) + (i < 10 ? ", " : "> >");
+        const int tp[12] = {g.S1, g.S2, g.S3, g.T2, g.T3, g.K, g.T2C, g.NT, g.UA, g.UB, g.UC, g.MW};
+        for (int i = 0; i < 12; i++) m.kname += std::to_string(tp[i]) + (i < 11 ? ", " : "> >");
         // algorithmic bytes: X and dY read, dX partials and factor partials written
         const double act = (double)B * HW;
         m.alg_bytes = 2.0 * act * (double)(S + T1 * T2 * T3) + 4.0 * (double)nslot * act * S +
