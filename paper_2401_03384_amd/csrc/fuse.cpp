@@ -107,9 +107,10 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     d.kw_sj = w.f_sj;
     d.colstride = 32 - (w.K - 1);
     d.ncb = (int32_t)((W + d.colstride - 1) / d.colstride);
-    // wavefronts: about two (fp32) or four (bf16) per SIMD of the 1024 SIMDs;
-    // each strip segment recomputes KH-1 rows of Z1
-    int64_t want = dt ? 4096 : 2048;
+    // wavefronts: about two per SIMD of the 1024 SIMDs; each strip segment
+    // recomputes KH-1 rows of Z1 (bf16 forward, C2: 4096 waves with 4-row
+    // segments 40 us, 2048 with 7-row segments 35 us; fp32 unchanged)
+    const int64_t want = 2048;
     int64_t segs = std::max<int64_t>(1, std::min<int64_t>(H, want / std::max<int64_t>(1, B * d.ncb)));
     d.seg_rows = (int32_t)((H + segs - 1) / segs);
     d.segs = (int32_t)((H + d.seg_rows - 1) / d.seg_rows);

@@ -397,6 +397,73 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
 // block takes 64 consecutive outputs (one per lane) of one g; its four
 // wavefronts sum contiguous quarters of the chunks with eight loads in flight,
 // then the quarters are added in a fixed order.
+__device__ __forceinline__ int64_t tc_out_offset(const TcDesc& d, int64_t g, int64_t m, int64_t n) {
+    if (d.off32) {
+        // every index and offset fits 31 bits: 32-bit divisions (64-bit ones
+        // are long software sequences)
+        uint32_t off = 0, x = (uint32_t)g;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            const uint32_t sz = (uint32_t)d.g_size[i];
+            off += (x % sz) * (uint32_t)d.g_sC[i];
+            x /= sz;
+        }
+        x = (uint32_t)m;
+        for (int i = d.nm - 1; i >= 0; --i) {
+            const uint32_t sz = (uint32_t)d.m_size[i];
+            off += (x % sz) * (uint32_t)d.m_sC[i];
+            x /= sz;
+        }
+        x = (uint32_t)n;
+        for (int i = d.nn - 1; i >= 0; --i) {
+            const uint32_t sz = (uint32_t)d.n_size[i];
+            off += (x % sz) * (uint32_t)d.n_sC[i];
+            x /= sz;
+        }
+        return off;
+    }
+    int64_t off = 0, x = g;
+    for (int i = d.ng - 1; i >= 0; --i) {
+        off += (x % d.g_size[i]) * d.g_sC[i];
+        x /= d.g_size[i];
+    }
+    x = m;
+    for (int i = d.nm - 1; i >= 0; --i) {
+        off += (x % d.m_size[i]) * d.m_sC[i];
+        x /= d.m_size[i];
+    }
+    x = n;
+    for (int i = d.nn - 1; i >= 0; --i) {
+        off += (x % d.n_size[i]) * d.n_sC[i];
+        x /= d.n_size[i];
+    }
+    return off;
+}
+
+// Few chunks (ksplit <= 8): one output a thread, its partials summed in
+// chunk order (in double); 256 outputs of one g a block.
+template <typename TC>
+__global__ void __launch_bounds__(256) tc_reduce_few(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
+    const int64_t MN = d.M * d.N, per_g = (MN + 255) / 256;
+    const int64_t g = blockIdx.x / per_g, mn = (blockIdx.x - g * per_g) * 256 + threadIdx.x;
+    if (g >= d.G || mn >= MN) return;
+    const float* p = P + g * d.ksplit * MN + mn;
+    float v[8];
+#pragma unroll
+    for (int c = 0; c < 8; c++) v[c] = c < d.ksplit ? p[c * MN] : 0.f;
+    double acc = 0.0;
+#pragma unroll
+    for (int c = 0; c < 8; c++) acc += v[c];
+    int64_t m, n;
+    if (d.off32) {
+        m = (uint32_t)mn / (uint32_t)d.N;
+        n = (uint32_t)mn - (uint32_t)m * (uint32_t)d.N;
+    } else {
+        m = mn / d.N;
+        n = mn - m * d.N;
+    }
+    store(C, tc_out_offset(d, g, m, n), (float)acc);
+}
+
 template <typename TC>
 __global__ void __launch_bounds__(256) tc_reduce(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
     __shared__ double q4[4][64];
@@ -423,22 +490,7 @@ __global__ void __launch_bounds__(256) tc_reduce(TcDesc d, const float* __restri
     if (wave != 0 || g >= d.G || mn >= MN) return;
     const double sum = (q4[0][lane] + q4[1][lane]) + (q4[2][lane] + q4[3][lane]);
     const int64_t m = mn / d.N, n = mn - m * d.N;
-    int64_t off = 0, x = g;
-    for (int i = d.ng - 1; i >= 0; --i) {
-        off += (x % d.g_size[i]) * d.g_sC[i];
-        x /= d.g_size[i];
-    }
-    x = m;
-    for (int i = d.nm - 1; i >= 0; --i) {
-        off += (x % d.m_size[i]) * d.m_sC[i];
-        x /= d.m_size[i];
-    }
-    x = n;
-    for (int i = d.nn - 1; i >= 0; --i) {
-        off += (x % d.n_size[i]) * d.n_sC[i];
-        x /= d.n_size[i];
-    }
-    store(C, off, (float)sum);
+    store(C, tc_out_offset(d, g, m, n), (float)sum);
 }
 
 template <typename T, typename TC>
@@ -482,8 +534,15 @@ hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, vo
     const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
     if ((ln.kind & 0xff) == K_TC_REDUCE) {
         dim3 g(ln.grid[0]), bl(256);
-        if (tC) hipLaunchKernelGGL((tc_reduce<bf16_t>), g, bl, 0, s, t, (const float*)d, (bf16_t*)c);
-        else hipLaunchKernelGGL((tc_reduce<float>), g, bl, 0, s, t, (const float*)d, (float*)c);
+        const int64_t per = t.ksplit <= 8 ? 256 : 64;   // outputs of one g a block
+        if ((int64_t)ln.grid[0] != t.G * ((t.M * t.N + per - 1) / per)) return hipErrorInvalidValue;
+        if (t.ksplit <= 8) {
+            if (tC) hipLaunchKernelGGL((tc_reduce_few<bf16_t>), g, bl, 0, s, t, (const float*)d, (bf16_t*)c);
+            else hipLaunchKernelGGL((tc_reduce_few<float>), g, bl, 0, s, t, (const float*)d, (float*)c);
+        } else {
+            if (tC) hipLaunchKernelGGL((tc_reduce<bf16_t>), g, bl, 0, s, t, (const float*)d, (bf16_t*)c);
+            else hipLaunchKernelGGL((tc_reduce<float>), g, bl, 0, s, t, (const float*)d, (float*)c);
+        }
         return hipGetLastError();
     }
     if (tIn) return tC ? tc_launch_t<bf16_t, bf16_t>(t, ln, a, b, c, d, s) : tc_launch_t<bf16_t, float>(t, ln, a, b, c, d, s);

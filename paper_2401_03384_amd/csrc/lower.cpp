@@ -993,10 +993,11 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     lr.kind = K_TC_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
     lr.d = part;
     lr.c = C.buf;
-    lr.grid[0] = (uint32_t)(Gt * cdiv(Mt * Nt, 64));   // 64 outputs of one g a block
+    // outputs of one g a block: 256 (one a thread) for at most 8 chunks, else 64
+    lr.grid[0] = (uint32_t)(Gt * cdiv(Mt * Nt, d.ksplit <= 8 ? 256 : 64));
     lr.block[0] = 256;
     set_desc(lr, d);
-    lr.kname = std::string("tc_reduce<") + tname(C.dtype) + ">";
+    lr.kname = std::string(d.ksplit <= 8 ? "tc_reduce_few<" : "tc_reduce<") + tname(C.dtype) + ">";
     out.push_back(lr);
     return true;
 }

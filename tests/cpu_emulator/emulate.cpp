@@ -1103,7 +1103,8 @@ bool run_tc_reduce(const Launch& ln, Ctx& c) {
     bool o1, o2;
     Buf P = resolve(ln.d, c, 0, o1), C = resolve(ln.c, c, 0, o2);
     REQ(o1 && o2, "unresolved buffer");
-    REQ((int64_t)ln.grid[0] == d.G * ((d.M * d.N + 63) / 64) && ln.block[0] == 256, "grid");   // 64 outputs of one g a block
+    const int64_t per = d.ksplit <= 8 ? 256 : 64;   // outputs of one g a block
+    REQ((int64_t)ln.grid[0] == d.G * ((d.M * d.N + per - 1) / per) && ln.block[0] == 256, "grid");
     bool ok = true;
     for (int64_t g = 0; g < d.G; g++)
         for (int64_t m = 0; m < d.M; m++)

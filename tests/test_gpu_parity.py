@@ -131,7 +131,9 @@ def test_parity_full_size(P, name):
     xs = [_dev(a, bf16) for a in ins]
     y = plan.forward(xs)
     torch.cuda.synchronize()
-    assert _rel(_host(y), O.eval_dense(e, ins)) <= tol
+    err = _rel(_host(y), O.eval_dense(e, ins))
+    _say(f"  Y rel-L2 {err:.3e}")
+    assert err <= tol
     del y
     if not w.backward:
         return
