@@ -322,7 +322,7 @@ def main():
         lt["time_ratio_vs_optimal"] = round(lt["ms_per_step"] / (t_step * 1e3), 3)
         line["left_to_right"] = lt
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_batch)
+        line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_batch, w.shapes[0][0]))
     print(json.dumps(line), flush=True)
 
 
