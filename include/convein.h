@@ -107,6 +107,18 @@ ce_status ce_expr_parse(const char* spec, int n_in, const int* ranks,
  * sizes are equal (default 0).  Must be called before ce_plan_create. */
 ce_status ce_expr_set_feature(ce_expr* e, int operand);
 
+/* Boundary handling of a convolved label (Appendix A: "same" size output;
+ * the zero-padded reading is used throughout, see ce_expr_set_conv). */
+typedef enum { CE_PAD_SAME_ZERO = 0 } ce_pad;
+
+/* Set the padding of convolved label `label` (its name in the string, e.g.
+ * "h" or "(h1)").  CE_PAD_SAME_ZERO (the default for every convolved label):
+ * output size = feature size, the filter centred with floor((K-1)/2) taps
+ * before, zero outside the feature.  Must be called before ce_plan_create.
+ * Errors: CE_ERR_ARG (NULL, unknown or not convolved label),
+ * CE_ERR_UNSUPPORTED (any other padding value). */
+ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad);
+
 /* Output rank and sizes (a convolved output label takes its feature size).
  *   rank   receives the output rank
  *   dims   if non-NULL, receives [rank] sizes */
@@ -119,6 +131,14 @@ void ce_expr_destroy(ce_expr* e);
 /* Plan flags. */
 #define CE_FLAG_GENERIC_ONLY 0x1u  /* run every step on the generic strided kernel */
 #define CE_FLAG_NO_FUSION 0x2u     /* one launch per pairwise step (no fused chains) */
+/* Keep every forward intermediate in the workspace for the backward instead of
+ * recomputing it (Section 3.3 trades memory for recomputation): ce_backward
+ * then skips the recompute launches and must receive the workspace the
+ * preceding ce_forward of the same inputs used, unchanged, and of at least
+ * ce_plan_workspace_size(p, 1) bytes (which covers the forward's).  A fused
+ * chain keeps its intermediates on chip and recomputes them there, so for
+ * such a plan the flag changes nothing. */
+#define CE_FLAG_SAVE_INTERMEDIATES 0x4u
 
 /* Choose the pairwise evaluation order with the fewest multiplications under
  * `mode` (Section 3.2, optimal sequencer; Appendix B tnn-cost), searching
@@ -179,7 +199,8 @@ ce_status ce_forward(const ce_plan* p, const void* const* in, void* out,
 /* Backward pass: gradients of L = <Y, dout> with respect to the operands
  * (Appendix B: g1 and g2 of every step, in reverse order).  Intermediates are
  * recomputed from the inputs (gradient checkpointing, Section 3.3), so no
- * forward call needs to precede it.
+ * forward call needs to precede it, unless the plan was created with
+ * CE_FLAG_SAVE_INTERMEDIATES (then the forward's workspace is read).
  *   in        [n_in] device pointers to the operands
  *   dout      device pointer to dL/dY (plan dtype, output layout)
  *   din       [n_in] device pointers receiving dL/d operand_i in the operand's

@@ -28,13 +28,16 @@ CE_COST_FWD = 0
 CE_COST_TRAIN_PAPER = 1
 CE_FLAG_GENERIC_ONLY = 0x1
 CE_FLAG_NO_FUSION = 0x2
+CE_FLAG_SAVE_INTERMEDIATES = 0x4
+CE_PAD_SAME_ZERO = 0
 
 _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR_UNSUPPORTED",
                  -4: "CE_ERR_ARG", -5: "CE_ERR_WORKSPACE", -6: "CE_ERR_OVERFLOW", -7: "CE_ERR_HIP"}
 
 # Every symbol the header declares (checked by the test-suite).
 EXPORTS = [
-    "ce_expr_parse", "ce_expr_set_feature", "ce_expr_output_shape", "ce_expr_destroy",
+    "ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
+    "ce_expr_destroy",
     "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps", "ce_plan_step",
     "ce_plan_cost", "ce_plan_left_to_right_cost", "ce_plan_workspace_size", "ce_plan_describe",
     "ce_plan_destroy", "ce_forward", "ce_backward", "ce_timing_begin", "ce_timing_begin_kernel",
@@ -62,6 +65,7 @@ def lib():
         L.ce_expr_parse.argtypes = [C.c_char_p, C.c_int, C.POINTER(C.c_int), C.POINTER(i64p),
                                     C.POINTER(vp)]
         L.ce_expr_set_feature.argtypes = [vp, C.c_int]
+        L.ce_expr_set_conv.argtypes = [vp, C.c_char_p, C.c_int]
         L.ce_expr_output_shape.argtypes = [vp, C.POINTER(C.c_int), i64p]
         L.ce_expr_destroy.argtypes = [vp]
         L.ce_expr_destroy.restype = None
@@ -88,7 +92,7 @@ def lib():
                                        C.POINTER(C.c_double)]
         L.ce_last_error.restype = C.c_char_p
         L.ce_version.restype = C.c_char_p
-        for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_output_shape",
+        for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
                      "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps",
                      "ce_plan_step", "ce_plan_cost", "ce_plan_left_to_right_cost",
                      "ce_plan_workspace_size", "ce_forward", "ce_backward", "ce_timing_begin",
@@ -136,6 +140,10 @@ def ce_expr_parse(spec: str, shapes) -> int:
 
 def ce_expr_set_feature(e: int, operand: int) -> None:
     _check(lib().ce_expr_set_feature(e, operand))
+
+
+def ce_expr_set_conv(e: int, label: str, pad: int = CE_PAD_SAME_ZERO) -> None:
+    _check(lib().ce_expr_set_conv(e, label.encode(), pad))
 
 
 def ce_expr_output_shape(e: int) -> tuple:

@@ -39,6 +39,22 @@ ce_status ce_expr_set_feature(ce_expr* e, int operand) {
     });
 }
 
+ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad) {
+    return guard([&] {
+        if (!e || !label) fail(CE_ERR_ARG, "NULL argument");
+        int id = -1;
+        for (int l = 0; l < e->num_labels(); l++) {
+            const std::string& nm = e->names[l];
+            if (nm == label || (nm.size() > 2 && nm.front() == '(' && nm.back() == ')' &&
+                                nm.compare(1, nm.size() - 2, label) == 0))
+                id = l;
+        }
+        if (id < 0) fail(CE_ERR_ARG, std::string("unknown label ") + label);
+        if (!e->is_conv(id)) fail(CE_ERR_ARG, std::string("label ") + label + " is not convolved");
+        if (pad != CE_PAD_SAME_ZERO) fail(CE_ERR_UNSUPPORTED, "only zero 'same' padding is implemented");
+    });
+}
+
 ce_status ce_expr_output_shape(const ce_expr* e, int* rank, int64_t* dims) {
     return guard([&] {
         if (!e || !rank) fail(CE_ERR_ARG, "NULL argument");

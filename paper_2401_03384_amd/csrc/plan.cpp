@@ -600,7 +600,8 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             WsItem it;
             it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * elem(dt);
             it.t0 = s;
-            it.t1 = consumer_step(c);
+            // saved for the backward: live to the end (never shared)
+            it.t1 = (flags & CE_FLAG_SAVE_INTERMEDIATES) ? (1 << 30) : consumer_step(c);
             it.id = c;
             items.push_back(it);
         }
@@ -726,7 +727,16 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.what = "unary bwd";
             for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
-        for (int s = 0; !fused_bwd && s + 1 < m; s++) {
+        // intermediates the forward left in the workspace (plans that keep
+        // any: a fused chain keeps none)
+        const bool saved = (flags & CE_FLAG_SAVE_INTERMEDIATES) && !fused_bwd && !items.empty();
+        if (saved) {
+            std::vector<WsItem> kept;
+            for (const WsItem& it : bitems)
+                if (it.id >= GRAD_ID) kept.push_back(it);
+            bitems.swap(kept);
+        }
+        for (int s = 0; !fused_bwd && !saved && s + 1 < m; s++) {
             const Step& st = p->steps[s];
             PairOp op;
             op.L = bval(st.a);
@@ -769,6 +779,14 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
         }
         drop_unused(bitems, p->bwd);
         p->ws_bwd = pack(bitems);
+        if (saved) {
+            // the backward's own items after the forward's region; the saved
+            // intermediates at their forward offsets
+            for (WsItem& it : bitems) it.offset += p->ws_fwd;
+            p->ws_bwd += p->ws_fwd;
+            for (const WsItem& it : items)
+                if (it.id < GRAD_ID) bitems.push_back(it);
+        }
         patch(p->bwd, bitems);
     }
     return p.release();

@@ -141,6 +141,11 @@ class _ConvEinsumFn(torch.autograd.Function):
         p = plan(spec, [t.shape for t in tensors], dtype, flags=flags)
         ctx.plan = p
         ctx.save_for_backward(*tensors)
+        ctx.ws = None
+        if flags & B.CE_FLAG_SAVE_INTERMEDIATES:
+            # the backward reads the intermediates this forward leaves in its workspace
+            ctx.ws = p.workspace(True, tensors[0].device)
+            return p.forward(list(tensors), workspace=ctx.ws)
         return p.forward(list(tensors))
 
     @staticmethod
@@ -148,7 +153,8 @@ class _ConvEinsumFn(torch.autograd.Function):
         tensors = ctx.saved_tensors
         p = ctx.plan
         needs = list(ctx.needs_input_grad[2:])
-        grads = p.backward(list(tensors), dy.contiguous().to(p.torch_dtype), needs=needs)
+        grads = p.backward(list(tensors), dy.contiguous().to(p.torch_dtype), needs=needs,
+                           workspace=ctx.ws)
         grads = [g.to(t.dtype) if g is not None else None for g, t in zip(grads, tensors)]
         return (None, None, *grads)
 

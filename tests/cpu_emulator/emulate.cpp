@@ -1303,17 +1303,18 @@ bool run_thinw(const Launch& ln, Ctx& c) {
 
 extern "C" {
 
-// Runs the forward (mode 0) or backward (mode 1) launch list of a
-// generic-only plan.  Buffers are host memory in the plan's storage types.
+// Runs the forward (mode 0), backward (mode 1) or forward then backward on
+// one workspace (mode 2) launch lists of a plan built with `flags`
+// (CE_FLAG_*).  Buffers are host memory in the plan's storage types.
 // Returns 0 on success, else writes a message to err.
 int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* dims, int bf16,
              int mode, void* const* ins, void* out, const void* dout, void* const* din,
-             char* err, int errlen, int generic_only) {
+             char* err, int errlen, int flags) {
+    const int generic_only = flags & CE_FLAG_GENERIC_ONLY;
     try {
         std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
-        std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32,
-                                             generic_only ? CE_FLAG_GENERIC_ONLY : 0, false,
-                                             nullptr, 0));
+        std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32, (unsigned)flags,
+                                             false, nullptr, 0));
         if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
         Ctx c;
         int es = bf16 ? 2 : 4;
@@ -1328,11 +1329,16 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
         for (auto d : e->out_dims()) onum *= d;
         c.out = {(unsigned char*)out, (size_t)onum * es};
         c.dout = {(unsigned char*)const_cast<void*>(dout), (size_t)onum * es};
-        size_t wsb = mode ? p->ws_bwd : p->ws_fwd;
+        size_t wsb = mode == 2 ? std::max(p->ws_fwd, p->ws_bwd) : mode ? p->ws_bwd : p->ws_fwd;
         std::vector<unsigned char> ws(wsb + 1, 0xCD);   // poisoned: unset reads show up
         c.ws = {ws.data(), wsb};
-        const auto& list = mode ? p->bwd : p->fwd;
-        for (const Launch& ln : list) {
+        std::vector<const Launch*> list;
+        if (mode != 1)
+            for (const Launch& ln : p->fwd) list.push_back(&ln);
+        if (mode != 0)
+            for (const Launch& ln : p->bwd) list.push_back(&ln);
+        for (const Launch* lp : list) {
+            const Launch& ln = *lp;
             int v = ln.kind & 0xff;
             bool generic = v == K_GENERIC_THREAD || v == K_GENERIC_WAVE || v == K_GENERIC_BLOCK;
             if (generic_only && !generic) {

@@ -293,3 +293,41 @@ def test_feature_operand_designation():
         assert B.ce_plan_cost(p)[0] == O.tree_cost(oe, (0, 1), "train_paper")
         B.ce_plan_destroy(p)
         B.ce_expr_destroy(e)
+
+
+def test_saved_intermediates_plan():
+    """CE_FLAG_SAVE_INTERMEDIATES: no recompute launches in an unfused
+    backward, the backward workspace covers the forward's; fused chains are
+    unchanged."""
+    w = W.WORKLOADS["C4"]
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    p0 = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, 0)
+    p1 = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, B.CE_FLAG_SAVE_INTERMEDIATES)
+    B.ce_expr_destroy(e)
+    assert "recompute" in B.ce_plan_describe(p0)
+    assert "recompute" not in B.ce_plan_describe(p1)
+    assert B.ce_plan_workspace_size(p1, 1) >= B.ce_plan_workspace_size(p1, 0) > 0
+    B.ce_plan_destroy(p0)
+    B.ce_plan_destroy(p1)
+    w = W.WORKLOADS["C2"]
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    p2 = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, B.CE_FLAG_SAVE_INTERMEDIATES)
+    B.ce_expr_destroy(e)
+    assert "fused CP chain backward" in B.ce_plan_describe(p2)
+    assert B.ce_plan_workspace_size(p2, 0) == 0
+    B.ce_plan_destroy(p2)
+
+
+def test_set_conv():
+    """Padding of a convolved label: zero 'same' accepted, anything else
+    unsupported; unknown or non-convolved labels are argument errors."""
+    e = B.ce_expr_parse("bshw,sthw->bthw|hw", [(1, 2, 5, 5), (2, 3, 3, 3)])
+    try:
+        B.ce_expr_set_conv(e, "h", B.CE_PAD_SAME_ZERO)
+        for label, pad, status in (("w", 1, B.CE_ERR_UNSUPPORTED), ("s", 0, B.CE_ERR_ARG),
+                                   ("z", 0, B.CE_ERR_ARG)):
+            with pytest.raises(B.CeError) as ex:
+                B.ce_expr_set_conv(e, label, pad)
+            assert ex.value.status == status
+    finally:
+        B.ce_expr_destroy(e)

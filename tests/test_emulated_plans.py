@@ -153,3 +153,42 @@ def test_emulated_plan_edge_cases(emul, spec, shapes, generic):
     g = _run(emul, spec, shapes, False, 1, ins, dy=dy, generic=generic)
     for a, b in zip(g, g_ref):
         assert _rel(a, b) <= 1e-6
+
+
+def _run_saved(L, spec, shapes, bf16, ins, dy, out_shape, flags):
+    """Forward then backward on one workspace (mode 2)."""
+    n = len(shapes)
+    ranks = (C.c_int * n)(*[len(s) for s in shapes])
+    bufs = [(C.c_int64 * len(s))(*s) for s in shapes]
+    dims = (C.POINTER(C.c_int64) * n)(*[C.cast(b, C.POINTER(C.c_int64)) for b in bufs])
+    st = [_to_storage(a, bf16) for a in ins]
+    inp = (C.c_void_p * n)(*[a.ctypes.data for a in st])
+    err = C.create_string_buffer(512)
+    out = np.zeros(out_shape, dtype=np.uint16 if bf16 else np.float32)
+    d = _to_storage(dy, bf16)
+    grads = [np.zeros(s, dtype=(np.uint16 if (bf16 and i == 0) else np.float32)) for i, s in enumerate(shapes)]
+    din = (C.c_void_p * n)(*[g.ctypes.data for g in grads])
+    rc = L.emul_run(spec.encode(), n, ranks, dims, int(bf16), 2, inp, out.ctypes.data_as(C.c_void_p),
+                    d.ctypes.data_as(C.c_void_p), din, err, 512, flags)
+    assert rc == 0, err.value.decode()
+    return _from_storage(out, bf16), [_from_storage(g, bf16 and i == 0) for i, g in enumerate(grads)]
+
+
+SAVE = 0x4   # CE_FLAG_SAVE_INTERMEDIATES
+
+
+@pytest.mark.parametrize("flags", [SAVE, SAVE | 0x1], ids=["fast", "generic"])
+@pytest.mark.parametrize("name", ["C2s", "C3t", "C4t", "C5at_f32", "C5bt"])
+def test_saved_intermediates(emul, name, flags):
+    """With the forward's intermediates kept in the workspace the backward
+    skips the recompute launches and still matches the oracle."""
+    w = CASES[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    y, g = _run_saved(emul, w.spec, w.shapes, bf16, ins, dy, w.out_shape, flags)
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= tol

@@ -144,3 +144,26 @@ def test_parity_full_size(P, name):
         err = _rel(_host(g), r)
         _say(f"  grad {i} rel-L2 {err:.3e}")
         assert err <= tol, (name, i, err)
+
+
+@pytest.mark.parametrize("name", ["C2s", "C3s", "C4s", "C5as_f32", "C5bs"])
+def test_saved_intermediates(P, name):
+    """CE_FLAG_SAVE_INTERMEDIATES: the backward reads the intermediates the
+    forward left in the shared workspace (no recompute) and matches the oracle."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} saved intermediates shapes={w.shapes}")
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    plan = P.Plan(w.spec, w.shapes, w.dtype, flags=P.CE_FLAG_SAVE_INTERMEDIATES)
+    xs = [_dev(a, bf16) for a in ins]
+    ws = plan.workspace(True, xs[0].device)
+    y = plan.forward(xs, workspace=ws)
+    grads = plan.backward(xs, _dev(dy, bf16), workspace=ws)
+    torch.cuda.synchronize()
+    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
+    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
+        err = _rel(_host(g), r)
+        assert err <= tol, (name, i, err)
