@@ -24,3 +24,29 @@ def load_layer_strings():
             name, spec, cite = [x.strip() for x in line.split(" | ")]
             out[name] = (spec, cite)
     return out
+
+
+# Small operand shapes for every executable layer string the paper prints
+# (tests/golden/layer_strings.txt): convolved labels 9 (or 10, 11) on the
+# feature side and 3 on the filter side, other labels 2 to 6.
+PAPER_SHAPES = {
+    "standard_conv": [(2, 3, 9, 9), (4, 3, 3, 3)],
+    "cp_conv": [(2, 6, 9, 9), (3, 5), (3, 6), (3, 3), (3, 3)],
+    "rcp_conv": [(2, 2, 3, 2, 9, 9), (4, 2, 2), (4, 3, 3), (4, 2, 2), (4, 3, 3)],
+    "tucker_conv": [(2, 6, 9, 9), (3, 5), (2, 6), (3, 2, 3, 3)],
+    "rtk_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2), (3, 3, 3), (2, 2, 2), (2, 3, 3), (2, 2, 3, 2)],
+    "tt_conv": [(2, 6, 9, 9), (2, 5), (2, 3, 3), (3, 2, 3), (2, 6)],
+    "rtt_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2), (2, 3, 3, 3), (3, 2, 2, 2), (2, 3, 3)],
+    "tr_conv": [(2, 6, 9, 9), (2, 3, 5), (3, 2, 3), (2, 2, 3), (2, 2, 6)],
+    "rtr_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2, 2), (2, 3, 3, 3), (3, 2, 2, 2), (2, 2, 3, 3)],
+    "bt_conv": [(2, 2, 3, 2, 9, 9), (2, 2, 2, 2), (2, 2, 3, 3), (2, 2, 2, 2), (2, 2, 3, 3),
+                (2, 2, 2, 2, 2)],
+    "ht_conv": [(1, 2, 3, 2, 9, 9), (2, 2, 2), (2, 3, 3), (2, 2, 2), (2, 3, 3), (2, 2, 2),
+                (2, 2, 2), (2, 2)],
+    "separable_depthwise": [(2, 5, 9, 9), (5, 3), (5, 3)],
+    "interleaved_group": [(2, 2, 3, 9, 9), (4, 2, 3, 3), (5, 3, 3, 3)],
+    "sequencer_example": [(4, 7, 9), (10, 5), (5, 4, 2), (6, 8, 9, 2)],
+    "conv1d": [(2, 3, 11), (4, 3, 3)],
+    "group_conv1d": [(2, 3, 2, 3), (2, 2, 2, 10)],
+    "three_way_contraction": [(2, 3, 4), (3, 5, 3), (4, 4, 5)],
+}

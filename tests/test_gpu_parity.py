@@ -11,6 +11,9 @@ import pytest
 
 import oracle as O
 import workloads as W
+from conftest import PAPER_SHAPES, load_layer_strings
+
+STRINGS = load_layer_strings()
 
 pytestmark = pytest.mark.gpu
 
@@ -162,6 +165,42 @@ def test_saved_intermediates(P, name):
     ws = plan.workspace(True, xs[0].device)
     y = plan.forward(xs, workspace=ws)
     grads = plan.backward(xs, _dev(dy, bf16), workspace=ws)
+    torch.cuda.synchronize()
+    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
+    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
+        err = _rel(_host(g), r)
+        assert err <= tol, (name, i, err)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(PAPER_SHAPES))
+def test_paper_layer_strings(P, name, dtype):
+    """Every layer string the paper prints (CP, reshaped CP, Tucker, reshaped
+    Tucker, tensor-train and -ring, block-term, hierarchical Tucker, separable
+    and interleaved group convolutions, conv1d, grouped conv, contractions)
+    through the default plan, forward and all gradients, against the oracle."""
+    spec = STRINGS[name][0]
+    shapes = PAPER_SHAPES[name]
+    bf16 = dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} {dtype} {spec} shapes={shapes}")
+    e = O.bind(O.parse(spec), shapes)
+    plan = P.Plan(spec, shapes, dtype)
+    if "not executable" in plan.describe():
+        pytest.skip("a convolved label held by more than two operands (multi-way) is planned, not executed")
+    rng = np.random.default_rng(7)
+    ins = [rng.standard_normal(s) for s in shapes]
+    if bf16:
+        ins = [W.round_to_bf16(a.astype(np.float32)).astype(np.float64) for a in ins]
+    else:
+        ins = [a.astype(np.float32).astype(np.float64) for a in ins]
+    out_shape = tuple(plan.out_shape)
+    dy = rng.standard_normal(out_shape)
+    dy = (W.round_to_bf16(dy.astype(np.float32)) if bf16 else dy.astype(np.float32)).astype(np.float64)
+    tree = O.optimal_tree(e)[0]
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
     torch.cuda.synchronize()
     assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
     for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
