@@ -21,7 +21,7 @@ from __future__ import annotations
 
 import itertools
 
-from .cost import step_cost
+from .cost import kept_labels, label_size, step_cost
 
 
 def leaves(t):
@@ -65,8 +65,39 @@ def count_trees(n):
     return c
 
 
-def optimal_tree(expr, mode: str = "fwd", return_all: bool = False):
-    """Cheapest tree by exhaustive search, ties broken by the smallest key."""
+def intermediate_size(expr, subset) -> int:
+    """Elements of the tensor that merges the operands in `subset`: the
+    product of the sizes of its kept labels (a convolved label at its largest
+    size among the merged operands)."""
+    n = 1
+    for l in kept_labels(expr, subset):
+        n *= label_size(expr, subset, l)
+    return n
+
+
+def max_intermediate(expr, t) -> int:
+    """Largest intermediate of tree t (its internal nodes except the root,
+    which is the output); 0 for a single step or a leaf."""
+    sizes = []
+
+    def rec(x, root):
+        if isinstance(x, int):
+            return
+        if not root:
+            sizes.append(intermediate_size(expr, leaves(x)))
+        rec(x[0], False)
+        rec(x[1], False)
+
+    rec(t, True)
+    return max(sizes, default=0)
+
+
+def optimal_tree(expr, mode: str = "fwd", return_all: bool = False, max_elements=None):
+    """Cheapest tree by exhaustive search, ties broken by the smallest key.
+
+    With `max_elements`, only trees whose every intermediate holds at most
+    that many elements compete (the memory-limited order of Section 3.2,
+    Figure 2); (None, None) when no tree qualifies."""
     memo = {}
 
     def sc(a, b):
@@ -82,6 +113,8 @@ def optimal_tree(expr, mode: str = "fwd", return_all: bool = False):
 
     best, best_cost, ties = None, None, []
     for t in all_trees(range(expr.n)):
+        if max_elements is not None and max_intermediate(expr, t) > max_elements:
+            continue
         c = cost(t)
         if best_cost is None or c < best_cost:
             best, best_cost, ties = t, c, [t]

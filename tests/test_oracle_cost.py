@@ -212,3 +212,51 @@ def test_sequencer_example_figure1():
     assert c == min(O.tree_cost(e, x) for x in O.all_trees(range(4)))
     assert (t, c) == ((0, ((1, 2), 3)), 144820)
     assert O.tree_cost(e, O.left_to_right_tree(4)) == 327240
+
+
+def _chain_dp(p, cap):
+    """Textbook matrix-chain interval DP (Cormen et al., Sec. 15.2) with every
+    proper sub-chain product limited to `cap` elements (p[i] * p[j+1]);
+    returns the least multiplication count, None when no parenthesisation fits."""
+    n = len(p) - 1
+    INF = float("inf")
+    m = [[0 if i == j else INF for j in range(n)] for i in range(n)]
+    for length in range(2, n + 1):
+        for i in range(n - length + 1):
+            j = i + length - 1
+            if length < n and p[i] * p[j + 1] > cap:
+                continue
+            for k in range(i, j):
+                c = m[i][k] + m[k + 1][j] + p[i] * p[k + 1] * p[j + 1]
+                m[i][j] = min(m[i][j], c)
+    return None if m[0][n - 1] == INF else m[0][n - 1]
+
+
+@pytest.mark.parametrize("cap", [10 ** 9, 175, 174, 150, 125, 100, 90, 60])
+def test_memory_limited_matrix_chain(cap):
+    """The memory-limited search (Section 3.2, Figure 2) on the Cormen chain
+    against an independent interval DP: same least cost under the cap (or
+    both infeasible), and the returned tree respects the cap."""
+    dims = [30, 35, 15, 5, 10, 20, 25]
+    labs = "abcdefg"
+    spec = ",".join(labs[i] + labs[i + 1] for i in range(6)) + "->ag"
+    e = _e(spec, [(dims[i], dims[i + 1]) for i in range(6)])
+    t, c = O.optimal_tree(e, max_elements=cap)
+    ref = _chain_dp(dims, cap)
+    if ref is None:
+        assert t is None
+    else:
+        assert c == ref
+        assert O.max_intermediate(e, t) <= cap
+    if cap >= 175:   # the unconstrained optimum's largest intermediate is A2A3, 35 x 5
+        assert t == ((0, (1, 2)), ((3, 4), 5))
+
+
+def test_intermediate_size_matches_pairwise_evaluation():
+    """intermediate_size equals the element count of the tensor the pairwise
+    evaluator produces for that subset (a convolved label at its feature size)."""
+    e = _e("bshw,rs,rt,rh,rw->bthw|hw", [(2, 5, 9, 7), (4, 5), (4, 6), (4, 3), (4, 2)])
+    assert O.intermediate_size(e, (0, 1)) == 2 * 4 * 9 * 7      # Z1[b, r, h, w]
+    assert O.intermediate_size(e, (1, 2)) == 4 * 5 * 6          # Us x Ut outer over r
+    assert O.intermediate_size(e, (3, 4)) == 4 * 3 * 2          # Kh x Kw
+    assert O.max_intermediate(e, ((((0, 1), 3), 4), 2)) == 2 * 4 * 9 * 7
