@@ -41,6 +41,8 @@ def parse_args():
     ap.add_argument("--generic", action="store_true", help="generic kernel only")
     ap.add_argument("--path", choices=["optimal", "ltr"], default="optimal",
                     help="pairwise order: the planner's optimum or the left-to-right baseline")
+    ap.add_argument("--max-elements", type=int, default=None,
+                    help="cap on the elements of every intermediate (memory-limited order)")
     ap.add_argument("--compare-ltr", action="store_true",
                     help="also time the left-to-right order on the same kernels")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
@@ -228,7 +230,7 @@ def main():
     # left-to-right in the list format of ce_plan_create_with_path
     ltr = [(0, 1)] + [(0, n_in - 1 - k) for k in range(1, n_in - 1)]
     path = ltr if args.path == "ltr" else None
-    ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path)
+    ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=args.max_elements)
     ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
     out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
     grads = [torch.empty(s, dtype=ref.grad_dtype(i), device=dev) for i, s in enumerate(w.shapes)]
@@ -240,7 +242,9 @@ def main():
 
     def step(fwd=True, bwd=True):
         e = P.ce_expr_parse(w.spec, shapes)
-        if path is None:
+        if path is None and args.max_elements is not None:
+            p = P.ce_plan_create_limited(e, P.CE_COST_FWD, cdt, flags, args.max_elements)
+        elif path is None:
             p = P.ce_plan_create(e, P.CE_COST_FWD, cdt, flags)
         else:
             p = P.ce_plan_create_with_path(e, path, cdt, flags)
@@ -310,6 +314,7 @@ def main():
                    "global_batch": w.shapes[0][0], "fwd_macs": macs,
                    "flops_per_step": 6 * macs,
                    "path": ("left-to-right" if path else "optimal")
+                   + (f", intermediates <= {args.max_elements} elements" if args.max_elements else "")
                    + (", generic kernel" if args.generic else "")},
         "workspace_bytes": {"fwd": ref.ws_fwd, "bwd": ref.ws_bwd},
         "fwd_ms": round(t_fwd * 1e3, 4),

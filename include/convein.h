@@ -150,6 +150,16 @@ void ce_expr_destroy(ce_expr* e);
 ce_status ce_plan_create(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype,
                          unsigned flags, ce_plan** out);
 
+/* Same, with a memory limit (Section 3.2, Figure 2: the paper's sequencer can
+ * trade multiplications for intermediate size): the cheapest order among
+ * those whose every intermediate tensor (every merged operand set except the
+ * whole expression) holds at most max_elements elements, sizes counted as in
+ * the planned layouts (a convolved label at its largest size in the set).
+ * Ties are broken as in ce_plan_create.  Errors: as ce_plan_create, and
+ * CE_ERR_UNSUPPORTED when no order fits the limit. */
+ce_status ce_plan_create_limited(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype,
+                                 unsigned flags, uint64_t max_elements, ce_plan** out);
+
 /* Same, with a caller-given order (e.g. the left-to-right baseline of
  * Section 5): `pairs` holds n_pairs = n_in - 1 pairs (i, j) of positions in
  * the current operand list; the merged tensor is appended to the end of the

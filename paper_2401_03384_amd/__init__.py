@@ -7,7 +7,7 @@ planner and the HIP kernels in libconvein.so (C ABI: include/convein.h).
 from .binding import (CeError, ce_backward, ce_expr_destroy, ce_expr_output_shape,
                       ce_expr_parse, ce_expr_set_conv, ce_expr_set_feature, ce_forward,
                       ce_last_error,
-                      ce_plan_cost, ce_plan_create, ce_plan_create_with_path, ce_plan_describe,
+                      ce_plan_cost, ce_plan_create, ce_plan_create_limited, ce_plan_create_with_path, ce_plan_describe,
                       ce_plan_destroy, ce_plan_left_to_right_cost, ce_plan_num_steps,
                       ce_plan_step, ce_plan_workspace_size, ce_timing_begin, ce_timing_begin_kernel,
                       ce_timing_end,
@@ -19,7 +19,7 @@ from .layer import Plan, plan, conv_einsum, contract_path
 __all__ = [
     "CeError", "ce_backward", "ce_expr_destroy", "ce_expr_output_shape", "ce_expr_parse",
     "ce_expr_set_conv", "ce_expr_set_feature", "ce_forward", "ce_last_error", "ce_plan_cost", "ce_plan_create",
-    "ce_plan_create_with_path", "ce_plan_describe", "ce_plan_destroy",
+    "ce_plan_create_limited", "ce_plan_create_with_path", "ce_plan_describe", "ce_plan_destroy",
     "ce_plan_left_to_right_cost", "ce_plan_num_steps", "ce_plan_step", "ce_plan_workspace_size",
     "ce_timing_begin", "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record",
     "ce_version", "lib", "LIB_PATH", "Plan", "plan", "conv_einsum", "contract_path",

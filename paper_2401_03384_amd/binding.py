@@ -38,7 +38,8 @@ _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR
 EXPORTS = [
     "ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
     "ce_expr_destroy",
-    "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps", "ce_plan_step",
+    "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_with_path", "ce_plan_num_steps",
+    "ce_plan_step",
     "ce_plan_cost", "ce_plan_left_to_right_cost", "ce_plan_workspace_size", "ce_plan_describe",
     "ce_plan_destroy", "ce_forward", "ce_backward", "ce_timing_begin", "ce_timing_begin_kernel",
     "ce_timing_end", "ce_timing_record", "ce_last_error", "ce_version",
@@ -70,6 +71,7 @@ def lib():
         L.ce_expr_destroy.argtypes = [vp]
         L.ce_expr_destroy.restype = None
         L.ce_plan_create.argtypes = [vp, C.c_int, C.c_int, C.c_uint, C.POINTER(vp)]
+        L.ce_plan_create_limited.argtypes = [vp, C.c_int, C.c_int, C.c_uint, C.c_uint64, C.POINTER(vp)]
         L.ce_plan_create_with_path.argtypes = [vp, C.POINTER(C.c_int), C.c_int, C.c_int, C.c_uint,
                                                C.POINTER(vp)]
         L.ce_plan_num_steps.argtypes = [vp, C.POINTER(C.c_int)]
@@ -93,7 +95,8 @@ def lib():
         L.ce_last_error.restype = C.c_char_p
         L.ce_version.restype = C.c_char_p
         for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
-                     "ce_plan_create", "ce_plan_create_with_path", "ce_plan_num_steps",
+                     "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_with_path",
+                     "ce_plan_num_steps",
                      "ce_plan_step", "ce_plan_cost", "ce_plan_left_to_right_cost",
                      "ce_plan_workspace_size", "ce_forward", "ce_backward", "ce_timing_begin",
                      "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record"):
@@ -161,6 +164,12 @@ def ce_expr_destroy(e: int) -> None:
 def ce_plan_create(e: int, mode: int = CE_COST_FWD, dtype: int = CE_F32, flags: int = 0) -> int:
     out = C.c_void_p()
     _check(lib().ce_plan_create(e, mode, dtype, flags, C.byref(out)))
+    return out.value
+
+
+def ce_plan_create_limited(e: int, mode: int, dtype: int, flags: int, max_elements: int) -> int:
+    out = C.c_void_p()
+    _check(lib().ce_plan_create_limited(e, mode, dtype, flags, max_elements, C.byref(out)))
     return out.value
 
 

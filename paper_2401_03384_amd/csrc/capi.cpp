@@ -75,6 +75,14 @@ ce_status ce_plan_create(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype, un
     });
 }
 
+ce_status ce_plan_create_limited(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
+                                 uint64_t max_elements, ce_plan** out) {
+    return guard([&] {
+        if (!e || !out) fail(CE_ERR_ARG, "NULL argument");
+        *out = make_plan(*e, mode, dtype, flags, false, nullptr, 0, max_elements);
+    });
+}
+
 ce_status ce_plan_create_with_path(const ce_expr* e, const int* pairs, int n_pairs, ce_dtype dtype,
                                    unsigned flags, ce_plan** out) {
     return guard([&] {

@@ -94,6 +94,16 @@ uint64_t step_cost_sat(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mo
     return add_sat(f, add_sat(mul_sat(plain, conv_ga), mul_sat(plain, conv_gb)));
 }
 
+// Elements of the tensor merging the operands in S (kept labels; a
+// convolved label at its largest size in S), saturating.
+uint64_t set_numel(const ce_expr& e, uint32_t S) {
+    const uint64_t k = kept_mask(e, S);
+    uint64_t n = 1;
+    for (int l = 0; l < e.num_labels(); l++)
+        if ((k >> l) & 1) n = mul_sat(n, (uint64_t)size_in_set(e, S, l));
+    return n;
+}
+
 std::string mask_str(uint32_t m) {
     std::string s = "{";
     bool first = true;
@@ -128,19 +138,29 @@ struct Builder {
     Builder(const ce_expr& e_, ce_plan& p_) : e(e_), p(p_), n(e_.n) {}
 
     // ---- search ---------------------------------------------------------
-    std::vector<uint32_t> optimal_splits(uint64_t* best_cost) {
+    // Cheapest split of every operand set (subset DP).  With a limit, a set
+    // other than the whole expression whose merged tensor exceeds `limit`
+    // elements is infeasible, and so is every split that uses one; returns
+    // false when the whole expression has no feasible split.
+    bool optimal_splits(uint64_t* best_cost, std::vector<uint32_t>& split,
+                        uint64_t limit = ~uint64_t(0)) {
         uint32_t full = (n >= 32) ? 0xffffffffu : ((1u << n) - 1);
         std::vector<uint64_t> best(size_t(full) + 1, 0);
-        std::vector<uint32_t> split(size_t(full) + 1, 0);
+        std::vector<char> feasible(size_t(full) + 1, 1);
+        split.assign(size_t(full) + 1, 0);
         for (uint32_t S = 1; S <= full; S++) {
             if (popcount64(S) == 1) continue;
+            if (S != full && limit != ~uint64_t(0) && set_numel(e, S) > limit) {
+                feasible[S] = 0;
+                continue;
+            }
             uint32_t low = S & (~S + 1), rest = S ^ low;
             uint64_t bc = kSat;
             uint32_t bA = 0;
             bool found = false;
             for (uint32_t sub = rest;; sub = (sub - 1) & rest) {
                 uint32_t A = sub | low, B = S ^ A;
-                if (B) {
+                if (B && feasible[A] && feasible[B]) {
                     uint64_t c = add_sat(add_sat(best[A], best[B]), step_cost_sat(e, A, B, p.mode));
                     if (!found || c < bc || (c == bc && A < bA)) {
                         bc = c;
@@ -152,9 +172,10 @@ struct Builder {
             }
             best[S] = bc;
             split[S] = bA;
+            feasible[S] = found;
         }
         *best_cost = best[full];
-        return split;
+        return feasible[full] != 0;
     }
 
     int build_tree(uint32_t S, const std::vector<uint32_t>& split) {
@@ -502,7 +523,7 @@ uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) 
 }
 
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
-                   bool use_path, const int* pairs, int n_pairs) {
+                   bool use_path, const int* pairs, int n_pairs, uint64_t max_elements) {
     if (!e.bound) fail(CE_ERR_ARG, "expression is not bound");
     if (mode != CE_COST_FWD && mode != CE_COST_TRAIN_PAPER) fail(CE_ERR_ARG, "bad cost mode");
     if (dtype != CE_F32 && dtype != CE_BF16) fail(CE_ERR_ARG, "bad dtype");
@@ -521,7 +542,10 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             bld.tree_from_pairs(pairs, n_pairs);
         } else {
             uint64_t best;
-            auto split = bld.optimal_splits(&best);
+            std::vector<uint32_t> split;
+            if (!bld.optimal_splits(&best, split, max_elements))
+                fail(CE_ERR_UNSUPPORTED, "no pairwise order keeps every intermediate within " +
+                                             std::to_string(max_elements) + " elements");
             bld.build_tree((n >= 32) ? 0xffffffffu : ((1u << n) - 1), split);
         }
     }

@@ -104,7 +104,8 @@ namespace ce {
 // Build a plan: the optimal order when use_path is false, else the order
 // given by `pairs` (opt_einsum path format, n_pairs = n_in - 1).
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
-                   bool use_path, const int* pairs, int n_pairs);
+                   bool use_path, const int* pairs, int n_pairs,
+                   uint64_t max_elements = ~uint64_t(0));
 
 // Text description of a plan (steps, costs, workspace, launches).
 std::string describe_plan(const ce_plan& p);

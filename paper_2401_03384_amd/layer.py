@@ -20,10 +20,11 @@ class Plan:
     """A planned conv_einsum layer: string, operand shapes, dtype.
 
     `path` (optional) is an opt_einsum-style list of pairs replacing the
-    optimal order (e.g. the left-to-right baseline)."""
+    optimal order (e.g. the left-to-right baseline); `max_elements` (optional)
+    caps the elements of every intermediate (the cheapest order that fits)."""
 
     def __init__(self, spec: str, shapes, dtype: str = "f32", mode: str = "fwd", flags: int = 0,
-                 path=None, feature_operand: int = 0):
+                 path=None, feature_operand: int = 0, max_elements=None):
         if dtype not in _DT:
             raise ValueError(f"dtype must be one of {list(_DT)}")
         self.spec = spec
@@ -37,7 +38,10 @@ class Plan:
             if feature_operand:
                 B.ce_expr_set_feature(self._expr, feature_operand)
             self.out_shape = B.ce_expr_output_shape(self._expr)
-            if path is None:
+            if path is None and max_elements is not None:
+                self._plan = B.ce_plan_create_limited(self._expr, _MODE[mode], _DT[dtype], flags,
+                                                      int(max_elements))
+            elif path is None:
                 self._plan = B.ce_plan_create(self._expr, _MODE[mode], _DT[dtype], flags)
             else:
                 self._plan = B.ce_plan_create_with_path(self._expr, path, _DT[dtype], flags)
@@ -165,9 +169,9 @@ def conv_einsum(spec: str, *tensors, flags: int = 0):
     return _ConvEinsumFn.apply(spec, flags, *tensors)
 
 
-def contract_path(spec: str, *shapes, mode: str = "fwd"):
+def contract_path(spec: str, *shapes, mode: str = "fwd", max_elements=None):
     """Planned order without executing: ([(lhs_mask, rhs_mask, macs)], info)."""
-    p = Plan(spec, shapes, "f32", mode)
+    p = Plan(spec, shapes, "f32", mode, max_elements=max_elements)
     info = {"total_cost": p.total_cost, "fwd_macs": p.fwd_macs,
             "left_to_right_cost": p.left_to_right_cost(), "text": p.describe()}
     return p.steps, info

@@ -1303,6 +1303,11 @@ bool run_thinw(const Launch& ln, Ctx& c) {
 
 extern "C" {
 
+// Cap on every intermediate's elements for the plans emul_run builds
+// (0: none; the memory-limited order of ce_plan_create_limited).
+static uint64_t g_limit = 0;
+void emul_set_limit(uint64_t max_elements) { g_limit = max_elements; }
+
 // Runs the forward (mode 0), backward (mode 1) or forward then backward on
 // one workspace (mode 2) launch lists of a plan built with `flags`
 // (CE_FLAG_*).  Buffers are host memory in the plan's storage types.
@@ -1314,7 +1319,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
     try {
         std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
         std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32, (unsigned)flags,
-                                             false, nullptr, 0));
+                                             false, nullptr, 0, g_limit ? g_limit : ~uint64_t(0)));
         if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
         Ctx c;
         int es = bf16 ? 2 : 4;

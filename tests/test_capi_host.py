@@ -310,3 +310,52 @@ def test_set_conv():
             assert ex.value.status == status
     finally:
         B.ce_expr_destroy(e)
+
+
+def _compare_limited(spec, shapes, limits):
+    """ce_plan_create_limited == the oracle's memory-limited search (tree,
+    per-step MACs, cost), or both infeasible."""
+    e = O.bind(O.parse(spec), shapes)
+    for cap in limits:
+        tree, cost = O.optimal_tree(e, "fwd", max_elements=cap)
+        ex = B.ce_expr_parse(spec, shapes)
+        try:
+            if tree is None:
+                with pytest.raises(B.CeError) as err:
+                    B.ce_plan_create_limited(ex, B.CE_COST_FWD, B.CE_F32, 0, cap)
+                assert err.value.status == B.CE_ERR_UNSUPPORTED
+                continue
+            p = B.ce_plan_create_limited(ex, B.CE_COST_FWD, B.CE_F32, 0, cap)
+        finally:
+            B.ce_expr_destroy(ex)
+        try:
+            assert _steps(p) == _oracle_steps(e, tree), (spec, cap)
+            assert B.ce_plan_cost(p)[0] == cost
+        finally:
+            B.ce_plan_destroy(p)
+
+
+def _limits_for(e):
+    """Caps around the largest intermediates of the unconstrained optimum and
+    of the left-to-right tree (so both feasible and infeasible caps occur)."""
+    t, _ = O.optimal_tree(e)
+    m = O.max_intermediate(e, t)
+    l = O.max_intermediate(e, O.left_to_right_tree(e.n))
+    return sorted({max(m, 1), max(m - 1, 1), max(m // 2, 1), max(l, 1), max(l - 1, 1), 1})
+
+
+@pytest.mark.parametrize("name", sorted(set(W.WORKLOADS) | {"C2s", "C3s", "C4s", "C5as"}))
+def test_limited_planner_matches_oracle_on_workloads(name):
+    w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS[name]
+    _compare_limited(w.spec, w.shapes, _limits_for(O.bind(O.parse(w.spec), w.shapes)))
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_limited_planner_matches_oracle_on_random_expressions(seed):
+    rnd = random.Random(5000 + seed)
+    for _ in range(4):
+        spec, shapes, _ = _random_expr(rnd)
+        e = O.bind(O.parse(spec), shapes)
+        if e.n > 6 or any(len(e.holders(l)) > 2 for l in e.conv):
+            continue
+        _compare_limited(spec, shapes, _limits_for(e))

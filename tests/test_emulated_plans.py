@@ -219,3 +219,27 @@ def test_emulated_paper_strings(emul, name, bf16):
     g = _run(emul, spec, shapes, bf16, 1, ins, dy=dy, generic=0)
     for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
         assert _rel(a, b) <= tol
+
+
+@pytest.mark.parametrize("name", ["C4s", "C5as", "C5bs"])
+def test_emulated_memory_limited(emul, name):
+    """The memory-limited order (cap just below the optimum's largest
+    intermediate), every launch bounds-checked, against the oracle along the
+    oracle's limited tree."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    cap = O.max_intermediate(e, O.optimal_tree(e)[0]) - 1
+    tree, _ = O.optimal_tree(e, max_elements=cap)
+    assert tree is not None
+    emul.emul_set_limit(C.c_uint64(cap))
+    try:
+        y = _run(emul, w.spec, w.shapes, bf16, 0, ins, out_shape=w.out_shape, generic=0)
+        g = _run(emul, w.spec, w.shapes, bf16, 1, ins, dy=dy, generic=0)
+    finally:
+        emul.emul_set_limit(C.c_uint64(0))
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= tol

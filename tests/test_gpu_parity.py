@@ -206,3 +206,28 @@ def test_paper_layer_strings(P, name, dtype):
     for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
         err = _rel(_host(g), r)
         assert err <= tol, (name, i, err)
+
+
+@pytest.mark.parametrize("name", ["C4s", "C5as", "C5bs"])
+def test_memory_limited_plan(P, name):
+    """A cap just below the optimum's largest intermediate forces another
+    order (the paper's memory/compute trade-off); it runs through the same
+    kernels and matches the oracle along the oracle's limited tree."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    cap = O.max_intermediate(e, O.optimal_tree(e)[0]) - 1
+    tree, _ = O.optimal_tree(e, max_elements=cap)
+    assert tree is not None
+    _say(f"case {name} limited to {cap} elements, tree {tree}")
+    plan = P.Plan(w.spec, w.shapes, w.dtype, max_elements=cap)
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
+    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
+        err = _rel(_host(g), r)
+        assert err <= tol, (name, i, err)
