@@ -92,9 +92,10 @@ CASES = {
     "C5bt": W.rcp_layer("C5bt", 1, (2, 2, 4), (2, 2, 4), 9, 8, 16, 5, "bf16", 24),
     "C4m": W.rtt_layer("C4m", 1, (4, 4, 8), (4, 4, 8), 5, 7, 16, 3, "f32", 26),
     "C5cs": W.PARITY_WORKLOADS["C5cs"],
-    # fused reshaped-CP forward: both instantiations, one and several row tiles
-    "C5as": W.PARITY_WORKLOADS["C5as"],
-    "C5bs": W.PARITY_WORKLOADS["C5bs"],
+    # fused reshaped-CP kernels: both instantiations (rank 4 keeps the CPU
+    # run short), one and several row tiles
+    "C5ar": W.rcp_layer("C5ar", 2, (8, 8, 8), (8, 8, 8), 7, 7, 4, 3, "bf16", 29),
+    "C5br": W.rcp_layer("C5br", 1, (4, 4, 8), (4, 4, 8), 11, 11, 4, 5, "bf16", 30),
     "C5bt2": W.PARITY_WORKLOADS["C5bt2"],
     "C5bt3": W.PARITY_WORKLOADS["C5bt3"],
     "C5cs_f32": W.PARITY_WORKLOADS["C5cs_f32"],
@@ -180,7 +181,7 @@ SAVE = 0x4   # CE_FLAG_SAVE_INTERMEDIATES
 
 
 @pytest.mark.parametrize("flags", [SAVE, SAVE | 0x1], ids=["fast", "generic"])
-@pytest.mark.parametrize("name", ["C2s", "C3t", "C4t", "C5at_f32", "C5bt"])
+@pytest.mark.parametrize("name", ["C2s", "C3t", "C4t", "C5at_f32", "C5br"])
 def test_saved_intermediates(emul, name, flags):
     """With the forward's intermediates kept in the workspace the backward
     skips the recompute launches and still matches the oracle."""
@@ -221,12 +222,12 @@ def test_emulated_paper_strings(emul, name, bf16):
         assert _rel(a, b) <= tol
 
 
-@pytest.mark.parametrize("name", ["C4s", "C5as", "C5bs"])
+@pytest.mark.parametrize("name", ["C4t", "C5at"])
 def test_emulated_memory_limited(emul, name):
     """The memory-limited order (cap just below the optimum's largest
     intermediate), every launch bounds-checked, against the oracle along the
     oracle's limited tree."""
-    w = W.PARITY_WORKLOADS[name]
+    w = CASES[name]
     bf16 = w.dtype == "bf16"
     tol = 2e-2 if bf16 else 1e-5
     ins, dy = W.make_inputs(w)
