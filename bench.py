@@ -43,6 +43,8 @@ def parse_args():
                     help="pairwise order: the planner's optimum or the left-to-right baseline")
     ap.add_argument("--max-elements", type=int, default=None,
                     help="cap on the elements of every intermediate (memory-limited order)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time forward + backward replayed from a HIP graph (no host work)")
     ap.add_argument("--compare-ltr", action="store_true",
                     help="also time the left-to-right order on the same kernels")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
@@ -322,6 +324,18 @@ def main():
         "plan_ms": round(t_plan * 1e3, 4),
         "roofline": roofline(records, dtype, share),
     }
+    if args.graph:
+        g = P.GraphStep(ref, xs, d)
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        tg = (time.perf_counter() - t0) / args.steps
+        line["graph"] = {"ms_per_step": round(tg * 1e3, 4), "tflops": round(6 * macs / tg / 1e12, 3),
+                         "note": "forward + backward replayed from one HIP graph; no parse or plan"}
     if args.compare_ltr and path is None:
         lt = compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args)
         lt["time_ratio_vs_optimal"] = round(lt["ms_per_step"] / (t_step * 1e3), 3)

@@ -14,7 +14,7 @@ from .binding import (CeError, ce_backward, ce_expr_destroy, ce_expr_output_shap
                       ce_timing_record, ce_version, lib, LIB_PATH,
                       CE_F32, CE_BF16, CE_COST_FWD, CE_COST_TRAIN_PAPER, CE_FLAG_GENERIC_ONLY,
                       CE_FLAG_NO_FUSION, CE_FLAG_SAVE_INTERMEDIATES, CE_PAD_SAME_ZERO)
-from .layer import Plan, plan, conv_einsum, contract_path
+from .layer import GraphStep, Plan, plan, conv_einsum, contract_path
 
 __all__ = [
     "CeError", "ce_backward", "ce_expr_destroy", "ce_expr_output_shape", "ce_expr_parse",
@@ -22,7 +22,7 @@ __all__ = [
     "ce_plan_create_limited", "ce_plan_create_with_path", "ce_plan_describe", "ce_plan_destroy",
     "ce_plan_left_to_right_cost", "ce_plan_num_steps", "ce_plan_step", "ce_plan_workspace_size",
     "ce_timing_begin", "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record",
-    "ce_version", "lib", "LIB_PATH", "Plan", "plan", "conv_einsum", "contract_path",
+    "ce_version", "lib", "LIB_PATH", "GraphStep", "Plan", "plan", "conv_einsum", "contract_path",
     "CE_F32", "CE_BF16", "CE_COST_FWD", "CE_COST_TRAIN_PAPER", "CE_FLAG_GENERIC_ONLY",
     "CE_FLAG_NO_FUSION", "CE_FLAG_SAVE_INTERMEDIATES", "CE_PAD_SAME_ZERO",
 ]

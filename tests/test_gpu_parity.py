@@ -231,3 +231,33 @@ def test_memory_limited_plan(P, name):
     for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
         err = _rel(_host(g), r)
         assert err <= tol, (name, i, err)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2s", "C3s", "C5as"])
+def test_graph_replay(P, name):
+    """Forward + backward captured as a HIP graph: three replays, with eager
+    work and synchronisations in between, each equal (bit for bit: the
+    kernels are deterministic) to the eager result."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    _say(f"case {name} graph replay")
+    ins, dy = W.make_inputs(w)
+    plan = P.Plan(w.spec, w.shapes, w.dtype)
+    xs = [_dev(a, bf16) for a in ins]
+    d = _dev(dy, bf16)
+    y_ref = plan.forward(xs)
+    g_ref = plan.backward(xs, d)
+    torch.cuda.synchronize()
+    step = P.GraphStep(plan, xs, d)
+    for k in range(3):
+        step.out.zero_()
+        for g in step.grads:
+            g.zero_()
+        step.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(step.out, y_ref), (name, k)
+        for i, (g, r) in enumerate(zip(step.grads, g_ref)):
+            assert torch.equal(g, r), (name, k, i)
+        # eager work between replays
+        plan.forward(xs)
+        torch.cuda.synchronize()
