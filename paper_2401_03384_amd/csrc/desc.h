@@ -101,6 +101,10 @@ struct ReduceDesc {
     int64_t sCm, sCn;
 };
 
+// Waves a block of the ordered partial sums (64 outputs a block), from the
+// number of partials alone, so that the summation order is fixed per shape.
+inline int reduce_waves(int64_t nsplit) { return nsplit <= 8 ? 1 : nsplit <= 64 ? 4 : 16; }
+
 // Up to four independent ordered sums (ReduceDesc each, fp32 outputs) in one
 // launch: part j owns blocks [block0[j], block0[j+1]); a part whose output
 // pointer is null (gradient not requested) is skipped.

@@ -268,12 +268,12 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
     lr.kind = K_REDUCE_MULTI;
     lr.extra = {Pus, din(us), Put, din(ut), Pkh, din(kh), Pkw, din(kw)};
     lr.grid[0] = (uint32_t)md.block0[4];
-    lr.block[0] = 256;
+    lr.block[0] = (uint32_t)(64 * reduce_waves(nb));
     lr.desc.resize(sizeof(md));
     std::memcpy(lr.desc.data(), &md, sizeof(md));
     lr.need = (1u << us.index) | (1u << ut.index) | (1u << kh.index) | (1u << kw.index);
     lr.what = "dUs, dUt, dKh, dKw: sums of block partials";
-    lr.kname = "reduce_multi";
+    lr.kname = "reduce_multi<" + std::to_string(reduce_waves(nb)) + ">";
     lr.alg_bytes = 4.0 * (double)nb * R * (d.S + d.T + d.KH + d.KW) + 4.0 * R * (d.S + d.T + d.KH + d.KW);
     out.push_back(lr);
     return true;

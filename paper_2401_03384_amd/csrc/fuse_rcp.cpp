@@ -289,12 +289,12 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         lr.kind = K_REDUCE_MULTI;
         lr.extra = {parts[0], outs[0], parts[1], outs[1], parts[2], outs[2], parts[3], outs[3]};
         lr.grid[0] = (uint32_t)md.block0[4];
-        lr.block[0] = 256;
+        lr.block[0] = (uint32_t)(64 * reduce_waves(nblk));
         lr.desc.resize(sizeof(md));
         std::memcpy(lr.desc.data(), &md, sizeof(md));
         lr.need = (1u << W1.index) | (1u << W2.index) | (1u << W3.index) | (1u << W0.index);
         lr.what = "dW1, dW2, dW3, dW0: sums of workgroup partials";
-        lr.kname = "reduce_multi";
+        lr.kname = "reduce_multi<" + std::to_string(reduce_waves(nblk)) + ">";
         lr.alg_bytes = 4.0 * (double)nblk * R * (n0 + n1 + n2 + n3) + 4.0 * R * (n0 + n1 + n2 + n3);
         out.push_back(lr);
         // dX: ordered sum of the per-(t1, t2 chunk) partials, rounded to bf16
@@ -310,12 +310,12 @@ bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch,
         lx.d = DXP;
         lx.c = din(X);
         lx.grid[0] = (uint32_t)((B * S * HW + 63) / 64);
-        lx.block[0] = 256;
+        lx.block[0] = (uint32_t)(64 * reduce_waves(nslot));
         lx.desc.resize(sizeof(rd));
         std::memcpy(lx.desc.data(), &rd, sizeof(rd));
         lx.need = 1u << X.index;
         lx.what = "dX: sum of the per-(t1, t2 chunk) partials";
-        lx.kname = "reduce_partials<unsigned short>";
+        lx.kname = "reduce_partials<" + std::to_string(reduce_waves(rd.nsplit)) + ", unsigned short>";
         lx.alg_bytes = 4.0 * (double)nslot * act * S + 2.0 * act * S;
         out.push_back(lx);
         return true;

@@ -314,43 +314,49 @@ __global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ 
     }
 }
 
-// C[e] = sum_s part[s][e]: a block takes 64 consecutive outputs (one per
-// lane); its 4 wavefronts sum contiguous quarters of s with 8 loads in
-// flight, then the quarters are added in a fixed order.
-template <typename TC>
+// C[e] = sum_s part[s][e]: 64 outputs a block; the NW waves of the block sum consecutive runs of the
+// partials (16 loads in flight a lane), then wave 0 adds the NW run sums in
+// wave order: a fixed order for a given NW, which the launcher derives from
+// nsplit alone (1 wave up to 8 partials, 4 up to 64, else 16).
+template <int NW, typename TC>
 __device__ __forceinline__ void reduce_block(const ReduceDesc& d, const float* __restrict__ part,
                                              TC* __restrict__ C, int64_t blk, double (*q)[64]) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = NW == 1 ? 0 : threadIdx.x >> 6;
     const int64_t mn = (int64_t)d.M * d.N;
     const int64_t e = blk * 64 + lane;
-    const int64_t per = (d.nsplit + 3) / 4;
+    const int64_t per = (d.nsplit + NW - 1) / NW;
     const int64_t s0 = wave * per, s1 = min(d.nsplit, s0 + per);
     double acc = 0.0;
     if (e < mn) {
         int64_t s = s0;
-        for (; s + 8 <= s1; s += 8) {
-            float v[8];
+        for (; s + 16 <= s1; s += 16) {
+            float v[16];
 #pragma unroll
-            for (int u = 0; u < 8; u++) v[u] = part[(s + u) * mn + e];
+            for (int u = 0; u < 16; u++) v[u] = part[(s + u) * mn + e];
 #pragma unroll
-            for (int u = 0; u < 8; u++) acc += v[u];
+            for (int u = 0; u < 16; u++) acc += v[u];
         }
         for (; s < s1; s++) acc += part[s * mn + e];
     }
-    q[wave][lane] = acc;
-    __syncthreads();
-    if (wave == 0 && e < mn) {
-        double t = (q[0][lane] + q[1][lane]) + (q[2][lane] + q[3][lane]);
+    if constexpr (NW > 1) {
+        q[wave][lane] = acc;
+        __syncthreads();
+        if (wave != 0) return;
+        acc = q[0][lane];
+#pragma unroll
+        for (int w = 1; w < NW; w++) acc += q[w][lane];
+    }
+    if (e < mn) {
         int64_t m = e / d.N, n = e - m * d.N;
-        store(C, m * d.sCm + n * d.sCn, (float)t);
+        store(C, m * d.sCm + n * d.sCn, (float)acc);
     }
 }
 
-template <typename TC>
-__global__ void __launch_bounds__(256) reduce_partials(ReduceDesc d, const float* __restrict__ part,
-                                                       TC* __restrict__ C) {
-    __shared__ double q[4][64];
-    reduce_block(d, part, C, blockIdx.x, q);
+template <int NW, typename TC>
+__global__ void __launch_bounds__(64 * NW) reduce_partials(ReduceDesc d, const float* __restrict__ part,
+                                                           TC* __restrict__ C) {
+    __shared__ double q[NW][64];
+    reduce_block<NW>(d, part, C, blockIdx.x, q);
 }
 
 struct MultiPtrs {
@@ -358,12 +364,13 @@ struct MultiPtrs {
     float* out[4];
 };
 
-__global__ void __launch_bounds__(256) reduce_multi(MultiReduceDesc d, MultiPtrs p) {
-    __shared__ double q[4][64];
+template <int NW>
+__global__ void __launch_bounds__(64 * NW) reduce_multi(MultiReduceDesc d, MultiPtrs p) {
+    __shared__ double q[NW][64];
     int j = 0;
     while (j + 1 < d.n && blockIdx.x >= d.block0[j + 1]) j++;
     if (!p.out[j]) return;   // uniform over the block
-    reduce_block(d.part[j], p.part[j], p.out[j], blockIdx.x - d.block0[j], q);
+    reduce_block<NW>(d.part[j], p.part[j], p.out[j], blockIdx.x - d.block0[j], q);
 }
 
 // ---------------------------------------------------------------------------
@@ -548,7 +555,14 @@ hipError_t launch_reduce_multi(const Launch& ln, const void* const* parts, void*
         p.part[j] = j < d.n ? (const float*)parts[j] : nullptr;
         p.out[j] = j < d.n ? (float*)outs[j] : nullptr;
     }
-    hipLaunchKernelGGL(reduce_multi, dim3(ln.grid[0]), dim3(256), 0, s, d, p);
+    // every part of one launch takes the wave count of the largest partial count
+    int64_t ns = 0;
+    for (int j = 0; j < d.n; j++) ns = d.part[j].nsplit > ns ? d.part[j].nsplit : ns;
+    switch (reduce_waves(ns)) {
+        case 1: hipLaunchKernelGGL(reduce_multi<1>, dim3(ln.grid[0]), dim3(64), 0, s, d, p); break;
+        case 4: hipLaunchKernelGGL(reduce_multi<4>, dim3(ln.grid[0]), dim3(256), 0, s, d, p); break;
+        default: hipLaunchKernelGGL(reduce_multi<16>, dim3(ln.grid[0]), dim3(1024), 0, s, d, p); break;
+    }
     return hipGetLastError();
 }
 
@@ -557,9 +571,19 @@ namespace {
 hipError_t launch_reduce(const Launch& ln, const void* part, void* c, hipStream_t s) {
     ReduceDesc d = desc_of<ReduceDesc>(ln);
     int tC = (ln.kind >> kBitOut) & 1;
-    dim3 g(ln.grid[0]), bl(256);
-    if (tC) hipLaunchKernelGGL((reduce_partials<bf16_t>), g, bl, 0, s, d, (const float*)part, (bf16_t*)c);
-    else hipLaunchKernelGGL((reduce_partials<float>), g, bl, 0, s, d, (const float*)part, (float*)c);
+    if ((int64_t)ln.grid[0] * 64 < (int64_t)d.M * d.N) return hipErrorInvalidValue;
+    dim3 g(ln.grid[0]);
+#define RP_LAUNCH(nw) \
+    do { \
+        if (tC) hipLaunchKernelGGL((reduce_partials<nw, bf16_t>), g, dim3(64 * nw), 0, s, d, (const float*)part, (bf16_t*)c); \
+        else hipLaunchKernelGGL((reduce_partials<nw, float>), g, dim3(64 * nw), 0, s, d, (const float*)part, (float*)c); \
+    } while (0)
+    switch (reduce_waves(d.nsplit)) {
+        case 1: RP_LAUNCH(1); break;
+        case 4: RP_LAUNCH(4); break;
+        default: RP_LAUNCH(16); break;
+    }
+#undef RP_LAUNCH
     return hipGetLastError();
 }
 

@@ -464,31 +464,36 @@ __global__ void __launch_bounds__(256) tc_reduce_few(TcDesc d, const float* __re
     store(C, tc_out_offset(d, g, m, n), (float)acc);
 }
 
-template <typename TC>
-__global__ void __launch_bounds__(256) tc_reduce(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
-    __shared__ double q4[4][64];
+// More chunks: 64 outputs of one g a block; its NW waves sum consecutive runs
+// of the chunks (16 loads in flight a lane), wave 0 adds the run sums in wave
+// order (NW from ksplit alone: 4 up to 64 chunks, else 16).
+template <int NW, typename TC>
+__global__ void __launch_bounds__(64 * NW) tc_reduce(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
+    __shared__ double q[NW][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t MN = d.M * d.N, per_g = (MN + 63) / 64;
     const int64_t g = blockIdx.x / per_g, mn = (blockIdx.x - g * per_g) * 64 + lane;
-    const int64_t quarter = (d.ksplit + 3) / 4;
-    const int64_t c0 = wave * quarter, c1 = min((int64_t)d.ksplit, c0 + quarter);
+    const int64_t run = (d.ksplit + NW - 1) / NW;
+    const int64_t c0 = wave * run, c1 = min((int64_t)d.ksplit, c0 + run);
     double acc = 0.0;
     if (g < d.G && mn < MN) {
         const float* p = P + g * d.ksplit * MN + mn;
         int64_t c = c0;
-        for (; c + 8 <= c1; c += 8) {
-            float v[8];
+        for (; c + 16 <= c1; c += 16) {
+            float v[16];
 #pragma unroll
-            for (int u = 0; u < 8; u++) v[u] = p[(c + u) * MN];
+            for (int u = 0; u < 16; u++) v[u] = p[(c + u) * MN];
 #pragma unroll
-            for (int u = 0; u < 8; u++) acc += v[u];
+            for (int u = 0; u < 16; u++) acc += v[u];
         }
         for (; c < c1; c++) acc += p[c * MN];
     }
-    q4[wave][lane] = acc;
+    q[wave][lane] = acc;
     __syncthreads();
     if (wave != 0 || g >= d.G || mn >= MN) return;
-    const double sum = (q4[0][lane] + q4[1][lane]) + (q4[2][lane] + q4[3][lane]);
+    double sum = q[0][lane];
+#pragma unroll
+    for (int w = 1; w < NW; w++) sum += q[w][lane];
     const int64_t m = mn / d.N, n = mn - m * d.N;
     store(C, tc_out_offset(d, g, m, n), (float)sum);
 }
@@ -539,9 +544,12 @@ hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, vo
         if (t.ksplit <= 8) {
             if (tC) hipLaunchKernelGGL((tc_reduce_few<bf16_t>), g, bl, 0, s, t, (const float*)d, (bf16_t*)c);
             else hipLaunchKernelGGL((tc_reduce_few<float>), g, bl, 0, s, t, (const float*)d, (float*)c);
+        } else if (t.ksplit <= 64) {
+            if (tC) hipLaunchKernelGGL((tc_reduce<4, bf16_t>), g, dim3(256), 0, s, t, (const float*)d, (bf16_t*)c);
+            else hipLaunchKernelGGL((tc_reduce<4, float>), g, dim3(256), 0, s, t, (const float*)d, (float*)c);
         } else {
-            if (tC) hipLaunchKernelGGL((tc_reduce<bf16_t>), g, bl, 0, s, t, (const float*)d, (bf16_t*)c);
-            else hipLaunchKernelGGL((tc_reduce<float>), g, bl, 0, s, t, (const float*)d, (float*)c);
+            if (tC) hipLaunchKernelGGL((tc_reduce<16, bf16_t>), g, dim3(1024), 0, s, t, (const float*)d, (bf16_t*)c);
+            else hipLaunchKernelGGL((tc_reduce<16, float>), g, dim3(1024), 0, s, t, (const float*)d, (float*)c);
         }
         return hipGetLastError();
     }

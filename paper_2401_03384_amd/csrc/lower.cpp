@@ -289,9 +289,9 @@ bool try_wgrad(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out
     lr.d = part;
     lr.c = C.buf;
     lr.grid[0] = (uint32_t)cdiv(M * N, 64);
-    lr.block[0] = 256;
+    lr.block[0] = (uint32_t)(64 * reduce_waves(rd.nsplit));
     set_desc(lr, rd);
-    lr.kname = std::string("reduce_partials<") + tname(C.dtype) + ">";
+    lr.kname = "reduce_partials<" + std::to_string(reduce_waves(rd.nsplit)) + ", " + tname(C.dtype) + ">";
     out.push_back(lr);
     return true;
 }
@@ -995,9 +995,10 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     lr.c = C.buf;
     // outputs of one g a block: 256 (one a thread) for at most 8 chunks, else 64
     lr.grid[0] = (uint32_t)(Gt * cdiv(Mt * Nt, d.ksplit <= 8 ? 256 : 64));
-    lr.block[0] = 256;
+    lr.block[0] = d.ksplit <= 64 ? 256 : 1024;
     set_desc(lr, d);
-    lr.kname = std::string(d.ksplit <= 8 ? "tc_reduce_few<" : "tc_reduce<") + tname(C.dtype) + ">";
+    lr.kname = d.ksplit <= 8 ? std::string("tc_reduce_few<") + tname(C.dtype) + ">"
+                             : std::string("tc_reduce<") + (d.ksplit <= 64 ? "4, " : "16, ") + tname(C.dtype) + ">";
     out.push_back(lr);
     return true;
 }

@@ -255,7 +255,10 @@ bool run_reduce(const Launch& ln, Ctx& c) {
 bool run_reduce_multi(const Launch& ln, Ctx& c) {
     MultiReduceDesc d = desc_of<MultiReduceDesc>(ln);
     REQ(d.n >= 1 && d.n <= 4 && ln.extra.size() == (size_t)(2 * d.n) && d.block0[0] == 0 &&
-        (int64_t)ln.grid[0] == d.block0[d.n] && ln.block[0] == 256, "multi-reduce shape");
+        (int64_t)ln.grid[0] == d.block0[d.n], "multi-reduce shape");
+    int64_t ns = 0;
+    for (int j = 0; j < d.n; j++) ns = std::max<int64_t>(ns, d.part[j].nsplit);
+    REQ(ln.block[0] == (uint32_t)(64 * reduce_waves(ns)), "multi-reduce block");
     for (int j = 0; j < d.n; j++) {
         const ReduceDesc& r = d.part[j];
         REQ((d.block0[j + 1] - d.block0[j]) * 64 >= (int64_t)r.M * r.N &&
