@@ -60,6 +60,7 @@ enum KernelKind : int32_t {
     K_RCP_FWD = 33,         // fused reshaped-CP chain forward (RcpDesc, desc_rcp.h)
     K_RCP_BWD = 34,         // fused reshaped-CP chain backward (RcpBwdDesc, desc_rcp.h)
     K_RCP_PREP = 35,        // its prepared factor table (RcpBwdDesc)
+    K_CCONV = 36,           // convolution contracted over one channel index, MFMA tiles (CconvDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -214,6 +215,31 @@ struct CredDesc {
     int64_t gchunk, nrb, nchunks;      // K_CREDW: batch indices per block, rank groups, chunks
     int64_t blocks;
     uint32_t lds_bytes, threads;
+};
+
+// Convolution contracted over one channel index, on bf16 MFMA tiles:
+//   Y[g][q][h][w] = sum_p sum_{th, tw} Z[g][p][h + dh(th)][w + dw(tw)] * F[p][q][fh(th)][fw(tw)]
+// with dh(t) = zh0 + zhs * t and fh(t) = fh0 + fhs * t (zhs, fhs = +-1; the
+// same along w), Z read as zero outside its H x W plane.  This is the forward
+// of a convolution step with a contraction (the Tucker core, Section 2.3) and,
+// with reversed taps, its input gradient.  Z and Y planes are dense (row
+// stride W); p, q and up to two batch dims have free strides.  A block takes
+// one g, TH output rows and 32 values of q: the filter slice [32][taps][Ppad]
+// and the zero-padded input rows [HP][WP][Ppad] (channels innermost) sit in
+// LDS as bf16 pairs, rows padded to pw_tab / pw_img 32-bit words.
+struct CconvDesc {
+    int32_t H, W, KH, KW;
+    int32_t zh0, zhs, zw0, zws;        // plane offset of tap t: z?0 + z?s * t
+    int32_t fh0, fhs, fw0, fws;        // filter index of tap t: f?0 + f?s * t
+    int32_t P, Q, Ppad, ng;            // contracted / output channels; P rounded up to 16; batch dims
+    int32_t TH, ntiles, nq, HP;        // output rows a tile; tiles; q tiles of 32; LDS input rows
+    int32_t WP, pw_img, pw_tab, tp;    // LDS input columns; word pitches of a pixel, of a q row, of a tap
+    int32_t pad0_, pad_;
+    int64_t G, g_size[2], g_sZ[2], g_sY[2];
+    int64_t z_numel, f_numel;          // elements of Z and F (byte ranges of the raw buffer loads, < 2^30)
+    int64_t z_sp, y_sq, f_sp, f_sq, f_sh, f_sw;
+    int64_t blocks;
+    uint32_t lds_bytes, pad2_;
 };
 
 // Contraction with a small output per batch index and a long reduction:

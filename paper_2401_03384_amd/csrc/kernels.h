@@ -25,6 +25,9 @@ hipError_t launch_thinw(const Launch& ln, const void* p, const void* q, void* pa
 // Plane convolution contracted over one index (K_CRED / K_CREDW, CredDesc):
 // z = the stacked planes, o = the filter (K_CRED) or the output gradient
 // (K_CREDW), y = the output plane (K_CRED) or the fp32 partials (K_CREDW).
+// Convolution contracted over one channel index (K_CCONV, CconvDesc): z = the
+// input planes, f = the filter, y = the output planes (bf16 or fp32).
+hipError_t launch_cconv(const Launch& ln, const void* z, const void* f, void* y, hipStream_t s);
 hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, hipStream_t s);
 
 // Thin channel mixing (K_THIN, GemmDesc): a = factor, b = activations, c = out.

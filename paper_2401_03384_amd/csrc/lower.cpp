@@ -794,6 +794,154 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     return true;
 }
 
+// ---- convolution contracted over one channel index, on MFMA tiles ----------
+//   C[u][q][h][w] = sum_p sum_taps Z[u][p][h + dh][w + dw] * O[p][q][fh][fw]
+// in bf16 (CconvDesc): the forward of a Tucker-core step and its input
+// gradient (taps reversed).  Few output channels stay with try_cred, the
+// filter gradient (taps as outputs) with try_tc.
+bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
+    if (!op.has_r || op.convs.size() != 2 || op.L.dtype != DT_BF16 || op.R.dtype != DT_BF16) return false;
+    const int zside = op.convs[0].aL != 0 ? 0 : 1;
+    const TensorRef& Z = zside == 0 ? op.L : op.R;
+    const TensorRef& O = zside == 0 ? op.R : op.L;
+    const TensorRef& C = op.C;
+    struct Cv {
+        int label;
+        int64_t J, H;
+        int bZ, bO;
+        int64_t gZ, gO;
+    } cv[2];
+    for (int k = 0; k < 2; k++) {
+        const ConvMap& cm = op.convs[k];
+        const int aZ = zside == 0 ? cm.aL : cm.aR, bZ = zside == 0 ? cm.bL : cm.bR;
+        const int aO = zside == 0 ? cm.aR : cm.aL, bO = zside == 0 ? cm.bR : cm.bL;
+        const int64_t gZ = zside == 0 ? cm.gL : cm.gR, gO = zside == 0 ? cm.gR : cm.gL;
+        const int64_t limZ = zside == 0 ? cm.limL : cm.limR, limO = zside == 0 ? cm.limR : cm.limL;
+        if (aZ != 1 || (bZ != 1 && bZ != -1) || aO != 0 || (bO != 1 && bO != -1)) return false;
+        // same-size planes, taps within the filter, offsets of at most a filter width
+        if (cm.O != limZ || cm.J < 1 || cm.J > 7) return false;
+        const int64_t f0 = gO, f1 = gO + bO * (cm.J - 1);
+        if (f0 < 0 || f0 >= limO || f1 < 0 || f1 >= limO) return false;
+        if (gZ < -cm.J || gZ > cm.J) return false;
+        if (!Z.has(cm.label) || !O.has(cm.label) || !C.has(cm.label)) return false;
+        cv[k] = {cm.label, cm.J, limZ, bZ, bO, gZ, gO};
+    }
+    if (Z.stride_of(cv[0].label) == 1) std::swap(cv[0], cv[1]);
+    const Cv& ch = cv[0];
+    const Cv& cw = cv[1];
+    const int64_t H = ch.H, W = cw.H;
+    if (Z.stride_of(cw.label) != 1 || Z.stride_of(ch.label) != W || C.stride_of(cw.label) != 1 ||
+        C.stride_of(ch.label) != W || C.dim_of(ch.label) != H || C.dim_of(cw.label) != W)
+        return false;
+    auto is_conv = [&](int l) { return l == ch.label || l == cw.label; };
+    struct Dm {
+        int64_t size, s1, s2;
+    };
+    auto merge = [](std::vector<Dm>& v) {
+        for (size_t i = 0; i + 1 < v.size();) {
+            if (v[i].s1 == v[i + 1].s1 * v[i + 1].size && v[i].s2 == v[i + 1].s2 * v[i + 1].size) {
+                v[i].size *= v[i + 1].size;
+                v[i].s1 = v[i + 1].s1;
+                v[i].s2 = v[i + 1].s2;
+                v.erase(v.begin() + i + 1);
+            } else {
+                i++;
+            }
+        }
+    };
+    // u: C's labels in Z only (strides in Z, C); q: C's labels in O only (O, C);
+    // p: the contracted ones (Z, O)
+    std::vector<Dm> U, Pd, Qd;
+    for (size_t k = 0; k < C.labels.size(); k++) {
+        const int l = C.labels[k];
+        if (is_conv(l)) continue;
+        const bool inZ = Z.has(l), inO = O.has(l);
+        if (inZ && !inO) U.push_back({C.dims[k], Z.stride_of(l), C.strides[k]});
+        else if (inO && !inZ) Qd.push_back({C.dims[k], O.stride_of(l), C.strides[k]});
+        else return false;
+    }
+    for (size_t k = 0; k < Z.labels.size(); k++) {
+        const int l = Z.labels[k];
+        if (is_conv(l) || C.has(l)) continue;
+        if (!O.has(l)) return false;
+        Pd.push_back({Z.dims[k], Z.strides[k], O.stride_of(l)});
+    }
+    for (int l : O.labels)
+        if (!is_conv(l) && !C.has(l) && !Z.has(l)) return false;
+    merge(U);
+    merge(Pd);
+    merge(Qd);
+    if (U.size() > 2 || Pd.size() != 1 || Qd.size() != 1) return false;
+    const int64_t P = Pd[0].size, Q = Qd[0].size;
+    if (P > 128 || Q <= 16) return false;
+    CconvDesc d;
+    std::memset(&d, 0, sizeof(d));
+    d.H = (int32_t)H;
+    d.W = (int32_t)W;
+    d.KH = (int32_t)ch.J;
+    d.KW = (int32_t)cw.J;
+    d.zh0 = (int32_t)ch.gZ;
+    d.zhs = ch.bZ;
+    d.zw0 = (int32_t)cw.gZ;
+    d.zws = cw.bZ;
+    d.fh0 = (int32_t)ch.gO;
+    d.fhs = ch.bO;
+    d.fw0 = (int32_t)cw.gO;
+    d.fws = cw.bO;
+    d.P = (int32_t)P;
+    d.Q = (int32_t)Q;
+    const int CB = P <= 16 ? 1 : P <= 32 ? 2 : P <= 64 ? 4 : 8;
+    d.Ppad = 16 * CB;
+    d.pw_img = 8 * CB + 4;
+    // tap runs padded by 4 words (lanes writing consecutive taps hit different
+    // banks), q rows to an odd multiple of 4 words (the MFMA reads of 32 rows)
+    d.tp = 8 * CB + 4;
+    d.pw_tab = d.KH * d.KW * d.tp;
+    if ((d.pw_tab / 4) % 2 == 0) d.pw_tab += 4;
+    d.WP = (int32_t)(W + d.KW - 1);
+    // output rows a block: the whole plane when two blocks' LDS fit a CU
+    auto lds_of = [&](int64_t th) { return 4 * (32 * (int64_t)d.pw_tab + (th + d.KH - 1) * d.WP * d.pw_img); };
+    int64_t TH = H;
+    while (TH > 1 && lds_of(TH) > 80 * 1024) TH = (TH + 1) / 2;
+    if (lds_of(TH) > 160 * 1024) return false;
+    d.TH = (int32_t)TH;
+    d.HP = (int32_t)(TH + d.KH - 1);
+    d.ntiles = (int32_t)cdiv(H, TH);
+    d.nq = (int32_t)cdiv(Q, 32);
+    d.lds_bytes = (uint32_t)lds_of(TH);
+    d.ng = (int32_t)U.size();
+    d.G = 1;
+    for (size_t i = 0; i < U.size(); i++) {
+        d.g_size[i] = U[i].size;
+        d.g_sZ[i] = U[i].s1;
+        d.g_sY[i] = U[i].s2;
+        d.G *= U[i].size;
+    }
+    d.z_sp = Pd[0].s1;
+    d.f_sp = Pd[0].s2;
+    d.f_sq = Qd[0].s1;
+    d.y_sq = Qd[0].s2;
+    d.f_sh = O.stride_of(ch.label);
+    d.f_sw = O.stride_of(cw.label);
+    d.z_numel = Z.numel();
+    d.f_numel = O.numel();
+    if (d.z_numel >= (int64_t(1) << 30) || d.f_numel >= (int64_t(1) << 30)) return false;
+    d.blocks = d.G * d.ntiles * d.nq;
+    if (d.blocks > 0x7fffffff) return false;
+    Launch ln;
+    ln.kind = K_CCONV | dt_bits(DT_BF16, DT_BF16, C.dtype);
+    ln.a = Z.buf;
+    ln.b = O.buf;
+    ln.c = C.buf;
+    ln.grid[0] = (uint32_t)d.blocks;
+    ln.block[0] = 256;
+    ln.lds = d.lds_bytes;
+    set_desc(ln, d);
+    ln.kname = "cconv<" + std::to_string(CB) + ", " + tname(C.dtype) + ">";
+    out.push_back(ln);
+    return true;
+}
+
 // ---- general contraction on MFMA tiles --------------------------------------
 bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     if (!op.has_r || op.convs.size() > 2 || op.L.dtype != op.R.dtype) return false;
@@ -1011,7 +1159,8 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
     std::vector<Launch> out;
     bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
                 (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
-                 try_cred(op, scratch, out) || try_thinw(op, scratch, out) || try_tc(op, scratch, out));
+                 try_cred(op, scratch, out) || try_cconv(op, out) || try_thinw(op, scratch, out) ||
+                 try_tc(op, scratch, out));
     if (!fast) {
         out.clear();
         Launch ln = lower_generic(op);

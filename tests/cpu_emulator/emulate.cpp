@@ -1128,6 +1128,56 @@ bool run_tc_reduce(const Launch& ln, Ctx& c) {
 // Plane convolution contracted over one index (K_CRED forward, K_CREDW
 // partials, K_CREDW_REDUCE chunk sum): the kernels' thread mapping, with
 // their LDS plane indices checked against the block's allocation, in double.
+// K_CCONV: the launcher's descriptor checks, then the sum it defines (every
+// operand read bounds-checked).
+bool run_cconv(const Launch& ln, Ctx& c) {
+    CconvDesc d = desc_of<CconvDesc>(ln);
+    const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    const int CB = d.Ppad / 16;
+    REQ(tIn == 1, "bf16 inputs");
+    REQ((CB == 1 || CB == 2 || CB == 4 || CB == 8) && d.Ppad == 16 * CB && d.TH >= 1 && d.HP == d.TH + d.KH - 1 &&
+            d.WP == d.W + d.KW - 1 && d.pw_img == 8 * CB + 4 && d.tp == 8 * CB + 4 && d.pw_tab >= d.KH * d.KW * d.tp && (d.pw_tab & 3) == 0 &&
+            d.P <= d.Ppad && d.nq * 32 >= d.Q && (int64_t)d.ntiles * d.TH >= d.H &&
+            d.lds_bytes == 4u * (uint32_t)(32 * d.pw_tab + d.HP * d.WP * d.pw_img) && d.lds_bytes <= 160 * 1024 &&
+            (int64_t)ln.grid[0] == d.G * d.ntiles * d.nq && d.blocks == (int64_t)ln.grid[0] && ln.block[0] == 256 &&
+            ln.lds == d.lds_bytes,
+        "cconv layout");
+    REQ((d.zhs == 1 || d.zhs == -1) && (d.zws == 1 || d.zws == -1) && (d.fhs == 1 || d.fhs == -1) &&
+            (d.fws == 1 || d.fws == -1) && d.ng >= 0 && d.ng <= 2 && d.z_numel > 0 && d.z_numel < (1ll << 30) &&
+            d.f_numel > 0 && d.f_numel < (1ll << 30),
+        "cconv taps");
+    bool ok = true, o1, o2, o3;
+    Buf Z = resolve(ln.a, c, 0, o1), F = resolve(ln.b, c, 0, o2), Y = resolve(ln.c, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    REQ((size_t)d.z_numel * 2 <= Z.bytes && (size_t)d.f_numel * 2 <= F.bytes, "cconv load ranges");
+    for (int64_t g = 0; g < d.G; g++) {
+        int64_t oz = 0, oy = 0, x = g;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            oz += (x % d.g_size[i]) * d.g_sZ[i];
+            oy += (x % d.g_size[i]) * d.g_sY[i];
+            x /= d.g_size[i];
+        }
+        for (int q = 0; q < d.Q; q++)
+            for (int h = 0; h < d.H; h++)
+                for (int w = 0; w < d.W; w++) {
+                    double acc = 0;
+                    for (int th = 0; th < d.KH; th++)
+                        for (int tw = 0; tw < d.KW; tw++) {
+                            const int hh = h + d.zh0 + d.zhs * th, ww = w + d.zw0 + d.zws * tw;
+                            if (hh < 0 || hh >= d.H || ww < 0 || ww >= d.W) continue;
+                            const int64_t fo = q * d.f_sq + (int64_t)(d.fh0 + d.fhs * th) * d.f_sh +
+                                               (int64_t)(d.fw0 + d.fws * tw) * d.f_sw;
+                            for (int p = 0; p < d.P; p++)
+                                acc += (double)ld(Z, 1, oz + p * d.z_sp + (int64_t)hh * d.W + ww, ok) *
+                                       ld(F, 1, fo + p * d.f_sp, ok);
+                        }
+                    st(Y, tC, oy + q * d.y_sq + (int64_t)h * d.W + w, (float)acc, ok);
+                }
+        REQ(ok, "out-of-bounds access (cconv)");
+    }
+    return true;
+}
+
 bool run_cred(const Launch& ln, Ctx& c) {
     CredDesc d = desc_of<CredDesc>(ln);
     const int kind = ln.kind & 0xff;
@@ -1369,6 +1419,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_TC ? run_tc(ln, c)
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
+                    : v == K_CCONV ? run_cconv(ln, c)
                     : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }

@@ -86,6 +86,10 @@ CASES = {
     "C2k5": W.cp_layer("C2k5t", 1, 32, 32, 6, 29, 32, 5, "f32", 18),
     "C3t": W.tucker2_layer("C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21),
     "C3t_f32": W.tucker2_layer("C3t_f32", 2, 32, 24, 7, 9, 8, 16, 3, "f32", 21),
+    # Tucker cores on MFMA tiles (ragged channels, 5 x 5 taps, row tiles)
+    "C3c": W.PARITY_WORKLOADS["C3c"],
+    "C3c5": W.PARITY_WORKLOADS["C3c5"],
+    "C3m": W.PARITY_WORKLOADS["C3m"],
     "C4t": W.rtt_layer("C4t", 1, (2, 4, 2), (2, 2, 4), 7, 6, 4, 3, "f32", 22),
     "C5at": W.rcp_layer("C5at", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "bf16", 23),
     "C5at_f32": W.rcp_layer("C5at_f32", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "f32", 23),

@@ -128,6 +128,11 @@ PARITY_WORKLOADS = {
     # (50 x 20, a middle tile with halo rows on both sides)
     "C5bt2": rcp_layer("C5bt2", 1, (4, 4, 8), (2, 4, 8), 23, 26, 4, 5, "bf16", 27),
     "C5bt3": rcp_layer("C5bt3", 1, (4, 4, 8), (3, 4, 8), 50, 20, 2, 5, "bf16", 28),
+    # Tucker cores on MFMA tiles: ragged channel counts (padded to 16 / 32),
+    # 5 x 5 taps, and an input too wide for one block's LDS (row tiles)
+    "C3c": tucker2_layer("C3c", 2, 24, 40, 5, 11, 20, 40, 3, "bf16", 31),
+    "C3c5": tucker2_layer("C3c5", 1, 16, 24, 6, 7, 36, 24, 5, "bf16", 32),
+    "C3m": tucker2_layer("C3m", 2, 16, 24, 6, 20, 128, 40, 3, "bf16", 33),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
