@@ -68,10 +68,13 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restri
         uint32_t w[PW2];
 #pragma unroll
         for (int pp = 0; pp < PW2; pp++) {
+            // no branches around the loads (a branch makes the wave wait for
+            // each pair in turn): channels past P load channel 0 and are masked
             const int p = 2 * pp;
-            const uint32_t lo = p < d.P ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)(2 * p * sp), 0) : 0u;
-            const uint32_t hi = p + 1 < d.P ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)(2 * (p + 1) * sp), 0) : 0u;
-            w[pp] = lo | (hi << 16);
+            const bool ok0 = p < d.P, ok1 = p + 1 < d.P;
+            const uint32_t lo = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, ok0 ? (int)(2 * p * sp) : 0, 0);
+            const uint32_t hi = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, ok1 ? (int)(2 * (p + 1) * sp) : 0, 0);
+            w[pp] = (ok0 ? lo : 0u) | ((ok1 ? hi : 0u) << 16);
         }
 #pragma unroll
         for (int u = 0; u < PW2; u += 4)
