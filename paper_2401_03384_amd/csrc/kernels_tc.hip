@@ -236,29 +236,27 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
             }
             return;
         }
+        // k positions past the slice's valid ones load nothing through the
+        // ok flag rather than a branch (every table entry below TK is
+        // written): a branch around each load made the wave wait for its
+        // table read before the next one
 #pragma unroll
         for (int j = 0; j < EA; j++) {
             const int kk = akk(j);
-            ra[j] = (T)0;
-            if (TM == 64 && kk >= kv) continue;   // tid / 64: uniform
             ra[j] = gload<T, IT>(A, rA, aoff + kA[t][kk], aok && kk < kv);
         }
         if (d.tapmask) {
 #pragma unroll
             for (int j = 0; j < EB; j++) {
-                const int kk = bkk(j);   // tid / 128: uniform
-                rb[j] = (T)0;
-                if (kk >= kv) continue;
-                const bool ok = bok && ((tmask >> kj[t][0][kk]) & 1u);
+                const int kk = bkk(j);
+                const bool ok = bok && kk < kv && ((tmask >> kj[t][0][kk]) & 1u);
                 rb[j] = gload<T, IT>(B, rB, boff + kB[t][kk], ok);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < EB; j++) {
                 const int kk = bkk(j);
-                rb[j] = (T)0;
-                if (kk >= kv) continue;
-                bool ok = bok;
+                bool ok = bok && kk < kv;
                 IT off = boff + kB[t][kk];
                 for (int c = 0; c < d.ncv; c++) {
                     const IT pos = bpa[c] + (IT)d.cv_b[c] * (IT)kj[t][c][kk];
