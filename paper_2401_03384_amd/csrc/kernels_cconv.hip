@@ -32,9 +32,12 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
 }
 
 // CB = Ppad / 16 channel blocks of one tap (compile time: the k loop of a tap unrolls)
-template <int CB, typename TC>
-__global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restrict__ Z,
-                                             const bf16_t* __restrict__ F, TC* __restrict__ Y) {
+// T = bf16_t: 32x32x16 bf16 MFMA, channels as bf16 pairs (Ppad = 16 CB);
+// T = float: 32x32x2 fp32 MFMA, one channel a word (Ppad = 8 CB), odd pitches
+template <int CB, typename T, typename TC>
+__global__ void __launch_bounds__(256) cconv(CconvDesc d, const T* __restrict__ Z,
+                                             const T* __restrict__ F, TC* __restrict__ Y) {
+    constexpr bool BF = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     uint32_t* tab = lds;                        // [32][pw_tab]: word t * tp + pp of row q
     uint32_t* img = lds + 32 * d.pw_tab;        // [HP * WP][pw_img]: word pp of a pixel
@@ -61,9 +64,22 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restri
     // byte offset in a register, the channel step a wave-uniform offset;
     // offsets past the range (q past Q, pixels outside the plane) read 0.
     constexpr uint32_t kOut = 0x80000000u;
-    const __amdgpu_buffer_rsrc_t rF = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(F), (short)0, (int)(2 * d.f_numel), 0x00020000);
+    constexpr uint32_t E = sizeof(T);
+    const __amdgpu_buffer_rsrc_t rF = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(F), (short)0, (int)(E * d.f_numel), 0x00020000);
     const __amdgpu_buffer_rsrc_t rZ =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Z + oz), (short)0, (int)(2 * (d.z_numel - oz)), 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(Z + oz), (short)0, (int)(E * (d.z_numel - oz)), 0x00020000);
+    // fp32: one channel a word, written one word at a time (odd pitches)
+    auto chans = [&](__amdgpu_buffer_rsrc_t r, uint32_t voff, int64_t sp, uint32_t* dst) {
+        uint32_t w[PW2];
+#pragma unroll
+        for (int p = 0; p < PW2; p++) {
+            const bool ok = p < d.P;
+            const uint32_t v = __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, ok ? (int)(4 * p * sp) : 0, 0);
+            w[p] = ok ? v : 0u;
+        }
+#pragma unroll
+        for (int p = 0; p < PW2; p++) dst[p] = w[p];
+    };
     auto pairs = [&](__amdgpu_buffer_rsrc_t r, uint32_t voff, int64_t sp, uint32_t* dst) {
         uint32_t w[PW2];
 #pragma unroll
@@ -84,19 +100,23 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restri
         const int q = ct / KT, t = ct - q * KT, tr = t / d.KW, tc = t - tr * d.KW;
         const int64_t o = (int64_t)(q0 + q) * d.f_sq + (int64_t)(d.fh0 + d.fhs * tr) * d.f_sh +
                           (int64_t)(d.fw0 + d.fws * tc) * d.f_sw;
-        pairs(rF, q0 + q < d.Q ? (uint32_t)(2 * o) : kOut, d.f_sp, tab + q * d.pw_tab + t * d.tp);
+        const uint32_t voff = q0 + q < d.Q ? (uint32_t)(E * o) : kOut;
+        if constexpr (BF) pairs(rF, voff, d.f_sp, tab + q * d.pw_tab + t * d.tp);
+        else chans(rF, voff, d.f_sp, tab + q * d.pw_tab + t * d.tp);
     }
     // input rows h0 + dhmin .. (HP rows), columns dwmin .. (WP)
     for (int px = threadIdx.x; px < d.HP * d.WP; px += 256) {
         const int rr = px / d.WP, cc = px - rr * d.WP;
         const int hh = h0 + dhmin + rr, ww = dwmin + cc;
         const bool in = hh >= 0 && hh < d.H && ww >= 0 && ww < d.W;
-        pairs(rZ, in ? (uint32_t)(2 * (hh * d.W + ww)) : kOut, d.z_sp, img + px * d.pw_img);
+        const uint32_t voff = in ? (uint32_t)(E * (hh * d.W + ww)) : kOut;
+        if constexpr (BF) pairs(rZ, voff, d.z_sp, img + px * d.pw_img);
+        else chans(rZ, voff, d.z_sp, img + px * d.pw_img);
     }
     __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hf = lane >> 5, cl = lane & 31;
     const int npx = th * d.W, ptiles = (npx + 31) / 32;
-    const uint32_t* arow = tab + cl * d.pw_tab + 4 * hf;
+    const uint32_t* arow = tab + cl * d.pw_tab + (BF ? 4 * hf : hf);
     for (int pt = 2 * wave; pt < ptiles; pt += 8) {
         const int n0 = pt * 32 + cl, n1 = n0 + 32;
         const bool v0 = n0 < npx, v1 = n1 < npx;
@@ -109,9 +129,25 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restri
         for (int t = 0; t < KT; t++) {
             const int tr = t / d.KW, tc = t - tr * d.KW;
             const int dr = d.zh0 + d.zhs * tr - dhmin, dc = d.zw0 + d.zws * tc - dwmin;
-            const uint32_t* b0 = img + ((r0 + dr) * d.WP + c0 + dc) * d.pw_img + 4 * hf;
-            const uint32_t* b1 = img + ((r1 + dr) * d.WP + c1 + dc) * d.pw_img + 4 * hf;
+            const uint32_t* b0 = img + ((r0 + dr) * d.WP + c0 + dc) * d.pw_img + (BF ? 4 * hf : hf);
+            const uint32_t* b1 = img + ((r1 + dr) * d.WP + c1 + dc) * d.pw_img + (BF ? 4 * hf : hf);
             const uint32_t* a = arow + t * d.tp;
+            if constexpr (!BF) {
+                // k step of two channels: lane half hf supplies channel 2i + hf
+                float af[4 * CB], bf0[4 * CB], bf1[4 * CB];
+#pragma unroll
+                for (int i = 0; i < 4 * CB; i++) {
+                    af[i] = __uint_as_float(a[2 * i]);
+                    bf0[i] = __uint_as_float(b0[2 * i]);
+                    bf1[i] = __uint_as_float(b1[2 * i]);
+                }
+#pragma unroll
+                for (int i = 0; i < 4 * CB; i++) {
+                    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf0[i], acc0, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf1[i], acc1, 0, 0, 0);
+                }
+                continue;
+            }
             uint4 av[CB], bv0[CB], bv1[CB];
 #pragma unroll
             for (int cb = 0; cb < CB; cb++) {
@@ -138,9 +174,9 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const bf16_t* __restri
     }
 }
 
-template <int CB, typename TC>
+template <int CB, typename T, typename TC>
 hipError_t cconv_go(const CconvDesc& d, dim3 g, const void* z, const void* f, void* y, hipStream_t s) {
-    auto k = cconv<CB, TC>;
+    auto k = cconv<CB, T, TC>;
     // dynamic LDS above 64 KB has to be allowed per kernel, once per device
     static std::atomic<uint64_t> allowed{0};
     if (d.lds_bytes > 64 * 1024) {
@@ -154,7 +190,7 @@ hipError_t cconv_go(const CconvDesc& d, dim3 g, const void* z, const void* f, vo
             allowed.fetch_or(1ull << dev);
         }
     }
-    hipLaunchKernelGGL(k, g, dim3(256), d.lds_bytes, s, d, (const bf16_t*)z, (const bf16_t*)f, (TC*)y);
+    hipLaunchKernelGGL(k, g, dim3(256), d.lds_bytes, s, d, (const T*)z, (const T*)f, (TC*)y);
     return hipGetLastError();
 }
 
@@ -163,12 +199,13 @@ hipError_t cconv_go(const CconvDesc& d, dim3 g, const void* z, const void* f, vo
 hipError_t launch_cconv(const Launch& ln, const void* z, const void* f, void* y, hipStream_t s) {
     CconvDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    const int tC = (ln.kind >> kBitOut) & 1;
-    const int CB = d.Ppad / 16;
+    const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
+    const int CB = d.Ppad / (tIn ? 16 : 8);
     // the descriptor's LDS layout is the one the kernel indexes
-    if (!(CB == 1 || CB == 2 || CB == 4 || CB == 8) || d.Ppad != 16 * CB || d.TH < 1 || d.HP != d.TH + d.KH - 1 ||
-        d.WP != d.W + d.KW - 1 || d.pw_img != 8 * CB + 4 || d.tp != 8 * CB + 4 ||
-        d.pw_tab < d.KH * d.KW * d.tp || (d.pw_tab & 3) ||
+    const bool lay = tIn ? (d.Ppad == 16 * CB && d.pw_img == 8 * CB + 4 && d.tp == 8 * CB + 4 && !(d.pw_tab & 3))
+                         : (d.Ppad == 8 * CB && d.pw_img == 8 * CB + 1 && d.tp == 8 * CB && (d.pw_tab & 1));
+    if (!(CB == 1 || CB == 2 || CB == 4 || CB == 8) || !lay || (!tIn && tC) || d.TH < 1 || d.HP != d.TH + d.KH - 1 ||
+        d.WP != d.W + d.KW - 1 || d.pw_tab < d.KH * d.KW * d.tp ||
         d.P > d.Ppad || d.nq * 32 < d.Q || d.z_numel <= 0 || d.z_numel >= (1ll << 30) || d.f_numel <= 0 ||
         d.f_numel >= (1ll << 30) || (int64_t)d.ntiles * d.TH < d.H ||
         d.lds_bytes != 4u * (uint32_t)(32 * d.pw_tab + d.HP * d.WP * d.pw_img) || d.lds_bytes > 160 * 1024 ||
@@ -177,8 +214,9 @@ hipError_t launch_cconv(const Launch& ln, const void* z, const void* f, void* y,
     const dim3 g(ln.grid[0]);
 #define CC_CASE(cb)                                                                          \
     case cb:                                                                                 \
-        if (tC) return cconv_go<cb, bf16_t>(d, g, z, f, y, s);                              \
-        else return cconv_go<cb, float>(d, g, z, f, y, s);
+        if (!tIn) return cconv_go<cb, float, float>(d, g, z, f, y, s);                      \
+        if (tC) return cconv_go<cb, bf16_t, bf16_t>(d, g, z, f, y, s);                      \
+        return cconv_go<cb, bf16_t, float>(d, g, z, f, y, s);
     switch (CB) {
         CC_CASE(1)
         CC_CASE(2)

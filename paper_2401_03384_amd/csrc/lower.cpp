@@ -800,7 +800,9 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
 // gradient (taps reversed).  Few output channels stay with try_cred, the
 // filter gradient (taps as outputs) with try_tc.
 bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
-    if (!op.has_r || op.convs.size() != 2 || op.L.dtype != DT_BF16 || op.R.dtype != DT_BF16) return false;
+    if (!op.has_r || op.convs.size() != 2 || op.L.dtype != op.R.dtype) return false;
+    const bool bf = op.L.dtype == DT_BF16;
+    if (!bf && op.C.dtype != DT_F32) return false;
     const int zside = op.convs[0].aL != 0 ? 0 : 1;
     const TensorRef& Z = zside == 0 ? op.L : op.R;
     const TensorRef& O = zside == 0 ? op.R : op.L;
@@ -873,7 +875,7 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     merge(Qd);
     if (U.size() > 2 || Pd.size() != 1 || Qd.size() != 1) return false;
     const int64_t P = Pd[0].size, Q = Qd[0].size;
-    if (P > 128 || Q <= 16) return false;
+    if (P > (bf ? 128 : 64) || Q <= 16) return false;
     CconvDesc d;
     std::memset(&d, 0, sizeof(d));
     d.H = (int32_t)H;
@@ -890,14 +892,18 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     d.fws = cw.bO;
     d.P = (int32_t)P;
     d.Q = (int32_t)Q;
-    const int CB = P <= 16 ? 1 : P <= 32 ? 2 : P <= 64 ? 4 : 8;
-    d.Ppad = 16 * CB;
-    d.pw_img = 8 * CB + 4;
+    // bf16: pairs of channels a word, 16 CB channels, 16-byte runs padded by 4
+    // words; fp32: a channel a word, 8 CB channels, odd pitches
+    const int unit = bf ? 16 : 8;
+    const int CB = P <= unit ? 1 : P <= 2 * unit ? 2 : P <= 4 * unit ? 4 : 8;
+    d.Ppad = unit * CB;
+    d.pw_img = bf ? 8 * CB + 4 : 8 * CB + 1;
     // tap runs padded by 4 words (lanes writing consecutive taps hit different
     // banks), q rows to an odd multiple of 4 words (the MFMA reads of 32 rows)
-    d.tp = 8 * CB + 4;
+    d.tp = bf ? 8 * CB + 4 : 8 * CB;
     d.pw_tab = d.KH * d.KW * d.tp;
-    if ((d.pw_tab / 4) % 2 == 0) d.pw_tab += 4;
+    if (bf && (d.pw_tab / 4) % 2 == 0) d.pw_tab += 4;
+    if (!bf) d.pw_tab += 1;
     d.WP = (int32_t)(W + d.KW - 1);
     // output rows a block: the whole plane when two blocks' LDS fit a CU
     auto lds_of = [&](int64_t th) { return 4 * (32 * (int64_t)d.pw_tab + (th + d.KH - 1) * d.WP * d.pw_img); };
@@ -929,7 +935,7 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     d.blocks = d.G * d.ntiles * d.nq;
     if (d.blocks > 0x7fffffff) return false;
     Launch ln;
-    ln.kind = K_CCONV | dt_bits(DT_BF16, DT_BF16, C.dtype);
+    ln.kind = K_CCONV | dt_bits(op.L.dtype, op.L.dtype, C.dtype);
     ln.a = Z.buf;
     ln.b = O.buf;
     ln.c = C.buf;
@@ -937,7 +943,7 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     ln.block[0] = 256;
     ln.lds = d.lds_bytes;
     set_desc(ln, d);
-    ln.kname = "cconv<" + std::to_string(CB) + ", " + tname(C.dtype) + ">";
+    ln.kname = "cconv<" + std::to_string(CB) + ", " + tname(op.L.dtype) + ", " + tname(C.dtype) + ">";
     out.push_back(ln);
     return true;
 }

@@ -1133,10 +1133,12 @@ bool run_tc_reduce(const Launch& ln, Ctx& c) {
 bool run_cconv(const Launch& ln, Ctx& c) {
     CconvDesc d = desc_of<CconvDesc>(ln);
     const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
-    const int CB = d.Ppad / 16;
-    REQ(tIn == 1, "bf16 inputs");
-    REQ((CB == 1 || CB == 2 || CB == 4 || CB == 8) && d.Ppad == 16 * CB && d.TH >= 1 && d.HP == d.TH + d.KH - 1 &&
-            d.WP == d.W + d.KW - 1 && d.pw_img == 8 * CB + 4 && d.tp == 8 * CB + 4 && d.pw_tab >= d.KH * d.KW * d.tp && (d.pw_tab & 3) == 0 &&
+    const int CB = d.Ppad / (tIn ? 16 : 8);
+    REQ(tIn == 1 || tC == 0, "fp32 inputs give fp32 outputs");
+    const bool lay = tIn ? (d.Ppad == 16 * CB && d.pw_img == 8 * CB + 4 && d.tp == 8 * CB + 4 && (d.pw_tab & 3) == 0)
+                         : (d.Ppad == 8 * CB && d.pw_img == 8 * CB + 1 && d.tp == 8 * CB && (d.pw_tab & 1) == 1);
+    REQ((CB == 1 || CB == 2 || CB == 4 || CB == 8) && lay && d.TH >= 1 && d.HP == d.TH + d.KH - 1 &&
+            d.WP == d.W + d.KW - 1 && d.pw_tab >= d.KH * d.KW * d.tp &&
             d.P <= d.Ppad && d.nq * 32 >= d.Q && (int64_t)d.ntiles * d.TH >= d.H &&
             d.lds_bytes == 4u * (uint32_t)(32 * d.pw_tab + d.HP * d.WP * d.pw_img) && d.lds_bytes <= 160 * 1024 &&
             (int64_t)ln.grid[0] == d.G * d.ntiles * d.nq && d.blocks == (int64_t)ln.grid[0] && ln.block[0] == 256 &&
@@ -1149,7 +1151,8 @@ bool run_cconv(const Launch& ln, Ctx& c) {
     bool ok = true, o1, o2, o3;
     Buf Z = resolve(ln.a, c, 0, o1), F = resolve(ln.b, c, 0, o2), Y = resolve(ln.c, c, 0, o3);
     REQ(o1 && o2 && o3, "unresolved buffer");
-    REQ((size_t)d.z_numel * 2 <= Z.bytes && (size_t)d.f_numel * 2 <= F.bytes, "cconv load ranges");
+    const size_t E = tIn ? 2 : 4;
+    REQ((size_t)d.z_numel * E <= Z.bytes && (size_t)d.f_numel * E <= F.bytes, "cconv load ranges");
     for (int64_t g = 0; g < d.G; g++) {
         int64_t oz = 0, oy = 0, x = g;
         for (int i = d.ng - 1; i >= 0; --i) {
@@ -1168,8 +1171,8 @@ bool run_cconv(const Launch& ln, Ctx& c) {
                             const int64_t fo = q * d.f_sq + (int64_t)(d.fh0 + d.fhs * th) * d.f_sh +
                                                (int64_t)(d.fw0 + d.fws * tw) * d.f_sw;
                             for (int p = 0; p < d.P; p++)
-                                acc += (double)ld(Z, 1, oz + p * d.z_sp + (int64_t)hh * d.W + ww, ok) *
-                                       ld(F, 1, fo + p * d.f_sp, ok);
+                                acc += (double)ld(Z, tIn, oz + p * d.z_sp + (int64_t)hh * d.W + ww, ok) *
+                                       ld(F, tIn, fo + p * d.f_sp, ok);
                         }
                     st(Y, tC, oy + q * d.y_sq + (int64_t)h * d.W + w, (float)acc, ok);
                 }

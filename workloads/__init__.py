@@ -133,6 +133,9 @@ PARITY_WORKLOADS = {
     "C3c": tucker2_layer("C3c", 2, 24, 40, 5, 11, 20, 40, 3, "bf16", 31),
     "C3c5": tucker2_layer("C3c5", 1, 16, 24, 6, 7, 36, 24, 5, "bf16", 32),
     "C3m": tucker2_layer("C3m", 2, 16, 24, 6, 20, 128, 40, 3, "bf16", 33),
+    # the same kernel in fp32 (Tucker core; the tensor-train layer's transposed conv)
+    "C3c_f32": tucker2_layer("C3c_f32", 2, 24, 40, 5, 11, 20, 40, 3, "f32", 31),
+    "C4c": rtt_layer("C4c", 1, (2, 2, 4), (2, 2, 2), 6, 7, 16, 3, "f32", 34),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
