@@ -136,6 +136,8 @@ PARITY_WORKLOADS = {
     # the same kernel in fp32 (Tucker core; the tensor-train layer's transposed conv)
     "C3c_f32": tucker2_layer("C3c_f32", 2, 24, 40, 5, 11, 20, 40, 3, "f32", 31),
     "C4c": rtt_layer("C4c", 1, (2, 2, 4), (2, 2, 2), 6, 7, 16, 3, "f32", 34),
+    # the full tensor-train chain at channel sizes of the 28x28 layer, small planes
+    "C4w": rtt_layer("C4w", 2, (4, 8, 8), (4, 8, 8), 9, 11, 16, 3, "f32", 35),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
