@@ -359,3 +359,25 @@ def test_limited_planner_matches_oracle_on_random_expressions(seed):
         if e.n > 6 or any(len(e.holders(l)) > 2 for l in e.conv):
             continue
         _compare_limited(spec, shapes, _limits_for(e))
+
+
+@pytest.mark.parametrize("name,steps", [
+    ("C3", ["step 1 fwd", "step 1 recompute", "step 1 grad lhs"]),
+    ("C3s_f32", ["step 1 fwd", "step 1 recompute", "step 1 grad lhs"]),
+    ("C4", ["step 3 grad lhs"]),
+    ("C3t", []),   # 16 output channels: the plane kernel, not MFMA tiles
+])
+def test_conv_contraction_kernel_selected(name, steps):
+    """Steps that convolve and contract one channel index with more than 16
+    output channels run on the MFMA conv-contraction kernel (kind 36), both
+    forward and input gradient; the filter gradient does not."""
+    w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS.get(name) or W.tucker2_layer(
+        "C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21)
+    p = _plan(w.spec, w.shapes, dtype=B.CE_BF16 if w.dtype == "bf16" else B.CE_F32)
+    text = B.ce_plan_describe(p)
+    B.ce_plan_destroy(p)
+    on36 = [l for l in text.splitlines() if "kernel 36:" in l]
+    for s in steps:
+        assert any(s in l for l in on36), (name, s, text)
+    assert len(on36) == len(steps), (name, on36)
+    assert not any("grad rhs" in l for l in on36)
