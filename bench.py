@@ -21,6 +21,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+# layer floors use the dense MFMA peak of the input type (157.3 / 2516.6 TFLOP/s)
+PEAK_LAYER_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
+# the five layers of the metric; C2 in float32 is the headline line itself
+CONFIGS = [("C2", "f32"), ("C2_bf16", "bf16"), ("C3", "bf16"), ("C4", "f32"), ("C5a", "bf16"),
+           ("C5b", "bf16")]
 # kernels whose arithmetic runs on the vector ALU (no MFMA tile fits their
 # contractions): peak = 256 CUs x 64 lanes x 2.4 GHz x flops per lane-op,
 # 4 for v_dot2_f32_bf16 (two products) and 2 for an fp32 FMA
@@ -47,6 +52,10 @@ def parse_args():
                     help="also time forward + backward replayed from a HIP graph (no host work)")
     ap.add_argument("--compare-ltr", action="store_true",
                     help="also time the left-to-right order on the same kernels")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-layer lines of the other configurations")
+    ap.add_argument("--sample-steps", type=int, default=100,
+                    help="individually timed steps for the median / min")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run plain device copies of this size (counter calibration)")
     return ap.parse_args()
@@ -91,7 +100,8 @@ def kernel_totals(records):
 
 def roofline(records, dtype, share):
     """Roofline of the dominant kernel from its live launch records (every
-    record is a launch of that kernel); `share` is its share of kernel time."""
+    record is a launch of that kernel, bracketed by HIP events on its own
+    stream); `share` is its share of kernel time."""
     by = kernel_totals(records)
     assert len(by) == 1, by.keys()
     kname, (ms, n, nbytes, flops) = next(iter(by.items()))
@@ -106,12 +116,37 @@ def roofline(records, dtype, share):
     else:
         achieved, peak, unit, bound = flops / n / avg_s / 1e12, PEAK_MFMA_TFLOPS[dtype], "TFLOP/s", "mfma"
     traffic = measured_traffic(kname, dtype)
+    extra = {}
+    if alu:
+        # the same work against the dense MFMA peak of its input type
+        mf = flops / n / avg_s / 1e12
+        extra = {"frac_vs_mfma_peak": round(mf / PEAK_LAYER_TFLOPS[dtype], 5)}
     return {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4),
+            "unit": unit, "frac": round(achieved / peak, 4), **extra,
             "traffic": None if traffic is None else round(traffic),
             "alg_bytes_per_launch": round(nbytes / n),
             "launches": n, "avg_us": round(ms / n * 1e3, 2),
+            "avg_us_timing": "HIP events bracketing each launch on its stream",
             "share_of_kernel_time": round(share, 3)}
+
+
+def prod(xs):
+    out = 1
+    for x in xs:
+        out *= int(x)
+    return out
+
+
+def layer_floor_us(w, dtype, macs):
+    """Forward + backward floor of a layer: max(F / MFMA peak, B / HBM peak)
+    with F = 6 x planned forward MACs and B = the compulsory bytes (X and dY
+    read, Y and dX written once in the input type; factors read once and
+    their float32 gradients written once)."""
+    e = 2 if dtype == "bf16" else 4
+    nx, ny = prod(w.shapes[0]), prod(w.out_shape)
+    nf = sum(prod(s) for s in w.shapes[1:])
+    nbytes = e * (2 * nx + 2 * ny) + nf * (e + 4)
+    return max(6 * macs / (PEAK_LAYER_TFLOPS[dtype] * 1e12), nbytes / (PEAK_HBM_GBS * 1e9)) * 1e6
 
 
 def launch_table(records, steps):
@@ -130,6 +165,18 @@ def launch_table(records, steps):
         lines.append(f"{ms * 1e3:9.1f} {ms / tot:6.1%} {nbytes / s / 1e9 if s else 0:8.0f} "
                      f"{flops / s / 1e12 if s else 0:7.2f}  {kname} | {step}")
     return "\n".join(lines)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(w, batch):
@@ -157,6 +204,7 @@ def cpu_baseline(w, batch):
             break
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(6 * macs * passes / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+            "cpu": cpu_model(), "host_cpus": os.cpu_count(),
             "kind": "oracle", "seconds": round(dt, 2), "passes": passes,
             "sample": f"{ws.name}: batch {batch} of {w.shapes[0][0]}, other sizes full; "
                       f"float64 pairwise forward + backward along the planned tree, "
@@ -195,13 +243,138 @@ def compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args):
             "steps": n}
 
 
+class Runner:
+    """One layer on the device: seeded inputs resident in HBM, output,
+    gradient and workspace buffers, and step() = parse + plan + forward +
+    backward through the C ABI on torch's current stream."""
+
+    def __init__(self, w, dtype, flags=0, path=None, max_elements=None):
+        import numpy as np
+        import torch
+        import paper_2401_03384_amd as P
+        import workloads as W
+
+        if dtype != w.dtype:
+            w = W.Workload(w.name, w.spec, w.shapes, dtype, w.seed, w.sigmas, w.out_shape, w.backward)
+        self.w, self.dtype, self.flags, self.path, self.max_elements = w, dtype, flags, path, max_elements
+        dev = torch.device("cuda:0")
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        ins, dy = W.make_inputs(w)
+        self.xs = [torch.from_numpy(a.astype(np.float32)).to(tdt).to(dev) for a in ins]
+        self.d = torch.from_numpy(dy.astype(np.float32)).to(tdt).to(dev)
+        del ins, dy
+        self.ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=max_elements)
+        ref = self.ref
+        self.ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
+        self.out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
+        self.grads = [torch.empty(s, dtype=ref.grad_dtype(i), device=dev) for i, s in enumerate(w.shapes)]
+        self.in_ptrs = [x.data_ptr() for x in self.xs]
+        self.g_ptrs = [g.data_ptr() for g in self.grads]
+        self.stream = torch.cuda.current_stream(dev).cuda_stream
+        self.shapes = [tuple(s) for s in w.shapes]
+        self.cdt = P.CE_BF16 if dtype == "bf16" else P.CE_F32
+        self.P, self.torch = P, torch
+
+    def step(self, fwd=True, bwd=True):
+        P, w = self.P, self.w
+        e = P.ce_expr_parse(w.spec, self.shapes)
+        if self.path is None and self.max_elements is not None:
+            p = P.ce_plan_create_limited(e, P.CE_COST_FWD, self.cdt, self.flags, self.max_elements)
+        elif self.path is None:
+            p = P.ce_plan_create(e, P.CE_COST_FWD, self.cdt, self.flags)
+        else:
+            p = P.ce_plan_create_with_path(e, self.path, self.cdt, self.flags)
+        P.ce_expr_destroy(e)
+        if fwd:
+            P.ce_forward(p, self.in_ptrs, self.out.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                         self.stream)
+        if bwd:
+            P.ce_backward(p, self.in_ptrs, self.d.data_ptr(), self.g_ptrs, self.ws.data_ptr(),
+                          self.ws.numel(), self.stream)
+        P.ce_plan_destroy(p)
+
+    def timed(self, n, **kw):
+        torch = self.torch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            self.step(**kw)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n
+
+    def sampled(self, n):
+        """n steps each bracketed by events on the launch stream: median,
+        min and mean in ms."""
+        torch = self.torch
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        torch.cuda.synchronize()
+        for a, b in evs:
+            a.record()
+            self.step()
+            b.record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) for a, b in evs)
+        return {"median_ms": round(ts[len(ts) // 2], 4), "min_ms": round(ts[0], 4),
+                "mean_ms": round(sum(ts) / len(ts), 4), "samples": n}
+
+    def dominant(self):
+        """One step with every launch timed: the kernel with the largest
+        total time and its share of the step's kernel time."""
+        P = self.P
+        P.ce_timing_begin()
+        self.step()
+        probe = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
+        by = kernel_totals(probe)
+        k = max(by, key=lambda x: by[x][0])
+        return k, by[k][0] / sum(v[0] for v in by.values())
+
+    def kernel_roofline(self, kname, share, n):
+        """Roofline of kernel `kname` over n steps, only its launches bracketed."""
+        P = self.P
+        P.ce_timing_begin_kernel(kname)
+        t = self.timed(n)
+        records = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
+        return t, roofline(records, self.dtype, share)
+
+
+def config_line(name, dtype, steps, samples):
+    """fwd+bwd figures of one configuration (see CONFIGS)."""
+    import workloads as W
+
+    r = Runner(W.WORKLOADS[name], dtype)
+    for _ in range(3):
+        r.step()
+    kname, share = r.dominant()
+    t, roof = r.kernel_roofline(kname, share, max(5, steps // 2))
+    t_mean = r.timed(steps)
+    smp = r.sampled(samples)
+    macs = r.ref.fwd_macs
+    floor = layer_floor_us(r.w, dtype, macs)
+    w = r.w
+    out = {"workload": f"{w.name}: {w.spec} X{list(w.shapes[0])}", "dtype": dtype,
+           "ms_per_step": round(t_mean * 1e3, 4), **smp,
+           "tflops": round(6 * macs / t_mean / 1e12, 3),
+           "floor_us": round(floor, 1), "floor_frac": round(floor / (t_mean * 1e6), 4),
+           "floor_frac_median": round(floor / (smp["median_ms"] * 1e3), 4),
+           "workspace_bytes": {"fwd": r.ref.ws_fwd, "bwd": r.ref.ws_bwd},
+           "dominant": {k: roof[k] for k in ("kernel", "bound", "achieved", "unit", "peak", "frac",
+                                             "avg_us", "share_of_kernel_time")
+                        if k in roof}}
+    if "frac_vs_mfma_peak" in roof:
+        out["dominant"]["frac_vs_mfma_peak"] = roof["frac_vs_mfma_peak"]
+    del r
+    import torch
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); multi-GPU is "
               "not part of this build", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     if args.calibrate_copy:
@@ -220,85 +393,42 @@ def main():
 
     w = W.WORKLOADS[args.workload]
     dtype = args.dtype or w.dtype
-    if dtype != w.dtype:
-        w = W.Workload(w.name, w.spec, w.shapes, dtype, w.seed, w.sigmas, w.out_shape, w.backward)
-    dev = torch.device("cuda:0")
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    ins, dy = W.make_inputs(w)
-    xs = [torch.from_numpy(a.astype(np.float32)).to(tdt).to(dev) for a in ins]
-    d = torch.from_numpy(dy.astype(np.float32)).to(tdt).to(dev)
     flags = P.CE_FLAG_GENERIC_ONLY if args.generic else 0
     n_in = len(w.shapes)
     # left-to-right in the list format of ce_plan_create_with_path
     ltr = [(0, 1)] + [(0, n_in - 1 - k) for k in range(1, n_in - 1)]
     path = ltr if args.path == "ltr" else None
-    ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=args.max_elements)
-    ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
-    out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
-    grads = [torch.empty(s, dtype=ref.grad_dtype(i), device=dev) for i, s in enumerate(w.shapes)]
-    in_ptrs = [x.data_ptr() for x in xs]
-    g_ptrs = [g.data_ptr() for g in grads]
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    shapes = [tuple(s) for s in w.shapes]
-    cdt = P.CE_BF16 if dtype == "bf16" else P.CE_F32
-
-    def step(fwd=True, bwd=True):
-        e = P.ce_expr_parse(w.spec, shapes)
-        if path is None and args.max_elements is not None:
-            p = P.ce_plan_create_limited(e, P.CE_COST_FWD, cdt, flags, args.max_elements)
-        elif path is None:
-            p = P.ce_plan_create(e, P.CE_COST_FWD, cdt, flags)
-        else:
-            p = P.ce_plan_create_with_path(e, path, cdt, flags)
-        P.ce_expr_destroy(e)
-        if fwd:
-            P.ce_forward(p, in_ptrs, out.data_ptr(), ws.data_ptr(), ws.numel(), stream)
-        if bwd:
-            P.ce_backward(p, in_ptrs, d.data_ptr(), g_ptrs, ws.data_ptr(), ws.numel(), stream)
-        P.ce_plan_destroy(p)
-
-    def timed(n, **kw):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(n):
-            step(**kw)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / n
+    r = Runner(w, dtype, flags, path, args.max_elements)
+    w, ref = r.w, r.ref
 
     for _ in range(args.warmup):
-        step()
+        r.step()
     torch.cuda.synchronize()
-    # one probe step with every launch timed names the dominant kernel (largest time)
-    P.ce_timing_begin()
-    step()
-    probe = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
-    by = kernel_totals(probe)
-    dominant = max(by, key=lambda k: by[k][0])
-    share = by[dominant][0] / sum(v[0] for v in by.values())
-    # timed region: whole steps; the dominant kernel's launches are bracketed
-    # by HIP events on their stream (the other launches run without events)
-    P.ce_timing_begin_kernel(dominant)
-    t_step = timed(args.steps)
-    n_rec = P.ce_timing_end()
-    records = [P.ce_timing_record(i) for i in range(n_rec)]
+    dominant, share = r.dominant()
+    # timed region: exactly --steps whole steps; the dominant kernel's launches
+    # are bracketed by HIP events on their stream (the other launches run
+    # without events in between)
+    t_step, roof = r.kernel_roofline(dominant, share, args.steps)
     if args.launch_table:
         P.ce_timing_begin()
-        timed(args.steps)
+        r.timed(args.steps)
         table = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
         print(launch_table(table, args.steps), file=sys.stderr, flush=True)
+    smp = r.sampled(max(args.sample_steps, args.steps))
     # forward-only and backward-only steps (reported beside the main figure)
-    t_fwd = timed(max(5, args.steps // 2), bwd=False)
-    t_bwd = timed(max(5, args.steps // 2), fwd=False)
+    t_fwd = r.timed(max(5, args.steps // 2), bwd=False)
+    t_bwd = r.timed(max(5, args.steps // 2), fwd=False)
     t0 = time.perf_counter()
     for _ in range(200):
-        e = P.ce_expr_parse(w.spec, shapes)
-        p = P.ce_plan_create(e, P.CE_COST_FWD, cdt, flags)
+        e = P.ce_expr_parse(w.spec, r.shapes)
+        p = P.ce_plan_create(e, P.CE_COST_FWD, r.cdt, flags)
         P.ce_expr_destroy(e)
         P.ce_plan_destroy(p)
     t_plan = (time.perf_counter() - t0) / 200
 
     macs = ref.fwd_macs
     value = 6 * macs / t_step / 1e12
+    floor = layer_floor_us(w, dtype, macs)
     line = {
         "metric": "effective TFLOP/s (fwd+bwd) of a CP-factorised 3x3 conv layer, 1 MI355X",
         "value": round(value, 3),
@@ -318,14 +448,17 @@ def main():
                    "path": ("left-to-right" if path else "optimal")
                    + (f", intermediates <= {args.max_elements} elements" if args.max_elements else "")
                    + (", generic kernel" if args.generic else "")},
+        "step_ms": smp,
+        "floor_us": round(floor, 1),
+        "floor_frac": round(floor / (t_step * 1e6), 4),
         "workspace_bytes": {"fwd": ref.ws_fwd, "bwd": ref.ws_bwd},
         "fwd_ms": round(t_fwd * 1e3, 4),
         "bwd_ms": round(t_bwd * 1e3, 4),
         "plan_ms": round(t_plan * 1e3, 4),
-        "roofline": roofline(records, dtype, share),
+        "roofline": roof,
     }
     if args.graph:
-        g = P.GraphStep(ref, xs, d)
+        g = P.GraphStep(ref, r.xs, r.d)
         for _ in range(3):
             g.replay()
         torch.cuda.synchronize()
@@ -337,9 +470,21 @@ def main():
         line["graph"] = {"ms_per_step": round(tg * 1e3, 4), "tflops": round(6 * macs / tg / 1e12, 3),
                          "note": "forward + backward replayed from one HIP graph; no parse or plan"}
     if args.compare_ltr and path is None:
-        lt = compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args)
+        lt = compare_ltr(w, dtype, r.xs, r.d, ltr, flags, r.stream, r.cdt, args)
         lt["time_ratio_vs_optimal"] = round(lt["ms_per_step"] / (t_step * 1e3), 3)
         line["left_to_right"] = lt
+    default_run = (args.workload == "C2" and dtype == "f32" and path is None and
+                   not args.max_elements and not args.generic)
+    if not args.no_configs and default_run:
+        del r
+        torch.cuda.empty_cache()
+        cfgs = {}
+        for name, dt in CONFIGS:
+            if name == "C2" and dt == "f32":
+                continue
+            cfgs[name] = config_line(name, dt, max(20, args.steps), args.sample_steps)
+            print(f"config {name}: {cfgs[name]['ms_per_step']} ms", file=sys.stderr, flush=True)
+        line["configs"] = cfgs
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_batch, w.shapes[0][0]))
     print(json.dumps(line), flush=True)

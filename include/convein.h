@@ -46,10 +46,18 @@
  *    *_parse / *_create calls and released by the *_destroy calls.  After
  *    creation they are immutable: one plan may be used from several threads
  *    and streams at once provided each call gets its own workspace.
- *  - Errors: every call returns a ce_status; on failure nothing has been
- *    launched, outputs are untouched, out-parameters are left unset, and
- *    ce_last_error() returns a message (thread-local, valid until the next
- *    call on the same thread).  No C++ exception crosses this interface.
+ *  - Errors: every call returns a ce_status and, on failure, ce_last_error()
+ *    returns a message (thread-local, valid until the next call on the same
+ *    thread); out-parameters are left unset.  No C++ exception crosses this
+ *    interface.  Every argument, size and workspace check of ce_forward /
+ *    ce_backward happens before the first launch, so a call that fails with
+ *    any status other than CE_ERR_HIP has enqueued nothing and left outputs,
+ *    gradients and workspace untouched.  CE_ERR_HIP means the HIP runtime
+ *    refused a launch (or an event record) part-way through the call's
+ *    sequence: the launches before it stay enqueued on the stream and may
+ *    already have written part of the output, of the gradients and of the
+ *    workspace, none of the later ones is enqueued, and the contents of all
+ *    of them are undefined until a later call succeeds.
  */
 #ifndef CONVEIN_H
 #define CONVEIN_H
@@ -139,6 +147,11 @@ void ce_expr_destroy(ce_expr* e);
  * chain keeps its intermediates on chip and recomputes them there, so for
  * such a plan the flag changes nothing. */
 #define CE_FLAG_SAVE_INTERMEDIATES 0x4u
+/* Make every launch of the general contraction kernel use 64-bit element
+ * offsets and predicated loads, the code path it takes for operands beyond
+ * 2 GiB, even where 32-bit offsets would do (results are the same; this lets
+ * small inputs exercise the wide-offset path). */
+#define CE_FLAG_WIDE_OFFSETS 0x8u
 
 /* Choose the pairwise evaluation order with the fewest multiplications under
  * `mode` (Section 3.2, optimal sequencer; Appendix B tnn-cost), searching
@@ -202,7 +215,9 @@ void ce_plan_destroy(ce_plan* p);
  *   ws        device workspace of ws_bytes >= ce_plan_workspace_size(p, 0),
  *             256-byte aligned (may be NULL when the size is 0)
  *   stream    HIP stream; all work is enqueued asynchronously on it
- * Errors: CE_ERR_ARG, CE_ERR_WORKSPACE, CE_ERR_UNSUPPORTED, CE_ERR_HIP. */
+ * Errors: CE_ERR_ARG, CE_ERR_WORKSPACE, CE_ERR_UNSUPPORTED (nothing
+ * enqueued); CE_ERR_HIP (a launch failed part-way: the earlier launches stay
+ * enqueued, `out` and `ws` are undefined, see the conventions above). */
 ce_status ce_forward(const ce_plan* p, const void* const* in, void* out,
                      void* ws, size_t ws_bytes, ce_stream stream);
 

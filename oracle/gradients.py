@@ -96,8 +96,8 @@ def grads_pairwise(expr: Expr, arrays, tree, dy):
         vals[A + B] = c
         return c, A + B
 
-    if isinstance(tree, int):
-        raise ValueError("a single operand has no pairwise steps")
+    # a single operand (no pairwise step): its gradient is dy broadcast over
+    # the labels its pre-sum removed
     _, S = fwd(tree)
     lroot = kept_labels(expr, S)
     droot = np.transpose(np.asarray(dy, np.float64), [expr.output.index(l) for l in lroot])

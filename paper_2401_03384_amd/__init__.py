@@ -13,7 +13,8 @@ from .binding import (CeError, ce_backward, ce_expr_destroy, ce_expr_output_shap
                       ce_timing_end,
                       ce_timing_record, ce_version, lib, LIB_PATH,
                       CE_F32, CE_BF16, CE_COST_FWD, CE_COST_TRAIN_PAPER, CE_FLAG_GENERIC_ONLY,
-                      CE_FLAG_NO_FUSION, CE_FLAG_SAVE_INTERMEDIATES, CE_PAD_SAME_ZERO)
+                      CE_FLAG_NO_FUSION, CE_FLAG_SAVE_INTERMEDIATES, CE_FLAG_WIDE_OFFSETS,
+                      CE_PAD_SAME_ZERO)
 from .layer import GraphStep, Plan, plan, conv_einsum, contract_path
 
 __all__ = [
@@ -24,5 +25,5 @@ __all__ = [
     "ce_timing_begin", "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record",
     "ce_version", "lib", "LIB_PATH", "GraphStep", "Plan", "plan", "conv_einsum", "contract_path",
     "CE_F32", "CE_BF16", "CE_COST_FWD", "CE_COST_TRAIN_PAPER", "CE_FLAG_GENERIC_ONLY",
-    "CE_FLAG_NO_FUSION", "CE_FLAG_SAVE_INTERMEDIATES", "CE_PAD_SAME_ZERO",
+    "CE_FLAG_NO_FUSION", "CE_FLAG_SAVE_INTERMEDIATES", "CE_FLAG_WIDE_OFFSETS", "CE_PAD_SAME_ZERO",
 ]

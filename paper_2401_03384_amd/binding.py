@@ -29,6 +29,7 @@ CE_COST_TRAIN_PAPER = 1
 CE_FLAG_GENERIC_ONLY = 0x1
 CE_FLAG_NO_FUSION = 0x2
 CE_FLAG_SAVE_INTERMEDIATES = 0x4
+CE_FLAG_WIDE_OFFSETS = 0x8
 CE_PAD_SAME_ZERO = 0
 
 _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR_UNSUPPORTED",

@@ -949,7 +949,7 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
 }
 
 // ---- general contraction on MFMA tiles --------------------------------------
-bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
+bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out, bool wide) {
     if (!op.has_r || op.convs.size() > 2 || op.L.dtype != op.R.dtype) return false;
     // B is the operand whose positions mix an output and a reduction index
     int bside = -1;   // 0: L is B, 1: R is B
@@ -1108,7 +1108,7 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out) {
     };
     const int64_t esz = At.dtype == DT_BF16 ? 2 : 4, lim31 = (int64_t)1 << 31;
     const int64_t eA = extent(At), eB = extent(Bt), eC = extent(C);
-    d.off32 = eA * esz < lim31 && eB * esz < lim31 && eC < lim31 ? 1 : 0;
+    d.off32 = !wide && eA * esz < lim31 && eB * esz < lim31 && eC < lim31 ? 1 : 0;
     d.extA = eA * esz;
     d.extB = eB * esz;
     // k-major tile loads: the innermost reduction dim is unit-stride in A and
@@ -1166,7 +1166,7 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
     bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
                 (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
                  try_cred(op, scratch, out) || try_cconv(op, out) || try_thinw(op, scratch, out) ||
-                 try_tc(op, scratch, out));
+                 try_tc(op, scratch, out, (flags & CE_FLAG_WIDE_OFFSETS) != 0));
     if (!fast) {
         out.clear();
         Launch ln = lower_generic(op);

@@ -829,8 +829,8 @@ std::string describe_plan(const ce_plan& p) {
             << mask_str(p.nodes[st.b].mask) << "  macs " << st.macs << "\n";
     }
     txt << "  workspace fwd " << p.ws_fwd << " B, bwd " << p.ws_bwd << " B\n";
-    for (auto& l : p.fwd) txt << "  fwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
-    for (auto& l : p.bwd) txt << "  bwd kernel " << (l.kind & 0xff) << ": " << l.what << "\n";
+    for (auto& l : p.fwd) txt << "  fwd " << l.kname << ": " << l.what << "\n";
+    for (auto& l : p.bwd) txt << "  bwd " << l.kname << ": " << l.what << "\n";
     if (!p.executable) txt << "  not executable: " << p.why_not << "\n";
     return txt.str();
 }

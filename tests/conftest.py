@@ -49,4 +49,27 @@ PAPER_SHAPES = {
     "conv1d": [(2, 3, 11), (4, 3, 3)],
     "group_conv1d": [(2, 3, 2, 3), (2, 2, 2, 10)],
     "three_way_contraction": [(2, 3, 4), (3, 5, 3), (4, 4, 5)],
+    "interleaved_group_sec2": [(2, 2, 3, 9, 9), (2, 4, 3, 3), (3, 5, 3, 3)],
+    "group_conv2d": [(2, 3, 2, 3, 3), (2, 2, 2, 9, 9)],
+    "tensor_conv": [(5, 2, 3), (3, 2, 4)],
+    "contraction": [(3, 2, 4), (3, 5, 2)],
+    "outer": [(2, 3, 2), (2, 2, 3)],
+    "batch": [(2, 3, 4), (2, 3, 5)],
+}
+
+# The method's degenerate and edge cases: (string, operand shapes, designated
+# feature operand).  Section 3.1 case (5) pre-sums, a single operand, the
+# feature side held by the second operand, equal feature / filter sizes
+# resolved by the designated feature operand, even filter sizes.
+EDGE_CASES = {
+    "self_contraction": ("bsm,mt->bt", [(3, 4, 5), (5, 6)], 0),
+    "self_contraction_conv": ("bsmh,mth->bth|h", [(2, 3, 4, 9), (4, 5, 3)], 0),
+    "single_operand_sum": ("ijk->i", [(3, 4, 5)], 0),
+    "single_operand_permute": ("ijk->kji", [(3, 4, 5)], 0),
+    "feature_second": ("tsh,bsh->bth|h", [(4, 3, 3), (2, 3, 11)], 0),
+    "feature_second_2d": ("tshw,bshw->bthw|hw", [(4, 3, 3, 2), (2, 3, 9, 8)], 0),
+    "equal_sizes_feature0": ("bsh,tsh->bth|h", [(2, 3, 5), (4, 3, 5)], 0),
+    "equal_sizes_feature1": ("bsh,tsh->bth|h", [(2, 3, 5), (4, 3, 5)], 1),
+    "even_filter_conv": ("bshw,tshw->bthw|hw", [(2, 3, 9, 10), (4, 3, 4, 4)], 0),
+    "even_filter_cp": ("bshw,rs,rt,rh,rw->bthw|hw", [(2, 6, 9, 9), (3, 6), (3, 5), (3, 4), (3, 2)], 0),
 }

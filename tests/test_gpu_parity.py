@@ -1,8 +1,17 @@
 """GPU parity: the HIP path (through the C ABI) against the float64 oracle.
 
-Reduced sizes compare every element of Y and of every gradient with the
-oracle's pairwise evaluation; full sizes compare with the oracle's dense
-evaluation.  Bar: rel-L2 <= 1e-5 for float32, <= 2e-2 for bfloat16 inputs.
+Reduced sizes compare Y and every gradient with the oracle's pairwise
+evaluation along the same tree; full sizes compare with the oracle's dense
+evaluation.  Every comparison (`_check`) applies two bars with the same
+tolerance tol (1e-5 for float32, 2e-2 for bfloat16 inputs):
+
+  * the whole tensor:   ||y - ref||_2 <= tol * ||ref||_2  (rel-L2), and
+  * every element:      |y_i - ref_i| <= tol * max_j |ref_j|,
+
+and prints the worst element's index.  For a correct result the largest
+element error relative to max|ref| is about the rel-L2 error (both are set by
+the rounding of the same sums), far below tol; a wrongly computed element
+fails the second bar whenever its true value exceeds tol * max|ref|.
 """
 import sys
 
@@ -11,7 +20,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from conftest import PAPER_SHAPES, load_layer_strings
+from conftest import EDGE_CASES, PAPER_SHAPES, load_layer_strings
 
 STRINGS = load_layer_strings()
 
@@ -47,6 +56,30 @@ def _say(*a):
     sys.stdout.flush()
 
 
+def _check(what, got, ref, tol):
+    """rel-L2 <= tol over the tensor and |got - ref| <= tol * max|ref| for
+    every element; prints both and the worst element (NaN fails both)."""
+    g = _host(got) if torch.is_tensor(got) else np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert g.shape == ref.shape, (what, g.shape, ref.shape)
+    d = np.abs(g - ref)
+    scale = max(float(np.abs(ref).max()), 1e-300)
+    i = int(np.argmax(d)) if d.size else 0
+    worst = float(d.ravel()[i]) / scale if d.size else 0.0
+    rel = _rel(g, ref)
+    idx = tuple(int(x) for x in np.unravel_index(i, ref.shape)) if d.size else ()
+    _say(f"  {what}: rel-L2 {rel:.3e}  worst element {idx} |err|/max|ref| {worst:.3e}")
+    assert rel <= tol, (what, "rel-L2", rel, tol)
+    assert worst <= tol, (what, "element", idx, worst, tol)
+
+
+def _check_all(name, y, y_ref, grads, g_ref, tol):
+    _check(f"{name} Y", y, y_ref, tol)
+    for i, (g, r) in enumerate(zip(grads, g_ref)):
+        if g is not None:
+            _check(f"{name} d{i}", g, r, tol)
+
+
 PARITY = sorted(W.PARITY_WORKLOADS)
 
 
@@ -65,15 +98,14 @@ def test_parity_reduced(P, name, generic):
     xs = [_dev(a, bf16) for a in ins]
     y = plan.forward(xs)
     torch.cuda.synchronize()
-    assert _rel(_host(y), y_ref) <= tol
+    _check(f"{name} Y", y, y_ref, tol)
     if not w.backward:
         return
     g_ref = O.grads_pairwise(e, ins, tree, dy)
     grads = plan.backward(xs, _dev(dy, bf16))
     torch.cuda.synchronize()
     for i, (g, r) in enumerate(zip(grads, g_ref)):
-        err = _rel(_host(g), r)
-        assert err <= tol, (name, i, err)
+        _check(f"{name} d{i}", g, r, tol)
 
 
 @pytest.mark.parametrize("name", ["C2s", "C3s_f32", "C5bs"])
@@ -114,8 +146,8 @@ def test_autograd_function(P):
     y.backward(_dev(dy, False))
     e = O.bind(O.parse(w.spec), w.shapes)
     g_ref = O.grads_dense(e, ins, dy)
-    for x, r in zip(xs, g_ref):
-        assert _rel(_host(x.grad), r) <= 1e-5
+    for i, (x, r) in enumerate(zip(xs, g_ref)):
+        _check(f"autograd d{i}", x.grad, r, 1e-5)
 
 
 FULL = ["C1", "C2", "C2_bf16", "C3", "C4", "C5a", "C5b"]
@@ -134,9 +166,7 @@ def test_parity_full_size(P, name):
     xs = [_dev(a, bf16) for a in ins]
     y = plan.forward(xs)
     torch.cuda.synchronize()
-    err = _rel(_host(y), O.eval_dense(e, ins))
-    _say(f"  Y rel-L2 {err:.3e}")
-    assert err <= tol
+    _check(f"{name} Y", y, O.eval_dense(e, ins), tol)
     del y
     if not w.backward:
         return
@@ -144,9 +174,7 @@ def test_parity_full_size(P, name):
     torch.cuda.synchronize()
     g_ref = O.grads_dense(e, ins, dy)
     for i, (g, r) in enumerate(zip(grads, g_ref)):
-        err = _rel(_host(g), r)
-        _say(f"  grad {i} rel-L2 {err:.3e}")
-        assert err <= tol, (name, i, err)
+        _check(f"{name} d{i}", g, r, tol)
 
 
 @pytest.mark.parametrize("name", ["C2s", "C3s", "C4s", "C5as_f32", "C5bs"])
@@ -166,10 +194,7 @@ def test_saved_intermediates(P, name):
     y = plan.forward(xs, workspace=ws)
     grads = plan.backward(xs, _dev(dy, bf16), workspace=ws)
     torch.cuda.synchronize()
-    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
-    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
-        err = _rel(_host(g), r)
-        assert err <= tol, (name, i, err)
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -202,10 +227,7 @@ def test_paper_layer_strings(P, name, dtype):
     y = plan.forward(xs)
     grads = plan.backward(xs, _dev(dy, bf16))
     torch.cuda.synchronize()
-    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
-    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
-        err = _rel(_host(g), r)
-        assert err <= tol, (name, i, err)
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
 
 
 @pytest.mark.parametrize("name", ["C4s", "C5as", "C5bs"])
@@ -227,10 +249,7 @@ def test_memory_limited_plan(P, name):
     y = plan.forward(xs)
     grads = plan.backward(xs, _dev(dy, bf16))
     torch.cuda.synchronize()
-    assert _rel(_host(y), O.eval_pairwise(e, ins, tree)) <= tol
-    for i, (g, r) in enumerate(zip(grads, O.grads_pairwise(e, ins, tree, dy))):
-        err = _rel(_host(g), r)
-        assert err <= tol, (name, i, err)
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
 
 
 @pytest.mark.parametrize("name", ["C1", "C2s", "C3s", "C5as"])
@@ -261,3 +280,98 @@ def test_graph_replay(P, name):
         # eager work between replays
         plan.forward(xs)
         torch.cuda.synchronize()
+
+
+def _random_case(spec, shapes, dtype, feat=0, seed=7):
+    """Seeded N(0,1) operands and dY for a small case, rounded to the storage
+    type; the oracle expression bound with the same feature operand."""
+    bf16 = dtype == "bf16"
+    e = O.bind(O.parse(spec), shapes, feature_operand=feat)
+    rng = np.random.default_rng(seed)
+    rnd = (lambda a: W.round_to_bf16(a.astype(np.float32))) if bf16 else (lambda a: a.astype(np.float32))
+    ins = [rnd(rng.standard_normal(s)).astype(np.float64) for s in shapes]
+    out_shape = tuple(e.out_sizes[l] for l in e.output)
+    dy = rnd(rng.standard_normal(out_shape)).astype(np.float64)
+    return e, ins, dy
+
+
+@pytest.mark.parametrize("generic", [False, True], ids=["default", "generic"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(EDGE_CASES))
+def test_edge_cases(P, name, dtype, generic):
+    """Pre-summed labels, single operands, the feature operand second, equal
+    feature / filter sizes with a designated feature operand, even filters:
+    forward and every gradient against the oracle along the same tree."""
+    spec, shapes, feat = EDGE_CASES[name]
+    bf16 = dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} {dtype} generic={generic} {spec} shapes={shapes} feature={feat}")
+    e, ins, dy = _random_case(spec, shapes, dtype, feat)
+    plan = P.Plan(spec, shapes, dtype, feature_operand=feat,
+                  flags=P.CE_FLAG_GENERIC_ONLY if generic else 0)
+    assert tuple(plan.out_shape) == dy.shape
+    tree = O.optimal_tree(e)[0]
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+
+
+LTR = ["C2s", "C2s_bf16", "C3s", "C4s", "C5bs", "C5as_f32"]
+
+
+@pytest.mark.parametrize("name", LTR)
+def test_left_to_right_plan(P, name):
+    """The paper's baseline order (((X, A), B), ...) on the same kernels,
+    against the oracle evaluated along the left-to-right tree."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    n = len(w.shapes)
+    path = [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)]
+    _say(f"case {name} left-to-right path {path}")
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.left_to_right_tree(n)
+    plan = P.Plan(w.spec, w.shapes, w.dtype, path=path)
+    assert [(a, b) for a, b, _ in plan.steps][0] == (1, 2)
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+
+
+@pytest.mark.parametrize("name,ltr", [("C2s", True), ("C2s_bf16", True), ("C4s", False),
+                                      ("C3s", False), ("C5as_f32", True)])
+def test_wide_offsets(P, name, ltr):
+    """CE_FLAG_WIDE_OFFSETS: the general contraction kernel's 64-bit offset
+    path (used for operands beyond 2 GiB) at small sizes, against the oracle
+    and bit-equal to the 32-bit path."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    n = len(w.shapes)
+    path = [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)] if ltr else None
+    tree = O.left_to_right_tree(n) if ltr else None
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    if tree is None:
+        tree = O.optimal_tree(e)[0]
+    flags = P.CE_FLAG_NO_FUSION
+    wide = P.Plan(w.spec, w.shapes, w.dtype, path=path, flags=flags | P.CE_FLAG_WIDE_OFFSETS)
+    narrow = P.Plan(w.spec, w.shapes, w.dtype, path=path, flags=flags)
+    assert "tc_gemm" in wide.describe(), "no launch of the general contraction kernel"
+    _say(f"case {name} wide offsets, tree {tree}")
+    xs = [_dev(a, bf16) for a in ins]
+    d = _dev(dy, bf16)
+    y = wide.forward(xs)
+    grads = wide.backward(xs, d)
+    y2 = narrow.forward(xs)
+    grads2 = narrow.backward(xs, d)
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+    assert torch.equal(y, y2)
+    for a, b in zip(grads, grads2):
+        assert torch.equal(a, b)

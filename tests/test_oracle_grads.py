@@ -99,3 +99,46 @@ def test_tucker_gradients_match_torch_autograd():
     ours = O.grads_dense(e, [X, Ui, G, Uo], dy)
     for a, t in zip(ours, tt):
         np.testing.assert_allclose(a, t.grad.numpy(), rtol=1e-11, atol=1e-11)
+
+
+EDGE = [
+    ("ijk->i", [(3, 4, 5)], 0),                 # one operand: a pre-sum only
+    ("ijk->kji", [(2, 3, 4)], 0),               # one operand: a transpose
+    ("bsm,mt->bt", [(2, 3, 4), (4, 5)], 0),     # s summed away before the step
+    ("tsh,bsh->bth|h", [(3, 2, 3), (2, 2, 7)], 0),   # the feature operand second
+    ("bsh,tsh->bth|h", [(2, 2, 5), (3, 2, 5)], 1),   # equal sizes, feature operand 1
+    ("bshw,tshw->bthw|hw", [(1, 2, 6, 5), (2, 2, 4, 2)], 0),   # even filters
+]
+
+
+@pytest.mark.parametrize("spec,shapes,feat", EDGE, ids=[c[0] for c in EDGE])
+def test_finite_differences_edge_cases(spec, shapes, feat):
+    """The method's degenerate cases (Section 3.1 case (5) pre-sums, single
+    operands, feature side second or chosen on equal sizes, even filters):
+    pairwise gradients against central differences of the plain definition."""
+    e = O.bind(O.parse(spec), shapes, feature_operand=feat)
+    g = np.random.default_rng(11)
+    arr = [g.standard_normal(s) for s in shapes]
+    y = O.eval_definition(e, arr)
+    dy = g.standard_normal(y.shape)
+    t = O.optimal_tree(e)[0]
+    np.testing.assert_allclose(O.eval_pairwise(e, arr, t), y, rtol=1e-12, atol=1e-12)
+    grads = O.grads_pairwise(e, arr, t, dy)
+    eps = 1e-6
+    for i, a in enumerate(arr):
+        for idx in list(np.ndindex(*a.shape))[::max(1, a.size // 12)]:
+            ap = [x.copy() for x in arr]
+            am = [x.copy() for x in arr]
+            ap[i][idx] += eps
+            am[i][idx] -= eps
+            fd = ((O.eval_definition(e, ap) - O.eval_definition(e, am)) * dy).sum() / (2 * eps)
+            assert abs(fd - grads[i][idx]) <= 1e-7 * max(1.0, abs(fd)), (i, idx)
+
+
+def test_single_operand_gradient_is_a_broadcast():
+    """Y[i] = sum_jk X[i,j,k]: dL/dX[i,j,k] = dY[i] for every j, k."""
+    e = O.bind(O.parse("ijk->i"), [(3, 4, 5)])
+    x = np.random.default_rng(3).standard_normal((3, 4, 5))
+    dy = np.array([1.5, -2.0, 0.25])
+    (gx,) = O.grads_pairwise(e, [x], 0, dy)
+    assert np.array_equal(gx, np.broadcast_to(dy[:, None, None], (3, 4, 5)))
