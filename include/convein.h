@@ -236,6 +236,30 @@ ce_status ce_forward(const ce_plan* p, const void* const* in, void* out,
 ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
                       void* const* din, void* ws, size_t ws_bytes, ce_stream stream);
 
+/* Workspace bytes that ce_backward_noalloc provides. */
+#define CE_NOALLOC_WORKSPACE_BYTES (64u << 20)
+
+/* ce_backward for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * The same launches as ce_backward, with the workspace taken from a fixed
+ * device array of CE_NOALLOC_WORKSPACE_BYTES (64 MiB) that the library holds
+ * on every GPU it runs on until the process ends; nothing is allocated.  The
+ * array's device address is looked up on the first call on a device.
+ *   in, dout, din   as ce_backward
+ *   stream          must belong to the current device (NULL: the default
+ *                   stream of the current device)
+ * Every call on one GPU uses the same array, which keeps the contents the
+ * last call left: calls that can overlap on one GPU (other streams, other
+ * threads, without ordering between them) race on it; calls ordered on one
+ * stream do not.  No part of the array has to start at any value: every
+ * launch writes what a later launch of the same call reads.
+ * Errors: as ce_backward; CE_ERR_WORKSPACE when ce_plan_workspace_size(p, 1)
+ * exceeds CE_NOALLOC_WORKSPACE_BYTES; CE_ERR_UNSUPPORTED for a plan created
+ * with CE_FLAG_SAVE_INTERMEDIATES (its backward reads the forward's
+ * workspace); CE_ERR_ARG when the stream belongs to another device. */
+ce_status ce_backward_noalloc(const ce_plan* p, const void* const* in, const void* dout,
+                              void* const* din, ce_stream stream);
+
 /* ---- launch timing (profiling harnesses) ---------------------------------- */
 
 /* Start recording on the calling thread: every kernel that ce_forward /

@@ -30,6 +30,7 @@ CE_FLAG_GENERIC_ONLY = 0x1
 CE_FLAG_NO_FUSION = 0x2
 CE_FLAG_SAVE_INTERMEDIATES = 0x4
 CE_FLAG_WIDE_OFFSETS = 0x8
+CE_NOALLOC_WORKSPACE_BYTES = 64 << 20
 CE_PAD_SAME_ZERO = 0
 
 _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR_UNSUPPORTED",
@@ -42,7 +43,7 @@ EXPORTS = [
     "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_with_path", "ce_plan_num_steps",
     "ce_plan_step",
     "ce_plan_cost", "ce_plan_left_to_right_cost", "ce_plan_workspace_size", "ce_plan_describe",
-    "ce_plan_destroy", "ce_forward", "ce_backward", "ce_timing_begin", "ce_timing_begin_kernel",
+    "ce_plan_destroy", "ce_forward", "ce_backward", "ce_backward_noalloc", "ce_timing_begin", "ce_timing_begin_kernel",
     "ce_timing_end", "ce_timing_record", "ce_last_error", "ce_version",
 ]
 
@@ -87,6 +88,7 @@ def lib():
         L.ce_plan_destroy.restype = None
         L.ce_forward.argtypes = [vp, C.POINTER(vp), vp, vp, C.c_size_t, vp]
         L.ce_backward.argtypes = [vp, C.POINTER(vp), vp, C.POINTER(vp), vp, C.c_size_t, vp]
+        L.ce_backward_noalloc.argtypes = [vp, C.POINTER(vp), vp, C.POINTER(vp), vp]
         L.ce_timing_begin.argtypes = []
         L.ce_timing_begin_kernel.argtypes = [C.c_char_p]
         L.ce_timing_end.argtypes = [C.POINTER(C.c_int)]
@@ -230,6 +232,12 @@ def ce_backward(p: int, in_ptrs, dout_ptr: int, din_ptrs, ws_ptr: int, ws_bytes:
     arr = _ptr_array(tuple(in_ptrs))
     darr = _ptr_array(tuple(d or None for d in din_ptrs))
     _check(lib().ce_backward(p, arr, dout_ptr, darr, ws_ptr or None, ws_bytes, stream or None))
+
+
+def ce_backward_noalloc(p: int, in_ptrs, dout_ptr: int, din_ptrs, stream: int) -> None:
+    arr = _ptr_array(tuple(in_ptrs))
+    darr = _ptr_array(tuple(d or None for d in din_ptrs))
+    _check(lib().ce_backward_noalloc(p, arr, dout_ptr, darr, stream or None))
 
 
 def ce_timing_begin() -> None:

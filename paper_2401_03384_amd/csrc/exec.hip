@@ -2,6 +2,7 @@
 // and enqueues the plan's launches on the caller's stream.  No host
 // synchronisation, no device allocation.
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -193,26 +194,94 @@ extern "C" ce_status ce_forward(const ce_plan* p, const void* const* in, void* o
     });
 }
 
+namespace ce {
+namespace {
+
+// Checks of a backward call; returns the bitmask of wanted gradients.
+uint32_t check_backward(const ce_plan* p, const void* const* in, const void* dout, void* const* din) {
+    if (!p || !in || !dout || !din) fail(CE_ERR_ARG, "NULL plan, inputs, dout or din");
+    if (!p->executable) fail(CE_ERR_UNSUPPORTED, p->why_not);
+    uint32_t wanted = 0;
+    for (int i = 0; i < p->e.n; i++) {
+        if (!in[i]) fail(CE_ERR_ARG, "input " + std::to_string(i) + " is NULL");
+        if (din[i]) wanted |= 1u << i;
+    }
+    return wanted;
+}
+
+void run_backward(const ce_plan* p, const void* const* in, const void* dout, void* const* din,
+                  uint32_t wanted, void* ws, hipStream_t s) {
+    if (!wanted) return;
+    Ptrs P{in, nullptr, dout, din, ws};
+    for (const Launch& ln : p->bwd) {
+        if (ln.need && !(ln.need & wanted)) continue;
+        hipError_t err = run_launch(ln, P, s);
+        if (err != hipSuccess)
+            fail(CE_ERR_HIP, std::string("kernel launch failed (") + ln.what + "): " +
+                                 hipGetErrorString(err));
+    }
+}
+
+// ---- workspace of the allocation-free backward ------------------------------
+// A fixed device array (one copy on every GPU the library's code object is
+// loaded on, held until the process ends).  Host code never uses the array's
+// name as an address: its device address is looked up once per device, with
+// that device current, and kept in scratch_addr.
+static __device__ __align__(256) unsigned char scratch[CE_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on that device).
+void* scratch_addr(hipStream_t s) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) fail(CE_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) fail(CE_ERR_UNSUPPORTED, "device index beyond 63");
+    if (s) {
+        int sdev = -1;
+        e = hipStreamGetDevice(s, &sdev);
+        if (e != hipSuccess) fail(CE_ERR_HIP, std::string("hipStreamGetDevice: ") + hipGetErrorString(e));
+        if (sdev != dev) fail(CE_ERR_ARG, "the stream belongs to another device than the current one");
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            fail(CE_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        g_scratch_addr[dev] = ptr;
+    }
+    return g_scratch_addr[dev];
+}
+
+}  // namespace
+}  // namespace ce
+
 extern "C" ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
                                  void* const* din, void* ws, size_t ws_bytes, ce_stream stream) {
     return guard([&] {
-        if (!p || !in || !dout || !din) fail(CE_ERR_ARG, "NULL plan, inputs, dout or din");
-        if (!p->executable) fail(CE_ERR_UNSUPPORTED, p->why_not);
-        uint32_t wanted = 0;
-        for (int i = 0; i < p->e.n; i++) {
-            if (!in[i]) fail(CE_ERR_ARG, "input " + std::to_string(i) + " is NULL");
-            if (din[i]) wanted |= 1u << i;
-        }
+        const uint32_t wanted = check_backward(p, in, dout, din);
         check_ws(p, p->ws_bwd, ws, ws_bytes);
-        if (!wanted) return;
-        Ptrs P{in, nullptr, dout, din, ws};
+        run_backward(p, in, dout, din, wanted, ws, (hipStream_t)stream);
+    });
+}
+
+extern "C" ce_status ce_backward_noalloc(const ce_plan* p, const void* const* in, const void* dout,
+                                         void* const* din, ce_stream stream) {
+    return guard([&] {
+        const uint32_t wanted = check_backward(p, in, dout, din);
+        if (p->flags & CE_FLAG_SAVE_INTERMEDIATES)
+            fail(CE_ERR_UNSUPPORTED, "a plan with CE_FLAG_SAVE_INTERMEDIATES reads the forward's workspace");
+        if (p->ws_bwd > (size_t)CE_NOALLOC_WORKSPACE_BYTES)
+            fail(CE_ERR_WORKSPACE, "the backward needs " + std::to_string(p->ws_bwd) +
+                                       " B of workspace, more than the " +
+                                       std::to_string((size_t)CE_NOALLOC_WORKSPACE_BYTES) +
+                                       " B the allocation-free entry point holds");
         hipStream_t s = (hipStream_t)stream;
-        for (const Launch& ln : p->bwd) {
-            if (ln.need && !(ln.need & wanted)) continue;
-            hipError_t err = run_launch(ln, P, s);
-            if (err != hipSuccess)
-                fail(CE_ERR_HIP, std::string("kernel launch failed (") + ln.what + "): " +
-                                     hipGetErrorString(err));
-        }
+        void* ws = scratch_addr(s);
+        run_backward(p, in, dout, din, wanted, ws, s);
     });
 }

@@ -381,3 +381,28 @@ def test_conv_contraction_kernel_selected(name, steps):
         assert any(s in l for l in on36), (name, s, text)
     assert len(on36) == len(steps), (name, on36)
     assert not any("grad rhs" in l for l in on36)
+
+
+def test_noalloc_backward_rejects_before_any_launch():
+    """ce_backward_noalloc's checks (no device work happens on these paths):
+    a backward workspace beyond CE_NOALLOC_WORKSPACE_BYTES, a plan that saves
+    intermediates, NULL arguments."""
+    w = W.WORKLOADS["C4"]
+    p = _plan(w.spec, w.shapes)
+    assert B.ce_plan_workspace_size(p, 1) > B.CE_NOALLOC_WORKSPACE_BYTES
+    fake = [0x1000 * (i + 1) for i in range(len(w.shapes))]
+    with pytest.raises(B.CeError) as ex:
+        B.ce_backward_noalloc(p, fake, 0x9000, fake, 0)
+    assert ex.value.status == B.CE_ERR_WORKSPACE
+    B.ce_plan_destroy(p)
+    w = W.PARITY_WORKLOADS["C2s"]
+    e = B.ce_expr_parse(w.spec, w.shapes)
+    p = B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, B.CE_FLAG_SAVE_INTERMEDIATES | B.CE_FLAG_NO_FUSION)
+    B.ce_expr_destroy(e)
+    with pytest.raises(B.CeError) as ex:
+        B.ce_backward_noalloc(p, fake, 0x9000, fake, 0)
+    assert ex.value.status == B.CE_ERR_UNSUPPORTED
+    with pytest.raises(B.CeError) as ex:
+        B.ce_backward_noalloc(p, fake, 0, fake, 0)
+    assert ex.value.status == B.CE_ERR_ARG
+    B.ce_plan_destroy(p)
