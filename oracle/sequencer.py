@@ -92,12 +92,17 @@ def max_intermediate(expr, t) -> int:
     return max(sizes, default=0)
 
 
-def optimal_tree(expr, mode: str = "fwd", return_all: bool = False, max_elements=None):
+def optimal_tree(expr, mode: str = "fwd", return_all: bool = False, max_elements=None,
+                 max_step_cost=None):
     """Cheapest tree by exhaustive search, ties broken by the smallest key.
 
-    With `max_elements`, only trees whose every intermediate holds at most
-    that many elements compete (the memory-limited order of Section 3.2,
-    Figure 2); (None, None) when no tree qualifies."""
+    With `max_step_cost`, only trees in which every pairwise step (every
+    internal node) costs at most that much under `mode` compete: the path
+    that meets a user-given cost cap at each node (Section 3.2, Figure 2,
+    the orange path).  With `max_elements`, only trees whose every
+    intermediate holds at most that many elements compete (a memory limit on
+    the intermediates, the other reading of the same trade-off).
+    (None, None) when no tree qualifies."""
     memo = {}
 
     def sc(a, b):
@@ -111,9 +116,17 @@ def optimal_tree(expr, mode: str = "fwd", return_all: bool = False, max_elements
             return 0
         return cost(t[0]) + cost(t[1]) + sc(_mask(t[0]), _mask(t[1]))
 
+    def steps_within(t):
+        if isinstance(t, int):
+            return True
+        return (sc(_mask(t[0]), _mask(t[1])) <= max_step_cost and steps_within(t[0])
+                and steps_within(t[1]))
+
     best, best_cost, ties = None, None, []
     for t in all_trees(range(expr.n)):
         if max_elements is not None and max_intermediate(expr, t) > max_elements:
+            continue
+        if max_step_cost is not None and not steps_within(t):
             continue
         c = cost(t)
         if best_cost is None or c < best_cost:

@@ -260,3 +260,65 @@ def test_intermediate_size_matches_pairwise_evaluation():
     assert O.intermediate_size(e, (1, 2)) == 4 * 5 * 6          # Us x Ut outer over r
     assert O.intermediate_size(e, (3, 4)) == 4 * 3 * 2          # Kh x Kw
     assert O.max_intermediate(e, ((((0, 1), 3), 4), 2)) == 2 * 4 * 9 * 7
+
+
+def _chain_dp_step_cap(p, cap):
+    """Matrix-chain interval DP (Cormen et al., Sec. 15.2) in which every
+    multiplication of two sub-chain products may cost at most `cap`
+    (p[i] * p[k+1] * p[j+1]); least total, None when nothing fits."""
+    n = len(p) - 1
+    INF = float("inf")
+    m = [[0 if i == j else INF for j in range(n)] for i in range(n)]
+    for length in range(2, n + 1):
+        for i in range(n - length + 1):
+            j = i + length - 1
+            for k in range(i, j):
+                step = p[i] * p[k + 1] * p[j + 1]
+                if step <= cap:
+                    m[i][j] = min(m[i][j], m[i][k] + m[k + 1][j] + step)
+    return None if m[0][n - 1] == INF else m[0][n - 1]
+
+
+@pytest.mark.parametrize("cap", [10 ** 9, 5250, 5249, 4500, 3750, 3000, 2625, 2000])
+def test_cost_capped_matrix_chain(cap):
+    """The per-node cost cap of Section 3.2, Figure 2 (the orange path) on the
+    Cormen chain against an independent interval DP: same least total (or both
+    infeasible), every step of the returned tree within the cap, and the
+    unconstrained optimum whenever its largest step (A1 x (A2A3), 5250) fits."""
+    dims = [30, 35, 15, 5, 10, 20, 25]
+    labs = "abcdefg"
+    spec = ",".join(labs[i] + labs[i + 1] for i in range(6)) + "->ag"
+    e = _e(spec, [(dims[i], dims[i + 1]) for i in range(6)])
+    t, c = O.optimal_tree(e, max_step_cost=cap)
+    ref = _chain_dp_step_cap(dims, cap)
+    if ref is None:
+        assert t is None
+    else:
+        assert c == ref
+        assert max(O.step_costs(e, t)) <= cap
+    if cap >= 5250:
+        assert t == ((0, (1, 2)), ((3, 4), 5)) and c == 15125
+    else:
+        assert ref is None or ref > 15125
+
+
+@pytest.mark.parametrize("name", ["rtt_conv", "tr_conv", "cp_conv"])
+def test_cost_cap_on_layer_strings(name):
+    """Layer strings of Appendix A.3: with a cap one below the optimum's
+    largest step, the capped search returns the cheapest tree whose every step
+    fits, checked against every tree; where no tree has a smaller largest step
+    (the CP layer: some step always contracts X with U_s), it returns none."""
+    import conftest
+    spec = conftest.load_layer_strings()[name][0]
+    shapes = conftest.PAPER_SHAPES[name]
+    e = _e(spec, shapes)
+    t0, c0 = O.optimal_tree(e)
+    big = max(O.step_costs(e, t0))
+    t1, c1 = O.optimal_tree(e, max_step_cost=big - 1)
+    fits = [x for x in O.all_trees(range(e.n)) if max(O.step_costs(e, x)) <= big - 1]
+    if not fits:
+        assert (t1, c1) == (None, None)
+        return
+    assert c1 == min(O.tree_cost(e, x) for x in fits) and c1 > c0
+    assert max(O.step_costs(e, t1)) <= big - 1
+    assert O.optimal_tree(e, max_step_cost=big) == (t0, c0)
