@@ -338,6 +338,22 @@ class Runner:
         return t, roofline(records, self.dtype, share)
 
 
+def max_batch_line(w):
+    """Largest batch whose training step fits an HBM budget (planning only):
+    the planned order vs left-to-right with recomputation and left-to-right
+    keeping every intermediate (both unfused), as in the paper's
+    maximum-batch comparison; budgets: 11 GiB and 288 GB."""
+    import paper_2401_03384_amd as P
+    out = {}
+    for label, budget in (("11GiB", 11 << 30), ("288GB", 288 * 10 ** 9)):
+        out[label] = {
+            "optimal": P.max_batch(w.spec, w.shapes, budget, w.dtype),
+            "ltr_recompute": P.max_batch(w.spec, w.shapes, budget, w.dtype, "ltr", fusion=False),
+            "ltr_keep_all": P.max_batch(w.spec, w.shapes, budget, w.dtype, "ltr", save=True,
+                                        fusion=False)}
+    return out
+
+
 def config_line(name, dtype, steps, samples):
     """fwd+bwd figures of one configuration (see CONFIGS)."""
     import workloads as W
@@ -363,6 +379,7 @@ def config_line(name, dtype, steps, samples):
                         if k in roof}}
     if "frac_vs_mfma_peak" in roof:
         out["dominant"]["frac_vs_mfma_peak"] = roof["frac_vs_mfma_peak"]
+    out["max_batch"] = max_batch_line(r.w)
     del r
     import torch
     torch.cuda.empty_cache()
@@ -452,6 +469,7 @@ def main():
         "floor_us": round(floor, 1),
         "floor_frac": round(floor / (t_step * 1e6), 4),
         "workspace_bytes": {"fwd": ref.ws_fwd, "bwd": ref.ws_bwd},
+        "max_batch": max_batch_line(w),
         "fwd_ms": round(t_fwd * 1e3, 4),
         "bwd_ms": round(t_bwd * 1e3, 4),
         "plan_ms": round(t_plan * 1e3, 4),

@@ -173,6 +173,44 @@ ce_status ce_plan_create(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype,
 ce_status ce_plan_create_limited(const ce_expr* e, ce_cost_mode mode, ce_dtype dtype,
                                  unsigned flags, uint64_t max_elements, ce_plan** out);
 
+/* Options of ce_plan_create_ex.  A zero cap means no cap. */
+typedef struct {
+    ce_cost_mode mode;        /* cost model of the search and of max_step_cost */
+    ce_dtype dtype;
+    unsigned flags;           /* CE_FLAG_* */
+    /* Per-node cost cap (Section 3.2, Figure 2, the path meeting a cost cap
+     * c at each node): only orders in which every pairwise step costs at most
+     * max_step_cost under `mode` compete. */
+    uint64_t max_step_cost;
+    /* Every intermediate holds at most max_elements elements (as
+     * ce_plan_create_limited). */
+    uint64_t max_elements;
+    /* Checkpointing (Section 3.3): bytes of forward intermediates the
+     * backward may read instead of recomputing.  0 recomputes every
+     * intermediate (the default of the other entry points); otherwise the
+     * planner keeps the set of intermediates the forward writes that avoids
+     * the most recompute multiplications with at most save_budget bytes in
+     * total (ties: fewer bytes, then the lower step indices).  As with
+     * CE_FLAG_SAVE_INTERMEDIATES (which keeps every one, whatever the
+     * budget), ce_backward must then receive the workspace of the preceding
+     * ce_forward of the same inputs, unchanged; the kept intermediates sit at
+     * its start, and ce_plan_workspace_size(p, 1) covers the forward's size. */
+    uint64_t save_budget;
+} ce_plan_options;
+
+/* The optimal order under the options' caps, with the options'
+ * checkpointing choice.  Errors: as ce_plan_create; CE_ERR_UNSUPPORTED when
+ * no order meets the caps. */
+ce_status ce_plan_create_ex(const ce_expr* e, const ce_plan_options* opt, ce_plan** out);
+
+/* Checkpointing choice of a plan: bit s of saved_steps is set when the
+ * result of step s is kept from the forward for the backward; saved_bytes
+ * is their total size, recompute_macs the multiplications of the steps the
+ * backward recomputes (on chip for a fused chain).  Any out-pointer may be
+ * NULL. */
+ce_status ce_plan_checkpoint(const ce_plan* p, uint64_t* saved_steps, uint64_t* saved_bytes,
+                             uint64_t* recompute_macs);
+
 /* Same, with a caller-given order (e.g. the left-to-right baseline of
  * Section 5): `pairs` holds n_pairs = n_in - 1 pairs (i, j) of positions in
  * the current operand list; the merged tensor is appended to the end of the
@@ -254,9 +292,10 @@ ce_status ce_backward(const ce_plan* p, const void* const* in, const void* dout,
  * stream do not.  No part of the array has to start at any value: every
  * launch writes what a later launch of the same call reads.
  * Errors: as ce_backward; CE_ERR_WORKSPACE when ce_plan_workspace_size(p, 1)
- * exceeds CE_NOALLOC_WORKSPACE_BYTES; CE_ERR_UNSUPPORTED for a plan created
- * with CE_FLAG_SAVE_INTERMEDIATES (its backward reads the forward's
- * workspace); CE_ERR_ARG when the stream belongs to another device. */
+ * exceeds CE_NOALLOC_WORKSPACE_BYTES; CE_ERR_UNSUPPORTED for a plan whose
+ * backward reads intermediates kept in the forward's workspace
+ * (CE_FLAG_SAVE_INTERMEDIATES or a save budget, see ce_plan_checkpoint);
+ * CE_ERR_ARG when the stream belongs to another device. */
 ce_status ce_backward_noalloc(const ce_plan* p, const void* const* in, const void* dout,
                               void* const* din, ce_stream stream);
 

@@ -29,7 +29,8 @@ before and K-1-floor((K-1)/2) after; the output keeps the feature size.
 from .notation import Expr, parse, bind
 from .cost import step_cost, kept_labels, label_size, tree_cost, step_costs
 from .sequencer import (all_trees, optimal_tree, left_to_right_tree, leaves,
-                        post_order_steps, count_trees, intermediate_size, max_intermediate)
+                        post_order_steps, count_trees, intermediate_size, max_intermediate,
+                        checkpoint_choice)
 from .evaluate import eval_definition, eval_pairwise, eval_dense, dense_kernel
 from .gradients import grads_pairwise, grads_dense
 
@@ -37,6 +38,7 @@ __all__ = [
     "Expr", "parse", "bind", "step_cost", "kept_labels", "label_size",
     "tree_cost", "step_costs", "all_trees", "optimal_tree", "left_to_right_tree",
     "leaves", "post_order_steps", "count_trees", "intermediate_size", "max_intermediate",
+    "checkpoint_choice",
     "eval_definition",
     "eval_pairwise", "eval_dense", "dense_kernel", "grads_pairwise", "grads_dense",
 ]

@@ -190,3 +190,32 @@ def post_order_steps(t):
 
     rec(t)
     return out
+
+
+def checkpoint_choice(expr, tree, budget_bytes: int, elem_bytes: int, mode: str = "fwd"):
+    """Which intermediates to keep from the forward for the backward
+    (Section 3.3: keeping intermediates costs memory, recomputing them costs
+    multiplications).  Every intermediate (every step result but the last) is
+    a candidate; keeping the result of step s spares its recompute, step_cost
+    of that step.  Returns (set of kept step indices in post order, kept
+    bytes, multiplications still recomputed): the subset with the largest
+    spared cost whose bytes (elements x elem_bytes) fit the budget; ties go
+    to fewer bytes, then to the smaller bitmask of step indices."""
+    steps = post_order_steps(tree)
+    costs = []
+    sizes = []
+    for a, b in steps[:-1]:
+        la, lb = leaves(a), leaves(b)
+        costs.append(step_cost(expr, la, lb, mode))
+        sizes.append(intermediate_size(expr, tuple(la) + tuple(lb)) * elem_bytes)
+    best = None
+    for mask in range(1 << len(costs)):
+        kept = [s for s in range(len(costs)) if (mask >> s) & 1]
+        w = sum(sizes[s] for s in kept)
+        if w > budget_bytes:
+            continue
+        v = sum(costs[s] for s in kept)
+        key_ = (-v, w, mask)
+        if best is None or key_ < best[0]:
+            best = (key_, set(kept), w, sum(costs) - v)
+    return best[1], best[2], best[3]

@@ -40,12 +40,20 @@ _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR
 EXPORTS = [
     "ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
     "ce_expr_destroy",
-    "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_with_path", "ce_plan_num_steps",
+    "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_ex", "ce_plan_checkpoint",
+    "ce_plan_create_with_path", "ce_plan_num_steps",
     "ce_plan_step",
     "ce_plan_cost", "ce_plan_left_to_right_cost", "ce_plan_workspace_size", "ce_plan_describe",
     "ce_plan_destroy", "ce_forward", "ce_backward", "ce_backward_noalloc", "ce_timing_begin", "ce_timing_begin_kernel",
     "ce_timing_end", "ce_timing_record", "ce_last_error", "ce_version",
 ]
+
+
+class PlanOptions(C.Structure):
+    """ce_plan_options of include/convein.h."""
+    _fields_ = [("mode", C.c_int), ("dtype", C.c_int), ("flags", C.c_uint),
+                ("max_step_cost", C.c_uint64), ("max_elements", C.c_uint64),
+                ("save_budget", C.c_uint64)]
 
 
 class CeError(RuntimeError):
@@ -74,6 +82,9 @@ def lib():
         L.ce_expr_destroy.restype = None
         L.ce_plan_create.argtypes = [vp, C.c_int, C.c_int, C.c_uint, C.POINTER(vp)]
         L.ce_plan_create_limited.argtypes = [vp, C.c_int, C.c_int, C.c_uint, C.c_uint64, C.POINTER(vp)]
+        L.ce_plan_create_ex.argtypes = [vp, C.POINTER(PlanOptions), C.POINTER(vp)]
+        L.ce_plan_checkpoint.argtypes = [vp, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                         C.POINTER(C.c_uint64)]
         L.ce_plan_create_with_path.argtypes = [vp, C.POINTER(C.c_int), C.c_int, C.c_int, C.c_uint,
                                                C.POINTER(vp)]
         L.ce_plan_num_steps.argtypes = [vp, C.POINTER(C.c_int)]
@@ -98,7 +109,8 @@ def lib():
         L.ce_last_error.restype = C.c_char_p
         L.ce_version.restype = C.c_char_p
         for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
-                     "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_with_path",
+                     "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_ex", "ce_plan_checkpoint",
+    "ce_plan_create_with_path",
                      "ce_plan_num_steps",
                      "ce_plan_step", "ce_plan_cost", "ce_plan_left_to_right_cost",
                      "ce_plan_workspace_size", "ce_forward", "ce_backward", "ce_timing_begin",
@@ -174,6 +186,21 @@ def ce_plan_create_limited(e: int, mode: int, dtype: int, flags: int, max_elemen
     out = C.c_void_p()
     _check(lib().ce_plan_create_limited(e, mode, dtype, flags, max_elements, C.byref(out)))
     return out.value
+
+
+def ce_plan_create_ex(e: int, mode: int, dtype: int, flags: int, max_step_cost: int = 0,
+                      max_elements: int = 0, save_budget: int = 0) -> int:
+    opt = PlanOptions(mode, dtype, flags, max_step_cost, max_elements, save_budget)
+    out = C.c_void_p()
+    _check(lib().ce_plan_create_ex(e, C.byref(opt), C.byref(out)))
+    return out.value
+
+
+def ce_plan_checkpoint(p: int):
+    """(saved step bitmask, saved bytes, recompute multiplications)."""
+    a, b, c = C.c_uint64(), C.c_uint64(), C.c_uint64()
+    _check(lib().ce_plan_checkpoint(p, C.byref(a), C.byref(b), C.byref(c)))
+    return a.value, b.value, c.value
 
 
 def ce_plan_create_with_path(e: int, pairs, dtype: int = CE_F32, flags: int = 0) -> int:

@@ -79,7 +79,30 @@ ce_status ce_plan_create_limited(const ce_expr* e, ce_cost_mode mode, ce_dtype d
                                  uint64_t max_elements, ce_plan** out) {
     return guard([&] {
         if (!e || !out) fail(CE_ERR_ARG, "NULL argument");
-        *out = make_plan(*e, mode, dtype, flags, false, nullptr, 0, max_elements);
+        PlanLimits lim;
+        lim.max_elements = max_elements;
+        *out = make_plan(*e, mode, dtype, flags, false, nullptr, 0, lim);
+    });
+}
+
+ce_status ce_plan_create_ex(const ce_expr* e, const ce_plan_options* opt, ce_plan** out) {
+    return guard([&] {
+        if (!e || !opt || !out) fail(CE_ERR_ARG, "NULL argument");
+        PlanLimits lim;
+        if (opt->max_elements) lim.max_elements = opt->max_elements;
+        if (opt->max_step_cost) lim.max_step_cost = opt->max_step_cost;
+        lim.save_budget = opt->save_budget;
+        *out = make_plan(*e, opt->mode, opt->dtype, opt->flags, false, nullptr, 0, lim);
+    });
+}
+
+ce_status ce_plan_checkpoint(const ce_plan* p, uint64_t* saved_steps, uint64_t* saved_bytes,
+                             uint64_t* recompute_macs) {
+    return guard([&] {
+        if (!p) fail(CE_ERR_ARG, "plan is NULL");
+        if (saved_steps) *saved_steps = p->save_mask;
+        if (saved_bytes) *saved_bytes = p->saved_bytes;
+        if (recompute_macs) *recompute_macs = p->recompute_macs;
     });
 }
 

@@ -273,8 +273,8 @@ extern "C" ce_status ce_backward_noalloc(const ce_plan* p, const void* const* in
                                          void* const* din, ce_stream stream) {
     return guard([&] {
         const uint32_t wanted = check_backward(p, in, dout, din);
-        if (p->flags & CE_FLAG_SAVE_INTERMEDIATES)
-            fail(CE_ERR_UNSUPPORTED, "a plan with CE_FLAG_SAVE_INTERMEDIATES reads the forward's workspace");
+        if (p->save_mask)
+            fail(CE_ERR_UNSUPPORTED, "the plan's backward reads intermediates from the forward's workspace");
         if (p->ws_bwd > (size_t)CE_NOALLOC_WORKSPACE_BYTES)
             fail(CE_ERR_WORKSPACE, "the backward needs " + std::to_string(p->ws_bwd) +
                                        " B of workspace, more than the " +

@@ -140,10 +140,12 @@ struct Builder {
     // ---- search ---------------------------------------------------------
     // Cheapest split of every operand set (subset DP).  With a limit, a set
     // other than the whole expression whose merged tensor exceeds `limit`
-    // elements is infeasible, and so is every split that uses one; returns
-    // false when the whole expression has no feasible split.
+    // elements is infeasible, and so is every split that uses one; a split
+    // whose own step costs more than `step_cap` is not taken (the per-node
+    // cost cap of Section 3.2, Figure 2).  Returns false when the whole
+    // expression has no feasible split.
     bool optimal_splits(uint64_t* best_cost, std::vector<uint32_t>& split,
-                        uint64_t limit = ~uint64_t(0)) {
+                        uint64_t limit = ~uint64_t(0), uint64_t step_cap = ~uint64_t(0)) {
         uint32_t full = (n >= 32) ? 0xffffffffu : ((1u << n) - 1);
         std::vector<uint64_t> best(size_t(full) + 1, 0);
         std::vector<char> feasible(size_t(full) + 1, 1);
@@ -161,7 +163,12 @@ struct Builder {
             for (uint32_t sub = rest;; sub = (sub - 1) & rest) {
                 uint32_t A = sub | low, B = S ^ A;
                 if (B && feasible[A] && feasible[B]) {
-                    uint64_t c = add_sat(add_sat(best[A], best[B]), step_cost_sat(e, A, B, p.mode));
+                    const uint64_t sc = step_cost_sat(e, A, B, p.mode);
+                    if (sc > step_cap) {
+                        if (!sub) break;
+                        continue;
+                    }
+                    uint64_t c = add_sat(add_sat(best[A], best[B]), sc);
                     if (!found || c < bc || (c == bc && A < bA)) {
                         bc = c;
                         bA = A;
@@ -523,7 +530,7 @@ uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) 
 }
 
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
-                   bool use_path, const int* pairs, int n_pairs, uint64_t max_elements) {
+                   bool use_path, const int* pairs, int n_pairs, const PlanLimits& lim) {
     if (!e.bound) fail(CE_ERR_ARG, "expression is not bound");
     if (mode != CE_COST_FWD && mode != CE_COST_TRAIN_PAPER) fail(CE_ERR_ARG, "bad cost mode");
     if (dtype != CE_F32 && dtype != CE_BF16) fail(CE_ERR_ARG, "bad dtype");
@@ -543,9 +550,11 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
         } else {
             uint64_t best;
             std::vector<uint32_t> split;
-            if (!bld.optimal_splits(&best, split, max_elements))
+            if (!bld.optimal_splits(&best, split, lim.max_elements, lim.max_step_cost))
                 fail(CE_ERR_UNSUPPORTED, "no pairwise order keeps every intermediate within " +
-                                             std::to_string(max_elements) + " elements");
+                                             std::to_string(lim.max_elements) +
+                                             " elements and every step within cost " +
+                                             std::to_string(lim.max_step_cost));
             bld.build_tree((n >= 32) ? 0xffffffffu : ((1u << n) - 1), split);
         }
     }
@@ -624,8 +633,7 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             WsItem it;
             it.bytes = (size_t)bld.tensor_of(c, dt, {}).numel() * elem(dt);
             it.t0 = s;
-            // saved for the backward: live to the end (never shared)
-            it.t1 = (flags & CE_FLAG_SAVE_INTERMEDIATES) ? (1 << 30) : consumer_step(c);
+            it.t1 = consumer_step(c);
             it.id = c;
             items.push_back(it);
         }
@@ -666,7 +674,66 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             if (fuse_rcp_forward(*p, rf)) p->fwd.assign(1, rf);
         }
         drop_unused(items, p->fwd);
-        p->ws_fwd = pack(items);
+        // Checkpointing (Section 3.3): the intermediates the forward writes
+        // may be kept for the backward instead of recomputed there; all of
+        // them with CE_FLAG_SAVE_INTERMEDIATES, else the set that avoids the
+        // most recompute multiplications within the save budget.
+        std::vector<int> cand;   // steps whose result the forward writes
+        for (int s = 0; s + 1 < m; s++)
+            for (const WsItem& it : items)
+                if (it.id == p->steps[s].c) cand.push_back(s);
+        auto node_bytes = [&](int s) {
+            return (uint64_t)bld.tensor_of(p->steps[s].c, dt, {}).numel() * elem(dt);
+        };
+        uint32_t save = 0;
+        if (flags & CE_FLAG_SAVE_INTERMEDIATES) {
+            for (int s : cand) save |= 1u << s;
+        } else if (lim.save_budget > 0) {
+            const size_t k = cand.size();
+            uint64_t best_v = 0, best_w = 0;
+            uint32_t best_m = 0;
+            for (uint32_t sub = 0; sub < (1u << k); sub++) {
+                uint64_t v = 0, w = 0;
+                uint32_t msk = 0;
+                for (size_t j = 0; j < k; j++)
+                    if ((sub >> j) & 1) {
+                        v += p->steps[cand[j]].macs;
+                        w += node_bytes(cand[j]);
+                        msk |= 1u << cand[j];
+                    }
+                if (w > lim.save_budget) continue;
+                if (v > best_v || (v == best_v && (w < best_w || (w == best_w && msk < best_m)))) {
+                    best_v = v;
+                    best_w = w;
+                    best_m = msk;
+                }
+            }
+            save = best_m;
+        }
+        p->save_mask = save;
+        p->saved_bytes = 0;
+        p->recompute_macs = 0;
+        for (int s : cand) {
+            if ((save >> s) & 1) p->saved_bytes += node_bytes(s);
+        }
+        auto saved_node = [&](int id) {
+            for (int s = 0; s + 1 < m; s++)
+                if (((save >> s) & 1) && p->steps[s].c == id) return true;
+            return false;
+        };
+        // kept intermediates first, back to back; the rest of the forward's
+        // items (and later the backward's own) packed after them
+        std::vector<WsItem> kept, rest;
+        for (const WsItem& it : items) (saved_node(it.id) ? kept : rest).push_back(it);
+        size_t base = 0;
+        for (WsItem& it : kept) {
+            it.offset = base;
+            base += align256(it.bytes);
+        }
+        p->ws_fwd = base + pack(rest);
+        for (WsItem& it : rest) it.offset += base;
+        items = rest;
+        items.insert(items.end(), kept.begin(), kept.end());
         patch(p->fwd, items);
 
         // ---------------- backward ----------------
@@ -751,16 +818,24 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.what = "unary bwd";
             for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
         }
-        // intermediates the forward left in the workspace (plans that keep
-        // any: a fused chain keeps none)
-        const bool saved = (flags & CE_FLAG_SAVE_INTERMEDIATES) && !fused_bwd && !items.empty();
-        if (saved) {
-            std::vector<WsItem> kept;
-            for (const WsItem& it : bitems)
-                if (it.id >= GRAD_ID) kept.push_back(it);
-            bitems.swap(kept);
+        // intermediates the forward left in the workspace are read there (a
+        // fused backward recomputes on chip and reads none)
+        if (fused_bwd) {
+            p->save_mask = save = 0;
+            p->saved_bytes = 0;
+            kept.clear();
+            base = 0;
+            for (int s = 0; s + 1 < m; s++) p->recompute_macs += p->steps[s].macs;
         }
-        for (int s = 0; !fused_bwd && !saved && s + 1 < m; s++) {
+        if (save) {
+            std::vector<WsItem> own;
+            for (const WsItem& it : bitems)
+                if (!saved_node(it.id)) own.push_back(it);
+            bitems.swap(own);
+        }
+        for (int s = 0; !fused_bwd && s + 1 < m; s++) {
+            if ((save >> s) & 1) continue;
+            p->recompute_macs += p->steps[s].macs;
             const Step& st = p->steps[s];
             PairOp op;
             op.L = bval(st.a);
@@ -803,13 +878,13 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
         }
         drop_unused(bitems, p->bwd);
         p->ws_bwd = pack(bitems);
-        if (saved) {
-            // the backward's own items after the forward's region; the saved
-            // intermediates at their forward offsets
-            for (WsItem& it : bitems) it.offset += p->ws_fwd;
-            p->ws_bwd += p->ws_fwd;
-            for (const WsItem& it : items)
-                if (it.id < GRAD_ID) bitems.push_back(it);
+        if (save) {
+            // the backward's own items after the kept intermediates, which
+            // stay at their forward offsets; the backward's size covers the
+            // forward's, so one buffer serves both calls
+            for (WsItem& it : bitems) it.offset += base;
+            p->ws_bwd = std::max(p->ws_bwd + base, p->ws_fwd);
+            bitems.insert(bitems.end(), kept.begin(), kept.end());
         }
         patch(p->bwd, bitems);
     }

@@ -92,6 +92,11 @@ struct ce_plan {
     uint64_t total_cost = 0, fwd_macs = 0, ltr_cost = 0;
     std::vector<ce::Launch> fwd, bwd;
     size_t ws_fwd = 0, ws_bwd = 0;
+    // intermediates the forward keeps for the backward (bit s: the result of
+    // step s), their bytes, and the multiplications of the recompute steps
+    // the backward still runs
+    uint32_t save_mask = 0;
+    uint64_t saved_bytes = 0, recompute_macs = 0;
     bool executable = true;
     std::string why_not;
     // description, built once on first request (plans are shared across threads)
@@ -101,11 +106,18 @@ struct ce_plan {
 
 namespace ce {
 
+// Limits of the search and the checkpointing choice of a plan.
+struct PlanLimits {
+    uint64_t max_elements = ~uint64_t(0);    // every intermediate's elements
+    uint64_t max_step_cost = ~uint64_t(0);   // every step's cost in the plan's mode
+    uint64_t save_budget = 0;                // bytes of intermediates kept for the backward
+};
+
 // Build a plan: the optimal order when use_path is false, else the order
 // given by `pairs` (opt_einsum path format, n_pairs = n_in - 1).
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
                    bool use_path, const int* pairs, int n_pairs,
-                   uint64_t max_elements = ~uint64_t(0));
+                   const PlanLimits& lim = PlanLimits());
 
 // Text description of a plan (steps, costs, workspace, launches).
 std::string describe_plan(const ce_plan& p);

@@ -5,6 +5,7 @@ stream; every step of the computation runs in the library's HIP kernels.
 """
 from __future__ import annotations
 
+import math
 import threading
 
 import torch
@@ -21,10 +22,15 @@ class Plan:
 
     `path` (optional) is an opt_einsum-style list of pairs replacing the
     optimal order (e.g. the left-to-right baseline); `max_elements` (optional)
-    caps the elements of every intermediate (the cheapest order that fits)."""
+    caps the elements of every intermediate and `max_step_cost` the cost of
+    every pairwise step (the cheapest order that fits); `save_budget`
+    (bytes) lets the backward read that much of the forward's intermediates
+    instead of recomputing them (the backward must then get the forward's
+    workspace, see `forward(..., workspace=)`)."""
 
     def __init__(self, spec: str, shapes, dtype: str = "f32", mode: str = "fwd", flags: int = 0,
-                 path=None, feature_operand: int = 0, max_elements=None):
+                 path=None, feature_operand: int = 0, max_elements=None, max_step_cost=None,
+                 save_budget=None):
         if dtype not in _DT:
             raise ValueError(f"dtype must be one of {list(_DT)}")
         self.spec = spec
@@ -38,7 +44,11 @@ class Plan:
             if feature_operand:
                 B.ce_expr_set_feature(self._expr, feature_operand)
             self.out_shape = B.ce_expr_output_shape(self._expr)
-            if path is None and max_elements is not None:
+            if path is None and (max_step_cost is not None or save_budget is not None):
+                self._plan = B.ce_plan_create_ex(self._expr, _MODE[mode], _DT[dtype], flags,
+                                                 int(max_step_cost or 0), int(max_elements or 0),
+                                                 int(save_budget or 0))
+            elif path is None and max_elements is not None:
                 self._plan = B.ce_plan_create_limited(self._expr, _MODE[mode], _DT[dtype], flags,
                                                       int(max_elements))
             elif path is None:
@@ -53,6 +63,7 @@ class Plan:
         self.total_cost, self.fwd_macs = B.ce_plan_cost(self._plan)
         self.ws_fwd = B.ce_plan_workspace_size(self._plan, 0)
         self.ws_bwd = B.ce_plan_workspace_size(self._plan, 1)
+        self.saved_steps, self.saved_bytes, self.recompute_macs = B.ce_plan_checkpoint(self._plan)
 
     def __del__(self):
         if getattr(self, "_plan", None):
@@ -209,3 +220,56 @@ def contract_path(spec: str, *shapes, mode: str = "fwd", max_elements=None):
     info = {"total_cost": p.total_cost, "fwd_macs": p.fwd_macs,
             "left_to_right_cost": p.left_to_right_cost(), "text": p.describe()}
     return p.steps, info
+
+
+def step_bytes(p: Plan) -> int:
+    """Device bytes one forward + backward of plan `p` holds: operands,
+    output and output gradient, operand gradients, and one workspace serving
+    both passes."""
+    e = 2 if p.dtype == "bf16" else 4
+    ins = sum(math.prod(s) for s in p.shapes) * e
+    out = 2 * math.prod(p.out_shape) * e
+    grads = sum(math.prod(s) * (e if i == p.feature_operand else 4) for i, s in enumerate(p.shapes))
+    return ins + out + grads + max(p.ws_fwd, p.ws_bwd)
+
+
+def max_batch(spec: str, shapes, budget_bytes: int, dtype: str = "f32", order: str = "optimal",
+              save: bool = False, fusion: bool = True, batch=((0, 0),), limit: int = 1 << 20) -> int:
+    """Largest batch size whose training step (step_bytes) fits in
+    budget_bytes: the one-layer analogue of the maximum-batch comparison of
+    Section 5 (Table 3).  `batch` lists the (operand, axis) pairs that carry
+    the batch size; order "optimal" is the planned order, "ltr" the
+    left-to-right baseline; save=True keeps every intermediate for the
+    backward (no checkpointing); fusion=False materialises every pairwise
+    result (one launch per step, as an evaluation without fused chains does).
+    0 when even a batch of one does not fit."""
+    n = len(shapes)
+    path = None
+    if order == "ltr":
+        path = [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)]
+    elif order != "optimal":
+        raise ValueError("order must be 'optimal' or 'ltr'")
+    flags = (B.CE_FLAG_SAVE_INTERMEDIATES if save else 0) | (0 if fusion else B.CE_FLAG_NO_FUSION)
+
+    def fits(bs):
+        shp = [list(s) for s in shapes]
+        for i, ax in batch:
+            shp[i][ax] = bs
+        try:
+            return step_bytes(Plan(spec, shp, dtype, flags=flags, path=path)) <= budget_bytes
+        except B.CeError:
+            return False
+
+    if not fits(1):
+        return 0
+    lo, hi = 1, 2
+    while hi <= limit and fits(hi):
+        lo, hi = hi, hi * 2
+    hi = min(hi, limit + 1)
+    while hi - lo > 1:     # fits(lo), not fits(hi)
+        mid = (lo + hi) // 2
+        if fits(mid):
+            lo = mid
+        else:
+            hi = mid
+    return lo

@@ -1362,7 +1362,9 @@ extern "C" {
 // Cap on every intermediate's elements for the plans emul_run builds
 // (0: none; the memory-limited order of ce_plan_create_limited).
 static uint64_t g_limit = 0;
+static uint64_t g_save_budget = 0;
 void emul_set_limit(uint64_t max_elements) { g_limit = max_elements; }
+void emul_set_save_budget(uint64_t bytes) { g_save_budget = bytes; }
 
 // Runs the forward (mode 0), backward (mode 1) or forward then backward on
 // one workspace (mode 2) launch lists of a plan built with `flags`
@@ -1374,8 +1376,11 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
     const int generic_only = flags & CE_FLAG_GENERIC_ONLY;
     try {
         std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
+        PlanLimits lim;
+        if (g_limit) lim.max_elements = g_limit;
+        lim.save_budget = g_save_budget;
         std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32, (unsigned)flags,
-                                             false, nullptr, 0, g_limit ? g_limit : ~uint64_t(0)));
+                                             false, nullptr, 0, lim));
         if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
         Ctx c;
         int es = bf16 ? 2 : 4;

@@ -406,3 +406,89 @@ def test_noalloc_backward_rejects_before_any_launch():
         B.ce_backward_noalloc(p, fake, 0, fake, 0)
     assert ex.value.status == B.CE_ERR_ARG
     B.ce_plan_destroy(p)
+
+
+@pytest.mark.parametrize("frac", [0.0, 0.3, 0.7, 1.0])
+@pytest.mark.parametrize("name", ["C1", "C2s", "C3s", "C4s", "C5bs"])
+def test_checkpoint_choice_matches_oracle(name, frac):
+    """ce_plan_create_ex with a save budget keeps the same intermediates as
+    the oracle's keep-or-recompute choice (Section 3.3), with the same bytes
+    and remaining recompute multiplications; the backward's workspace covers
+    the forward's whenever anything is kept."""
+    w = W.PARITY_WORKLOADS[name]
+    elem = 2 if w.dtype == "bf16" else 4
+    e = O.bind(O.parse(w.spec), w.shapes)
+    t = O.optimal_tree(e)[0]
+    total = O.checkpoint_choice(e, t, 10 ** 18, elem)[1]
+    budget = int(frac * total)
+    x = B.ce_expr_parse(w.spec, w.shapes)
+    p = B.ce_plan_create_ex(x, B.CE_COST_FWD, B.CE_BF16 if elem == 2 else B.CE_F32,
+                            B.CE_FLAG_NO_FUSION, save_budget=budget)
+    B.ce_expr_destroy(x)
+    try:
+        mask, nbytes, rec = B.ce_plan_checkpoint(p)
+        kept, wb, rest = O.checkpoint_choice(e, t, budget, elem)
+        assert mask == sum(1 << s for s in kept)
+        assert (nbytes, rec) == (wb, rest)
+        if mask:
+            assert B.ce_plan_workspace_size(p, 1) >= B.ce_plan_workspace_size(p, 0) >= nbytes
+    finally:
+        B.ce_plan_destroy(p)
+
+
+@pytest.mark.parametrize("name", ["C2s", "C4s", "C5bs", "rtt_conv", "tr_conv"])
+def test_cost_cap_plan_matches_oracle(name):
+    """ce_plan_create_ex with a per-step cost cap (Section 3.2, Figure 2)
+    returns the oracle's capped tree, or CE_ERR_UNSUPPORTED when the oracle
+    finds none."""
+    if name in PAPER_SHAPES:
+        w = W.Workload(name, STRINGS[name][0], tuple(PAPER_SHAPES[name]), "f32", 0, (), ())
+    else:
+        w = W.PARITY_WORKLOADS[name]
+    e = O.bind(O.parse(w.spec), w.shapes)
+    t0 = O.optimal_tree(e)[0]
+    steps0 = O.step_costs(e, t0)
+    for cap in sorted(set(steps0), reverse=True)[:3] + [max(steps0) - 1, min(steps0)]:
+        tree, cost = O.optimal_tree(e, max_step_cost=cap)
+        x = B.ce_expr_parse(w.spec, w.shapes)
+        try:
+            if tree is None:
+                with pytest.raises(B.CeError) as ex:
+                    B.ce_plan_create_ex(x, B.CE_COST_FWD, B.CE_F32, 0, max_step_cost=cap)
+                assert ex.value.status == B.CE_ERR_UNSUPPORTED
+                continue
+            p = B.ce_plan_create_ex(x, B.CE_COST_FWD, B.CE_F32, 0, max_step_cost=cap)
+        finally:
+            B.ce_expr_destroy(x)
+        try:
+            assert _steps(p) == _oracle_steps(e, tree), (name, cap)
+            assert B.ce_plan_cost(p)[0] == cost
+        finally:
+            B.ce_plan_destroy(p)
+
+
+@pytest.mark.parametrize("name", ["C2", "C4", "C5b"])
+def test_max_batch(name):
+    """The one-layer analogue of the paper's maximum-batch table (Section 5,
+    Table 3) under an 11 GiB budget: the returned batch fits and one more
+    does not, and the planned order admits at least the batch of the
+    left-to-right order with recomputation, which admits at least that of
+    left-to-right keeping every intermediate (both unfused)."""
+    import paper_2401_03384_amd as P
+    w = W.WORKLOADS[name]
+    budget = 11 << 30
+    opt = P.max_batch(w.spec, w.shapes, budget, w.dtype)
+    ckpt = P.max_batch(w.spec, w.shapes, budget, w.dtype, "ltr", fusion=False)
+    keep = P.max_batch(w.spec, w.shapes, budget, w.dtype, "ltr", save=True, fusion=False)
+    assert opt >= ckpt >= keep >= 1
+
+    def need(bs, **kw):
+        shp = [list(s) for s in w.shapes]
+        shp[0][0] = bs
+        return P.step_bytes(P.Plan(w.spec, shp, w.dtype, **kw))
+
+    assert need(opt) <= budget < need(opt + 1)
+    n = len(w.shapes)
+    ltr = [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)]
+    assert need(keep, path=ltr, flags=B.CE_FLAG_SAVE_INTERMEDIATES | B.CE_FLAG_NO_FUSION) <= budget
+    assert need(keep + 1, path=ltr, flags=B.CE_FLAG_SAVE_INTERMEDIATES | B.CE_FLAG_NO_FUSION) > budget

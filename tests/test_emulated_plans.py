@@ -250,3 +250,26 @@ def test_emulated_memory_limited(emul, name):
     assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
     for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
         assert _rel(a, b) <= tol
+
+
+@pytest.mark.parametrize("name,flags", [("C2s", 0x2), ("C3t", 0), ("C4t", 0), ("C5at_f32", 0),
+                                        ("C5br", 0x2)])
+def test_emulated_save_budget(emul, name, flags):
+    """Checkpointing under a save budget (half the intermediates' bytes):
+    the forward keeps the chosen intermediates, the backward reads them and
+    recomputes the rest on one bounds-checked workspace; vs the oracle."""
+    w = CASES[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    total = O.checkpoint_choice(e, tree, 10 ** 18, 2 if bf16 else 4)[1]
+    emul.emul_set_save_budget(C.c_uint64(total // 2))
+    try:
+        y, g = _run_saved(emul, w.spec, w.shapes, bf16, ins, dy, w.out_shape, flags)
+    finally:
+        emul.emul_set_save_budget(C.c_uint64(0))
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= tol

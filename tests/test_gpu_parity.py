@@ -375,3 +375,49 @@ def test_wide_offsets(P, name, ltr):
     assert torch.equal(y, y2)
     for a, b in zip(grads, grads2):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("name,nofuse", [("C2s", True), ("C3s", False), ("C4s", False),
+                                         ("C5bs", True), ("C5as_f32", False)])
+def test_save_budget(P, name, nofuse):
+    """Checkpointing under a save budget (Section 3.3): the forward keeps the
+    chosen intermediates in the workspace, the backward reads them and
+    recomputes the rest; against the oracle."""
+    w = W.PARITY_WORKLOADS[name]
+    bf16 = w.dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes)
+    tree = O.optimal_tree(e)[0]
+    total = O.checkpoint_choice(e, tree, 10 ** 18, 2 if bf16 else 4)[1]
+    flags = P.CE_FLAG_NO_FUSION if nofuse else 0
+    plan = P.Plan(w.spec, w.shapes, w.dtype, flags=flags, save_budget=total // 2)
+    _say(f"case {name} save budget {total // 2} of {total} B: kept steps {plan.saved_steps:#x}, "
+         f"{plan.saved_bytes} B, recompute {plan.recompute_macs} MACs")
+    assert plan.saved_steps != 0
+    xs = [_dev(a, bf16) for a in ins]
+    ws = plan.workspace(True, xs[0].device)
+    y = plan.forward(xs, workspace=ws)
+    grads = plan.backward(xs, _dev(dy, bf16), workspace=ws)
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+
+
+@pytest.mark.parametrize("name", ["rtt_conv", "tr_conv"])
+def test_cost_capped_plan(P, name):
+    """A per-step cost cap one below the optimum's largest step (Section 3.2,
+    Figure 2) forces another order; it runs on the same kernels and matches
+    the oracle along the oracle's capped tree."""
+    spec, shapes = STRINGS[name][0], PAPER_SHAPES[name]
+    e, ins, dy = _random_case(spec, shapes, "f32")
+    t0 = O.optimal_tree(e)[0]
+    cap = max(O.step_costs(e, t0)) - 1
+    tree, _ = O.optimal_tree(e, max_step_cost=cap)
+    assert tree is not None and tree != t0
+    plan = P.Plan(spec, shapes, "f32", max_step_cost=cap)
+    _say(f"case {name} step cost cap {cap}: tree {tree}")
+    xs = [_dev(a, False) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, False))
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), 1e-5)

@@ -322,3 +322,40 @@ def test_cost_cap_on_layer_strings(name):
     assert c1 == min(O.tree_cost(e, x) for x in fits) and c1 > c0
     assert max(O.step_costs(e, t1)) <= big - 1
     assert O.optimal_tree(e, max_step_cost=big) == (t0, c0)
+
+
+def test_checkpoint_choice_hand_values():
+    """Keep-or-recompute choice on the tiny CP layer (Section 3.3), hand
+    values: the planned tree's intermediates are Z1 = X*Us, Z2 = Z1 conv Kh,
+    Z3 = Z2 conv Kw, each [b=2, r=8, 8, 8] = 1024 elements (4096 B in fp32),
+    spared recompute costs 16384, 3072 and 3072 multiplications."""
+    e = _e("bshw,rs,rt,rh,rw->bthw|hw", [(2, 16, 8, 8), (8, 16), (8, 16), (8, 3), (8, 3)])
+    t = O.optimal_tree(e)[0]
+    assert O.checkpoint_choice(e, t, 0, 4) == (set(), 0, 16384 + 3072 + 3072)
+    assert O.checkpoint_choice(e, t, 4095, 4) == (set(), 0, 22528)
+    assert O.checkpoint_choice(e, t, 4096, 4) == ({0}, 4096, 6144)
+    # two fit: Z1 and the lower-indexed of the two equal conv results
+    assert O.checkpoint_choice(e, t, 8192 + 100, 4) == ({0, 1}, 8192, 3072)
+    assert O.checkpoint_choice(e, t, 10 ** 9, 4) == ({0, 1, 2}, 12288, 0)
+    # bf16 halves the bytes
+    assert O.checkpoint_choice(e, t, 4096, 2) == ({0, 1}, 4096, 3072)
+
+
+def test_checkpoint_choice_is_the_best_subset():
+    """Against a direct scan of every subset of the tensor-train layer's
+    intermediates: no subset within the budget spares more."""
+    import conftest
+    spec = conftest.load_layer_strings()["rtt_conv"][0]
+    e = _e(spec, conftest.PAPER_SHAPES["rtt_conv"])
+    t = O.optimal_tree(e)[0]
+    steps = O.post_order_steps(t)[:-1]
+    sizes = [O.intermediate_size(e, O.leaves(a) + O.leaves(b)) * 4 for a, b in steps]
+    costs = [O.step_cost(e, O.leaves(a), O.leaves(b)) for a, b in steps]
+    for budget in [0, min(sizes), sum(sizes) // 2, sum(sizes) - 1, sum(sizes)]:
+        kept, w, rest = O.checkpoint_choice(e, t, budget, 4)
+        assert w <= budget and w == sum(sizes[s] for s in kept)
+        assert rest == sum(costs) - sum(costs[s] for s in kept)
+        best = max(sum(c for c, k in zip(costs, m) if k)
+                   for m in itertools.product([0, 1], repeat=len(steps))
+                   if sum(s for s, k in zip(sizes, m) if k) <= budget)
+        assert sum(costs) - rest == best
