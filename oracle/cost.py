@@ -29,6 +29,10 @@ side a convolved label counts (output size) * (filter size); for the
 gradient of the filter side it counts (feature size) * (output size), as in
 the Appendix B example cost(g1) = BHWX'Y'TS, cost(g2) = BXYX'Y'TS.  With
 same padding the output size equals the feature size.
+
+A strided convolved label (stride s) has ceil(I / s) output positions; a step
+that convolves it counts (output size) * (filter size), the multiplications
+it does (I * J for s = 1), and the merged tensor holds the output size.
 """
 from __future__ import annotations
 
@@ -50,7 +54,17 @@ def kept_labels(expr: Expr, subset):
     return res
 
 
+def stride_of(expr: Expr, label) -> int:
+    return (expr.stride or {}).get(label, 1)
+
+
 def label_size(expr: Expr, subset, label):
+    """Size of `label` in the tensor merging the operands in `subset`: the
+    largest size among them, except a strided convolved label once both of
+    its holders are merged, which has ceil(I / s) output positions."""
+    s = stride_of(expr, label)
+    if s > 1 and all(i in subset for i in expr.holders(label)):
+        return -(-expr.sizes[expr.feature[label]][label] // s)
     return max(expr.sizes[i][label] for i in subset if label in expr.inputs[i])
 
 
@@ -66,29 +80,28 @@ def step_cost(expr: Expr, A, B, mode: str = "fwd") -> int:
     A, B = set(A), set(B)
     la, lb = kept_labels(expr, A), kept_labels(expr, B)
     plain = 1
-    both = []          # (feature size, filter size, feature on A?)
+    both = []          # (feature size, filter size, feature on A?, output size)
     for l in la + [x for x in lb if x not in la]:
         if l in la and l in lb and l in expr.conv:
             ia, ib = label_size(expr, A, l), label_size(expr, B, l)
             if _feature_side_is_a(expr, A, B, l):
-                both.append((ia, ib, True))
+                both.append((ia, ib, True, -(-ia // stride_of(expr, l))))
             else:
-                both.append((ib, ia, False))
+                both.append((ib, ia, False, -(-ib // stride_of(expr, l))))
         elif l in la:
             plain *= label_size(expr, A, l)
         else:
             plain *= label_size(expr, B, l)
     f = plain
-    for feat, filt, _ in both:
-        f *= feat * filt
+    for feat, filt, _, out in both:
+        f *= out * filt
     if mode == "fwd":
         return f
     if mode != "train_paper":
         raise ValueError(mode)
     ga = plain   # gradient w.r.t. the operand on side A
     gb = plain
-    for feat, filt, fa in both:
-        out = feat                      # same padding
+    for feat, filt, fa, out in both:
         if fa:
             ga *= out * filt
             gb *= feat * out

@@ -26,7 +26,7 @@ import itertools
 
 import numpy as np
 
-from .cost import kept_labels, label_size
+from .cost import kept_labels, label_size, stride_of
 from .notation import Expr
 
 
@@ -44,35 +44,39 @@ def _einsum(letters, a, la, b, lb, lc):
     return np.einsum(sub, a, b, optimize=True)
 
 
-def shift(a, axis, tap, K):
-    """out[p] = a[p + tap - floor((K-1)/2)] (zero where that index leaves the
-    array): the feature operand as seen by filter tap `tap`."""
+def shift(a, axis, tap, K, stride=1):
+    """out[p] = a[stride*p + tap - floor((K-1)/2)] for p in [0, ceil(n/stride))
+    (zero where that index leaves the array): the feature operand as seen by
+    filter tap `tap`."""
     n = a.shape[axis]
-    off = tap - (K - 1) // 2
-    out = np.zeros_like(a)
-    lo, hi = max(0, -off), min(n, n - off)
-    if lo < hi:
-        dst = [slice(None)] * a.ndim
-        src = [slice(None)] * a.ndim
-        dst[axis] = slice(lo, hi)
-        src[axis] = slice(lo + off, hi + off)
-        out[tuple(dst)] = a[tuple(src)]
+    m = -(-n // stride)
+    p = np.arange(m)
+    q = stride * p + tap - (K - 1) // 2
+    ok = (q >= 0) & (q < n)
+    shape = list(a.shape)
+    shape[axis] = m
+    out = np.zeros(shape, dtype=np.float64)
+    dst = [slice(None)] * a.ndim
+    dst[axis] = p[ok]
+    out[tuple(dst)] = np.take(a, q[ok], axis=axis)
     return out
 
 
-def shift_adjoint(g, axis, tap, K):
-    """Adjoint of shift(): out[q] = g[q - tap + floor((K-1)/2)], zero where
-    that index leaves the array."""
-    n = g.shape[axis]
-    off = -(tap - (K - 1) // 2)
-    out = np.zeros_like(g)
-    lo, hi = max(0, -off), min(n, n - off)
-    if lo < hi:
-        dst = [slice(None)] * g.ndim
-        src = [slice(None)] * g.ndim
-        dst[axis] = slice(lo, hi)
-        src[axis] = slice(lo + off, hi + off)
-        out[tuple(dst)] = g[tuple(src)]
+def shift_adjoint(g, axis, tap, K, n=None, stride=1):
+    """Adjoint of shift() for a feature of length n (default: g's length):
+    out[stride*p + tap - floor((K-1)/2)] = g[p] where that index lies in
+    [0, n), zero elsewhere (distinct p give distinct positions)."""
+    m = g.shape[axis]
+    n = m if n is None else n
+    p = np.arange(m)
+    q = stride * p + tap - (K - 1) // 2
+    ok = (q >= 0) & (q < n)
+    shape = list(g.shape)
+    shape[axis] = n
+    out = np.zeros(shape, dtype=np.float64)
+    dst = [slice(None)] * g.ndim
+    dst[axis] = q[ok]
+    out[tuple(dst)] = np.take(g, p[ok], axis=axis)
     return out
 
 
@@ -107,12 +111,12 @@ def pair_step(expr, letters, a, A, b, B):
         for (l, fa), k in zip(convs, combo):
             if fa:
                 K = label_size(expr, B, l)
-                xa = shift(xa, ca.index(l), k, K)
+                xa = shift(xa, ca.index(l), k, K, stride_of(expr, l))
                 xb = np.take(xb, k, axis=cb.index(l))
                 cb.remove(l)
             else:
                 K = label_size(expr, A, l)
-                xb = shift(xb, cb.index(l), k, K)
+                xb = shift(xb, cb.index(l), k, K, stride_of(expr, l))
                 xa = np.take(xa, k, axis=ca.index(l))
                 ca.remove(l)
         term = _einsum(letters, xa, ca, xb, cb, lc)
@@ -163,8 +167,9 @@ def eval_pairwise(expr: Expr, arrays, tree, keep_intermediates: bool = False):
 def eval_definition(expr: Expr, arrays):
     """Y[o] = sum over every label not in the output and over the taps of
     each convolved label of the product of all operands' entries; the feature
-    operand of a convolved label is read at p + k - c (zero outside), its
-    filter operand at tap k, the output at p."""
+    operand of a convolved label is read at s*p + k - c (zero outside; s the
+    label's stride, 1 unless given), its filter operand at tap k, the output
+    at p."""
     conv2 = {l: expr.feature[l] for l in expr.conv if l in expr.feature}
     for l in expr.conv:
         if len(expr.holders(l)) > 2:
@@ -193,7 +198,7 @@ def eval_definition(expr: Expr, arrays):
                     for l in labs:
                         if l in conv2:
                             if i == conv2[l]:
-                                pos = ov[l] + kv[l] - (K[l] - 1) // 2
+                                pos = stride_of(expr, l) * ov[l] + kv[l] - (K[l] - 1) // 2
                                 if pos < 0 or pos >= expr.sizes[i][l]:
                                     prod = 0.0
                                     break
@@ -232,7 +237,8 @@ def dense_kernel(expr: Expr, arrays, feature_operand: int = 0):
 
 def eval_dense(expr: Expr, arrays, feature_operand: int = 0):
     """Y = X (*) W_dense: zero-pad X along each convolved label, then add one
-    einsum per filter tap over the shifted window."""
+    einsum per filter tap over the shifted window (every s-th position for a
+    label of stride s)."""
     W, lw = dense_kernel(expr, arrays, feature_operand)
     X = np.asarray(arrays[feature_operand], np.float64)
     lx = list(expr.inputs[feature_operand])
@@ -255,7 +261,10 @@ def eval_dense(expr: Expr, arrays, feature_operand: int = 0):
         win = [slice(None)] * X.ndim
         widx = [slice(None)] * W.ndim
         for l, k in zip(convs, combo):
-            win[lx.index(l)] = slice(k, k + X.shape[lx.index(l)])
+            # padded position s*p + k for the output positions p
+            s = stride_of(expr, l)
+            m = expr.out_sizes[l]
+            win[lx.index(l)] = slice(k, k + s * (m - 1) + 1, s)
             widx[lw.index(l)] = k
         term = _einsum(letters, Xp[tuple(win)], lx, W[tuple(widx)], lw_red, expr.output)
         Y = term if Y is None else Y + term

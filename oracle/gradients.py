@@ -21,7 +21,7 @@ import itertools
 
 import numpy as np
 
-from .cost import kept_labels, label_size
+from .cost import kept_labels, label_size, stride_of
 from .evaluate import (_letters, _einsum, shift, shift_adjoint, step_convs,
                        leaf_tensor, dense_kernel, pair_step)
 from .notation import Expr
@@ -41,24 +41,25 @@ def pair_adjoint(expr, letters, a, A, b, B, dc):
         xa, xb, ca, cb = a, b, list(la), list(lb)
         a_shifts, b_shifts, a_taps, b_taps = [], [], [], []
         for (l, fa), k in zip(convs, combo):
+            s = stride_of(expr, l)
             if fa:
                 K = label_size(expr, B, l)
-                xa = shift(xa, ca.index(l), k, K)
-                a_shifts.append((l, k, K))
+                a_shifts.append((l, k, K, xa.shape[ca.index(l)], s))
+                xa = shift(xa, ca.index(l), k, K, s)
                 b_taps.append((l, k))
                 xb = np.take(xb, k, axis=cb.index(l))
                 cb.remove(l)
             else:
                 K = label_size(expr, A, l)
-                xb = shift(xb, cb.index(l), k, K)
-                b_shifts.append((l, k, K))
+                b_shifts.append((l, k, K, xb.shape[cb.index(l)], s))
+                xb = shift(xb, cb.index(l), k, K, s)
                 a_taps.append((l, k))
                 xa = np.take(xa, k, axis=ca.index(l))
                 ca.remove(l)
         # adjoint w.r.t. the (shifted / tap-sliced) view of a
         ga = _einsum(letters, dc, lc, xb, cb, ca)
-        for l, k, K in a_shifts:
-            ga = shift_adjoint(ga, ca.index(l), k, K)
+        for l, k, K, n, s in a_shifts:
+            ga = shift_adjoint(ga, ca.index(l), k, K, n, s)
         idx = [slice(None)] * da.ndim
         for l, k in a_taps:
             idx[la.index(l)] = k
@@ -68,8 +69,8 @@ def pair_adjoint(expr, letters, a, A, b, B, dc):
         else:
             da += ga
         gb = _einsum(letters, xa, ca, dc, lc, cb)
-        for l, k, K in b_shifts:
-            gb = shift_adjoint(gb, cb.index(l), k, K)
+        for l, k, K, n, s in b_shifts:
+            gb = shift_adjoint(gb, cb.index(l), k, K, n, s)
         idx = [slice(None)] * db.ndim
         for l, k in b_taps:
             idx[lb.index(l)] = k
@@ -144,30 +145,32 @@ def grads_dense(expr: Expr, arrays, dy, feature_operand: int = 0):
     convs = list(expr.conv)
     Ks = [W.shape[lw.index(l)] for l in convs]
     lw_red = [l for l in lw if l not in convs]
-    # dX: every output position p receives from taps k the entry at q = p + k - c;
-    # with dY padded by (K-1-c, c), dY[q - k + c] is the slice starting at K-1-k.
-    pads_y = [(0, 0)] * dy.ndim
+    # Output position p read the zero-padded X at s*p + k for tap k (padding c
+    # before, K-1-c after): dX is accumulated in the padded frame at those
+    # positions and cropped; dW[k] pairs the same window of X with dY.
     pads_x = [(0, 0)] * X.ndim
     for l, K in zip(convs, Ks):
         c = (K - 1) // 2
-        pads_y[expr.output.index(l)] = (K - 1 - c, c)
         pads_x[lx.index(l)] = (c, K - 1 - c)
-    dyp = np.pad(dy, pads_y)
     Xp = np.pad(X, pads_x)
-    dX = np.zeros_like(X)
+    dXp = np.zeros_like(Xp)
     dW = np.zeros_like(W)
     for combo in itertools.product(*[range(K) for K in Ks]):
-        ywin = [slice(None)] * dy.ndim
         xwin = [slice(None)] * X.ndim
         widx = [slice(None)] * W.ndim
         for l, K, k in zip(convs, Ks, combo):
-            n = dy.shape[expr.output.index(l)]
-            ywin[expr.output.index(l)] = slice(K - 1 - k, K - 1 - k + n)
-            xwin[lx.index(l)] = slice(k, k + X.shape[lx.index(l)])
+            s = stride_of(expr, l)
+            m = dy.shape[expr.output.index(l)]
+            xwin[lx.index(l)] = slice(k, k + s * (m - 1) + 1, s)
             widx[lw.index(l)] = k
         Wk = W[tuple(widx)]
-        dX += _einsum(letters, dyp[tuple(ywin)], expr.output, Wk, lw_red, lx)
+        dXp[tuple(xwin)] += _einsum(letters, dy, expr.output, Wk, lw_red, lx)
         dW[tuple(widx)] += _einsum(letters, Xp[tuple(xwin)], lx, dy, expr.output, lw_red)
+    crop = [slice(None)] * X.ndim
+    for l, K in zip(convs, Ks):
+        c = (K - 1) // 2
+        crop[lx.index(l)] = slice(c, c + X.shape[lx.index(l)])
+    dX = dXp[tuple(crop)]
     out = []
     for i in range(expr.n):
         if i == feature_operand:
@@ -178,8 +181,8 @@ def grads_dense(expr: Expr, arrays, dy, feature_operand: int = 0):
         for l in li:
             if l not in lw and not any(l in expr.inputs[j] for j in others):
                 raise NotImplementedError("factor with a self-contracted label")
-        sub = "".join(letters[l] for l in lw) + "," + \
-            ",".join("".join(letters[l] for l in expr.inputs[j]) for j in others) + \
+        sub = ",".join(["".join(letters[l] for l in lw)] +
+                       ["".join(letters[l] for l in expr.inputs[j]) for j in others]) + \
             "->" + "".join(letters[l] for l in li)
         ops = [dW] + [np.asarray(arrays[j], np.float64) for j in others]
         out.append(np.einsum(sub, *ops, optimize=True))

@@ -50,6 +50,7 @@ class Expr:
     sizes: list = None      # per operand: {label: size}; set by bind()
     feature: dict = None    # conv label -> operand index of its feature side
     out_sizes: dict = None  # output label -> size
+    stride: dict = None     # conv label -> stride (absent: 1)
 
     @property
     def n(self):
@@ -106,7 +107,7 @@ def parse(spec: str) -> Expr:
     return Expr(inputs=inputs, output=output, conv=conv)
 
 
-def bind(expr: Expr, shapes, feature_operand: int = 0) -> Expr:
+def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
     """Attach operand sizes and resolve the feature side of each convolved label.
 
     Feature side (Appendix B, 'Convolution Varieties'): of the two operands
@@ -115,6 +116,11 @@ def bind(expr: Expr, shapes, feature_operand: int = 0) -> Expr:
     wins if it is one of the two, otherwise the operand with the lower index.
     A convolved label held by more than two operands is multi-way; it is kept
     (its cost is defined) but has no feature side.
+
+    `strides` maps a convolved label held by two operands to its stride s >= 1
+    (a strided convolution is one of the non-commutative varieties of
+    Appendix B): output position p reads the feature at s*p + k - c, and the
+    output keeps ceil(I / s) positions (I = feature size).
     """
     if len(shapes) != expr.n:
         raise ValueError("one shape per operand is required")
@@ -146,10 +152,19 @@ def bind(expr: Expr, shapes, feature_operand: int = 0) -> Expr:
                 feature[l] = feature_operand
             else:
                 feature[l] = min(a, b)
+    stride = {}
+    for l, st in (strides or {}).items():
+        if l not in feature:
+            raise ValueError(f"stride of {l}: only a convolved label held by two operands is strided")
+        if int(st) < 1:
+            raise ValueError(f"stride of {l} must be >= 1")
+        if int(st) > 1:
+            stride[l] = int(st)
     out_sizes = {}
     for l in expr.output:
-        if l in feature:            # same padding keeps the feature size
-            out_sizes[l] = sizes[feature[l]][l]
+        if l in feature:            # same padding keeps the feature size (ceil(I / s) when strided)
+            s_ = stride.get(l, 1)
+            out_sizes[l] = -(-sizes[feature[l]][l] // s_)
         elif l in expr.conv:        # one holder, or multi-way: the largest size
             out_sizes[l] = max(sizes[i][l] for i in expr.holders(l))
         else:
@@ -157,4 +172,5 @@ def bind(expr: Expr, shapes, feature_operand: int = 0) -> Expr:
     expr.sizes = sizes
     expr.feature = feature
     expr.out_sizes = out_sizes
+    expr.stride = stride
     return expr

@@ -176,3 +176,71 @@ def test_self_contracted_label_is_presummed():
     ref = np.einsum("bsm,mt->bt", X, A)
     np.testing.assert_allclose(O.eval_pairwise(e, [X, A], (0, 1)), ref, rtol=1e-12)
     np.testing.assert_allclose(O.eval_definition(e, [X, A]), ref, rtol=1e-12)
+
+
+STRIDED = [
+    # (H, W, K, stride): odd and even feature sizes, 3x3, 7x7 (a ResNet stem),
+    # 1x1 (a strided shortcut), strides 2 and 3
+    (9, 9, 3, 2), (8, 10, 3, 2), (11, 12, 7, 2), (8, 7, 1, 2), (10, 9, 3, 3),
+]
+
+
+@pytest.mark.parametrize("H,W_,K,s", STRIDED)
+def test_strided_conv_matches_torch(H, W_, K, s):
+    """A strided convolution (Appendix B, a non-commutative variety) against
+    PyTorch CPU float64 conv2d(stride=s, padding=(K-1)//2) and its autograd:
+    the definition, the pairwise evaluation and the dense evaluation."""
+    g = np.random.default_rng(40 + K + s)
+    X = g.standard_normal((2, 3, H, W_))
+    F = g.standard_normal((4, 3, K, K))
+    e = O.bind(O.parse("bshw,tshw->bthw|hw"), [X.shape, F.shape], strides={"h": s, "w": s})
+    xt = torch.tensor(X, requires_grad=True)
+    ft = torch.tensor(F, requires_grad=True)
+    y = torch.nn.functional.conv2d(xt, ft, stride=s, padding=(K - 1) // 2)
+    assert tuple(e.out_sizes[l] for l in "bthw") == tuple(y.shape)
+    dy = g.standard_normal(tuple(y.shape))
+    (y * torch.tensor(dy)).sum().backward()
+    ref = y.detach().numpy()
+    t = O.optimal_tree(e)[0]
+    np.testing.assert_allclose(O.eval_definition(e, [X, F]), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.eval_pairwise(e, [X, F], t), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.eval_dense(e, [X, F]), ref, rtol=1e-12, atol=1e-12)
+    for gp, gd, tt in zip(O.grads_pairwise(e, [X, F], t, dy), O.grads_dense(e, [X, F], dy),
+                          (xt, ft)):
+        np.testing.assert_allclose(gp, tt.grad.numpy(), rtol=1e-11, atol=1e-11)
+        np.testing.assert_allclose(gd, tt.grad.numpy(), rtol=1e-11, atol=1e-11)
+
+
+def test_strided_cp_layer_every_tree_matches_torch():
+    """CP layer with stride 2 on h and w: every one of the 105 trees, the
+    definition and the dense evaluation equal torch conv2d with the
+    reconstructed kernel; the convolved labels of every intermediate holding
+    both sides have ceil(I / 2) positions."""
+    g = np.random.default_rng(41)
+    B, S, T, R, H, W_, K = 2, 3, 4, 2, 7, 8, 3
+    arr = [g.standard_normal(s) for s in [(B, S, H, W_), (R, S), (R, T), (R, K), (R, K)]]
+    e = O.bind(O.parse("bshw,rs,rt,rh,rw->bthw|hw"), [a.shape for a in arr],
+               strides={"h": 2, "w": 2})
+    Wd = np.einsum("rs,rt,rh,rw->tshw", *arr[1:])
+    ref = torch.nn.functional.conv2d(torch.tensor(arr[0]), torch.tensor(Wd), stride=2,
+                                     padding=1).numpy()
+    np.testing.assert_allclose(O.eval_definition(e, arr), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.eval_dense(e, arr), ref, rtol=1e-12, atol=1e-12)
+    for t in O.all_trees(range(5)):
+        np.testing.assert_allclose(O.eval_pairwise(e, arr, t), ref, rtol=1e-11, atol=1e-11)
+    assert O.intermediate_size(e, (0, 3)) == B * S * R * 4 * W_      # h convolved: ceil(7/2)
+    assert O.intermediate_size(e, (0, 1, 3, 4)) == B * R * 4 * 4
+
+
+def test_strided_cost():
+    """The strided step counts output positions times taps: a 3x3 stride-2
+    convolution of X[2, 3, 9, 9] with W[4, 3, 3, 3] does 2*4*3*5*5*3*3
+    multiplications; with stride 1 it would be 2*4*3*9*9*3*3."""
+    e = O.bind(O.parse("bshw,tshw->bthw|hw"), [(2, 3, 9, 9), (4, 3, 3, 3)],
+               strides={"h": 2, "w": 2})
+    assert O.step_cost(e, (0,), (1,)) == 2 * 4 * 3 * 5 * 5 * 3 * 3
+    # training (Appendix B): g1 = output * filter, g2 = feature * output per label
+    assert O.step_cost(e, (0,), (1,), "train_paper") == 2 * 4 * 3 * (
+        (5 * 3) ** 2 + (5 * 3) ** 2 + (9 * 5) ** 2)
+    e1 = O.bind(O.parse("bshw,tshw->bthw|hw"), [(2, 3, 9, 9), (4, 3, 3, 3)])
+    assert O.step_cost(e1, (0,), (1,)) == 2 * 4 * 3 * 9 * 9 * 3 * 3

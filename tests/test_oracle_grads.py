@@ -142,3 +142,30 @@ def test_single_operand_gradient_is_a_broadcast():
     dy = np.array([1.5, -2.0, 0.25])
     (gx,) = O.grads_pairwise(e, [x], 0, dy)
     assert np.array_equal(gx, np.broadcast_to(dy[:, None, None], (3, 4, 5)))
+
+
+@pytest.mark.parametrize("spec,shapes,strides", [
+    ("bshw,rs,rt,rh,rw->bthw|hw", [(1, 2, 5, 6), (2, 2), (2, 3), (2, 3), (2, 3)], {"h": 2, "w": 2}),
+    ("bsh,tsh->bth|h", [(2, 2, 9), (3, 2, 4)], {"h": 3}),
+    ("tsh,bsh->bth|h", [(3, 2, 1), (2, 2, 7)], {"h": 2}),
+])
+def test_finite_differences_strided(spec, shapes, strides):
+    """Strided convolutions (Appendix B, non-commutative varieties): pairwise
+    gradients along the optimal tree against central differences of the
+    plain definition."""
+    e = O.bind(O.parse(spec), shapes, strides=strides)
+    g = np.random.default_rng(12)
+    arr = [g.standard_normal(s) for s in shapes]
+    y = O.eval_definition(e, arr)
+    dy = g.standard_normal(y.shape)
+    t = O.optimal_tree(e)[0]
+    grads = O.grads_pairwise(e, arr, t, dy)
+    eps = 1e-6
+    for i, a in enumerate(arr):
+        for idx in list(np.ndindex(*a.shape))[::max(1, a.size // 10)]:
+            ap = [x.copy() for x in arr]
+            am = [x.copy() for x in arr]
+            ap[i][idx] += eps
+            am[i][idx] -= eps
+            fd = ((O.eval_definition(e, ap) - O.eval_definition(e, am)) * dy).sum() / (2 * eps)
+            assert abs(fd - grads[i][idx]) <= 1e-7 * max(1.0, abs(fd)), (i, idx)
