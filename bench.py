@@ -56,6 +56,10 @@ def parse_args():
                     help="skip the per-layer lines of the other configurations")
     ap.add_argument("--sample-steps", type=int, default=100,
                     help="individually timed steps for the median / min")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only the ResNet-34 CP-layer sweep: planned vs left-to-right order")
+    ap.add_argument("--sweep-batch", type=int, default=16,
+                    help="batch of the timed sweep steps (FLOPs are also given at 128)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run plain device copies of this size (counter calibration)")
     return ap.parse_args()
@@ -248,7 +252,7 @@ class Runner:
     gradient and workspace buffers, and step() = parse + plan + forward +
     backward through the C ABI on torch's current stream."""
 
-    def __init__(self, w, dtype, flags=0, path=None, max_elements=None):
+    def __init__(self, w, dtype, flags=0, path=None, max_elements=None, strides=None):
         import numpy as np
         import torch
         import paper_2401_03384_amd as P
@@ -257,13 +261,15 @@ class Runner:
         if dtype != w.dtype:
             w = W.Workload(w.name, w.spec, w.shapes, dtype, w.seed, w.sigmas, w.out_shape, w.backward)
         self.w, self.dtype, self.flags, self.path, self.max_elements = w, dtype, flags, path, max_elements
+        self.strides = dict(strides or {})
         dev = torch.device("cuda:0")
         tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
         ins, dy = W.make_inputs(w)
         self.xs = [torch.from_numpy(a.astype(np.float32)).to(tdt).to(dev) for a in ins]
         self.d = torch.from_numpy(dy.astype(np.float32)).to(tdt).to(dev)
         del ins, dy
-        self.ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=max_elements)
+        self.ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=max_elements,
+                          strides=self.strides)
         ref = self.ref
         self.ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
         self.out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
@@ -278,6 +284,8 @@ class Runner:
     def step(self, fwd=True, bwd=True):
         P, w = self.P, self.w
         e = P.ce_expr_parse(w.spec, self.shapes)
+        for label, st in self.strides.items():
+            P.ce_expr_set_stride(e, label, st)
         if self.path is None and self.max_elements is not None:
             p = P.ce_plan_create_limited(e, P.CE_COST_FWD, self.cdt, self.flags, self.max_elements)
         elif self.path is None:
@@ -386,6 +394,47 @@ def config_line(name, dtype, steps, samples):
     return out
 
 
+def sweep(args):
+    """ResNet-34's convolutions as CP layers at compression rate 100% (the
+    paper's per-layer FLOPs comparison, Section 5, Table 2): for the planned
+    and the left-to-right order on the same kernels, forward FLOPs at batch
+    128, and forward + backward time, FLOP rate and workspace at
+    --sweep-batch.  One JSON line."""
+    import torch
+    import paper_2401_03384_amd as P
+    import workloads as W
+
+    ltr = [(0, 1), (0, 3), (0, 2), (0, 1)]
+    rows = []
+    for name, *_ in W.RESNET34_CONVS:
+        w128, st = W.resnet34_cp_layer(name, batch=128)
+        row = {"layer": name, "stride": st.get("h", 1), "rank": w128.shapes[1][0],
+               "X": list(w128.shapes[0])}
+        for order, path in (("optimal", None), ("left_to_right", ltr)):
+            p128 = P.Plan(w128.spec, w128.shapes, "f32", strides=st, path=path)
+            w, _ = W.resnet34_cp_layer(name, batch=args.sweep_batch)
+            r = Runner(w, args.dtype or "f32", path=path, strides=st)
+            for _ in range(2):
+                r.step()
+            n = 3 if order == "left_to_right" else 10
+            t = r.timed(n)
+            row[order] = {"fwd_gflop_b128": round(2 * p128.fwd_macs / 1e9, 3),
+                          "ms_fwd_bwd": round(t * 1e3, 4),
+                          "tflops": round(6 * r.ref.fwd_macs / t / 1e12, 2),
+                          "workspace_gb": [round(r.ref.ws_fwd / 1e9, 3), round(r.ref.ws_bwd / 1e9, 3)],
+                          "steps": [[a, b] for a, b, _ in r.ref.steps]}
+            del r
+            torch.cuda.empty_cache()
+        row["flop_ratio"] = round(row["left_to_right"]["fwd_gflop_b128"] /
+                                  row["optimal"]["fwd_gflop_b128"], 2)
+        row["time_ratio"] = round(row["left_to_right"]["ms_fwd_bwd"] / row["optimal"]["ms_fwd_bwd"], 2)
+        print(f"sweep {name}: {row['flop_ratio']}x FLOPs, {row['time_ratio']}x time", file=sys.stderr,
+              flush=True)
+        rows.append(row)
+    print(json.dumps({"sweep": "ResNet-34 CP layers, compression rate 100%", "dtype": args.dtype or "f32",
+                      "timed_batch": args.sweep_batch, "layers": rows}), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -403,6 +452,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
+        return
+
+    if args.sweep:
+        sweep(args)
         return
 
     import paper_2401_03384_amd as P

@@ -26,9 +26,11 @@
  *    Varieties'); equal sizes go to the designated feature operand when it is
  *    one of the two (operand 0 unless ce_expr_set_feature says otherwise),
  *    else to the lower operand index.
- *  - Convolution: cross-correlation, stride 1, zero 'same' padding:
- *        out[p] = sum_k feat[p + k - floor((K-1)/2)] * filt[k],  p in [0, I)
- *    with feat zero outside [0, I).  The output keeps the feature size I.
+ *  - Convolution: cross-correlation, zero 'same' padding, stride 1 unless
+ *    ce_expr_set_stride says otherwise:
+ *        out[p] = sum_k feat[s*p + k - floor((K-1)/2)] * filt[k],
+ *    p in [0, ceil(I / s)), with feat zero outside [0, I).  With stride 1 the
+ *    output keeps the feature size I.
  *  - A label held by one operand only and absent from the output is summed
  *    away (Section 3.1, case (5)) before the pairwise steps.
  *  - A convolved label held by more than two operands (multi-way) can be
@@ -127,7 +129,21 @@ typedef enum { CE_PAD_SAME_ZERO = 0 } ce_pad;
  * CE_ERR_UNSUPPORTED (any other padding value). */
 ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad);
 
-/* Output rank and sizes (a convolved output label takes its feature size).
+/* Stride of convolved label `label` (Appendix B, 'Convolution Varieties': a
+ * strided convolution is one of the non-commutative kinds, supported for a
+ * label held by exactly two operands).  With stride s the output keeps
+ * ceil(I / s) positions, output position p reading the feature at
+ * s*p + k - floor((K-1)/2) (zero outside [0, I)): for odd K this is
+ * PyTorch's conv with stride s and padding (K-1)/2.  A pairwise step that
+ * convolves the label costs (output positions) x (filter size) for it.
+ * Default 1.  Must be called before ce_plan_create; the fused chains are not
+ * used for a plan with a strided label.
+ * Errors: CE_ERR_ARG (NULL, unknown or not convolved label, stride < 1),
+ * CE_ERR_UNSUPPORTED (the label is not held by exactly two operands). */
+ce_status ce_expr_set_stride(ce_expr* e, const char* label, int stride);
+
+/* Output rank and sizes (a convolved output label takes its feature size,
+ * ceil(size / stride) when strided).
  *   rank   receives the output rank
  *   dims   if non-NULL, receives [rank] sizes */
 ce_status ce_expr_output_shape(const ce_expr* e, int* rank, int64_t* dims);

@@ -5,7 +5,7 @@ Evaluates tensorial convolution layers written as conv_einsum strings
 planner and the HIP kernels in libconvein.so (C ABI: include/convein.h).
 """
 from .binding import (CeError, ce_backward, ce_backward_noalloc, ce_expr_destroy, ce_expr_output_shape,
-                      ce_expr_parse, ce_expr_set_conv, ce_expr_set_feature, ce_forward,
+                      ce_expr_parse, ce_expr_set_conv, ce_expr_set_feature, ce_expr_set_stride, ce_forward,
                       ce_last_error,
                       ce_plan_checkpoint, ce_plan_cost, ce_plan_create, ce_plan_create_ex, ce_plan_create_limited, ce_plan_create_with_path, ce_plan_describe,
                       ce_plan_destroy, ce_plan_left_to_right_cost, ce_plan_num_steps,
@@ -19,7 +19,7 @@ from .layer import GraphStep, Plan, plan, conv_einsum, contract_path, max_batch,
 
 __all__ = [
     "CeError", "ce_backward", "ce_backward_noalloc", "ce_expr_destroy", "ce_expr_output_shape", "ce_expr_parse",
-    "ce_expr_set_conv", "ce_expr_set_feature", "ce_forward", "ce_last_error", "ce_plan_cost", "ce_plan_create",
+    "ce_expr_set_conv", "ce_expr_set_feature", "ce_expr_set_stride", "ce_forward", "ce_last_error", "ce_plan_cost", "ce_plan_create",
     "ce_plan_create_limited", "ce_plan_create_ex", "ce_plan_checkpoint", "ce_plan_create_with_path", "ce_plan_describe", "ce_plan_destroy",
     "ce_plan_left_to_right_cost", "ce_plan_num_steps", "ce_plan_step", "ce_plan_workspace_size",
     "ce_timing_begin", "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record",

@@ -38,7 +38,8 @@ _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR
 
 # Every symbol the header declares (checked by the test-suite).
 EXPORTS = [
-    "ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
+    "ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_set_stride",
+    "ce_expr_output_shape",
     "ce_expr_destroy",
     "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_ex", "ce_plan_checkpoint",
     "ce_plan_create_with_path", "ce_plan_num_steps",
@@ -77,6 +78,7 @@ def lib():
                                     C.POINTER(vp)]
         L.ce_expr_set_feature.argtypes = [vp, C.c_int]
         L.ce_expr_set_conv.argtypes = [vp, C.c_char_p, C.c_int]
+        L.ce_expr_set_stride.argtypes = [vp, C.c_char_p, C.c_int]
         L.ce_expr_output_shape.argtypes = [vp, C.POINTER(C.c_int), i64p]
         L.ce_expr_destroy.argtypes = [vp]
         L.ce_expr_destroy.restype = None
@@ -108,7 +110,8 @@ def lib():
                                        C.POINTER(C.c_double)]
         L.ce_last_error.restype = C.c_char_p
         L.ce_version.restype = C.c_char_p
-        for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_output_shape",
+        for name in ("ce_expr_parse", "ce_expr_set_feature", "ce_expr_set_conv", "ce_expr_set_stride",
+    "ce_expr_output_shape",
                      "ce_plan_create", "ce_plan_create_limited", "ce_plan_create_ex", "ce_plan_checkpoint",
     "ce_plan_create_with_path",
                      "ce_plan_num_steps",
@@ -162,6 +165,10 @@ def ce_expr_set_feature(e: int, operand: int) -> None:
 
 def ce_expr_set_conv(e: int, label: str, pad: int = CE_PAD_SAME_ZERO) -> None:
     _check(lib().ce_expr_set_conv(e, label.encode(), pad))
+
+
+def ce_expr_set_stride(e: int, label: str, stride: int) -> None:
+    _check(lib().ce_expr_set_stride(e, label.encode(), int(stride)))
 
 
 def ce_expr_output_shape(e: int) -> tuple:

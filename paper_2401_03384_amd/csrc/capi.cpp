@@ -16,6 +16,21 @@ void set_last_error(const std::string& msg) { g_last_error = msg; }
 
 using namespace ce;
 
+namespace {
+// Label id of `label` (its name as written, e.g. "h" or "(h1)", or the name
+// inside the parentheses), -1 if unknown.
+int find_label(const ce_expr& e, const char* label) {
+    int id = -1;
+    for (int l = 0; l < e.num_labels(); l++) {
+        const std::string& nm = e.names[l];
+        if (nm == label || (nm.size() > 2 && nm.front() == '(' && nm.back() == ')' &&
+                            nm.compare(1, nm.size() - 2, label) == 0))
+            id = l;
+    }
+    return id;
+}
+}  // namespace
+
 extern "C" {
 
 const char* ce_last_error(void) { return g_last_error.c_str(); }
@@ -42,16 +57,24 @@ ce_status ce_expr_set_feature(ce_expr* e, int operand) {
 ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad) {
     return guard([&] {
         if (!e || !label) fail(CE_ERR_ARG, "NULL argument");
-        int id = -1;
-        for (int l = 0; l < e->num_labels(); l++) {
-            const std::string& nm = e->names[l];
-            if (nm == label || (nm.size() > 2 && nm.front() == '(' && nm.back() == ')' &&
-                                nm.compare(1, nm.size() - 2, label) == 0))
-                id = l;
-        }
+        int id = find_label(*e, label);
         if (id < 0) fail(CE_ERR_ARG, std::string("unknown label ") + label);
         if (!e->is_conv(id)) fail(CE_ERR_ARG, std::string("label ") + label + " is not convolved");
         if (pad != CE_PAD_SAME_ZERO) fail(CE_ERR_UNSUPPORTED, "only zero 'same' padding is implemented");
+    });
+}
+
+ce_status ce_expr_set_stride(ce_expr* e, const char* label, int stride) {
+    return guard([&] {
+        if (!e || !label) fail(CE_ERR_ARG, "NULL argument");
+        int id = find_label(*e, label);
+        if (id < 0) fail(CE_ERR_ARG, std::string("unknown label ") + label);
+        if (!e->is_conv(id)) fail(CE_ERR_ARG, std::string("label ") + label + " is not convolved");
+        if (stride < 1) fail(CE_ERR_ARG, "stride must be >= 1");
+        if (popcount64(e->holders[id]) != 2)
+            fail(CE_ERR_UNSUPPORTED, std::string("label ") + label +
+                                         ": a stride needs a convolved label held by exactly two operands");
+        e->stride[id] = stride;
     });
 }
 

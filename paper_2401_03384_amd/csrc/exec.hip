@@ -22,14 +22,17 @@ struct Ptrs {
 };
 
 void* resolve(const BufRef& b, const Ptrs& P) {
+    void* base = nullptr;
     switch (b.kind) {
-        case BUF_IN: return const_cast<void*>(P.in[b.index]);
-        case BUF_OUT: return P.out;
-        case BUF_DOUT: return const_cast<void*>(P.dout);
-        case BUF_DIN: return P.din ? P.din[b.index] : nullptr;
-        case BUF_WS: return (char*)P.ws + b.offset;
+        case BUF_IN: base = const_cast<void*>(P.in[b.index]); break;
+        case BUF_OUT: base = P.out; break;
+        case BUF_DOUT: base = const_cast<void*>(P.dout); break;
+        case BUF_DIN: base = P.din ? P.din[b.index] : nullptr; break;
+        case BUF_WS: base = (char*)P.ws + b.offset; break;
         default: return nullptr;
     }
+    // a view that starts inside the buffer (phases of a strided transposed conv)
+    return base ? (void*)((char*)base + b.shift) : nullptr;
 }
 
 hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {

@@ -56,7 +56,10 @@ int ce_expr::feature_of(int l) const {
 
 int64_t ce_expr::out_size(int l) const {
     int f = feature_of(l);
-    if (f >= 0) return size_in(f, l);
+    if (f >= 0) {
+        const int64_t s = stride_of(l);
+        return (size_in(f, l) + s - 1) / s;   // ceil(I / s) positions (I for stride 1)
+    }
     int64_t m = 0;
     for (int i = 0; i < n; i++)
         if ((holders[l] >> i) & 1) m = std::max(m, size_in(i, l));
@@ -156,6 +159,7 @@ ce_expr* parse_expr(const char* spec, int n_in, const int* ranks, const int64_t*
     e->out_mask = out_mask;
     e->dims.resize(n_in);
     e->holders.assign(e->names.size(), 0);
+    e->stride.assign(e->names.size(), 1);
     for (int i = 0; i < n_in; i++) {
         if (ranks[i] != (int)ops[i].size())
             fail(CE_ERR_SHAPE, "operand " + std::to_string(i) + ": rank " + std::to_string(ranks[i]) +

@@ -21,6 +21,7 @@ struct ce_expr {
     uint64_t conv = 0;                          // bit per convolved label
     uint64_t out_mask = 0;                      // bit per output label
     std::vector<uint32_t> holders;              // label -> bitmask of operands holding it
+    std::vector<int> stride;                    // label -> stride of a convolved label (1: none)
     int feature_operand = 0;
     bool bound = false;
 
@@ -32,6 +33,7 @@ struct ce_expr {
     // feature operand of a two-way convolved label (-1 if none)
     int feature_of(int l) const;
     int64_t out_size(int l) const;
+    int stride_of(int l) const { return l < (int)stride.size() ? stride[l] : 1; }
     std::vector<int64_t> out_dims() const;
 };
 

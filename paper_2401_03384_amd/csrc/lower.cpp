@@ -1163,7 +1163,7 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
                              ScratchAlloc& scratch) {
     (void)e;
     std::vector<Launch> out;
-    bool fast = !(flags & CE_FLAG_GENERIC_ONLY) &&
+    bool fast = !(flags & CE_FLAG_GENERIC_ONLY) && !op.generic_only &&
                 (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
                  try_cred(op, scratch, out) || try_cconv(op, out) || try_thinw(op, scratch, out) ||
                  try_tc(op, scratch, out, (flags & CE_FLAG_WIDE_OFFSETS) != 0));

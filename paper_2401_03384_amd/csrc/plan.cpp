@@ -56,8 +56,9 @@ uint64_t kept_mask(const ce_expr& e, uint32_t S) {
 
 // Size of label l in the intermediate of S: the largest size among S's
 // operands holding it (for a convolved label, the feature size once both
-// sides are merged).
+// sides are merged; for a strided one, its ceil(I / s) output positions).
 int64_t size_in_set(const ce_expr& e, uint32_t S, int l) {
+    if (e.stride_of(l) > 1 && (e.holders[l] & S) == e.holders[l]) return e.out_size(l);
     int64_t m = 0;
     for (int i = 0; i < e.n; i++)
         if (((S >> i) & 1) && ((e.holders[l] >> i) & 1)) m = std::max(m, e.size_in(i, l));
@@ -80,8 +81,10 @@ uint64_t step_cost_sat(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mo
         if (ia && ib && e.is_conv(l)) {
             uint64_t sa = size_in_set(e, A, l), sb = size_in_set(e, B, l);
             bool fa = feature_on_a(e, A, B, l);
-            uint64_t feat = fa ? sa : sb, filt = fa ? sb : sa, out = feat;
-            conv_f = mul_sat(conv_f, mul_sat(feat, filt));
+            const uint64_t st = (uint64_t)e.stride_of(l);
+            uint64_t feat = fa ? sa : sb, filt = fa ? sb : sa, out = (feat + st - 1) / st;
+            // forward: output positions x taps (feature x filter for stride 1)
+            conv_f = mul_sat(conv_f, mul_sat(out, filt));
             // gradient of the feature side: output * filter; of the filter side: feature * output
             conv_ga = mul_sat(conv_ga, fa ? mul_sat(out, filt) : mul_sat(feat, out));
             conv_gb = mul_sat(conv_gb, fa ? mul_sat(feat, out) : mul_sat(out, filt));
@@ -284,40 +287,118 @@ struct Builder {
             int64_t I = size_in_set(e, fa ? A : B, l);
             int64_t K = size_in_set(e, fa ? B : A, l);
             int64_t c = (K - 1) / 2;
+            const int s = e.stride_of(l);
+            const int64_t Oq = (I + s - 1) / s;   // output positions
             ConvMap m{};
             m.label = l;
             if (which == 0) {
-                // C[p] = sum_j feat[p + j - c] * filt[j]
-                m.O = I;
+                // C[p] = sum_j feat[s*p + j - c] * filt[j]
+                m.O = Oq;
                 m.J = K;
-                if (fa) { m.aL = 1; m.bL = 1; m.gL = -c; m.limL = I; m.aR = 0; m.bR = 1; m.gR = 0; m.limR = K; }
-                else    { m.aL = 0; m.bL = 1; m.gL = 0; m.limL = K; m.aR = 1; m.bR = 1; m.gR = -c; m.limR = I; }
+                if (fa) { m.aL = s; m.bL = 1; m.gL = -c; m.limL = I; m.aR = 0; m.bR = 1; m.gR = 0; m.limR = K; }
+                else    { m.aL = 0; m.bL = 1; m.gL = 0; m.limL = K; m.aR = s; m.bR = 1; m.gR = -c; m.limR = I; }
             } else if (which == 1) {
                 // L = dC, R = B, output dA
-                if (fa) {  // dA[q] = sum_j dC[q - j + c] B[j]
+                if (fa) {  // dA[q] = sum_j dC[q - j + c] B[j]  (stride 1; see phase_split)
                     m.O = I; m.J = K;
-                    m.aL = 1; m.bL = -1; m.gL = c; m.limL = I;
+                    m.aL = 1; m.bL = -1; m.gL = c; m.limL = Oq;
                     m.aR = 0; m.bR = 1; m.gR = 0; m.limR = K;
-                } else {   // dA[k] = sum_j dC[j] B[j + k - c]
-                    m.O = K; m.J = I;
-                    m.aL = 0; m.bL = 1; m.gL = 0; m.limL = I;
-                    m.aR = 1; m.bR = 1; m.gR = -c; m.limR = I;
+                } else {   // dA[k] = sum_p dC[p] B[s*p + k - c]
+                    m.O = K; m.J = Oq;
+                    m.aL = 0; m.bL = 1; m.gL = 0; m.limL = Oq;
+                    m.aR = 1; m.bR = s; m.gR = -c; m.limR = I;
                 }
             } else {
                 // L = A, R = dC, output dB
-                if (fa) {  // dB[k] = sum_j A[j + k - c] dC[j]
-                    m.O = K; m.J = I;
-                    m.aL = 1; m.bL = 1; m.gL = -c; m.limL = I;
-                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = I;
-                } else {   // dB[q] = sum_j A[j] dC[q - j + c]
+                if (fa) {  // dB[k] = sum_p A[s*p + k - c] dC[p]
+                    m.O = K; m.J = Oq;
+                    m.aL = 1; m.bL = s; m.gL = -c; m.limL = I;
+                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = Oq;
+                } else {   // dB[q] = sum_j A[j] dC[q - j + c]  (stride 1; see phase_split)
                     m.O = I; m.J = K;
                     m.aL = 0; m.bL = 1; m.gL = 0; m.limL = K;
-                    m.aR = 1; m.bR = -1; m.gR = c; m.limR = I;
+                    m.aR = 1; m.bR = -1; m.gR = c; m.limR = Oq;
                 }
             }
             v.push_back(m);
         }
         return v;
+    }
+
+    // The gradient of the feature side of a strided convolution (a
+    // transposed convolution) as stride-1-shaped ops: for output positions
+    // q = s*q' + r of residue r, only taps j = j0 + s*j' with
+    // j0 = (r + c) mod s reach them, reading dC at q' - j' + (r + c - j0)/s.
+    // Each phase is the op on views of the output (positions r, r + s, ...)
+    // and of the filter (taps j0, j0 + s, ...), every phase of every strided
+    // label once; labels of stride 1 keep their single map.  `op` is the
+    // gradient op of step `st` (which = 1: dA, 2: dB) with maps from
+    // conv_maps; returns the phase ops (just `op` when nothing is strided).
+    std::vector<PairOp> phase_split(const Step& st, int which, const PairOp& op) const {
+        uint32_t A = p.nodes[st.a].mask, B = p.nodes[st.b].mask;
+        std::vector<int> idx;   // maps to split: strided, gradient of the feature side
+        for (size_t k = 0; k < op.convs.size(); k++) {
+            const int l = op.convs[k].label;
+            const bool fa = feature_on_a(e, A, B, l);
+            if (e.stride_of(l) > 1 && ((which == 1) == fa)) idx.push_back((int)k);
+        }
+        if (idx.empty()) return {op};
+        // the filter operand of the op: R for dA (which 1), L for dB (which 2)
+        const bool filt_is_r = which == 1;
+        const size_t esC = op.C.dtype == DT_BF16 ? 2 : 4;
+        const TensorRef& F0 = filt_is_r ? op.R : op.L;
+        const size_t esF = F0.dtype == DT_BF16 ? 2 : 4;
+        int64_t nph = 1;
+        for (int k : idx) nph *= e.stride_of(op.convs[k].label);
+        std::vector<PairOp> out;
+        for (int64_t ph = 0; ph < nph; ph++) {
+            PairOp q = op;
+            TensorRef& F = filt_is_r ? q.R : q.L;
+            bool empty = false, none = false;
+            int64_t x = ph;
+            for (int k : idx) {
+                ConvMap& m = q.convs[k];
+                const int l = m.label;
+                const int64_t s = e.stride_of(l);
+                const int64_t r = x % s;
+                x /= s;
+                const int64_t I = m.O, K = m.J, c = (K - 1) / 2;
+                const int64_t j0 = (r + c) % s;
+                const int64_t Q = I > r ? (I - r + s - 1) / s : 0;
+                const int64_t J = K > j0 ? (K - j0 + s - 1) / s : 0;
+                if (Q == 0) none = true;
+                const int pc = q.C.pos(l), pf = F.pos(l);
+                q.C.buf.shift += (int64_t)(r * q.C.strides[pc] * (int64_t)esC);
+                q.C.dims[pc] = Q;
+                q.C.strides[pc] *= s;
+                m.O = Q;
+                if (J == 0) {
+                    // no tap reaches these positions: every term is skipped
+                    empty = true;
+                    F.dims[pf] = 1;
+                    m.J = 1;
+                } else {
+                    F.buf.shift += (int64_t)(j0 * F.strides[pf] * (int64_t)esF);
+                    F.dims[pf] = J;
+                    F.strides[pf] *= s;
+                    m.J = J;
+                }
+                const int64_t g = (r + c - j0) / s;
+                if (filt_is_r) {
+                    m.gL = g;
+                    m.limR = empty ? 0 : m.J;
+                } else {
+                    m.gR = g;
+                    m.limL = empty ? 0 : m.J;
+                }
+            }
+            if (none) continue;
+            q.macs = op.macs / nph;
+            q.what = op.what + " phase " + std::to_string(ph);
+            q.generic_only = empty;
+            out.push_back(q);
+        }
+        return out;
     }
 
     bool has_multiway() const {
@@ -532,6 +613,10 @@ uint64_t pair_cost(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mode) 
 ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned flags,
                    bool use_path, const int* pairs, int n_pairs, const PlanLimits& lim) {
     if (!e.bound) fail(CE_ERR_ARG, "expression is not bound");
+    for (int l = 0; l < e.num_labels(); l++)
+        if (e.stride_of(l) > 1 && e.feature_of(l) < 0)
+            fail(CE_ERR_UNSUPPORTED, "label " + e.names[l] +
+                                         ": a stride needs a convolved label held by exactly two operands");
     if (mode != CE_COST_FWD && mode != CE_COST_TRAIN_PAPER) fail(CE_ERR_ARG, "bad cost mode");
     if (dtype != CE_F32 && dtype != CE_BF16) fail(CE_ERR_ARG, "bad dtype");
     std::unique_ptr<ce_plan> p(new ce_plan());
@@ -574,6 +659,11 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
     }
     DType dt = dtype == CE_BF16 ? DT_BF16 : DT_F32;
     int m = (int)p->steps.size();
+    // the fused chains are written for stride-1 convolutions
+    bool strided = false;
+    for (int l = 0; l < E.num_labels(); l++)
+        if (E.stride_of(l) > 1) strided = true;
+    if (strided) flags |= CE_FLAG_NO_FUSION;
 
     if (p->executable) {
         // Workspace items: intermediates (id = node), their gradients
@@ -861,7 +951,8 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 op.need = p->nodes[st.a].mask;
                 op.what = "step " + std::to_string(s) + " grad lhs " + tensor_str(E, op.L) + "," +
                           tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
+                for (const PairOp& q : bld.phase_split(st, 1, op))
+                    for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
             }
             {
                 PairOp op;
@@ -873,7 +964,8 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                 op.need = p->nodes[st.b].mask;
                 op.what = "step " + std::to_string(s) + " grad rhs " + tensor_str(E, op.L) + "," +
                           tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                for (auto& l : lower_op(E, op, flags, bs)) p->bwd.push_back(l);
+                for (const PairOp& q : bld.phase_split(st, 2, op))
+                    for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
             }
         }
         drop_unused(bitems, p->bwd);

@@ -17,6 +17,7 @@ struct BufRef {
     BufKind kind = BUF_NONE;
     int index = 0;        // operand index for BUF_IN / BUF_DIN
     size_t offset = 0;    // byte offset for BUF_WS
+    int64_t shift = 0;    // further byte offset of a view into the buffer (any kind)
 };
 
 struct TensorRef {
@@ -52,6 +53,7 @@ struct PairOp {
     uint32_t need = 0;     // backward: run only if a wanted gradient lies below
     uint64_t macs = 0;     // multiplications of the pairwise step it belongs to
     std::string what;
+    bool generic_only = false;   // lower on the generic kernel (an op whose terms are all skipped)
 };
 
 struct Launch {

@@ -73,3 +73,24 @@ EDGE_CASES = {
     "even_filter_conv": ("bshw,tshw->bthw|hw", [(2, 3, 9, 10), (4, 3, 4, 4)], 0),
     "even_filter_cp": ("bshw,rs,rt,rh,rw->bthw|hw", [(2, 6, 9, 9), (3, 6), (3, 5), (3, 4), (3, 2)], 0),
 }
+
+
+# Strided convolutions (Appendix B varieties): name -> (string, shapes,
+# strides as "label=stride,...").  3x3 and 7x7 with stride 2, a strided 1x1
+# (taps reach only every other position), stride 3, CP and Tucker layers,
+# the feature operand second.
+STRIDED_CASES = {
+    "conv3_s2": ("bshw,tshw->bthw|hw", [(2, 3, 9, 8), (5, 3, 3, 3)], "h=2,w=2"),
+    "conv7_s2": ("bshw,tshw->bthw|hw", [(1, 3, 13, 12), (4, 3, 7, 7)], "h=2,w=2"),
+    "conv1_s2": ("bshw,tshw->bthw|hw", [(2, 6, 7, 8), (5, 6, 1, 1)], "h=2,w=2"),
+    "conv3_s3h": ("bshw,tshw->bthw|hw", [(2, 3, 10, 9), (4, 3, 3, 3)], "h=3"),
+    "cp_s2": ("bshw,rs,rt,rh,rw->bthw|hw", [(2, 6, 9, 10), (4, 6), (4, 5), (4, 3), (4, 3)],
+              "h=2,w=2"),
+    "tucker_s2": ("bshw,sp,pqhw,qt->bthw|hw", [(2, 8, 9, 9), (8, 4), (4, 6, 3, 3), (6, 5)],
+                  "h=2,w=2"),
+    "feature_second_s2": ("tsh,bsh->bth|h", [(4, 3, 3), (2, 3, 11)], "h=2"),
+}
+
+
+def strides_of(text):
+    return {kv.split("=")[0]: int(kv.split("=")[1]) for kv in text.split(",") if kv}

@@ -42,7 +42,7 @@ struct Ctx {
     std::string err;
 };
 
-Buf resolve(const BufRef& b, Ctx& c, int esize, bool& ok) {
+Buf resolve_base(const BufRef& b, Ctx& c, bool& ok) {
     ok = true;
     switch (b.kind) {
         case BUF_IN: return c.in[b.index];
@@ -58,7 +58,18 @@ Buf resolve(const BufRef& b, Ctx& c, int esize, bool& ok) {
         }
         default: ok = false; return Buf();
     }
+}
+
+// The buffer a launch operand refers to, from its view shift on (bounds
+// checks then count from the view's first byte to the buffer's end).
+Buf resolve(const BufRef& b, Ctx& c, int esize, bool& ok) {
+    Buf r = resolve_base(b, c, ok);
     (void)esize;
+    if (!ok || !r.base || b.shift == 0) return r;
+    if (b.shift < 0 || (size_t)b.shift > r.bytes) { ok = false; return Buf(); }
+    r.base += b.shift;
+    r.bytes -= (size_t)b.shift;
+    return r;
 }
 
 float ld(const Buf& b, int dt, int64_t i, bool& ok) {
@@ -1365,6 +1376,12 @@ static uint64_t g_limit = 0;
 static uint64_t g_save_budget = 0;
 void emul_set_limit(uint64_t max_elements) { g_limit = max_elements; }
 void emul_set_save_budget(uint64_t bytes) { g_save_budget = bytes; }
+// Strides of convolved labels for the next plans: "h=2,w=2" ("" for none).
+static std::string g_strides;
+void emul_set_strides(const char* spec) { g_strides = spec ? spec : ""; }
+// 1: the next plans take the left-to-right order ((0,1),(0,n-2),...,(0,1))
+static int g_ltr = 0;
+void emul_set_path(int ltr) { g_ltr = ltr; }
 
 // Runs the forward (mode 0), backward (mode 1) or forward then backward on
 // one workspace (mode 2) launch lists of a plan built with `flags`
@@ -1376,11 +1393,30 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
     const int generic_only = flags & CE_FLAG_GENERIC_ONLY;
     try {
         std::unique_ptr<ce_expr> e(parse_expr(spec, n, ranks, dims));
+        for (size_t pos = 0; pos < g_strides.size();) {
+            size_t eq = g_strides.find('=', pos), end = g_strides.find(',', pos);
+            if (end == std::string::npos) end = g_strides.size();
+            const std::string lab = g_strides.substr(pos, eq - pos);
+            const int st = std::atoi(g_strides.substr(eq + 1, end - eq - 1).c_str());
+            if (ce_expr_set_stride(e.get(), lab.c_str(), st) != CE_OK) {
+                std::snprintf(err, errlen, "bad stride %s", lab.c_str());
+                return 3;
+            }
+            pos = end + 1;
+        }
         PlanLimits lim;
         if (g_limit) lim.max_elements = g_limit;
         lim.save_budget = g_save_budget;
+        std::vector<int> pairs;
+        if (g_ltr && n > 1) {
+            pairs = {0, 1};
+            for (int k = 1; k < n - 1; k++) {
+                pairs.push_back(0);
+                pairs.push_back(n - 1 - k);
+            }
+        }
         std::unique_ptr<ce_plan> p(make_plan(*e, CE_COST_FWD, bf16 ? CE_BF16 : CE_F32, (unsigned)flags,
-                                             false, nullptr, 0, lim));
+                                             !pairs.empty(), pairs.data(), (int)pairs.size() / 2, lim));
         if (!p->executable) { std::snprintf(err, errlen, "not executable"); return 2; }
         Ctx c;
         int es = bf16 ? 2 : 4;

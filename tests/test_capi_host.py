@@ -492,3 +492,58 @@ def test_max_batch(name):
     ltr = [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)]
     assert need(keep, path=ltr, flags=B.CE_FLAG_SAVE_INTERMEDIATES | B.CE_FLAG_NO_FUSION) <= budget
     assert need(keep + 1, path=ltr, flags=B.CE_FLAG_SAVE_INTERMEDIATES | B.CE_FLAG_NO_FUSION) > budget
+
+
+def _plan_strided(spec, shapes, strides, mode=B.CE_COST_FWD, path=None):
+    e = B.ce_expr_parse(spec, shapes)
+    try:
+        for l, s in strides.items():
+            B.ce_expr_set_stride(e, l, s)
+        if path is not None:
+            return B.ce_plan_create_with_path(e, path, B.CE_F32, 0)
+        return B.ce_plan_create(e, mode, B.CE_F32, 0)
+    finally:
+        B.ce_expr_destroy(e)
+
+
+@pytest.mark.parametrize("scale", [1, 8])
+@pytest.mark.parametrize("name", [r[0] for r in W.RESNET34_CONVS])
+def test_strided_planner_matches_oracle(name, scale):
+    """ResNet-34 convolutions as CP layers (strides 1 and 2, 7x7, 3x3, 1x1),
+    full and reduced size: the planner's tree, per-step multiplications and
+    totals equal the oracle's in both cost modes, the left-to-right cost too,
+    and the output shape is ceil(size / stride)."""
+    w, st = W.resnet34_cp_layer(name, batch=128 if scale == 1 else 2, scale=scale)
+    e = O.bind(O.parse(w.spec), w.shapes, strides=st)
+    for mode, cmode in (("fwd", B.CE_COST_FWD), ("train_paper", B.CE_COST_TRAIN_PAPER)):
+        tree, cost = O.optimal_tree(e, mode)
+        p = _plan_strided(w.spec, w.shapes, st, cmode)
+        try:
+            assert _steps(p) == _oracle_steps(e, tree), (name, mode)
+            total, fwd = B.ce_plan_cost(p)
+            assert total == cost and fwd == O.tree_cost(e, tree, "fwd")
+            assert B.ce_plan_left_to_right_cost(p) == O.tree_cost(e, O.left_to_right_tree(5), mode)
+        finally:
+            B.ce_plan_destroy(p)
+    x = B.ce_expr_parse(w.spec, w.shapes)
+    for l, s in st.items():
+        B.ce_expr_set_stride(x, l, s)
+    assert B.ce_expr_output_shape(x) == tuple(w.out_shape)
+    B.ce_expr_destroy(x)
+
+
+def test_stride_errors():
+    x = B.ce_expr_parse("bshw,tshw->bthw|hw", [(1, 2, 5, 5), (3, 2, 3, 3)])
+    try:
+        for label, s, status in (("h", 0, B.CE_ERR_ARG), ("q", 2, B.CE_ERR_ARG),
+                                 ("s", 2, B.CE_ERR_ARG)):
+            with pytest.raises(B.CeError) as ex:
+                B.ce_expr_set_stride(x, label, s)
+            assert ex.value.status == status
+    finally:
+        B.ce_expr_destroy(x)
+    x = B.ce_expr_parse("bfshw,fghw,sthw->bgthw|hw", [(1, 2, 2, 7, 7), (2, 2, 3, 3), (2, 2, 3, 3)])
+    with pytest.raises(B.CeError) as ex:
+        B.ce_expr_set_stride(x, "h", 2)
+    assert ex.value.status == B.CE_ERR_UNSUPPORTED
+    B.ce_expr_destroy(x)

@@ -13,7 +13,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from conftest import PAPER_SHAPES, ROOT, load_layer_strings
+from conftest import STRIDED_CASES, strides_of, PAPER_SHAPES, ROOT, load_layer_strings
 
 STRINGS = load_layer_strings()
 
@@ -273,3 +273,54 @@ def test_emulated_save_budget(emul, name, flags):
     assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
     for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
         assert _rel(a, b) <= tol
+
+
+@pytest.mark.parametrize("generic", [0, 1], ids=["fast", "generic"])
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(STRIDED_CASES))
+def test_emulated_strided(emul, name, bf16, generic):
+    """Strided convolutions (Appendix B varieties): forward, and the backward
+    whose transposed convolutions run as stride-1 phases on views of the
+    gradient and the filter; every access bounds-checked; vs the oracle."""
+    spec, shapes, st = STRIDED_CASES[name]
+    e = O.bind(O.parse(spec), shapes, strides=strides_of(st))
+    tol = 2e-2 if bf16 else 1e-5
+    rng = np.random.default_rng(9)
+    ins = [rng.standard_normal(s).astype(np.float32) for s in shapes]
+    ins = [(W.round_to_bf16(a) if bf16 else a).astype(np.float64) for a in ins]
+    out_shape = tuple(e.out_sizes[l] for l in e.output)
+    dy = rng.standard_normal(out_shape).astype(np.float32)
+    dy = (W.round_to_bf16(dy) if bf16 else dy).astype(np.float64)
+    tree = O.optimal_tree(e)[0]
+    emul.emul_set_strides(st.encode())
+    try:
+        y = _run(emul, spec, shapes, bf16, 0, ins, out_shape=out_shape, generic=generic)
+        g = _run(emul, spec, shapes, bf16, 1, ins, dy=dy, generic=generic)
+    finally:
+        emul.emul_set_strides(b"")
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= tol
+
+
+@pytest.mark.parametrize("order", ["optimal", "ltr"])
+@pytest.mark.parametrize("name", ["conv1", "conv3_1", "conv3_sc", "conv5_x"])
+def test_emulated_resnet34_cp_layers(emul, name, order):
+    """ResNet-34 convolutions as CP layers at reduced size, the planned and
+    the left-to-right order, every launch bounds-checked, vs the oracle."""
+    w, strides = W.resnet34_cp_layer(name, batch=1, scale=8)
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes, strides=strides)
+    tree = O.left_to_right_tree(5) if order == "ltr" else O.optimal_tree(e)[0]
+    st = ",".join(f"{k}={v}" for k, v in strides.items())
+    emul.emul_set_strides(st.encode())
+    emul.emul_set_path(1 if order == "ltr" else 0)
+    try:
+        y = _run(emul, w.spec, w.shapes, False, 0, ins, out_shape=w.out_shape, generic=0)
+        g = _run(emul, w.spec, w.shapes, False, 1, ins, dy=dy, generic=0)
+    finally:
+        emul.emul_set_strides(b"")
+        emul.emul_set_path(0)
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= 1e-5
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= 1e-5

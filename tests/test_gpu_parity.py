@@ -20,7 +20,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from conftest import EDGE_CASES, PAPER_SHAPES, load_layer_strings
+from conftest import EDGE_CASES, PAPER_SHAPES, STRIDED_CASES, load_layer_strings, strides_of
 
 STRINGS = load_layer_strings()
 
@@ -282,11 +282,11 @@ def test_graph_replay(P, name):
         torch.cuda.synchronize()
 
 
-def _random_case(spec, shapes, dtype, feat=0, seed=7):
+def _random_case(spec, shapes, dtype, feat=0, seed=7, strides=None):
     """Seeded N(0,1) operands and dY for a small case, rounded to the storage
     type; the oracle expression bound with the same feature operand."""
     bf16 = dtype == "bf16"
-    e = O.bind(O.parse(spec), shapes, feature_operand=feat)
+    e = O.bind(O.parse(spec), shapes, feature_operand=feat, strides=strides)
     rng = np.random.default_rng(seed)
     rnd = (lambda a: W.round_to_bf16(a.astype(np.float32))) if bf16 else (lambda a: a.astype(np.float32))
     ins = [rnd(rng.standard_normal(s)).astype(np.float64) for s in shapes]
@@ -421,3 +421,51 @@ def test_cost_capped_plan(P, name):
     grads = plan.backward(xs, _dev(dy, False))
     torch.cuda.synchronize()
     _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), 1e-5)
+
+
+@pytest.mark.parametrize("generic", [False, True], ids=["default", "generic"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(STRIDED_CASES))
+def test_strided(P, name, dtype, generic):
+    """Strided convolutions (Appendix B varieties): forward, and the backward
+    whose transposed convolutions run as stride-1 phases on views of the
+    gradient and the filter; against the oracle."""
+    spec, shapes, st = STRIDED_CASES[name]
+    strides = strides_of(st)
+    bf16 = dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    _say(f"case {name} {dtype} generic={generic} {spec} shapes={shapes} strides={strides}")
+    e, ins, dy = _random_case(spec, shapes, dtype, strides=strides)
+    plan = P.Plan(spec, shapes, dtype, strides=strides,
+                  flags=P.CE_FLAG_GENERIC_ONLY if generic else 0)
+    assert tuple(plan.out_shape) == dy.shape
+    tree = O.optimal_tree(e)[0]
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    _check_all(name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+
+
+@pytest.mark.parametrize("order", ["optimal", "ltr"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", [r[0] for r in W.RESNET34_CONVS])
+def test_resnet34_cp_layers(P, name, dtype, order):
+    """The ResNet-34 convolutions as CP layers (7x7 stem, 3x3 and strided
+    3x3, strided 1x1 shortcuts) at reduced size (channels and input / 8),
+    the planned and the left-to-right order, against the oracle along the
+    same tree."""
+    w, strides = W.resnet34_cp_layer(name, batch=2, scale=8, dtype=dtype)
+    bf16 = dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    ins, dy = W.make_inputs(w)
+    e = O.bind(O.parse(w.spec), w.shapes, strides=strides)
+    path = [(0, 1), (0, 3), (0, 2), (0, 1)] if order == "ltr" else None
+    tree = O.left_to_right_tree(5) if order == "ltr" else O.optimal_tree(e)[0]
+    _say(f"case {w.name} {dtype} {order} shapes={w.shapes} strides={strides} tree {tree}")
+    plan = P.Plan(w.spec, w.shapes, dtype, strides=strides, path=path)
+    xs = [_dev(a, bf16) for a in ins]
+    y = plan.forward(xs)
+    grads = plan.backward(xs, _dev(dy, bf16))
+    torch.cuda.synchronize()
+    _check_all(w.name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)

@@ -25,6 +25,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "PARITY_WORKLOADS", "make_inputs", "cp_layer",
+           "RESNET34_CONVS", "cp_rank", "resnet34_cp_layer",
            "tucker2_layer", "rtt_layer", "rcp_layer", "round_to_bf16", "bf16_bits", "f32_bits"]
 
 
@@ -143,6 +144,53 @@ PARITY_WORKLOADS = {
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
     "C5cs_f32": rcp_layer("C5cs_f32", 16, (2, 2, 4), (2, 2, 4), 16, 16, 8, 5, "f32", 20),
 }
+
+
+# The convolutions of ResNet-34 on 224 x 224 inputs (stem, the four stages'
+# first and repeated 3x3 convolutions, and the strided 1x1 shortcuts) as CP
+# layers: (name, C_in, C_out, input size, kernel size, stride).  These are the
+# layer shapes of the paper's per-layer FLOPs comparison (Section 5, Table 2:
+# ResNet-34, CP layers, compression rate 100%).
+RESNET34_CONVS = [
+    ("conv1", 3, 64, 224, 7, 2),
+    ("conv2_x", 64, 64, 56, 3, 1),
+    ("conv3_1", 64, 128, 56, 3, 2),
+    ("conv3_x", 128, 128, 28, 3, 1),
+    ("conv3_sc", 64, 128, 56, 1, 2),
+    ("conv4_1", 128, 256, 28, 3, 2),
+    ("conv4_x", 256, 256, 14, 3, 1),
+    ("conv4_sc", 128, 256, 28, 1, 2),
+    ("conv5_1", 256, 512, 14, 3, 2),
+    ("conv5_x", 512, 512, 7, 3, 1),
+    ("conv5_sc", 256, 512, 14, 1, 2),
+]
+
+
+def cp_rank(s, t, k, cr=1.0):
+    """CP rank whose factors hold cr times the parameters of the dense
+    t x s x k x k kernel: R (s + t + 2k) = cr * t s k^2, rounded down (at
+    least 1)."""
+    return max(1, int(cr * t * s * k * k) // (s + t + 2 * k))
+
+
+def resnet34_cp_layer(name, batch=128, cr=1.0, scale=1, dtype="f32", seed=50):
+    """CP layer of a ResNet-34 convolution (RESNET34_CONVS) with strides on h
+    and w; `scale` divides the channel counts and the input size (at least
+    3 channels, 5 positions) for reduced-size cases.  Returns (Workload,
+    strides)."""
+    row = {r[0]: r for r in RESNET34_CONVS}[name]
+    _, s, t, hw, k, st = row
+    if scale > 1:
+        s, t, hw = max(3, s // scale), max(3, t // scale), max(5, hw // scale)
+    r = cp_rank(s, t, k, cr)
+    out = -(-hw // st)
+    sg = _kaiming_sigma(s * k * k, r, 4)
+    w = Workload(f"{name}_b{batch}" + (f"_s{scale}" if scale > 1 else ""),
+                 "bshw,rs,rt,rh,rw->bthw|hw",
+                 ((batch, s, hw, hw), (r, s), (r, t), (r, k), (r, k)), dtype, seed,
+                 (1.0, sg, sg, sg, sg), (batch, t, out, out), True,
+                 note=f"ResNet-34 {name} as a CP layer, stride {st}")
+    return w, ({"h": st, "w": st} if st > 1 else {})
 
 
 def round_to_bf16(x) -> np.ndarray:
