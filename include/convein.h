@@ -33,9 +33,8 @@
  *    output keeps the feature size I.
  *  - A label held by one operand only and absent from the output is summed
  *    away (Section 3.1, case (5)) before the pairwise steps.
- *  - A convolved label held by more than two operands (multi-way) can be
- *    parsed and planned (its cost uses the larger size) but not executed:
- *    ce_forward / ce_backward return CE_ERR_UNSUPPORTED.
+ *  - A convolved label held by more than two operands (multi-way) is
+ *    convolved circularly (see ce_expr_set_conv, CE_PAD_CIRCULAR).
  *  - Tensors are dense, row-major, in the label order written in the string
  *    (operands) or after '->' (output).  Element type is the plan's dtype,
  *    except gradients of operands other than the feature operand, which are
@@ -75,7 +74,7 @@ typedef enum {
     CE_OK = 0,
     CE_ERR_PARSE = -1,        /* malformed string */
     CE_ERR_SHAPE = -2,        /* ranks or sizes inconsistent with the string */
-    CE_ERR_UNSUPPORTED = -3,  /* valid but not executable (multi-way convolution, too many operands) */
+    CE_ERR_UNSUPPORTED = -3,  /* valid but not supported (too many operands or loop dimensions) */
     CE_ERR_ARG = -4,          /* null or out-of-range argument */
     CE_ERR_WORKSPACE = -5,    /* workspace too small or misaligned */
     CE_ERR_OVERFLOW = -6,     /* a cost or a size exceeds 64 bits */
@@ -118,15 +117,27 @@ ce_status ce_expr_parse(const char* spec, int n_in, const int* ranks,
 ce_status ce_expr_set_feature(ce_expr* e, int operand);
 
 /* Boundary handling of a convolved label (Appendix A: "same" size output;
- * the zero-padded reading is used throughout, see ce_expr_set_conv). */
-typedef enum { CE_PAD_SAME_ZERO = 0 } ce_pad;
+ * Appendix B: circular convolution, the only kind for a label held by more
+ * than two operands). */
+typedef enum { CE_PAD_SAME_ZERO = 0, CE_PAD_CIRCULAR = 1 } ce_pad;
 
 /* Set the padding of convolved label `label` (its name in the string, e.g.
- * "h" or "(h1)").  CE_PAD_SAME_ZERO (the default for every convolved label):
- * output size = feature size, the filter centred with floor((K-1)/2) taps
- * before, zero outside the feature.  Must be called before ce_plan_create.
- * Errors: CE_ERR_ARG (NULL, unknown or not convolved label),
- * CE_ERR_UNSUPPORTED (any other padding value). */
+ * "h" or "(h1)").
+ *   CE_PAD_SAME_ZERO (the default for a label held by two operands): output
+ *     size = feature size, the filter centred with floor((K-1)/2) taps
+ *     before, zero outside the feature (cross-correlation).
+ *   CE_PAD_CIRCULAR (the default, and the only choice, for a label held by
+ *     three or more operands): commutative circular convolution; every holder
+ *     is zero-padded to N, the largest of its sizes, and positions add modulo
+ *     N:  out[p] = sum over i_1 + ... + i_m = p (mod N) of prod_k T_k[i_k],
+ *     p in [0, N).  A tensor merging two or more holders has N positions; a
+ *     step merging sides of sizes a and b costs a * b for the label.  Steps
+ *     with a circular label run on the generic kernel.
+ * Must be called before ce_plan_create.
+ * Errors: CE_ERR_ARG (NULL, unknown or not convolved label, unknown
+ * padding, CE_PAD_CIRCULAR on a label held by one operand),
+ * CE_ERR_UNSUPPORTED (CE_PAD_SAME_ZERO on a label held by more than two
+ * operands). */
 ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad);
 
 /* Stride of convolved label `label` (Appendix B, 'Convolution Varieties': a

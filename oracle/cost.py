@@ -30,6 +30,11 @@ gradient of the filter side it counts (feature size) * (output size), as in
 the Appendix B example cost(g1) = BHWX'Y'TS, cost(g2) = BXYX'Y'TS.  With
 same padding the output size equals the feature size.
 
+A circular label (Appendix B: multi-way labels are convolved circularly)
+counts a * b in a step merging sides of sizes a and b (every pair of
+positions meets once, in the forward and in each gradient), and a tensor
+that merges two or more of its holders holds its N positions.
+
 A strided convolved label (stride s) has ceil(I / s) output positions; a step
 that convolves it counts (output size) * (filter size), the multiplications
 it does (I * J for s = 1), and the merged tensor holds the output size.
@@ -58,10 +63,20 @@ def stride_of(expr: Expr, label) -> int:
     return (expr.stride or {}).get(label, 1)
 
 
+def is_circular(expr: Expr, label) -> bool:
+    return label in (expr.circular or ())
+
+
 def label_size(expr: Expr, subset, label):
     """Size of `label` in the tensor merging the operands in `subset`: the
     largest size among them, except a strided convolved label once both of
-    its holders are merged, which has ceil(I / s) output positions."""
+    its holders are merged, which has ceil(I / s) output positions, and a
+    circular label once two or more of its holders are merged, which has the
+    N positions of the circular convolution (its largest size overall)."""
+    if is_circular(expr, label):
+        hold = expr.holders(label)
+        if sum(1 for i in hold if i in subset) >= 2:
+            return max(expr.sizes[i][label] for i in hold)
     s = stride_of(expr, label)
     if s > 1 and all(i in subset for i in expr.holders(label)):
         return -(-expr.sizes[expr.feature[label]][label] // s)
@@ -81,8 +96,11 @@ def step_cost(expr: Expr, A, B, mode: str = "fwd") -> int:
     la, lb = kept_labels(expr, A), kept_labels(expr, B)
     plain = 1
     both = []          # (feature size, filter size, feature on A?, output size)
+    circ = 1           # circular labels: every pair of positions once
     for l in la + [x for x in lb if x not in la]:
-        if l in la and l in lb and l in expr.conv:
+        if l in la and l in lb and is_circular(expr, l):
+            circ *= label_size(expr, A, l) * label_size(expr, B, l)
+        elif l in la and l in lb and l in expr.conv:
             ia, ib = label_size(expr, A, l), label_size(expr, B, l)
             if _feature_side_is_a(expr, A, B, l):
                 both.append((ia, ib, True, -(-ia // stride_of(expr, l))))
@@ -92,6 +110,7 @@ def step_cost(expr: Expr, A, B, mode: str = "fwd") -> int:
             plain *= label_size(expr, A, l)
         else:
             plain *= label_size(expr, B, l)
+    plain *= circ
     f = plain
     for feat, filt, _, out in both:
         f *= out * filt

@@ -26,7 +26,7 @@ import itertools
 
 import numpy as np
 
-from .cost import kept_labels, label_size, stride_of
+from .cost import kept_labels, label_size, stride_of, is_circular
 from .notation import Expr
 
 
@@ -80,18 +80,40 @@ def shift_adjoint(g, axis, tap, K, n=None, stride=1):
     return out
 
 
+def circ_shift(a, axis, tap, N):
+    """out[p] = a[(p - tap) mod N] for p in [0, N), a zero-padded to length N:
+    the side of a circular convolution as seen by position `tap` of the other
+    side."""
+    n = a.shape[axis]
+    q = (np.arange(N) - tap) % N
+    ok = q < n
+    shape = list(a.shape)
+    shape[axis] = N
+    out = np.zeros(shape, dtype=np.float64)
+    dst = [slice(None)] * a.ndim
+    dst[axis] = np.arange(N)[ok]
+    out[tuple(dst)] = np.take(a, q[ok], axis=axis)
+    return out
+
+
+def circ_shift_adjoint(g, axis, tap, N, n):
+    """Adjoint of circ_shift() for a side of length n: out[i] = g[(i + tap)
+    mod N], i in [0, n)."""
+    return np.take(g, (np.arange(n) + tap) % N, axis=axis)
+
+
 def step_convs(expr: Expr, A, B):
     """Convolved labels performed by the step merging operand sets A and B:
-    [(label, feature on A?)]."""
+    [(label, feature on A?)] for linear labels, [(label, None)] for circular
+    ones (taps over side B)."""
     la, lb = kept_labels(expr, A), kept_labels(expr, B)
     res = []
     for l in la:
         if l in lb and l in expr.conv:
-            if l not in expr.feature:
-                raise NotImplementedError(
-                    f"label {l} is convolved in more than two operands (multi-way); "
-                    "only two-way convolution is evaluated")
-            res.append((l, expr.feature[l] in set(A)))
+            if is_circular(expr, l):
+                res.append((l, None))
+            else:
+                res.append((l, expr.feature[l] in set(A)))
     return res
 
 
@@ -103,13 +125,19 @@ def pair_step(expr, letters, a, A, b, B):
     convs = step_convs(expr, A, B)
     taps = []
     for l, fa in convs:
-        K = label_size(expr, B, l) if fa else label_size(expr, A, l)
+        K = label_size(expr, B, l) if fa or fa is None else label_size(expr, A, l)
         taps.append(range(K))
     acc = None
     for combo in itertools.product(*taps):
         xa, xb, ca, cb = a, b, list(la), list(lb)
         for (l, fa), k in zip(convs, combo):
-            if fa:
+            if fa is None:
+                # circular: side A at (p - k) mod N against position k of side B
+                N = label_size(expr, tuple(A) + tuple(B), l)
+                xa = circ_shift(xa, ca.index(l), k, N)
+                xb = np.take(xb, k, axis=cb.index(l))
+                cb.remove(l)
+            elif fa:
                 K = label_size(expr, B, l)
                 xa = shift(xa, ca.index(l), k, K, stride_of(expr, l))
                 xb = np.take(xb, k, axis=cb.index(l))
@@ -169,11 +197,15 @@ def eval_definition(expr: Expr, arrays):
     each convolved label of the product of all operands' entries; the feature
     operand of a convolved label is read at s*p + k - c (zero outside; s the
     label's stride, 1 unless given), its filter operand at tap k, the output
-    at p."""
+    at p; a circular label's holders are read at positions summing to p
+    modulo N (zero past a holder's size)."""
     conv2 = {l: expr.feature[l] for l in expr.conv if l in expr.feature}
-    for l in expr.conv:
-        if len(expr.holders(l)) > 2:
-            raise NotImplementedError("multi-way convolution")
+    # circular labels: the first holder is read at (p - sum of the other
+    # holders' positions) mod N, the others at every position
+    circ = [l for l in expr.conv if is_circular(expr, l)]
+    first = {l: expr.holders(l)[0] for l in circ}
+    N = {l: expr.out_sizes[l] for l in circ}
+    ctaps = [(l, i) for l in circ for i in expr.holders(l)[1:]]
     K = {}
     for l, f in conv2.items():
         other = [i for i in expr.holders(l) if i != f][0]
@@ -190,13 +222,24 @@ def eval_definition(expr: Expr, arrays):
         s = 0.0
         for r in itertools.product(*[range(red_size[l]) for l in red]):
             rv = dict(zip(red, r))
-            for kk in itertools.product(*[range(K[l]) for l in conv2]):
+            for kk in itertools.product(*[range(K[l]) for l in conv2],
+                                        *[range(expr.sizes[i][l]) for l, i in ctaps]):
                 kv = dict(zip(conv2, kk))
+                cv = dict(zip(ctaps, kk[len(conv2):]))
                 prod = 1.0
                 for i, labs in enumerate(expr.inputs):
                     idx = []
                     for l in labs:
-                        if l in conv2:
+                        if l in first:
+                            if i == first[l]:
+                                pos = (ov[l] - sum(cv[(l, j)] for j in expr.holders(l)[1:])) % N[l]
+                                if pos >= expr.sizes[i][l]:
+                                    prod = 0.0
+                                    break
+                                idx.append(pos)
+                            else:
+                                idx.append(cv[(l, i)])
+                        elif l in conv2:
                             if i == conv2[l]:
                                 pos = stride_of(expr, l) * ov[l] + kv[l] - (K[l] - 1) // 2
                                 if pos < 0 or pos >= expr.sizes[i][l]:

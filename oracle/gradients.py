@@ -22,7 +22,8 @@ import itertools
 import numpy as np
 
 from .cost import kept_labels, label_size, stride_of
-from .evaluate import (_letters, _einsum, shift, shift_adjoint, step_convs,
+from .evaluate import (_letters, _einsum, shift, shift_adjoint, step_convs, circ_shift,
+                       circ_shift_adjoint,
                        leaf_tensor, dense_kernel, pair_step)
 from .notation import Expr
 
@@ -34,15 +35,22 @@ def pair_adjoint(expr, letters, a, A, b, B, dc):
     convs = step_convs(expr, A, B)
     taps = []
     for l, fa in convs:
-        taps.append(range(label_size(expr, B, l) if fa else label_size(expr, A, l)))
+        taps.append(range(label_size(expr, B, l) if fa or fa is None else label_size(expr, A, l)))
     da = np.zeros_like(a)
     db = np.zeros_like(b)
     for combo in itertools.product(*taps):
         xa, xb, ca, cb = a, b, list(la), list(lb)
-        a_shifts, b_shifts, a_taps, b_taps = [], [], [], []
+        a_shifts, b_shifts, a_taps, b_taps, a_circ = [], [], [], [], []
         for (l, fa), k in zip(convs, combo):
             s = stride_of(expr, l)
-            if fa:
+            if fa is None:
+                N = label_size(expr, tuple(A) + tuple(B), l)
+                a_circ.append((l, k, N, xa.shape[ca.index(l)]))
+                xa = circ_shift(xa, ca.index(l), k, N)
+                b_taps.append((l, k))
+                xb = np.take(xb, k, axis=cb.index(l))
+                cb.remove(l)
+            elif fa:
                 K = label_size(expr, B, l)
                 a_shifts.append((l, k, K, xa.shape[ca.index(l)], s))
                 xa = shift(xa, ca.index(l), k, K, s)
@@ -60,6 +68,8 @@ def pair_adjoint(expr, letters, a, A, b, B, dc):
         ga = _einsum(letters, dc, lc, xb, cb, ca)
         for l, k, K, n, s in a_shifts:
             ga = shift_adjoint(ga, ca.index(l), k, K, n, s)
+        for l, k, N, n in a_circ:
+            ga = circ_shift_adjoint(ga, ca.index(l), k, N, n)
         idx = [slice(None)] * da.ndim
         for l, k in a_taps:
             idx[la.index(l)] = k

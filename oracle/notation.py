@@ -51,6 +51,7 @@ class Expr:
     feature: dict = None    # conv label -> operand index of its feature side
     out_sizes: dict = None  # output label -> size
     stride: dict = None     # conv label -> stride (absent: 1)
+    circular: set = None    # conv labels convolved circularly (commutative)
 
     @property
     def n(self):
@@ -107,7 +108,7 @@ def parse(spec: str) -> Expr:
     return Expr(inputs=inputs, output=output, conv=conv)
 
 
-def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
+def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None, circular=()) -> Expr:
     """Attach operand sizes and resolve the feature side of each convolved label.
 
     Feature side (Appendix B, 'Convolution Varieties'): of the two operands
@@ -121,6 +122,14 @@ def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
     (a strided convolution is one of the non-commutative varieties of
     Appendix B): output position p reads the feature at s*p + k - c, and the
     output keeps ceil(I / s) positions (I = feature size).
+
+    Circular convolution (Appendix B: the only kind supported for a label held
+    by more than two operands, and commutative): every holder is zero-padded
+    to N, the largest of its sizes, and indices add modulo N,
+        out[p] = sum over i_1 + ... + i_m = p (mod N) of prod_k T_k[i_k],
+    p in [0, N).  Labels held by three or more operands are circular; a
+    two-way label is circular when listed in `circular` (then it has no
+    feature side).
     """
     if len(shapes) != expr.n:
         raise ValueError("one shape per operand is required")
@@ -140,10 +149,18 @@ def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
             if l in common and common[l] != d:
                 raise ValueError(f"label {l}: size {d} in operand {i} != {common[l]}")
             common[l] = d
+    circ = set()
+    for l in expr.conv:
+        if len(expr.holders(l)) > 2:
+            circ.add(l)
+    for l in circular or ():
+        if l not in expr.conv or len(expr.holders(l)) < 2:
+            raise ValueError(f"circular {l}: a convolved label held by two or more operands")
+        circ.add(l)
     feature = {}
     for l in expr.conv:
         hold = expr.holders(l)
-        if len(hold) == 2:
+        if len(hold) == 2 and l not in circ:
             a, b = hold
             da, db = sizes[a][l], sizes[b][l]
             if da != db:
@@ -165,7 +182,7 @@ def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
         if l in feature:            # same padding keeps the feature size (ceil(I / s) when strided)
             s_ = stride.get(l, 1)
             out_sizes[l] = -(-sizes[feature[l]][l] // s_)
-        elif l in expr.conv:        # one holder, or multi-way: the largest size
+        elif l in expr.conv:        # one holder, or circular: the largest size N
             out_sizes[l] = max(sizes[i][l] for i in expr.holders(l))
         else:
             out_sizes[l] = common[l]
@@ -173,4 +190,5 @@ def bind(expr: Expr, shapes, feature_operand: int = 0, strides=None) -> Expr:
     expr.feature = feature
     expr.out_sizes = out_sizes
     expr.stride = stride
+    expr.circular = circ
     return expr

@@ -14,7 +14,7 @@ from .binding import (CeError, ce_backward, ce_backward_noalloc, ce_expr_destroy
                       ce_timing_record, ce_version, lib, LIB_PATH,
                       CE_F32, CE_BF16, CE_COST_FWD, CE_COST_TRAIN_PAPER, CE_FLAG_GENERIC_ONLY,
                       CE_FLAG_NO_FUSION, CE_FLAG_SAVE_INTERMEDIATES, CE_FLAG_WIDE_OFFSETS, CE_NOALLOC_WORKSPACE_BYTES,
-                      CE_PAD_SAME_ZERO)
+                      CE_PAD_SAME_ZERO, CE_PAD_CIRCULAR)
 from .layer import GraphStep, Plan, plan, conv_einsum, contract_path, max_batch, step_bytes
 
 __all__ = [
@@ -25,5 +25,5 @@ __all__ = [
     "ce_timing_begin", "ce_timing_begin_kernel", "ce_timing_end", "ce_timing_record",
     "ce_version", "lib", "LIB_PATH", "GraphStep", "Plan", "plan", "conv_einsum", "contract_path", "max_batch", "step_bytes",
     "CE_F32", "CE_BF16", "CE_COST_FWD", "CE_COST_TRAIN_PAPER", "CE_FLAG_GENERIC_ONLY",
-    "CE_FLAG_NO_FUSION", "CE_FLAG_SAVE_INTERMEDIATES", "CE_FLAG_WIDE_OFFSETS", "CE_NOALLOC_WORKSPACE_BYTES", "CE_PAD_SAME_ZERO",
+    "CE_FLAG_NO_FUSION", "CE_FLAG_SAVE_INTERMEDIATES", "CE_FLAG_WIDE_OFFSETS", "CE_NOALLOC_WORKSPACE_BYTES", "CE_PAD_SAME_ZERO", "CE_PAD_CIRCULAR",
 ]

@@ -32,6 +32,7 @@ CE_FLAG_SAVE_INTERMEDIATES = 0x4
 CE_FLAG_WIDE_OFFSETS = 0x8
 CE_NOALLOC_WORKSPACE_BYTES = 64 << 20
 CE_PAD_SAME_ZERO = 0
+CE_PAD_CIRCULAR = 1
 
 _STATUS_NAMES = {0: "CE_OK", -1: "CE_ERR_PARSE", -2: "CE_ERR_SHAPE", -3: "CE_ERR_UNSUPPORTED",
                  -4: "CE_ERR_ARG", -5: "CE_ERR_WORKSPACE", -6: "CE_ERR_OVERFLOW", -7: "CE_ERR_HIP"}

@@ -60,7 +60,19 @@ ce_status ce_expr_set_conv(ce_expr* e, const char* label, ce_pad pad) {
         int id = find_label(*e, label);
         if (id < 0) fail(CE_ERR_ARG, std::string("unknown label ") + label);
         if (!e->is_conv(id)) fail(CE_ERR_ARG, std::string("label ") + label + " is not convolved");
-        if (pad != CE_PAD_SAME_ZERO) fail(CE_ERR_UNSUPPORTED, "only zero 'same' padding is implemented");
+        const int holders = popcount64(e->holders[id]);
+        if (pad == CE_PAD_SAME_ZERO) {
+            if (holders > 2)
+                fail(CE_ERR_UNSUPPORTED, std::string("label ") + label +
+                                             " is held by more than two operands: only circular");
+            e->circular[id] = 0;
+        } else if (pad == CE_PAD_CIRCULAR) {
+            if (holders < 2)
+                fail(CE_ERR_ARG, std::string("label ") + label + " is held by one operand only");
+            e->circular[id] = 1;
+        } else {
+            fail(CE_ERR_ARG, "unknown padding");
+        }
     });
 }
 

@@ -23,7 +23,8 @@ constexpr int kMaxConv = 4;   // convolved labels of one step
 // pos = a * p + b * j + g must lie in [0, lim) or the term is skipped.  This
 // covers the forward step (feature read at p + j - c, filter at j), the
 // gradient of the feature side (dC read at p - j + c) and the gradient of the
-// filter side (feature read at j + p - c, dC at j).
+// filter side (feature read at j + p - c, dC at j).  For a circular label the
+// position is first taken modulo N (cv_modL / cv_modR): indices add modulo N.
 struct GenericDesc {
     int32_t nout, nred, nconv;
     int32_t has_r;                     // 0: R is absent (treated as 1)
@@ -34,6 +35,8 @@ struct GenericDesc {
     int32_t cv_aL[kMaxConv], cv_bL[kMaxConv], cv_aR[kMaxConv], cv_bR[kMaxConv];
     int64_t cv_gL[kMaxConv], cv_limL[kMaxConv], cv_sL[kMaxConv];
     int64_t cv_gR[kMaxConv], cv_limR[kMaxConv], cv_sR[kMaxConv];
+    // circular labels: a position is first reduced modulo cv_mod? (0: not)
+    int64_t cv_modL[kMaxConv], cv_modR[kMaxConv];
 };
 
 enum KernelKind : int32_t {

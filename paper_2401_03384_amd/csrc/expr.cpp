@@ -45,7 +45,7 @@ int64_t ce_expr::size_in(int i, int l) const {
 }
 
 int ce_expr::feature_of(int l) const {
-    if (!is_conv(l) || ce::popcount64(holders[l]) != 2) return -1;
+    if (!is_conv(l) || ce::popcount64(holders[l]) != 2 || is_circular(l)) return -1;
     int a = ce::lowest_bit(holders[l]);
     int b = ce::lowest_bit(holders[l] & ~(1u << a));
     int64_t da = size_in(a, l), db = size_in(b, l);
@@ -160,6 +160,7 @@ ce_expr* parse_expr(const char* spec, int n_in, const int* ranks, const int64_t*
     e->dims.resize(n_in);
     e->holders.assign(e->names.size(), 0);
     e->stride.assign(e->names.size(), 1);
+    e->circular.assign(e->names.size(), 0);
     for (int i = 0; i < n_in; i++) {
         if (ranks[i] != (int)ops[i].size())
             fail(CE_ERR_SHAPE, "operand " + std::to_string(i) + ": rank " + std::to_string(ranks[i]) +
@@ -184,6 +185,10 @@ ce_expr* parse_expr(const char* spec, int n_in, const int* ranks, const int64_t*
             s = d;
         }
     }
+    // a label convolved among three or more operands is circular (the only
+    // multi-way kind, Appendix B 'Convolution Varieties')
+    for (int l = 0; l < e->num_labels(); l++)
+        if (e->is_conv(l) && ce::popcount64(e->holders[l]) > 2) e->circular[l] = 1;
     e->bound = true;
     return e.release();
 }

@@ -22,6 +22,7 @@ struct ce_expr {
     uint64_t out_mask = 0;                      // bit per output label
     std::vector<uint32_t> holders;              // label -> bitmask of operands holding it
     std::vector<int> stride;                    // label -> stride of a convolved label (1: none)
+    std::vector<uint8_t> circular;              // label -> convolved circularly (commutative)
     int feature_operand = 0;
     bool bound = false;
 
@@ -34,6 +35,7 @@ struct ce_expr {
     int feature_of(int l) const;
     int64_t out_size(int l) const;
     int stride_of(int l) const { return l < (int)stride.size() ? stride[l] : 1; }
+    bool is_circular(int l) const { return l < (int)circular.size() && circular[l]; }
     std::vector<int64_t> out_dims() const;
 };
 

@@ -3,7 +3,7 @@
 // Evaluates any pairwise step of the forward or backward pass described by a
 // GenericDesc: contraction, batch and outer-product labels by strides, each
 // convolved label by its affine position map with zero outside the operand
-// (same padding).  It is the reference HIP implementation every specialised
+// (same padding), or taken modulo N for a circular label.  It is the reference HIP implementation every specialised
 // kernel is checked against, and the fallback for steps no specialised kernel
 // takes.  Accumulation is float32; long reductions are split over the lanes
 // of a wavefront or a block and summed by a fixed butterfly / tree, so results
@@ -81,6 +81,8 @@ __device__ __forceinline__ float term(const GenericDesc& d, const TL* __restrict
             int64_t p = op.conv_p[k];
             int64_t pl = d.cv_aL[k] * p + d.cv_bL[k] * j + d.cv_gL[k];
             int64_t pr = d.cv_aR[k] * p + d.cv_bR[k] * j + d.cv_gR[k];
+            if (d.cv_modL[k]) pl = ((pl % d.cv_modL[k]) + d.cv_modL[k]) % d.cv_modL[k];
+            if (d.cv_modR[k]) pr = ((pr % d.cv_modR[k]) + d.cv_modR[k]) % d.cv_modR[k];
             if (pl < 0 || pl >= d.cv_limL[k] || pr < 0 || pr >= d.cv_limR[k]) return 0.f;
             offL += pl * d.cv_sL[k];
             offR += pr * d.cv_sR[k];

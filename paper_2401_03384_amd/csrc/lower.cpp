@@ -1163,7 +1163,10 @@ std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
                              ScratchAlloc& scratch) {
     (void)e;
     std::vector<Launch> out;
-    bool fast = !(flags & CE_FLAG_GENERIC_ONLY) && !op.generic_only &&
+    bool circular = false;   // circular maps run on the generic kernel only
+    for (const ConvMap& cm : op.convs)
+        if (cm.modL || cm.modR) circular = true;
+    bool fast = !(flags & CE_FLAG_GENERIC_ONLY) && !op.generic_only && !circular &&
                 (try_gemm(op, out) || try_wgrad(op, scratch, out) || try_dw(op, scratch, out) ||
                  try_cred(op, scratch, out) || try_cconv(op, out) || try_thinw(op, scratch, out) ||
                  try_tc(op, scratch, out, (flags & CE_FLAG_WIDE_OFFSETS) != 0));

@@ -59,6 +59,8 @@ uint64_t kept_mask(const ce_expr& e, uint32_t S) {
 // sides are merged; for a strided one, its ceil(I / s) output positions).
 int64_t size_in_set(const ce_expr& e, uint32_t S, int l) {
     if (e.stride_of(l) > 1 && (e.holders[l] & S) == e.holders[l]) return e.out_size(l);
+    // a circular label with two or more holders merged: its N positions
+    if (e.is_circular(l) && popcount64(e.holders[l] & S) >= 2) return e.out_size(l);
     int64_t m = 0;
     for (int i = 0; i < e.n; i++)
         if (((S >> i) & 1) && ((e.holders[l] >> i) & 1)) m = std::max(m, e.size_in(i, l));
@@ -78,7 +80,10 @@ uint64_t step_cost_sat(const ce_expr& e, uint32_t A, uint32_t B, ce_cost_mode mo
     for (int l = 0; l < e.num_labels(); l++) {
         bool ia = (ka >> l) & 1, ib = (kb >> l) & 1;
         if (!ia && !ib) continue;
-        if (ia && ib && e.is_conv(l)) {
+        if (ia && ib && e.is_circular(l)) {
+            // every pair of positions meets once (forward and each gradient)
+            plain = mul_sat(plain, mul_sat((uint64_t)size_in_set(e, A, l), (uint64_t)size_in_set(e, B, l)));
+        } else if (ia && ib && e.is_conv(l)) {
             uint64_t sa = size_in_set(e, A, l), sb = size_in_set(e, B, l);
             bool fa = feature_on_a(e, A, B, l);
             const uint64_t st = (uint64_t)e.stride_of(l);
@@ -283,6 +288,29 @@ struct Builder {
         uint64_t ka = kept_mask(e, A), kb = kept_mask(e, B);
         for (int l = 0; l < e.num_labels(); l++) {
             if (!e.is_conv(l) || !((ka >> l) & 1) || !((kb >> l) & 1)) continue;
+            if (e.is_circular(l)) {
+                // C[p] = sum_j A[(p - j) mod N] B[j]; dA[i] = sum_j dC[(i + j) mod N] B[j];
+                // dB[j] = sum_i A[i] dC[(i + j) mod N]
+                const int64_t sa = size_in_set(e, A, l), sb = size_in_set(e, B, l);
+                const int64_t N = e.out_size(l);
+                ConvMap m{};
+                m.label = l;
+                if (which == 0) {
+                    m.O = N; m.J = sb;
+                    m.aL = 1; m.bL = -1; m.gL = 0; m.limL = sa; m.modL = N;
+                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = sb;
+                } else if (which == 1) {
+                    m.O = sa; m.J = sb;
+                    m.aL = 1; m.bL = 1; m.gL = 0; m.limL = N; m.modL = N;
+                    m.aR = 0; m.bR = 1; m.gR = 0; m.limR = sb;
+                } else {
+                    m.O = sb; m.J = sa;
+                    m.aL = 0; m.bL = 1; m.gL = 0; m.limL = sa;
+                    m.aR = 1; m.bR = 1; m.gR = 0; m.limR = N; m.modR = N;
+                }
+                v.push_back(m);
+                continue;
+            }
             bool fa = feature_on_a(e, A, B, l);
             int64_t I = size_in_set(e, fa ? A : B, l);
             int64_t K = size_in_set(e, fa ? B : A, l);
@@ -401,11 +429,6 @@ struct Builder {
         return out;
     }
 
-    bool has_multiway() const {
-        for (int l = 0; l < e.num_labels(); l++)
-            if (e.is_conv(l) && popcount64(e.holders[l]) > 2) return true;
-        return false;
-    }
 };
 
 // ---- workspace layout: greedy interval packing ---------------------------
@@ -561,6 +584,8 @@ Launch lower_generic(const PairOp& op) {
         d.cv_gR[k] = m.gR;
         d.cv_limR[k] = m.limR;
         d.cv_sR[k] = op.has_r ? op.R.stride_of(m.label) : 0;
+        d.cv_modL[k] = m.modL;
+        d.cv_modR[k] = m.modR;
     }
     Launch ln;
     ln.a = op.L.buf;
@@ -653,17 +678,16 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
     p->ltr_cost = bld.left_to_right_cost();
     bld.assign_layouts();
 
-    if (bld.has_multiway()) {
-        p->executable = false;
-        p->why_not = "a convolved label is held by more than two operands (multi-way)";
-    }
+    for (int l = 0; l < E.num_labels(); l++)
+        if (E.is_circular(l) && E.stride_of(l) > 1)
+            fail(CE_ERR_UNSUPPORTED, "label " + E.names[l] + ": a circular convolution has no stride");
     DType dt = dtype == CE_BF16 ? DT_BF16 : DT_F32;
     int m = (int)p->steps.size();
-    // the fused chains are written for stride-1 convolutions
-    bool strided = false;
+    // the fused chains are written for stride-1, zero-padded convolutions
+    bool special = false;
     for (int l = 0; l < E.num_labels(); l++)
-        if (E.stride_of(l) > 1) strided = true;
-    if (strided) flags |= CE_FLAG_NO_FUSION;
+        if (E.stride_of(l) > 1 || E.is_circular(l)) special = true;
+    if (special) flags |= CE_FLAG_NO_FUSION;
 
     if (p->executable) {
         // Workspace items: intermediates (id = node), their gradients

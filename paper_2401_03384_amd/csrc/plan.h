@@ -34,8 +34,8 @@ struct TensorRef {
 };
 
 // One convolved label of a pairwise step (see GenericDesc): output index p in
-// [0, O), reduction index j in [0, J), operand position a*p + b*j + g, valid
-// in [0, lim).
+// [0, O), reduction index j in [0, J), operand position a*p + b*j + g (taken
+// modulo `mod` for a circular label), valid in [0, lim).
 struct ConvMap {
     int label;
     int64_t O, J;
@@ -43,6 +43,7 @@ struct ConvMap {
     int64_t gL, limL;
     int aR, bR;
     int64_t gR, limR;
+    int64_t modL = 0, modR = 0;   // circular label: position taken modulo N first
 };
 
 // C = sum over the reduced labels (and taps) of L * R.

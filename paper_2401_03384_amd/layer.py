@@ -27,11 +27,12 @@ class Plan:
     (bytes) lets the backward read that much of the forward's intermediates
     instead of recomputing them (the backward must then get the forward's
     workspace, see `forward(..., workspace=)`); `strides` maps convolved
-    labels to their stride."""
+    labels to their stride; `circular` lists two-way convolved labels to
+    convolve circularly (labels of three or more operands always are)."""
 
     def __init__(self, spec: str, shapes, dtype: str = "f32", mode: str = "fwd", flags: int = 0,
                  path=None, feature_operand: int = 0, max_elements=None, max_step_cost=None,
-                 save_budget=None, strides=None):
+                 save_budget=None, strides=None, circular=()):
         if dtype not in _DT:
             raise ValueError(f"dtype must be one of {list(_DT)}")
         self.spec = spec
@@ -47,6 +48,8 @@ class Plan:
             self.strides = dict(strides or {})
             for label, st in self.strides.items():
                 B.ce_expr_set_stride(self._expr, label, st)
+            for label in circular:
+                B.ce_expr_set_conv(self._expr, label, B.CE_PAD_CIRCULAR)
             self.out_shape = B.ce_expr_output_shape(self._expr)
             if path is None and (max_step_cost is not None or save_budget is not None):
                 self._plan = B.ce_plan_create_ex(self._expr, _MODE[mode], _DT[dtype], flags,

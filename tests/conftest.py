@@ -72,6 +72,21 @@ EDGE_CASES = {
     "equal_sizes_feature1": ("bsh,tsh->bth|h", [(2, 3, 5), (4, 3, 5)], 1),
     "even_filter_conv": ("bshw,tshw->bthw|hw", [(2, 3, 9, 10), (4, 3, 4, 4)], 0),
     "even_filter_cp": ("bshw,rs,rt,rh,rw->bthw|hw", [(2, 6, 9, 9), (3, 6), (3, 5), (3, 4), (3, 2)], 0),
+    # three and four convolved labels in one step (conv3d, conv4d; Section 3.1)
+    "conv3d": ("bsdhw,tsdhw->btdhw|dhw", [(2, 3, 6, 7, 8), (4, 3, 3, 3, 3)], 0),
+    "conv4d": ("bsdhwx,tsdhwx->btdhwx|dhwx", [(1, 2, 5, 6, 4, 5), (3, 2, 3, 3, 2, 3)], 0),
+}
+
+# Circular (commutative) convolutions, Appendix B: (string, shapes, two-way
+# labels made circular).  Labels held by three or more operands are circular
+# by default.
+CIRCULAR_CASES = {
+    "circ_3way_1d": ("bi,ci,di->bcdi|i", [(2, 9), (3, 3), (2, 4)], ()),
+    "circ_2way": ("bsh,tsh->bth|h", [(2, 3, 8), (4, 3, 5)], ("h",)),
+    "circ_2way_2d": ("bshw,tshw->bthw|hw", [(2, 3, 7, 6), (4, 3, 3, 4)], ("h", "w")),
+    "circ_interleaved": ("bmshw,nmhw,tshw->bnthw|hw",
+                         [(2, 3, 4, 9, 10), (5, 3, 3, 3), (4, 4, 5, 2)], ()),
+    "circ_4way": ("ai,bi,ci,di->abcdi|i", [(2, 7), (2, 3), (1, 7), (2, 2)], ()),
 }
 
 

@@ -140,6 +140,8 @@ bool run_generic(const Launch& ln, Ctx& c) {
                 int64_t p = oidx[d.cv_out[k]], j = ridx[d.cv_red[k]];
                 int64_t pl = d.cv_aL[k] * p + d.cv_bL[k] * j + d.cv_gL[k];
                 int64_t pr = d.cv_aR[k] * p + d.cv_bR[k] * j + d.cv_gR[k];
+                if (d.cv_modL[k]) pl = ((pl % d.cv_modL[k]) + d.cv_modL[k]) % d.cv_modL[k];
+                if (d.cv_modR[k]) pr = ((pr % d.cv_modR[k]) + d.cv_modR[k]) % d.cv_modR[k];
                 if (pl < 0 || pl >= d.cv_limL[k] || pr < 0 || pr >= d.cv_limR[k]) { skip = true; break; }
                 aL += pl * d.cv_sL[k];
                 aR += pr * d.cv_sR[k];
@@ -1379,6 +1381,9 @@ void emul_set_save_budget(uint64_t bytes) { g_save_budget = bytes; }
 // Strides of convolved labels for the next plans: "h=2,w=2" ("" for none).
 static std::string g_strides;
 void emul_set_strides(const char* spec) { g_strides = spec ? spec : ""; }
+// Two-way convolved labels made circular for the next plans: "h,w" ("" none).
+static std::string g_circular;
+void emul_set_circular(const char* spec) { g_circular = spec ? spec : ""; }
 // 1: the next plans take the left-to-right order ((0,1),(0,n-2),...,(0,1))
 static int g_ltr = 0;
 void emul_set_path(int ltr) { g_ltr = ltr; }
@@ -1407,6 +1412,16 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
         PlanLimits lim;
         if (g_limit) lim.max_elements = g_limit;
         lim.save_budget = g_save_budget;
+        for (size_t pos = 0; pos < g_circular.size();) {
+            size_t end = g_circular.find(',', pos);
+            if (end == std::string::npos) end = g_circular.size();
+            const std::string lab = g_circular.substr(pos, end - pos);
+            if (ce_expr_set_conv(e.get(), lab.c_str(), CE_PAD_CIRCULAR) != CE_OK) {
+                std::snprintf(err, errlen, "bad circular label %s", lab.c_str());
+                return 3;
+            }
+            pos = end + 1;
+        }
         std::vector<int> pairs;
         if (g_ltr && n > 1) {
             pairs = {0, 1};

@@ -216,11 +216,11 @@ def test_execution_errors_before_any_device_call():
     L = B.lib()
     fake = C.c_void_p(0x1000)
     ins = (C.c_void_p * 2)(fake, fake)
-    # multi-way convolution: planned, not executable
+    # a circular plan with a too small workspace
     p = _plan("bfhw,fghw,sghw->bshw|hw", [(1, 2, 5, 5), (2, 3, 3, 3), (4, 3, 3, 3)])
     ins3 = (C.c_void_p * 3)(fake, fake, fake)
-    assert L.ce_forward(p, ins3, fake, fake, 1 << 20, None) == B.CE_ERR_UNSUPPORTED
-    assert "multi-way" in B.ce_last_error()
+    assert B.ce_plan_workspace_size(p, 0) > 0
+    assert L.ce_forward(p, ins3, fake, fake, 0, None) == B.CE_ERR_WORKSPACE
     B.ce_plan_destroy(p)
     p = _plan("bshw,tshw->bthw|hw", [(2, 3, 8, 8), (4, 3, 3, 3)])
     assert L.ce_forward(p, ins, None, None, 0, None) == B.CE_ERR_ARG
@@ -298,16 +298,30 @@ def test_saved_intermediates_plan():
 
 
 def test_set_conv():
-    """Padding of a convolved label: zero 'same' accepted, anything else
-    unsupported; unknown or non-convolved labels are argument errors."""
+    """Padding of a convolved label: zero 'same' or circular on a two-way
+    label, circular only on a multi-way label; unknown paddings, unknown or
+    non-convolved labels are argument errors."""
     e = B.ce_expr_parse("bshw,sthw->bthw|hw", [(1, 2, 5, 5), (2, 3, 3, 3)])
     try:
         B.ce_expr_set_conv(e, "h", B.CE_PAD_SAME_ZERO)
-        for label, pad, status in (("w", 1, B.CE_ERR_UNSUPPORTED), ("s", 0, B.CE_ERR_ARG),
+        B.ce_expr_set_conv(e, "w", B.CE_PAD_CIRCULAR)
+        for label, pad, status in (("w", 7, B.CE_ERR_ARG), ("s", 0, B.CE_ERR_ARG),
                                    ("z", 0, B.CE_ERR_ARG)):
             with pytest.raises(B.CeError) as ex:
                 B.ce_expr_set_conv(e, label, pad)
             assert ex.value.status == status
+        with pytest.raises(B.CeError) as ex:
+            B.ce_expr_set_stride(e, "w", 2)
+            B.ce_plan_destroy(B.ce_plan_create(e, B.CE_COST_FWD, B.CE_F32, 0))
+        assert ex.value.status == B.CE_ERR_UNSUPPORTED
+    finally:
+        B.ce_expr_destroy(e)
+    e = B.ce_expr_parse("bfhw,fghw,sghw->bshw|hw", [(1, 2, 5, 5), (2, 3, 3, 3), (4, 3, 3, 3)])
+    try:
+        B.ce_expr_set_conv(e, "h", B.CE_PAD_CIRCULAR)
+        with pytest.raises(B.CeError) as ex:
+            B.ce_expr_set_conv(e, "w", B.CE_PAD_SAME_ZERO)
+        assert ex.value.status == B.CE_ERR_UNSUPPORTED
     finally:
         B.ce_expr_destroy(e)
 

@@ -13,7 +13,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from conftest import STRIDED_CASES, strides_of, PAPER_SHAPES, ROOT, load_layer_strings
+from conftest import CIRCULAR_CASES, EDGE_CASES, STRIDED_CASES, strides_of, PAPER_SHAPES, ROOT, load_layer_strings
 
 STRINGS = load_layer_strings()
 
@@ -211,8 +211,6 @@ def test_emulated_paper_strings(emul, name, bf16):
     spec = STRINGS[name][0]
     shapes = PAPER_SHAPES[name]
     e = O.bind(O.parse(spec), shapes)
-    if any(len(e.holders(l)) > 2 for l in e.conv):
-        pytest.skip("a convolved label held by more than two operands is planned, not executed")
     tol = 2e-2 if bf16 else 1e-5
     rng = np.random.default_rng(7)
     ins = [rng.standard_normal(s).astype(np.float32) for s in shapes]
@@ -321,6 +319,50 @@ def test_emulated_resnet34_cp_layers(emul, name, order):
     finally:
         emul.emul_set_strides(b"")
         emul.emul_set_path(0)
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= 1e-5
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= 1e-5
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(CIRCULAR_CASES))
+def test_emulated_circular(emul, name, bf16):
+    """Circular convolutions (two-, three- and four-way), every access of the
+    generic kernel's modulo positions bounds-checked, against the oracle."""
+    spec, shapes, circ = CIRCULAR_CASES[name]
+    e = O.bind(O.parse(spec), shapes, circular=circ)
+    tol = 2e-2 if bf16 else 1e-5
+    rng = np.random.default_rng(5)
+    ins = [rng.standard_normal(s).astype(np.float32) for s in shapes]
+    ins = [(W.round_to_bf16(a) if bf16 else a).astype(np.float64) for a in ins]
+    out_shape = tuple(e.out_sizes[l] for l in e.output)
+    dy = rng.standard_normal(out_shape).astype(np.float32)
+    dy = (W.round_to_bf16(dy) if bf16 else dy).astype(np.float64)
+    tree = O.optimal_tree(e)[0]
+    emul.emul_set_circular(",".join(circ).encode())
+    try:
+        y = _run(emul, spec, shapes, bf16, 0, ins, out_shape=out_shape, generic=0)
+        g = _run(emul, spec, shapes, bf16, 1, ins, dy=dy, generic=0)
+    finally:
+        emul.emul_set_circular(b"")
+    assert _rel(y, O.eval_pairwise(e, ins, tree)) <= tol
+    for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
+        assert _rel(a, b) <= tol
+
+
+@pytest.mark.parametrize("name", ["conv3d", "conv4d"])
+def test_emulated_convnd(emul, name):
+    """Three and four convolved labels in one step (Section 3.1: conv3d and
+    beyond), bounds-checked, vs the oracle."""
+    spec, shapes, _ = EDGE_CASES[name]
+    e = O.bind(O.parse(spec), shapes)
+    rng = np.random.default_rng(6)
+    ins = [rng.standard_normal(s).astype(np.float32).astype(np.float64) for s in shapes]
+    out_shape = tuple(e.out_sizes[l] for l in e.output)
+    dy = rng.standard_normal(out_shape).astype(np.float32).astype(np.float64)
+    tree = O.optimal_tree(e)[0]
+    y = _run(emul, spec, shapes, False, 0, ins, out_shape=out_shape, generic=0)
+    g = _run(emul, spec, shapes, False, 1, ins, dy=dy, generic=0)
     assert _rel(y, O.eval_pairwise(e, ins, tree)) <= 1e-5
     for a, b in zip(g, O.grads_pairwise(e, ins, tree, dy)):
         assert _rel(a, b) <= 1e-5

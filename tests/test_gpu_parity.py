@@ -20,7 +20,8 @@ import pytest
 
 import oracle as O
 import workloads as W
-from conftest import EDGE_CASES, PAPER_SHAPES, STRIDED_CASES, load_layer_strings, strides_of
+from conftest import (CIRCULAR_CASES, EDGE_CASES, PAPER_SHAPES, STRIDED_CASES, load_layer_strings,
+                      strides_of)
 
 STRINGS = load_layer_strings()
 
@@ -202,8 +203,10 @@ def test_saved_intermediates(P, name):
 def test_paper_layer_strings(P, name, dtype):
     """Every layer string the paper prints (CP, reshaped CP, Tucker, reshaped
     Tucker, tensor-train and -ring, block-term, hierarchical Tucker, separable
-    and interleaved group convolutions, conv1d, grouped conv, contractions)
-    through the default plan, forward and all gradients, against the oracle."""
+    and interleaved group convolutions (circular: h, w held by three
+    operands), the Figure 1 sequence example (circular j), conv1d, grouped
+    conv, mode convolution, contractions, outer and batch products) through
+    the default plan, forward and all gradients, against the oracle."""
     spec = STRINGS[name][0]
     shapes = PAPER_SHAPES[name]
     bf16 = dtype == "bf16"
@@ -211,8 +214,6 @@ def test_paper_layer_strings(P, name, dtype):
     _say(f"case {name} {dtype} {spec} shapes={shapes}")
     e = O.bind(O.parse(spec), shapes)
     plan = P.Plan(spec, shapes, dtype)
-    if "not executable" in plan.describe():
-        pytest.skip("a convolved label held by more than two operands (multi-way) is planned, not executed")
     rng = np.random.default_rng(7)
     ins = [rng.standard_normal(s) for s in shapes]
     if bf16:
@@ -282,11 +283,11 @@ def test_graph_replay(P, name):
         torch.cuda.synchronize()
 
 
-def _random_case(spec, shapes, dtype, feat=0, seed=7, strides=None):
+def _random_case(spec, shapes, dtype, feat=0, seed=7, strides=None, circular=()):
     """Seeded N(0,1) operands and dY for a small case, rounded to the storage
     type; the oracle expression bound with the same feature operand."""
     bf16 = dtype == "bf16"
-    e = O.bind(O.parse(spec), shapes, feature_operand=feat, strides=strides)
+    e = O.bind(O.parse(spec), shapes, feature_operand=feat, strides=strides, circular=circular)
     rng = np.random.default_rng(seed)
     rnd = (lambda a: W.round_to_bf16(a.astype(np.float32))) if bf16 else (lambda a: a.astype(np.float32))
     ins = [rnd(rng.standard_normal(s)).astype(np.float64) for s in shapes]
@@ -469,3 +470,29 @@ def test_resnet34_cp_layers(P, name, dtype, order):
     grads = plan.backward(xs, _dev(dy, bf16))
     torch.cuda.synchronize()
     _check_all(w.name, y, O.eval_pairwise(e, ins, tree), grads, O.grads_pairwise(e, ins, tree, dy), tol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(CIRCULAR_CASES))
+def test_circular(P, name, dtype):
+    """Circular convolutions (Appendix B: commutative, the only kind for a
+    label held by three or more operands), two-, three- and four-way, through
+    the planned order and every other tree's first steps, against the oracle
+    along the same tree."""
+    spec, shapes, circ = CIRCULAR_CASES[name]
+    bf16 = dtype == "bf16"
+    tol = 2e-2 if bf16 else 1e-5
+    e, ins, dy = _random_case(spec, shapes, dtype, circular=circ)
+    n = len(shapes)
+    paths = [None, [(0, 1)] + [(0, n - 1 - k) for k in range(1, n - 1)]]
+    trees = [O.optimal_tree(e)[0], O.left_to_right_tree(n)]
+    xs = [_dev(a, bf16) for a in ins]
+    for path, tree in zip(paths, trees):
+        _say(f"case {name} {dtype} {spec} shapes={shapes} tree {tree}")
+        plan = P.Plan(spec, shapes, dtype, path=path, circular=circ)
+        assert tuple(plan.out_shape) == dy.shape
+        y = plan.forward(xs)
+        grads = plan.backward(xs, _dev(dy, bf16))
+        torch.cuda.synchronize()
+        _check_all(name, y, O.eval_pairwise(e, ins, tree), grads,
+                   O.grads_pairwise(e, ins, tree, dy), tol)

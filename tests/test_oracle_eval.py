@@ -161,12 +161,74 @@ def test_constant_input_border_closed_form():
         np.testing.assert_allclose(y[0, :, h, w], Ut[0] * Us.sum() * sh * sw, rtol=1e-13)
 
 
-def test_multiway_convolution_is_not_evaluated():
-    e = _e(STRINGS["interleaved_group"][0], [(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)])
-    with pytest.raises(NotImplementedError):
-        O.eval_definition(e, _rand([(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)]))
-    with pytest.raises(NotImplementedError):
-        O.eval_pairwise(e, _rand([(1, 2, 2, 5, 5), (2, 2, 3, 3), (2, 2, 3, 3)]), ((0, 1), 2))
+def _circ_fft(arrays_axes, N):
+    """Circular convolution of 1-D signals (zero-padded to N) by the DFT
+    identity: ifft(prod fft(a_k, N))."""
+    f = np.ones(N, dtype=complex)
+    for a in arrays_axes:
+        f = f * np.fft.fft(a, N)
+    return np.fft.ifft(f).real
+
+
+@pytest.mark.parametrize("sizes", [(9, 3, 4), (6, 6, 6), (5, 7, 2), (4, 4, 9)])
+def test_multiway_circular_matches_dft(sizes):
+    """A label held by three operands is convolved circularly (Appendix B):
+    the definition and every pairwise tree equal the DFT identity (numpy.fft)
+    with N the largest size; the result is the same in every order
+    (commutative and associative)."""
+    g = np.random.default_rng(sum(sizes))
+    arr = [g.standard_normal(n) for n in sizes]
+    e = _e("i,i,i->i|i", [(n,) for n in sizes])
+    assert e.circular == {"i"} and e.out_sizes["i"] == max(sizes)
+    ref = _circ_fft(arr, max(sizes))
+    np.testing.assert_allclose(O.eval_definition(e, arr), ref, rtol=1e-12, atol=1e-12)
+    for t in O.all_trees(range(3)):
+        np.testing.assert_allclose(O.eval_pairwise(e, arr, t), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_two_way_circular_matches_dft():
+    """A two-way label chosen circular: batched 1-D circular convolution,
+    y[b, t] = sum_s x[b, s] (*) f[t, s], by the DFT along h."""
+    g = np.random.default_rng(3)
+    X, F = g.standard_normal((2, 3, 8)), g.standard_normal((4, 3, 5))
+    e = O.bind(O.parse("bsh,tsh->bth|h"), [X.shape, F.shape], circular=("h",))
+    ref = np.fft.ifft(np.einsum("bsh,tsh->bth", np.fft.fft(X, 8, axis=-1),
+                                np.fft.fft(F, 8, axis=-1))).real
+    np.testing.assert_allclose(O.eval_definition(e, [X, F]), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.eval_pairwise(e, [X, F], (0, 1)), ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("name", ["interleaved_group", "interleaved_group_sec2"])
+def test_interleaved_group_conv_matches_dft(name):
+    """The interleaved group convolutions of Section 2.2 and Appendix A.3.1
+    (h, w held by three operands, circular): the definition and every tree
+    equal the 2-D DFT identity, a product of the three transforms summed over
+    the contracted channels."""
+    spec = STRINGS[name][0]
+    shapes = [(1, 2, 2, 5, 6), (2, 2, 3, 3), (3, 2, 2, 4)] if name == "interleaved_group" \
+        else [(1, 2, 2, 5, 6), (2, 2, 3, 3), (2, 3, 2, 4)]
+    g = np.random.default_rng(4)
+    arr = [g.standard_normal(s) for s in shapes]
+    e = _e(spec, shapes)
+    N = (5, 6)
+    F = [np.fft.fft2(a, N) for a in arr]
+    lhs, out = spec.split("|")[0].split("->")
+    ops = lhs.split(",")
+    ref = np.fft.ifft2(np.einsum(",".join(ops) + "->" + out, *F), axes=(-2, -1)).real
+    np.testing.assert_allclose(O.eval_definition(e, arr), ref, rtol=1e-11, atol=1e-11)
+    for t in O.all_trees(range(3)):
+        np.testing.assert_allclose(O.eval_pairwise(e, arr, t), ref, rtol=1e-11, atol=1e-11)
+
+
+def test_circular_cost_hand_values():
+    """A circular step meets every pair of positions once: sizes 9, 3, 4 give
+    9*3 then (N = 9)*4 along ((0,1),2), and 3*4 then 9*9 along (0,(1,2))
+    (merging two holders gives an N-position tensor)."""
+    e = _e("i,i,i->i|i", [(9,), (3,), (4,)])
+    assert O.step_costs(e, ((0, 1), 2)) == [27, 36]
+    assert O.step_costs(e, (0, (1, 2))) == [12, 81]
+    assert O.intermediate_size(e, (1, 2)) == 9
+    assert O.optimal_tree(e) == (((0, 1), 2), 63)
 
 
 def test_self_contracted_label_is_presummed():

@@ -169,3 +169,34 @@ def test_finite_differences_strided(spec, shapes, strides):
             am[i][idx] -= eps
             fd = ((O.eval_definition(e, ap) - O.eval_definition(e, am)) * dy).sum() / (2 * eps)
             assert abs(fd - grads[i][idx]) <= 1e-7 * max(1.0, abs(fd)), (i, idx)
+
+
+@pytest.mark.parametrize("spec,shapes,circ", [
+    ("i,i,i->i|i", [(9,), (3,), (4,)], ()),
+    ("bsh,tsh->bth|h", [(2, 2, 7), (3, 2, 4)], ("h",)),
+    ("bmshw,nmhw,tshw->bnthw|hw", [(1, 2, 2, 4, 5), (2, 2, 2, 3), (2, 2, 3, 2)], ()),
+])
+def test_finite_differences_circular(spec, shapes, circ):
+    """Circular (commutative) convolutions, multi-way and two-way: pairwise
+    gradients along every tree against central differences of the plain
+    definition, and the multilinearity identity."""
+    e = O.bind(O.parse(spec), shapes, circular=circ)
+    g = np.random.default_rng(13)
+    arr = [g.standard_normal(s) for s in shapes]
+    y = O.eval_definition(e, arr)
+    dy = g.standard_normal(y.shape)
+    ydy = float((y * dy).sum())
+    for t in O.all_trees(range(e.n)):
+        grads = O.grads_pairwise(e, arr, t, dy)
+        for a, gr in zip(arr, grads):
+            assert abs(float((a * gr).sum()) - ydy) <= 1e-10 * max(1.0, abs(ydy))
+    grads = O.grads_pairwise(e, arr, O.optimal_tree(e)[0], dy)
+    eps = 1e-6
+    for i, a in enumerate(arr):
+        for idx in list(np.ndindex(*a.shape))[::max(1, a.size // 10)]:
+            ap = [x.copy() for x in arr]
+            am = [x.copy() for x in arr]
+            ap[i][idx] += eps
+            am[i][idx] -= eps
+            fd = ((O.eval_definition(e, ap) - O.eval_definition(e, am)) * dy).sum() / (2 * eps)
+            assert abs(fd - grads[i][idx]) <= 1e-7 * max(1.0, abs(fd)), (i, idx)
