@@ -64,6 +64,8 @@ enum KernelKind : int32_t {
     K_RCP_BWD = 34,         // fused reshaped-CP chain backward (RcpBwdDesc, desc_rcp.h)
     K_RCP_PREP = 35,        // its prepared factor table (RcpBwdDesc)
     K_CCONV = 36,           // convolution contracted over one channel index, MFMA tiles (CconvDesc)
+    K_TT_FWD = 37,          // fused contraction + convolution of a tensor-train chain (TtDesc)
+    K_TT_PREP = 38,         // its convolution's A operands in load order (TtDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -283,6 +285,29 @@ struct CpBwdDesc {
     // share the wave's dY tile: o_tz == o_yt, tz_stride == yt_bytes)
     uint32_t o_xl, xl_bytes, tz_stride;
     int32_t lx;
+};
+
+// Two consecutive steps of a (reshaped) tensor-train layer fused so that the
+// first step's result never leaves the chip:
+//   Z[b][g][u][r][p] = sum_k X[b][k][u][p] * F1[g][k][r]                (step A)
+//   Y[b][g][t][p]    = sum_{u, r, taps} Z[b][g][u][r][p + tap - c] * F2[t][u][r][tap]   (step B)
+// p = (h, w) over an H x W plane (dense, w unit-stride, in X and Y), the
+// taps KH x KW with zero 'same' padding.  Each index set (b, g, k, u, r, t)
+// is one linear index per tensor (its labels' strides chain).  A block takes
+// one (b, g) and TH output rows: per u it forms the R = 16 channels of Z on
+// the TH + KH - 1 rows it needs (MFMA 16x16x4: M = r, N = 16 pixels,
+// K = k) in LDS, then accumulates step B on MFMA 16x16x4 tiles whose M rows
+// are (t, one of two output rows) and whose K runs over (r, KH + 1 tap rows,
+// KW tap columns), so the T <= 8 output channels fill the tile.
+struct TtDesc {
+    int32_t B, G, K1, U, R, T, H, W;
+    int32_t TH, nbands, XT, PW, plane, ncombo;
+    int64_t x_sb, x_sk, x_su, y_sb, y_sg, y_st;
+    int64_t f1_sg, f1_sk, f1_sr;
+    int64_t f2_st, f2_su, f2_sr, f2_sh, f2_sw;
+    int64_t x_numel, f1_numel, f2_numel;   // element extents of the operands (< 2^29)
+    int64_t blocks;
+    uint32_t lds_bytes, xcd_remap;          // xcd_remap: blocks % 8 == 0, runs of a sample on one XCD
 };
 
 }  // namespace ce

@@ -50,6 +50,11 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
                                   resolve(ln.extra[2], P)};
             return launch_cp_fwd(ln, ops, c, s);
         }
+        case K_TT_FWD:
+        case K_TT_PREP: {
+            const void* ops[4] = {a, b, resolve(ln.extra[0], P), resolve(ln.extra[1], P)};
+            return launch_tt_fwd(ln, ops, c, s);
+        }
         case K_RCP_FWD: {
             const void* ops[5] = {a, b, resolve(ln.extra[0], P), resolve(ln.extra[1], P),
                                   resolve(ln.extra[2], P)};

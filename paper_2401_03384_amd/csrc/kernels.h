@@ -37,6 +37,10 @@ hipError_t launch_thin(const Launch& ln, const void* a, const void* b, void* c, 
 // K_TC_REDUCE: d = partials, c = C).
 hipError_t launch_tc(const Launch& ln, const void* a, const void* b, void* c, void* d, hipStream_t s);
 
+// Fused tensor-train contraction + convolution forward (K_TT_FWD) and its
+// prepared convolution operands (K_TT_PREP): ops = {X, F1, F2, A2}, y = Y.
+hipError_t launch_tt_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
+
 // Fused CP chain forward: ops = {X, Us, Kh, Kw, Ut}.
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s);
 

@@ -769,18 +769,68 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.what = "unary";
             for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
         }
+        std::vector<PairOp> fops(m);
         for (int s = 0; s < m; s++) {
             const Step& st = p->steps[s];
-            PairOp op;
+            PairOp& op = fops[s];
             op.L = fval(st.a);
             op.R = fval(st.b);
             op.C = fval(st.c);
             op.convs = bld.conv_maps(st, 0);
             op.macs = st.macs;
+            op.need = 0x7fffffff;
             op.what = "step " + std::to_string(s) + " fwd " + tensor_str(E, op.L) + "," +
                       tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
+        }
+        // a contraction whose result only feeds a convolution of the
+        // tensor-train pattern runs fused with it (the result stays on chip)
+        std::vector<int> fused_to(m, -1), fused_from(m, -1);
+        std::vector<Launch> fused(m);
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) {
+            for (int s = 0; s + 1 < m; s++) {
+                const int cs = consumer_step(p->steps[s].c);
+                if (cs >= m || fused_from[s] >= 0 || fused_to[s] >= 0 || fused_from[cs] >= 0) continue;
+                Launch ln;
+                if (!fuse_tt_forward(fops[s], fops[cs], ln)) continue;
+                fused_to[s] = cs;
+                fused_from[cs] = s;
+                ln.need = 0;
+                ln.what = "fused tensor-train steps " + std::to_string(s) + "+" + std::to_string(cs) + ": " +
+                          fops[s].what.substr(fops[s].what.find("fwd ") + 4) + " then " +
+                          fops[cs].what.substr(fops[cs].what.find("fwd ") + 4);
+                fused[cs] = ln;
+                // the producer's operands are read at the consumer's position now
+                for (const TensorRef* t : {&fops[s].L, &fops[s].R})
+                    if (t->buf.kind == BUF_WS)
+                        for (WsItem& it : items)
+                            if (it.id == t->buf.index) it.t1 = std::max(it.t1, cs);
+            }
+        }
+        for (int s = 0; s < m; s++) {
+            if (fused_to[s] >= 0) continue;
+            if (fused_from[s] >= 0) {
+                // the convolution's A operands laid out in load order, then the fused launch
+                Launch ln = fused[s];
+                TtDesc td;
+                std::memcpy(&td, ln.desc.data(), sizeof(td));
+                fs.t = s;
+                const BufRef a2 = fs.alloc((size_t)td.U * 48 * 64 * 4);
+                ln.extra.push_back(a2);
+                Launch prep = ln;
+                prep.kind = K_TT_PREP;
+                prep.grid[0] = (uint32_t)(((int64_t)td.U * 48 * 64 + 255) / 256);
+                prep.block[0] = 256;
+                prep.lds = 0;
+                prep.kname = "tt_prep";
+                prep.alg_bytes = (double)td.U * 48 * 64 * 4;
+                prep.alg_flops = 0;
+                p->fwd.push_back(prep);
+                p->fwd.push_back(ln);
+                continue;
+            }
+            fops[s].need = 0;
             fs.t = s;
-            for (auto& l : lower_op(E, op, flags, fs)) p->fwd.push_back(l);
+            for (auto& l : lower_op(E, fops[s], flags, fs)) p->fwd.push_back(l);
         }
         if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) {
             fuse_launches(p->fwd, false);

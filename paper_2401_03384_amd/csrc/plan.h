@@ -159,6 +159,12 @@ bool fuse_rcp_forward(const ce_plan& p, Launch& out);
 // factor gradients per workgroup), then their ordered sums.
 bool fuse_rcp_backward(const Launch& f, const ce_plan& p, ScratchAlloc& scratch, std::vector<Launch>& out);
 
+// A contraction step `prod` and the convolution step `cons` that consumes its
+// result as one fused launch (K_TT_FWD), when their labels and layouts fit
+// the fused kernel; `out` reads the producer's operands and the consumer's
+// other operand and writes the consumer's result.
+bool fuse_tt_forward(const PairOp& prod, const PairOp& cons, Launch& out);
+
 // Lowering of one pairwise op to launches: a specialised kernel when the
 // op's label structure fits one (unless CE_FLAG_GENERIC_ONLY), else generic.
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,

@@ -1194,6 +1194,80 @@ bool run_cconv(const Launch& ln, Ctx& c) {
     return true;
 }
 
+// K_TT_FWD: the launcher's descriptor checks, then the two sums it defines
+// (Z of one (b, g, u) at a time), every operand access bounds-checked.
+bool run_tt_fwd(const Launch& ln, Ctx& c) {
+    TtDesc d = desc_of<TtDesc>(ln);
+    const int n1 = (d.K1 + 3) / 4;
+    const int XT = d.XT, PW = 16 * XT + 2, plane = ((6 * PW - 16 + 63) / 64) * 64 + 16;
+    REQ(n1 >= 1 && n1 <= 16 && d.R == 16 && d.T >= 1 && d.T <= 8 && d.TH == 4 && d.U >= 1 && d.G >= 1 &&
+            d.B >= 1 && d.H >= 1 && d.W >= 1 && (XT == 1 || XT == 2 || XT == 4) && d.W <= 16 * XT &&
+            d.PW == PW && d.plane == plane && plane >= 6 * PW && d.lds_bytes == (uint32_t)(16 * plane * 4) &&
+            d.ncombo == 2 * XT && (int64_t)d.nbands * 4 >= d.H && d.blocks == (int64_t)d.B * d.G * d.nbands &&
+            ((ln.kind & 0xff) == K_TT_PREP ||
+             ((int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256 && ln.lds == d.lds_bytes)) &&
+            (!d.xcd_remap || d.blocks % 8 == 0) && d.x_numel > 0 && d.x_numel < (1ll << 29) &&
+            d.f1_numel > 0 && d.f1_numel < (1ll << 29) && d.f2_numel > 0 && d.f2_numel < (1ll << 29),
+        "tt_fwd layout");
+    REQ(ln.extra.size() == 2, "tt_fwd operands");
+    bool ok = true, o1, o2, o3, o4, o5;
+    Buf X = resolve(ln.a, c, 0, o1), F1 = resolve(ln.b, c, 0, o2), F2 = resolve(ln.extra[0], c, 0, o3),
+        Y = resolve(ln.c, c, 0, o4), A2 = resolve(ln.extra[1], c, 0, o5);
+    REQ(o1 && o2 && o3 && o4 && o5, "unresolved buffer");
+    REQ((size_t)d.U * 48 * 64 * 4 <= A2.bytes, "tt_fwd operand table");
+    if ((ln.kind & 0xff) == K_TT_PREP) {
+        // the table the main launch reads: F2 placed at the tap rows of row pairs
+        REQ((int64_t)ln.grid[0] * 256 >= (int64_t)d.U * 48 * 64 && ln.block[0] == 256, "tt_prep grid");
+        for (int64_t i = 0; i < (int64_t)d.U * 48 * 64; i++) {
+            const int j = (int)(i & 3), lane = (int)((i >> 2) & 63);
+            const int s4 = (int)((i >> 8) % 12), u = (int)((i >> 8) / 12), s2 = 4 * s4 + j;
+            const int q = lane >> 4, c16 = lane & 15, t3 = c16 & 7, dy = c16 >> 3;
+            const int rh = s2 & 3, kw = (s2 >> 2) % 3, khp = (s2 >> 2) / 3, kh = khp - dy;
+            float v = 0.f;
+            if (t3 < d.T && kh >= 0 && kh < 3)
+                v = ld(F2, 0, t3 * d.f2_st + u * d.f2_su + (4 * rh + q) * d.f2_sr + kh * d.f2_sh + kw * d.f2_sw, ok);
+            st(A2, 0, i, v, ok);
+        }
+        REQ(ok, "out-of-bounds access (tt_prep)");
+        return true;
+    }
+    REQ((size_t)d.x_numel * 4 <= X.bytes && (size_t)d.f1_numel * 4 <= F1.bytes && (size_t)d.f2_numel * 4 <= F2.bytes,
+        "tt_fwd load ranges");
+    const int64_t HW = (int64_t)d.H * d.W;
+    std::vector<double> z((size_t)d.R * HW), y((size_t)d.T * HW);
+    for (int64_t b = 0; b < d.B; b++)
+        for (int g = 0; g < d.G; g++) {
+            std::fill(y.begin(), y.end(), 0.0);
+            for (int u = 0; u < d.U; u++) {
+                std::fill(z.begin(), z.end(), 0.0);
+                for (int k = 0; k < d.K1; k++)
+                    for (int r = 0; r < d.R; r++) {
+                        const double f = ld(F1, 0, g * d.f1_sg + k * d.f1_sk + r * d.f1_sr, ok);
+                        const int64_t xo = b * d.x_sb + k * d.x_sk + u * d.x_su;
+                        for (int64_t p = 0; p < HW; p++) z[r * HW + p] += f * ld(X, 0, xo + p, ok);
+                    }
+                for (int t = 0; t < d.T; t++)
+                    for (int r = 0; r < d.R; r++)
+                        for (int kh = 0; kh < 3; kh++)
+                            for (int kw = 0; kw < 3; kw++) {
+                                const double f = ld(F2, 0, t * d.f2_st + u * d.f2_su + r * d.f2_sr + kh * d.f2_sh +
+                                                                kw * d.f2_sw, ok);
+                                for (int h = 0; h < d.H; h++)
+                                    for (int w = 0; w < d.W; w++) {
+                                        const int hh = h + kh - 1, ww = w + kw - 1;
+                                        if (hh < 0 || hh >= d.H || ww < 0 || ww >= d.W) continue;
+                                        y[t * HW + h * d.W + w] += f * z[r * HW + hh * d.W + ww];
+                                    }
+                            }
+            }
+            for (int t = 0; t < d.T; t++)
+                for (int64_t p = 0; p < HW; p++)
+                    st(Y, 0, b * d.y_sb + g * d.y_sg + t * d.y_st + p, (float)y[t * HW + p], ok);
+            REQ(ok, "out-of-bounds access (tt_fwd)");
+        }
+    return true;
+}
+
 bool run_cred(const Launch& ln, Ctx& c) {
     CredDesc d = desc_of<CredDesc>(ln);
     const int kind = ln.kind & 0xff;
@@ -1479,6 +1553,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
                     : v == K_CCONV ? run_cconv(ln, c)
+                    : v == K_TT_FWD || v == K_TT_PREP ? run_tt_fwd(ln, c)
                     : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
             if (!ok) { std::snprintf(err, errlen, "%s", c.err.c_str()); return 4; }

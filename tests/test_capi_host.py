@@ -561,3 +561,23 @@ def test_stride_errors():
         B.ce_expr_set_stride(x, "h", 2)
     assert ex.value.status == B.CE_ERR_UNSUPPORTED
     B.ce_expr_destroy(x)
+
+
+@pytest.mark.parametrize("name", ["C4", "C4s", "C4w", "C4x2", "C4x4", "C4x1"])
+def test_tensor_train_forward_fused(name):
+    """The reshaped tensor-train layer's contraction X x W12 and the
+    convolution consuming its result run as one fused launch: the forward
+    workspace holds only the two merged cores (no X12)."""
+    w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS[name]
+    p = _plan(w.spec, w.shapes)
+    try:
+        text = B.ce_plan_describe(p)
+        fwd = [l for l in text.splitlines() if l.startswith("  fwd ")]
+        assert sum("tt_fwd<" in l for l in fwd) == 1 and sum("tt_prep" in l for l in fwd) == 1, text
+        assert len(fwd) == 4, text
+        e = O.bind(O.parse(w.spec), w.shapes)
+        tree = O.optimal_tree(e)[0]
+        x12 = max(O.intermediate_size(e, O.leaves(a) + O.leaves(b)) for a, b in O.post_order_steps(tree)[:-1])
+        assert B.ce_plan_workspace_size(p, 0) < x12 * 4
+    finally:
+        B.ce_plan_destroy(p)

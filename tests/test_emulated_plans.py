@@ -28,6 +28,7 @@ def emul(tmp_path_factory):
            os.path.join(ROOT, "tests", "cpu_emulator", "emulate.cpp"),
            os.path.join(SRC, "expr.cpp"), os.path.join(SRC, "plan.cpp"),
            os.path.join(SRC, "lower.cpp"), os.path.join(SRC, "fuse.cpp"), os.path.join(SRC, "fuse_rcp.cpp"),
+           os.path.join(SRC, "fuse_tt.cpp"),
            os.path.join(SRC, "capi.cpp"), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -97,6 +98,10 @@ CASES = {
     "C5at_f32": W.rcp_layer("C5at_f32", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "f32", 23),
     "C5bt": W.rcp_layer("C5bt", 1, (2, 2, 4), (2, 2, 4), 9, 8, 16, 5, "bf16", 24),
     "C4m": W.rtt_layer("C4m", 1, (4, 4, 8), (4, 4, 8), 5, 7, 16, 3, "f32", 26),
+    # fused contraction + convolution: 30, 40 and 16 columns, ragged bands, t3 < 8, K1 = 24
+    "C4x2": W.PARITY_WORKLOADS["C4x2"],
+    "C4x4": W.PARITY_WORKLOADS["C4x4"],
+    "C4x1": W.PARITY_WORKLOADS["C4x1"],
     "C5cs": W.PARITY_WORKLOADS["C5cs"],
     # fused reshaped-CP kernels: both instantiations (rank 4 keeps the CPU
     # run short), one and several row tiles

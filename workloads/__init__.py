@@ -139,6 +139,12 @@ PARITY_WORKLOADS = {
     "C4c": rtt_layer("C4c", 1, (2, 2, 4), (2, 2, 2), 6, 7, 16, 3, "f32", 34),
     # the full tensor-train chain at channel sizes of the 28x28 layer, small planes
     "C4w": rtt_layer("C4w", 2, (4, 8, 8), (4, 8, 8), 9, 11, 16, 3, "f32", 35),
+    # the fused contraction + convolution with 17-32 and 33-64 columns, ragged
+    # row bands, fewer than 8 output channels, and a contraction of 12 (not a
+    # multiple of 4) or 8 terms
+    "C4x2": rtt_layer("C4x2", 2, (4, 8, 4), (4, 4, 4), 21, 30, 16, 3, "f32", 36),
+    "C4x4": rtt_layer("C4x4", 2, (3, 8, 4), (4, 4, 6), 9, 40, 16, 3, "f32", 37),
+    "C4x1": rtt_layer("C4x1", 3, (4, 8, 4), (4, 8, 5), 6, 16, 16, 3, "f32", 38),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
