@@ -171,8 +171,11 @@ void ce_expr_destroy(ce_expr* e);
  * then skips the recompute launches and must receive the workspace the
  * preceding ce_forward of the same inputs used, unchanged, and of at least
  * ce_plan_workspace_size(p, 1) bytes (which covers the forward's).  A fused
- * chain keeps its intermediates on chip and recomputes them there, so for
- * such a plan the flag changes nothing. */
+ * chain whose backward is fused too (the CP and reshaped-CP chains) keeps its
+ * intermediates on chip and recomputes them there, so for such a plan the
+ * flag changes nothing; a fusion of the forward alone (the tensor-train
+ * contraction + convolution) is not used with this flag, so the forward
+ * writes the intermediate the backward then reads. */
 #define CE_FLAG_SAVE_INTERMEDIATES 0x4u
 /* Make every launch of the general contraction kernel use 64-bit element
  * offsets and predicated loads, the code path it takes for operands beyond

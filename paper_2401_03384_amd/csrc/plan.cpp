@@ -783,10 +783,12 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
                       tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
         }
         // a contraction whose result only feeds a convolution of the
-        // tensor-train pattern runs fused with it (the result stays on chip)
+        // tensor-train pattern runs fused with it (the result stays on chip;
+        // not when the caller asks to keep intermediates for the backward)
         std::vector<int> fused_to(m, -1), fused_from(m, -1);
         std::vector<Launch> fused(m);
-        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION)) {
+        if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) &&
+            !(flags & CE_FLAG_SAVE_INTERMEDIATES) && lim.save_budget == 0) {
             for (int s = 0; s + 1 < m; s++) {
                 const int cs = consumer_step(p->steps[s].c);
                 if (cs >= m || fused_from[s] >= 0 || fused_to[s] >= 0 || fused_from[cs] >= 0) continue;
