@@ -66,6 +66,7 @@ enum KernelKind : int32_t {
     K_CCONV = 36,           // convolution contracted over one channel index, MFMA tiles (CconvDesc)
     K_TT_FWD = 37,          // fused contraction + convolution of a tensor-train chain (TtDesc)
     K_TT_PREP = 38,         // its convolution's A operands in load order (TtDesc)
+    K_WGCONV = 39,          // K_CREDW's partials on fp32 MFMA tiles (CredDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -206,6 +207,10 @@ struct TcDesc {
 //           plane; u = rank (one dim), s = batch (up to two dims); O = the
 //           output gradient; writes partials P[chunk][u][m][tap], summed in
 //           chunk order by K_CREDW_REDUCE.
+//   K_WGCONV (filter gradient, fp32, on MFMA tiles): the same partials as
+//           K_CREDW with u in blocks of 128 (nrb blocks) and every (m, tap)
+//           in one block; O's planes sit in LDS with a zero halo, PH rows of
+//           pitch PWp, double-buffered.
 // Planes (Z, the output of K_CRED, O of K_CREDW) are dense: row stride W,
 // unit columns.  ch, cw: zero padding before the first row / column.
 struct CredDesc {

@@ -29,6 +29,9 @@ hipError_t launch_thinw(const Launch& ln, const void* p, const void* q, void* pa
 // input planes, f = the filter, y = the output planes (bf16 or fp32).
 hipError_t launch_cconv(const Launch& ln, const void* z, const void* f, void* y, hipStream_t s);
 hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, hipStream_t s);
+// Its filter gradient on fp32 MFMA tiles (K_WGCONV): z = the stacked planes,
+// o = the output gradient, part = the fp32 partials (summed by K_CREDW_REDUCE).
+hipError_t launch_wgconv(const Launch& ln, const void* z, const void* o, void* part, hipStream_t s);
 
 // Thin channel mixing (K_THIN, GemmDesc): a = factor, b = activations, c = out.
 hipError_t launch_thin(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s);

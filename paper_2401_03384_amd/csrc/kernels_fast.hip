@@ -693,6 +693,7 @@ hipError_t launch_fast(const Launch& ln, const void* a, const void* b, void* c, 
         case K_CRED: return launch_cred(ln, b, a, c, s);
         case K_CCONV: return launch_cconv(ln, a, b, c, s);
         case K_CREDW: return launch_cred(ln, a, b, d, s);
+        case K_WGCONV: return launch_wgconv(ln, a, b, d, s);
         case K_CREDW_REDUCE: return launch_cred(ln, nullptr, d, c, s);
         case K_THINW:
         case K_THINW_REDUCE: return launch_thinw(ln, a, b, d, c, s);

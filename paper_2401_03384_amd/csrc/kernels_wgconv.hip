@@ -1,0 +1,311 @@
+// Filter gradient of a plane convolution contracted over one shared index, on
+// fp32 16x16x4 MFMA tiles (CredDesc; the same partial sums as K_CREDW):
+//
+//   P[chunk][u][m][tap] = sum_{g in chunk} sum_j Z[g][u][j + tap - c] * O[g][m][j]
+//                       = sum_{g in chunk} sum_p Z[g][u][p] * O[g][m][p - tap + c]
+//
+// (Appendix B: g2 of a convolution step, the output gradient correlated with
+// the step's input over every pixel and batch index).  Moving the shift from
+// Z onto O, the second form reads every Z value once, unshifted: Z is the
+// large operand (one plane per rank index u and batch index g), O the small
+// one (a few channels m).  As a matrix product: rows u, columns n = (m, tap),
+// reduction over (g, p).
+//
+// A block is four wavefronts with 32 rows of u each; a wavefront holds two
+// row tiles x NT column tiles of 16 in MFMA accumulators.  The pixels of one
+// plane go in groups of 16: lane (i, kq) (i = lane % 16, kq = lane / 16)
+// loads Z[u0 + i][q0 + 4kq .. q0 + 4kq + 3] with one 16-byte load per row
+// tile; element t of it is the lane's K value of the group's MFMA t (pixel
+// q0 + 4kq + t).  The column operand of MFMA t is O at the lane's column
+// (m, tap) and the pixel q0 + 4kq + t shifted by the tap, read from LDS, where
+// the planes of the current g sit with a zero halo (tap offsets are constant
+// per lane).  The planes of g + 1 load into registers while g's groups run
+// (double-buffered LDS); the row loads run two groups ahead.
+#include <atomic>
+#include <cstdint>
+#include <cstring>
+
+#include "desc.h"
+#include "hip_util.h"
+#include "kernels.h"
+
+namespace ce {
+namespace {
+
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+
+constexpr int kWgStage = 8;   // float4 of the next planes a thread holds while it computes
+
+__device__ __forceinline__ int64_t wg_zoff(const CredDesc& d, int64_t g) {
+    int64_t oz = 0;
+    for (int i = d.ng - 1; i >= 0; --i) {
+        oz += (g % d.g_size[i]) * d.g_sZ[i];
+        g /= d.g_size[i];
+    }
+    return oz;
+}
+__device__ __forceinline__ int64_t wg_ooff(const CredDesc& d, int64_t g) {
+    int64_t oy = 0;
+    for (int i = d.ng - 1; i >= 0; --i) {
+        oy += (g % d.g_size[i]) * d.g_sY[i];
+        g /= d.g_size[i];
+    }
+    return oy;
+}
+
+template <int NT, bool VEC>
+__global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __restrict__ Z,
+                                                 const float* __restrict__ O, float* __restrict__ P) {
+    extern __shared__ float4 lds4[];
+    float* pl = reinterpret_cast<float*>(lds4);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int W = d.W, HW = d.H * d.W, WP = d.PWp, PLN = d.PH * d.PWp;
+    const int KK = d.KH * d.KW, N = d.M * KK, BUF = d.M * PLN;
+    const int top = d.KH - 1 - d.ch, left = d.KW - 1 - d.cw;   // halo before the interior
+    const int64_t ub = blockIdx.x % d.nrb, ck = blockIdx.x / d.nrb;
+    const int64_t g0 = ck * d.gchunk, g1 = min(d.G, g0 + d.gchunk);
+    const int i16 = lane & 15, kq = lane >> 4;
+    const int64_t ua = ub * 128 + wave * 32 + i16, uc = ua + 16;
+    const bool oka = ua < d.R, okc = uc < d.R;
+    const int64_t za = (oka ? ua : 0) * d.z_sr, zc = (okc ? uc : 0) * d.z_sr;
+
+    // LDS offset of this lane's column (m, tap) in every column tile
+    int toff[NT];
+#pragma unroll
+    for (int j = 0; j < NT; j++) {
+        const int n = 16 * j + i16;
+        toff[j] = 0;
+        if (n < N) {
+            const int m = n / KK, t = n - m * KK, jh = t / d.KW, jw = t - jh * d.KW;
+            toff[j] = m * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw);
+        }
+    }
+
+    // planes of O[g] into buffer `buf`: interior only (the halo stays zero).
+    // The prefetched path holds kWgStage float4 a thread across the groups of
+    // the current g; a float4 is four pixels of one row (W % 4 == 0), and its
+    // offsets are recomputed where they are used from an opaque copy of the
+    // thread index (hoisted out of the loop they would hold 3 kWgStage
+    // registers for its life).
+    const int n4 = (d.M * HW + 3) / 4;   // float4 of one g's planes
+    const bool pref = VEC && W % 4 == 0 && n4 <= 256 * kWgStage;
+    auto put = [&](int buf, int e, float v) {
+        const int m = e / HW, p = e - m * HW, h = p / W, w = p - h * W;
+        pl[buf * BUF + m * PLN + (h + top) * WP + (w + left)] = v;
+    };
+    auto stage_load = [&](int64_t g, float4 (&sv)[kWgStage]) {
+        const float* src = O + wg_ooff(d, g);
+        int t0 = tid;
+        asm volatile("" : "+v"(t0));
+#pragma unroll
+        for (int k = 0; k < kWgStage; k++) {
+            const int e4 = t0 + 256 * k;
+            if (e4 < n4) {
+                const int e = 4 * e4, m = e / HW, p = e - m * HW;
+                sv[k] = *reinterpret_cast<const float4*>(src + m * d.o_sm + p);
+            }
+        }
+    };
+    auto stage_store = [&](int buf, const float4 (&sv)[kWgStage]) {
+        int t0 = tid;
+        asm volatile("" : "+v"(t0));
+#pragma unroll
+        for (int k = 0; k < kWgStage; k++) {
+            const int e4 = t0 + 256 * k;
+            if (e4 < n4) {
+                const int e = 4 * e4, m = e / HW, p = e - m * HW, h = p / W, w = p - h * W;
+                float* dst = pl + buf * BUF + m * PLN + (h + top) * WP + (w + left);
+                dst[0] = sv[k].x;
+                dst[1] = sv[k].y;
+                dst[2] = sv[k].z;
+                dst[3] = sv[k].w;
+            }
+        }
+    };
+    auto stage_direct = [&](int64_t g, int buf) {   // without the register prefetch
+        const float* src = O + wg_ooff(d, g);
+        for (int e = tid; e < d.M * HW; e += 256) {
+            const int m = e / HW, p = e - m * HW;
+            put(buf, e, src[m * d.o_sm + p]);
+        }
+    };
+
+    for (int e = tid; e < 2 * BUF; e += 256) pl[e] = 0.f;
+    __syncthreads();
+    if (g0 < g1) {
+        if (pref) {
+            float4 sv[kWgStage];
+            stage_load(g0, sv);
+            stage_store(0, sv);
+        } else {
+            stage_direct(g0, 0);
+        }
+    }
+    __syncthreads();
+
+    // row loads: items (g, group) in order, two ahead of the one computed
+    const int NG = (HW + 15) / 16;
+    int64_t lg = g0;
+    int lq = 0;
+    int64_t loz = g0 < g1 ? wg_zoff(d, g0) : 0;
+    auto load_item = [&](float4 (&dst)[2]) {
+        dst[0] = dst[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (lg < g1) {
+            const int q = 16 * lq + 4 * kq;
+            if constexpr (VEC) {
+                if (q < HW) {
+                    if (oka) dst[0] = *reinterpret_cast<const float4*>(Z + loz + za + q);
+                    if (okc) dst[1] = *reinterpret_cast<const float4*>(Z + loz + zc + q);
+                }
+            } else {
+                float a[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int t = 0; t < 4; t++)
+                    if (q + t < HW) {
+                        if (oka) a[t] = Z[loz + za + q + t];
+                        if (okc) c[t] = Z[loz + zc + q + t];
+                    }
+                dst[0] = make_float4(a[0], a[1], a[2], a[3]);
+                dst[1] = make_float4(c[0], c[1], c[2], c[3]);
+            }
+        }
+        if (++lq == NG) {
+            lq = 0;
+            ++lg;
+            if (lg < g1) loz = wg_zoff(d, lg);
+        }
+    };
+
+    f32x4 acc[2][NT];
+#pragma unroll
+    for (int mt = 0; mt < 2; mt++)
+#pragma unroll
+        for (int j = 0; j < NT; j++) acc[mt][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+    float4 ra0[2], ra1[2], rn[2];
+    load_item(ra0);
+    load_item(ra1);
+    for (int64_t g = g0; g < g1; g++) {
+        const int cur = (int)((g - g0) & 1);
+        const bool more = g + 1 < g1;
+        float4 sv[kWgStage];
+        if (more && pref) stage_load(g + 1, sv);
+        const float* pb = pl + cur * BUF;
+        // (h, w) of this lane's first pixel of the group
+        int h0 = (4 * kq) / W, w0 = 4 * kq - ((4 * kq) / W) * W;
+        for (int grp = 0; grp < NG; grp++) {
+            load_item(rn);
+            const int q = 16 * grp + 4 * kq;
+            int bt[4];
+            {
+                int h = h0, w = w0;
+#pragma unroll
+                for (int t = 0; t < 4; t++) {
+                    bt[t] = (q + t < HW) ? h * WP + w : 0;
+                    if (++w == W) {
+                        w = 0;
+                        ++h;
+                    }
+                }
+            }
+            float bv[NT][4];
+#pragma unroll
+            for (int t = 0; t < 4; t++)
+#pragma unroll
+                for (int j = 0; j < NT; j++) bv[j][t] = pb[bt[t] + toff[j]];
+            const float a0[4] = {ra0[0].x, ra0[0].y, ra0[0].z, ra0[0].w};
+            const float a1[4] = {ra0[1].x, ra0[1].y, ra0[1].z, ra0[1].w};
+#pragma unroll
+            for (int t = 0; t < 4; t++)
+#pragma unroll
+                for (int j = 0; j < NT; j++) {
+                    acc[0][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[t], bv[j][t], acc[0][j], 0, 0, 0);
+                    acc[1][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[t], bv[j][t], acc[1][j], 0, 0, 0);
+                }
+            ra0[0] = ra1[0];
+            ra0[1] = ra1[1];
+            ra1[0] = rn[0];
+            ra1[1] = rn[1];
+            w0 += 16;
+            while (w0 >= W) {
+                w0 -= W;
+                ++h0;
+            }
+        }
+        if (more) {
+            if (pref) stage_store(1 - cur, sv);
+            else stage_direct(g + 1, 1 - cur);
+        }
+        __syncthreads();
+    }
+
+    // accumulator r of a lane: row 4 kq + r of the tile, column i16
+#pragma unroll
+    for (int mt = 0; mt < 2; mt++)
+#pragma unroll
+        for (int j = 0; j < NT; j++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const int64_t u = ub * 128 + wave * 32 + 16 * mt + 4 * kq + r;
+                const int n = 16 * j + i16;
+                if (u < d.R && n < N) P[(ck * d.R + u) * N + n] = acc[mt][j][r];
+            }
+}
+
+template <int NT>
+hipError_t wgconv_nt(const CredDesc& d, bool vec, const float* z, const float* o, float* part, hipStream_t s) {
+    auto k = vec ? wgconv<NT, true> : wgconv<NT, false>;
+    static std::atomic<uint64_t> ok{0};
+    // dynamic LDS above 64 KB has to be allowed per kernel, once per device
+    if (d.lds_bytes > 64 * 1024) {
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+        if (dev < 0 || dev >= 64 || d.lds_bytes > 160 * 1024) return hipErrorInvalidValue;
+        if (!(ok.load() & (1ull << dev))) {
+            e = hipFuncSetAttribute((const void*)wgconv<NT, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    160 * 1024);
+            if (e == hipSuccess)
+                e = hipFuncSetAttribute((const void*)wgconv<NT, false>,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (e != hipSuccess) return e;
+            ok.fetch_or(1ull << dev);
+        }
+    }
+    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, z, o, part);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_wgconv(const Launch& ln, const void* z, const void* o, void* part, hipStream_t s) {
+    CredDesc d;
+    std::memcpy(&d, ln.desc.data(), sizeof(d));
+    const int KK = d.KH * d.KW, N = d.M * KK, NT = (N + 15) / 16;
+    // the shapes the kernel assumes (the lowering guarantees them)
+    if (((ln.kind >> kBitIn) & 1) || d.M < 1 || KK < 1 || NT < 1 || NT > 6 || d.H < 1 || d.W < 1 ||
+        d.PH != d.H + d.KH - 1 || d.PWp < d.W + d.KW - 1 || d.ch < 0 || d.ch >= d.KH || d.cw < 0 ||
+        d.cw >= d.KW || d.nrb != (d.R + 127) / 128 || d.gchunk < 1 || d.nchunks != (d.G + d.gchunk - 1) / d.gchunk ||
+        d.blocks != d.nrb * d.nchunks || d.lds_bytes != (uint32_t)(2 * d.M * d.PH * d.PWp * 4) ||
+        d.lds_bytes > 160 * 1024 || (int64_t)d.H * d.W * d.M >= (1ll << 30) || ln.grid[0] != (uint32_t)d.blocks ||
+        ln.block[0] != 256)
+        return hipErrorInvalidValue;
+    // 16-byte loads: rows of Z and of O start at multiples of four floats
+    const int64_t HW = (int64_t)d.H * d.W;
+    bool vec = HW % 4 == 0 && d.z_sr % 4 == 0 && (d.M == 1 || d.o_sm % 4 == 0) && (uintptr_t)z % 16 == 0 &&
+               (uintptr_t)o % 16 == 0;
+    for (int i = 0; i < d.ng; i++) vec = vec && d.g_sZ[i] % 4 == 0 && d.g_sY[i] % 4 == 0;
+    const float* Z = (const float*)z;
+    const float* O = (const float*)o;
+    float* Pp = (float*)part;
+    switch (NT) {
+        case 1: return wgconv_nt<1>(d, vec, Z, O, Pp, s);
+        case 2: return wgconv_nt<2>(d, vec, Z, O, Pp, s);
+        case 3: return wgconv_nt<3>(d, vec, Z, O, Pp, s);
+        case 4: return wgconv_nt<4>(d, vec, Z, O, Pp, s);
+        case 5: return wgconv_nt<5>(d, vec, Z, O, Pp, s);
+        default: return wgconv_nt<6>(d, vec, Z, O, Pp, s);
+    }
+}
+
+}  // namespace ce

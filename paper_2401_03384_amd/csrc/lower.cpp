@@ -696,6 +696,68 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     std::vector<Dm>& Rd = wgrad ? U : S;
     if (Bd.size() > 2 || Rd.size() > 1 || Mv.size() > 1) return false;
     const int64_t M = Mv.empty() ? 1 : Mv[0].size;
+    if (wgrad && Z.dtype == DT_F32 && O.dtype == DT_F32 && M * KH * KW <= 96) {
+        // fp32 filter gradient on MFMA tiles: u in blocks of 128 rows, the
+        // batch split into about two blocks a CU, two LDS copies of O's planes
+        CredDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.H = (int32_t)H;
+        d.W = (int32_t)W;
+        d.KH = (int32_t)KH;
+        d.KW = (int32_t)KW;
+        d.ch = (int32_t)pch;
+        d.cw = (int32_t)pcw;
+        d.M = (int32_t)M;
+        d.o_sm = Mv.empty() ? 0 : Mv[0].s1;
+        d.c_sm = Mv.empty() ? 0 : Mv[0].s2;
+        d.PH = (int32_t)(H + KH - 1);
+        d.PWp = (int32_t)(W + KW - 1);
+        d.ng = (int32_t)Bd.size();
+        d.G = 1;
+        for (size_t i = 0; i < Bd.size(); i++) {
+            d.g_size[i] = Bd[i].size;
+            d.g_sZ[i] = Bd[i].s1;
+            d.g_sY[i] = Bd[i].s2;
+            d.G *= Bd[i].size;
+        }
+        d.R = Rd.empty() ? 1 : Rd[0].size;
+        d.z_sr = Rd.empty() ? 0 : Rd[0].s1;
+        d.c_sr = Rd.empty() ? 0 : Rd[0].s2;
+        d.c_sh = C.stride_of(ch.label);
+        d.c_sw = C.stride_of(cw.label);
+        d.nrb = cdiv(d.R, 128);
+        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(512, d.nrb)));
+        d.gchunk = cdiv(d.G, chunks);
+        d.nchunks = cdiv(d.G, d.gchunk);
+        d.blocks = d.nrb * d.nchunks;
+        d.threads = 256;
+        const int64_t lds = 2 * M * d.PH * d.PWp * 4;
+        if (lds <= 160 * 1024 && d.blocks <= 0x7fffffff && H * W * M < ((int64_t)1 << 30)) {
+            d.lds_bytes = (uint32_t)lds;
+            const BufRef part = scratch.alloc((size_t)(d.nchunks * d.R * M * KH * KW * 4));
+            Launch ln;
+            ln.kind = K_WGCONV | dt_bits(DT_F32, DT_F32, DT_F32);
+            ln.a = Z.buf;
+            ln.b = O.buf;
+            ln.d = part;
+            ln.grid[0] = (uint32_t)d.blocks;
+            ln.block[0] = 256;
+            ln.lds = d.lds_bytes;
+            set_desc(ln, d);
+            ln.kname = "wgconv<" + std::to_string((M * KH * KW + 15) / 16) + ">";
+            out.push_back(ln);
+            Launch lr;
+            lr.kind = K_CREDW_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
+            lr.d = part;
+            lr.c = C.buf;
+            lr.grid[0] = (uint32_t)cdiv(d.R * M * KH * KW, 64);   // 64 outputs per block
+            lr.block[0] = 256;
+            set_desc(lr, d);
+            lr.kname = std::string("credw_reduce<") + tname(C.dtype) + ">";
+            out.push_back(lr);
+            return true;
+        }
+    }
     const int MO = M == 1 ? 1 : M <= 4 ? 4 : M <= 8 ? 8 : 16;
     if (M > 16 || (wgrad && (MO > 8 || MO * KH * KW > 72))) return false;
     CredDesc d;

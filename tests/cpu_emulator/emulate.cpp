@@ -1376,6 +1376,88 @@ bool run_cred(const Launch& ln, Ctx& c) {
     return true;
 }
 
+// K_WGCONV (the K_CREDW partials on fp32 MFMA tiles): the launcher's
+// descriptor checks; every Z / O / partial index and every LDS word the
+// kernel's lanes touch, walked block by block with its own offset
+// arithmetic; then the partial sums it defines, in double.
+bool run_wgconv(const Launch& ln, Ctx& c) {
+    CredDesc d = desc_of<CredDesc>(ln);
+    const int KK = d.KH * d.KW, N = d.M * KK, NT = (N + 15) / 16;
+    REQ(((ln.kind >> kBitIn) & 1) == 0 && d.M >= 1 && KK >= 1 && NT >= 1 && NT <= 6 && d.H >= 1 && d.W >= 1 &&
+            d.PH == d.H + d.KH - 1 && d.PWp >= d.W + d.KW - 1 && d.ch >= 0 && d.ch < d.KH && d.cw >= 0 &&
+            d.cw < d.KW && d.nrb == (d.R + 127) / 128 && d.gchunk >= 1 &&
+            d.nchunks == (d.G + d.gchunk - 1) / d.gchunk && d.blocks == d.nrb * d.nchunks &&
+            d.lds_bytes == (uint32_t)(2 * d.M * d.PH * d.PWp * 4) && d.lds_bytes <= 160 * 1024 &&
+            (int64_t)d.H * d.W * d.M < (1ll << 30) && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256 &&
+            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2,
+        "wgconv layout");
+    bool ok = true, o1, o2, o3;
+    Buf Z = resolve(ln.a, c, 0, o1), O = resolve(ln.b, c, 0, o2), Pb = resolve(ln.d, c, 0, o3);
+    REQ(o1 && o2 && o3, "unresolved buffer");
+    const int64_t HW = (int64_t)d.H * d.W, WP = d.PWp, PLN = (int64_t)d.PH * d.PWp, BUF = d.M * PLN;
+    const int64_t zn = (int64_t)(Z.bytes / 4), on = (int64_t)(O.bytes / 4), pn = (int64_t)(Pb.bytes / 4);
+    const int top = d.KH - 1 - d.ch, left = d.KW - 1 - d.cw;
+    auto offs = [&](int64_t g, int64_t& oz, int64_t& oy) {
+        oz = oy = 0;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            const int64_t x = g % d.g_size[i];
+            g /= d.g_size[i];
+            oz += x * d.g_sZ[i];
+            oy += x * d.g_sY[i];
+        }
+    };
+    // every lane's LDS column offset and the largest shifted-plane read
+    int64_t toff_max = 0;
+    for (int n = 0; n < N; n++) {
+        const int m = n / KK, t = n % KK, jh = t / d.KW, jw = t % d.KW;
+        toff_max = std::max<int64_t>(toff_max, m * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw));
+    }
+    REQ((d.H - 1) * WP + (d.W - 1) + toff_max < BUF, "wgconv lds read range");
+    REQ((int64_t)(d.M - 1) * PLN + (d.H - 1 + top) * WP + (d.W - 1 + left) < BUF, "wgconv lds write range");
+    for (int64_t b = 0; b < d.blocks; b++) {
+        const int64_t ub = b % d.nrb, ck = b / d.nrb;
+        const int64_t g0 = ck * d.gchunk, g1 = std::min(d.G, g0 + d.gchunk);
+        for (int64_t g = g0; g < g1; g++) {
+            int64_t oz, oy;
+            offs(g, oz, oy);
+            // the staged planes of O (all threads together read every element)
+            for (int m = 0; m < d.M; m++)
+                REQ(oy + m * d.o_sm >= 0 && oy + m * d.o_sm + HW <= on, "wgconv O range");
+            // the row loads of the block's 128 rows
+            for (int64_t r = 0; r < 128; r++) {
+                const int64_t u = ub * 128 + r;
+                if (u >= d.R) continue;
+                REQ(oz + u * d.z_sr >= 0 && oz + u * d.z_sr + HW <= zn, "wgconv Z range");
+            }
+        }
+        for (int64_t r = 0; r < 128; r++) {
+            const int64_t u = ub * 128 + r;
+            if (u >= d.R) continue;
+            REQ((ck * d.R + u) * N + N <= pn, "wgconv partial range");
+            std::vector<double> acc((size_t)N, 0.0);
+            for (int64_t g = g0; g < g1; g++) {
+                int64_t oz, oy;
+                offs(g, oz, oy);
+                for (int64_t h = 0; h < d.H; h++)
+                    for (int64_t w = 0; w < d.W; w++) {
+                        const double z = ld(Z, 0, oz + u * d.z_sr + h * d.W + w, ok);
+                        for (int m = 0; m < d.M; m++)
+                            for (int jh = 0; jh < d.KH; jh++)
+                                for (int jw = 0; jw < d.KW; jw++) {
+                                    const int64_t hh = h - jh + d.ch, ww = w - jw + d.cw;
+                                    if (hh < 0 || hh >= d.H || ww < 0 || ww >= d.W) continue;
+                                    acc[(size_t)(m * KK + jh * d.KW + jw)] +=
+                                        z * ld(O, 0, oy + m * d.o_sm + hh * d.W + ww, ok);
+                                }
+                    }
+            }
+            for (int n = 0; n < N; n++) st(Pb, 0, (ck * d.R + u) * N + n, (float)acc[(size_t)n], ok);
+        }
+    }
+    REQ(ok, "out-of-bounds access (wgconv)");
+    return true;
+}
+
 // Small-output contraction over a long reduction: per-block partials over
 // the block's outer rows (K_THINW), then the ordered chunk sum (K_THINW_REDUCE).
 bool run_thinw(const Launch& ln, Ctx& c) {
@@ -1553,6 +1635,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : v == K_TC_REDUCE ? run_tc_reduce(ln, c)
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
                     : v == K_CCONV ? run_cconv(ln, c)
+                    : v == K_WGCONV ? run_wgconv(ln, c)
                     : v == K_TT_FWD || v == K_TT_PREP ? run_tt_fwd(ln, c)
                     : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
