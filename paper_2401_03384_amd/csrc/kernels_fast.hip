@@ -16,6 +16,7 @@
 //                         of the axis are staged in LDS, taps in registers.
 //  dw_tapgrad / reduce    filter-tap gradients: per-block partial sums, then
 //                         an ordered reduction over the blocks of each row.
+#include <atomic>
 #include <cstring>
 
 #include "desc.h"
@@ -202,6 +203,196 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmDesc d, const bf16_t* __res
             int m = m0 + i * 32 + mfma32_row(r, lane);
             if (m < d.M) store(C, oC + (int64_t)m * d.sCm + n, acc[i][r]);
         }
+}
+
+// The same channel mix in bf16 over flattened columns f = g * N + n (N a
+// multiple of 4, rows of B and C 8-byte aligned), so that small planes fill
+// whole 128-column tiles: a block takes TM rows x 128 columns, a wavefront one
+// 32-column MFMA tile.  K goes in chunks of TK (64, or 256 when K <= 256, so
+// that a block makes one memory round trip); the next chunk's elements load
+// into registers while the current chunk's MFMAs run (one LDS copy, two
+// barriers a chunk).  Thread mapping: B, four consecutive columns (one 8-byte
+// row piece) x k rows 4(tid / 32) + 32 h + {0..3}; A, TM x TK / 256
+// consecutive k of one row.
+template <typename TC, int MT, int TK>
+__global__ void __launch_bounds__(256) gemm_bf16f(GemmDesc d, const bf16_t* __restrict__ A,
+                                                  const bf16_t* __restrict__ B, TC* __restrict__ C) {
+    constexpr int TM = 32 * MT, TN = 128, LDK = TK + 8, KH = TK / 32;
+    constexpr int AE = TM * TK / 256;   // A elements a thread
+    extern __shared__ __attribute__((aligned(16))) bf16_t lds_g[];
+    bf16_t(*As)[LDK] = reinterpret_cast<bf16_t(*)[LDK]>(lds_g);
+    bf16_t(*Bs)[LDK] = reinterpret_cast<bf16_t(*)[LDK]>(lds_g + TM * LDK);   // transposed: [n][k]
+    const int nt = (int)(blockIdx.x % d.ntiles), mt = (int)(blockIdx.x / d.ntiles);
+    const int m0 = mt * TM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int64_t G = 1;
+    for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
+    const int64_t NF = G * d.N;
+    // this thread's four B columns (one g, since N % 4 == 0)
+    const int nq = tid & 31, kq = 4 * (tid >> 5);
+    const int64_t fb = (int64_t)nt * TN + 4 * nq;
+    const bool colok = fb < NF;
+    int64_t ob = 0;
+    {
+        const int64_t g = colok ? fb / d.N : 0;
+        int64_t oA, oC;
+        gemm_offsets(d, g, oA, ob, oC);
+        ob += colok ? fb - g * d.N : 0;   // columns past the end read column 0 (masked)
+    }
+    // this thread's A elements e: tile index tid + 256 e, rows fastest when
+    // A's rows are unit-stride (so that a load instruction reads consecutive
+    // elements), else k fastest; either way element e sits at a fixed stride
+    // from element 0 (256 / TM k-steps or 256 / TK rows)
+    const bool mfast = d.sAm == 1 && d.sAk != 1;
+    auto a_at = [&](int e, int& m, int& k) {
+        const int i = tid + 256 * e;
+        if (mfast) {
+            m = i % TM;
+            k = i / TM;
+        } else {
+            m = i / TK;
+            k = i % TK;
+        }
+    };
+    int am0, ak0;
+    a_at(0, am0, ak0);
+    const int64_t a_step = (int64_t)(256 / TM) * d.sAk;   // rows-fastest layout
+    const bf16_t* pa = A + (int64_t)min(m0 + am0, d.M - 1) * d.sAm + (int64_t)ak0 * d.sAk;
+    // B rows of this thread: kq + 32 h + r, r = 0..3 (columns past the end read column 0)
+    const bf16_t* pb = B + ob + (int64_t)kq * d.sBk;
+    const int64_t sb = d.sBk;
+    uint2 vb[KH][4];
+    bf16_t va[AE];
+    // Full chunks load without guards; the last, partial chunk clamps each
+    // address and masks the value (a guard around a load would become a branch
+    // and a wait per load).
+    auto load = [&](int k0) {
+        const bf16_t* p = pb + (int64_t)k0 * sb;
+        const uint32_t ckeep = colok ? 0xffffffffu : 0u;
+        if (k0 + TK <= d.K) {
+#pragma unroll
+            for (int h = 0; h < KH; h++)
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const uint2 v = *(const uint2*)(p + (32 * h + r) * sb);
+                    vb[h][r] = make_uint2(v.x & ckeep, v.y & ckeep);
+                }
+            if (mfast) {
+                // one row (clamped) for every element, k steps of 256 / TM
+                const bf16_t* q = pa + (int64_t)k0 * d.sAk;
+                const bool rowok = m0 + am0 < d.M;
+#pragma unroll
+                for (int e = 0; e < AE; e++) {
+                    const bf16_t v = q[e * a_step];
+                    va[e] = rowok ? v : (bf16_t)0;
+                }
+            } else {
+                // one k for every element, rows 256 / TK apart (each clamped)
+                const int64_t ko = (int64_t)(k0 + ak0) * d.sAk;
+#pragma unroll
+                for (int e = 0; e < AE; e++) {
+                    const int mr = m0 + am0 + e * (256 / TK), mc = mr < d.M ? mr : d.M - 1;
+                    const bf16_t v = A[(int64_t)mc * d.sAm + ko];
+                    va[e] = mr < d.M ? v : (bf16_t)0;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int h = 0; h < KH; h++)
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const int k = k0 + kq + 32 * h + r, kc = k < d.K ? k : d.K - 1;
+                    const uint2 v = *(const uint2*)(B + ob + (int64_t)kc * sb);
+                    const uint32_t keep = k < d.K ? ckeep : 0u;
+                    vb[h][r] = make_uint2(v.x & keep, v.y & keep);
+                }
+#pragma unroll
+            for (int e = 0; e < AE; e++) {
+                int m, k;
+                a_at(e, m, k);
+                m += m0;
+                k += k0;
+                const int mc = m < d.M ? m : d.M - 1, kc = k < d.K ? k : d.K - 1;
+                const bf16_t v = A[(int64_t)mc * d.sAm + (int64_t)kc * d.sAk];
+                va[e] = (m < d.M && k < d.K) ? v : (bf16_t)0;
+            }
+        }
+    };
+    f32x16 acc[MT];
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
+    load(0);
+    for (int k0 = 0; k0 < d.K; k0 += TK) {
+        __syncthreads();   // the previous chunk's LDS reads are done
+#pragma unroll
+        for (int e = 0; e < AE; e++) {
+            int m, k;
+            a_at(e, m, k);
+            As[m][k] = va[e];
+        }
+#pragma unroll
+        for (int h = 0; h < KH; h++)
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                // column 4 nq + j, k rows kq + 32 h + 0..3: one 8-byte LDS write
+                auto half = [&](int r) {
+                    const uint2 v = vb[h][r];
+                    const uint32_t w = (j < 2) ? v.x : v.y;
+                    return (j & 1) ? (w >> 16) : (w & 0xffffu);
+                };
+                uint2 w;
+                w.x = half(0) | (half(1) << 16);
+                w.y = half(2) | (half(3) << 16);
+                *(uint2*)&Bs[4 * nq + j][kq + 32 * h] = w;
+            }
+        __syncthreads();
+        if (k0 + TK < d.K) load(k0 + TK);
+        const int kend = min(TK, d.K - k0);
+#pragma unroll
+        for (int kk = 0; kk < TK; kk += 16) {
+            if (kk >= kend) break;
+            const bf16x8 b = lds_bf16x8(&Bs[wave * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+#pragma unroll
+            for (int i = 0; i < MT; i++) {
+                const bf16x8 a = lds_bf16x8(&As[i * 32 + (lane & 31)][kk + 8 * (lane >> 5)]);
+                acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+            }
+        }
+    }
+    const int64_t f = (int64_t)nt * TN + wave * 32 + (lane & 31);
+    if (f >= NF) return;
+    const int64_t g = f / d.N, n = f - g * d.N;
+    int64_t oA, oB, oC;
+    gemm_offsets(d, g, oA, oB, oC);
+#pragma unroll
+    for (int i = 0; i < MT; i++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+            const int m = m0 + i * 32 + mfma32_row(r, lane);
+            if (m < d.M) store(C, oC + (int64_t)m * d.sCm + n, acc[i][r]);
+        }
+}
+
+template <typename TC, int MT, int TK>
+hipError_t gemm_bf16f_launch(const GemmDesc& d, dim3 g, const bf16_t* A, const bf16_t* B, TC* C, hipStream_t s) {
+    constexpr uint32_t lds = (32 * MT + 128) * (TK + 8) * 2;
+    if constexpr (lds > 64 * 1024) {
+        static std::atomic<uint64_t> ok{0};
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+        if (dev < 0 || dev >= 64) return hipErrorInvalidValue;
+        if (!(ok.load() & (1ull << dev))) {
+            e = hipFuncSetAttribute((const void*)gemm_bf16f<TC, MT, TK>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)lds);
+            if (e != hipSuccess) return e;
+            ok.fetch_or(1ull << dev);
+        }
+    }
+    hipLaunchKernelGGL((gemm_bf16f<TC, MT, TK>), g, dim3(256), lds, s, d, A, B, C);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -497,6 +688,26 @@ hipError_t launch_gemm(const Launch& ln, const void* a, const void* b, void* c, 
     // vector loads need 16 B (fp32) / 8 B (bf16) aligned rows of B
     bool vec = (opt & 2) && ((uintptr_t)b % (tIn ? 8 : 16) == 0);
     dim3 g(ln.grid[0]), bl(256);
+    if (tIn && (opt & 4)) {
+        // flattened columns: 8-byte rows of B (N, sBk and the batch strides
+        // multiples of 4 were checked by the lowering; here the base)
+        if ((uintptr_t)b % 8 != 0 || d.N % 4 != 0) return hipErrorInvalidValue;
+        const bf16_t* A = (const bf16_t*)a;
+        const bf16_t* B = (const bf16_t*)b;
+        const bool one = false;   // 256-wide chunks (one block a CU) measured slower
+        if (tC) {
+            bf16_t* C = (bf16_t*)c;
+            if (MT == 2) return one ? gemm_bf16f_launch<bf16_t, 2, 256>(d, g, A, B, C, s)
+                                    : gemm_bf16f_launch<bf16_t, 2, 64>(d, g, A, B, C, s);
+            return one ? gemm_bf16f_launch<bf16_t, 1, 256>(d, g, A, B, C, s)
+                       : gemm_bf16f_launch<bf16_t, 1, 64>(d, g, A, B, C, s);
+        }
+        float* C = (float*)c;
+        if (MT == 2) return one ? gemm_bf16f_launch<float, 2, 256>(d, g, A, B, C, s)
+                                : gemm_bf16f_launch<float, 2, 64>(d, g, A, B, C, s);
+        return one ? gemm_bf16f_launch<float, 1, 256>(d, g, A, B, C, s)
+                   : gemm_bf16f_launch<float, 1, 64>(d, g, A, B, C, s);
+    }
     if (tIn) {
         const bf16_t* A = (const bf16_t*)a;
         const bf16_t* B = (const bf16_t*)b;

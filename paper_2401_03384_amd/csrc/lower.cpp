@@ -181,17 +181,28 @@ bool try_gemm(const PairOp& op, std::vector<Launch>& out) {
         if (d.blocks > 0x7fffffff) continue;
         bool vec = (d.sBk % 4 == 0);
         for (int i = 0; i < d.ng; i++) vec = vec && (d.g_sB[i] % 4 == 0);
+        // bf16 with 8-byte rows: tiles of 32 rows over the flattened (batch,
+        // column) index
+        const bool flat = D.dtype == DT_BF16 && vec && N % 4 == 0 && G * N < ((int64_t)1 << 31);
+        if (flat) {
+            const int64_t nt = cdiv(G * N, 128);
+            MT = 1;
+            d.mtiles = (int32_t)cdiv(M, 32 * MT);
+            d.ntiles = (int32_t)nt;
+            d.blocks = (int64_t)d.mtiles * d.ntiles;
+        }
         Launch ln;
         ln.kind = K_GEMM | dt_bits(D.dtype, F.dtype, C.dtype) |
-                  (((MT == 2 ? 1 : 0) | (vec ? 2 : 0)) << kShiftOpt);
+                  (((MT == 2 ? 1 : 0) | (vec ? 2 : 0) | (flat ? 4 : 0)) << kShiftOpt);
         ln.a = fbuf;
         ln.b = dbuf;
         ln.c = C.buf;
         ln.grid[0] = (uint32_t)d.blocks;
         ln.block[0] = 256;
         set_desc(ln, d);
-        ln.kname = std::string(D.dtype == DT_BF16 ? "gemm_bf16<" : "gemm_f32<") + tname(C.dtype) +
-                   (MT == 2 ? ", 2, " : ", 1, ") + (vec ? "true>" : "false>");
+        ln.kname = flat ? std::string("gemm_bf16f<") + tname(C.dtype) + (MT == 2 ? ", 2>" : ", 1>")
+                        : std::string(D.dtype == DT_BF16 ? "gemm_bf16<" : "gemm_f32<") + tname(C.dtype) +
+                              (MT == 2 ? ", 2, " : ", 1, ") + (vec ? "true>" : "false>");
         out.push_back(ln);
         return true;
     }

@@ -187,6 +187,53 @@ bool run_gemm(const Launch& ln, Ctx& c) {
         const int64_t runs = Gall * d.N;
         REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks * 256 >= runs && (d.blocks - 1) * 256 < runs &&
             ln.block[0] == 256, "grid");
+    } else if ((ln.kind >> kShiftOpt) & 4) {
+        // flattened columns: tiles of 128 over G x N, 8-byte rows of B
+        bool al = tIn && d.N % 4 == 0 && d.sBk % 4 == 0 && Gall * d.N < ((int64_t)1 << 31);
+        for (int i = 0; i < d.ng; i++) al = al && d.g_sB[i] % 4 == 0;
+        REQ(al, "flat gemm alignment");
+        REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks == (int64_t)d.mtiles * d.ntiles && ln.block[0] == 256,
+            "grid");
+        REQ(d.mtiles * 32 * MT >= d.M && (int64_t)d.ntiles * 128 >= Gall * d.N, "tiles do not cover");
+        // the kernel's loads, thread by thread (K in chunks of 64): B at the
+        // thread's column group (column 0 past the end) and rows kq + 32 h + r
+        // (clamped to K - 1 in a partial chunk); A one row (rows fastest) or
+        // one k (k fastest) per thread, clamped the same way
+        const int TM = 32 * MT, TK = 64, AE = TM * TK / 256;
+        const bool mfast = d.sAm == 1 && d.sAk != 1;
+        const int64_t NF = Gall * d.N;
+        bool okl = true;
+        for (int64_t blk = 0; blk < d.blocks && okl; blk++) {
+            const int64_t nt = blk % d.ntiles, mt = blk / d.ntiles;
+            const int m0 = (int)mt * TM;
+            for (int tid = 0; tid < 256 && okl; tid++) {
+                const int nq = tid & 31, kq = 4 * (tid >> 5);
+                const int64_t fb = nt * 128 + 4 * nq;
+                const bool colok = fb < NF;
+                int64_t g = colok ? fb / d.N : 0, ob = 0, x = g;
+                for (int i = d.ng - 1; i >= 0; --i) { ob += (x % d.g_size[i]) * d.g_sB[i]; x /= d.g_size[i]; }
+                ob += colok ? fb - g * d.N : 0;
+                for (int k0 = 0; k0 < d.K; k0 += TK) {
+                    const bool full = k0 + TK <= d.K;
+                    for (int h = 0; h < 2; h++)
+                        for (int r = 0; r < 4; r++) {
+                            int k = k0 + kq + 32 * h + r;
+                            if (!full) k = std::min(k, d.K - 1);
+                            const int64_t i0 = ob + (int64_t)k * d.sBk;
+                            okl = okl && i0 >= 0 && (size_t)(i0 + 4) * 2 <= B.bytes && i0 % 4 == 0;
+                        }
+                    for (int e = 0; e < AE; e++) {
+                        const int i = tid + 256 * e;
+                        int m = mfast ? i % TM : i / TK, k = mfast ? i / TM : i % TK;
+                        m = std::min(m0 + m, d.M - 1);
+                        k = std::min(k0 + k, d.K - 1);
+                        const int64_t ia = (int64_t)m * d.sAm + (int64_t)k * d.sAk;
+                        okl = okl && ia >= 0 && (size_t)(ia + 1) * 2 <= A.bytes;
+                    }
+                }
+            }
+        }
+        REQ(okl, "flat gemm load out of range");
     } else {
         REQ(ln.grid[0] == (uint32_t)d.blocks && d.blocks == (int64_t)d.mtiles * d.ntiles * Gall, "grid");
         REQ(d.mtiles * 32 * MT >= d.M && d.ntiles * 128 >= d.N, "tiles do not cover");

@@ -134,6 +134,11 @@ PARITY_WORKLOADS = {
     "C3c": tucker2_layer("C3c", 2, 24, 40, 5, 11, 20, 40, 3, "bf16", 31),
     "C3c5": tucker2_layer("C3c5", 1, 16, 24, 6, 7, 36, 24, 5, "bf16", 32),
     "C3m": tucker2_layer("C3m", 2, 16, 24, 6, 20, 128, 40, 3, "bf16", 33),
+    # channel mixes over flattened (batch, pixel) columns: 144-pixel planes
+    # across 128-column tiles, reductions of 96 and 48 (a partial 64-chunk),
+    # ragged row tiles (40, 72 rows); and 256 rows in 64-row tiles
+    "C3f": tucker2_layer("C3f", 3, 96, 72, 12, 12, 40, 48, 3, "bf16", 41),
+    "C3f2": tucker2_layer("C3f2", 32, 72, 256, 16, 16, 24, 40, 3, "bf16", 42),
     # the same kernel in fp32 (Tucker core; the tensor-train layer's transposed conv)
     "C3c_f32": tucker2_layer("C3c_f32", 2, 24, 40, 5, 11, 20, 40, 3, "f32", 31),
     "C4c": rtt_layer("C4c", 1, (2, 2, 4), (2, 2, 2), 6, 7, 16, 3, "f32", 34),
