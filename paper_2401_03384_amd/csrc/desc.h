@@ -207,10 +207,11 @@ struct TcDesc {
 //           plane; u = rank (one dim), s = batch (up to two dims); O = the
 //           output gradient; writes partials P[chunk][u][m][tap], summed in
 //           chunk order by K_CREDW_REDUCE.
-//   K_WGCONV (filter gradient, fp32, on MFMA tiles): the same partials as
-//           K_CREDW with u in blocks of 128 (nrb blocks) and every (m, tap)
-//           in one block; O's planes sit in LDS with a zero halo, PH rows of
-//           pitch PWp, double-buffered.
+//   K_WGCONV (filter gradient on fp32 MFMA tiles, fp32 or bf16 planes): the
+//           same partials as K_CREDW with u in blocks of 64 rt (nrb blocks)
+//           and the columns (m, tap) in ncb blocks of 16 nct; a block's mb
+//           planes of O sit in LDS with a zero halo (PH rows of pitch PWp,
+//           fp32), double-buffered.
 // Planes (Z, the output of K_CRED, O of K_CREDW) are dense: row stride W,
 // unit columns.  ch, cw: zero padding before the first row / column.
 struct CredDesc {
@@ -225,6 +226,10 @@ struct CredDesc {
     int64_t gchunk, nrb, nchunks;      // K_CREDW: batch indices per block, rank groups, chunks
     int64_t blocks;
     uint32_t lds_bytes, threads;
+    // K_WGCONV: column blocks of 16 * (column tiles) columns (m, tap), row
+    // tiles of 16 a wavefront (rows a block: 64 * rt), channel planes a
+    // block stages (mb)
+    int32_t ncb, nct, rt, mb;
 };
 
 // Convolution contracted over one channel index, on bf16 MFMA tiles:

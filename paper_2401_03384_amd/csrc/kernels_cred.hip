@@ -330,7 +330,7 @@ hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, 
     std::memcpy(&d, ln.desc.data(), sizeof(d));
     const int kind = ln.kind & 0xff;
     const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
-    if (d.M < 1 || d.M > 16) return hipErrorInvalidValue;
+    if (d.M < 1) return hipErrorInvalidValue;
     if (kind == K_CREDW_REDUCE) {
         // here o = the partials, y = the output
         dim3 g((uint32_t)((d.R * d.M * d.KH * d.KW + 63) / 64)), bl(256);
@@ -338,6 +338,7 @@ hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, 
         else hipLaunchKernelGGL(credw_reduce<float>, g, bl, 0, s, d, (const float*)o, (float*)y);
         return hipGetLastError();
     }
+    if (d.M > 16) return hipErrorInvalidValue;   // the partial-sum kernels: M <= 16
     const bool wgrad = kind == K_CREDW;
     if (!wgrad && tIn != tC) return hipErrorInvalidValue;   // forward keeps the input type
     // four-wide loads: every row start of Z (and of the plane operand of the

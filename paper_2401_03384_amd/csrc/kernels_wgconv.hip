@@ -7,20 +7,23 @@
 // (Appendix B: g2 of a convolution step, the output gradient correlated with
 // the step's input over every pixel and batch index).  Moving the shift from
 // Z onto O, the second form reads every Z value once, unshifted: Z is the
-// large operand (one plane per rank index u and batch index g), O the small
-// one (a few channels m).  As a matrix product: rows u, columns n = (m, tap),
-// reduction over (g, p).
+// large operand (one plane per rank index u and batch index g), O the other
+// one.  As a matrix product: rows u, columns n = (m, tap), reduction over
+// (g, p).  Planes are fp32 or bf16 (converted to fp32 as they load; the
+// products and sums are fp32).
 //
-// A block is four wavefronts with 32 rows of u each; a wavefront holds two
-// row tiles x NT column tiles of 16 in MFMA accumulators.  The pixels of one
-// plane go in groups of 16: lane (i, kq) (i = lane % 16, kq = lane / 16)
-// loads Z[u0 + i][q0 + 4kq .. q0 + 4kq + 3] with one 16-byte load per row
-// tile; element t of it is the lane's K value of the group's MFMA t (pixel
-// q0 + 4kq + t).  The column operand of MFMA t is O at the lane's column
-// (m, tap) and the pixel q0 + 4kq + t shifted by the tap, read from LDS, where
-// the planes of the current g sit with a zero halo (tap offsets are constant
-// per lane).  The planes of g + 1 load into registers while g's groups run
-// (double-buffered LDS); the row loads run two groups ahead.
+// A block is four wavefronts with RT row tiles of 16 each (64 RT rows of u)
+// and NT column tiles of 16 (a column block: the block stages only the planes
+// of O its columns need).  The pixels of one plane go in groups of 16: lane
+// (i, kq) (i = lane % 16, kq = lane / 16) loads Z[u0 + i][q0 + 4kq .. +3] with
+// one 16-byte (fp32) or 8-byte (bf16) load per row tile; element t of it is
+// the lane's K value of the group's MFMA t (pixel q0 + 4kq + t).  The column
+// operand of MFMA t is O at the lane's column (m, tap) and the pixel
+// q0 + 4kq + t shifted by the tap, read from LDS, where the planes of the
+// current g sit with a zero halo (tap offsets are constant per lane).  The
+// planes of g + 1 load into registers while g's groups run (double-buffered
+// LDS); the row loads run kWgAhead groups ahead.
+#include <algorithm>
 #include <atomic>
 #include <cstdint>
 #include <cstring>
@@ -35,6 +38,7 @@ namespace {
 typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
 
 constexpr int kWgStage = 8;   // float4 of the next planes a thread holds while it computes
+constexpr int kWgAhead = 2;   // groups of row loads in flight ahead of the one computed
 
 __device__ __forceinline__ int64_t wg_zoff(const CredDesc& d, int64_t g) {
     int64_t oz = 0;
@@ -53,48 +57,63 @@ __device__ __forceinline__ int64_t wg_ooff(const CredDesc& d, int64_t g) {
     return oy;
 }
 
-template <int NT, bool VEC>
-__global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __restrict__ Z,
-                                                 const float* __restrict__ O, float* __restrict__ P) {
+// four consecutive elements from p (fp32: one 16-byte load; bf16: one 8-byte load)
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4(const bf16_t* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+}
+
+template <typename T, int RT, int NT, bool VEC>
+__global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const T* __restrict__ Z, const T* __restrict__ O,
+                                                 float* __restrict__ P) {
     extern __shared__ float4 lds4[];
     float* pl = reinterpret_cast<float*>(lds4);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int W = d.W, HW = d.H * d.W, WP = d.PWp, PLN = d.PH * d.PWp;
-    const int KK = d.KH * d.KW, N = d.M * KK, BUF = d.M * PLN;
+    const int KK = d.KH * d.KW, N = d.M * KK, BUF = d.mb * PLN;
     const int top = d.KH - 1 - d.ch, left = d.KW - 1 - d.cw;   // halo before the interior
-    const int64_t ub = blockIdx.x % d.nrb, ck = blockIdx.x / d.nrb;
+    const int64_t ub = blockIdx.x % d.nrb, rest = blockIdx.x / d.nrb;
+    const int cb = (int)(rest % d.ncb);
+    const int64_t ck = rest / d.ncb;
     const int64_t g0 = ck * d.gchunk, g1 = min(d.G, g0 + d.gchunk);
     const int i16 = lane & 15, kq = lane >> 4;
-    const int64_t ua = ub * 128 + wave * 32 + i16, uc = ua + 16;
-    const bool oka = ua < d.R, okc = uc < d.R;
-    const int64_t za = (oka ? ua : 0) * d.z_sr, zc = (okc ? uc : 0) * d.z_sr;
+    // this block's columns and the planes of O they read
+    const int n0 = cb * 16 * NT, mlo = n0 / KK;
+    const int mhi = min(d.M, (n0 + 16 * NT - 1) / KK + 1), MB = mhi - mlo;
+    // rows of this wavefront's row tiles
+    const int64_t urow = ub * 64 * RT + wave * 16 * RT + i16;
+    bool rok[RT];
+    int64_t zr[RT];
+#pragma unroll
+    for (int mt = 0; mt < RT; mt++) {
+        rok[mt] = urow + 16 * mt < d.R;
+        zr[mt] = (rok[mt] ? urow + 16 * mt : 0) * d.z_sr;
+    }
 
     // LDS offset of this lane's column (m, tap) in every column tile
     int toff[NT];
 #pragma unroll
     for (int j = 0; j < NT; j++) {
-        const int n = 16 * j + i16;
+        const int n = n0 + 16 * j + i16;
         toff[j] = 0;
         if (n < N) {
             const int m = n / KK, t = n - m * KK, jh = t / d.KW, jw = t - jh * d.KW;
-            toff[j] = m * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw);
+            toff[j] = (m - mlo) * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw);
         }
     }
 
-    // planes of O[g] into buffer `buf`: interior only (the halo stays zero).
-    // The prefetched path holds kWgStage float4 a thread across the groups of
-    // the current g; a float4 is four pixels of one row (W % 4 == 0), and its
-    // offsets are recomputed where they are used from an opaque copy of the
-    // thread index (hoisted out of the loop they would hold 3 kWgStage
-    // registers for its life).
-    const int n4 = (d.M * HW + 3) / 4;   // float4 of one g's planes
+    // planes mlo..mhi-1 of O[g] into buffer `buf`: interior only (the halo
+    // stays zero).  The prefetched path holds kWgStage float4 a thread across
+    // the groups of the current g; a float4 is four pixels of one row
+    // (W % 4 == 0), and its offsets are recomputed where they are used from an
+    // opaque copy of the thread index (hoisted out of the loop they would hold
+    // 3 kWgStage registers for its life).
+    const int n4 = (MB * HW + 3) / 4;   // float4 of one g's planes
     const bool pref = VEC && W % 4 == 0 && n4 <= 256 * kWgStage;
-    auto put = [&](int buf, int e, float v) {
-        const int m = e / HW, p = e - m * HW, h = p / W, w = p - h * W;
-        pl[buf * BUF + m * PLN + (h + top) * WP + (w + left)] = v;
-    };
     auto stage_load = [&](int64_t g, float4 (&sv)[kWgStage]) {
-        const float* src = O + wg_ooff(d, g);
+        const T* src = O + wg_ooff(d, g) + (int64_t)mlo * d.o_sm;
         int t0 = tid;
         asm volatile("" : "+v"(t0));
 #pragma unroll
@@ -102,7 +121,7 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
             const int e4 = t0 + 256 * k;
             if (e4 < n4) {
                 const int e = 4 * e4, m = e / HW, p = e - m * HW;
-                sv[k] = *reinterpret_cast<const float4*>(src + m * d.o_sm + p);
+                sv[k] = ld4(src + m * d.o_sm + p);
             }
         }
     };
@@ -123,10 +142,10 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
         }
     };
     auto stage_direct = [&](int64_t g, int buf) {   // without the register prefetch
-        const float* src = O + wg_ooff(d, g);
-        for (int e = tid; e < d.M * HW; e += 256) {
-            const int m = e / HW, p = e - m * HW;
-            put(buf, e, src[m * d.o_sm + p]);
+        const T* src = O + wg_ooff(d, g) + (int64_t)mlo * d.o_sm;
+        for (int e = tid; e < MB * HW; e += 256) {
+            const int m = e / HW, p = e - m * HW, h = p / W, w = p - h * W;
+            pl[buf * BUF + m * PLN + (h + top) * WP + (w + left)] = load(src, m * d.o_sm + p);
         }
     };
 
@@ -148,25 +167,26 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
     int64_t lg = g0;
     int lq = 0;
     int64_t loz = g0 < g1 ? wg_zoff(d, g0) : 0;
-    auto load_item = [&](float4 (&dst)[2]) {
-        dst[0] = dst[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto load_item = [&](float4 (&dst)[RT]) {
+#pragma unroll
+        for (int mt = 0; mt < RT; mt++) dst[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
         if (lg < g1) {
             const int q = 16 * lq + 4 * kq;
             if constexpr (VEC) {
                 if (q < HW) {
-                    if (oka) dst[0] = *reinterpret_cast<const float4*>(Z + loz + za + q);
-                    if (okc) dst[1] = *reinterpret_cast<const float4*>(Z + loz + zc + q);
+#pragma unroll
+                    for (int mt = 0; mt < RT; mt++)
+                        if (rok[mt]) dst[mt] = ld4(Z + loz + zr[mt] + q);
                 }
             } else {
-                float a[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int t = 0; t < 4; t++)
-                    if (q + t < HW) {
-                        if (oka) a[t] = Z[loz + za + q + t];
-                        if (okc) c[t] = Z[loz + zc + q + t];
-                    }
-                dst[0] = make_float4(a[0], a[1], a[2], a[3]);
-                dst[1] = make_float4(c[0], c[1], c[2], c[3]);
+                for (int mt = 0; mt < RT; mt++) {
+                    float a[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int t = 0; t < 4; t++)
+                        if (q + t < HW && rok[mt]) a[t] = load(Z, loz + zr[mt] + q + t);
+                    dst[mt] = make_float4(a[0], a[1], a[2], a[3]);
+                }
             }
         }
         if (++lq == NG) {
@@ -176,15 +196,17 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
         }
     };
 
-    f32x4 acc[2][NT];
+    f32x4 acc[RT][NT];
 #pragma unroll
-    for (int mt = 0; mt < 2; mt++)
+    for (int mt = 0; mt < RT; mt++)
 #pragma unroll
         for (int j = 0; j < NT; j++) acc[mt][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    float4 ra0[2], ra1[2], rn[2];
-    load_item(ra0);
-    load_item(ra1);
+    // ring of row loads: ra[0] is the group computed now, ra[1..kWgAhead-1]
+    // and rn the ones in flight
+    float4 ra[kWgAhead][RT], rn[RT];
+#pragma unroll
+    for (int i = 0; i < kWgAhead; i++) load_item(ra[i]);
     for (int64_t g = g0; g < g1; g++) {
         const int cur = (int)((g - g0) & 1);
         const bool more = g + 1 < g1;
@@ -213,19 +235,21 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
             for (int t = 0; t < 4; t++)
 #pragma unroll
                 for (int j = 0; j < NT; j++) bv[j][t] = pb[bt[t] + toff[j]];
-            const float a0[4] = {ra0[0].x, ra0[0].y, ra0[0].z, ra0[0].w};
-            const float a1[4] = {ra0[1].x, ra0[1].y, ra0[1].z, ra0[1].w};
 #pragma unroll
             for (int t = 0; t < 4; t++)
 #pragma unroll
-                for (int j = 0; j < NT; j++) {
-                    acc[0][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[t], bv[j][t], acc[0][j], 0, 0, 0);
-                    acc[1][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[t], bv[j][t], acc[1][j], 0, 0, 0);
+                for (int mt = 0; mt < RT; mt++) {
+                    const float a = t == 0 ? ra[0][mt].x : t == 1 ? ra[0][mt].y : t == 2 ? ra[0][mt].z : ra[0][mt].w;
+#pragma unroll
+                    for (int j = 0; j < NT; j++)
+                        acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[j][t], acc[mt][j], 0, 0, 0);
                 }
-            ra0[0] = ra1[0];
-            ra0[1] = ra1[1];
-            ra1[0] = rn[0];
-            ra1[1] = rn[1];
+#pragma unroll
+            for (int mt = 0; mt < RT; mt++) {
+#pragma unroll
+                for (int i = 0; i + 1 < kWgAhead; i++) ra[i][mt] = ra[i + 1][mt];
+                ra[kWgAhead - 1][mt] = rn[mt];
+            }
             w0 += 16;
             while (w0 >= W) {
                 w0 -= W;
@@ -241,20 +265,20 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const float* __rest
 
     // accumulator r of a lane: row 4 kq + r of the tile, column i16
 #pragma unroll
-    for (int mt = 0; mt < 2; mt++)
+    for (int mt = 0; mt < RT; mt++)
 #pragma unroll
         for (int j = 0; j < NT; j++)
 #pragma unroll
             for (int r = 0; r < 4; r++) {
-                const int64_t u = ub * 128 + wave * 32 + 16 * mt + 4 * kq + r;
-                const int n = 16 * j + i16;
+                const int64_t u = ub * 64 * RT + wave * 16 * RT + 16 * mt + 4 * kq + r;
+                const int n = n0 + 16 * j + i16;
                 if (u < d.R && n < N) P[(ck * d.R + u) * N + n] = acc[mt][j][r];
             }
 }
 
-template <int NT>
-hipError_t wgconv_nt(const CredDesc& d, bool vec, const float* z, const float* o, float* part, hipStream_t s) {
-    auto k = vec ? wgconv<NT, true> : wgconv<NT, false>;
+template <typename T, int RT, int NT>
+hipError_t wgconv_go(const CredDesc& d, bool vec, const void* z, const void* o, float* part, hipStream_t s) {
+    auto k = vec ? wgconv<T, RT, NT, true> : wgconv<T, RT, NT, false>;
     static std::atomic<uint64_t> ok{0};
     // dynamic LDS above 64 KB has to be allowed per kernel, once per device
     if (d.lds_bytes > 64 * 1024) {
@@ -263,16 +287,16 @@ hipError_t wgconv_nt(const CredDesc& d, bool vec, const float* z, const float* o
         if (e != hipSuccess) return e;
         if (dev < 0 || dev >= 64 || d.lds_bytes > 160 * 1024) return hipErrorInvalidValue;
         if (!(ok.load() & (1ull << dev))) {
-            e = hipFuncSetAttribute((const void*)wgconv<NT, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    160 * 1024);
+            e = hipFuncSetAttribute((const void*)wgconv<T, RT, NT, true>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
             if (e == hipSuccess)
-                e = hipFuncSetAttribute((const void*)wgconv<NT, false>,
+                e = hipFuncSetAttribute((const void*)wgconv<T, RT, NT, false>,
                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
             if (e != hipSuccess) return e;
             ok.fetch_or(1ull << dev);
         }
     }
-    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, z, o, part);
+    hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)z, (const T*)o, part);
     return hipGetLastError();
 }
 
@@ -281,30 +305,42 @@ hipError_t wgconv_nt(const CredDesc& d, bool vec, const float* z, const float* o
 hipError_t launch_wgconv(const Launch& ln, const void* z, const void* o, void* part, hipStream_t s) {
     CredDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    const int KK = d.KH * d.KW, N = d.M * KK, NT = (N + 15) / 16;
+    const int bf = (ln.kind >> kBitIn) & 1;
+    const int KK = d.KH * d.KW, N = d.M * KK;
     // the shapes the kernel assumes (the lowering guarantees them)
-    if (((ln.kind >> kBitIn) & 1) || d.M < 1 || KK < 1 || NT < 1 || NT > 6 || d.H < 1 || d.W < 1 ||
+    const bool nct_ok = bf ? (d.nct == 6 || (d.nct == 3 && N <= 48)) : (d.nct >= 1 && d.nct <= 6);
+    if (d.M < 1 || KK < 1 || !nct_ok || (d.rt != 1 && d.rt != 2) || (!bf && d.rt != 2) ||
+        d.ncb != (N + 16 * d.nct - 1) / (16 * d.nct) || d.mb < 1 || d.mb > d.M || d.H < 1 || d.W < 1 ||
         d.PH != d.H + d.KH - 1 || d.PWp < d.W + d.KW - 1 || d.ch < 0 || d.ch >= d.KH || d.cw < 0 ||
-        d.cw >= d.KW || d.nrb != (d.R + 127) / 128 || d.gchunk < 1 || d.nchunks != (d.G + d.gchunk - 1) / d.gchunk ||
-        d.blocks != d.nrb * d.nchunks || d.lds_bytes != (uint32_t)(2 * d.M * d.PH * d.PWp * 4) ||
-        d.lds_bytes > 160 * 1024 || (int64_t)d.H * d.W * d.M >= (1ll << 30) || ln.grid[0] != (uint32_t)d.blocks ||
-        ln.block[0] != 256)
+        d.cw >= d.KW || d.nrb != (d.R + 64 * d.rt - 1) / (64 * d.rt) || d.gchunk < 1 ||
+        d.nchunks != (d.G + d.gchunk - 1) / d.gchunk || d.blocks != (int64_t)d.nrb * d.ncb * d.nchunks ||
+        d.lds_bytes != (uint32_t)(2 * d.mb * d.PH * d.PWp * 4) || d.lds_bytes > 160 * 1024 ||
+        (int64_t)d.H * d.W * d.M >= (1ll << 30) || ln.grid[0] != (uint32_t)d.blocks || ln.block[0] != 256)
         return hipErrorInvalidValue;
-    // 16-byte loads: rows of Z and of O start at multiples of four floats
+    // every column block's planes fit the mb staged
+    for (int cb = 0; cb < d.ncb; cb++) {
+        const int n0 = cb * 16 * d.nct, mlo = n0 / KK, mhi = std::min(d.M, (n0 + 16 * d.nct - 1) / KK + 1);
+        if (mhi - mlo > d.mb) return hipErrorInvalidValue;
+    }
+    // wide loads: rows of Z and of O start at multiples of four elements
     const int64_t HW = (int64_t)d.H * d.W;
-    bool vec = HW % 4 == 0 && d.z_sr % 4 == 0 && (d.M == 1 || d.o_sm % 4 == 0) && (uintptr_t)z % 16 == 0 &&
-               (uintptr_t)o % 16 == 0;
+    const uintptr_t al = bf ? 8 : 16;
+    bool vec = HW % 4 == 0 && d.z_sr % 4 == 0 && (d.M == 1 || d.o_sm % 4 == 0) && (uintptr_t)z % al == 0 &&
+               (uintptr_t)o % al == 0;
     for (int i = 0; i < d.ng; i++) vec = vec && d.g_sZ[i] % 4 == 0 && d.g_sY[i] % 4 == 0;
-    const float* Z = (const float*)z;
-    const float* O = (const float*)o;
     float* Pp = (float*)part;
-    switch (NT) {
-        case 1: return wgconv_nt<1>(d, vec, Z, O, Pp, s);
-        case 2: return wgconv_nt<2>(d, vec, Z, O, Pp, s);
-        case 3: return wgconv_nt<3>(d, vec, Z, O, Pp, s);
-        case 4: return wgconv_nt<4>(d, vec, Z, O, Pp, s);
-        case 5: return wgconv_nt<5>(d, vec, Z, O, Pp, s);
-        default: return wgconv_nt<6>(d, vec, Z, O, Pp, s);
+    if (bf) {
+        if (d.rt == 1) return d.nct == 6 ? wgconv_go<bf16_t, 1, 6>(d, vec, z, o, Pp, s)
+                                         : wgconv_go<bf16_t, 1, 3>(d, vec, z, o, Pp, s);
+        return d.nct == 6 ? wgconv_go<bf16_t, 2, 6>(d, vec, z, o, Pp, s) : wgconv_go<bf16_t, 2, 3>(d, vec, z, o, Pp, s);
+    }
+    switch (d.nct) {
+        case 1: return wgconv_go<float, 2, 1>(d, vec, z, o, Pp, s);
+        case 2: return wgconv_go<float, 2, 2>(d, vec, z, o, Pp, s);
+        case 3: return wgconv_go<float, 2, 3>(d, vec, z, o, Pp, s);
+        case 4: return wgconv_go<float, 2, 4>(d, vec, z, o, Pp, s);
+        case 5: return wgconv_go<float, 2, 5>(d, vec, z, o, Pp, s);
+        default: return wgconv_go<float, 2, 6>(d, vec, z, o, Pp, s);
     }
 }
 

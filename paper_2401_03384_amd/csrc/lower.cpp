@@ -707,9 +707,12 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
     std::vector<Dm>& Rd = wgrad ? U : S;
     if (Bd.size() > 2 || Rd.size() > 1 || Mv.size() > 1) return false;
     const int64_t M = Mv.empty() ? 1 : Mv[0].size;
-    if (wgrad && Z.dtype == DT_F32 && O.dtype == DT_F32 && M * KH * KW <= 96) {
-        // fp32 filter gradient on MFMA tiles: u in blocks of 128 rows, the
-        // batch split into about two blocks a CU, two LDS copies of O's planes
+    if (wgrad && Z.dtype == O.dtype) {
+        // filter gradient on fp32 MFMA tiles: rows u in blocks of 64 rt, the
+        // columns (m, tap) in blocks of 16 nct (each block stages the planes
+        // of O its columns read), the batch split into about two blocks a CU
+        const bool bf = Z.dtype == DT_BF16;
+        const int64_t N = M * KH * KW, KK = KH * KW;
         CredDesc d;
         std::memset(&d, 0, sizeof(d));
         d.H = (int32_t)H;
@@ -736,18 +739,26 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
         d.c_sr = Rd.empty() ? 0 : Rd[0].s2;
         d.c_sh = C.stride_of(ch.label);
         d.c_sw = C.stride_of(cw.label);
-        d.nrb = cdiv(d.R, 128);
-        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(512, d.nrb)));
+        d.rt = (bf && d.R <= 64) ? 1 : 2;
+        d.nct = bf ? (N <= 48 ? 3 : 6) : (int32_t)std::min<int64_t>(6, cdiv(N, 16));
+        d.ncb = (int32_t)cdiv(N, 16 * d.nct);
+        d.mb = 1;
+        for (int64_t cb = 0; cb < d.ncb; cb++) {
+            const int64_t n0 = cb * 16 * d.nct, mlo = n0 / KK, mhi = std::min<int64_t>(M, (n0 + 16 * d.nct - 1) / KK + 1);
+            d.mb = (int32_t)std::max<int64_t>(d.mb, mhi - mlo);
+        }
+        d.nrb = cdiv(d.R, 64 * d.rt);
+        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(d.G, cdiv(512, d.nrb * d.ncb)));
         d.gchunk = cdiv(d.G, chunks);
         d.nchunks = cdiv(d.G, d.gchunk);
-        d.blocks = d.nrb * d.nchunks;
+        d.blocks = d.nrb * d.ncb * d.nchunks;
         d.threads = 256;
-        const int64_t lds = 2 * M * d.PH * d.PWp * 4;
+        const int64_t lds = 2 * (int64_t)d.mb * d.PH * d.PWp * 4;
         if (lds <= 160 * 1024 && d.blocks <= 0x7fffffff && H * W * M < ((int64_t)1 << 30)) {
             d.lds_bytes = (uint32_t)lds;
-            const BufRef part = scratch.alloc((size_t)(d.nchunks * d.R * M * KH * KW * 4));
+            const BufRef part = scratch.alloc((size_t)(d.nchunks * d.R * N * 4));
             Launch ln;
-            ln.kind = K_WGCONV | dt_bits(DT_F32, DT_F32, DT_F32);
+            ln.kind = K_WGCONV | dt_bits(Z.dtype, Z.dtype, DT_F32);
             ln.a = Z.buf;
             ln.b = O.buf;
             ln.d = part;
@@ -755,13 +766,14 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
             ln.block[0] = 256;
             ln.lds = d.lds_bytes;
             set_desc(ln, d);
-            ln.kname = "wgconv<" + std::to_string((M * KH * KW + 15) / 16) + ">";
+            ln.kname = std::string("wgconv<") + tname(Z.dtype) + ", " + std::to_string(d.rt) + ", " +
+                       std::to_string(d.nct) + ">";
             out.push_back(ln);
             Launch lr;
             lr.kind = K_CREDW_REDUCE | dt_bits(DT_F32, DT_F32, C.dtype);
             lr.d = part;
             lr.c = C.buf;
-            lr.grid[0] = (uint32_t)cdiv(d.R * M * KH * KW, 64);   // 64 outputs per block
+            lr.grid[0] = (uint32_t)cdiv(d.R * N, 64);   // 64 outputs per block
             lr.block[0] = 256;
             set_desc(lr, d);
             lr.kname = std::string("credw_reduce<") + tname(C.dtype) + ">";

@@ -1321,7 +1321,7 @@ bool run_cred(const Launch& ln, Ctx& c) {
     const bool wgrad = kind == K_CREDW;
     int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
     const int KK = d.KH * d.KW, MO = d.M == 1 ? 1 : d.M <= 4 ? 4 : d.M <= 8 ? 8 : 16;
-    REQ(d.M >= 1 && d.M <= 16, "channels");
+    REQ(d.M >= 1, "channels");
     bool ok = true, o1, o2, o3;
     if (kind == K_CREDW_REDUCE) {
         Buf Pb = resolve(ln.d, c, 0, o1), Cb = resolve(ln.c, c, 0, o2);
@@ -1339,6 +1339,7 @@ bool run_cred(const Launch& ln, Ctx& c) {
         REQ(ok, "out-of-bounds access (credw reduce)");
         return true;
     }
+    REQ(d.M <= 16, "channels");
     Buf Z = resolve(wgrad ? ln.a : ln.b, c, 0, o1), O = resolve(wgrad ? ln.b : ln.a, c, 0, o2);
     Buf Y = resolve(wgrad ? ln.d : ln.c, c, 0, o3);
     REQ(o1 && o2 && o3, "unresolved buffer");
@@ -1429,20 +1430,24 @@ bool run_cred(const Launch& ln, Ctx& c) {
 // arithmetic; then the partial sums it defines, in double.
 bool run_wgconv(const Launch& ln, Ctx& c) {
     CredDesc d = desc_of<CredDesc>(ln);
-    const int KK = d.KH * d.KW, N = d.M * KK, NT = (N + 15) / 16;
-    REQ(((ln.kind >> kBitIn) & 1) == 0 && d.M >= 1 && KK >= 1 && NT >= 1 && NT <= 6 && d.H >= 1 && d.W >= 1 &&
+    const int tIn = (ln.kind >> kBitIn) & 1;
+    const int KK = d.KH * d.KW, N = d.M * KK;
+    const bool nct_ok = tIn ? (d.nct == 6 || (d.nct == 3 && N <= 48)) : (d.nct >= 1 && d.nct <= 6);
+    REQ(d.M >= 1 && KK >= 1 && nct_ok && (d.rt == 1 || d.rt == 2) && (tIn || d.rt == 2) &&
+            d.ncb == (N + 16 * d.nct - 1) / (16 * d.nct) && d.mb >= 1 && d.mb <= d.M && d.H >= 1 && d.W >= 1 &&
             d.PH == d.H + d.KH - 1 && d.PWp >= d.W + d.KW - 1 && d.ch >= 0 && d.ch < d.KH && d.cw >= 0 &&
-            d.cw < d.KW && d.nrb == (d.R + 127) / 128 && d.gchunk >= 1 &&
-            d.nchunks == (d.G + d.gchunk - 1) / d.gchunk && d.blocks == d.nrb * d.nchunks &&
-            d.lds_bytes == (uint32_t)(2 * d.M * d.PH * d.PWp * 4) && d.lds_bytes <= 160 * 1024 &&
+            d.cw < d.KW && d.nrb == (d.R + 64 * d.rt - 1) / (64 * d.rt) && d.gchunk >= 1 &&
+            d.nchunks == (d.G + d.gchunk - 1) / d.gchunk && d.blocks == (int64_t)d.nrb * d.ncb * d.nchunks &&
+            d.lds_bytes == (uint32_t)(2 * d.mb * d.PH * d.PWp * 4) && d.lds_bytes <= 160 * 1024 &&
             (int64_t)d.H * d.W * d.M < (1ll << 30) && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256 &&
             ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2,
         "wgconv layout");
     bool ok = true, o1, o2, o3;
     Buf Z = resolve(ln.a, c, 0, o1), O = resolve(ln.b, c, 0, o2), Pb = resolve(ln.d, c, 0, o3);
     REQ(o1 && o2 && o3, "unresolved buffer");
-    const int64_t HW = (int64_t)d.H * d.W, WP = d.PWp, PLN = (int64_t)d.PH * d.PWp, BUF = d.M * PLN;
-    const int64_t zn = (int64_t)(Z.bytes / 4), on = (int64_t)(O.bytes / 4), pn = (int64_t)(Pb.bytes / 4);
+    const int64_t HW = (int64_t)d.H * d.W, WP = d.PWp, PLN = (int64_t)d.PH * d.PWp, BUF = d.mb * PLN;
+    const size_t es = tIn ? 2 : 4;
+    const int64_t zn = (int64_t)(Z.bytes / es), on = (int64_t)(O.bytes / es), pn = (int64_t)(Pb.bytes / 4);
     const int top = d.KH - 1 - d.ch, left = d.KW - 1 - d.cw;
     auto offs = [&](int64_t g, int64_t& oz, int64_t& oy) {
         oz = oy = 0;
@@ -1453,52 +1458,53 @@ bool run_wgconv(const Launch& ln, Ctx& c) {
             oy += x * d.g_sY[i];
         }
     };
-    // every lane's LDS column offset and the largest shifted-plane read
-    int64_t toff_max = 0;
-    for (int n = 0; n < N; n++) {
-        const int m = n / KK, t = n % KK, jh = t / d.KW, jw = t % d.KW;
-        toff_max = std::max<int64_t>(toff_max, m * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw));
-    }
-    REQ((d.H - 1) * WP + (d.W - 1) + toff_max < BUF, "wgconv lds read range");
-    REQ((int64_t)(d.M - 1) * PLN + (d.H - 1 + top) * WP + (d.W - 1 + left) < BUF, "wgconv lds write range");
+    const int rows = 64 * d.rt;
     for (int64_t b = 0; b < d.blocks; b++) {
-        const int64_t ub = b % d.nrb, ck = b / d.nrb;
+        const int64_t ub = b % d.nrb, rest = b / d.nrb, ck = rest / d.ncb;
+        const int cb = (int)(rest % d.ncb);
+        const int n0 = cb * 16 * d.nct, mlo = n0 / KK, mhi = std::min(d.M, (n0 + 16 * d.nct - 1) / KK + 1);
+        REQ(mhi - mlo <= d.mb, "wgconv planes of a column block");
+        // the block's LDS reads (its columns' shifted planes) and writes (the interior)
+        int64_t toff_max = 0;
+        for (int n = n0; n < std::min(N, n0 + 16 * d.nct); n++) {
+            const int m = n / KK, t = n % KK, jh = t / d.KW, jw = t % d.KW;
+            toff_max = std::max<int64_t>(toff_max, (m - mlo) * PLN + (d.KH - 1 - jh) * WP + (d.KW - 1 - jw));
+        }
+        REQ((d.H - 1) * WP + (d.W - 1) + toff_max < BUF, "wgconv lds read range");
+        REQ((int64_t)(mhi - mlo - 1) * PLN + (d.H - 1 + top) * WP + (d.W - 1 + left) < BUF, "wgconv lds write range");
         const int64_t g0 = ck * d.gchunk, g1 = std::min(d.G, g0 + d.gchunk);
         for (int64_t g = g0; g < g1; g++) {
             int64_t oz, oy;
             offs(g, oz, oy);
-            // the staged planes of O (all threads together read every element)
-            for (int m = 0; m < d.M; m++)
+            for (int m = mlo; m < mhi; m++)
                 REQ(oy + m * d.o_sm >= 0 && oy + m * d.o_sm + HW <= on, "wgconv O range");
-            // the row loads of the block's 128 rows
-            for (int64_t r = 0; r < 128; r++) {
-                const int64_t u = ub * 128 + r;
+            for (int64_t r = 0; r < rows; r++) {
+                const int64_t u = ub * rows + r;
                 if (u >= d.R) continue;
                 REQ(oz + u * d.z_sr >= 0 && oz + u * d.z_sr + HW <= zn, "wgconv Z range");
             }
         }
-        for (int64_t r = 0; r < 128; r++) {
-            const int64_t u = ub * 128 + r;
+        for (int64_t r = 0; r < rows; r++) {
+            const int64_t u = ub * rows + r;
             if (u >= d.R) continue;
-            REQ((ck * d.R + u) * N + N <= pn, "wgconv partial range");
+            const int nend = std::min(N, n0 + 16 * d.nct);
+            REQ((ck * d.R + u) * N + nend <= pn, "wgconv partial range");
             std::vector<double> acc((size_t)N, 0.0);
             for (int64_t g = g0; g < g1; g++) {
                 int64_t oz, oy;
                 offs(g, oz, oy);
                 for (int64_t h = 0; h < d.H; h++)
                     for (int64_t w = 0; w < d.W; w++) {
-                        const double z = ld(Z, 0, oz + u * d.z_sr + h * d.W + w, ok);
-                        for (int m = 0; m < d.M; m++)
-                            for (int jh = 0; jh < d.KH; jh++)
-                                for (int jw = 0; jw < d.KW; jw++) {
-                                    const int64_t hh = h - jh + d.ch, ww = w - jw + d.cw;
-                                    if (hh < 0 || hh >= d.H || ww < 0 || ww >= d.W) continue;
-                                    acc[(size_t)(m * KK + jh * d.KW + jw)] +=
-                                        z * ld(O, 0, oy + m * d.o_sm + hh * d.W + ww, ok);
-                                }
+                        const double z = ld(Z, tIn, oz + u * d.z_sr + h * d.W + w, ok);
+                        for (int n = n0; n < nend; n++) {
+                            const int m = n / KK, t = n % KK, jh = t / d.KW, jw = t % d.KW;
+                            const int64_t hh = h - jh + d.ch, ww = w - jw + d.cw;
+                            if (hh < 0 || hh >= d.H || ww < 0 || ww >= d.W) continue;
+                            acc[(size_t)n] += z * ld(O, tIn, oy + m * d.o_sm + hh * d.W + ww, ok);
+                        }
                     }
             }
-            for (int n = 0; n < N; n++) st(Pb, 0, (ck * d.R + u) * N + n, (float)acc[(size_t)n], ok);
+            for (int n = n0; n < nend; n++) st(Pb, 0, (ck * d.R + u) * N + n, (float)acc[(size_t)n], ok);
         }
     }
     REQ(ok, "out-of-bounds access (wgconv)");

@@ -345,7 +345,7 @@ def test_left_to_right_plan(P, name):
 
 
 @pytest.mark.parametrize("name,ltr", [("C2s", True), ("C2s_bf16", True), ("C4s", False),
-                                      ("C3s", False), ("C5as_f32", True)])
+                                      ("C3c5", False), ("C5as_f32", True)])
 def test_wide_offsets(P, name, ltr):
     """CE_FLAG_WIDE_OFFSETS: the general contraction kernel's 64-bit offset
     path (used for operands beyond 2 GiB) at small sizes, against the oracle
