@@ -67,6 +67,7 @@ enum KernelKind : int32_t {
     K_TT_FWD = 37,          // fused contraction + convolution of a tensor-train chain (TtDesc)
     K_TT_PREP = 38,         // its convolution's A operands in load order (TtDesc)
     K_WGCONV = 39,          // K_CREDW's partials on fp32 MFMA tiles (CredDesc)
+    K_GPAIR = 40,           // both gradients of a channel-mixing step from one read of dC (GpairDesc)
 };
 
 // Launch kind = variant | element-type bits (1 = bfloat16, 0 = float32).
@@ -106,6 +107,23 @@ struct ReduceDesc {
     int32_t M, N;
     int64_t nsplit;
     int64_t sCm, sCn;
+};
+
+// Both gradients of a channel-mixing step C[g][k][n] = sum_m A[g][m][n] F[k][m]
+// (fp32) from one read of the output gradient G = dC:
+//   dA[g][m][n] = sum_k F[k][m] G[g][k][n]
+//   P[blk][F's layout] = sum over the block's g and every n of A[g][m][n] G[g][k][n]
+// n: unit-stride in A, G and dA; k = (k1, k2) with k2 fastest (K = K1 K2);
+// g: up to two dims.  A block takes gper consecutive g, all n in tiles of 64
+// and the reduction over k in nkc chunks of 64; M <= 32, K <= 64 nkc <= 512.
+struct GpairDesc {
+    int32_t M, K, K1, K2, N, ng;
+    int32_t nkc, ntiles;
+    int64_t G, gper, blocks;
+    int64_t g_size[2], g_sA[2], g_sG[2], g_sD[2];
+    int64_t sAm, sDm, sFm, sG1, sG2, sF1, sF2;
+    int64_t fnumel;            // elements of F (dense): one partial's size
+    uint32_t lds_bytes, pad_;
 };
 
 // Waves a block of the ordered partial sums (64 outputs a block), from the

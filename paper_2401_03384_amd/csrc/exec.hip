@@ -75,6 +75,7 @@ hipError_t raw_launch(const Launch& ln, const Ptrs& P, hipStream_t s) {
             for (int i = 0; i < 8; i++) ops[3 + i] = resolve(ln.extra[i], P);
             return launch_cp_bwd(ln, ops, s);
         }
+        case K_GPAIR: return launch_gpair(ln, a, b, c, resolve(ln.extra[0], P), d, s);
         case K_REDUCE_MULTI: {
             const void* parts[4] = {};
             void* outs[4] = {};

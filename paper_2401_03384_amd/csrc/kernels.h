@@ -33,6 +33,12 @@ hipError_t launch_cred(const Launch& ln, const void* z, const void* o, void* y, 
 // o = the output gradient, part = the fp32 partials (summed by K_CREDW_REDUCE).
 hipError_t launch_wgconv(const Launch& ln, const void* z, const void* o, void* part, hipStream_t s);
 
+// Both gradients of a channel-mixing step (K_GPAIR, GpairDesc): a = the
+// step's activation input A, f = its factor F, g = the output gradient, da =
+// dA (NULL: not wanted), part = the per-block partials of dF.
+hipError_t launch_gpair(const Launch& ln, const void* a, const void* f, const void* g, void* da, void* part,
+                        hipStream_t s);
+
 // Thin channel mixing (K_THIN, GemmDesc): a = factor, b = activations, c = out.
 hipError_t launch_thin(const Launch& ln, const void* a, const void* b, void* c, hipStream_t s);
 

@@ -1242,7 +1242,190 @@ bool try_tc(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out, b
     return true;
 }
 
+// ---- both gradients of a channel-mixing step in one launch -----------------
+// The step C[g][k][n] = sum_m A[g][m][n] F[k][m] (fp32); gl = its "grad lhs"
+// op (dC x rhs -> d lhs), gr = its "grad rhs" op (lhs x dC -> d rhs).
+bool try_gpair_ops(const PairOp& gl, const PairOp& gr, ScratchAlloc& scratch, std::vector<Launch>& out,
+                   int& fside) {
+    if (!gl.has_r || !gr.has_r || !gl.convs.empty() || !gr.convs.empty()) return false;
+    const TensorRef& Gt = gl.L;   // the output gradient
+    for (int side = 0; side < 2; side++) {
+        // side 0: lhs = A (activation), rhs = F; side 1: lhs = F, rhs = A
+        const TensorRef& At = side == 0 ? gr.L : gl.R;
+        const TensorRef& Ft = side == 0 ? gl.R : gr.L;
+        const TensorRef& dAt = side == 0 ? gl.C : gr.C;
+        const TensorRef& dFt = side == 0 ? gr.C : gl.C;
+        if (At.dtype != DT_F32 || Ft.dtype != DT_F32 || Gt.dtype != DT_F32 || dAt.dtype != DT_F32 ||
+            dFt.dtype != DT_F32)
+            continue;
+        // dA and dF have the layouts of A and F
+        bool same = dAt.labels == At.labels && dFt.labels == Ft.labels && dFt.strides == Ft.strides;
+        if (!same) continue;
+        // label classes
+        std::vector<int> ml, kl, gl_, nl;
+        bool ok = true;
+        for (int l : At.labels) {
+            const bool inF = Ft.has(l), inG = Gt.has(l);
+            if (inF && inG) ok = false;
+            else if (inF) ml.push_back(l);
+            else if (!inG) ok = false;
+        }
+        for (int l : Ft.labels)
+            if (!At.has(l)) {
+                if (Gt.has(l)) kl.push_back(l);
+                else ok = false;
+            }
+        for (int l : Gt.labels)
+            if (!At.has(l) && !Ft.has(l)) ok = false;
+        if (!ok || ml.empty() || kl.empty()) continue;
+        // n: the innermost labels of G, unit-stride runs in A, G and dA
+        int64_t expect = 1;
+        for (int k = (int)Gt.labels.size() - 1; k >= 0; --k) {
+            const int l = Gt.labels[k];
+            if (!At.has(l) || Ft.has(l)) break;
+            if (Gt.strides[k] != expect || At.stride_of(l) != expect || dAt.stride_of(l) != expect) break;
+            nl.insert(nl.begin(), l);
+            expect *= Gt.dims[k];
+        }
+        if (nl.empty()) continue;
+        const int64_t N = expect;
+        for (int l : Gt.labels)
+            if (At.has(l) && std::find(nl.begin(), nl.end(), l) == nl.end()) gl_.push_back(l);
+        // m: one merged dim in A, dA and F
+        int64_t M, sAm, sDm, sFm, t1, t2;
+        if (!merged(At, ml, M, sAm) || !merged(dAt, ml, t1, sDm) || !merged(Ft, ml, t2, sFm)) {
+            // try m in F's order
+            std::vector<int> mf;
+            for (int l : Ft.labels)
+                if (std::find(ml.begin(), ml.end(), l) != ml.end()) mf.push_back(l);
+            if (!merged(At, mf, M, sAm) || !merged(dAt, mf, t1, sDm) || !merged(Ft, mf, t2, sFm)) continue;
+        }
+        // k: G's order, split into at most two runs that chain in G and F
+        std::vector<int> kg;
+        for (int l : Gt.labels)
+            if (std::find(kl.begin(), kl.end(), l) != kl.end()) kg.push_back(l);
+        std::vector<std::vector<int>> runs;
+        for (int l : kg) {
+            if (!runs.empty()) {
+                std::vector<int> t = runs.back();
+                t.push_back(l);
+                int64_t a, b, c, e;
+                if (merged(Gt, t, a, b) && merged(Ft, t, c, e)) {
+                    runs.back() = t;
+                    continue;
+                }
+            }
+            runs.push_back({l});
+        }
+        if (runs.size() > 2) continue;
+        int64_t K1 = 1, sG1 = 0, sF1 = 0, K2, sG2, sF2, tk;
+        if (!merged(Gt, runs.back(), K2, sG2) || !merged(Ft, runs.back(), tk, sF2)) continue;
+        if (runs.size() == 2 && (!merged(Gt, runs[0], K1, sG1) || !merged(Ft, runs[0], tk, sF1))) continue;
+        const int64_t K = K1 * K2;
+        // g: merged runs in A, G and dA (at most two)
+        std::vector<BDim> bd;
+        for (int l : gl_) bd.push_back({At.dim_of(l), At.stride_of(l), Gt.stride_of(l), dAt.stride_of(l)});
+        bd = merge_dims(bd);
+        if (bd.size() > 2 || M > 32 || K > 512) continue;
+        int64_t G = 1;
+        for (const BDim& b : bd) G *= b.size;
+        int64_t fnumel = 1;
+        for (int64_t dm : Ft.dims) fnumel *= dm;
+        // F dense (the partials take its layout)
+        {
+            int64_t ext = 1;
+            for (size_t i = 0; i < Ft.dims.size(); i++) ext += (Ft.dims[i] - 1) * Ft.strides[i];
+            if (ext != fnumel) continue;
+        }
+        GpairDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.M = (int32_t)M;
+        d.K = (int32_t)K;
+        d.K1 = (int32_t)K1;
+        d.K2 = (int32_t)K2;
+        d.N = (int32_t)N;
+        d.ng = (int32_t)bd.size();
+        d.nkc = K <= 64 ? 1 : K <= 128 ? 2 : K <= 256 ? 4 : 8;
+        d.ntiles = (int32_t)cdiv(N, 64);
+        for (size_t i = 0; i < bd.size(); i++) {
+            d.g_size[i] = bd[i].size;
+            d.g_sA[i] = bd[i].s0;
+            d.g_sG[i] = bd[i].s1;
+            d.g_sD[i] = bd[i].s2;
+        }
+        d.sAm = sAm;
+        d.sDm = sDm;
+        d.sFm = sFm;
+        d.sG1 = sG1;
+        d.sG2 = sG2;
+        d.sF1 = sF1;
+        d.sF2 = sF2;
+        d.G = G;
+        d.gper = cdiv(G, 1024);
+        d.blocks = cdiv(G, d.gper);
+        d.fnumel = fnumel;
+        d.lds_bytes = (uint32_t)(4 * (d.nkc * 64 * 33 + 2 * 64 * 65 + 2 * 32 * 65));
+        if (N >= ((int64_t)1 << 31) || fnumel >= ((int64_t)1 << 31) || d.blocks * fnumel > ((int64_t)1 << 28))
+            continue;
+        const BufRef part = scratch.alloc((size_t)(d.blocks * fnumel * 4));
+        Launch ln;
+        ln.kind = K_GPAIR | dt_bits(DT_F32, DT_F32, DT_F32);
+        ln.a = At.buf;
+        ln.b = Ft.buf;
+        ln.c = Gt.buf;
+        ln.d = part;
+        ln.extra = {dAt.buf};
+        ln.grid[0] = (uint32_t)d.blocks;
+        ln.block[0] = 512;
+        ln.lds = d.lds_bytes;
+        set_desc(ln, d);
+        ln.kname = "gpair<" + std::to_string(d.nkc) + ">";
+        out.push_back(ln);
+        ReduceDesc rd;
+        rd.M = 1;
+        rd.N = (int32_t)fnumel;
+        rd.nsplit = d.blocks;
+        rd.sCm = 0;
+        rd.sCn = 1;
+        Launch lr;
+        lr.kind = K_REDUCE | dt_bits(DT_F32, DT_F32, DT_F32);
+        lr.d = part;
+        lr.c = dFt.buf;
+        lr.grid[0] = (uint32_t)cdiv(fnumel, 64);
+        lr.block[0] = (uint32_t)(64 * reduce_waves(rd.nsplit));
+        set_desc(lr, rd);
+        lr.kname = "reduce_partials<" + std::to_string(reduce_waves(rd.nsplit)) + ", float>";
+        out.push_back(lr);
+        fside = side;
+        return true;
+    }
+    return false;
+}
+
 }  // namespace
+
+// Both gradient ops of one step in a single fused launch (plus its ordered
+// partial sum) when they match try_gpair_ops; empty otherwise.
+std::vector<Launch> lower_grad_pair(const PairOp& gl, const PairOp& gr, unsigned flags, ScratchAlloc& scratch) {
+    std::vector<Launch> out;
+    if ((flags & (CE_FLAG_GENERIC_ONLY | CE_FLAG_NO_FUSION)) || gl.generic_only || gr.generic_only) return out;
+    int fside = 0;
+    if (!try_gpair_ops(gl, gr, scratch, out, fside)) {
+        out.clear();
+        return out;
+    }
+    const double bytes = tensor_bytes(gl.L) + tensor_bytes(gl.R) + tensor_bytes(gr.L) + tensor_bytes(gl.C) +
+                         tensor_bytes(gr.C);
+    out[0].need = gl.need | gr.need;
+    out[0].what = gl.what + " + " + gr.what.substr(gr.what.find("grad"));
+    out[0].alg_bytes = bytes;
+    out[0].alg_flops = 4.0 * (double)gl.macs;
+    // the partial sum runs when the factor's gradient is wanted (side 0: the
+    // factor is the step's rhs, its gradient the grad rhs op's)
+    out[1].need = fside == 0 ? gr.need : gl.need;
+    out[1].what = out[0].what;
+    return out;
+}
 
 std::vector<Launch> lower_op(const ce_expr& e, const PairOp& op, unsigned flags,
                              ScratchAlloc& scratch) {

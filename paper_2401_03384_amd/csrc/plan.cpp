@@ -1017,32 +1017,34 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             const Step& st = p->steps[s];
             TensorRef dC = bgrad(st.c);
             bs.t = T(s);
-            {
-                PairOp op;
-                op.L = dC;
-                op.R = bval(st.b);
-                op.C = bgrad(st.a);
-                op.convs = bld.conv_maps(st, 1);
-                op.macs = st.macs;
-                op.need = p->nodes[st.a].mask;
-                op.what = "step " + std::to_string(s) + " grad lhs " + tensor_str(E, op.L) + "," +
-                          tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                for (const PairOp& q : bld.phase_split(st, 1, op))
-                    for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
+            PairOp gl, gr;
+            gl.L = dC;
+            gl.R = bval(st.b);
+            gl.C = bgrad(st.a);
+            gl.convs = bld.conv_maps(st, 1);
+            gl.macs = st.macs;
+            gl.need = p->nodes[st.a].mask;
+            gl.what = "step " + std::to_string(s) + " grad lhs " + tensor_str(E, gl.L) + "," +
+                      tensor_str(E, gl.R) + "->" + tensor_str(E, gl.C);
+            gr.L = bval(st.a);
+            gr.R = dC;
+            gr.C = bgrad(st.b);
+            gr.convs = bld.conv_maps(st, 2);
+            gr.macs = st.macs;
+            gr.need = p->nodes[st.b].mask;
+            gr.what = "step " + std::to_string(s) + " grad rhs " + tensor_str(E, gr.L) + "," +
+                      tensor_str(E, gr.R) + "->" + tensor_str(E, gr.C);
+            // a channel-mixing step: both gradients from one read of dC
+            std::vector<Launch> pair;
+            if (gl.convs.empty() && gr.convs.empty()) pair = lower_grad_pair(gl, gr, flags, bs);
+            if (!pair.empty()) {
+                for (auto& l : pair) p->bwd.push_back(l);
+                continue;
             }
-            {
-                PairOp op;
-                op.L = bval(st.a);
-                op.R = dC;
-                op.C = bgrad(st.b);
-                op.convs = bld.conv_maps(st, 2);
-                op.macs = st.macs;
-                op.need = p->nodes[st.b].mask;
-                op.what = "step " + std::to_string(s) + " grad rhs " + tensor_str(E, op.L) + "," +
-                          tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
-                for (const PairOp& q : bld.phase_split(st, 2, op))
-                    for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
-            }
+            for (const PairOp& q : bld.phase_split(st, 1, gl))
+                for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
+            for (const PairOp& q : bld.phase_split(st, 2, gr))
+                for (auto& l : lower_op(E, q, flags, bs)) p->bwd.push_back(l);
         }
         drop_unused(bitems, p->bwd);
         p->ws_bwd = pack(bitems);

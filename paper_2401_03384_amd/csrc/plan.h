@@ -135,6 +135,10 @@ struct ScratchAlloc {
     virtual ~ScratchAlloc() = default;
 };
 
+// Both gradients of one step (gl: grad lhs, gr: grad rhs) as one fused
+// launch and its partial sum, or nothing when they do not match.
+std::vector<Launch> lower_grad_pair(const PairOp& gl, const PairOp& gr, unsigned flags, ScratchAlloc& scratch);
+
 // The generic strided kernel for any pairwise op.
 Launch lower_generic(const PairOp& op);
 

@@ -1511,6 +1511,75 @@ bool run_wgconv(const Launch& ln, Ctx& c) {
     return true;
 }
 
+// K_GPAIR (both gradients of a channel-mixing step): the launcher's
+// descriptor checks, the range of every index the kernel's loads and stores
+// reach (block by block, with its own offset arithmetic), then dA and the
+// per-block partials of dF in double.
+bool run_gpair(const Launch& ln, Ctx& c) {
+    GpairDesc d = desc_of<GpairDesc>(ln);
+    const int nkc = d.nkc;
+    const uint32_t lds = (uint32_t)(4 * (nkc * 64 * 33 + 2 * 64 * 65 + 2 * 32 * 65));
+    REQ(((ln.kind >> kBitIn) & 1) == 0 && d.M >= 1 && d.M <= 32 && d.K >= 1 && d.K2 >= 1 && d.K1 * d.K2 == d.K &&
+            (nkc == 1 || nkc == 2 || nkc == 4 || nkc == 8) && d.K <= 64 * nkc && d.N >= 1 &&
+            d.ntiles == (d.N + 63) / 64 && d.gper >= 1 && d.blocks == (d.G + d.gper - 1) / d.gper &&
+            d.lds_bytes == lds && lds <= 160 * 1024 && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 512 &&
+            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2 && ln.extra.size() == 1,
+        "gpair layout");
+    bool ok = true, o1, o2, o3, o4, o5;
+    Buf A = resolve(ln.a, c, 0, o1), F = resolve(ln.b, c, 0, o2), G = resolve(ln.c, c, 0, o3),
+        Pb = resolve(ln.d, c, 0, o4), dA = resolve(ln.extra[0], c, 0, o5);
+    REQ(o1 && o2 && o3 && o4 && o5, "unresolved buffer");
+    const int64_t an = (int64_t)(A.bytes / 4), fn = (int64_t)(F.bytes / 4), gn = (int64_t)(G.bytes / 4),
+                  pn = (int64_t)(Pb.bytes / 4);
+    auto offs = [&](int64_t g, int64_t& oa, int64_t& og, int64_t& od) {
+        oa = og = od = 0;
+        for (int i = d.ng - 1; i >= 0; --i) {
+            const int64_t x = g % d.g_size[i];
+            g /= d.g_size[i];
+            oa += x * d.g_sA[i];
+            og += x * d.g_sG[i];
+            od += x * d.g_sD[i];
+        }
+    };
+    auto fidx = [&](int k, int m) { return (int64_t)(k / d.K2) * d.sF1 + (int64_t)(k % d.K2) * d.sF2 + (int64_t)m * d.sFm; };
+    // F reads and partial writes: every (k, m) in range, the partial layout dense
+    for (int k = 0; k < d.K; k++)
+        for (int m = 0; m < d.M; m++) {
+            const int64_t i = fidx(k, m);
+            REQ(i >= 0 && i < fn && i < d.fnumel, "gpair F / partial index");
+        }
+    REQ(d.blocks * d.fnumel <= pn, "gpair partial range");
+    std::vector<double> acc((size_t)d.fnumel);
+    for (int64_t blk = 0; blk < d.blocks; blk++) {
+        std::fill(acc.begin(), acc.end(), 0.0);
+        const int64_t g0 = blk * d.gper, g1 = std::min(d.G, g0 + d.gper);
+        for (int64_t g = g0; g < g1; g++) {
+            int64_t oa, og, od;
+            offs(g, oa, og, od);
+            // the rows the kernel loads: G rows k (all n), A rows m (all n)
+            for (int k = 0; k < d.K; k++) {
+                const int64_t r = og + (int64_t)(k / d.K2) * d.sG1 + (int64_t)(k % d.K2) * d.sG2;
+                REQ(r >= 0 && r + d.N <= gn, "gpair G range");
+            }
+            for (int m = 0; m < d.M; m++) REQ(oa + m * d.sAm >= 0 && oa + m * d.sAm + d.N <= an, "gpair A range");
+            for (int m = 0; m < d.M; m++)
+                for (int64_t n = 0; n < d.N; n++) {
+                    double sa = 0;
+                    for (int k = 0; k < d.K; k++) {
+                        const double gv = ld(G, 0, og + (int64_t)(k / d.K2) * d.sG1 + (int64_t)(k % d.K2) * d.sG2 + n, ok);
+                        sa += ld(F, 0, fidx(k, m), ok) * gv;
+                        acc[(size_t)fidx(k, m)] += ld(A, 0, oa + m * d.sAm + n, ok) * gv;
+                    }
+                    if (dA.base) st(dA, 0, od + m * d.sDm + n, (float)sa, ok);
+                }
+        }
+        for (int k = 0; k < d.K; k++)
+            for (int m = 0; m < d.M; m++) st(Pb, 0, blk * d.fnumel + fidx(k, m), (float)acc[(size_t)fidx(k, m)], ok);
+    }
+    REQ(ok, "out-of-bounds access (gpair)");
+    return true;
+}
+
 // Small-output contraction over a long reduction: per-block partials over
 // the block's outer rows (K_THINW), then the ordered chunk sum (K_THINW_REDUCE).
 bool run_thinw(const Launch& ln, Ctx& c) {
@@ -1689,6 +1758,7 @@ int emul_run(const char* spec, int n, const int* ranks, const int64_t* const* di
                     : (v == K_CRED || v == K_CREDW || v == K_CREDW_REDUCE) ? run_cred(ln, c)
                     : v == K_CCONV ? run_cconv(ln, c)
                     : v == K_WGCONV ? run_wgconv(ln, c)
+                    : v == K_GPAIR ? run_gpair(ln, c)
                     : v == K_TT_FWD || v == K_TT_PREP ? run_tt_fwd(ln, c)
                     : (v == K_THINW || v == K_THINW_REDUCE) ? run_thinw(ln, c)
                     : (c.err = "unknown launch kind", false);
