@@ -120,10 +120,29 @@ def _random_expr(rnd):
 
 @pytest.mark.parametrize("seed", range(40))
 def test_planner_matches_oracle_on_random_expressions(seed):
+    # 40 x 25 = 1000 random expressions of 2 to 6 operands
     rnd = random.Random(1000 + seed)
-    for _ in range(6):
+    for _ in range(25):
         spec, shapes, feat = _random_expr(rnd)
         _compare(spec, shapes, feature=feat)
+
+
+# The tensor-train layer with every core split into a chain of two-way and
+# three-way factors: eight operands, 135,135 binary trees (the planner's
+# stress case; the C4 sizes, TT ranks 16).
+SPLIT_TT = ("b(s1)(s2)(s3)hw,(s1)(a1),(a1)(s2)(a2),(a2)(s3)(a3),(a3)hw(a4),(a4)(t1)(a5),(a5)(t2)(a6),(a6)(t3)"
+            "->b(t1)(t2)(t3)hw|hw",
+            [(64, 4, 8, 8, 28, 28), (4, 16), (16, 8, 16), (16, 8, 16), (16, 3, 3, 16), (16, 4, 16),
+             (16, 8, 16), (16, 8)])
+
+
+def test_planner_eight_operand_split_chain():
+    spec, shapes = SPLIT_TT
+    e = O.bind(O.parse(spec), shapes)
+    best, cost, ties = O.optimal_tree(e, return_all=True)
+    assert len(ties) == 1 and cost == 526802944   # unique optimum
+    assert O.count_trees(8) == 135135
+    _compare(spec, shapes)
 
 
 def test_user_path_and_left_to_right():
