@@ -118,6 +118,25 @@ __global__ void __launch_bounds__(256) tt_fwd(TtDesc d, const float* __restrict_
 #pragma unroll
     for (int j = 0; j < MAXC; j++) acc[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
     const int npx = 6 * d.W, ntile = (npx + 15) >> 4;
+    // phase-1 B operands (X) of this wave's tiles ti = wave + 4 j of step u:
+    // those of step u + 1 load while step u's phase 2 runs
+    constexpr int MAXT1 = (6 * XT + 3) / 4;
+    float bv[MAXT1][NS1];
+    auto load_x = [&](int u) {
+#pragma unroll
+        for (int j = 0; j < MAXT1; j++) {
+            const int ti = wave + 4 * j;
+            const int e = (ti << 4) + c16;
+            const int rr = e / d.W, cc = e - rr * d.W;
+            const int y = y0 - 1 + rr;
+            const bool ok = ti < ntile && e < npx && y >= 0 && y < d.H;
+            const int64_t o = b * d.x_sb + (int64_t)q * d.x_sk + (int64_t)u * d.x_su + (int64_t)y * d.W + cc;
+            const int voff = ok ? (int)(4 * o) : kOut;
+#pragma unroll
+            for (int s = 0; s < NS1; s++) bv[j][s] = ldf(rX, voff, (int)(16 * s * d.x_sk));
+        }
+    };
+    load_x(0);
     __syncthreads();
 
     for (int u = 0; u < d.U; u++) {
@@ -134,25 +153,30 @@ __global__ void __launch_bounds__(256) tt_fwd(TtDesc d, const float* __restrict_
                 a2[4 * s4 + 3] = v.w;
             }
         }
-        // phase 1: Z of this u on rows y0 - 1 .. y0 + 4 into LDS
-        for (int ti = wave; ti < ntile; ti += 4) {
+        // phase 1: Z of this u on rows y0 - 1 .. y0 + 4 into LDS (operands
+        // loaded during the previous step)
+        f32x4 z[MAXT1];
+#pragma unroll
+        for (int j = 0; j < MAXT1; j++) {
+            z[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+            if (wave + 4 * j < ntile) {
+#pragma unroll
+                for (int s = 0; s < NS1; s++)
+                    z[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[s], bv[j][s], z[j], 0, 0, 0);
+            }
+        }
+        // the next step's operands, in flight during this step's phase 2
+        if (u + 1 < d.U) load_x(u + 1);
+        mfma_drain();
+#pragma unroll
+        for (int j = 0; j < MAXT1; j++) {
+            const int ti = wave + 4 * j;
             const int e = (ti << 4) + c16;
-            const int rr = e / d.W, cc = e - rr * d.W;
-            const int y = y0 - 1 + rr;
-            const bool ok = e < npx && y >= 0 && y < d.H;
-            const int64_t o = b * d.x_sb + (int64_t)q * d.x_sk + (int64_t)u * d.x_su + (int64_t)y * d.W + cc;
-            const int voff = ok ? (int)(4 * o) : kOut;
-            float bv[NS1];
-#pragma unroll
-            for (int s = 0; s < NS1; s++) bv[s] = ldf(rX, voff, (int)(16 * s * d.x_sk));
-            f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < NS1; s++) z = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[s], bv[s], z, 0, 0, 0);
-            mfma_drain();
-            if (e < npx) {
+            if (ti < ntile && e < npx) {
+                const int rr = e / d.W, cc = e - rr * d.W;
                 float* dst = zc + (4 * q) * PL + rr * PW + cc + 1;
 #pragma unroll
-                for (int i = 0; i < 4; i++) dst[i * PL] = z[i];
+                for (int i = 0; i < 4; i++) dst[i * PL] = z[j][i];
             }
         }
         __syncthreads();
