@@ -248,6 +248,7 @@ struct CredDesc {
     // tiles of 16 a wavefront (rows a block: 64 * rt), channel planes a
     // block stages (mb)
     int32_t ncb, nct, rt, mb;
+    int64_t zext;   // K_WGCONV: elements of Z from its base (its buffer loads are range-checked)
 };
 
 // Convolution contracted over one channel index, on bf16 MFMA tiles:

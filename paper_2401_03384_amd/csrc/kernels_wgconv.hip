@@ -22,7 +22,8 @@
 // q0 + 4kq + t shifted by the tap, read from LDS, where the planes of the
 // current g sit with a zero halo (tap offsets are constant per lane).  The
 // planes of g + 1 load into registers while g's groups run (double-buffered
-// LDS); the row loads run kWgAhead groups ahead.
+// LDS); the row loads run kWgSlots groups ahead, each into the register
+// slot it is computed from.
 #include <algorithm>
 #include <atomic>
 #include <cstdint>
@@ -38,7 +39,7 @@ namespace {
 typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
 
 constexpr int kWgStage = 8;   // float4 of the next planes a thread holds while it computes
-constexpr int kWgAhead = 2;   // groups of row loads in flight ahead of the one computed
+constexpr int kWgSlots = 3;   // register slots of row loads (items loaded ahead of the one computed)
 
 __device__ __forceinline__ int64_t wg_zoff(const CredDesc& d, int64_t g) {
     int64_t oz = 0;
@@ -55,6 +56,27 @@ __device__ __forceinline__ int64_t wg_ooff(const CredDesc& d, int64_t g) {
         g /= d.g_size[i];
     }
     return oy;
+}
+
+// Raw buffer loads (a wave-uniform resource: base and byte range; per-lane
+// byte offsets): offsets past the range read zero, so a load needs no guard.
+constexpr int kWgOut = (int)0x80000000u;
+__device__ __forceinline__ float4 bld4(__amdgpu_buffer_rsrc_t r, int voff, float*) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 v = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 bld4(__amdgpu_buffer_rsrc_t r, int voff, bf16_t*) {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    const u2 u = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, 0, 0));
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+}
+__device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, int voff, float*) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, 0, 0));
+}
+__device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, int voff, bf16_t*) {
+    return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, 0, 0) << 16);
 }
 
 // four consecutive elements from p (fp32: one 16-byte load; bf16: one 8-byte load)
@@ -162,37 +184,43 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const T* __restrict
     }
     __syncthreads();
 
-    // row loads: items (g, group) in order, two ahead of the one computed
+    // row loads: items (g, group) in order, each loaded kWgSlots items before
+    // it is computed into a fixed register slot (the item loop is unrolled by
+    // kWgSlots, so no register moves wait on loads in flight).  The load
+    // cursor's batch offset changes once a g (a uniform branch).
     const int NG = (HW + 15) / 16;
+    auto zoff = [&](int64_t g) { return g < g1 ? wg_zoff(d, g) : (int64_t)0; };
     int64_t lg = g0;
-    int lq = 0;
-    int64_t loz = g0 < g1 ? wg_zoff(d, g0) : 0;
-    auto load_item = [&](float4 (&dst)[RT]) {
+    int lgrp = 0;
+    int64_t loz = zoff(g0);
+    // Z through a range-checked buffer (its extent < 2^31 bytes, checked by the
+    // lowering): rows past R, pixels past the plane and items past the chunk
+    // take an offset past the range and read zero, so no load is guarded
+    const __amdgpu_buffer_rsrc_t rZ =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(Z), (short)0, (int)(d.zext * (int64_t)sizeof(T)), 0x00020000);
+    auto next_load = [&](float4 (&dst)[RT]) {
+        const int q = 16 * lgrp + 4 * kq;
+        const bool ok = lg < g1;
 #pragma unroll
-        for (int mt = 0; mt < RT; mt++) dst[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (lg < g1) {
-            const int q = 16 * lq + 4 * kq;
+        for (int mt = 0; mt < RT; mt++) {
+            const int64_t e = loz + zr[mt] + q;
             if constexpr (VEC) {
-                if (q < HW) {
-#pragma unroll
-                    for (int mt = 0; mt < RT; mt++)
-                        if (rok[mt]) dst[mt] = ld4(Z + loz + zr[mt] + q);
-                }
+                const int voff = (ok && rok[mt] && q < HW) ? (int)(e * (int64_t)sizeof(T)) : kWgOut;
+                dst[mt] = bld4(rZ, voff, (T*)nullptr);
             } else {
+                float a[4];
 #pragma unroll
-                for (int mt = 0; mt < RT; mt++) {
-                    float a[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int t = 0; t < 4; t++)
-                        if (q + t < HW && rok[mt]) a[t] = load(Z, loz + zr[mt] + q + t);
-                    dst[mt] = make_float4(a[0], a[1], a[2], a[3]);
+                for (int t = 0; t < 4; t++) {
+                    const int voff = (ok && rok[mt] && q + t < HW) ? (int)((e + t) * (int64_t)sizeof(T)) : kWgOut;
+                    a[t] = bld1(rZ, voff, (T*)nullptr);
                 }
+                dst[mt] = make_float4(a[0], a[1], a[2], a[3]);
             }
         }
-        if (++lq == NG) {
-            lq = 0;
+        if (++lgrp == NG) {
+            lgrp = 0;
             ++lg;
-            if (lg < g1) loz = wg_zoff(d, lg);
+            loz = zoff(lg);
         }
     };
 
@@ -202,65 +230,75 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const T* __restrict
 #pragma unroll
         for (int j = 0; j < NT; j++) acc[mt][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    // ring of row loads: ra[0] is the group computed now, ra[1..kWgAhead-1]
-    // and rn the ones in flight
-    float4 ra[kWgAhead][RT], rn[RT];
+    float4 ra[kWgSlots][RT];
 #pragma unroll
-    for (int i = 0; i < kWgAhead; i++) load_item(ra[i]);
-    for (int64_t g = g0; g < g1; g++) {
-        const int cur = (int)((g - g0) & 1);
-        const bool more = g + 1 < g1;
-        float4 sv[kWgStage];
-        if (more && pref) stage_load(g + 1, sv);
-        const float* pb = pl + cur * BUF;
-        // (h, w) of this lane's first pixel of the group
-        int h0 = (4 * kq) / W, w0 = 4 * kq - ((4 * kq) / W) * W;
-        for (int grp = 0; grp < NG; grp++) {
-            load_item(rn);
-            const int q = 16 * grp + 4 * kq;
-            int bt[4];
-            {
-                int h = h0, w = w0;
+    for (int sl = 0; sl < kWgSlots; sl++) next_load(ra[sl]);
+    // (h, w) of this lane's first pixel of a group, and the step to the next group
+    const int h00 = (4 * kq) / W, w00 = 4 * kq - h00 * W, dh = 16 / W, dw = 16 - dh * W;
+    int h0 = h00, w0 = w00, grp = 0, cur = 0;
+    int64_t g = g0;
+    bool more = g0 + 1 < g1;
+    float4 sv[kWgStage];
+    if (more && pref) stage_load(g0 + 1, sv);
+    const int64_t total = (g1 - g0) * NG;
+    for (int64_t it = 0; it < total; it += kWgSlots) {
 #pragma unroll
-                for (int t = 0; t < 4; t++) {
-                    bt[t] = (q + t < HW) ? h * WP + w : 0;
-                    if (++w == W) {
-                        w = 0;
-                        ++h;
+        for (int sl = 0; sl < kWgSlots; sl++) {
+            if (it + sl < total) {
+                const float* pb = pl + cur * BUF;
+                const int q = 16 * grp + 4 * kq;
+                int bt[4];
+                {
+                    int h = h0, w = w0;
+#pragma unroll
+                    for (int t = 0; t < 4; t++) {
+                        bt[t] = (q + t < HW) ? h * WP + w : 0;
+                        if (++w == W) {
+                            w = 0;
+                            ++h;
+                        }
                     }
                 }
-            }
-            float bv[NT][4];
+                float bv[NT][4];
 #pragma unroll
-            for (int t = 0; t < 4; t++)
+                for (int t = 0; t < 4; t++)
 #pragma unroll
-                for (int j = 0; j < NT; j++) bv[j][t] = pb[bt[t] + toff[j]];
+                    for (int j = 0; j < NT; j++) bv[j][t] = pb[bt[t] + toff[j]];
 #pragma unroll
-            for (int t = 0; t < 4; t++)
+                for (int t = 0; t < 4; t++)
 #pragma unroll
-                for (int mt = 0; mt < RT; mt++) {
-                    const float a = t == 0 ? ra[0][mt].x : t == 1 ? ra[0][mt].y : t == 2 ? ra[0][mt].z : ra[0][mt].w;
+                    for (int mt = 0; mt < RT; mt++) {
+                        const float4 v = ra[sl][mt];
+                        const float a = t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
 #pragma unroll
-                    for (int j = 0; j < NT; j++)
-                        acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[j][t], acc[mt][j], 0, 0, 0);
+                        for (int j = 0; j < NT; j++)
+                            acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[j][t], acc[mt][j], 0, 0, 0);
+                    }
+                // the item kWgSlots ahead into this slot
+                next_load(ra[sl]);
+                w0 += dw;
+                h0 += dh;
+                if (w0 >= W) {
+                    w0 -= W;
+                    ++h0;
                 }
-#pragma unroll
-            for (int mt = 0; mt < RT; mt++) {
-#pragma unroll
-                for (int i = 0; i + 1 < kWgAhead; i++) ra[i][mt] = ra[i + 1][mt];
-                ra[kWgAhead - 1][mt] = rn[mt];
-            }
-            w0 += 16;
-            while (w0 >= W) {
-                w0 -= W;
-                ++h0;
+                if (++grp == NG) {
+                    // end of this g: the next g's planes into the other buffer
+                    if (more) {
+                        if (pref) stage_store(1 - cur, sv);
+                        else stage_direct(g + 1, 1 - cur);
+                    }
+                    __syncthreads();
+                    cur ^= 1;
+                    ++g;
+                    grp = 0;
+                    h0 = h00;
+                    w0 = w00;
+                    more = g + 1 < g1;
+                    if (more && pref) stage_load(g + 1, sv);
+                }
             }
         }
-        if (more) {
-            if (pref) stage_store(1 - cur, sv);
-            else stage_direct(g + 1, 1 - cur);
-        }
-        __syncthreads();
     }
 
     // accumulator r of a lane: row 4 kq + r of the tile, column i16
@@ -315,7 +353,8 @@ hipError_t launch_wgconv(const Launch& ln, const void* z, const void* o, void* p
         d.cw >= d.KW || d.nrb != (d.R + 64 * d.rt - 1) / (64 * d.rt) || d.gchunk < 1 ||
         d.nchunks != (d.G + d.gchunk - 1) / d.gchunk || d.blocks != (int64_t)d.nrb * d.ncb * d.nchunks ||
         d.lds_bytes != (uint32_t)(2 * d.mb * d.PH * d.PWp * 4) || d.lds_bytes > 160 * 1024 ||
-        (int64_t)d.H * d.W * d.M >= (1ll << 30) || ln.grid[0] != (uint32_t)d.blocks || ln.block[0] != 256)
+        (int64_t)d.H * d.W * d.M >= (1ll << 30) || ln.grid[0] != (uint32_t)d.blocks || ln.block[0] != 256 ||
+        d.zext < 1 || d.zext * (bf ? 2 : 4) >= (1ll << 31))
         return hipErrorInvalidValue;
     // every column block's planes fit the mb staged
     for (int cb = 0; cb < d.ncb; cb++) {

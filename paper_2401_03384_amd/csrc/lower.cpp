@@ -754,7 +754,11 @@ bool try_cred(const PairOp& op, ScratchAlloc& scratch, std::vector<Launch>& out)
         d.blocks = d.nrb * d.ncb * d.nchunks;
         d.threads = 256;
         const int64_t lds = 2 * (int64_t)d.mb * d.PH * d.PWp * 4;
-        if (lds <= 160 * 1024 && d.blocks <= 0x7fffffff && H * W * M < ((int64_t)1 << 30)) {
+        int64_t zext = 1;
+        for (size_t i = 0; i < Z.dims.size(); i++) zext += (Z.dims[i] - 1) * Z.strides[i];
+        d.zext = zext;
+        const bool zfits = zext * (bf ? 2 : 4) < ((int64_t)1 << 31);   // 32-bit buffer offsets
+        if (zfits && lds <= 160 * 1024 && d.blocks <= 0x7fffffff && H * W * M < ((int64_t)1 << 30)) {
             d.lds_bytes = (uint32_t)lds;
             const BufRef part = scratch.alloc((size_t)(d.nchunks * d.R * N * 4));
             Launch ln;

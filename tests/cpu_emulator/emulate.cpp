@@ -1430,6 +1430,7 @@ bool run_cred(const Launch& ln, Ctx& c) {
 // arithmetic; then the partial sums it defines, in double.
 bool run_wgconv(const Launch& ln, Ctx& c) {
     CredDesc d = desc_of<CredDesc>(ln);
+    bool o1_ = true;
     const int tIn = (ln.kind >> kBitIn) & 1;
     const int KK = d.KH * d.KW, N = d.M * KK;
     const bool nct_ok = tIn ? (d.nct == 6 || (d.nct == 3 && N <= 48)) : (d.nct >= 1 && d.nct <= 6);
@@ -1440,7 +1441,8 @@ bool run_wgconv(const Launch& ln, Ctx& c) {
             d.nchunks == (d.G + d.gchunk - 1) / d.gchunk && d.blocks == (int64_t)d.nrb * d.ncb * d.nchunks &&
             d.lds_bytes == (uint32_t)(2 * d.mb * d.PH * d.PWp * 4) && d.lds_bytes <= 160 * 1024 &&
             (int64_t)d.H * d.W * d.M < (1ll << 30) && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256 &&
-            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2,
+            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2 && d.zext >= 1 &&
+            d.zext * (tIn ? 2 : 4) < (1ll << 31) && (size_t)d.zext * (tIn ? 2 : 4) <= resolve(ln.a, c, 0, o1_).bytes,
         "wgconv layout");
     bool ok = true, o1, o2, o3;
     Buf Z = resolve(ln.a, c, 0, o1), O = resolve(ln.b, c, 0, o2), Pb = resolve(ln.d, c, 0, o3);
@@ -1481,7 +1483,8 @@ bool run_wgconv(const Launch& ln, Ctx& c) {
             for (int64_t r = 0; r < rows; r++) {
                 const int64_t u = ub * rows + r;
                 if (u >= d.R) continue;
-                REQ(oz + u * d.z_sr >= 0 && oz + u * d.z_sr + HW <= zn, "wgconv Z range");
+                REQ(oz + u * d.z_sr >= 0 && oz + u * d.z_sr + HW <= zn && oz + u * d.z_sr + HW <= d.zext,
+                    "wgconv Z range");
             }
         }
         for (int64_t r = 0; r < rows; r++) {
