@@ -268,10 +268,13 @@ struct CconvDesc {
     int32_t P, Q, Ppad, ng;            // contracted / output channels; P rounded up to 16; batch dims
     int32_t TH, ntiles, nq, HP;        // output rows a tile; tiles; q tiles of 32; LDS input rows
     int32_t WP, pw_img, pw_tab, tp;    // LDS input columns; word pitches of a pixel, of a q row, of a tap
-    int32_t pad0_, pad_;
+    // rega (fp32, P <= 8, at most 9 taps): a block covers every q tile of its
+    // rows, the filter operands stay in registers and LDS holds the input rows
+    int32_t rega, pad_;
     int64_t G, g_size[2], g_sZ[2], g_sY[2];
     int64_t z_numel, f_numel;          // elements of Z and F (byte ranges of the raw buffer loads, < 2^30)
     int64_t z_sp, y_sq, f_sp, f_sq, f_sh, f_sw;
+    int64_t y_ext;                     // rega: elements of Y one g spans (its stores are range-checked)
     int64_t blocks;
     uint32_t lds_bytes, pad2_;
 };

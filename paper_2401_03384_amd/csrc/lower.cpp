@@ -994,16 +994,26 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     if (bf && (d.pw_tab / 4) % 2 == 0) d.pw_tab += 4;
     if (!bf) d.pw_tab += 1;
     d.WP = (int32_t)(W + d.KW - 1);
-    // output rows a block: the whole plane when two blocks' LDS fit a CU
-    auto lds_of = [&](int64_t th) { return 4 * (32 * (int64_t)d.pw_tab + (th + d.KH - 1) * d.WP * d.pw_img); };
+    d.y_sq = Qd[0].s2;
+    // fp32 with at most eight channels and nine taps: the filter operands of a
+    // q tile fit a wavefront's registers, LDS holds the input rows only
+    const int64_t y_ext = (Q - 1) * d.y_sq + H * W;
+    d.rega = !bf && CB == 1 && d.KH * d.KW <= 9 && d.y_sq >= 1 && y_ext * 4 < ((int64_t)1 << 31);
+    // output rows a block: the whole plane when two blocks' LDS fit a CU (four
+    // for rega, whose LDS is the input rows only)
+    auto lds_of = [&](int64_t th) {
+        return 4 * ((d.rega ? 0 : 32 * (int64_t)d.pw_tab) + (th + d.KH - 1) * d.WP * d.pw_img);
+    };
+    const int64_t lds_cap = d.rega ? 40 * 1024 : 80 * 1024;
     int64_t TH = H;
-    while (TH > 1 && lds_of(TH) > 80 * 1024) TH = (TH + 1) / 2;
+    while (TH > 1 && lds_of(TH) > lds_cap) TH = (TH + 1) / 2;
     if (lds_of(TH) > 160 * 1024) return false;
     d.TH = (int32_t)TH;
     d.HP = (int32_t)(TH + d.KH - 1);
     d.ntiles = (int32_t)cdiv(H, TH);
     d.nq = (int32_t)cdiv(Q, 32);
     d.lds_bytes = (uint32_t)lds_of(TH);
+    d.y_ext = d.rega ? y_ext : 0;
     d.ng = (int32_t)U.size();
     d.G = 1;
     for (size_t i = 0; i < U.size(); i++) {
@@ -1015,13 +1025,12 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     d.z_sp = Pd[0].s1;
     d.f_sp = Pd[0].s2;
     d.f_sq = Qd[0].s1;
-    d.y_sq = Qd[0].s2;
     d.f_sh = O.stride_of(ch.label);
     d.f_sw = O.stride_of(cw.label);
     d.z_numel = Z.numel();
     d.f_numel = O.numel();
     if (d.z_numel >= (int64_t(1) << 30) || d.f_numel >= (int64_t(1) << 30)) return false;
-    d.blocks = d.G * d.ntiles * d.nq;
+    d.blocks = d.G * d.ntiles * (d.rega ? 1 : d.nq);
     if (d.blocks > 0x7fffffff) return false;
     Launch ln;
     ln.kind = K_CCONV | dt_bits(op.L.dtype, op.L.dtype, C.dtype);
@@ -1032,7 +1041,8 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     ln.block[0] = 256;
     ln.lds = d.lds_bytes;
     set_desc(ln, d);
-    ln.kname = "cconv<" + std::to_string(CB) + ", " + tname(op.L.dtype) + ", " + tname(C.dtype) + ">";
+    ln.kname = d.rega ? "cconv_r<" + std::to_string(d.KH * d.KW) + ">"
+                      : "cconv<" + std::to_string(CB) + ", " + tname(op.L.dtype) + ", " + tname(C.dtype) + ">";
     out.push_back(ln);
     return true;
 }

@@ -1195,14 +1195,26 @@ bool run_cconv(const Launch& ln, Ctx& c) {
     const int tIn = (ln.kind >> kBitIn) & 1, tC = (ln.kind >> kBitOut) & 1;
     const int CB = d.Ppad / (tIn ? 16 : 8);
     REQ(tIn == 1 || tC == 0, "fp32 inputs give fp32 outputs");
+    if (d.rega) {
+        // fp32, P <= 8, at most nine taps, input rows alone in LDS, every q
+        // tile in one block; its stores span y_ext elements from the g's base
+        REQ(!tIn && d.Ppad == 8 && d.P >= 1 && d.P <= 8 && d.pw_img == 9 && d.KH * d.KW <= 9 && d.TH >= 1 &&
+                d.HP == d.TH + d.KH - 1 && d.WP == d.W + d.KW - 1 && d.nq >= 1 && d.nq * 32 >= d.Q &&
+                (int64_t)d.ntiles * d.TH >= d.H && d.y_sq >= 1 &&
+                d.y_ext == (int64_t)(d.Q - 1) * d.y_sq + (int64_t)d.H * d.W && d.y_ext * 4 < (1ll << 31) &&
+                d.lds_bytes == 4u * (uint32_t)(d.HP * d.WP * d.pw_img) && d.lds_bytes <= 160 * 1024 &&
+                (int64_t)ln.grid[0] == d.G * d.ntiles && d.blocks == (int64_t)ln.grid[0] && ln.block[0] == 256 &&
+                ln.lds == d.lds_bytes,
+            "cconv_r layout");
+    }
     const bool lay = tIn ? (d.Ppad == 16 * CB && d.pw_img == 8 * CB + 4 && d.tp == 8 * CB + 4 && (d.pw_tab & 3) == 0)
                          : (d.Ppad == 8 * CB && d.pw_img == 8 * CB + 1 && d.tp == 8 * CB && (d.pw_tab & 1) == 1);
-    REQ((CB == 1 || CB == 2 || CB == 4 || CB == 8) && lay && d.TH >= 1 && d.HP == d.TH + d.KH - 1 &&
+    REQ(d.rega || ((CB == 1 || CB == 2 || CB == 4 || CB == 8) && lay && d.TH >= 1 && d.HP == d.TH + d.KH - 1 &&
             d.WP == d.W + d.KW - 1 && d.pw_tab >= d.KH * d.KW * d.tp &&
             d.P <= d.Ppad && d.nq * 32 >= d.Q && (int64_t)d.ntiles * d.TH >= d.H &&
             d.lds_bytes == 4u * (uint32_t)(32 * d.pw_tab + d.HP * d.WP * d.pw_img) && d.lds_bytes <= 160 * 1024 &&
             (int64_t)ln.grid[0] == d.G * d.ntiles * d.nq && d.blocks == (int64_t)ln.grid[0] && ln.block[0] == 256 &&
-            ln.lds == d.lds_bytes,
+            ln.lds == d.lds_bytes),
         "cconv layout");
     REQ((d.zhs == 1 || d.zhs == -1) && (d.zws == 1 || d.zws == -1) && (d.fhs == 1 || d.fhs == -1) &&
             (d.fws == 1 || d.fws == -1) && d.ng >= 0 && d.ng <= 2 && d.z_numel > 0 && d.z_numel < (1ll << 30) &&
@@ -1234,7 +1246,9 @@ bool run_cconv(const Launch& ln, Ctx& c) {
                                 acc += (double)ld(Z, tIn, oz + p * d.z_sp + (int64_t)hh * d.W + ww, ok) *
                                        ld(F, tIn, fo + p * d.f_sp, ok);
                         }
-                    st(Y, tC, oy + q * d.y_sq + (int64_t)h * d.W + w, (float)acc, ok);
+                    const int64_t yo = q * d.y_sq + (int64_t)h * d.W + w;
+                    if (d.rega) REQ(yo >= 0 && yo < d.y_ext, "cconv_r store range");
+                    st(Y, tC, oy + yo, (float)acc, ok);
                 }
         REQ(ok, "out-of-bounds access (cconv)");
     }

@@ -102,6 +102,11 @@ CASES = {
     "C4x2": W.PARITY_WORKLOADS["C4x2"],
     "C4x4": W.PARITY_WORKLOADS["C4x4"],
     "C4x1": W.PARITY_WORKLOADS["C4x1"],
+    # transposed convolution with register-held filter operands: a partial q
+    # tile with 7 channels, a 2 x 2 filter, two row tiles
+    "C4q": W.PARITY_WORKLOADS["C4q"],
+    "C4k2": W.PARITY_WORKLOADS["C4k2"],
+    "C4p": W.PARITY_WORKLOADS["C4p"],
     "C5cs": W.PARITY_WORKLOADS["C5cs"],
     # fused reshaped-CP kernels: both instantiations (rank 4 keeps the CPU
     # run short), one and several row tiles

@@ -150,6 +150,12 @@ PARITY_WORKLOADS = {
     "C4x2": rtt_layer("C4x2", 2, (4, 8, 4), (4, 4, 4), 21, 30, 16, 3, "f32", 36),
     "C4x4": rtt_layer("C4x4", 2, (3, 8, 4), (4, 4, 6), 9, 40, 16, 3, "f32", 37),
     "C4x1": rtt_layer("C4x1", 3, (4, 8, 4), (4, 8, 5), 6, 16, 16, 3, "f32", 38),
+    # the transposed convolution with its filter operands in registers: a
+    # partial q tile (48 columns) and 7 channels on a ragged plane, a 2 x 2
+    # filter, a 40 x 36 plane in two row tiles
+    "C4q": rtt_layer("C4q", 2, (4, 8, 3), (4, 8, 7), 9, 11, 16, 3, "f32", 43),
+    "C4k2": rtt_layer("C4k2", 2, (4, 8, 3), (4, 8, 7), 9, 11, 16, 2, "f32", 44),
+    "C4p": rtt_layer("C4p", 1, (4, 8, 3), (4, 8, 7), 40, 36, 16, 3, "f32", 45),
     # enough reduction per rank for the streaming factor-gradient kernel
     # (ragged 15 x 15 planes, and 16 x 16 with four-wide loads)
     "C5cs": rcp_layer("C5cs", 20, (2, 2, 4), (2, 2, 4), 15, 15, 8, 3, "bf16", 19),
