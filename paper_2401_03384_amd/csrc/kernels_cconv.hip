@@ -114,7 +114,7 @@ __global__ void __launch_bounds__(256) cconv(CconvDesc d, const T* __restrict__ 
         else chans(rZ, voff, d.z_sp, img + px * d.pw_img);
     }
     __syncthreads();
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hf = lane >> 5, cl = lane & 31;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), hf = lane >> 5, cl = lane & 31;
     const int npx = th * d.W, ptiles = (npx + 31) / 32;
     const uint32_t* arow = tab + cl * d.pw_tab + (BF ? 4 * hf : hf);
     for (int pt = 2 * wave; pt < ptiles; pt += 8) {

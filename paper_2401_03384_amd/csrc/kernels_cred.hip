@@ -249,7 +249,7 @@ template <typename TC>
 __global__ void __launch_bounds__(256) credw_reduce(CredDesc d, const float* __restrict__ P, TC* __restrict__ C) {
     __shared__ double q4[4][64];
     const int KK = d.KH * d.KW;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t per_chunk = d.R * d.M * KK;
     const int64_t t = (int64_t)blockIdx.x * 64 + lane;
     const int64_t quarter = (d.nchunks + 3) / 4;

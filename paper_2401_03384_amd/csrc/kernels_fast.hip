@@ -71,7 +71,7 @@ __global__ void __launch_bounds__(256) gemm_f32(GemmDesc d, const float* __restr
     int64_t oA, oB, oC;
     gemm_offsets(d, bid, oA, oB, oC);
     const int m0 = mt * TM, n0 = nt * TN;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     f32x16 acc[MT];
 #pragma unroll
     for (int i = 0; i < MT; i++)
@@ -138,7 +138,7 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmDesc d, const bf16_t* __res
     int64_t oA, oB, oC;
     gemm_offsets(d, bid, oA, oB, oC);
     const int m0 = mt * TM, n0 = nt * TN;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     f32x16 acc[MT];
 #pragma unroll
     for (int i = 0; i < MT; i++)
@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(256) gemm_bf16f(GemmDesc d, const bf16_t* __re
     bf16_t(*Bs)[LDK] = reinterpret_cast<bf16_t(*)[LDK]>(lds_g + TM * LDK);   // transposed: [n][k]
     const int nt = (int)(blockIdx.x % d.ntiles), mt = (int)(blockIdx.x / d.ntiles);
     const int m0 = mt * TM;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int64_t G = 1;
     for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
     const int64_t NF = G * d.N;
@@ -424,7 +424,7 @@ __global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ 
     const int64_t kbeg = (int64_t)kc * d.kchunk;
     const int64_t kend = min(d.K, kbeg + d.kchunk);
     const int m0 = mt * TM, n0 = nt * TN;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     f32x16 acc;
 #pragma unroll
@@ -512,7 +512,7 @@ __global__ void __launch_bounds__(256) wgrad(WgradDesc d, const T* __restrict__ 
 template <int NW, typename TC>
 __device__ __forceinline__ void reduce_block(const ReduceDesc& d, const float* __restrict__ part,
                                              TC* __restrict__ C, int64_t blk, double (*q)[64]) {
-    const int lane = threadIdx.x & 63, wave = NW == 1 ? 0 : threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = NW == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t mn = (int64_t)d.M * d.N;
     const int64_t e = blk * 64 + lane;
     const int64_t per = (d.nsplit + NW - 1) / NW;
@@ -613,7 +613,7 @@ __global__ void __launch_bounds__(256) dw_tapgrad(DwDesc d, const T* __restrict_
     const int slabsz = d.A * d.inner;
     const int total = nsl * slabsz;
     const int64_t base = slab0 * slabsz;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     for (int e = tid; e < total; e += 256) buf[e] = load(in, base + e);
     __syncthreads();
     float acc[KT];
@@ -645,7 +645,7 @@ __global__ void __launch_bounds__(256) dw_tapreduce(DwDesc d, const float* __res
                                                     TC* __restrict__ out) {
     __shared__ double red[4][KT];
     const int64_t r = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t run = d.r_div / d.spb;              // consecutive blocks of one row
     const int64_t period = run * d.r_size;
     const int64_t cnt = (d.nblocks / period) * run;   // partials of row r

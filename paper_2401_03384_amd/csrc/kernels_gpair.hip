@@ -57,7 +57,7 @@ __global__ void __launch_bounds__(512, 1) gpair(GpairDesc d, const float* __rest
     float* Fs = reinterpret_cast<float*>(lds4);               // [NKC * 64][kGpLF]
     float* Gs = Fs + NKC * 64 * kGpLF;                        // [2][64][kGpLG]
     float* As = Gs + 2 * 64 * kGpLG;                          // [2][32][kGpLG]
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int mt = wave >> 2, q = wave & 3, i16 = lane & 15, kq = lane >> 4;
     const int M = d.M, K = d.K, N = d.N;
     const int64_t g0 = (int64_t)blockIdx.x * d.gper, g1 = min(d.G, g0 + d.gper);

@@ -173,7 +173,7 @@ __global__ void __launch_bounds__(C::NT, C::MW) rcp_bwd(RcpBwdDesc d, const uint
                                                 const uint32_t* __restrict__ TB) {
     extern __shared__ uint32_t lds_words[];
     DevMem m{lds_words};
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int64_t blk;
     int b, t1, tile, chunk, h0, h1;
     rcpb::block_coords_b(d, blockIdx.x, blk, b, t1, tile, chunk);

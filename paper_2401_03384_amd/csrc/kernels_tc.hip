@@ -76,7 +76,7 @@ __global__ void __launch_bounds__(256) tc_gemm(TcDesc d, const T* __restrict__ A
     __shared__ IT mAt[KM ? TM : 1], nBt[KM ? TN : 1];
     __shared__ IT npa[KM ? 2 : 1][KM ? TN : 1];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, cl = lane & 31, hf = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), cl = lane & 31, hf = lane >> 5;
     int64_t bid = blockIdx.x;
     const int nt = (int)(bid % d.ntiles);
     bid /= d.ntiles;
@@ -468,7 +468,7 @@ __global__ void __launch_bounds__(256) tc_reduce_few(TcDesc d, const float* __re
 template <int NW, typename TC>
 __global__ void __launch_bounds__(64 * NW) tc_reduce(TcDesc d, const float* __restrict__ P, TC* __restrict__ C) {
     __shared__ double q[NW][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t MN = d.M * d.N, per_g = (MN + 63) / 64;
     const int64_t g = blockIdx.x / per_g, mn = (blockIdx.x - g * per_g) * 64 + lane;
     const int64_t run = (d.ksplit + NW - 1) / NW;

@@ -158,7 +158,7 @@ __global__ void __launch_bounds__(256) thinw(ThinwDesc d, const T* __restrict__ 
         }
     }
     // wave sums, then the four waves in order
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
     for (int m = 0; m < MM; m++)
 #pragma unroll

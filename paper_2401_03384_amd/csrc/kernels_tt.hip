@@ -86,7 +86,7 @@ __global__ void __launch_bounds__(256) tt_fwd(TtDesc d, const float* __restrict_
     constexpr int NS2 = 4 * 3 * 4;              // (tap row 0..3, tap column 0..2, r / 4)
     constexpr int MAXC = (2 * XT + 3) / 4;      // output tiles of a wave
     extern __shared__ __attribute__((aligned(16))) float zc[];   // [16][PL]
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, q = lane >> 4, c16 = lane & 15;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), q = lane >> 4, c16 = lane & 15;
     int64_t bid = blockIdx.x;
     if (d.xcd_remap) {
         // consecutive block ids go to different XCDs: give each XCD a

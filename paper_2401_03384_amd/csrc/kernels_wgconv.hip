@@ -92,7 +92,7 @@ __global__ void __launch_bounds__(256, 2) wgconv(CredDesc d, const T* __restrict
                                                  float* __restrict__ P) {
     extern __shared__ float4 lds4[];
     float* pl = reinterpret_cast<float*>(lds4);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int W = d.W, HW = d.H * d.W, WP = d.PWp, PLN = d.PH * d.PWp;
     const int KK = d.KH * d.KW, N = d.M * KK, BUF = d.mb * PLN;
     const int top = d.KH - 1 - d.ch, left = d.KW - 1 - d.cw;   // halo before the interior
