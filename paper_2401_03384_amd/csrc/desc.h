@@ -123,6 +123,7 @@ struct GpairDesc {
     int64_t g_size[2], g_sA[2], g_sG[2], g_sD[2];
     int64_t sAm, sDm, sFm, sG1, sG2, sF1, sF2;
     int64_t fnumel;            // elements of F (dense): one partial's size
+    int64_t gext, aext;        // elements one g's rows of G and of A span (buffer-load ranges, < 2^29)
     uint32_t lds_bytes, pad_;
 };
 

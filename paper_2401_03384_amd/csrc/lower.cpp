@@ -1378,8 +1378,11 @@ bool try_gpair_ops(const PairOp& gl, const PairOp& gr, ScratchAlloc& scratch, st
         d.gper = cdiv(G, 1024);
         d.blocks = cdiv(G, d.gper);
         d.fnumel = fnumel;
-        d.lds_bytes = (uint32_t)(4 * (d.nkc * 64 * 33 + 2 * 64 * 65 + 2 * 32 * 65));
-        if (N >= ((int64_t)1 << 31) || fnumel >= ((int64_t)1 << 31) || d.blocks * fnumel > ((int64_t)1 << 28))
+        d.lds_bytes = (uint32_t)(4 * (32 * (64 * d.nkc + 4) + 2 * 64 * 96 + 2 * 32 * 68));
+        d.gext = (K1 - 1) * sG1 + (K2 - 1) * sG2 + N;
+        d.aext = (M - 1) * sAm + N;
+        if (N >= ((int64_t)1 << 31) || fnumel >= ((int64_t)1 << 31) || d.blocks * fnumel > ((int64_t)1 << 28) ||
+            d.gext * 4 >= ((int64_t)1 << 31) || d.aext * 4 >= ((int64_t)1 << 31) || sG1 < 0 || sG2 < 0 || sAm < 0)
             continue;
         const BufRef part = scratch.alloc((size_t)(d.blocks * fnumel * 4));
         Launch ln;
@@ -1390,7 +1393,7 @@ bool try_gpair_ops(const PairOp& gl, const PairOp& gr, ScratchAlloc& scratch, st
         ln.d = part;
         ln.extra = {dAt.buf};
         ln.grid[0] = (uint32_t)d.blocks;
-        ln.block[0] = 512;
+        ln.block[0] = 1024;
         ln.lds = d.lds_bytes;
         set_desc(ln, d);
         ln.kname = "gpair<" + std::to_string(d.nkc) + ">";

@@ -1535,12 +1535,14 @@ bool run_wgconv(const Launch& ln, Ctx& c) {
 bool run_gpair(const Launch& ln, Ctx& c) {
     GpairDesc d = desc_of<GpairDesc>(ln);
     const int nkc = d.nkc;
-    const uint32_t lds = (uint32_t)(4 * (nkc * 64 * 33 + 2 * 64 * 65 + 2 * 32 * 65));
+    const uint32_t lds = (uint32_t)(4 * (32 * (64 * nkc + 4) + 2 * 64 * 96 + 2 * 32 * 68));
     REQ(((ln.kind >> kBitIn) & 1) == 0 && d.M >= 1 && d.M <= 32 && d.K >= 1 && d.K2 >= 1 && d.K1 * d.K2 == d.K &&
             (nkc == 1 || nkc == 2 || nkc == 4 || nkc == 8) && d.K <= 64 * nkc && d.N >= 1 &&
             d.ntiles == (d.N + 63) / 64 && d.gper >= 1 && d.blocks == (d.G + d.gper - 1) / d.gper &&
-            d.lds_bytes == lds && lds <= 160 * 1024 && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 512 &&
-            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2 && ln.extra.size() == 1,
+            d.lds_bytes == lds && lds <= 160 * 1024 && (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 1024 &&
+            ln.lds == d.lds_bytes && d.ng >= 0 && d.ng <= 2 && ln.extra.size() == 1 && d.sG1 >= 0 && d.sG2 >= 0 &&
+            d.sAm >= 0 && d.gext == (int64_t)(d.K1 - 1) * d.sG1 + (int64_t)(d.K2 - 1) * d.sG2 + d.N &&
+            d.gext * 4 < (1ll << 31) && d.aext == (int64_t)(d.M - 1) * d.sAm + d.N && d.aext * 4 < (1ll << 31),
         "gpair layout");
     bool ok = true, o1, o2, o3, o4, o5;
     Buf A = resolve(ln.a, c, 0, o1), F = resolve(ln.b, c, 0, o2), G = resolve(ln.c, c, 0, o3),
@@ -1576,9 +1578,12 @@ bool run_gpair(const Launch& ln, Ctx& c) {
             // the rows the kernel loads: G rows k (all n), A rows m (all n)
             for (int k = 0; k < d.K; k++) {
                 const int64_t r = og + (int64_t)(k / d.K2) * d.sG1 + (int64_t)(k % d.K2) * d.sG2;
-                REQ(r >= 0 && r + d.N <= gn, "gpair G range");
+                REQ(r >= 0 && r + d.N <= gn && r - og + d.N <= d.gext, "gpair G range");
             }
-            for (int m = 0; m < d.M; m++) REQ(oa + m * d.sAm >= 0 && oa + m * d.sAm + d.N <= an, "gpair A range");
+            // the buffer ranges (one g's slice from its base) lie inside the tensors
+            REQ(og >= 0 && og + d.gext <= gn && oa >= 0 && oa + d.aext <= an, "gpair G / A slice");
+            for (int m = 0; m < d.M; m++)
+                REQ(oa + m * d.sAm >= 0 && oa + m * d.sAm + d.N <= an && m * d.sAm + d.N <= d.aext, "gpair A range");
             for (int m = 0; m < d.M; m++)
                 for (int64_t n = 0; n < d.N; n++) {
                     double sa = 0;
