@@ -68,11 +68,14 @@ constexpr int kNumRcpCfgs = 2;
 // Backward instantiations (same fields; UA, UB, UC bound the units (pixel,
 // s3), (pixel, t2) and (plane, row, 4 columns) of one tile per thread).
 constexpr RcpCfgInfo kRcpBwdCfgs[] = {
-    // 8x8x8 modes, 3x3 (tiles up to 64 pixels); one workgroup per CU
+    // 8x8x8 modes, 3x3 (tiles up to 64 pixels); one workgroup per CU (C5a: whole 7x7
+    // planes, 449 us; 4-row tiles 689 us, 2-row 1242 us, a t2 chunk of 4 750 us)
     {8, 8, 8, 8, 8, 3, 8, 512, 1, 1, 2, 2},
-    // 4x4x8 modes, 5x5 (tiles up to 112 pixels); registers capped at 128 so that two
-    // workgroups share a CU (their barrier waits overlap; measured 7% faster despite spills)
-    {4, 4, 8, 4, 8, 5, 2, 448, 2, 1, 1, 4},
+    // 4x4x8 modes, 5x5 (tiles up to 64 pixels); 256 threads with registers capped at 128,
+    // so that four workgroups share a CU and their barrier waits overlap (C5b: 2-row tiles,
+    // 3584 workgroups, 1.96 ms; 448 threads and 4-row tiles 2.38 ms; 448 threads without
+    // the cap 2.60 ms; a t2 chunk of 4 3.1-3.4 ms; 1-row tiles 2.9 ms)
+    {4, 4, 8, 4, 8, 5, 2, 256, 2, 1, 1, 4},
 };
 constexpr int kNumRcpBwdCfgs = 2;
 
