@@ -60,8 +60,11 @@ struct RcpCfgInfo {
     int MW;   // backward: waves per SIMD the register budget is set for (launch bound)
 };
 constexpr RcpCfgInfo kRcpCfgs[] = {
-    {8, 8, 8, 8, 8, 3, 8, 256, 1, 2, 4, 0},    // 8x8x8 modes, 3x3 (tiles up to 9 x 7 with halo)
-    {4, 4, 8, 4, 8, 5, 2, 448, 4, 2, 4, 0},    // 4x4x8 modes, 5x5 (tiles up to 16 x 28 with halo)
+    // 8x8x8 modes, 3x3 (tiles up to 9 x 7 with halo); a t2 chunk of 4 (C5a 97 us; 8: 109, 2: 137)
+    {8, 8, 8, 8, 8, 3, 4, 256, 1, 2, 4, 0},
+    // 4x4x8 modes, 5x5 (tiles up to 18 x 28 with halo); 512 threads (C5b 307 us; 448: 328;
+    // 256 threads with twice the units a thread: 443; a t2 chunk of 1: 475)
+    {4, 4, 8, 4, 8, 5, 2, 512, 4, 2, 4, 0},
 };
 constexpr int kNumRcpCfgs = 2;
 
