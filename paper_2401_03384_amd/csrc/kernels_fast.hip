@@ -211,9 +211,9 @@ __global__ void __launch_bounds__(256) gemm_bf16(GemmDesc d, const bf16_t* __res
 // 32-column MFMA tile.  K goes in chunks of TK (64, or 256 when K <= 256, so
 // that a block makes one memory round trip); the next chunk's elements load
 // into registers while the current chunk's MFMAs run (one LDS copy, two
-// barriers a chunk).  Thread mapping: B, four consecutive columns (one 8-byte
-// row piece) x k rows 4(tid / 32) + 32 h + {0..3}; A, TM x TK / 256
-// consecutive k of one row.
+// barriers a chunk).  Thread mapping: B, four consecutive columns 4(tid / 8)
+// (one 8-byte row piece) x k rows 4(tid % 8) + 32 h + {0..3}, transposed into
+// LDS rows [n][k] by byte permutes; A, TM x TK / 256 consecutive k of one row.
 template <typename TC, int MT, int TK>
 __global__ void __launch_bounds__(256) gemm_bf16f(GemmDesc d, const bf16_t* __restrict__ A,
                                                   const bf16_t* __restrict__ B, TC* __restrict__ C) {
@@ -228,8 +228,10 @@ __global__ void __launch_bounds__(256) gemm_bf16f(GemmDesc d, const bf16_t* __re
     int64_t G = 1;
     for (int i = 0; i < d.ng; i++) G *= d.g_size[i];
     const int64_t NF = G * d.N;
-    // this thread's four B columns (one g, since N % 4 == 0)
-    const int nq = tid & 31, kq = 4 * (tid >> 5);
+    // this thread's four B columns (one g, since N % 4 == 0) and k rows: eight
+    // consecutive lanes take eight k groups of one column quad, so that the
+    // transposed 8-byte LDS writes of sixteen lanes cover 32 distinct words
+    const int nq = tid >> 3, kq = 4 * (tid & 7);
     const int64_t fb = (int64_t)nt * TN + 4 * nq;
     const bool colok = fb < NF;
     int64_t ob = 0;
@@ -336,15 +338,14 @@ __global__ void __launch_bounds__(256) gemm_bf16f(GemmDesc d, const bf16_t* __re
         for (int h = 0; h < KH; h++)
 #pragma unroll
             for (int j = 0; j < 4; j++) {
-                // column 4 nq + j, k rows kq + 32 h + 0..3: one 8-byte LDS write
-                auto half = [&](int r) {
-                    const uint2 v = vb[h][r];
-                    const uint32_t w = (j < 2) ? v.x : v.y;
-                    return (j & 1) ? (w >> 16) : (w & 0xffffu);
-                };
+                // column 4 nq + j, k rows kq + 32 h + 0..3: one 8-byte LDS write;
+                // each word pairs column j of two k rows (one byte permute:
+                // selector 0x05040100 takes the low halves, 0x07060302 the high)
+                const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+                auto col = [&](int r) { return (j < 2) ? vb[h][r].x : vb[h][r].y; };
                 uint2 w;
-                w.x = half(0) | (half(1) << 16);
-                w.y = half(2) | (half(3) << 16);
+                w.x = __builtin_amdgcn_perm(col(1), col(0), sel);
+                w.y = __builtin_amdgcn_perm(col(3), col(2), sel);
                 *(uint2*)&Bs[4 * nq + j][kq + 32 * h] = w;
             }
         __syncthreads();
