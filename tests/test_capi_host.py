@@ -402,14 +402,15 @@ def test_limited_planner_matches_oracle_on_random_expressions(seed):
 ])
 def test_conv_contraction_kernel_selected(name, steps):
     """Steps that convolve and contract one channel index with more than 16
-    output channels run on the MFMA conv-contraction kernel (cconv), both
-    forward and input gradient; the filter gradient does not."""
+    output channels run on the MFMA conv-contraction kernel (cconv, or its
+    register-filter form cconv_r for fp32 with at most 8 channels and 9
+    taps), both forward and input gradient; the filter gradient does not."""
     w = W.WORKLOADS.get(name) or W.PARITY_WORKLOADS.get(name) or W.tucker2_layer(
         "C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21)
     p = _plan(w.spec, w.shapes, dtype=B.CE_BF16 if w.dtype == "bf16" else B.CE_F32)
     text = B.ce_plan_describe(p)
     B.ce_plan_destroy(p)
-    on36 = [l for l in text.splitlines() if "cconv<" in l]
+    on36 = [l for l in text.splitlines() if "cconv<" in l or "cconv_r<" in l]
     for s in steps:
         assert any(s in l for l in on36), (name, s, text)
     assert len(on36) == len(steps), (name, on36)
