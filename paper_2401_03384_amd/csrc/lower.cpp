@@ -964,7 +964,10 @@ bool try_cconv(const PairOp& op, std::vector<Launch>& out) {
     merge(Qd);
     if (U.size() > 2 || Pd.size() != 1 || Qd.size() != 1) return false;
     const int64_t P = Pd[0].size, Q = Qd[0].size;
-    if (P > (bf ? 128 : 64) || Q <= 16) return false;
+    // fp32: at most 8 contracted channels.  With more, the general contraction
+    // is faster (64 channels, 3x3: a 64 x 64 dense step 517 against 1631 us, a
+    // Tucker core over 14 x 14 planes 50 + 15 against 390 us)
+    if (P > (bf ? 128 : 8) || Q <= 16) return false;
     CconvDesc d;
     std::memset(&d, 0, sizeof(d));
     d.H = (int32_t)H;

@@ -92,6 +92,7 @@ CASES = {
     "C3c5": W.PARITY_WORKLOADS["C3c5"],
     "C3m": W.PARITY_WORKLOADS["C3m"],
     "C3c_f32": W.PARITY_WORKLOADS["C3c_f32"],
+    "C3p5": W.PARITY_WORKLOADS["C3p5"],
     "C4c": W.PARITY_WORKLOADS["C4c"],
     "C4t": W.rtt_layer("C4t", 1, (2, 4, 2), (2, 2, 4), 7, 6, 4, 3, "f32", 22),
     "C5at": W.rcp_layer("C5at", 2, (4, 2, 4), (2, 4, 2), 5, 7, 16, 3, "bf16", 23),

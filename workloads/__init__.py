@@ -141,6 +141,9 @@ PARITY_WORKLOADS = {
     "C3f2": tucker2_layer("C3f2", 32, 72, 256, 16, 16, 24, 40, 3, "bf16", 42),
     # the same kernel in fp32 (Tucker core; the tensor-train layer's transposed conv)
     "C3c_f32": tucker2_layer("C3c_f32", 2, 24, 40, 5, 11, 20, 40, 3, "f32", 31),
+    # the fp32 conv-contraction kernel proper (6 contracted channels, 5 x 5
+    # taps, a ragged 12 x 13 plane)
+    "C3p5": tucker2_layer("C3p5", 2, 32, 24, 12, 13, 6, 40, 5, "f32", 47),
     "C4c": rtt_layer("C4c", 1, (2, 2, 4), (2, 2, 2), 6, 7, 16, 3, "f32", 34),
     # the full tensor-train chain at channel sizes of the 28x28 layer, small planes
     "C4w": rtt_layer("C4w", 2, (4, 8, 8), (4, 8, 8), 9, 11, 16, 3, "f32", 35),
