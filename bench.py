@@ -408,9 +408,15 @@ def sweep(args):
     rows = []
     for name, *_ in W.RESNET34_CONVS:
         w128, st = W.resnet34_cp_layer(name, batch=128)
-        row = {"layer": name, "stride": st.get("h", 1), "rank": w128.shapes[1][0],
-               "X": list(w128.shapes[0])}
-        for order, path in (("optimal", None), ("left_to_right", ltr)):
+        rows.append({"layer": name, "stride": st.get("h", 1), "rank": w128.shapes[1][0],
+                     "X": list(w128.shapes[0])})
+    # every layer's planned order first, then every left-to-right run: a step
+    # timed right after a left-to-right run (gigabytes of workspace allocated
+    # and freed) ran several times slower than the same step alone
+    for order, path in (("optimal", None), ("left_to_right", ltr)):
+        for row in rows:
+            name = row["layer"]
+            w128, st = W.resnet34_cp_layer(name, batch=128)
             p128 = P.Plan(w128.spec, w128.shapes, "f32", strides=st, path=path)
             w, _ = W.resnet34_cp_layer(name, batch=args.sweep_batch)
             r = Runner(w, args.dtype or "f32", path=path, strides=st)
@@ -425,12 +431,11 @@ def sweep(args):
                           "steps": [[a, b] for a, b, _ in r.ref.steps]}
             del r
             torch.cuda.empty_cache()
+            print(f"sweep {name} {order}: {row[order]['ms_fwd_bwd']} ms", file=sys.stderr, flush=True)
+    for row in rows:
         row["flop_ratio"] = round(row["left_to_right"]["fwd_gflop_b128"] /
                                   row["optimal"]["fwd_gflop_b128"], 2)
         row["time_ratio"] = round(row["left_to_right"]["ms_fwd_bwd"] / row["optimal"]["ms_fwd_bwd"], 2)
-        print(f"sweep {name}: {row['flop_ratio']}x FLOPs, {row['time_ratio']}x time", file=sys.stderr,
-              flush=True)
-        rows.append(row)
     print(json.dumps({"sweep": "ResNet-34 CP layers, compression rate 100%", "dtype": args.dtype or "f32",
                       "timed_batch": args.sweep_batch, "layers": rows}), flush=True)
 
