@@ -35,8 +35,11 @@ ALU_BOUND = {"rcp_fwd": 157.3, "rcp_bwd": 157.3, "cred": 78.6, "credw": 78.6}
 def parse_args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    # the chip's clocks rise over tens of milliseconds of load: 500 steps of
+    # the default layer (about 90 ms) reach the steady state, 5 steps do not
+    # (C2 fp32: 0.227 ms a step after 5, 0.183 ms after 200)
+    ap.add_argument("--warmup", type=int, default=500)
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--dtype", default=None, help="f32 or bf16 (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -215,6 +218,22 @@ def cpu_baseline(w, batch):
                       f"{passes} passes"}
 
 
+def warm(step, min_steps, min_s=0.1):
+    """Untimed steps until at least min_steps have run and min_s seconds have
+    passed: the GPU clocks ramp up over tens of milliseconds of load, and
+    every layer here is set up after host work that leaves the GPU idle."""
+    import torch
+
+    t0 = time.perf_counter()
+    n = 0
+    while n < min_steps or time.perf_counter() - t0 < min_s:
+        step()
+        n += 1
+        if n % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
 def compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args):
     """The paper's baseline order on the same kernels: forward + backward time,
     forward multiplications and workspace of the left-to-right plan."""
@@ -233,9 +252,7 @@ def compare_ltr(w, dtype, xs, d, ltr, flags, stream, cdt, args):
         P.ce_forward(pl.handle, in_ptrs, out.data_ptr(), ws.data_ptr(), ws.numel(), stream)
         P.ce_backward(pl.handle, in_ptrs, d.data_ptr(), g_ptrs, ws.data_ptr(), ws.numel(), stream)
 
-    for _ in range(2):
-        run()
-    torch.cuda.synchronize()
+    warm(run, 2)
     n = max(3, args.steps // 5)
     t0 = time.perf_counter()
     for _ in range(n):
@@ -367,8 +384,7 @@ def config_line(name, dtype, steps, samples):
     import workloads as W
 
     r = Runner(W.WORKLOADS[name], dtype)
-    for _ in range(3):
-        r.step()
+    warm(r.step, 3)
     kname, share = r.dominant()
     t, roof = r.kernel_roofline(kname, share, max(5, steps // 2))
     t_mean = r.timed(steps)
@@ -420,8 +436,7 @@ def sweep(args):
             p128 = P.Plan(w128.spec, w128.shapes, "f32", strides=st, path=path)
             w, _ = W.resnet34_cp_layer(name, batch=args.sweep_batch)
             r = Runner(w, args.dtype or "f32", path=path, strides=st)
-            for _ in range(2):
-                r.step()
+            warm(r.step, 2)
             n = 3 if order == "left_to_right" else 10
             t = r.timed(n)
             row[order] = {"fwd_gflop_b128": round(2 * p128.fwd_macs / 1e9, 3),
