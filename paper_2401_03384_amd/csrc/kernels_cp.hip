@@ -285,15 +285,20 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
     const int cl = lane & 31;
 
-    // X rows as B-operand slots (the same slot layout as arow), loaded one row
-    // ahead through a raw buffer: rows and lanes outside the image read zeros
+    // X rows as B-operand slots (the same slot layout as arow), loaded PD rows
+    // ahead through a raw buffer: rows and lanes outside the image read zeros,
+    // and so do the rows past the segment's last (X row h1 - 1 + CH), which
+    // the last rows' prefetches would otherwise fetch for nothing
     constexpr uint32_t E = sizeof(T);
+    constexpr int PD = BF ? 1 : 2;
     const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(NS * d.x_ss * E));
     const uint32_t xcs = (uint32_t)(d.x_ss * E);
     const uint32_t kOut = 0x80000000u;   // past the range: reads 0
     const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
-    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
-    uint32_t xa[NS / 2];
+    const int xlast = min(H - 1, h1 - 1 + CH);
+    auto xoff = [&](int row) { return (row >= 0 && row <= xlast) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    // fp32: two row buffers, the rows of the walk alternating between them
+    uint32_t xa[NS / 2], xb[NS / 2];
     // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in a; side(c),
     // c = 0..NS/4-1, is memory work issued along the chain (see piped)
     auto gemm1 = [&](const uint32_t (&a)[NS / 2], auto side) {
@@ -397,6 +402,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     }
 #pragma unroll
     for (int u = 0; u < NS / 2; u++) xa[u] = xp[(KH - 1) % NP][u];
+    if constexpr (PD == 2) arow<T, NS>(xb, rX, xoff(h0 + CH + 1), xcs);
     // Y rows through a raw buffer (one sample; stores past the range are
     // dropped): the lane's column and channel 4*half in the lane offset, the
     // rest of the channel in the uniform offset (Y's channel stride is X's)
@@ -412,7 +418,8 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         const int mb = item >> 4, i = item & 15, ch = 32 * mb + row32(i, 0);   // + 4 half, in yv0
         bstore(accYp[mb][i], (T*)nullptr, rYo, (ch & 1) ? v0 + xcs : v0, (uint32_t)(2 * (ch >> 1)) * xcs);
     };
-    auto fwd_row = [&](int h, auto PST) {
+    // row h: Z1 of X row h + CH from cur, which then takes X row h + CH + PD
+    auto fwd_row = [&](int h, auto PST, uint32_t (&cur)[NS / 2]) {
         // The tap and Ut tables are re-read from LDS every row: the offsets
         // pass through an empty asm so the loads are not hoisted out of the
         // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
@@ -423,8 +430,10 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         const float* KwP = (const float*)(smem + o_kw);
         // fp32: memory work along the chains (their MFMAs leave the issue free
         // for it): the stores of Y row h - 1 along Z1 (pst), the loads of the
-        // next X row along GEMM2.  bf16 (short chains): the loads right after
-        // Z1, the stores at the end of the row.
+        // X row two rows ahead along GEMM2 (a whole row of latency cover: under
+        // the load of the full chip a half row was not enough).  bf16 (short
+        // chains): the loads of the next row right after Z1, the stores at the
+        // end of the row.
         const uint32_t pv0 = yv0 + (uint32_t)((h - 1) * W) * E;
         auto side_a = [&](int c) {   // c = 0..NS/4-1
             if constexpr (!BF && decltype(PST)::value) {
@@ -434,15 +443,15 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
                     if (c * PS + j < 16 * MB2) store_y(c * PS + j, pv0);
             }
         };
-        ring[KH - 1] = gemm1(xa, side_a);
-        const uint32_t xo = xoff(h + KH - CH);   // the next row's, used one row later
-        if constexpr (BF) arow<T, NS>(xa, rX, xo, xcs);
+        ring[KH - 1] = gemm1(cur, side_a);
+        const uint32_t xo = xoff(h + CH + PD);   // used PD rows later
+        if constexpr (BF) arow<T, NS>(cur, rX, xo, xcs);
         auto side_b = [&](int c) {   // c = 0..15
             if constexpr (BF) return;
             constexpr int PX = (NS / 2 + 15) / 16;
 #pragma unroll
             for (int j = 0; j < PX; j++)
-                if (c * PX + j < NS / 2) xa[c * PX + j] = aslot<T>(rX, xo, xcs, c * PX + j);
+                if (c * PX + j < NS / 2) cur[c * PX + j] = aslot<T>(rX, xo, xcs, c * PX + j);
         };
         // conv along h
         f32x16 z2;
@@ -527,14 +536,25 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
             gemm2(accYp);
         }
     };
-    // The first row runs outside the loop: the loop is then entered, like its
+    // The first rows run outside the loop: the loop is then entered, like its
     // back edge, with a Y row pending and the same memory operations
     // outstanding, so the wait counts the compiler derives for the prefetched
-    // X row at the loop head are those of the steady state.
+    // X rows at the loop head are those of the steady state.  fp32: the loop
+    // takes two rows (buffers xa, xb), a last odd row follows it.
     const std::true_type yes;
     const std::false_type no;
-    fwd_row(h0, no);
-    for (int h = h0 + 1; h < h1; h++) fwd_row(h, yes);
+    fwd_row(h0, no, xa);
+    if constexpr (PD == 1) {
+        for (int h = h0 + 1; h < h1; h++) fwd_row(h, yes, xa);
+    } else if (h0 + 1 < h1) {
+        fwd_row(h0 + 1, yes, xb);
+        int h = h0 + 2;
+        for (; h + 1 < h1; h += 2) {
+            fwd_row(h, yes, xa);
+            fwd_row(h + 1, yes, xb);
+        }
+        if (h < h1) fwd_row(h, yes, xa);
+    }
     if constexpr (!BF) {
         const uint32_t lv0 = yv0 + (uint32_t)((h1 - 1) * W) * E;
 #pragma unroll
