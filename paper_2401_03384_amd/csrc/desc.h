@@ -169,9 +169,11 @@ struct CpDesc {
     int64_t kh_sr, kh_sj, kw_sr, kw_sj;
     int64_t waves, blocks;
     // LDS operand tables, laid out by the planner: UsL [32][lda] at 0, the
-    // permuted Ut operands at o_ut, the permuted taps at o_kh / o_kw
+    // permuted Ut operands at o_ut, the permuted taps at o_kh / o_kw, the
+    // vertical taps reversed (for segments walked upwards) at o_khr
     uint32_t lds_bytes, o_ut, o_kh, o_kw;
     int32_t lda;
+    uint32_t o_khr;
 };
 
 // General contraction on MFMA tiles:

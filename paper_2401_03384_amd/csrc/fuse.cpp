@@ -31,6 +31,8 @@ void cp_tables(CpDesc& d, bool bf) {
     o += (size_t)16 * 2 * d.KH * 4;
     d.o_kw = (uint32_t)o;
     o += (size_t)16 * 2 * d.KW * 4;
+    d.o_khr = (uint32_t)o;
+    o += (size_t)16 * 2 * d.KH * 4;
     d.lds_bytes = (uint32_t)al16(o);
 }
 

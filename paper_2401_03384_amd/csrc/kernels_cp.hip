@@ -258,7 +258,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     constexpr int TT = 32 * MB2, NS = 32 * MS;
     constexpr int CH = (KH - 1) / 2, HWW = (KW - 1) / 2;
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    const int S = d.S, H = d.H, W = d.W;
+    const int H = d.H, W = d.W;
     const int LDA = d.lda;
     T* UsL = (T*)smem;
     const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -280,7 +280,17 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     }
     const int col = cb * d.colstride - HWW + (lane & 31);
     const bool colok = col >= 0 && col < W;
-    const int h0 = seg * d.seg_rows, h1 = min(H, h0 + d.seg_rows);
+    // Rows in walk order: for bf16, odd segments walk upwards (walk row r is
+    // image row H - 1 - r, and the vertical taps are taken reversed), so that
+    // the two segments at every boundary read its halo rows at the same time,
+    // both at their starts or both at their ends, and the second read finds
+    // them in L2 (C2 bf16: forward + backward 86.0 -> 84.5 us; for fp32 the
+    // step measured 1.5% slower, with a forward no faster).  h0, h1 bound the
+    // segment in walk rows.
+    const bool up = BF && (seg & 1) != 0;
+    const int p0 = seg * d.seg_rows, p1 = min(H, p0 + d.seg_rows);
+    const int h0 = up ? H - p1 : p0, h1 = up ? H - p0 : p1;
+    auto prow = [&](int r) { return up ? H - 1 - r : r; };
     const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
     T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
     const int cl = lane & 31;
@@ -296,7 +306,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const uint32_t kOut = 0x80000000u;   // past the range: reads 0
     const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
     const int xlast = min(H - 1, h1 - 1 + CH);
-    auto xoff = [&](int row) { return (row >= 0 && row <= xlast) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    auto xoff = [&](int row) { return (row >= 0 && row <= xlast) ? xa0 + (uint32_t)(prow(row) * W) * E : kOut; };
     // fp32: two row buffers, the rows of the walk alternating between them
     uint32_t xa[NS / 2], xb[NS / 2];
     // Z1[r][col] = sum_s Us[r][s] X[s][row][col] for the row held in a; side(c),
@@ -387,7 +397,12 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     }
 #pragma unroll
     for (int q = 0; q < QT; q++) UtP[tid + 256 * q] = vt[q];
-    if (tid < NKH) KhP[tid] = vkh;
+    if (tid < NKH) {
+        // and the same taps reversed at o_khr, for the upward walk
+        const int j = tid % KH;
+        KhP[tid] = vkh;
+        ((float*)(smem + d.o_khr))[tid + KH - 1 - 2 * j] = vkh;
+    }
     if (tid < NKW) KwP[tid] = vkw;
     }
     __syncthreads();
@@ -423,7 +438,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         // The tap and Ut tables are re-read from LDS every row: the offsets
         // pass through an empty asm so the loads are not hoisted out of the
         // loop, where they would hold 16*(KH+KW+MB2) registers for its life.
-        uint32_t o_ut = d.o_ut, o_kh = d.o_kh, o_kw = d.o_kw;
+        uint32_t o_ut = d.o_ut, o_kh = up ? d.o_khr : d.o_kh, o_kw = d.o_kw;
         asm volatile("" : "+s"(o_ut), "+s"(o_kh), "+s"(o_kw));
         const T* UtP = (const T*)(smem + o_ut);
         const float* KhP = (const float*)(smem + o_kh);
@@ -434,7 +449,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         // the load of the full chip a half row was not enough).  bf16 (short
         // chains): the loads of the next row right after Z1, the stores at the
         // end of the row.
-        const uint32_t pv0 = yv0 + (uint32_t)((h - 1) * W) * E;
+        const uint32_t pv0 = yv0 + (uint32_t)(prow(h - 1) * W) * E;
         auto side_a = [&](int c) {   // c = 0..NS/4-1
             if constexpr (!BF && decltype(PST)::value) {
                 constexpr int NC = NS / 4, PS = (16 * MB2 + NC - 1) / NC;
@@ -525,7 +540,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
             f32x16 acc2[MB2];
             gemm2(acc2);
             if (store_lane) {
-                T* yr = Yc + (int64_t)h * W;
+                T* yr = Yc + (int64_t)prow(h) * W;
 #pragma unroll
                 for (int mb = 0; mb < MB2; mb++)
 #pragma unroll
@@ -556,7 +571,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         if (h < h1) fwd_row(h, yes, xa);
     }
     if constexpr (!BF) {
-        const uint32_t lv0 = yv0 + (uint32_t)((h1 - 1) * W) * E;
+        const uint32_t lv0 = yv0 + (uint32_t)(prow(h1 - 1) * W) * E;
 #pragma unroll
         for (int item = 0; item < 16 * MB2; item++) store_y(item, lv0);
     }
@@ -754,7 +769,9 @@ __global__ void __launch_bounds__(256, 1)
     const T* UsT = (const T*)(smem + d.o_ust);
     const int hs = h0 - CH;
     // A-operand row offsets: rows outside the image (and lanes outside it) read zeros
-    auto xoff = [&](int row) { return (row >= 0 && row < H) ? xa0 + (uint32_t)(row * W) * E : kOut; };
+    // (X rows past h1 are not read: the last row's prefetch would fetch one for nothing)
+    const int xlast = min(H - 1, h1);
+    auto xoff = [&](int row) { return (row >= 0 && row <= xlast) ? xa0 + (uint32_t)(row * W) * E : kOut; };
     auto yoff = [&](int row) { return (row >= 0 && row < H) ? ya0 + (uint32_t)(row * W) * E : kOut; };
     // dX: a zero range drops every store when the gradient is not wanted
     const __amdgpu_buffer_rsrc_t rD =

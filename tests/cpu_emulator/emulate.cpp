@@ -435,7 +435,8 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     REQ(d.o_ut >= (uint64_t)32 * d.lda * (bf ? 2 : 4) && d.o_ut % 16 == 0, "UtP offset");
     REQ(d.o_kh >= d.o_ut + (bf ? (uint64_t)2 * 2 * d.T * 8 * 2 : (uint64_t)16 * 2 * d.T * 4), "Kh offset");
     REQ(d.o_kw >= d.o_kh + (uint64_t)16 * 2 * d.KH * 4, "Kw offset");
-    REQ(d.lds_bytes >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4 && d.lds_bytes <= 64 * 1024 &&
+    REQ(d.o_khr >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4, "reversed Kh offset");
+    REQ(d.lds_bytes >= d.o_khr + (uint64_t)16 * 2 * d.KH * 4 && d.lds_bytes <= 64 * 1024 &&
         ln.lds == d.lds_bytes, "LDS size");
     const int H = d.H, W = d.W, R = d.R, ch = (d.KH - 1) / 2, cw = (d.KW - 1) / 2;
     std::vector<double> z1((size_t)R * H * W), z2((size_t)R * H * W), z3v((size_t)R * H * W);
