@@ -51,6 +51,9 @@ def parse_args():
                     help="pairwise order: the planner's optimum or the left-to-right baseline")
     ap.add_argument("--max-elements", type=int, default=None,
                     help="cap on the elements of every intermediate (memory-limited order)")
+    ap.add_argument("--save-budget", type=float, default=None, metavar="MiB",
+                    help="checkpointing: MiB of forward intermediates the backward may read "
+                         "instead of recomputing (default: recompute every one)")
     ap.add_argument("--graph", action="store_true",
                     help="also time forward + backward replayed from a HIP graph (no host work)")
     ap.add_argument("--compare-ltr", action="store_true",
@@ -269,7 +272,7 @@ class Runner:
     gradient and workspace buffers, and step() = parse + plan + forward +
     backward through the C ABI on torch's current stream."""
 
-    def __init__(self, w, dtype, flags=0, path=None, max_elements=None, strides=None):
+    def __init__(self, w, dtype, flags=0, path=None, max_elements=None, strides=None, save_budget=None):
         import numpy as np
         import torch
         import paper_2401_03384_amd as P
@@ -278,6 +281,7 @@ class Runner:
         if dtype != w.dtype:
             w = W.Workload(w.name, w.spec, w.shapes, dtype, w.seed, w.sigmas, w.out_shape, w.backward)
         self.w, self.dtype, self.flags, self.path, self.max_elements = w, dtype, flags, path, max_elements
+        self.save_budget = save_budget
         self.strides = dict(strides or {})
         dev = torch.device("cuda:0")
         tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -286,7 +290,7 @@ class Runner:
         self.d = torch.from_numpy(dy.astype(np.float32)).to(tdt).to(dev)
         del ins, dy
         self.ref = P.Plan(w.spec, w.shapes, dtype, flags=flags, path=path, max_elements=max_elements,
-                          strides=self.strides)
+                          strides=self.strides, save_budget=save_budget)
         ref = self.ref
         self.ws = torch.empty(max(ref.ws_fwd, ref.ws_bwd, 1), dtype=torch.uint8, device=dev)
         self.out = torch.empty(ref.out_shape, dtype=tdt, device=dev)
@@ -303,7 +307,10 @@ class Runner:
         e = P.ce_expr_parse(w.spec, self.shapes)
         for label, st in self.strides.items():
             P.ce_expr_set_stride(e, label, st)
-        if self.path is None and self.max_elements is not None:
+        if self.path is None and self.save_budget is not None:
+            p = P.ce_plan_create_ex(e, P.CE_COST_FWD, self.cdt, self.flags, 0, self.max_elements or 0,
+                                    self.save_budget)
+        elif self.path is None and self.max_elements is not None:
             p = P.ce_plan_create_limited(e, P.CE_COST_FWD, self.cdt, self.flags, self.max_elements)
         elif self.path is None:
             p = P.ce_plan_create(e, P.CE_COST_FWD, self.cdt, self.flags)
@@ -361,6 +368,16 @@ class Runner:
         t = self.timed(n)
         records = [P.ce_timing_record(i) for i in range(P.ce_timing_end())]
         return t, roofline(records, self.dtype, share)
+
+
+def checkpoint_line(plan):
+    """The plan's checkpointing choice: steps whose results the forward keeps
+    for the backward, their bytes, and the multiplications recomputed."""
+    import paper_2401_03384_amd as P
+
+    steps, nbytes, macs = P.ce_plan_checkpoint(plan.handle)
+    return {"saved_steps": [s for s in range(64) if steps >> s & 1], "saved_bytes": nbytes,
+            "recompute_macs": macs}
 
 
 def max_batch_line(w):
@@ -488,7 +505,8 @@ def main():
     # left-to-right in the list format of ce_plan_create_with_path
     ltr = [(0, 1)] + [(0, n_in - 1 - k) for k in range(1, n_in - 1)]
     path = ltr if args.path == "ltr" else None
-    r = Runner(w, dtype, flags, path, args.max_elements)
+    budget = None if args.save_budget is None else int(args.save_budget * 2**20)
+    r = Runner(w, dtype, flags, path, args.max_elements, save_budget=budget)
     w, ref = r.w, r.ref
 
     for _ in range(args.warmup):
@@ -540,11 +558,13 @@ def main():
                    "flops_per_step": 6 * macs,
                    "path": ("left-to-right" if path else "optimal")
                    + (f", intermediates <= {args.max_elements} elements" if args.max_elements else "")
+                   + (f", save budget {args.save_budget} MiB" if budget is not None else "")
                    + (", generic kernel" if args.generic else "")},
         "step_ms": smp,
         "floor_us": round(floor, 1),
         "floor_frac": round(floor / (t_step * 1e6), 4),
         "workspace_bytes": {"fwd": ref.ws_fwd, "bwd": ref.ws_bwd},
+        "checkpoint": checkpoint_line(ref),
         "max_batch": max_batch_line(w),
         "fwd_ms": round(t_fwd * 1e3, 4),
         "bwd_ms": round(t_bwd * 1e3, 4),
@@ -568,7 +588,7 @@ def main():
         lt["time_ratio_vs_optimal"] = round(lt["ms_per_step"] / (t_step * 1e3), 3)
         line["left_to_right"] = lt
     default_run = (args.workload == "C2" and dtype == "f32" and path is None and
-                   not args.max_elements and not args.generic)
+                   not args.max_elements and not args.generic and budget is None)
     if not args.no_configs and default_run:
         del r
         torch.cuda.empty_cache()

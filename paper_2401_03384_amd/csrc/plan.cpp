@@ -782,16 +782,22 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
             op.what = "step " + std::to_string(s) + " fwd " + tensor_str(E, op.L) + "," +
                       tensor_str(E, op.R) + "->" + tensor_str(E, op.C);
         }
+        auto node_bytes = [&](int s) {
+            return (uint64_t)bld.tensor_of(p->steps[s].c, dt, {}).numel() * elem(dt);
+        };
         // a contraction whose result only feeds a convolution of the
-        // tensor-train pattern runs fused with it (the result stays on chip;
-        // not when the caller asks to keep intermediates for the backward)
+        // tensor-train pattern runs fused with it (the result stays on chip);
+        // not when the caller asks to keep every intermediate for the
+        // backward, nor when the save budget can hold that result (keeping it
+        // then spares its recompute, which the fused chain cannot)
         std::vector<int> fused_to(m, -1), fused_from(m, -1);
         std::vector<Launch> fused(m);
         if (!(flags & CE_FLAG_GENERIC_ONLY) && !(flags & CE_FLAG_NO_FUSION) &&
-            !(flags & CE_FLAG_SAVE_INTERMEDIATES) && lim.save_budget == 0) {
+            !(flags & CE_FLAG_SAVE_INTERMEDIATES)) {
             for (int s = 0; s + 1 < m; s++) {
                 const int cs = consumer_step(p->steps[s].c);
                 if (cs >= m || fused_from[s] >= 0 || fused_to[s] >= 0 || fused_from[cs] >= 0) continue;
+                if (lim.save_budget > 0 && node_bytes(s) <= lim.save_budget) continue;
                 Launch ln;
                 if (!fuse_tt_forward(fops[s], fops[cs], ln)) continue;
                 fused_to[s] = cs;
@@ -848,9 +854,6 @@ ce_plan* make_plan(const ce_expr& e, ce_cost_mode mode, ce_dtype dtype, unsigned
         for (int s = 0; s + 1 < m; s++)
             for (const WsItem& it : items)
                 if (it.id == p->steps[s].c) cand.push_back(s);
-        auto node_bytes = [&](int s) {
-            return (uint64_t)bld.tensor_of(p->steps[s].c, dt, {}).numel() * elem(dt);
-        };
         uint32_t save = 0;
         if (flags & CE_FLAG_SAVE_INTERMEDIATES) {
             for (int s : cand) save |= 1u << s;
