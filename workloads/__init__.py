@@ -119,6 +119,13 @@ PARITY_WORKLOADS = {
     # with a one-row segment at the bottom (4-row and 2-row segments)
     "C2seg": cp_layer("C2seg", 128, 32, 32, 29, 16, 32, 3, "f32", 21),
     "C2seg_bf16": cp_layer("C2seg_bf16", 64, 64, 64, 23, 20, 32, 3, "bf16", 22),
+    # enough samples that the fused forward walks segments of several rows:
+    # 6-row segments (the two-row loop, no odd row; backward: one 12-row
+    # segment), 4-row segments over 13 rows (a 1-row last segment; backward
+    # 7-row segments), and bf16 5-row segments (odd ones walked upwards)
+    "C2fseg6": cp_layer("C2fseg6", 1024, 32, 32, 12, 8, 32, 3, "f32", 23),
+    "C2fseg4": cp_layer("C2fseg4", 512, 32, 32, 13, 8, 32, 3, "f32", 24),
+    "C2fseg5_bf16": cp_layer("C2fseg5_bf16", 1024, 32, 32, 10, 8, 32, 3, "bf16", 25),
     "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
     "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
     "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
