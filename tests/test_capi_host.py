@@ -472,6 +472,34 @@ def test_checkpoint_choice_matches_oracle(name, frac):
         B.ce_plan_destroy(p)
 
 
+def test_checkpoint_keeps_tensor_train_fusion():
+    """Under a save budget that cannot hold the tensor-train producer's
+    result, the forward stays fused (that result never reaches memory) and
+    only the small merged factors are kept; a budget that holds it unfuses
+    the forward and keeps it, so the backward recomputes nothing."""
+    w = W.WORKLOADS["C4"]
+    x = B.ce_expr_parse(w.spec, w.shapes)
+    try:
+        p0 = B.ce_plan_create(x, B.CE_COST_FWD, B.CE_F32, 0)
+        fused_ws = B.ce_plan_workspace_size(p0, 0)
+        big = 4 * 64 * 128 * 2 * 16 * 28 * 28   # the rank-expanded input, fp32
+        small = B.ce_plan_create_ex(x, B.CE_COST_FWD, B.CE_F32, 0, save_budget=16 << 20)
+        whole = B.ce_plan_create_ex(x, B.CE_COST_FWD, B.CE_F32, 0, save_budget=big + (1 << 20))
+    finally:
+        B.ce_expr_destroy(x)
+    try:
+        mask, nbytes, rec = B.ce_plan_checkpoint(small)
+        assert "fused tensor-train" in B.ce_plan_describe(small)
+        assert 0 < nbytes < (1 << 20) and rec > 0
+        assert B.ce_plan_workspace_size(small, 0) < fused_ws + (1 << 20)
+        mask, nbytes, rec = B.ce_plan_checkpoint(whole)
+        assert "fused tensor-train" not in B.ce_plan_describe(whole)
+        assert nbytes >= big and rec == 0
+    finally:
+        for p in (p0, small, whole):
+            B.ce_plan_destroy(p)
+
+
 @pytest.mark.parametrize("name", ["C2s", "C4s", "C5bs", "rtt_conv", "tr_conv"])
 def test_cost_cap_plan_matches_oracle(name):
     """ce_plan_create_ex with a per-step cost cap (Section 3.2, Figure 2)
