@@ -13,8 +13,8 @@ Blanks are ignored.  A label may occur at most once per operand and once in
 the output.  A label that is not convolved must have one size everywhere
 (Appendix A, contraction: the method fails when sizes of the same letter
 differ); a convolved label may carry a different size in each operand
-(Section 2.2: 'the same letter is used for different modes, even if their
-dimension sizes differ').
+(Section 2.2 lets one letter name convolved modes of unequal sizes, such as
+an image axis and the filter axis it is convolved with).
 """
 from __future__ import annotations
 
