@@ -78,8 +78,8 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     if (w.nslab != B * R * H || w.A != W || w.inner != 1 || w.r_div != H || w.r_size != R ||
         w.sign != 1 || w.off != -((w.K - 1) / 2))
         return false;
-    // register-resident strips: rank 32, S and T in {32, 64}, 3x3 or 5x5 filters
-    if (R != 32 || !(T == 32 || T == 64) || !(S == 32 || S == 64) || h.K != w.K || !(h.K == 3 || h.K == 5))
+    // register-resident strips: rank at most 32 (ranks past R as zero rows), S and T in {32, 64}, 3x3 or 5x5 filters
+    if (R < 1 || R > 32 || !(T == 32 || T == 64) || !(S == 32 || S == 64) || h.K != w.K || !(h.K == 3 || h.K == 5))
         return false;
     // one sample of X and of Y within a 32-bit byte range (raw buffer loads and
     // stores), both with channel stride H*W
@@ -188,8 +188,9 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
         if (x.kind != BUF_IN) return false;
     if (f.a.index != feature_operand) return false;   // dX is in the input type
     const CpDesc c = desc<CpDesc>(f);
-    // 3x3 filters and S = T in {32, 64} (the kernel's register budget)
-    if (c.KH != 3 || c.KW != 3 || c.S != c.T || !(c.T == 32 || c.T == 64) || c.R != 32) return false;
+    // 3x3 filters, S = T in {32, 64} (the kernel's register budget), rank at
+    // most 32 (one rank a lane; ranks past R run as zero rows)
+    if (c.KH != 3 || c.KW != 3 || c.S != c.T || !(c.T == 32 || c.T == 64) || c.R < 1 || c.R > 32) return false;
     const int dt = dtin(f);
     // one sample of X, dY and dX is addressed with 31-bit byte offsets
     const int64_t e_in = dt ? 2 : 4;

@@ -365,30 +365,31 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     static_assert(NKH <= 256 && NKW <= 256, "tap tables fit one pass");
     T vs[QS], vt[QT];
     float vkh = 0.f, vkw = 0.f;
-    // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t] (bf16), UtP[i][hf][t] = Ut[row32(i, 32*hf)][t] (fp32)
-    auto ut_src = [&](int e) {
-        if constexpr (BF) {
-            const int j = e & 7, t = (e >> 3) % TT, hf = (e / (8 * TT)) & 1, q = e / (16 * TT);
-            return row32(8 * q + j, 32 * hf) * d.ut_sr + t * d.ut_st;
-        } else {
-            const int t = e % TT, hf = (e / TT) & 1, i = e / (2 * TT);
-            return row32(i, 32 * hf) * d.ut_sr + t * d.ut_st;
-        }
+    // UtP[q][hf][t][j] = Ut[row32(8q+j, 32*hf)][t] (bf16), UtP[i][hf][t] = Ut[row32(i, 32*hf)][t] (fp32).
+    // A rank of R < 32 leaves ranks R..31 of every table zero: their Z1, Z2
+    // and Z3 rows are zero and add nothing to Y.
+    auto ut_rank = [&](int e) {
+        if constexpr (BF) return row32(8 * (e / (16 * TT)) + (e & 7), 32 * ((e / (8 * TT)) & 1));
+        else return row32(e / (2 * TT), 32 * ((e / TT) & 1));
     };
+    auto ut_col = [&](int e) { return BF ? (e >> 3) % TT : e % TT; };
 #pragma unroll
     for (int q = 0; q < QS; q++) {
         const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-        vs[q] = Us[r * d.us_sr + s * d.us_ss];
+        vs[q] = r < d.R ? Us[r * d.us_sr + s * d.us_ss] : (T)0;
     }
 #pragma unroll
-    for (int q = 0; q < QT; q++) vt[q] = Ut[ut_src(tid + 256 * q)];
+    for (int q = 0; q < QT; q++) {
+        const int e = tid + 256 * q, r = ut_rank(e);
+        vt[q] = r < d.R ? Ut[r * d.ut_sr + ut_col(e) * d.ut_st] : (T)0;
+    }
     if (tid < NKH) {
-        const int j = tid % KH, hf = (tid / KH) & 1, i = tid / (2 * KH);
-        vkh = load(Kh, row32(i, 32 * hf) * d.kh_sr + j * d.kh_sj);
+        const int j = tid % KH, hf = (tid / KH) & 1, r = row32(tid / (2 * KH), 32 * hf);
+        vkh = r < d.R ? load(Kh, r * d.kh_sr + j * d.kh_sj) : 0.f;
     }
     if (tid < NKW) {
-        const int j = tid % KW, hf = (tid / KW) & 1, i = tid / (2 * KW);
-        vkw = load(Kw, row32(i, 32 * hf) * d.kw_sr + j * d.kw_sj);
+        const int j = tid % KW, hf = (tid / KW) & 1, r = row32(tid / (2 * KW), 32 * hf);
+        vkw = r < d.R ? load(Kw, r * d.kw_sr + j * d.kw_sj) : 0.f;
     }
 #pragma unroll
     for (int q = 0; q < QS; q++) {
@@ -744,9 +745,9 @@ __global__ void __launch_bounds__(256, 1)
     const uint32_t ya0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * hf * ycs : kOut;
     float kh[KH], kw[KW];                            // this lane's rank: r = cl
 #pragma unroll
-    for (int j = 0; j < KH; j++) kh[j] = load(Kh, cl * d.kh_sr + j * d.kh_sj);
+    for (int j = 0; j < KH; j++) kh[j] = cl < d.R ? load(Kh, cl * d.kh_sr + j * d.kh_sj) : 0.f;
 #pragma unroll
-    for (int j = 0; j < KW; j++) kw[j] = load(Kw, cl * d.kw_sr + j * d.kw_sj);
+    for (int j = 0; j < KW; j++) kw[j] = cl < d.R ? load(Kw, cl * d.kw_sr + j * d.kw_sj) : 0.f;
 
     f32x16 ring[KH], dr[KH], accUt[MT], accUs[MS];
 #pragma unroll
@@ -816,16 +817,16 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int q = 0; q < QS; q++) {
             const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-            vs[q] = Us[r * d.us_sr + s * d.us_ss];
+            vs[q] = r < d.R ? Us[r * d.us_sr + s * d.us_ss] : (T)0;
             if constexpr (BF) {
                 const int s2 = e / 32, r2 = e - s2 * 32;
-                vu[q] = Us[r2 * d.us_sr + s2 * d.us_ss];
+                vu[q] = r2 < d.R ? Us[r2 * d.us_sr + s2 * d.us_ss] : (T)0;
             }
         }
 #pragma unroll
         for (int q = 0; q < QT; q++) {
             const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
-            vt[q] = Ut[r * d.ut_sr + t * d.ut_st];
+            vt[q] = r < d.R ? Ut[r * d.ut_sr + t * d.ut_st] : (T)0;
         }
         T* usa = (T*)smem;
         T* uta = (T*)(smem + d.o_uta);
@@ -1187,16 +1188,17 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int i = 0; i < 16; i++) red[wave * 32 * NT + row32(i, lane) * NT + 32 * n + cl] = accUt[n][i];
     __syncthreads();
-    for (int e = tid; e < 32 * NT; e += 256)
-        Put[blk * 32 * NT + e] = ((red[e] + red[32 * NT + e]) + red[64 * NT + e]) + red[96 * NT + e];
+    const int RR = d.R;   // partial rows a block (ranks R..31 are zero and not written)
+    for (int e = tid; e < RR * NT; e += 256)
+        Put[blk * RR * NT + e] = ((red[e] + red[32 * NT + e]) + red[64 * NT + e]) + red[96 * NT + e];
     __syncthreads();
 #pragma unroll
     for (int n = 0; n < MS; n++)
 #pragma unroll
         for (int i = 0; i < 16; i++) red[wave * 32 * NS + row32(i, lane) * NS + 32 * n + cl] = accUs[n][i];
     __syncthreads();
-    for (int e = tid; e < 32 * NS; e += 256)
-        Pus[blk * 32 * NS + e] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
+    for (int e = tid; e < RR * NS; e += 256)
+        Pus[blk * RR * NS + e] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
     __syncthreads();
     // taps: red[wave][half][r][KH + KW], summed over waves and halves in order
     constexpr int NJ = KH + KW;
@@ -1210,8 +1212,9 @@ __global__ void __launch_bounds__(256, 1)
         float v = 0.f;
 #pragma unroll
         for (int q = 0; q < 8; q++) v += red[q * 32 * NJ + e];
-        if (jj < KW) Pkw[blk * 32 * KW + r * KW + jj] = v;
-        else Pkh[blk * 32 * KH + r * KH + (jj - KW)] = v;
+        if (r >= RR) continue;
+        if (jj < KW) Pkw[blk * RR * KW + r * KW + jj] = v;
+        else Pkh[blk * RR * KH + r * KH + (jj - KW)] = v;
     }
 }
 
@@ -1253,7 +1256,7 @@ hipError_t launch_cpb_ty(const CpBwdDesc& d, const void* const* o, hipStream_t s
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s) {
     CpDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    if (d.R != 32 || !(d.T == 32 || d.T == 64)) return hipErrorInvalidValue;
+    if (d.R < 1 || d.R > 32 || !(d.T == 32 || d.T == 64)) return hipErrorInvalidValue;
     int bf = (ln.kind >> kBitIn) & 1;
     return bf ? launch_cp_ty<bf16_t>(d, ops, y, s) : launch_cp_ty<float>(d, ops, y, s);
 }
@@ -1262,7 +1265,7 @@ hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipS
 hipError_t launch_cp_bwd(const Launch& ln, const void* const* ops, hipStream_t s) {
     CpBwdDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    if (d.R != 32 || d.S != d.T || !(d.T == 32 || d.T == 64) || d.KH != d.KW) return hipErrorInvalidValue;
+    if (d.R < 1 || d.R > 32 || d.S != d.T || !(d.T == 32 || d.T == 64) || d.KH != d.KW) return hipErrorInvalidValue;
     int bf = (ln.kind >> kBitIn) & 1;
     return bf ? launch_cpb_ty<bf16_t>(d, ops, s) : launch_cpb_ty<float>(d, ops, s);
 }

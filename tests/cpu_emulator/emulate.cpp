@@ -423,7 +423,7 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     Buf Kh = resolve(ln.extra[0], c, 0, o4), Kw = resolve(ln.extra[1], c, 0, o5),
         Ut = resolve(ln.extra[2], c, 0, o6);
     REQ(o4 && o5 && o6, "unresolved buffer");
-    REQ(d.R == 32 && (d.T == 32 || d.T == 64) && d.S % 32 == 0, "sizes");
+    REQ(d.R >= 1 && d.R <= 32 && (d.T == 32 || d.T == 64) && d.S % 32 == 0, "sizes");
     REQ(d.KH == d.KW && (d.KH == 3 || d.KH == 5), "filter size");
     REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
         (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
@@ -945,7 +945,7 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
         REQ(o, "unresolved buffer");
     }
     Buf &Us = F[0], &Kh = F[1], &Kw = F[2], &Ut = F[3], &Pus = F[4], &Put = F[5], &Pkh = F[6], &Pkw = F[7];
-    REQ(d.R == 32 && d.S == d.T && (d.T == 32 || d.T == 64) && d.KH == 3 && d.KW == 3, "sizes");
+    REQ(d.R >= 1 && d.R <= 32 && d.S == d.T && (d.T == 32 || d.T == 64) && d.KH == 3 && d.KW == 3, "sizes");
     REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
         (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
     REQ((int64_t)d.segs * d.seg_rows >= d.H && (int64_t)(d.segs - 1) * d.seg_rows < d.H, "segments");

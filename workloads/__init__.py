@@ -126,6 +126,10 @@ PARITY_WORKLOADS = {
     "C2fseg6": cp_layer("C2fseg6", 1024, 32, 32, 12, 8, 32, 3, "f32", 23),
     "C2fseg4": cp_layer("C2fseg4", 512, 32, 32, 13, 8, 32, 3, "f32", 24),
     "C2fseg5_bf16": cp_layer("C2fseg5_bf16", 1024, 32, 32, 10, 8, 32, 3, "bf16", 25),
+    # fused CP chains with ranks below 32 (ranks past R run as zero rows)
+    "C2r16": cp_layer("C2r16", 3, 64, 64, 13, 37, 16, 3, "f32", 26),
+    "C2r8_bf16": cp_layer("C2r8_bf16", 3, 32, 64, 11, 19, 8, 3, "bf16", 27),
+    "C2r20k5": cp_layer("C2r20k5", 2, 64, 32, 12, 29, 20, 5, "f32", 28),
     "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
     "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
     "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
