@@ -22,11 +22,16 @@ size_t al16(size_t x) { return (x + 15) & ~size_t(15); }
 // operand rows; bf16 rows padded to keep 16-byte k-runs aligned), Ut permuted
 // to the accumulator-layout pairing of GEMM2 (fp32 [16][2][T], bf16
 // [2][2][T][8]) and the taps permuted the same way ([16][2][K]).
+// Channel counts below 32 or between 32 and 64 run padded to 32 or 64 (the
+// kernels' channel blocks): the tables hold zeros there.
+int pad32(int n) { return 32 * ((n + 31) / 32); }
+
 void cp_tables(CpDesc& d, bool bf) {
-    d.lda = bf ? d.S + 8 : d.S + 1;
+    const int SP = pad32(d.S), TP = pad32(d.T);
+    d.lda = bf ? SP + 8 : SP + 1;
     size_t o = al16((size_t)32 * d.lda * (bf ? 2 : 4));
     d.o_ut = (uint32_t)o;
-    o = al16(o + (bf ? (size_t)2 * 2 * d.T * 8 * 2 : (size_t)16 * 2 * d.T * 4));
+    o = al16(o + (bf ? (size_t)2 * 2 * TP * 8 * 2 : (size_t)16 * 2 * TP * 4));
     d.o_kh = (uint32_t)o;
     o += (size_t)16 * 2 * d.KH * 4;
     d.o_kw = (uint32_t)o;
@@ -78,8 +83,9 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     if (w.nslab != B * R * H || w.A != W || w.inner != 1 || w.r_div != H || w.r_size != R ||
         w.sign != 1 || w.off != -((w.K - 1) / 2))
         return false;
-    // register-resident strips: rank at most 32 (ranks past R as zero rows), S and T in {32, 64}, 3x3 or 5x5 filters
-    if (R < 1 || R > 32 || !(T == 32 || T == 64) || !(S == 32 || S == 64) || h.K != w.K || !(h.K == 3 || h.K == 5))
+    // register-resident strips: rank at most 32 (ranks past R as zero rows),
+    // S and T at most 64 (padded to 32 or 64), 3x3 or 5x5 filters
+    if (R < 1 || R > 32 || T < 1 || T > 64 || S < 1 || S > 64 || h.K != w.K || !(h.K == 3 || h.K == 5))
         return false;
     // one sample of X and of Y within a 32-bit byte range (raw buffer loads and
     // stores), both with channel stride H*W
@@ -134,8 +140,8 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     fused.need = g1.need | d1.need | d2.need | g2.need;
     fused.what = "fused CP chain: " + g1.what + " | " + d1.what + " | " + d2.what + " | " + g2.what;
     fused.kname = std::string("cp_fwd<") + (dt ? "unsigned short" : "float") + ", " +
-                  std::to_string(h.K) + ", " + std::to_string(w.K) + ", " + std::to_string(T / 32) + ", " +
-                  std::to_string(S / 32) + ">";
+                  std::to_string(h.K) + ", " + std::to_string(w.K) + ", " + std::to_string(pad32((int)T) / 32) + ", " +
+                  std::to_string(pad32((int)S) / 32) + ">";
     fused.alg_bytes = g1.alg_bytes + d1.alg_bytes + d2.alg_bytes + g2.alg_bytes;
     fused.alg_flops = g1.alg_flops + d1.alg_flops + d2.alg_flops + g2.alg_flops;
     // algorithmic bytes of the fused launch: X, factors and Y only
@@ -148,8 +154,9 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
 // LDS of the fused backward (see CpBwdDesc).
 void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     const size_t e = bf ? 2 : 4;
-    d.lda_s = bf ? d.S + 8 : d.S + 1;
-    d.lda_t = bf ? d.T + 8 : d.T + 1;
+    const int SP = pad32(d.S), TP = pad32(d.T);
+    d.lda_s = bf ? SP + 8 : SP + 1;
+    d.lda_t = bf ? TP + 8 : TP + 1;
     d.ldu = bf ? 32 + 8 : 0;
     d.ly = bf ? 40 : 33;
     d.lx = bf ? 40 : 36;   // 8-byte (bf16) / 16-byte (fp32) column runs stay aligned
@@ -157,9 +164,9 @@ void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     d.o_uta = (uint32_t)o;
     o = al16(o + (size_t)32 * d.lda_t * e);
     d.o_ust = (uint32_t)o;
-    if (bf) o = al16(o + (size_t)d.S * d.ldu * 2);
-    const size_t tz = (size_t)32 * 33 * 4, yt = al16((size_t)d.T * d.ly * e);
-    const size_t xl = al16((size_t)3 * d.S * d.lx * e);
+    if (bf) o = al16(o + (size_t)SP * d.ldu * 2);
+    const size_t tz = (size_t)32 * 33 * 4, yt = al16((size_t)TP * d.ly * e);
+    const size_t xl = al16((size_t)3 * SP * d.lx * e);
     // the dZ1 transpose tile gets its own space when everything fits, else it
     // shares the wave's dY tile (used earlier in each row)
     const bool share = o + 4 * (tz + yt + xl) > (size_t)160 * 1024;
@@ -172,7 +179,7 @@ void cp_bwd_tables(CpBwdDesc& d, bool bf) {
     d.o_xl = (uint32_t)o;
     d.xl_bytes = (uint32_t)xl;
     o += 4 * xl;
-    d.red_bytes = (uint32_t)(4 * std::max<size_t>({(size_t)4 * 32 * d.S, (size_t)4 * 32 * d.T,
+    d.red_bytes = (uint32_t)(4 * std::max<size_t>({(size_t)4 * 32 * SP, (size_t)4 * 32 * TP,
                                                    (size_t)8 * 32 * (d.KH + d.KW)}));
     d.lds_bytes = (uint32_t)std::max<size_t>(al16(o), d.red_bytes);
 }
@@ -188,9 +195,12 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
         if (x.kind != BUF_IN) return false;
     if (f.a.index != feature_operand) return false;   // dX is in the input type
     const CpDesc c = desc<CpDesc>(f);
-    // 3x3 filters, S = T in {32, 64} (the kernel's register budget), rank at
-    // most 32 (one rank a lane; ranks past R run as zero rows)
-    if (c.KH != 3 || c.KW != 3 || c.S != c.T || !(c.T == 32 || c.T == 64) || c.R < 1 || c.R > 32) return false;
+    // 3x3 filters, S and T padded to the same channel block count (32 or 64:
+    // the kernel's register budget), rank at most 32 (one rank a lane; ranks
+    // past R run as zero rows)
+    if (c.KH != 3 || c.KW != 3 || c.S < 1 || c.S > 64 || c.T < 1 || c.T > 64 || pad32(c.S) != pad32(c.T) ||
+        c.R < 1 || c.R > 32)
+        return false;
     const int dt = dtin(f);
     // one sample of X, dY and dX is addressed with 31-bit byte offsets
     const int64_t e_in = dt ? 2 : 4;
@@ -244,7 +254,7 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
     m.need = (1u << f.a.index) | (1u << us.index) | (1u << kh.index) | (1u << kw.index) | (1u << ut.index);
     m.what = "fused CP chain backward";
     m.kname = std::string("cp_bwd<") + (dt ? "unsigned short" : "float") + ", 3, 3, " +
-              std::to_string(d.T / 32) + ", " + std::to_string(d.S / 32) + ">";
+              std::to_string(pad32(d.T) / 32) + ", " + std::to_string(pad32(d.S) / 32) + ">";
     // algorithmic bytes: X and dY read, dX written, factors read, partials written
     const double e = dt ? 2 : 4;
     const double act = (double)d.B * d.S * d.H * d.W;   // S = T

@@ -249,7 +249,9 @@ __device__ __forceinline__ uint32_t aslot(__amdgpu_buffer_rsrc_t r, uint32_t vof
 
 // Two blocks per CU (256 VGPRs a lane) except for the bf16 5x5 variant, whose
 // larger ring and bf16 operand packing do not fit that without spilling.
-template <typename T, int KH, int KW, int MB2, int MS>
+// PT: T is not a whole number of 32-channel blocks (bf16 stores then go
+// through the range-checked Y buffer, which drops the padded channels)
+template <typename T, int KH, int KW, int MB2, int MS, bool PT = false>
 __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_fwd(CpDesc d, const T* __restrict__ X,
                                               const T* __restrict__ Us, const T* __restrict__ Kh,
                                               const T* __restrict__ Kw, const T* __restrict__ Ut,
@@ -292,7 +294,6 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     const int h0 = up ? H - p1 : p0, h1 = up ? H - p0 : p1;
     auto prow = [&](int r) { return up ? H - 1 - r : r; };
     const bool store_lane = colok && (lane & 31) >= HWW && (lane & 31) < 32 - HWW;
-    T* Yc = Y + (int64_t)b * d.y_sb + (colok ? col : 0);
     const int cl = lane & 31;
 
     // X rows as B-operand slots (the same slot layout as arow), loaded PD rows
@@ -301,7 +302,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     // the last rows' prefetches would otherwise fetch for nothing
     constexpr uint32_t E = sizeof(T);
     constexpr int PD = BF ? 1 : 2;
-    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(NS * d.x_ss * E));
+    const __amdgpu_buffer_rsrc_t rX = brsrc(X + (int64_t)b * d.x_sb, (uint32_t)(d.S * d.x_ss * E));
     const uint32_t xcs = (uint32_t)(d.x_ss * E);
     const uint32_t kOut = 0x80000000u;   // past the range: reads 0
     const uint32_t xa0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * half * xcs : kOut;
@@ -376,35 +377,45 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
 #pragma unroll
     for (int q = 0; q < QS; q++) {
         const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-        vs[q] = r < d.R ? Us[r * d.us_sr + s * d.us_ss] : (T)0;
+        vs[q] = Us[min(r, d.R - 1) * d.us_sr + min(s, d.S - 1) * d.us_ss];
     }
 #pragma unroll
     for (int q = 0; q < QT; q++) {
-        const int e = tid + 256 * q, r = ut_rank(e);
-        vt[q] = r < d.R ? Ut[r * d.ut_sr + ut_col(e) * d.ut_st] : (T)0;
+        const int e = tid + 256 * q;
+        vt[q] = Ut[min(ut_rank(e), d.R - 1) * d.ut_sr + min(ut_col(e), d.T - 1) * d.ut_st];
     }
+    // (every load unconditional, at a clamped index: a load under a condition
+    // makes the compiler wait for all outstanding loads, the first X row's
+    // included, before the next memory use; the padding is zeroed at the stores)
     if (tid < NKH) {
         const int j = tid % KH, hf = (tid / KH) & 1, r = row32(tid / (2 * KH), 32 * hf);
-        vkh = r < d.R ? load(Kh, r * d.kh_sr + j * d.kh_sj) : 0.f;
+        vkh = load(Kh, min(r, d.R - 1) * d.kh_sr + j * d.kh_sj);
     }
     if (tid < NKW) {
         const int j = tid % KW, hf = (tid / KW) & 1, r = row32(tid / (2 * KW), 32 * hf);
-        vkw = r < d.R ? load(Kw, r * d.kw_sr + j * d.kw_sj) : 0.f;
+        vkw = load(Kw, min(r, d.R - 1) * d.kw_sr + j * d.kw_sj);
     }
 #pragma unroll
     for (int q = 0; q < QS; q++) {
         const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-        UsL[r * LDA + s] = vs[q];
+        UsL[r * LDA + s] = r < d.R && s < d.S ? vs[q] : (T)0;
     }
 #pragma unroll
-    for (int q = 0; q < QT; q++) UtP[tid + 256 * q] = vt[q];
+    for (int q = 0; q < QT; q++) {
+        const int e = tid + 256 * q;
+        UtP[e] = ut_rank(e) < d.R && ut_col(e) < d.T ? vt[q] : (T)0;
+    }
     if (tid < NKH) {
         // and the same taps reversed at o_khr, for the upward walk
-        const int j = tid % KH;
-        KhP[tid] = vkh;
-        ((float*)(smem + d.o_khr))[tid + KH - 1 - 2 * j] = vkh;
+        const int j = tid % KH, hf = (tid / KH) & 1, r = row32(tid / (2 * KH), 32 * hf);
+        const float v = r < d.R ? vkh : 0.f;
+        KhP[tid] = v;
+        ((float*)(smem + d.o_khr))[tid + KH - 1 - 2 * j] = v;
     }
-    if (tid < NKW) KwP[tid] = vkw;
+    if (tid < NKW) {
+        const int hf = (tid / KW) & 1, r = row32(tid / (2 * KW), 32 * hf);
+        KwP[tid] = r < d.R ? vkw : 0.f;
+    }
     }
     __syncthreads();
     if (!wok) return;
@@ -422,7 +433,7 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
     // Y rows through a raw buffer (one sample; stores past the range are
     // dropped): the lane's column and channel 4*half in the lane offset, the
     // rest of the channel in the uniform offset (Y's channel stride is X's)
-    const __amdgpu_buffer_rsrc_t rYo = brsrc(Y + (int64_t)b * d.y_sb, (uint32_t)(TT * d.x_ss * E));
+    const __amdgpu_buffer_rsrc_t rYo = brsrc(Y + (int64_t)b * d.y_sb, (uint32_t)(d.T * d.x_ss * E));
     const uint32_t yv0 = store_lane ? (uint32_t)(col * E) + 4u * half * xcs : kOut;
     // Y row h - 1, stored along the next row's first chain
     f32x16 accYp[MB2];
@@ -540,8 +551,20 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
         if constexpr (BF) {
             f32x16 acc2[MB2];
             gemm2(acc2);
-            if (store_lane) {
-                T* yr = Yc + (int64_t)prow(h) * W;
+            if constexpr (PT) {
+                // through the Y buffer (as the fp32 stores): lanes outside the
+                // strip's own columns and padded channels fall outside its range
+                const uint32_t pv = yv0 + (uint32_t)(prow(h) * W) * E;
+#pragma unroll
+                for (int mb = 0; mb < MB2; mb++)
+#pragma unroll
+                    for (int i = 0; i < 16; i++) {
+                        const int ch = 32 * mb + row32(i, 0);   // + 4 half, in yv0
+                        bstore(acc2[mb][i], (T*)nullptr, rYo, (ch & 1) ? pv + xcs : pv,
+                               (uint32_t)(2 * (ch >> 1)) * xcs);
+                    }
+            } else if (store_lane) {
+                T* yr = Y + (int64_t)b * d.y_sb + col + (int64_t)prow(h) * W;
 #pragma unroll
                 for (int mb = 0; mb < MB2; mb++)
 #pragma unroll
@@ -580,8 +603,11 @@ __global__ void __launch_bounds__(256, (sizeof(T) == 2 && KH == 5) ? 1 : 2) cp_f
 
 template <typename T, int K, int MB2>
 hipError_t launch_cp_t(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
-    if (d.S != 32 && d.S != 64) return hipErrorInvalidValue;
-    auto k = d.S == 32 ? cp_fwd<T, K, K, MB2, 1> : cp_fwd<T, K, K, MB2, 2>;
+    if (d.S < 1 || d.S > 64) return hipErrorInvalidValue;
+    // bf16 with a padded T stores through the Y buffer (fp32 always does)
+    const bool pt = sizeof(T) == 2 && d.T != 32 * MB2;
+    auto k = d.S <= 32 ? (pt ? cp_fwd<T, K, K, MB2, 1, true> : cp_fwd<T, K, K, MB2, 1>)
+                       : (pt ? cp_fwd<T, K, K, MB2, 2, true> : cp_fwd<T, K, K, MB2, 2>);
     hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)ops[0],
                        (const T*)ops[1], (const T*)ops[2], (const T*)ops[3], (const T*)ops[4], (T*)y);
     return hipGetLastError();
@@ -590,9 +616,9 @@ hipError_t launch_cp_t(const CpDesc& d, const void* const* ops, void* y, hipStre
 template <typename T>
 hipError_t launch_cp_ty(const CpDesc& d, const void* const* ops, void* y, hipStream_t s) {
     if (d.KH == 3 && d.KW == 3)
-        return d.T == 32 ? launch_cp_t<T, 3, 1>(d, ops, y, s) : launch_cp_t<T, 3, 2>(d, ops, y, s);
+        return d.T <= 32 ? launch_cp_t<T, 3, 1>(d, ops, y, s) : launch_cp_t<T, 3, 2>(d, ops, y, s);
     if (d.KH == 5 && d.KW == 5)
-        return d.T == 32 ? launch_cp_t<T, 5, 1>(d, ops, y, s) : launch_cp_t<T, 5, 2>(d, ops, y, s);
+        return d.T <= 32 ? launch_cp_t<T, 5, 1>(d, ops, y, s) : launch_cp_t<T, 5, 2>(d, ops, y, s);
     return hipErrorInvalidValue;
 }
 
@@ -745,9 +771,11 @@ __global__ void __launch_bounds__(256, 1)
     const uint32_t ya0 = colok ? (uint32_t)(col * E) + (BF ? 8u : 1u) * hf * ycs : kOut;
     float kh[KH], kw[KW];                            // this lane's rank: r = cl
 #pragma unroll
-    for (int j = 0; j < KH; j++) kh[j] = cl < d.R ? load(Kh, cl * d.kh_sr + j * d.kh_sj) : 0.f;
+    // (a lane past the rank R reads rank R - 1's taps: its Z1 and dZ3 rows are
+    // zero, so they multiply zeros, and its tap gradients are not written)
+    for (int j = 0; j < KH; j++) kh[j] = load(Kh, min(cl, d.R - 1) * d.kh_sr + j * d.kh_sj);
 #pragma unroll
-    for (int j = 0; j < KW; j++) kw[j] = cl < d.R ? load(Kw, cl * d.kw_sr + j * d.kw_sj) : 0.f;
+    for (int j = 0; j < KW; j++) kw[j] = load(Kw, min(cl, d.R - 1) * d.kw_sr + j * d.kw_sj);
 
     f32x16 ring[KH], dr[KH], accUt[MT], accUs[MS];
 #pragma unroll
@@ -817,32 +845,33 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int q = 0; q < QS; q++) {
             const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-            vs[q] = r < d.R ? Us[r * d.us_sr + s * d.us_ss] : (T)0;
+            vs[q] = Us[min(r, d.R - 1) * d.us_sr + min(s, d.S - 1) * d.us_ss];
             if constexpr (BF) {
                 const int s2 = e / 32, r2 = e - s2 * 32;
-                vu[q] = r2 < d.R ? Us[r2 * d.us_sr + s2 * d.us_ss] : (T)0;
+                vu[q] = Us[min(r2, d.R - 1) * d.us_sr + min(s2, d.S - 1) * d.us_ss];
             }
         }
 #pragma unroll
         for (int q = 0; q < QT; q++) {
             const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
-            vt[q] = r < d.R ? Ut[r * d.ut_sr + t * d.ut_st] : (T)0;
+            vt[q] = Ut[min(r, d.R - 1) * d.ut_sr + min(t, d.T - 1) * d.ut_st];
         }
         T* usa = (T*)smem;
         T* uta = (T*)(smem + d.o_uta);
 #pragma unroll
         for (int q = 0; q < QS; q++) {
             const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-            usa[r * LDA_S + s] = vs[q];
+            // (loads at clamped indices; ranks past R and padded channels zeroed here)
+            usa[r * LDA_S + s] = r < d.R && s < d.S ? vs[q] : (T)0;
             if constexpr (BF) {
                 const int s2 = e / 32, r2 = e - s2 * 32;
-                ((T*)(smem + d.o_ust))[s2 * LDU + r2] = vu[q];
+                ((T*)(smem + d.o_ust))[s2 * LDU + r2] = r2 < d.R && s2 < d.S ? vu[q] : (T)0;
             }
         }
 #pragma unroll
         for (int q = 0; q < QT; q++) {
             const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
-            uta[r * LDA_T + t] = vt[q];
+            uta[r * LDA_T + t] = r < d.R && t < d.T ? vt[q] : (T)0;
         }
     }
     __syncthreads();
@@ -1188,17 +1217,25 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int i = 0; i < 16; i++) red[wave * 32 * NT + row32(i, lane) * NT + 32 * n + cl] = accUt[n][i];
     __syncthreads();
-    const int RR = d.R;   // partial rows a block (ranks R..31 are zero and not written)
-    for (int e = tid; e < RR * NT; e += 256)
-        Put[blk * RR * NT + e] = ((red[e] + red[32 * NT + e]) + red[64 * NT + e]) + red[96 * NT + e];
+    // partials [R][T] and [R][S] a block: ranks past R and padded channels
+    // are zero and not written
+    const int RR = d.R, TR = d.T, SR = d.S;
+    for (int e = tid; e < RR * NT; e += 256) {
+        const int r = e / NT, t = e - r * NT;
+        if (t < TR)
+            Put[blk * RR * TR + r * TR + t] = ((red[e] + red[32 * NT + e]) + red[64 * NT + e]) + red[96 * NT + e];
+    }
     __syncthreads();
 #pragma unroll
     for (int n = 0; n < MS; n++)
 #pragma unroll
         for (int i = 0; i < 16; i++) red[wave * 32 * NS + row32(i, lane) * NS + 32 * n + cl] = accUs[n][i];
     __syncthreads();
-    for (int e = tid; e < RR * NS; e += 256)
-        Pus[blk * RR * NS + e] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
+    for (int e = tid; e < RR * NS; e += 256) {
+        const int r = e / NS, s = e - r * NS;
+        if (s < SR)
+            Pus[blk * RR * SR + r * SR + s] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
+    }
     __syncthreads();
     // taps: red[wave][half][r][KH + KW], summed over waves and halves in order
     constexpr int NJ = KH + KW;
@@ -1246,7 +1283,7 @@ hipError_t launch_cpb_t(const CpBwdDesc& d, const void* const* o, hipStream_t s)
 
 template <typename T>
 hipError_t launch_cpb_ty(const CpBwdDesc& d, const void* const* o, hipStream_t s) {
-    const int m = d.T / 32;
+    const int m = (d.T + 31) / 32;
     if (d.KH == 3) return m == 1 ? launch_cpb_t<T, 3, 1>(d, o, s) : launch_cpb_t<T, 3, 2>(d, o, s);
     return hipErrorInvalidValue;
 }
@@ -1256,7 +1293,7 @@ hipError_t launch_cpb_ty(const CpBwdDesc& d, const void* const* o, hipStream_t s
 hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipStream_t s) {
     CpDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    if (d.R < 1 || d.R > 32 || !(d.T == 32 || d.T == 64)) return hipErrorInvalidValue;
+    if (d.R < 1 || d.R > 32 || d.T < 1 || d.T > 64) return hipErrorInvalidValue;
     int bf = (ln.kind >> kBitIn) & 1;
     return bf ? launch_cp_ty<bf16_t>(d, ops, y, s) : launch_cp_ty<float>(d, ops, y, s);
 }
@@ -1265,7 +1302,9 @@ hipError_t launch_cp_fwd(const Launch& ln, const void* const* ops, void* y, hipS
 hipError_t launch_cp_bwd(const Launch& ln, const void* const* ops, hipStream_t s) {
     CpBwdDesc d;
     std::memcpy(&d, ln.desc.data(), sizeof(d));
-    if (d.R < 1 || d.R > 32 || d.S != d.T || !(d.T == 32 || d.T == 64) || d.KH != d.KW) return hipErrorInvalidValue;
+    if (d.R < 1 || d.R > 32 || d.S < 1 || d.T < 1 || d.T > 64 || (d.S + 31) / 32 != (d.T + 31) / 32 ||
+        d.KH != d.KW)
+        return hipErrorInvalidValue;
     int bf = (ln.kind >> kBitIn) & 1;
     return bf ? launch_cpb_ty<bf16_t>(d, ops, s) : launch_cpb_ty<float>(d, ops, s);
 }

@@ -423,7 +423,7 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     Buf Kh = resolve(ln.extra[0], c, 0, o4), Kw = resolve(ln.extra[1], c, 0, o5),
         Ut = resolve(ln.extra[2], c, 0, o6);
     REQ(o4 && o5 && o6, "unresolved buffer");
-    REQ(d.R >= 1 && d.R <= 32 && (d.T == 32 || d.T == 64) && d.S % 32 == 0, "sizes");
+    REQ(d.R >= 1 && d.R <= 32 && d.T >= 1 && d.T <= 64 && d.S >= 1 && d.S <= 64, "sizes");
     REQ(d.KH == d.KW && (d.KH == 3 || d.KH == 5), "filter size");
     REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
         (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
@@ -431,9 +431,10 @@ bool run_cp_fwd(const Launch& ln, Ctx& c) {
     REQ(d.waves == (int64_t)d.B * d.ncb * d.segs && d.blocks * 4 >= d.waves &&
         (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
     // operand tables: UsL 32 x lda at 0, UtP at o_ut, tap tables at o_kh / o_kw
-    REQ(d.lda >= d.S + (bf ? 8 : 1) && (!bf || (d.lda * 2) % 16 == 0), "UsL rows");
+    const int64_t SPf = 32 * ((d.S + 31) / 32), TPf = 32 * ((d.T + 31) / 32);   // padded channel blocks
+    REQ(d.lda >= SPf + (bf ? 8 : 1) && (!bf || (d.lda * 2) % 16 == 0), "UsL rows");
     REQ(d.o_ut >= (uint64_t)32 * d.lda * (bf ? 2 : 4) && d.o_ut % 16 == 0, "UtP offset");
-    REQ(d.o_kh >= d.o_ut + (bf ? (uint64_t)2 * 2 * d.T * 8 * 2 : (uint64_t)16 * 2 * d.T * 4), "Kh offset");
+    REQ(d.o_kh >= d.o_ut + (bf ? (uint64_t)2 * 2 * TPf * 8 * 2 : (uint64_t)16 * 2 * TPf * 4), "Kh offset");
     REQ(d.o_kw >= d.o_kh + (uint64_t)16 * 2 * d.KH * 4, "Kw offset");
     REQ(d.o_khr >= d.o_kw + (uint64_t)16 * 2 * d.KW * 4, "reversed Kh offset");
     REQ(d.lds_bytes >= d.o_khr + (uint64_t)16 * 2 * d.KH * 4 && d.lds_bytes <= 64 * 1024 &&
@@ -945,7 +946,8 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
         REQ(o, "unresolved buffer");
     }
     Buf &Us = F[0], &Kh = F[1], &Kw = F[2], &Ut = F[3], &Pus = F[4], &Put = F[5], &Pkh = F[6], &Pkw = F[7];
-    REQ(d.R >= 1 && d.R <= 32 && d.S == d.T && (d.T == 32 || d.T == 64) && d.KH == 3 && d.KW == 3, "sizes");
+    REQ(d.R >= 1 && d.R <= 32 && d.S >= 1 && d.T >= 1 && d.T <= 64 && (d.S + 31) / 32 == (d.T + 31) / 32 &&
+        d.KH == 3 && d.KW == 3, "sizes");
     REQ(d.colstride == 32 - (d.KW - 1) && (int64_t)d.ncb * d.colstride >= d.W &&
         (int64_t)(d.ncb - 1) * d.colstride < d.W, "strips");
     REQ((int64_t)d.segs * d.seg_rows >= d.H && (int64_t)(d.segs - 1) * d.seg_rows < d.H, "segments");
@@ -953,14 +955,15 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
         (int64_t)ln.grid[0] == d.blocks && ln.block[0] == 256, "grid");
     // LDS: tables, transpose tiles, dY tiles, reduction area
     const uint64_t e = bf ? 2 : 4;
-    REQ(d.lda_s >= d.S + (bf ? 8 : 1) && d.lda_t >= d.T + (bf ? 8 : 1) &&
+    const uint64_t SP = 32 * ((d.S + 31) / 32), TP = 32 * ((d.T + 31) / 32);   // padded channel blocks
+    REQ(d.lda_s >= SP + (bf ? 8 : 1) && d.lda_t >= TP + (bf ? 8 : 1) &&
         (!bf || ((d.lda_s * 2) % 16 == 0 && (d.lda_t * 2) % 16 == 0)), "table rows");
     REQ(d.o_uta >= 32 * d.lda_s * e && d.o_uta % 16 == 0, "UtA offset");
     REQ(d.o_ust >= d.o_uta + 32 * d.lda_t * e && d.o_ust % 16 == 0, "UsT offset");
     REQ(!bf || (d.ldu >= 32 + 8 && (d.ldu * 2) % 16 == 0), "UsT rows");
-    REQ(d.o_tz >= d.o_ust + (bf ? (uint64_t)d.S * d.ldu * 2 : 0) && d.o_tz % 16 == 0, "tile offset");
+    REQ(d.o_tz >= d.o_ust + (bf ? (uint64_t)SP * d.ldu * 2 : 0) && d.o_tz % 16 == 0, "tile offset");
     REQ(d.ly >= 32 + (bf ? 8 : 1) && (!bf || (d.ly * 2) % 8 == 0), "dY tile rows");
-    REQ(d.yt_bytes >= (uint64_t)d.T * d.ly * e && d.yt_bytes % 16 == 0 && d.o_yt % 16 == 0, "dY tiles");
+    REQ(d.yt_bytes >= (uint64_t)TP * d.ly * e && d.yt_bytes % 16 == 0 && d.o_yt % 16 == 0, "dY tiles");
     REQ(d.tz_stride >= 32 * 33 * 4 && d.tz_stride % 16 == 0, "transpose tiles");
     if (d.o_tz == d.o_yt)   // the transpose tile shares the wave's dY tile
         REQ(d.tz_stride == d.yt_bytes, "shared tiles");
@@ -968,10 +971,10 @@ bool run_cp_bwd(const Launch& ln, Ctx& c) {
         REQ(d.o_yt >= d.o_tz + 4 * (uint64_t)d.tz_stride, "tile regions");
     // X-row rings: three rows of S channels, aligned column runs
     REQ(d.lx >= 32 + (bf ? 8 : 4) && (d.lx * e) % (bf ? 8 : 16) == 0 && d.o_xl % 16 == 0 &&
-        d.xl_bytes >= 3 * (uint64_t)d.S * d.lx * e && d.xl_bytes % 16 == 0, "X rings");
+        d.xl_bytes >= 3 * SP * d.lx * e && d.xl_bytes % 16 == 0, "X rings");
     REQ(d.o_xl >= d.o_yt + 4 * (uint64_t)d.yt_bytes && d.lds_bytes >= d.o_xl + 4 * (uint64_t)d.xl_bytes,
         "LDS tiles");
-    REQ(d.red_bytes >= (uint64_t)4 * std::max({(uint64_t)4 * 32 * d.S, (uint64_t)4 * 32 * d.T,
+    REQ(d.red_bytes >= (uint64_t)4 * std::max({(uint64_t)4 * 32 * SP, (uint64_t)4 * 32 * TP,
                                                (uint64_t)8 * 32 * (d.KH + d.KW)}) &&
         d.lds_bytes >= d.red_bytes && d.lds_bytes <= 160 * 1024 && ln.lds == d.lds_bytes, "LDS size");
     const int B = d.B, S = d.S, R = d.R, T = d.T, H = d.H, W = d.W, K = d.KH, c3 = (K - 1) / 2;

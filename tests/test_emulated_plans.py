@@ -89,6 +89,10 @@ CASES = {
     "C2r16": W.cp_layer("C2r16t", 2, 32, 32, 5, 37, 16, 3, "f32", 26),
     "C2r8_bf16": W.cp_layer("C2r8t_bf16", 2, 32, 64, 5, 19, 8, 3, "bf16", 27),
     "C2r20k5": W.cp_layer("C2r20k5t", 1, 32, 32, 6, 29, 20, 5, "f32", 28),
+    # channel counts off the 32 / 64 blocks
+    "C2c48": W.cp_layer("C2c48t", 2, 48, 40, 5, 37, 24, 3, "f32", 29),
+    "C2c16_bf16": W.cp_layer("C2c16t_bf16", 2, 16, 16, 5, 19, 8, 3, "bf16", 30),
+    "C2c20k5": W.cp_layer("C2c20k5t", 1, 20, 56, 6, 29, 32, 5, "f32", 31),
     "C3t": W.tucker2_layer("C3t", 2, 32, 24, 7, 9, 8, 16, 3, "bf16", 21),
     "C3t_f32": W.tucker2_layer("C3t_f32", 2, 32, 24, 7, 9, 8, 16, 3, "f32", 21),
     # Tucker cores on MFMA tiles (ragged channels, 5 x 5 taps, row tiles)

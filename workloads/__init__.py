@@ -130,6 +130,10 @@ PARITY_WORKLOADS = {
     "C2r16": cp_layer("C2r16", 3, 64, 64, 13, 37, 16, 3, "f32", 26),
     "C2r8_bf16": cp_layer("C2r8_bf16", 3, 32, 64, 11, 19, 8, 3, "bf16", 27),
     "C2r20k5": cp_layer("C2r20k5", 2, 64, 32, 12, 29, 20, 5, "f32", 28),
+    # channel counts off the 32 / 64 blocks (padded with zero table entries)
+    "C2c48": cp_layer("C2c48", 2, 48, 40, 13, 37, 24, 3, "f32", 29),
+    "C2c16_bf16": cp_layer("C2c16_bf16", 3, 16, 16, 11, 19, 8, 3, "bf16", 30),
+    "C2c20k5": cp_layer("C2c20k5", 2, 20, 56, 12, 29, 32, 5, "f32", 31),
     "C3s": tucker2_layer("C3s", 3, 256, 256, 11, 13, 64, 64, 3, "bf16", 13),
     "C3s_f32": tucker2_layer("C3s_f32", 3, 256, 256, 11, 13, 64, 64, 3, "f32", 13),
     "C4s": rtt_layer("C4s", 2, (4, 8, 8), (4, 8, 8), 13, 13, 16, 3, "f32", 14),
