@@ -141,7 +141,7 @@ bool match_cp_fwd(const std::vector<Launch>& v, size_t i, Launch& fused) {
     fused.what = "fused CP chain: " + g1.what + " | " + d1.what + " | " + d2.what + " | " + g2.what;
     fused.kname = std::string("cp_fwd<") + (dt ? "unsigned short" : "float") + ", " +
                   std::to_string(h.K) + ", " + std::to_string(w.K) + ", " + std::to_string(pad32((int)T) / 32) + ", " +
-                  std::to_string(pad32((int)S) / 32) + ">";
+                  std::to_string(pad32((int)S) / 32) + ((dt == 1 && T != pad32((int)T)) ? ", true>" : ", false>");
     fused.alg_bytes = g1.alg_bytes + d1.alg_bytes + d2.alg_bytes + g2.alg_bytes;
     fused.alg_flops = g1.alg_flops + d1.alg_flops + d2.alg_flops + g2.alg_flops;
     // algorithmic bytes of the fused launch: X, factors and Y only
