@@ -254,7 +254,8 @@ bool fuse_cp_backward(const Launch& f, int feature_operand, ScratchAlloc& scratc
     m.need = (1u << f.a.index) | (1u << us.index) | (1u << kh.index) | (1u << kw.index) | (1u << ut.index);
     m.what = "fused CP chain backward";
     m.kname = std::string("cp_bwd<") + (dt ? "unsigned short" : "float") + ", 3, 3, " +
-              std::to_string(pad32(d.T) / 32) + ", " + std::to_string(pad32(d.S) / 32) + ">";
+              std::to_string(pad32(d.T) / 32) + ", " + std::to_string(pad32(d.S) / 32) +
+              ((d.R == 32 && d.S == pad32(d.S) && d.T == pad32(d.T)) ? ", false>" : ", true>");
     // algorithmic bytes: X and dY read, dX written, factors read, partials written
     const double e = dt ? 2 : 4;
     const double act = (double)d.B * d.S * d.H * d.W;   // S = T

@@ -711,7 +711,11 @@ template <typename T> constexpr int cp_bwd_pitch_u() { return 40; }
 template <typename T> constexpr int cp_bwd_pitch_y() { return sizeof(T) == 2 ? 40 : 33; }
 template <typename T> constexpr int cp_bwd_pitch_x() { return sizeof(T) == 2 ? 40 : 36; }
 
-template <typename T, int KH, int KW, int MT, int MS>
+// GEN: a rank below 32 or channel counts off the 32-channel blocks (clamped
+// table loads, zeroed padding, compacted partials); the whole-block shapes
+// compile without any of that (it moved the scheduling of the row loop and
+// cost about 1.6 % of the kernel's time at R = 32, S = T = 64).
+template <typename T, int KH, int KW, int MT, int MS, bool GEN>
 __global__ void __launch_bounds__(256, 1)
     cp_bwd(CpBwdDesc d, const T* __restrict__ X, const T* __restrict__ dY,
            const T* __restrict__ Us, const T* __restrict__ Kh, const T* __restrict__ Kw,
@@ -773,9 +777,9 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
     // (a lane past the rank R reads rank R - 1's taps: its Z1 and dZ3 rows are
     // zero, so they multiply zeros, and its tap gradients are not written)
-    for (int j = 0; j < KH; j++) kh[j] = load(Kh, min(cl, d.R - 1) * d.kh_sr + j * d.kh_sj);
+    for (int j = 0; j < KH; j++) kh[j] = load(Kh, (GEN ? min(cl, d.R - 1) : cl) * d.kh_sr + j * d.kh_sj);
 #pragma unroll
-    for (int j = 0; j < KW; j++) kw[j] = load(Kw, min(cl, d.R - 1) * d.kw_sr + j * d.kw_sj);
+    for (int j = 0; j < KW; j++) kw[j] = load(Kw, (GEN ? min(cl, d.R - 1) : cl) * d.kw_sr + j * d.kw_sj);
 
     f32x16 ring[KH], dr[KH], accUt[MT], accUs[MS];
 #pragma unroll
@@ -845,16 +849,17 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int q = 0; q < QS; q++) {
             const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
-            vs[q] = Us[min(r, d.R - 1) * d.us_sr + min(s, d.S - 1) * d.us_ss];
+            vs[q] = GEN ? Us[min(r, d.R - 1) * d.us_sr + min(s, d.S - 1) * d.us_ss] : Us[r * d.us_sr + s * d.us_ss];
             if constexpr (BF) {
                 const int s2 = e / 32, r2 = e - s2 * 32;
-                vu[q] = Us[min(r2, d.R - 1) * d.us_sr + min(s2, d.S - 1) * d.us_ss];
+                vu[q] = GEN ? Us[min(r2, d.R - 1) * d.us_sr + min(s2, d.S - 1) * d.us_ss]
+                            : Us[r2 * d.us_sr + s2 * d.us_ss];
             }
         }
 #pragma unroll
         for (int q = 0; q < QT; q++) {
             const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
-            vt[q] = Ut[min(r, d.R - 1) * d.ut_sr + min(t, d.T - 1) * d.ut_st];
+            vt[q] = GEN ? Ut[min(r, d.R - 1) * d.ut_sr + min(t, d.T - 1) * d.ut_st] : Ut[r * d.ut_sr + t * d.ut_st];
         }
         T* usa = (T*)smem;
         T* uta = (T*)(smem + d.o_uta);
@@ -862,16 +867,16 @@ __global__ void __launch_bounds__(256, 1)
         for (int q = 0; q < QS; q++) {
             const int e = tid + 256 * q, r = e / NS, s = e - r * NS;
             // (loads at clamped indices; ranks past R and padded channels zeroed here)
-            usa[r * LDA_S + s] = r < d.R && s < d.S ? vs[q] : (T)0;
+            usa[r * LDA_S + s] = !GEN || (r < d.R && s < d.S) ? vs[q] : (T)0;
             if constexpr (BF) {
                 const int s2 = e / 32, r2 = e - s2 * 32;
-                ((T*)(smem + d.o_ust))[s2 * LDU + r2] = r2 < d.R && s2 < d.S ? vu[q] : (T)0;
+                ((T*)(smem + d.o_ust))[s2 * LDU + r2] = !GEN || (r2 < d.R && s2 < d.S) ? vu[q] : (T)0;
             }
         }
 #pragma unroll
         for (int q = 0; q < QT; q++) {
             const int e = tid + 256 * q, r = e / NT, t = e - r * NT;
-            uta[r * LDA_T + t] = r < d.R && t < d.T ? vt[q] : (T)0;
+            uta[r * LDA_T + t] = !GEN || (r < d.R && t < d.T) ? vt[q] : (T)0;
         }
     }
     __syncthreads();
@@ -1219,10 +1224,11 @@ __global__ void __launch_bounds__(256, 1)
     __syncthreads();
     // partials [R][T] and [R][S] a block: ranks past R and padded channels
     // are zero and not written
-    const int RR = d.R, TR = d.T, SR = d.S;
+    // (whole-block shapes: R = 32, T = NT, S = NS, the same layout with no checks)
+    const int RR = GEN ? d.R : 32, TR = GEN ? d.T : NT, SR = GEN ? d.S : NS;
     for (int e = tid; e < RR * NT; e += 256) {
         const int r = e / NT, t = e - r * NT;
-        if (t < TR)
+        if (!GEN || t < TR)
             Put[blk * RR * TR + r * TR + t] = ((red[e] + red[32 * NT + e]) + red[64 * NT + e]) + red[96 * NT + e];
     }
     __syncthreads();
@@ -1233,7 +1239,7 @@ __global__ void __launch_bounds__(256, 1)
     __syncthreads();
     for (int e = tid; e < RR * NS; e += 256) {
         const int r = e / NS, s = e - r * NS;
-        if (s < SR)
+        if (!GEN || s < SR)
             Pus[blk * RR * SR + r * SR + s] = ((red[e] + red[32 * NS + e]) + red[64 * NS + e]) + red[96 * NS + e];
     }
     __syncthreads();
@@ -1249,7 +1255,7 @@ __global__ void __launch_bounds__(256, 1)
         float v = 0.f;
 #pragma unroll
         for (int q = 0; q < 8; q++) v += red[q * 32 * NJ + e];
-        if (r >= RR) continue;
+        if (GEN && r >= RR) continue;
         if (jj < KW) Pkw[blk * RR * KW + r * KW + jj] = v;
         else Pkh[blk * RR * KH + r * KH + (jj - KW)] = v;
     }
@@ -1259,21 +1265,22 @@ constexpr uint32_t kMaxLds = 160 * 1024;   // LDS of one gfx950 CU
 
 template <typename T, int K, int M>
 hipError_t launch_cpb_t(const CpBwdDesc& d, const void* const* o, hipStream_t s) {
-    auto k = cp_bwd<T, K, K, M, M>;
+    const bool gen = !(d.R == 32 && d.S == 32 * M && d.T == 32 * M);
+    auto k = gen ? cp_bwd<T, K, K, M, M, true> : cp_bwd<T, K, K, M, M, false>;
     // the kernel's compile-time LDS pitches must be the descriptor's
     if (d.lda_s != cp_bwd_pitch_s<T, 32 * M>() || d.lda_t != cp_bwd_pitch_s<T, 32 * M>() || d.ly != cp_bwd_pitch_y<T>() ||
         d.lx != cp_bwd_pitch_x<T>() || (sizeof(T) == 2 && d.ldu != cp_bwd_pitch_u<T>()))
         return hipErrorInvalidValue;
     // dynamic LDS above 64 KB has to be allowed per kernel, once per device
-    static std::atomic<uint64_t> allowed{0};
+    static std::atomic<uint64_t> allowed[2];   // per kernel (gen), a bit per device
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     if (dev < 0 || dev >= 64 || d.lds_bytes > kMaxLds) return hipErrorInvalidValue;
-    if (!(allowed.load() & (1ull << dev))) {
+    if (!(allowed[gen].load() & (1ull << dev))) {
         e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
         if (e != hipSuccess) return e;
-        allowed.fetch_or(1ull << dev);
+        allowed[gen].fetch_or(1ull << dev);
     }
     hipLaunchKernelGGL(k, dim3((uint32_t)d.blocks), dim3(256), d.lds_bytes, s, d, (const T*)o[0],
                        (const T*)o[1], (const T*)o[3], (const T*)o[4], (const T*)o[5], (const T*)o[6],
